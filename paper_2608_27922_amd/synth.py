@@ -1,0 +1,210 @@
+"""Seeded synthetic inputs for the DensityKV hot path.
+
+Stand-ins for the post-RoPE keys, values and queries that the paper's video
+backbone (Wan2.1-T2V-1.3B: d_k = d_v = 128, 1,560 tokens per latent frame,
+3-frame blocks of N = 4,680 candidates; Supp. D) would produce.  The module
+only draws numbers: it holds none of the method's arithmetic and is the one
+piece shared by the tests, the oracle runs and the benchmark.
+
+Recipe (per (config, layer, head), independent NumPy PCG64 streams from base
+seed 0, the paper's generation seed):
+  * cluster centres c_j = g / |g| with g ~ N(0, I_d);
+  * a token is c_z + 0.3 * eps, eps ~ N(0, I_d) per component, z uniform over
+    the active clusters;
+  * keys are snapped to the 1/64 grid, clip(rint(64 x), -127, 127) / 64, so
+    that every key-key Gram is exact in fp32 (the contract that makes the
+    oracle and the kernels agree bit for bit);
+  * values and queries are fresh mixture draws rounded to the storage dtype.
+Config specifics: near-duplicates of bank tokens (config 2), centre drift by
+a 0.05 random-walk step per block (configs 3 and 5), 256 clusters with
+16 active per block and a recurring active set every 10 blocks (config 4),
+per-head budgets drawn from {2340, 4680, 9360, 18720} (config 5).
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, Optional, Tuple
+
+import numpy as np
+
+GRID = 64          # keys are integers / 64
+GRID_MAX = 127     # |integer| <= 127
+
+
+@dataclass(frozen=True)
+class Config:
+    key: int
+    name: str
+    layers: int
+    heads: int
+    d: int
+    dtype: str                 # "bf16" or "f32"
+    n_cand: int                # N candidates per block
+    n_query: int
+    n_window: int
+    budget: int                # per-head budget (max budget when ragged)
+    clusters: int
+    blocks: int                # number of updates in the run
+    group_size: int            # heads sharing one admitted prefix length
+    sigma2_log2: int           # sigma^2 = d_k / 2 (Supp. B bandwidth calibration)
+    starts_full: bool = False  # bank built first from a block of `budget` tokens
+    dup_frac: float = 0.0
+    drift: float = 0.0
+    active: int = 0            # active clusters per block (0: all)
+    revisit: int = 0           # recurring active set period (0: none)
+    ragged: Tuple[int, ...] = ()
+
+    @property
+    def banks(self) -> int:
+        return self.layers * self.heads
+
+
+CONFIGS: Dict[int, Config] = {
+    1: Config(1, "tiny", 1, 2, 64, "f32", 64, 64, 64, 256, 8, 1, 2, 5, starts_full=True),
+    2: Config(2, "single_layer", 1, 12, 128, "bf16", 4680, 4680, 4680, 4680, 64, 1, 12, 6,
+              starts_full=True, dup_frac=0.3),
+    3: Config(3, "rollout", 30, 12, 128, "bf16", 4680, 4680, 4680, 9360, 64, 20, 12, 6,
+              drift=0.05),
+    4: Config(4, "long_rollout", 30, 12, 128, "bf16", 4680, 4680, 4680, 18720, 256, 80, 12, 6,
+              active=16, revisit=10),
+    5: Config(5, "headwise_budgets", 30, 12, 128, "bf16", 4680, 4680, 4680, 18720, 64, 160, 1, 6,
+              drift=0.05, ragged=(2340, 4680, 9360, 18720)),
+}
+
+ROLE_CENTRES, ROLE_K, ROLE_V, ROLE_Q, ROLE_DUP, ROLE_BUDGET, ROLE_DRIFT, ROLE_ACTIVE = range(8)
+
+
+def _rng(seed: int, *key: int) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence([seed, *key]))
+
+
+def snap_keys(x: np.ndarray) -> np.ndarray:
+    """Round to the 1/64 key grid (float32, exact in bf16)."""
+    return (np.clip(np.rint(x * GRID), -GRID_MAX, GRID_MAX) / GRID).astype(np.float32)
+
+
+def to_storage(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Round float values to the storage dtype, returned as float32 holding exact values."""
+    x = np.asarray(x, np.float32)
+    if dtype == "f32":
+        return x
+    if dtype != "bf16":
+        raise ValueError(dtype)
+    b = x.view(np.uint32).astype(np.uint64)
+    rounded = (b + 0x7FFF + ((b >> 16) & 1)) & 0xFFFF0000  # round to nearest even
+    return rounded.astype(np.uint32).view(np.float32)
+
+
+def budgets(cfg: Config, seed: int = 0) -> np.ndarray:
+    """Per-(layer, head) budgets, shape (layers * heads,)."""
+    if not cfg.ragged:
+        return np.full(cfg.banks, cfg.budget, np.int32)
+    r = _rng(seed, cfg.key, ROLE_BUDGET)
+    return np.asarray(cfg.ragged, np.int32)[r.integers(0, len(cfg.ragged), cfg.banks)]
+
+
+class HeadStream:
+    """Seeded token source of one (config, layer, head).
+
+    block(t) returns (K, V, Q) for block t: K, V with `n` rows, Q with
+    cfg.n_query rows.  Blocks are indexed from 0; the drift state is advanced
+    deterministically, so any block can be requested in any order."""
+
+    def __init__(self, cfg: Config, layer: int, head: int, seed: int = 0):
+        self.cfg, self.layer, self.head, self.seed = cfg, layer, head, seed
+        r = _rng(seed, cfg.key, layer, head, ROLE_CENTRES)
+        g = r.standard_normal((cfg.clusters, cfg.d))
+        self._c0 = g / np.linalg.norm(g, axis=1, keepdims=True)
+        self._centres = {0: self._c0}
+        self._dup_src: Optional[np.ndarray] = None
+
+    def centres(self, t: int) -> np.ndarray:
+        if self.cfg.drift == 0.0:
+            return self._c0
+        last = max(k for k in self._centres if k <= t)
+        c = self._centres[last]
+        for s in range(last + 1, t + 1):
+            u = _rng(self.seed, self.cfg.key, self.layer, self.head, ROLE_DRIFT, s).standard_normal(c.shape)
+            u /= np.linalg.norm(u, axis=1, keepdims=True)
+            c = c + self.cfg.drift * u
+            c = c / np.linalg.norm(c, axis=1, keepdims=True)
+            self._centres[s] = c
+        return c
+
+    def active_set(self, t: int) -> np.ndarray:
+        cfg = self.cfg
+        if cfg.active == 0:
+            return np.arange(cfg.clusters)
+        if cfg.revisit and t >= cfg.revisit and t % cfg.revisit == 0:
+            return self.active_set(t - cfg.revisit)
+        r = _rng(self.seed, cfg.key, self.layer, self.head, ROLE_ACTIVE, t)
+        return np.sort(r.choice(cfg.clusters, cfg.active, replace=False))
+
+    def _mixture(self, role: int, t: int, n: int) -> np.ndarray:
+        r = _rng(self.seed, self.cfg.key, self.layer, self.head, role, t)
+        act = self.active_set(t)
+        z = act[r.integers(0, act.size, n)]
+        noise = r.standard_normal((n, self.cfg.d), dtype=np.float32)
+        return self.centres(t)[z].astype(np.float32) + np.float32(0.3) * noise
+
+    def keys(self, t: int, n: int) -> np.ndarray:
+        return snap_keys(self._mixture(ROLE_K, t, n))
+
+    def values(self, t: int, n: int) -> np.ndarray:
+        return to_storage(self._mixture(ROLE_V, t, n), self.cfg.dtype)
+
+    def queries(self, t: int) -> np.ndarray:
+        return to_storage(self._mixture(ROLE_Q, t, self.cfg.n_query), self.cfg.dtype)
+
+    def near_duplicates(self, K: np.ndarray, bank_keys: np.ndarray, t: int) -> np.ndarray:
+        """Replace a fraction cfg.dup_frac of the rows of K by near-duplicates
+        (cosine > 0.95) of uniformly drawn rows of bank_keys."""
+        cfg = self.cfg
+        n = K.shape[0]
+        r = _rng(self.seed, cfg.key, self.layer, self.head, ROLE_DUP, t)
+        k = int(round(cfg.dup_frac * n))
+        rows = np.sort(r.choice(n, k, replace=False))
+        src = r.integers(0, bank_keys.shape[0], k)
+        out = K.copy()
+        for i, s in zip(rows, src):
+            base = bank_keys[s].astype(np.float64)
+            while True:
+                x = snap_keys(base + 0.05 * r.standard_normal(cfg.d))
+                cos = float(x @ base) / (np.linalg.norm(x) * np.linalg.norm(base) + 1e-30)
+                if cos > 0.95:
+                    break
+            out[i] = x
+        return out
+
+
+def single_update_case(cfg: Config, layer: int = 0, seed: int = 0, heads: Optional[range] = None):
+    """Inputs of a starts-full configuration (configs 1 and 2) for one layer.
+
+    Returns a dict of stacked float32 arrays over the layer's heads:
+      init_K, init_V  (H, budget, d)  block 0: builds the full initial bank
+      seg_K, seg_V    (H, N, d)       block 1: the incoming segment
+      q               (H, Nq, d)      block 2 queries
+      win_K, win_V    (H, W, d)       block 2 keys/values: the local window
+    """
+    heads = range(cfg.heads) if heads is None else heads
+    out = {k: [] for k in ("init_K", "init_V", "seg_K", "seg_V", "q", "win_K", "win_V")}
+    for h in heads:
+        s = HeadStream(cfg, layer, h, seed)
+        iK = s.keys(0, cfg.budget)
+        out["init_K"].append(iK)
+        out["init_V"].append(s.values(0, cfg.budget))
+        sK = s.keys(1, cfg.n_cand)
+        if cfg.dup_frac:
+            sK = s.near_duplicates(sK, iK, 1)
+        out["seg_K"].append(sK)
+        out["seg_V"].append(s.values(1, cfg.n_cand))
+        out["q"].append(s.queries(2))
+        out["win_K"].append(s.keys(2, cfg.n_window))
+        out["win_V"].append(s.values(2, cfg.n_window))
+    return {k: np.stack(v) for k, v in out.items()}
+
+
+def random_grid_keys(rng: np.random.Generator, shape, scale: float = 0.5) -> np.ndarray:
+    """Generic grid keys for small tests (not a config workload)."""
+    return snap_keys(scale * rng.standard_normal(shape))

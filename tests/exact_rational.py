@@ -1,0 +1,83 @@
+"""Exact rational brute force of the DensityKV update, for tiny banks (test pin only).
+
+Independent of ``oracle/``: it works in ``fractions.Fraction`` and, for every
+tested prefix length r, builds the hypothetical multiset bank (+) P_r and
+recomputes each historical state's density from its definition (Eq. 3),
+instead of using cached densities and cumulative sums.  After the commit every
+density is recomputed from scratch over the final bank.  This is the paper's
+update (Sec. 3.4, Eqs. 5-12; Supp. C, Algorithm 1) evaluated in real
+arithmetic, so any oracle decision on a well-separated tiny case must agree
+with it, and every oracle fixed-point density must round to it.
+"""
+
+from fractions import Fraction as F
+
+
+def weight(a, b, sigma2, p):
+    """(1 + |a - b|^2 / sigma^2)^-p with eps = 1 (Eq. 2)."""
+    d2 = sum((F(x) - F(y)) ** 2 for x, y in zip(a, b))
+    return F(1) / (F(1) + d2 / F(sigma2)) ** p
+
+
+def phi(keys, i, sigma2, p):
+    """Soft-Riesz density of entry i in the indexed multiset ``keys`` (Eq. 3)."""
+    return sum((weight(keys[i], keys[j], sigma2, p) for j in range(len(keys)) if j != i), F(0))
+
+
+def update(bank, cands, M, sigma2=1, p=1, tau=F(2), delta=F(1, 10 ** 6), block_id=1):
+    """bank: list of dicts {key, b, prov}; cands: list of key tuples (source order).
+
+    Returns (new_bank, info) where new_bank lists dicts {key, rho, b, prov} in the
+    commit layout survivors-in-place / admitted-into-holes-then-appended."""
+    N, m = len(cands), len(bank)
+    R = min(N, M)
+    keys = [s["key"] for s in bank]
+    if m == 0:
+        pi = list(range(N))
+        scores = None
+    else:
+        scores = [sum((weight(k, x, sigma2, p) / s["b"] for k, s in zip(keys, bank)), F(0)) / m
+                  for x in cands]
+        pi = sorted(range(N), key=lambda x: (scores[x], x))
+    c, proj = [], []
+    for r in range(R + 1):
+        hyp = keys + [cands[pi[j]] for j in range(r)]
+        pr = [phi(hyp, i, sigma2, p) for i in range(m)]
+        proj.append(pr)
+        c.append(sum(1 for i in range(m) if pr[i] / bank[i]["b"] >= tau))
+    e = [max(0, m + r - M) for r in range(R + 1)]
+    feas = [r for r in range(R + 1) if c[r] <= e[r]]
+    r_star = max(feas) if feas else 0
+    pr = proj[r_star]
+    viol = [i for i in range(m) if pr[i] / bank[i]["b"] >= tau]
+    evict = list(viol)
+    rest = sorted((i for i in range(m) if i not in viol), key=lambda i: (-pr[i], bank[i]["prov"], i))
+    evict += rest[: max(0, e[r_star] - len(evict))]
+    evict = sorted(evict)
+    admitted = sorted(pi[:r_star])
+    # commit layout
+    slots = {i: dict(bank[i]) for i in range(m) if i not in evict}
+    holes = list(evict)
+    for k, x in enumerate(admitted):
+        s = holes[k] if k < len(holes) else m + k - len(holes)
+        slots[s] = {"key": cands[x], "b": None, "prov": (block_id << 32) | x}
+    m_new = m - len(evict) + len(admitted)
+    low = [s for s in range(m_new) if s not in slots]
+    high = sorted(s for s in slots if s >= m_new)
+    for dst, src in zip(low, high):
+        slots[dst] = slots.pop(src)
+    new_bank = [slots[s] for s in range(m_new)]
+    fk = [s["key"] for s in new_bank]
+    for i, s in enumerate(new_bank):
+        s["rho"] = phi(fk, i, sigma2, p)
+        if s["b"] is None:
+            s["b"] = max(s["rho"], delta)
+    info = dict(r_star=r_star, pi=pi, scores=scores, c=c, e=e, evicted=evict, admitted=admitted,
+                violators=viol, projected=pr)
+    return new_bank, info
+
+
+def build(cands, M, **kw):
+    """A bank produced by the empty-bank rule from ``cands``."""
+    bank, _ = update([], cands, M, **kw)
+    return bank
