@@ -1,0 +1,263 @@
+"""Thin ctypes binding of libdensitykv.so (include/densitykv.h), same entry-point names.
+
+Argument marshalling only: torch tensors supply device memory and the current
+HIP stream; every step of the hot path runs in the library's kernels.  There is
+no fallback: if the library has not been built, loading raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdensitykv.so")
+
+DKV_BF16, DKV_F32 = 0, 1
+MAX_CANDIDATES, MAX_CAPACITY, MAX_BLOCK_ID = 8191, 32767, 16777215
+ENTRY_POINTS = ("densitykv_workspace_size", "densitykv_score", "densitykv_update_bank",
+                "densitykv_bank_attention", "densitykv_pair_weight_q23", "densitykv_status_string")
+
+_vp = ctypes.c_void_p
+
+
+class DkvBank(ctypes.Structure):
+    _fields_ = [("num_banks", ctypes.c_int32), ("group_size", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("capacity", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("k", _vp), ("v", _vp), ("knorm", _vp), ("rho", _vp),
+                ("base", _vp), ("prov", _vp), ("occupancy", _vp), ("budget", _vp)]
+
+
+class DkvSegment(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("block_id", ctypes.c_int32), ("k", _vp), ("v", _vp)]
+
+
+class DkvParams(ctypes.Structure):
+    _fields_ = [("sigma2_log2", ctypes.c_int32), ("p", ctypes.c_int32), ("tau_num", ctypes.c_int32),
+                ("tau_log2_den", ctypes.c_int32), ("delta_q", ctypes.c_int64), ("flags", ctypes.c_uint32)]
+
+
+class DkvUpdateOut(ctypes.Structure):
+    _fields_ = [("r_star", _vp), ("n_admitted", _vp), ("n_evicted", _vp), ("admitted", _vp),
+                ("evicted", _vp), ("order", _vp), ("score_q", _vp), ("first_cross", _vp),
+                ("rho_tilde", _vp)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_27922_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.densitykv_workspace_size.argtypes = [P(DkvBank), ctypes.c_int32, P(ctypes.c_size_t)]
+        L.densitykv_score.argtypes = [P(DkvBank), P(DkvSegment), P(DkvParams), _vp, _vp, _vp, _vp,
+                                      ctypes.c_size_t, _vp]
+        L.densitykv_update_bank.argtypes = [P(DkvBank), P(DkvSegment), P(DkvParams), P(DkvUpdateOut), _vp,
+                                            ctypes.c_size_t, _vp]
+        L.densitykv_bank_attention.argtypes = [P(DkvBank), _vp, ctypes.c_int32, _vp, _vp, ctypes.c_int32, _vp,
+                                               ctypes.c_float, _vp]
+        L.densitykv_pair_weight_q23.argtypes = [_vp, ctypes.c_int64, P(DkvParams), _vp, _vp]
+        L.densitykv_status_string.argtypes = [ctypes.c_int]
+        L.densitykv_status_string.restype = ctypes.c_char_p
+        for name in ENTRY_POINTS[:-1]:
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+class DkvError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {lib().densitykv_status_string(status).decode()} ({status})")
+
+
+def _check(status: int, where: str):
+    if status != 0:
+        raise DkvError(status, where)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+@dataclass(frozen=True)
+class Params:
+    """Method parameters (defaults: sigma = 8 -> sigma^2 = 2^6, p = 2, tau = 2, delta = 1e-6)."""
+
+    sigma2_log2: int = 6
+    p: int = 2
+    tau_num: int = 2
+    tau_log2_den: int = 0
+    delta_q: int = 8
+    flags: int = 0
+
+    def c(self) -> DkvParams:
+        return DkvParams(self.sigma2_log2, self.p, self.tau_num, self.tau_log2_den, self.delta_q, self.flags)
+
+
+def _dtype_code(dt: torch.dtype) -> int:
+    if dt == torch.bfloat16:
+        return DKV_BF16
+    if dt == torch.float32:
+        return DKV_F32
+    raise ValueError(f"unsupported dtype {dt}")
+
+
+class Bank:
+    """Device state of B = num_banks (layer, head) banks, row stride `capacity`."""
+
+    def __init__(self, num_banks: int, capacity: int, head_dim: int, dtype=torch.bfloat16,
+                 group_size: int = 1, budget=None, device="cuda"):
+        self.B, self.Mcap, self.d, self.gs = num_banks, capacity, head_dim, group_size
+        self.dtype = dtype
+        dev = torch.device(device)
+        self.k = torch.zeros(num_banks, capacity, head_dim, dtype=dtype, device=dev)
+        self.v = torch.zeros_like(self.k)
+        self.knorm = torch.zeros(num_banks, capacity, dtype=torch.float32, device=dev)
+        self.rho = torch.zeros(num_banks, capacity, dtype=torch.int64, device=dev)
+        self.base = torch.zeros_like(self.rho)
+        self.prov = torch.zeros_like(self.rho)
+        self.occupancy = torch.zeros(num_banks, dtype=torch.int32, device=dev)
+        if budget is None:
+            budget = torch.full((num_banks,), capacity, dtype=torch.int32)
+        self.budget = torch.as_tensor(budget, dtype=torch.int32).to(dev).contiguous()
+
+    def c(self) -> DkvBank:
+        return DkvBank(self.B, self.gs, self.d, self.Mcap, _dtype_code(self.dtype), self.k.data_ptr(),
+                       self.v.data_ptr(), self.knorm.data_ptr(), self.rho.data_ptr(), self.base.data_ptr(),
+                       self.prov.data_ptr(), self.occupancy.data_ptr(), self.budget.data_ptr())
+
+    def state_dict(self):
+        """Checkpoint of the bank state (device tensors cloned)."""
+        return {n: getattr(self, n).clone() for n in ("k", "v", "knorm", "rho", "base", "prov", "occupancy", "budget")}
+
+    def load_state_dict(self, sd):
+        for n, t in sd.items():
+            getattr(self, n).copy_(t)
+
+
+def workspace_size(bank: Bank, n_cand: int) -> int:
+    out = ctypes.c_size_t(0)
+    cb = bank.c()
+    _check(lib().densitykv_workspace_size(ctypes.byref(cb), int(n_cand), ctypes.byref(out)), "workspace_size")
+    return int(out.value)
+
+
+def alloc_workspace(bank: Bank, n_cand: int) -> torch.Tensor:
+    return torch.empty(workspace_size(bank, n_cand), dtype=torch.uint8, device=bank.k.device)
+
+
+def _segment(seg_k: Optional[torch.Tensor], seg_v: Optional[torch.Tensor], n: int, block_id: int):
+    return DkvSegment(int(n), int(block_id), None if seg_k is None else seg_k.data_ptr(),
+                      None if seg_v is None else seg_v.data_ptr())
+
+
+def _check_seg(bank: Bank, seg_k, seg_v):
+    if seg_k is None:
+        return 0
+    if seg_k.dim() != 3 or seg_k.shape[0] != bank.B or seg_k.shape[2] != bank.d:
+        raise ValueError("segment keys must be [num_banks, n, head_dim]")
+    if seg_v is None or seg_v.shape != seg_k.shape:
+        raise ValueError("segment values must match the keys' shape")
+    for t in (seg_k, seg_v):
+        if t.dtype != bank.dtype or not t.is_contiguous() or t.device != bank.k.device:
+            raise ValueError("segment tensors must be contiguous, on the bank's device, in the bank dtype")
+    return int(seg_k.shape[1])
+
+
+def score(bank: Bank, seg_k: torch.Tensor, seg_v: torch.Tensor, params: Params = Params(),
+          want_q=True, want_f32=True, want_density=False, workspace: Optional[torch.Tensor] = None):
+    """densitykv_score: returns (score_q [B,N] int64 | None, score_f32 [B,N] | None, density [B,Mcap] | None)."""
+    n = _check_seg(bank, seg_k, seg_v)
+    dev = bank.k.device
+    sq = torch.zeros(bank.B, n, dtype=torch.int64, device=dev) if want_q else None
+    sf = torch.zeros(bank.B, n, dtype=torch.float32, device=dev) if want_f32 else None
+    dens = torch.zeros(bank.B, bank.Mcap, dtype=torch.int64, device=dev) if want_density else None
+    ws = workspace if workspace is not None else alloc_workspace(bank, n)
+    cb, cs, cp = bank.c(), _segment(seg_k, seg_v, n, 0), params.c()
+    _check(lib().densitykv_score(ctypes.byref(cb), ctypes.byref(cs), ctypes.byref(cp), _ptr(sq), _ptr(sf),
+                                 _ptr(dens), _ptr(ws), ws.numel(), _stream()), "score")
+    return sq, sf, dens
+
+
+class UpdateOut:
+    """Optional device outputs of one update (allocated on request)."""
+
+    def __init__(self, bank: Bank, n: int, trace: bool = False):
+        dev, B = bank.k.device, bank.B
+        G = B // bank.gs
+        i32 = dict(dtype=torch.int32, device=dev)
+        self.r_star = torch.zeros(G, **i32)
+        self.n_admitted = torch.zeros(B, **i32)
+        self.n_evicted = torch.zeros(B, **i32)
+        self.admitted = torch.zeros(B, max(n, 1), **i32)
+        self.evicted = torch.zeros(B, bank.Mcap, **i32)
+        self.order = torch.zeros(B, max(n, 1), **i32) if trace else None
+        self.score_q = torch.zeros(B, max(n, 1), dtype=torch.int64, device=dev) if trace else None
+        self.first_cross = torch.full((B, bank.Mcap), -1, **i32) if trace else None
+        self.rho_tilde = torch.zeros(B, bank.Mcap, dtype=torch.int64, device=dev) if trace else None
+
+    def c(self) -> DkvUpdateOut:
+        f = lambda t: None if t is None else t.data_ptr()
+        return DkvUpdateOut(f(self.r_star), f(self.n_admitted), f(self.n_evicted), f(self.admitted),
+                            f(self.evicted), f(self.order), f(self.score_q), f(self.first_cross),
+                            f(self.rho_tilde))
+
+
+def update_bank(bank: Bank, seg_k: Optional[torch.Tensor], seg_v: Optional[torch.Tensor], block_id: int,
+                params: Params = Params(), workspace: Optional[torch.Tensor] = None,
+                out: Optional[UpdateOut] = None) -> Optional[UpdateOut]:
+    """densitykv_update_bank: updates `bank` in place on the current stream."""
+    n = _check_seg(bank, seg_k, seg_v)
+    ws = workspace if workspace is not None else alloc_workspace(bank, n)
+    cb, cs, cp = bank.c(), _segment(seg_k, seg_v, n, block_id), params.c()
+    co = out.c() if out is not None else None
+    _check(lib().densitykv_update_bank(ctypes.byref(cb), ctypes.byref(cs), ctypes.byref(cp),
+                                       ctypes.byref(co) if co is not None else None, _ptr(ws), ws.numel(),
+                                       _stream()), "update_bank")
+    return out
+
+
+def bank_attention(bank: Bank, q: torch.Tensor, win_k: Optional[torch.Tensor], win_v: Optional[torch.Tensor],
+                   softmax_scale: Optional[float] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """densitykv_bank_attention: softmax(q [bank; window]^T * scale) [bank; window]."""
+    if q.dim() != 3 or q.shape[0] != bank.B or q.shape[2] != bank.d or q.dtype != bank.dtype or not q.is_contiguous():
+        raise ValueError("q must be a contiguous [num_banks, n_query, head_dim] tensor in the bank dtype")
+    nw = 0
+    if win_k is not None:
+        if win_k.shape[0] != bank.B or win_k.shape[2] != bank.d or win_v is None or win_v.shape != win_k.shape:
+            raise ValueError("window must be [num_banks, n_window, head_dim] keys and values")
+        if not (win_k.is_contiguous() and win_v.is_contiguous()) or win_k.dtype != bank.dtype or win_v.dtype != bank.dtype:
+            raise ValueError("window tensors must be contiguous in the bank dtype")
+        nw = int(win_k.shape[1])
+    if out is None:
+        out = torch.empty_like(q)
+    scale = (1.0 / bank.d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    cb = bank.c()
+    _check(lib().densitykv_bank_attention(ctypes.byref(cb), _ptr(q), int(q.shape[1]), _ptr(win_k), _ptr(win_v),
+                                          nw, _ptr(out), ctypes.c_float(scale), _stream()), "bank_attention")
+    return out
+
+
+def pair_weight_q23(d2: torch.Tensor, params: Params = Params()) -> torch.Tensor:
+    """densitykv_pair_weight_q23 over a float32 device tensor of squared distances."""
+    d2 = d2.contiguous()
+    w = torch.empty(d2.shape, dtype=torch.int32, device=d2.device)
+    cp = params.c()
+    _check(lib().densitykv_pair_weight_q23(_ptr(d2), d2.numel(), ctypes.byref(cp), _ptr(w), _stream()),
+           "pair_weight_q23")
+    return w

@@ -1,0 +1,196 @@
+// C ABI of the DensityKV hot path: argument checks, workspace carving and the
+// enqueueing of the kernel sequences (see include/densitykv.h for the contract).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+
+#include "dkv_internal.hpp"
+
+namespace dkv {
+
+static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t workspace_layout(int B, int G, int Mcap, int N, Workspace *ws, char *base) {
+  size_t off = 0;
+  const size_t Bz = (size_t)B, Mz = (size_t)Mcap, Nz = (size_t)(N > 0 ? N : 1);
+  const int nck = (N + kCkStride - 1) / kCkStride;
+  auto take = [&](size_t bytes) -> char * {
+    char *p = base ? base + off : nullptr;
+    off += align256(bytes);
+    return p;
+  };
+  Workspace w{};
+  w.m = (int32_t *)take(Bz * 4);
+  w.M = (int32_t *)take(Bz * 4);
+  w.R = (int32_t *)take(Bz * 4);
+  w.E = (int32_t *)take(Bz * 4);
+  w.e = (int32_t *)take(Bz * 4);
+  w.r_star = (int32_t *)take((size_t)G * 4);
+  w.n_ev = (int32_t *)take(Bz * 4);
+  w.m_new = (int32_t *)take(Bz * 4);
+  w.cnorm = (float *)take(Bz * Nz * 4);
+  w.bs = (float *)take(Bz * Mz * 4);
+  w.acol = (int64_t *)take(Bz * Nz * 8);
+  w.wcol = (int64_t *)take(Bz * Nz * 8);
+  w.skey = (uint64_t *)take(Bz * Nz * 8);
+  w.order = (int32_t *)take(Bz * Nz * 4);
+  w.rank = (int32_t *)take(Bz * Nz * 4);
+  w.first = (int32_t *)take(Bz * Mz * 4);
+  w.ck = (uint32_t *)take(Bz * Mz * (size_t)(nck > 0 ? nck : 1) * 4);
+  w.rho_t = (int64_t *)take(Bz * Mz * 8);
+  w.dest = (int32_t *)take(Bz * Mz * 4);
+  w.ev_list = (int32_t *)take(Bz * Mz * 4);
+  w.adm_list = (int32_t *)take(Bz * Nz * 4);
+  w.adm_dest = (int32_t *)take(Bz * Nz * 4);
+  w.sub = (int64_t *)take(Bz * Mz * 8);
+  w.sub_adm = (int64_t *)take(Bz * Nz * 8);
+  w.mut_adm = (int64_t *)take(Bz * Nz * 8);
+  w.nck = nck > 0 ? nck : 1;
+  if (ws) *ws = w;
+  return off;
+}
+
+}  // namespace dkv
+
+using namespace dkv;
+
+namespace {
+
+int check_bank(const dkv_bank *bk) {
+  if (!bk) return DKV_ERR_INVALID;
+  if (bk->dtype != DKV_BF16 && bk->dtype != DKV_F32) return DKV_ERR_INVALID;
+  if (bk->head_dim != 64 && bk->head_dim != 128) return DKV_ERR_UNSUPPORTED;
+  if (bk->num_banks < 1 || bk->group_size < 1 || bk->num_banks % bk->group_size != 0) return DKV_ERR_SHAPE;
+  if (bk->capacity < 1 || bk->capacity > DKV_MAX_CAPACITY) return DKV_ERR_SHAPE;
+  if (!bk->k || !bk->v || !bk->knorm || !bk->rho || !bk->base || !bk->prov || !bk->occupancy || !bk->budget)
+    return DKV_ERR_INVALID;
+  return DKV_OK;
+}
+
+int check_segment(const dkv_segment *sg) {
+  if (!sg) return DKV_ERR_INVALID;
+  if (sg->n < 0 || sg->n > DKV_MAX_CANDIDATES) return DKV_ERR_SHAPE;
+  if (sg->block_id < 0 || sg->block_id > DKV_MAX_BLOCK_ID) return DKV_ERR_RANGE;
+  if (sg->n > 0 && (!sg->k || !sg->v)) return DKV_ERR_INVALID;
+  return DKV_OK;
+}
+
+int check_params(const dkv_params *p, Prm *out, int block_id) {
+  if (!p) return DKV_ERR_INVALID;
+  if (p->flags != 0) return DKV_ERR_INVALID;
+  if (p->p != 1 && p->p != 2 && p->p != 4) return DKV_ERR_UNSUPPORTED;
+  if (p->sigma2_log2 < -8 || p->sigma2_log2 > 16) return DKV_ERR_UNSUPPORTED;
+  if (p->tau_log2_den < 0 || p->tau_log2_den > 8) return DKV_ERR_RANGE;
+  if (p->tau_num < 1 || p->tau_num > (1 << 16)) return DKV_ERR_RANGE;
+  if (p->tau_num <= (1 << p->tau_log2_den)) return DKV_ERR_RANGE;  // tau > 1
+  if (p->delta_q < 1 || p->delta_q > (int64_t(1) << 40)) return DKV_ERR_RANGE;
+  out->inv_sigma2 = ldexpf(1.0f, -p->sigma2_log2);
+  out->p = p->p;
+  out->tau_num = p->tau_num;
+  out->tau_shift = p->tau_log2_den;
+  out->delta_q = p->delta_q;
+  out->block_id = block_id;
+  return DKV_OK;
+}
+
+Geom geom_of(const dkv_bank *bk, int n) {
+  Geom g;
+  g.B = bk->num_banks;
+  g.gs = bk->group_size;
+  g.G = bk->num_banks / bk->group_size;
+  g.d = bk->head_dim;
+  g.Mcap = bk->capacity;
+  g.N = n;
+  g.dtype = bk->dtype;
+  return g;
+}
+
+}  // namespace
+
+extern "C" {
+
+int densitykv_workspace_size(const dkv_bank *bank, int32_t n_cand, size_t *bytes) {
+  int rc = check_bank(bank);
+  if (rc) return rc;
+  if (!bytes) return DKV_ERR_INVALID;
+  if (n_cand < 0 || n_cand > DKV_MAX_CANDIDATES) return DKV_ERR_SHAPE;
+  *bytes = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity, n_cand,
+                            nullptr, nullptr);
+  return DKV_OK;
+}
+
+int densitykv_score(const dkv_bank *bank, const dkv_segment *seg, const dkv_params *prm,
+                    int64_t *cand_score_q, float *cand_score_f32, int64_t *bank_density_q,
+                    void *workspace, size_t workspace_bytes, void *stream) {
+  int rc = check_bank(bank);
+  if (!rc) rc = check_segment(seg);
+  Prm p{};
+  if (!rc) rc = check_params(prm, &p, seg->block_id);
+  if (rc) return rc;
+  Workspace ws{};
+  const size_t need = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity,
+                                       seg->n, &ws, static_cast<char *>(workspace));
+  if (!workspace || workspace_bytes < need) return DKV_ERR_WORKSPACE;
+  const Geom g = geom_of(bank, seg->n);
+  hipError_t e = launch_score(*bank, *seg, g, p, cand_score_q, cand_score_f32, bank_density_q, ws,
+                              static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DKV_OK : DKV_ERR_HIP;
+}
+
+int densitykv_update_bank(dkv_bank *bank, const dkv_segment *seg, const dkv_params *prm, dkv_update_out *out,
+                          void *workspace, size_t workspace_bytes, void *stream) {
+  int rc = check_bank(bank);
+  if (!rc) rc = check_segment(seg);
+  Prm p{};
+  if (!rc) rc = check_params(prm, &p, seg->block_id);
+  if (rc) return rc;
+  Workspace ws{};
+  const size_t need = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity,
+                                       seg->n, &ws, static_cast<char *>(workspace));
+  if (!workspace || workspace_bytes < need) return DKV_ERR_WORKSPACE;
+  const Geom g = geom_of(bank, seg->n);
+  hipError_t e = launch_update(*bank, *seg, g, p, out, ws, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DKV_OK : DKV_ERR_HIP;
+}
+
+int densitykv_bank_attention(const dkv_bank *bank, const void *q, int32_t n_query, const void *win_k,
+                             const void *win_v, int32_t n_window, void *out, float softmax_scale,
+                             void *stream) {
+  int rc = check_bank(bank);
+  if (rc) return rc;
+  if (n_query < 0 || n_window < 0 || n_query > (1 << 24) || n_window > (1 << 24)) return DKV_ERR_SHAPE;
+  if (n_query > 0 && (!q || !out)) return DKV_ERR_INVALID;
+  if (n_window > 0 && (!win_k || !win_v)) return DKV_ERR_INVALID;
+  if (!(softmax_scale > 0.0f) || softmax_scale > 1e6f) return DKV_ERR_RANGE;
+  const Geom g = geom_of(bank, 0);
+  hipError_t e = launch_attention(*bank, q, n_query, win_k, win_v, n_window, out, softmax_scale, g,
+                                  static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DKV_OK : DKV_ERR_HIP;
+}
+
+int densitykv_pair_weight_q23(const float *d2, int64_t n, const dkv_params *prm, int32_t *w_q23,
+                              void *stream) {
+  Prm p{};
+  int rc = check_params(prm, &p, 0);
+  if (rc) return rc;
+  if (n < 0) return DKV_ERR_SHAPE;
+  if (n > 0 && (!d2 || !w_q23)) return DKV_ERR_INVALID;
+  hipError_t e = launch_pair_weight(d2, n, p, w_q23, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DKV_OK : DKV_ERR_HIP;
+}
+
+const char *densitykv_status_string(int status) {
+  switch (status) {
+    case DKV_OK: return "ok";
+    case DKV_ERR_INVALID: return "invalid argument";
+    case DKV_ERR_SHAPE: return "shape or size out of range";
+    case DKV_ERR_UNSUPPORTED: return "unsupported head_dim, p or sigma^2";
+    case DKV_ERR_WORKSPACE: return "workspace missing or too small";
+    case DKV_ERR_RANGE: return "parameter out of fixed-point range";
+    case DKV_ERR_HIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

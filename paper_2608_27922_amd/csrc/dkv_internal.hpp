@@ -1,0 +1,115 @@
+// Internal declarations shared by the DensityKV HIP sources (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/densitykv.h"
+
+namespace dkv {
+
+constexpr uint32_t kQ23 = 1u << 23;          // weight 1.0 in fixed point
+constexpr uint32_t kMagic = 0x4B000000u;     // bit pattern of 2^23 as binary32
+constexpr int kCkStride = 256;               // prefix checkpoint spacing (candidates)
+constexpr int kSortMax = 8192;               // padded sort size (N <= 8191)
+
+// ---------------------------------------------------------------------------
+// Workspace: one carve of the caller's buffer, every array 256-byte aligned.
+// ---------------------------------------------------------------------------
+struct Workspace {
+  int32_t *m;          // [B] occupancy on entry (clamped)
+  int32_t *M;          // [B] budget (clamped to [0, Mcap])
+  int32_t *R;          // [B] largest tested prefix of the bank's group
+  int32_t *E;          // [B] score exponent
+  int32_t *e;          // [B] e_{r*}
+  int32_t *r_star;     // [G]
+  int32_t *n_ev;       // [B]
+  int32_t *m_new;      // [B]
+  float *cnorm;        // [B, N]   |k_x|^2 of candidates
+  float *bs;           // [B, Mcap] score scale of each bank state
+  int64_t *acol;       // [B, N]   S_x
+  int64_t *wcol;       // [B, N]   sum_i W_ix over the whole pre-update bank
+  uint64_t *skey;      // [B, N]   sort keys (S_x << 13) | x
+  int32_t *order;      // [B, N]   pi
+  int32_t *rank;       // [B, N]   position of x in pi
+  int32_t *first;      // [B, Mcap] first crossing prefix length
+  uint32_t *ck;        // [B, Mcap, nck] prefix sums over each 256-candidate tile
+  int64_t *rho_t;      // [B, Mcap] rho + P(r*)
+  int32_t *dest;       // [B, Mcap] final slot of each pre-update slot, -1 if evicted
+  int32_t *ev_list;    // [B, Mcap] evicted slots ascending
+  int32_t *adm_list;   // [B, N]   admitted source indices ascending
+  int32_t *adm_dest;   // [B, N]   final slot of each admitted candidate
+  int64_t *sub;        // [B, Mcap] sum of weights to the evicted states (survivors)
+  int64_t *sub_adm;    // [B, N]   sum of weights to the evicted states (admitted)
+  int64_t *mut_adm;    // [B, N]   sum of weights to all admitted (admitted, incl. self)
+  int nck;
+};
+
+size_t workspace_layout(int B, int G, int Mcap, int N, Workspace *ws, char *base);
+
+// Geometry and parameters passed by value to every kernel.
+struct Geom {
+  int B, G, gs, d, Mcap, N, dtype;
+};
+struct Prm {
+  float inv_sigma2;  // 2^-sigma2_log2 (exact)
+  int p;
+  int tau_num, tau_shift;
+  int64_t delta_q;
+  int block_id;
+};
+
+// Launchers (host functions defined in the .hip sources; return hipError_t).
+hipError_t launch_update(const dkv_bank &bank, const dkv_segment &seg, const Geom &g,
+                         const Prm &p, const dkv_update_out *out, const Workspace &ws,
+                         hipStream_t s);
+hipError_t launch_score(const dkv_bank &bank, const dkv_segment &seg, const Geom &g,
+                        const Prm &p, int64_t *score_q, float *score_f32, int64_t *density,
+                        const Workspace &ws, hipStream_t s);
+hipError_t launch_attention(const dkv_bank &bank, const void *q, int nq, const void *wk,
+                            const void *wv, int nw, void *out, float scale, const Geom &g,
+                            hipStream_t s);
+hipError_t launch_pair_weight(const float *d2, int64_t n, const Prm &p, int32_t *w,
+                              hipStream_t s);
+
+#if defined(__HIPCC__)
+// ---------------------------------------------------------------------------
+// Device helpers
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {  // RNE, finite inputs
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+template <int DT>
+__device__ __forceinline__ float load_elem(const void *p, size_t i) {
+  if constexpr (DT == DKV_BF16) {
+    return bf16_bits_to_f32(static_cast<const uint16_t *>(p)[i]);
+  } else {
+    return static_cast<const float *>(p)[i];
+  }
+}
+
+// Soft-Riesz weight (eps = 1): w = 1 / (1 + d2 / sigma^2)^p, each step one
+// binary32 operation rounded to nearest even; the reciprocal is the IEEE
+// correctly rounded division.  d2 * inv_sigma2 is exact (power of two).
+__device__ __forceinline__ float pair_weight(float d2, float inv_sigma2, int p) {
+  float t = 1.0f + d2 * inv_sigma2;
+  float tp = t;
+  if (p >= 2) tp = t * t;
+  if (p == 4) tp = tp * tp;
+  return 1.0f / tp;
+}
+// RNE(w * scale) for w * scale in [0, 2^23]: fma(w, scale, 2^23) lands in
+// [2^23, 2^24] where one ulp is 1, so its bit pattern minus that of 2^23 is
+// the rounded integer.
+__device__ __forceinline__ uint32_t q23_round(float w, float scale) {
+  return __float_as_uint(__builtin_fmaf(w, scale, 8388608.0f)) - kMagic;
+}
+#endif
+
+}  // namespace dkv

@@ -1,0 +1,821 @@
+// DensityKV bank update and candidate scoring on gfx950.
+//
+// One update of every bank from one block (Supp. C, Algorithm 1) is the kernel
+// sequence below, all on the caller's stream, with r* kept on the device:
+//
+//   k_prep          clamp occupancy/budget, tested prefix R of the group (Eq. 11),
+//                   score scale 1/b of every bank state (Eq. 6)
+//   k_cand_norms    |k_x|^2 of every candidate
+//   k_score_gram    S_x = sum_i RNE(w_ix / b_i scaled) and Wcol_x = sum_i W_ix (Eq. 6)
+//   k_sort          stable ascending order of S_x, ties by source index (Alg. 1)
+//   k_cross_gram    prefix sums over the ordered candidates, first violating
+//                   prefix of every bank state (Eqs. 8-9), tile checkpoints
+//   k_feasible      c_r for every r, e_r (Eq. 10), r* of each group (Eq. 11)
+//   k_fixup         projected density rho~(r*) of every bank state
+//   k_select        mandatory + densest eviction (Sec. 3.4 step 3), commit plan
+//   k_maint_gram    weights to the evicted and to the co-admitted states (Supp. C)
+//   k_commit        exact density maintenance, baselines (Eq. 5), K/V placement
+//
+// Arithmetic: keys on the 1/64 grid give exact fp32 inner products; weights are
+// binary32 with round-to-nearest-even; every sum is an integer sum of Q23
+// terms, so results do not depend on tiling or thread order.
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+#include "dkv_internal.hpp"
+
+namespace dkv {
+
+namespace {
+
+constexpr int kThreads = 256;    // Gram kernels: one thread per row item
+constexpr int kTile = 32;        // columns staged in LDS per step
+constexpr int kBig = 1024;       // one-workgroup-per-bank kernels
+constexpr uint64_t kRhoMax = (1ull << 40) - 1;
+
+__device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
+
+// ---------------------------------------------------------------------------
+// Block-wide scans for kBig threads (16 waves of 64 lanes).
+// ---------------------------------------------------------------------------
+__device__ int block_excl_scan(int v, int *total, int *tmp /*[16]*/) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) tmp[wid] = x;
+  __syncthreads();
+  if (wid == 0) {
+    int t = lane < nw ? tmp[lane] : 0;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      int y = __shfl_up(t, o, 64);
+      if (lane >= o) t += y;
+    }
+    if (lane < nw) tmp[lane] = t;
+  }
+  __syncthreads();
+  int pre = (wid > 0 ? tmp[wid - 1] : 0) + x - v;
+  *total = tmp[nw - 1];
+  __syncthreads();
+  return pre;
+}
+
+__device__ int block_max(int v, int *tmp) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+  if (lane == 0) tmp[wid] = v;
+  __syncthreads();
+  int r = tmp[0];
+  for (int w = 1; w < nw; ++w) r = max(r, tmp[w]);
+  __syncthreads();
+  return r;
+}
+
+// Row key loaded into registers as float.
+template <int D, int DT>
+__device__ __forceinline__ void load_row(float (&kr)[D], const void *base, size_t row) {
+#pragma unroll
+  for (int j = 0; j < D; ++j) kr[j] = load_elem<DT>(base, row * D + j);
+}
+
+template <int D>
+__device__ __forceinline__ float dot_row(const float (&kr)[D], const float *col) {
+  float g = 0.0f;
+#pragma unroll
+  for (int j = 0; j < D; ++j) g = __builtin_fmaf(kr[j], col[j], g);
+  return g;
+}
+
+// ---------------------------------------------------------------------------
+// k_prep: one workgroup (256 threads) per bank.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_prep(dkv_bank bank, Geom g, Workspace ws) {
+  const int b = blockIdx.x;
+  __shared__ float red[kThreads / 64];
+  const int Mb = clampi(bank.budget[b], 0, g.Mcap);
+  const int m = clampi(bank.occupancy[b], 0, Mb);
+  // Tested prefix lengths 0..R: R = min(N, every budget of the group).
+  int R = g.N;
+  const int g0 = (b / g.gs) * g.gs;
+  for (int j = 0; j < g.gs; ++j) R = min(R, clampi(bank.budget[g0 + j], 0, g.Mcap));
+  // Score scale: inv_i = fp32(2^23 / b_i) (fp64 division, one rounding to fp32);
+  // E = binary exponent of max_i inv_i; bs_i = inv_i * 2^(23 - E) <= 2^23.
+  float mx = 0.0f;
+  for (int i = threadIdx.x; i < m; i += kThreads) {
+    int64_t bi = bank.base[(size_t)b * g.Mcap + i];
+    bi = bi < 1 ? 1 : bi;
+    float inv = (float)(8388608.0 / (double)bi);
+    mx = fmaxf(mx, inv);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  int E = 0;
+  if (m > 0) frexpf(mx, &E);
+  for (int i = threadIdx.x; i < m; i += kThreads) {
+    int64_t bi = bank.base[(size_t)b * g.Mcap + i];
+    bi = bi < 1 ? 1 : bi;
+    float inv = (float)(8388608.0 / (double)bi);
+    ws.bs[(size_t)b * g.Mcap + i] = ldexpf(inv, 23 - E);
+  }
+  if (threadIdx.x == 0) {
+    ws.m[b] = m;
+    ws.M[b] = Mb;
+    ws.R[b] = R;
+    ws.E[b] = E;
+  }
+}
+
+template <int D, int DT>
+__global__ __launch_bounds__(kThreads) void k_cand_norms(const void *seg_k, Geom g, Workspace ws) {
+  const int b = blockIdx.y, x = blockIdx.x * kThreads + threadIdx.x;
+  if (x >= g.N) return;
+  const size_t row = (size_t)b * g.N + x;
+  float s = 0.0f;
+  for (int j = 0; j < D; ++j) {
+    float v = load_elem<DT>(seg_k, row * D + j);
+    s = __builtin_fmaf(v, v, s);
+  }
+  ws.cnorm[row] = s;
+}
+
+// ---------------------------------------------------------------------------
+// k_score_gram: thread = candidate x; loop over every bank state i.
+// ---------------------------------------------------------------------------
+template <int D, int DT>
+__global__ __launch_bounds__(kThreads) void k_score_gram(dkv_bank bank, const void *seg_k, Geom g,
+                                                         Prm p, Workspace ws, int64_t *out_q,
+                                                         float *out_f) {
+  const int b = blockIdx.y, x = blockIdx.x * kThreads + threadIdx.x;
+  const int m = ws.m[b];
+  const bool act = x < g.N;
+  __shared__ float tk[kTile][D];
+  __shared__ float tn[kTile], tb[kTile];
+  float kr[D];
+  float nr = 0.0f;
+  if (act) {
+    load_row<D, DT>(kr, seg_k, (size_t)b * g.N + x);
+    nr = ws.cnorm[(size_t)b * g.N + x];
+  }
+  uint64_t A = 0, Wsum = 0;
+  for (int i0 = 0; i0 < m; i0 += kTile) {
+    const int nc = min(kTile, m - i0);
+    __syncthreads();
+    for (int t = threadIdx.x; t < kTile * D; t += kThreads) {
+      const int c = t / D, j = t % D;
+      tk[c][j] = c < nc ? load_elem<DT>(bank.k, ((size_t)b * g.Mcap + i0 + c) * D + j) : 0.0f;
+    }
+    if (threadIdx.x < kTile) {
+      const int c = threadIdx.x;
+      tn[c] = c < nc ? bank.knorm[(size_t)b * g.Mcap + i0 + c] : 0.0f;
+      tb[c] = c < nc ? ws.bs[(size_t)b * g.Mcap + i0 + c] : 0.0f;
+    }
+    __syncthreads();
+    if (act) {
+      uint32_t a32 = 0, w32 = 0;
+      for (int c = 0; c < nc; ++c) {
+        const float gd = dot_row<D>(kr, tk[c]);
+        const float d2 = (nr + tn[c]) - 2.0f * gd;
+        const float w = pair_weight(d2, p.inv_sigma2, p.p);
+        a32 += q23_round(w, tb[c]);
+        w32 += q23_round(w, 8388608.0f);
+      }
+      A += a32;
+      Wsum += w32;
+    }
+  }
+  if (!act) return;
+  const size_t o = (size_t)b * g.N + x;
+  if (ws.acol) {
+    ws.acol[o] = (int64_t)A;
+    ws.wcol[o] = (int64_t)Wsum;
+    ws.skey[o] = (A << 13) | (uint64_t)x;
+  }
+  if (out_q) out_q[o] = (int64_t)A;
+  if (out_f) out_f[o] = m > 0 ? (float)(ldexp((double)A, ws.E[b] - 23) / (double)m) : 0.0f;
+}
+
+// ---------------------------------------------------------------------------
+// k_sort: bitonic sort of the unique keys of one bank in LDS.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBig) void k_sort(Geom g, Workspace ws, int32_t *out_order) {
+  const int b = blockIdx.x;
+  __shared__ uint64_t s[kSortMax];
+  int P = 2;
+  while (P < g.N) P <<= 1;
+  for (int i = threadIdx.x; i < P; i += kBig)
+    s[i] = i < g.N ? ws.skey[(size_t)b * g.N + i] : ~0ull;
+  __syncthreads();
+  for (int k = 2; k <= P; k <<= 1) {
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int t = threadIdx.x; t < (P >> 1); t += kBig) {
+        const int i = ((t / j) * 2 * j) + (t % j);
+        const int ij = i + j;
+        const bool up = (i & k) == 0;
+        const uint64_t a = s[i], c = s[ij];
+        if ((a > c) == up) {
+          s[i] = c;
+          s[ij] = a;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int j = threadIdx.x; j < g.N; j += kBig) {
+    const int x = (int)(s[j] & 0x1FFFull);
+    ws.order[(size_t)b * g.N + j] = x;
+    ws.rank[(size_t)b * g.N + x] = j;
+    if (out_order) out_order[(size_t)b * g.N + j] = x;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_cross_gram: thread = bank state i; running prefix over the ordered
+// candidates; first prefix length r with 2^k (rho_i + P_i(r)) >= T b_i.
+// ---------------------------------------------------------------------------
+template <int D, int DT>
+__global__ __launch_bounds__(kThreads) void k_cross_gram(dkv_bank bank, const void *seg_k, Geom g,
+                                                         Prm p, Workspace ws, int32_t *out_first) {
+  const int b = blockIdx.y, i = blockIdx.x * kThreads + threadIdx.x;
+  const int m = ws.m[b], R = ws.R[b];
+  if (blockIdx.x * kThreads >= m) return;  // uniform: no live state in this block
+  const bool act = i < m;
+  __shared__ float tk[kTile][D];
+  __shared__ float tn[kTile];
+  float kr[D];
+  float nr = 0.0f;
+  int64_t thr = 0;
+  const size_t row = (size_t)b * g.Mcap + i;
+  if (act) {
+    load_row<D, DT>(kr, bank.k, row);
+    nr = bank.knorm[row];
+    const int64_t lim = ((int64_t)p.tau_num * bank.base[row] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
+    thr = lim - bank.rho[row];
+  }
+  int first = thr <= 0 ? 0 : R + 1;
+  int64_t P = 0;
+  uint32_t tile_sum = 0;
+  for (int j0 = 0; j0 < R; j0 += kTile) {
+    const int nc = min(kTile, R - j0);
+    __syncthreads();
+    for (int t = threadIdx.x; t < kTile * D; t += kThreads) {
+      const int c = t / D, j = t % D;
+      float v = 0.0f;
+      if (c < nc) {
+        const int x = ws.order[(size_t)b * g.N + j0 + c];
+        v = load_elem<DT>(seg_k, ((size_t)b * g.N + x) * D + j);
+      }
+      tk[c][j] = v;
+    }
+    if (threadIdx.x < kTile) {
+      const int c = threadIdx.x;
+      tn[c] = c < nc ? ws.cnorm[(size_t)b * g.N + ws.order[(size_t)b * g.N + j0 + c]] : 0.0f;
+    }
+    __syncthreads();
+    if (act) {
+      for (int c = 0; c < nc; ++c) {
+        const float gd = dot_row<D>(kr, tk[c]);
+        const float d2 = (nr + tn[c]) - 2.0f * gd;
+        const uint32_t W = q23_round(pair_weight(d2, p.inv_sigma2, p.p), 8388608.0f);
+        P += W;
+        tile_sum += W;
+        if (first > R && P >= thr) first = j0 + c + 1;
+        const int done = j0 + c + 1;
+        if ((done % kCkStride) == 0) {
+          ws.ck[row * ws.nck + (done / kCkStride - 1)] = tile_sum;
+          tile_sum = 0;
+        }
+      }
+    }
+  }
+  if (!act) return;
+  ws.first[row] = first;
+  if (out_first) out_first[row] = first;
+}
+
+// ---------------------------------------------------------------------------
+// k_feasible: one workgroup per group.  c_r = #{i : first_i <= r}; feasible
+// iff c_r <= e_r for every bank of the group; r* = largest feasible r.
+// ---------------------------------------------------------------------------
+__device__ void block_inclusive_scan_lds(int *a, int n, int *tmp) {
+  const int per = (n + kBig - 1) / kBig;
+  const int lo = min(n, (int)threadIdx.x * per), hi = min(n, lo + per);
+  int s = 0;
+  for (int i = lo; i < hi; ++i) s += a[i];
+  int tot;
+  int pre = block_excl_scan(s, &tot, tmp);
+  for (int i = lo; i < hi; ++i) {
+    pre += a[i];
+    a[i] = pre;
+  }
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kBig) void k_feasible(Geom g, Workspace ws, int32_t *out_rstar) {
+  const int grp = blockIdx.x;
+  __shared__ int hist[kSortMax + 1];
+  __shared__ unsigned char ok[kSortMax + 1];
+  __shared__ int tmp[16];
+  const int b0 = grp * g.gs;
+  const int R = ws.R[b0];
+  for (int r = threadIdx.x; r <= R; r += kBig) ok[r] = 1;
+  for (int j = 0; j < g.gs; ++j) {
+    const int b = b0 + j;
+    const int m = ws.m[b], M = ws.M[b];
+    for (int r = threadIdx.x; r <= R; r += kBig) hist[r] = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < m; i += kBig) {
+      const int t = ws.first[(size_t)b * g.Mcap + i];
+      if (t <= R) atomicAdd(&hist[t], 1);
+    }
+    __syncthreads();
+    block_inclusive_scan_lds(hist, R + 1, tmp);
+    for (int r = threadIdx.x; r <= R; r += kBig) {
+      const int e = max(0, m + r - M);
+      if (hist[r] > e) ok[r] = 0;
+    }
+    __syncthreads();
+  }
+  int best = 0;
+  for (int r = threadIdx.x; r <= R; r += kBig)
+    if (ok[r]) best = max(best, r);
+  best = block_max(best, tmp);
+  if (threadIdx.x == 0) {
+    ws.r_star[grp] = best;
+    if (out_rstar) out_rstar[grp] = best;
+  }
+  for (int j = threadIdx.x; j < g.gs; j += kBig) {
+    const int b = b0 + j;
+    ws.e[b] = max(0, ws.m[b] + best - ws.M[b]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_fixup: rho~_i(r*) = rho_i + checkpointed tiles + the partial tile.
+// ---------------------------------------------------------------------------
+template <int D, int DT>
+__global__ __launch_bounds__(kThreads) void k_fixup(dkv_bank bank, const void *seg_k, Geom g, Prm p,
+                                                    Workspace ws, int64_t *out_rho_t) {
+  const int b = blockIdx.y, i = blockIdx.x * kThreads + threadIdx.x;
+  const int m = ws.m[b];
+  if (blockIdx.x * kThreads >= m) return;
+  const bool act = i < m;
+  const int rs = ws.r_star[b / g.gs];
+  const int full = rs / kCkStride;
+  __shared__ float tk[kTile][D];
+  __shared__ float tn[kTile];
+  float kr[D];
+  float nr = 0.0f;
+  int64_t P = 0;
+  const size_t row = (size_t)b * g.Mcap + i;
+  if (act) {
+    load_row<D, DT>(kr, bank.k, row);
+    nr = bank.knorm[row];
+    for (int t = 0; t < full; ++t) P += ws.ck[row * ws.nck + t];
+  }
+  for (int j0 = full * kCkStride; j0 < rs; j0 += kTile) {
+    const int nc = min(kTile, rs - j0);
+    __syncthreads();
+    for (int t = threadIdx.x; t < kTile * D; t += kThreads) {
+      const int c = t / D, j = t % D;
+      float v = 0.0f;
+      if (c < nc) {
+        const int x = ws.order[(size_t)b * g.N + j0 + c];
+        v = load_elem<DT>(seg_k, ((size_t)b * g.N + x) * D + j);
+      }
+      tk[c][j] = v;
+    }
+    if (threadIdx.x < kTile) {
+      const int c = threadIdx.x;
+      tn[c] = c < nc ? ws.cnorm[(size_t)b * g.N + ws.order[(size_t)b * g.N + j0 + c]] : 0.0f;
+    }
+    __syncthreads();
+    if (act) {
+      for (int c = 0; c < nc; ++c) {
+        const float gd = dot_row<D>(kr, tk[c]);
+        const float d2 = (nr + tn[c]) - 2.0f * gd;
+        P += q23_round(pair_weight(d2, p.inv_sigma2, p.p), 8388608.0f);
+      }
+    }
+  }
+  if (!act) return;
+  const int64_t rt = bank.rho[row] + P;
+  ws.rho_t[row] = rt;
+  if (out_rho_t) out_rho_t[row] = rt;
+}
+
+// ---------------------------------------------------------------------------
+// k_select: one workgroup per bank.  Violators at r* are evicted; the fill
+// takes the non-violators with the largest rho~(r*), ties by provenance, then
+// slot (key (2^40-1-rho~, prov, slot) ascending, found by MSB radix select).
+// Then the commit plan: evicted list, admitted list, final slot of everything.
+// ---------------------------------------------------------------------------
+enum : unsigned char { ST_NONE = 0, ST_CAND = 1, ST_SEL = 2, ST_VIOL = 3 };
+
+__device__ __forceinline__ int sel_digit(const Workspace &ws, const dkv_bank &bank, size_t row, int slot,
+                                         int pass) {
+  if (pass < 5) {
+    const uint64_t w0 = kRhoMax - (uint64_t)ws.rho_t[row];
+    return (int)((w0 >> (8 * (4 - pass))) & 0xFF);
+  }
+  if (pass < 13) {
+    const uint64_t w1 = (uint64_t)bank.prov[row];
+    return (int)((w1 >> (8 * (12 - pass))) & 0xFF);
+  }
+  return (int)(((uint32_t)slot >> (8 * (14 - pass))) & 0xFF);
+}
+
+__global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspace ws,
+                                                 dkv_update_out out) {
+  const int b = blockIdx.x;
+  const int m = ws.m[b];
+  const int rs = ws.r_star[b / g.gs];
+  const int e = ws.e[b];
+  __shared__ unsigned char st[DKV_MAX_CAPACITY + 1];
+  __shared__ int hist[256];
+  __shared__ int tmp[16];
+  __shared__ int sh_bucket, sh_below, sh_cnt;
+  const size_t rb = (size_t)b * g.Mcap;
+
+  // violators and candidates for the fill
+  int nv_local = 0;
+  for (int i = threadIdx.x; i < m; i += kBig) {
+    const bool v = ws.first[rb + i] <= rs;
+    st[i] = v ? ST_VIOL : ST_CAND;
+    nv_local += v;
+  }
+  int nv;
+  (void)block_excl_scan(nv_local, &nv, tmp);
+  int need = e - nv;
+  if (need > 0) {
+    for (int pass = 0; pass < 15; ++pass) {
+      for (int t = threadIdx.x; t < 256; t += kBig) hist[t] = 0;
+      __syncthreads();
+      for (int i = threadIdx.x; i < m; i += kBig)
+        if (st[i] == ST_CAND) atomicAdd(&hist[sel_digit(ws, bank, rb + i, i, pass)], 1);
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        int cum = 0, d = 0;
+        while (d < 255 && cum + hist[d] < need) cum += hist[d++];
+        sh_bucket = d;
+        sh_below = cum;
+        sh_cnt = hist[d];
+      }
+      __syncthreads();
+      const int bk = sh_bucket, below = sh_below, cnt = sh_cnt;
+      const bool finish = (need - below) == cnt;
+      for (int i = threadIdx.x; i < m; i += kBig) {
+        if (st[i] != ST_CAND) continue;
+        const int dg = sel_digit(ws, bank, rb + i, i, pass);
+        if (dg < bk || (dg == bk && finish)) st[i] = ST_SEL;
+        else if (dg > bk) st[i] = ST_NONE;
+      }
+      need -= below;
+      __syncthreads();
+      if (finish) break;
+    }
+  }
+
+  // evicted list (ascending slots) and rank of each evicted slot
+  const int per = (m + kBig - 1) / kBig;
+  const int lo = min(m, (int)threadIdx.x * per), hi = min(m, lo + per);
+  int cnt_local = 0;
+  for (int i = lo; i < hi; ++i) cnt_local += (st[i] == ST_VIOL || st[i] == ST_SEL);
+  int n_ev;
+  int pos = block_excl_scan(cnt_local, &n_ev, tmp);
+  for (int i = lo; i < hi; ++i) {
+    if (st[i] == ST_VIOL || st[i] == ST_SEL) {
+      ws.ev_list[rb + pos] = i;
+      ws.dest[rb + i] = -1 - pos;  // provisional: encodes the evicted rank
+      ++pos;
+    } else {
+      ws.dest[rb + i] = i;
+    }
+  }
+  // admitted list: source indices x with rank(x) < r*, ascending
+  const int N = g.N;
+  const size_t nb = (size_t)b * N;
+  const int perN = (N + kBig - 1) / kBig;
+  const int loN = min(N, (int)threadIdx.x * perN), hiN = min(N, loN + perN);
+  int ca = 0;
+  for (int x = loN; x < hiN; ++x) ca += ws.rank[nb + x] < rs;
+  int n_adm;
+  int pa = block_excl_scan(ca, &n_adm, tmp);
+  __syncthreads();
+  const int m_new = m - n_ev + rs;
+  for (int x = loN; x < hiN; ++x) {
+    if (ws.rank[nb + x] < rs) {
+      ws.adm_list[nb + pa] = x;
+      ws.adm_dest[nb + pa] = pa < n_ev ? ws.ev_list[rb + pa] : m + (pa - n_ev);
+      ++pa;
+    }
+  }
+  __syncthreads();
+  if (n_ev > rs) {
+    // More evicted than admitted: close the holes below m_new with the
+    // occupants at or beyond m_new, both in ascending slot order.
+    // occupied(s) after placement: survivor, or an evicted slot filled by an
+    // admitted candidate (evicted rank < r*).
+    int mv_local = 0, lh_local = 0;
+    for (int i = lo; i < hi; ++i) {
+      const int dsl = ws.dest[rb + i];
+      const bool occ = dsl >= 0 || (-1 - dsl) < rs;
+      mv_local += occ && i >= m_new;
+      lh_local += !occ && i < m_new;
+    }
+    int n_mv, n_lh;
+    int pm = block_excl_scan(mv_local, &n_mv, tmp);
+    int ph = block_excl_scan(lh_local, &n_lh, tmp);
+    // hole list -> stash in sub[] (free until k_maint_gram) as slot numbers
+    for (int i = lo; i < hi; ++i) {
+      const int dsl = ws.dest[rb + i];
+      const bool occ = dsl >= 0 || (-1 - dsl) < rs;
+      if (!occ && i < m_new) ws.sub[rb + (ph++)] = i;
+    }
+    __syncthreads();
+    for (int i = lo; i < hi; ++i) {
+      const int dsl = ws.dest[rb + i];
+      const bool occ = dsl >= 0 || (-1 - dsl) < rs;
+      if (occ && i >= m_new) {
+        const int to = (int)ws.sub[rb + pm];
+        ++pm;
+        if (dsl >= 0) {
+          ws.dest[rb + i] = to;  // moving survivor
+        } else {
+          ws.adm_dest[nb + (-1 - dsl)] = to;  // admitted candidate placed in a high hole
+        }
+      }
+    }
+    __syncthreads();
+  }
+  // finalize dest: evicted -> -1; outputs
+  for (int i = lo; i < hi; ++i)
+    if (ws.dest[rb + i] < 0) ws.dest[rb + i] = -1;
+  if (out.evicted) {
+    for (int j = threadIdx.x; j < g.Mcap; j += kBig) out.evicted[rb + j] = j < n_ev ? ws.ev_list[rb + j] : -1;
+  }
+  if (out.admitted) {
+    for (int j = threadIdx.x; j < N; j += kBig) out.admitted[nb + j] = j < n_adm ? ws.adm_list[nb + j] : -1;
+  }
+  if (threadIdx.x == 0) {
+    ws.n_ev[b] = n_ev;
+    ws.m_new[b] = m_new;
+    bank.occupancy[b] = m_new;
+    if (out.n_evicted) out.n_evicted[b] = n_ev;
+    if (out.n_admitted) out.n_admitted[b] = rs;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_maint_gram: virtual rows [0, Mcap) = pre-update slots (survivors),
+// [Mcap, Mcap + N) = admitted list entries.  Sums of weights to the evicted
+// states (all rows) and to the admitted candidates (admitted rows only).
+// ---------------------------------------------------------------------------
+template <int D, int DT>
+__global__ __launch_bounds__(kThreads) void k_maint_gram(dkv_bank bank, const void *seg_k, Geom g,
+                                                         Prm p, Workspace ws) {
+  const int b = blockIdx.y, v = blockIdx.x * kThreads + threadIdx.x;
+  const int m = ws.m[b], n_ev = ws.n_ev[b];
+  const int rs = ws.r_star[b / g.gs];
+  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
+  bool surv = false, adm = false;
+  if (v < g.Mcap) surv = v < m && ws.dest[rb + v] >= 0;
+  else adm = (v - g.Mcap) < rs && (v - g.Mcap) < g.N;
+  const bool act = surv || adm;
+  if (!__syncthreads_or(act)) return;
+  const bool any_adm = __syncthreads_or(adm);
+  __shared__ float tk[kTile][D];
+  __shared__ float tn[kTile];
+  float kr[D];
+  float nr = 0.0f;
+  if (surv) {
+    load_row<D, DT>(kr, bank.k, rb + v);
+    nr = bank.knorm[rb + v];
+  } else if (adm) {
+    const int x = ws.adm_list[nb + (v - g.Mcap)];
+    load_row<D, DT>(kr, seg_k, nb + x);
+    nr = ws.cnorm[nb + x];
+  }
+  int64_t s_ev = 0, s_adm = 0;
+  for (int j0 = 0; j0 < n_ev; j0 += kTile) {
+    const int nc = min(kTile, n_ev - j0);
+    __syncthreads();
+    for (int t = threadIdx.x; t < kTile * D; t += kThreads) {
+      const int c = t / D, j = t % D;
+      tk[c][j] = c < nc ? load_elem<DT>(bank.k, (rb + ws.ev_list[rb + j0 + c]) * D + j) : 0.0f;
+    }
+    if (threadIdx.x < kTile) {
+      const int c = threadIdx.x;
+      tn[c] = c < nc ? bank.knorm[rb + ws.ev_list[rb + j0 + c]] : 0.0f;
+    }
+    __syncthreads();
+    if (act) {
+      for (int c = 0; c < nc; ++c) {
+        const float d2 = (nr + tn[c]) - 2.0f * dot_row<D>(kr, tk[c]);
+        s_ev += q23_round(pair_weight(d2, p.inv_sigma2, p.p), 8388608.0f);
+      }
+    }
+  }
+  if (any_adm) {
+    for (int j0 = 0; j0 < rs; j0 += kTile) {
+      const int nc = min(kTile, rs - j0);
+      __syncthreads();
+      for (int t = threadIdx.x; t < kTile * D; t += kThreads) {
+        const int c = t / D, j = t % D;
+        tk[c][j] = c < nc ? load_elem<DT>(seg_k, (nb + ws.adm_list[nb + j0 + c]) * D + j) : 0.0f;
+      }
+      if (threadIdx.x < kTile) {
+        const int c = threadIdx.x;
+        tn[c] = c < nc ? ws.cnorm[nb + ws.adm_list[nb + j0 + c]] : 0.0f;
+      }
+      __syncthreads();
+      if (adm) {
+        for (int c = 0; c < nc; ++c) {
+          const float d2 = (nr + tn[c]) - 2.0f * dot_row<D>(kr, tk[c]);
+          s_adm += q23_round(pair_weight(d2, p.inv_sigma2, p.p), 8388608.0f);
+        }
+      }
+    }
+  }
+  if (surv) ws.sub[rb + v] = s_ev;
+  if (adm) {
+    ws.sub_adm[nb + (v - g.Mcap)] = s_ev;
+    ws.mut_adm[nb + (v - g.Mcap)] = s_adm;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_commit: one wave per virtual row; new densities, baselines and placement.
+// ---------------------------------------------------------------------------
+template <int D, int DT>
+__global__ __launch_bounds__(kThreads) void k_commit(dkv_bank bank, dkv_segment seg, Geom g, Prm p,
+                                                     Workspace ws) {
+  using E = typename std::conditional<DT == DKV_BF16, uint16_t, float>::type;
+  const int b = blockIdx.y;
+  const int lane = threadIdx.x & 63;
+  const int v = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  const int m = ws.m[b];
+  const int rs = ws.r_star[b / g.gs];
+  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
+  E *K = static_cast<E *>(bank.k);
+  E *V = static_cast<E *>(bank.v);
+  const E *SK = static_cast<const E *>(seg.k);
+  const E *SV = static_cast<const E *>(seg.v);
+  if (v < g.Mcap) {
+    if (v >= m) return;
+    const int to = ws.dest[rb + v];
+    if (to < 0) return;
+    const int64_t rho = ws.rho_t[rb + v] - ws.sub[rb + v];
+    if (to != v) {
+      for (int j = lane; j < D; j += 64) {
+        K[(rb + to) * D + j] = K[(rb + v) * D + j];
+        V[(rb + to) * D + j] = V[(rb + v) * D + j];
+      }
+    }
+    if (lane == 0) {
+      bank.rho[rb + to] = rho;
+      if (to != v) {
+        bank.base[rb + to] = bank.base[rb + v];
+        bank.prov[rb + to] = bank.prov[rb + v];
+        bank.knorm[rb + to] = bank.knorm[rb + v];
+      }
+    }
+  } else {
+    const int k = v - g.Mcap;
+    if (k >= rs || k >= g.N) return;
+    const int x = ws.adm_list[nb + k];
+    const int to = ws.adm_dest[nb + k];
+    for (int j = lane; j < D; j += 64) {
+      K[(rb + to) * D + j] = SK[(nb + x) * D + j];
+      V[(rb + to) * D + j] = SV[(nb + x) * D + j];
+    }
+    if (lane == 0) {
+      const int64_t rho = ws.wcol[nb + x] - ws.sub_adm[nb + k] + ws.mut_adm[nb + k] - (int64_t)kQ23;
+      bank.rho[rb + to] = rho;
+      bank.base[rb + to] = rho > p.delta_q ? rho : p.delta_q;
+      bank.prov[rb + to] = ((int64_t)p.block_id << 32) | (int64_t)x;
+      bank.knorm[rb + to] = ws.cnorm[nb + x];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// k_bank_density: Phi over the bank of every live slot, from scratch (Eq. 3).
+// ---------------------------------------------------------------------------
+template <int D, int DT>
+__global__ __launch_bounds__(kThreads) void k_bank_density(dkv_bank bank, Geom g, Prm p, Workspace ws,
+                                                           int64_t *out) {
+  const int b = blockIdx.y, i = blockIdx.x * kThreads + threadIdx.x;
+  const int m = ws.m[b];
+  if (blockIdx.x * kThreads >= m) return;
+  const bool act = i < m;
+  const size_t rb = (size_t)b * g.Mcap;
+  __shared__ float tk[kTile][D];
+  __shared__ float tn[kTile];
+  float kr[D];
+  float nr = 0.0f;
+  if (act) {
+    load_row<D, DT>(kr, bank.k, rb + i);
+    nr = bank.knorm[rb + i];
+  }
+  int64_t s = 0;
+  for (int j0 = 0; j0 < m; j0 += kTile) {
+    const int nc = min(kTile, m - j0);
+    __syncthreads();
+    for (int t = threadIdx.x; t < kTile * D; t += kThreads) {
+      const int c = t / D, j = t % D;
+      tk[c][j] = c < nc ? load_elem<DT>(bank.k, (rb + j0 + c) * D + j) : 0.0f;
+    }
+    if (threadIdx.x < kTile) tn[threadIdx.x] = threadIdx.x < nc ? bank.knorm[rb + j0 + threadIdx.x] : 0.0f;
+    __syncthreads();
+    if (act) {
+      for (int c = 0; c < nc; ++c) {
+        if (j0 + c == i) continue;  // j != i by index
+        const float d2 = (nr + tn[c]) - 2.0f * dot_row<D>(kr, tk[c]);
+        s += q23_round(pair_weight(d2, p.inv_sigma2, p.p), 8388608.0f);
+      }
+    }
+  }
+  if (act) out[rb + i] = s;
+}
+
+__global__ void k_pair_weight(const float *d2, int64_t n, Prm p, int32_t *w) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) w[i] = (int32_t)q23_round(pair_weight(d2[i], p.inv_sigma2, p.p), 8388608.0f);
+}
+
+inline dim3 grid2(int n, int per, int B) { return dim3((unsigned)((n + per - 1) / per), (unsigned)B); }
+
+template <int D, int DT>
+hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                       const dkv_update_out *outp, const Workspace &ws, hipStream_t s) {
+  dkv_update_out out = outp ? *outp : dkv_update_out{};
+  k_prep<<<g.B, kThreads, 0, s>>>(bank, g, ws);
+  if (g.N > 0) {
+    k_cand_norms<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(seg.k, g, ws);
+    k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.score_q, nullptr);
+    k_sort<<<g.B, kBig, 0, s>>>(g, ws, out.order);
+    k_cross_gram<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.first_cross);
+  } else {
+    // no candidates: no prefix to test; first crossing is 0 for violators only
+    k_cross_gram<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.first_cross);
+  }
+  k_feasible<<<g.G, kBig, 0, s>>>(g, ws, out.r_star);
+  k_fixup<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.rho_tilde);
+  k_select<<<g.B, kBig, 0, s>>>(bank, g, ws, out);
+  k_maint_gram<D, DT><<<grid2(g.Mcap + g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws);
+  k_commit<D, DT><<<grid2(g.Mcap + g.N, kThreads / 64, g.B), kThreads, 0, s>>>(bank, seg, g, p, ws);
+  return hipGetLastError();
+}
+
+template <int D, int DT>
+hipError_t score_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                      int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws,
+                      hipStream_t s) {
+  k_prep<<<g.B, kThreads, 0, s>>>(bank, g, ws);
+  if (g.N > 0 && (score_q || score_f)) {
+    Workspace w2 = ws;
+    w2.acol = nullptr;  // scoring only: no sort keys needed
+    k_cand_norms<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(seg.k, g, ws);
+    k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, w2, score_q, score_f);
+  }
+  if (density)
+    k_bank_density<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, g, p, ws, density);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_update(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                         const dkv_update_out *out, const Workspace &ws, hipStream_t s) {
+  if (g.d == 128 && g.dtype == DKV_BF16) return update_impl<128, DKV_BF16>(bank, seg, g, p, out, ws, s);
+  if (g.d == 128 && g.dtype == DKV_F32) return update_impl<128, DKV_F32>(bank, seg, g, p, out, ws, s);
+  if (g.d == 64 && g.dtype == DKV_BF16) return update_impl<64, DKV_BF16>(bank, seg, g, p, out, ws, s);
+  return update_impl<64, DKV_F32>(bank, seg, g, p, out, ws, s);
+}
+
+hipError_t launch_score(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                        int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws,
+                        hipStream_t s) {
+  if (g.d == 128 && g.dtype == DKV_BF16) return score_impl<128, DKV_BF16>(bank, seg, g, p, score_q, score_f, density, ws, s);
+  if (g.d == 128 && g.dtype == DKV_F32) return score_impl<128, DKV_F32>(bank, seg, g, p, score_q, score_f, density, ws, s);
+  if (g.d == 64 && g.dtype == DKV_BF16) return score_impl<64, DKV_BF16>(bank, seg, g, p, score_q, score_f, density, ws, s);
+  return score_impl<64, DKV_F32>(bank, seg, g, p, score_q, score_f, density, ws, s);
+}
+
+hipError_t launch_pair_weight(const float *d2, int64_t n, const Prm &p, int32_t *w, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = (n + 255) / 256;
+  k_pair_weight<<<(unsigned)blocks, 256, 0, s>>>(d2, n, p, w);
+  return hipGetLastError();
+}
+
+}  // namespace dkv

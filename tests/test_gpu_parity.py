@@ -1,0 +1,302 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.  Needs an MI355X.
+
+Discrete results (candidate order, first crossings, r*, eviction sets, the
+committed bank layout, densities, baselines, K/V bytes) must be bit-identical;
+attention must be within the row-normalised max error 2e-2 (bf16) / 1e-5 (fp32).
+"""
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+from oracle import Q23, BankState, attention, candidate_scores, density_from_scratch, weight_q23  # noqa: E402
+from paper_2608_27922_amd import api, synth  # noqa: E402
+from gpu_util import (assert_bank_equal, assert_trace_equal, attention_error, dev, host, mirror,  # noqa: E402
+                      oracle_params, oracle_step)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    api.lib()
+
+
+def _log(msg):
+    print(msg, flush=True)
+
+
+# ----------------------------------------------------------------------------- per-pair contract
+
+@pytest.mark.parametrize("s,p", [(6, 2), (5, 2), (6, 1), (6, 4), (4, 2), (8, 2), (0, 1)])
+def test_pair_weight_exhaustive(s, p):
+    """Every squared distance the key grid can produce (d2 * 2^12 in [0, 8258048])."""
+    _log(f"pair weight sweep s={s} p={p}")
+    n = np.arange(0, 8_258_049, dtype=np.float64)
+    d2 = n / 4096.0
+    ref = weight_q23(d2, oracle_params(api.Params(sigma2_log2=s, p=p)))
+    got = api.pair_weight_q23(torch.from_numpy(d2.astype(np.float32)).cuda(), api.Params(sigma2_log2=s, p=p))
+    got = got.cpu().numpy().astype(np.int64)
+    bad = np.nonzero(got != ref)[0]
+    assert bad.size == 0, f"{bad.size} mismatches, first d2*4096={n[bad[:5]]} got {got[bad[:5]]} ref {ref[bad[:5]]}"
+
+
+# ----------------------------------------------------------------------------- rollouts
+
+def _run_rollout(cfg, blocks, prm, budgets=None, dup_every=0, trace=True, init_full=False, check_every=1):
+    """Rollout over one layer of `cfg`: GPU update + oracle update per block, compared."""
+    B, gs, d, dt = cfg.heads, cfg.group_size, cfg.d, cfg.dtype
+    if budgets is None:
+        budgets = np.full(B, cfg.budget, np.int32)
+    Mcap = int(max(budgets))
+    bank = api.Bank(B, Mcap, d, dtype=torch.bfloat16 if dt == "bf16" else torch.float32, group_size=gs,
+                    budget=torch.from_numpy(np.asarray(budgets, np.int32)))
+    obanks = [BankState.empty(int(budgets[b]), d) for b in range(B)]
+    op = oracle_params(prm)
+    streams = [synth.HeadStream(cfg, 0, h) for h in range(B)]
+    for t in range(blocks):
+        n = Mcap if (init_full and t == 0) else cfg.n_cand
+        K = np.stack([s.keys(t, n) for s in streams])
+        V = np.stack([s.values(t, n) for s in streams])
+        if dup_every and t > 0 and t % dup_every == 0:
+            for h in range(B):
+                if obanks[h].m:
+                    K[h] = streams[h].near_duplicates(K[h], obanks[h].K.astype(np.float32), t)
+        out = api.UpdateOut(bank, n, trace=trace)
+        api.update_bank(bank, dev(K, dt), dev(V, dt), t, prm, out=out)
+        torch.cuda.synchronize()
+        new, recs = oracle_step(obanks, K, V, t, op, gs)
+        if t % check_every == 0 or t == blocks - 1:
+            if trace:
+                assert_trace_equal(out, recs, gs, obanks, n, ctx=f"block {t}")
+            for b in range(B):
+                assert_bank_equal(bank, b, new[b], ctx=f"block {t}")
+        obanks = new
+    return bank, obanks
+
+
+SMALL = dict(key=77, name="small", layers=1, n_query=40, n_window=24, clusters=6, blocks=6, sigma2_log2=4,
+             drift=0.05)
+
+
+@pytest.mark.parametrize("dt,d", [("bf16", 128), ("f32", 64), ("bf16", 64), ("f32", 128)])
+def test_rollout_small_shared_prefix(dt, d):
+    """6 banks in 2 groups of 3, budget 300 (ragged tiles), 200 candidates per block,
+    near-duplicate blocks to force mandatory evictions."""
+    _log(f"rollout small dt={dt} d={d}")
+    cfg = synth.Config(heads=6, d=d, dtype=dt, n_cand=200, budget=300, group_size=3, **SMALL)
+    _run_rollout(cfg, 6, api.Params(sigma2_log2=4 if d == 64 else 5), dup_every=2)
+
+
+def test_rollout_checkpoint_tiles():
+    """N = 700 > 256 candidates: prefix checkpoints plus a partial tile at r*."""
+    _log("rollout checkpoint tiles")
+    cfg = synth.Config(heads=4, d=128, dtype="bf16", n_cand=700, budget=1000, group_size=2, **SMALL)
+    _run_rollout(cfg, 4, api.Params(sigma2_log2=5), dup_every=2)
+
+
+def test_rollout_ragged_budgets_independent_heads():
+    """group_size = 1 with per-head budgets (the independent per-head variant)."""
+    _log("rollout ragged budgets")
+    cfg = synth.Config(heads=5, d=128, dtype="bf16", n_cand=150, budget=400, group_size=1, **SMALL)
+    _run_rollout(cfg, 6, api.Params(sigma2_log2=5), budgets=np.array([120, 400, 260, 150, 333], np.int32),
+                 dup_every=2)
+
+
+def test_rollout_group_ragged_budgets():
+    """Shared prefix over a group whose budgets differ: r <= min budget, e_r per head."""
+    _log("rollout group ragged budgets")
+    cfg = synth.Config(heads=4, d=64, dtype="f32", n_cand=90, budget=200, group_size=4, **SMALL)
+    _run_rollout(cfg, 5, api.Params(sigma2_log2=4), budgets=np.array([200, 130, 170, 90], np.int32),
+                 dup_every=2)
+
+
+@pytest.mark.parametrize("tau,p,s", [((3, 1), 2, 5), ((3, 0), 1, 6), ((2, 0), 4, 6)])
+def test_rollout_parameter_sweep(tau, p, s):
+    """tau in {1.5, 3}, p in {1, 4}, sigma^2 in {32, 64} (the paper's sweeps)."""
+    _log(f"rollout params tau={tau} p={p} s={s}")
+    cfg = synth.Config(heads=3, d=128, dtype="bf16", n_cand=120, budget=250, group_size=3, **SMALL)
+    _run_rollout(cfg, 5, api.Params(sigma2_log2=s, p=p, tau_num=tau[0], tau_log2_den=tau[1]), dup_every=2)
+
+
+def test_empty_bank_more_candidates_than_budget():
+    """Alg. 1 first branch: first min(N, M) source-ordered candidates, N > M."""
+    _log("empty bank N > M")
+    cfg = synth.Config(heads=2, d=128, dtype="bf16", n_cand=300, budget=170, group_size=2, **SMALL)
+    _run_rollout(cfg, 1, api.Params(sigma2_log2=5))
+
+
+def test_zero_candidates_and_determinism():
+    """N = 0 leaves a valid bank unchanged; the same update twice gives identical bits."""
+    _log("zero candidates + determinism")
+    cfg = synth.Config(heads=3, d=128, dtype="bf16", n_cand=100, budget=150, group_size=3, **SMALL)
+    bank, obanks = _run_rollout(cfg, 3, api.Params(sigma2_log2=5), dup_every=2)
+    before = bank.state_dict()
+    api.update_bank(bank, None, None, 9, api.Params(sigma2_log2=5))
+    torch.cuda.synchronize()
+    for n, t in bank.state_dict().items():
+        assert torch.equal(t, before[n]), n
+    # determinism: replay one update from a checkpoint twice
+    s = synth.HeadStream(cfg, 0, 0)
+    K = np.stack([synth.HeadStream(cfg, 0, h).keys(11, 100) for h in range(3)])
+    V = np.stack([synth.HeadStream(cfg, 0, h).values(11, 100) for h in range(3)])
+    results = []
+    for _ in range(2):
+        bank.load_state_dict(before)
+        api.update_bank(bank, dev(K, "bf16"), dev(V, "bf16"), 11, api.Params(sigma2_log2=5))
+        torch.cuda.synchronize()
+        results.append(bank.state_dict())
+    for n in results[0]:
+        assert torch.equal(results[0][n], results[1][n]), n
+    del s
+
+
+def test_all_duplicate_candidates():
+    """Every candidate is an exact copy of one bank key: weights of exactly 1 everywhere."""
+    _log("all-duplicate candidates")
+    prm = api.Params(sigma2_log2=5)
+    B, d, M, N = 2, 128, 64, 40
+    rng = np.random.default_rng(4)
+    bank = api.Bank(B, M, d, dtype=torch.bfloat16, group_size=2)
+    K0 = synth.random_grid_keys(rng, (B, M, d))
+    V0 = synth.to_storage(rng.standard_normal((B, M, d)), "bf16")
+    api.update_bank(bank, dev(K0, "bf16"), dev(V0, "bf16"), 0, prm)
+    obanks, _ = oracle_step([BankState.empty(M, d) for _ in range(B)], K0, V0, 0, oracle_params(prm), 2)
+    K1 = np.repeat(K0[:, 3:4], N, axis=1)
+    V1 = synth.to_storage(rng.standard_normal((B, N, d)), "bf16")
+    out = api.UpdateOut(bank, N, trace=True)
+    api.update_bank(bank, dev(K1, "bf16"), dev(V1, "bf16"), 1, prm, out=out)
+    torch.cuda.synchronize()
+    new, recs = oracle_step(obanks, K1, V1, 1, oracle_params(prm), 2)
+    assert_trace_equal(out, recs, 2, obanks, N)
+    for b in range(B):
+        assert_bank_equal(bank, b, new[b])
+
+
+def test_corrupted_bank_is_compacted():
+    """Outside the paper's precondition (states already violating): r* = 0, violators
+    are evicted and the survivors beyond the new occupancy close the holes."""
+    _log("corrupted bank")
+    prm = api.Params(sigma2_log2=5)
+    B, d, M = 2, 64, 100
+    rng = np.random.default_rng(8)
+    bank = api.Bank(B, M, d, dtype=torch.float32, group_size=1)
+    K0 = synth.random_grid_keys(rng, (B, 60, d))
+    V0 = synth.to_storage(rng.standard_normal((B, 60, d)), "f32")
+    api.update_bank(bank, dev(K0, "f32"), dev(V0, "f32"), 0, prm)
+    torch.cuda.synchronize()
+    for b in range(B):
+        for s in (2, 7, 30):
+            bank.base[b, s] = bank.rho[b, s] // 4
+    obanks = [mirror(bank, b) for b in range(B)]
+    K1 = synth.random_grid_keys(rng, (B, 10, d))
+    V1 = synth.to_storage(rng.standard_normal((B, 10, d)), "f32")
+    out = api.UpdateOut(bank, 10, trace=True)
+    api.update_bank(bank, dev(K1, "f32"), dev(V1, "f32"), 1, prm, out=out)
+    torch.cuda.synchronize()
+    new, recs = oracle_step(obanks, K1, V1, 1, oracle_params(prm), 1)
+    assert all(r.r_star == 0 for r in recs)
+    assert_trace_equal(out, recs, 1, obanks, 10)
+    for b in range(B):
+        assert_bank_equal(bank, b, new[b])
+
+
+# ----------------------------------------------------------------------------- score entry point
+
+def test_score_and_bank_density():
+    _log("score + density")
+    prm = api.Params(sigma2_log2=5)
+    cfg = synth.Config(heads=3, d=128, dtype="bf16", n_cand=130, budget=260, group_size=3, **SMALL)
+    bank, obanks = _run_rollout(cfg, 3, prm, trace=False)
+    K = np.stack([synth.HeadStream(cfg, 0, h).keys(9, 130) for h in range(3)])
+    V = np.stack([synth.HeadStream(cfg, 0, h).values(9, 130) for h in range(3)])
+    sq, sf, dens = api.score(bank, dev(K, "bf16"), dev(V, "bf16"), prm, want_density=True)
+    torch.cuda.synchronize()
+    op = oracle_params(prm)
+    for b in range(3):
+        S, E, s_real = candidate_scores(obanks[b].K, obanks[b].base, K[b].astype(np.float64), op)
+        assert np.array_equal(sq[b].cpu().numpy(), S)
+        assert np.allclose(sf[b].cpu().numpy(), s_real, rtol=1e-6, atol=0)
+        m = obanks[b].m
+        assert np.array_equal(dens[b, :m].cpu().numpy(), density_from_scratch(obanks[b].K, op))
+        assert np.array_equal(dens[b, :m].cpu().numpy(), obanks[b].rho)
+
+
+# ----------------------------------------------------------------------------- configs 1 and 2
+
+def _starts_full_case(key):
+    cfg = synth.CONFIGS[key]
+    prm = api.Params(sigma2_log2=cfg.sigma2_log2)
+    case = synth.single_update_case(cfg)
+    return cfg, prm, case
+
+
+@pytest.mark.parametrize("key", [1, 2])
+def test_config_update_and_attention(key):
+    """Config 1 (tiny, fp32) and config 2 (one layer x 12 heads, d 128, bf16, N = M = 4680,
+    30% near-duplicates): bank built by the empty-bank rule, one update, then attention."""
+    _log(f"config {key}")
+    cfg, prm, case = _starts_full_case(key)
+    B, gs, d, dt, M, N = cfg.heads, cfg.group_size, cfg.d, cfg.dtype, cfg.budget, cfg.n_cand
+    op = oracle_params(prm)
+    bank = api.Bank(B, M, d, dtype=torch.bfloat16 if dt == "bf16" else torch.float32, group_size=gs)
+    ob = [BankState.empty(M, d) for _ in range(B)]
+    for blk, (Kn, Vn) in enumerate([("init_K", "init_V"), ("seg_K", "seg_V")]):
+        K, V = case[Kn], case[Vn]
+        out = api.UpdateOut(bank, K.shape[1], trace=True)
+        api.update_bank(bank, dev(K, dt), dev(V, dt), blk, prm, out=out)
+        torch.cuda.synchronize()
+        _log(f"  block {blk}: GPU done, running oracle")
+        new, recs = oracle_step(ob, K, V, blk, op, gs)
+        assert_trace_equal(out, recs, gs, ob, K.shape[1], ctx=f"config {key} block {blk}")
+        for b in range(B):
+            assert_bank_equal(bank, b, new[b], ctx=f"config {key} block {blk}")
+        ob = new
+        _log(f"  block {blk}: r* = {recs[0].r_star}, evicted {[int(x) for x in out.n_evicted.cpu()][:4]}")
+    q, wk, wv = case["q"], case["win_K"], case["win_V"]
+    o = api.bank_attention(bank, dev(q, dt), dev(wk, dt), dev(wv, dt))
+    torch.cuda.synchronize()
+    got = host(o)
+    tol = 2e-2 if dt == "bf16" else 1e-5
+    worst = 0.0
+    for b in range(B):
+        ref = attention(q[b], ob[b].K, ob[b].V, wk[b], wv[b], 1.0 / np.sqrt(d))
+        worst = max(worst, attention_error(got[b], ref))
+    _log(f"  attention max row-normalised error {worst:.3e} (tol {tol})")
+    assert worst <= tol
+
+
+# ----------------------------------------------------------------------------- attention edge cases
+
+@pytest.mark.parametrize("dt,d", [("bf16", 128), ("f32", 64), ("bf16", 64), ("f32", 128)])
+def test_attention_edge_cases(dt, d):
+    _log(f"attention edges {dt} {d}")
+    rng = np.random.default_rng(21)
+    B, M = 4, 300
+    tdt = torch.bfloat16 if dt == "bf16" else torch.float32
+    bank = api.Bank(B, M, d, dtype=tdt, group_size=1, budget=torch.tensor([300, 0, 77, 5], dtype=torch.int32))
+    occ = [300, 0, 77, 5]
+    Kb = synth.to_storage(rng.standard_normal((B, M, d)), dt)
+    Vb = synth.to_storage(rng.standard_normal((B, M, d)), dt)
+    bank.k.copy_(dev(Kb, dt))
+    bank.v.copy_(dev(Vb, dt))
+    bank.occupancy.copy_(torch.tensor(occ, dtype=torch.int32))
+    tol = 2e-2 if dt == "bf16" else 1e-5
+    for nq, nw in [(97, 33), (1, 0), (130, 1), (64, 200)]:
+        q = synth.to_storage(rng.standard_normal((B, nq, d)), dt)
+        wk = synth.to_storage(rng.standard_normal((B, nw, d)), dt)
+        wv = synth.to_storage(rng.standard_normal((B, nw, d)), dt)
+        o = api.bank_attention(bank, dev(q, dt), dev(wk, dt) if nw else None, dev(wv, dt) if nw else None)
+        torch.cuda.synchronize()
+        got = host(o)
+        for b in range(B):
+            m = occ[b]
+            if m + nw == 0:
+                assert np.all(got[b] == 0)
+                continue
+            ref = attention(q[b], Kb[b, :m], Vb[b, :m], wk[b], wv[b], 1.0 / np.sqrt(d))
+            err = attention_error(got[b], ref)
+            assert err <= tol, (nq, nw, b, err)
