@@ -1,0 +1,156 @@
+#!/usr/bin/env python3
+"""Benchmark of the DensityKV hot path on one MI355X.
+
+A step is one pass of the whole hot path over one block: the density-guided
+update of every (layer, head) bank from the block's candidates, then the
+attention of the next block's queries over the retained bank plus the local
+window.  Workload (default): one layer x 12 heads, d = 128, bf16, per-head
+budget 4,680, banks start full (built by the empty-bank rule), one incoming
+segment of 4,680 candidates with 30% near-duplicates, 4,680 queries over
+bank + a 4,680-token window.  Every step restores the pre-update bank with a
+device-to-device copy (inside the timed region) so that all steps do the same
+work.
+
+Prints one JSON line.  value = candidate tokens per second per layer-head for
+the whole step (update + attention); the update-only rate and the attention
+TFLOP/s are reported beside it, with the roofline of the dominant kernel and
+the CPU oracle timed on a bounded sample.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2, help="workload: 1 (tiny) or 2 (one layer, 12 heads)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-heads", type=int, default=1, help="heads in the oracle sample")
+    return ap.parse_args()
+
+
+def cpu_baseline(case, cfg, n_heads):
+    """The oracle, as it stands, on a bounded sample: one update + one attention for
+    `n_heads` heads treated as one group (rank 0 only)."""
+    from oracle import BankState, Params, attention, update_layer
+    prm = Params(sigma2_log2=cfg.sigma2_log2)
+    hs = range(n_heads)
+    banks = [BankState.empty(cfg.budget, cfg.d) for _ in hs]
+    banks, _ = update_layer(banks, [case["init_K"][h].astype(np.float64) for h in hs],
+                            [case["init_V"][h] for h in hs], 0, prm)
+    t0 = time.perf_counter()
+    banks, _ = update_layer(banks, [case["seg_K"][h].astype(np.float64) for h in hs],
+                            [case["seg_V"][h] for h in hs], 1, prm)
+    t1 = time.perf_counter()
+    for h in hs:
+        attention(case["q"][h], banks[h].K, banks[h].V, case["win_K"][h], case["win_V"][h], 1.0 / np.sqrt(cfg.d))
+    t2 = time.perf_counter()
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    step_s = (t2 - t0) / n_heads  # per layer-head
+    return {"value": cfg.n_cand / step_s, "unit": "tokens/s per layer-head", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{n_heads} head(s) of the same workload: one update (N={cfg.n_cand} into a full bank of "
+                      f"{cfg.budget}) + one attention ({cfg.n_query} queries over bank + {cfg.n_window} window), "
+                      f"update {t1 - t0:.2f} s, attention {t2 - t1:.2f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                                   "(banks shard by layer without communication; see the design notes)"}))
+        sys.exit(2)
+    import torch
+    from paper_2608_27922_amd import api, synth
+
+    cfg = synth.CONFIGS[args.config]
+    if not cfg.starts_full:
+        raise SystemExit("bench workload must be a single-update configuration (1 or 2)")
+    torch.cuda.set_device(0)
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    case = synth.single_update_case(cfg)
+    to = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dt).cuda().contiguous()
+    prm = api.Params(sigma2_log2=cfg.sigma2_log2)
+    B, N, d = cfg.heads, cfg.n_cand, cfg.d
+    bank = api.Bank(B, cfg.budget, d, dtype=dt, group_size=cfg.group_size)
+    init_k, init_v = to(case["init_K"]), to(case["init_V"])
+    seg_k, seg_v = to(case["seg_K"]), to(case["seg_V"])
+    q, wk, wv = to(case["q"]), to(case["win_K"]), to(case["win_V"])
+    ws = api.alloc_workspace(bank, max(N, cfg.budget))
+    api.update_bank(bank, init_k, init_v, 0, prm, workspace=ws)   # starts full (empty-bank rule)
+    torch.cuda.synchronize()
+    snap = bank.state_dict()
+    out = torch.empty_like(q)
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        bank.load_state_dict(snap)
+        if ev is not None:
+            ev[0].record(stream)
+        api.update_bank(bank, seg_k, seg_v, 1, prm, workspace=ws)
+        if ev is not None:
+            ev[1].record(stream)
+        api.bank_attention(bank, q, wk, wv, out=out)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for k in range(args.steps):
+        step(evs[k])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_step = total_ms / args.steps
+    upd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    att_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    m_after = bank.occupancy.cpu().numpy()
+    att_flops = float(sum(4.0 * cfg.n_query * (int(m) + cfg.n_window) * d for m in m_after))
+    att_tflops = att_flops / (att_ms * 1e-3) / 1e12
+    value = N / (ms_step * 1e-3)   # every bank processes N candidates per step, concurrently
+
+    result = {
+        "metric": "bank-update tokens/s per layer-head + bank-attention TFLOP/s (roofline %)",
+        "value": round(value, 1),
+        "unit": "tokens/s per layer-head",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": f"config {cfg.key} ({cfg.name}): {cfg.layers} layer x {cfg.heads} heads, d={d}, "
+                               f"{cfg.dtype}, budget {cfg.budget} (starts full), segment {N} (30% near-duplicates), "
+                               f"{cfg.n_query} queries over bank + {cfg.n_window}-token window",
+                   "banks": B, "group_size": cfg.group_size, "candidates": N, "budget": cfg.budget,
+                   "queries": cfg.n_query, "window": cfg.n_window, "head_dim": d},
+        "update_ms": round(upd_ms, 4),
+        "update_tokens_per_s_per_layer_head": round(N / (upd_ms * 1e-3), 1),
+        "attention_ms": round(att_ms, 4),
+        "attention_tflops": round(att_tflops, 2),
+        "roofline": {"bound": "mfma", "kernel": "bank attention", "achieved": round(att_tflops, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(case, cfg, args.cpu_heads)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
