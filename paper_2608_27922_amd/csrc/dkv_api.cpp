@@ -41,6 +41,7 @@ size_t workspace_layout(int B, int G, int Mcap, int N, Workspace *ws, char *base
   w.rho_t = (int64_t *)take(Bz * Mz * 8);
   w.dest = (int32_t *)take(Bz * Mz * 4);
   w.ev_list = (int32_t *)take(Bz * Mz * 4);
+  w.surv_list = (int32_t *)take(Bz * Mz * 4);
   w.adm_list = (int32_t *)take(Bz * Nz * 4);
   w.adm_dest = (int32_t *)take(Bz * Nz * 4);
   w.sub = (int64_t *)take(Bz * Mz * 8);

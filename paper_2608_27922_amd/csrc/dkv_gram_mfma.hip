@@ -1,0 +1,615 @@
+// Key-key Gram stages of the DensityKV update on bf16 MFMA (gfx950).
+//
+// Every Gram stage evaluates Soft-Riesz weights w(k_i, k_j) (Eq. 2) for a set
+// of "row" items against a stream of "column" items and reduces them per row:
+//
+//   k_score_mfma   rows = candidates, columns = all bank states:
+//                  S_x = sum_i RNE(w_ix bs_i), Wcol_x = sum_i W_ix  (Eq. 6)
+//   k_cross_mfma   rows = bank states, columns = candidates in score order:
+//                  running prefix P_i(r) and the first r with a violation
+//                  (Eqs. 8-9), prefix checkpoints every 256 candidates
+//   k_rowsum_mfma  plain row sums for the r* fix-up, the exact maintenance
+//                  (Supp. C) and the from-scratch bank density (Eq. 3)
+//
+// Layout: a workgroup of 4 waves owns 128 row items; wave w owns 32 of them,
+// held for the whole kernel as the B operand of v_mfma_f32_32x32x16_bf16
+// (lane l <-> row item l % 32).  Column items stream through LDS in tiles of 32
+// (double-buffered, padded rows) and form the A operand, so each lane ends up
+// with 16 weights of its own row item and reduces them in registers.
+//
+// Exactness: with keys on the 1/64 grid every partial sum of the contraction
+// is an exact multiple of 2^-18 below 2^24 units, so the MFMA result
+//   u = (|k_i|^2 + |k_j|^2 - 2 <k_i, k_j>) / sigma^2
+// is exact.  The norms enter through one extra K step (each norm / sigma^2 is
+// split exactly into three bf16 pieces) and the row keys are pre-scaled by
+// -2 / sigma^2 (exact in bf16).  The epilogue is the binary32 contract:
+// t = 1 + u, t^p, correctly rounded reciprocal (rcp + one FMA correction, exact
+// for every significand), RNE(w * 2^23) via one FMA, integer sums.
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+#include "dkv_internal.hpp"
+
+namespace dkv {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 4;
+constexpr int kRowsPerWG = 32 * kWaves;
+constexpr int kCT = 32;  // column items per tile
+
+template <int D>
+struct TileCfg {
+  static constexpr int kSteps = D / 16;     // K steps over the key
+  static constexpr int kStride = D + 24;    // bf16 per LDS row: key, 16 aug, 8 pad (odd multiple of 16 B)
+  static constexpr int kChunks = D / 8;     // 16-byte chunks per key
+};
+
+__device__ __forceinline__ uint16_t bf16_rne_bits(float f) { return f32_to_bf16_bits(f); }
+
+// Exact split of x (at most 24 significant bits) into three bf16 values.
+__device__ __forceinline__ void split3(float x, uint16_t &h, uint16_t &m, uint16_t &l) {
+  h = bf16_rne_bits(x);
+  float r = x - bf16_bits_to_f32(h);
+  m = bf16_rne_bits(r);
+  float r2 = r - bf16_bits_to_f32(m);
+  l = bf16_rne_bits(r2);
+}
+
+constexpr uint16_t kOne = 0x3F80;  // bf16 1.0
+
+template <int P>
+__device__ __forceinline__ uint32_t weight_raw(float u, float scale) {
+  // raw bits of fma(w, scale, 2^23): kMagic + RNE(w * scale)
+  const float t = 1.0f + u;
+  float tp = t;
+  if constexpr (P >= 2) tp = t * t;
+  if constexpr (P == 4) tp = tp * tp;
+  const float y = __builtin_amdgcn_rcpf(tp);
+  const float e = __builtin_fmaf(-tp, y, 1.0f);
+  const float w = __builtin_fmaf(e, y, y);
+  return __float_as_uint(__builtin_fmaf(w, scale, 8388608.0f));
+}
+
+// Row fragment: B operand of every K step for this lane's row item.
+template <int D>
+struct RowFrag {
+  bf16x8 b[TileCfg<D>::kSteps + 1];
+};
+
+// Load the B operand for row item (lane % 32): keys scaled by -2/sigma^2, then
+// the aug step [1, 1, 1, n_hi, n_mid, n_lo, 0, 0] (half 0) / zeros (half 1).
+template <int D>
+__device__ __forceinline__ void load_row_frag(RowFrag<D> &rf, const uint16_t *key, float norm, bool valid,
+                                              float neg2_inv_s2, float inv_s2) {
+  const int h = (threadIdx.x & 63) >> 5;
+#pragma unroll
+  for (int kk = 0; kk < TileCfg<D>::kSteps; ++kk) {
+    u32x4 raw = {0, 0, 0, 0};
+    if (valid) raw = *reinterpret_cast<const u32x4 *>(key + 16 * kk + 8 * h);
+    u32x4 sc;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float lo = bf16_bits_to_f32((uint16_t)(raw[q] & 0xFFFF)) * neg2_inv_s2;
+      const float hi = bf16_bits_to_f32((uint16_t)(raw[q] >> 16)) * neg2_inv_s2;
+      sc[q] = (uint32_t)bf16_rne_bits(lo) | ((uint32_t)bf16_rne_bits(hi) << 16);
+    }
+    rf.b[kk] = __builtin_bit_cast(bf16x8, sc);
+  }
+  u32x4 aug = {0, 0, 0, 0};
+  if (valid && h == 0) {
+    uint16_t nh, nm, nl;
+    split3(norm * inv_s2, nh, nm, nl);
+    aug[0] = (uint32_t)kOne | ((uint32_t)kOne << 16);
+    aug[1] = (uint32_t)kOne | ((uint32_t)nh << 16);
+    aug[2] = (uint32_t)nm | ((uint32_t)nl << 16);
+    aug[3] = 0;
+  }
+  rf.b[TileCfg<D>::kSteps] = __builtin_bit_cast(bf16x8, aug);
+}
+
+// Column tile staging: each of the 256 threads moves 16-byte chunks of the
+// tile's keys; 32 threads write the aug columns.
+template <int D>
+struct ColStage {
+  u32x4 chunk[(kCT * TileCfg<D>::kChunks) / (64 * kWaves)];
+  u32x4 aug0;
+};
+
+// item_row(i) returns the element offset of column item i's key, or -1.
+template <int D, class RowOf, class NormOf>
+__device__ __forceinline__ void stage_load(ColStage<D> &st, const uint16_t *base, int j0, int ncols,
+                                           RowOf row_of, NormOf norm_of, float inv_s2) {
+  constexpr int kPer = (kCT * TileCfg<D>::kChunks) / (64 * kWaves);
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const int c = threadIdx.x + q * 64 * kWaves;
+    const int item = c / TileCfg<D>::kChunks, ch = c % TileCfg<D>::kChunks;
+    u32x4 v = {0, 0, 0, 0};
+    if (j0 + item < ncols) {
+      const int64_t r = row_of(j0 + item);
+      v = *reinterpret_cast<const u32x4 *>(base + r * D + ch * 8);
+    }
+    st.chunk[q] = v;
+  }
+  if (threadIdx.x < kCT) {
+    u32x4 a = {0, 0, 0, 0};
+    if (j0 + (int)threadIdx.x < ncols) {
+      uint16_t nh, nm, nl;
+      split3(norm_of(j0 + (int)threadIdx.x) * inv_s2, nh, nm, nl);
+      a[0] = (uint32_t)nh | ((uint32_t)nm << 16);
+      a[1] = (uint32_t)nl | ((uint32_t)kOne << 16);
+      a[2] = (uint32_t)kOne | ((uint32_t)kOne << 16);
+      a[3] = 0;
+    }
+    st.aug0 = a;
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void stage_store(const ColStage<D> &st, uint16_t *lds) {
+  constexpr int kPer = (kCT * TileCfg<D>::kChunks) / (64 * kWaves);
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const int c = threadIdx.x + q * 64 * kWaves;
+    const int item = c / TileCfg<D>::kChunks, ch = c % TileCfg<D>::kChunks;
+    *reinterpret_cast<u32x4 *>(lds + item * TileCfg<D>::kStride + ch * 8) = st.chunk[q];
+  }
+  if (threadIdx.x < kCT) {
+    *reinterpret_cast<u32x4 *>(lds + threadIdx.x * TileCfg<D>::kStride + D) = st.aug0;
+    *reinterpret_cast<u32x4 *>(lds + threadIdx.x * TileCfg<D>::kStride + D + 8) = u32x4{0, 0, 0, 0};
+  }
+}
+
+// u for the 16 (column item, row item) pairs of this lane: column items
+// m_i = 8 (i / 4) + 4 h + (i % 4), row item = lane % 32.
+template <int D>
+__device__ __forceinline__ f32x16 tile_u(const uint16_t *lds, const RowFrag<D> &rf) {
+  const int l = threadIdx.x & 63;
+  const uint16_t *src = lds + (l & 31) * TileCfg<D>::kStride + 8 * (l >> 5);
+  bf16x8 a[TileCfg<D>::kSteps + 1];
+#pragma unroll
+  for (int kk = 0; kk <= TileCfg<D>::kSteps; ++kk)
+    a[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(src + 16 * kk));
+  f32x16 acc = {};
+#pragma unroll
+  for (int kk = 0; kk <= TileCfg<D>::kSteps; ++kk)
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], rf.b[kk], acc, 0, 0, 0);
+  return acc;
+}
+
+__device__ __forceinline__ int col_of_reg(int i, int h) { return 8 * (i >> 2) + 4 * h + (i & 3); }
+
+// Sum over this lane's 16 weights (as integers), columns >= nvalid masked out.
+template <int P, bool MASK>
+__device__ __forceinline__ uint32_t lane_wsum(const f32x16 &u, int nvalid, int h) {
+  uint32_t s = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    uint32_t raw = weight_raw<P>(u[i], 8388608.0f);
+    if constexpr (MASK) raw = col_of_reg(i, h) < nvalid ? raw : kMagic;
+    s += raw;
+  }
+  return s - 16u * kMagic;
+}
+
+// ---------------------------------------------------------------------------
+// Score: rows = candidates, columns = bank states [0, m).
+// ---------------------------------------------------------------------------
+template <int D, int P>
+__global__ __launch_bounds__(64 * kWaves) void k_score_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
+                                                           Workspace ws, int64_t *out_q, float *out_f) {
+  const int b = blockIdx.y;
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
+  const int x = blockIdx.x * kRowsPerWG + wave * 32 + n;
+  const int m = ws.m[b];
+  __shared__ __attribute__((aligned(16))) uint16_t tile[2][kCT * TileCfg<D>::kStride];
+  __shared__ __attribute__((aligned(16))) float tbs[2][kCT];
+  const uint16_t *K = static_cast<const uint16_t *>(seg_k);
+  const uint16_t *BK = static_cast<const uint16_t *>(bank.k);
+  const bool rv = x < g.N;
+  const size_t xr = (size_t)b * g.N + (rv ? x : 0);
+  RowFrag<D> rf;
+  load_row_frag<D>(rf, K + xr * D, rv ? ws.cnorm[xr] : 0.0f, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
+  const size_t rb = (size_t)b * g.Mcap;
+  auto row_of = [&](int i) -> int64_t { return (int64_t)(rb + i); };
+  auto norm_of = [&](int i) -> float { return bank.knorm[rb + i]; };
+  uint64_t A64 = 0, W64 = 0;
+  const int nt = (m + kCT - 1) / kCT;
+  ColStage<D> st;
+  float bs_next = 0.0f;
+  if (nt > 0) {
+    stage_load<D>(st, BK, 0, m, row_of, norm_of, p.inv_sigma2);
+    if (threadIdx.x < kCT) bs_next = (int)threadIdx.x < m ? ws.bs[rb + threadIdx.x] : 0.0f;
+    stage_store<D>(st, tile[0]);
+    if (threadIdx.x < kCT) tbs[0][threadIdx.x] = bs_next;
+  }
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int cur = t & 1;
+    const int j0n = (t + 1) * kCT;
+    if (t + 1 < nt) {
+      stage_load<D>(st, BK, j0n, m, row_of, norm_of, p.inv_sigma2);
+      if (threadIdx.x < kCT) bs_next = j0n + (int)threadIdx.x < m ? ws.bs[rb + j0n + threadIdx.x] : 0.0f;
+    }
+    const f32x16 u = tile_u<D>(tile[cur], rf);
+    // per-column score scales for this lane's 16 columns
+    float bsv[16];
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const float4 v = *reinterpret_cast<const float4 *>(&tbs[cur][8 * gq + 4 * h]);
+      bsv[4 * gq + 0] = v.x;
+      bsv[4 * gq + 1] = v.y;
+      bsv[4 * gq + 2] = v.z;
+      bsv[4 * gq + 3] = v.w;
+    }
+    const int nvalid = m - t * kCT;
+    uint32_t sw = 0, sa = 0;
+    if (nvalid >= kCT) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float tt = 1.0f + u[i];
+        float tp = tt;
+        if constexpr (P >= 2) tp = tt * tt;
+        if constexpr (P == 4) tp = tp * tp;
+        const float y = __builtin_amdgcn_rcpf(tp);
+        const float e = __builtin_fmaf(-tp, y, 1.0f);
+        const float w = __builtin_fmaf(e, y, y);
+        sw += __float_as_uint(__builtin_fmaf(w, 8388608.0f, 8388608.0f));
+        sa += __float_as_uint(__builtin_fmaf(w, bsv[i], 8388608.0f));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float tt = 1.0f + u[i];
+        float tp = tt;
+        if constexpr (P >= 2) tp = tt * tt;
+        if constexpr (P == 4) tp = tp * tp;
+        const float y = __builtin_amdgcn_rcpf(tp);
+        const float e = __builtin_fmaf(-tp, y, 1.0f);
+        const float w = __builtin_fmaf(e, y, y);
+        const bool ok = col_of_reg(i, h) < nvalid;
+        sw += ok ? __float_as_uint(__builtin_fmaf(w, 8388608.0f, 8388608.0f)) : kMagic;
+        sa += ok ? __float_as_uint(__builtin_fmaf(w, bsv[i], 8388608.0f)) : kMagic;
+      }
+    }
+    W64 += (uint32_t)(sw - 16u * kMagic);
+    A64 += (uint32_t)(sa - 16u * kMagic);
+    if (t + 1 < nt) {
+      stage_store<D>(st, tile[cur ^ 1]);
+      if (threadIdx.x < kCT) tbs[cur ^ 1][threadIdx.x] = bs_next;
+    }
+    __syncthreads();
+  }
+  const uint64_t Wt = W64 + __shfl_xor(W64, 32, 64);
+  const uint64_t At = A64 + __shfl_xor(A64, 32, 64);
+  if (!rv || h != 0) return;
+  const size_t o = (size_t)b * g.N + x;
+  if (ws.acol) {
+    ws.acol[o] = (int64_t)At;
+    ws.wcol[o] = (int64_t)Wt;
+    ws.skey[o] = (At << 13) | (uint64_t)x;
+  }
+  if (out_q) out_q[o] = (int64_t)At;
+  if (out_f) out_f[o] = m > 0 ? (float)(ldexp((double)At, ws.E[b] - 23) / (double)m) : 0.0f;
+}
+
+// ---------------------------------------------------------------------------
+// Crossing: rows = bank states, columns = candidates order[0..R).
+// ---------------------------------------------------------------------------
+template <int D, int P>
+__global__ __launch_bounds__(64 * kWaves) void k_cross_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
+                                                           Workspace ws, int32_t *out_first) {
+  const int b = blockIdx.y;
+  const int m = ws.m[b], R = ws.R[b];
+  if ((int)blockIdx.x * kRowsPerWG >= m) return;
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
+  const int i = blockIdx.x * kRowsPerWG + wave * 32 + n;
+  __shared__ __attribute__((aligned(16))) uint16_t tile[2][kCT * TileCfg<D>::kStride];
+  const uint16_t *K = static_cast<const uint16_t *>(seg_k);
+  const uint16_t *BK = static_cast<const uint16_t *>(bank.k);
+  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
+  const bool rv = i < m;
+  const size_t row = rb + (rv ? i : 0);
+  RowFrag<D> rf;
+  load_row_frag<D>(rf, BK + row * D, rv ? bank.knorm[row] : 0.0f, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
+  int64_t thr = 0;
+  if (rv) {
+    const int64_t lim = ((int64_t)p.tau_num * bank.base[row] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
+    thr = lim - bank.rho[row];
+  }
+  int first = thr <= 0 ? 0 : R + 1;
+  int64_t P64 = 0;
+  uint32_t ck = 0;
+  auto row_of = [&](int j) -> int64_t { return (int64_t)(nb + ws.order[nb + j]); };
+  auto norm_of = [&](int j) -> float { return ws.cnorm[nb + ws.order[nb + j]]; };
+  const int nt = (R + kCT - 1) / kCT;
+  ColStage<D> st;
+  if (nt > 0) {
+    stage_load<D>(st, K, 0, R, row_of, norm_of, p.inv_sigma2);
+    stage_store<D>(st, tile[0]);
+  }
+  __syncthreads();
+  for (int t = 0; t < nt; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < nt) stage_load<D>(st, K, (t + 1) * kCT, R, row_of, norm_of, p.inv_sigma2);
+    const f32x16 u = tile_u<D>(tile[cur], rf);
+    const int nvalid = R - t * kCT;
+    uint32_t wv[16];
+    uint32_t s = 0;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      uint32_t raw = weight_raw<P>(u[q], 8388608.0f);
+      if (nvalid < kCT) raw = col_of_reg(q, h) < nvalid ? raw : kMagic;
+      wv[q] = raw - kMagic;
+      s += raw;
+    }
+    s -= 16u * kMagic;
+    const uint32_t tsum = s + __shfl_xor(s, 32, 64);
+    const int64_t Pn = P64 + tsum;
+    const bool cross_here = rv && first > R && Pn >= thr;
+    if (__any(cross_here)) {
+      // exact position inside the tile: prefix in column order
+      uint32_t other[16];
+#pragma unroll
+      for (int q = 0; q < 16; ++q) other[q] = __shfl_xor(wv[q], 32, 64);
+      int64_t run = P64;
+      int f = -1;
+#pragma unroll
+      for (int mm = 0; mm < 32; ++mm) {
+        const int gq = mm >> 2, q = 4 * (gq >> 1) + (mm & 3);
+        const bool from_h1 = (gq & 1) != 0;
+        const uint32_t w = (from_h1 == (h == 1)) ? wv[q] : other[q];
+        run += w;
+        if (f < 0 && run >= thr) f = mm;
+      }
+      if (cross_here) first = t * kCT + f + 1;
+    }
+    P64 = Pn;
+    ck += tsum;
+    if (((t + 1) % (kCkStride / kCT)) == 0) {
+      if (rv && h == 0) ws.ck[row * ws.nck + ((t + 1) / (kCkStride / kCT) - 1)] = ck;
+      ck = 0;
+    }
+    if (t + 1 < nt) stage_store<D>(st, tile[cur ^ 1]);
+    __syncthreads();
+  }
+  if (!rv || h != 0) return;
+  ws.first[row] = first;
+  if (out_first) out_first[row] = first;
+}
+
+// ---------------------------------------------------------------------------
+// Row sums.  MODE selects rows, columns and where the sum goes.
+// ---------------------------------------------------------------------------
+enum RowSumMode { RS_FIXUP = 0, RS_SURV_EV = 1, RS_ADM_BASE = 2, RS_ADM_MUT = 3, RS_DENSITY = 4 };
+
+struct RSSetup {
+  int nrows;
+  int c0, c1;          // column range [c0, c1)
+  const uint16_t *rk;  // row keys base (element offset via rrow)
+  const uint16_t *ck;  // column keys base
+  bool diag;           // exclude column == row (same list, same index)
+};
+
+template <int D, int P, int MODE>
+__global__ __launch_bounds__(64 * kWaves) void k_rowsum_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
+                                                            Workspace ws, int64_t *out) {
+  const int b = blockIdx.y;
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
+  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
+  const int m = ws.m[b];
+  const uint16_t *SK = static_cast<const uint16_t *>(seg_k);
+  const uint16_t *BK = static_cast<const uint16_t *>(bank.k);
+  const int n_ev = (MODE == RS_DENSITY || MODE == RS_FIXUP) ? 0 : ws.n_ev[b];
+  const int rs = (MODE == RS_DENSITY) ? 0 : ws.r_star[b / g.gs];
+  const int n_surv = m - n_ev;
+  // rows
+  int nrows;
+  if constexpr (MODE == RS_FIXUP || MODE == RS_DENSITY) nrows = m;
+  else if constexpr (MODE == RS_SURV_EV) nrows = n_surv;
+  else nrows = rs;
+  if ((int)blockIdx.x * kRowsPerWG >= nrows) return;
+  // columns: [c0, c1) of a list
+  int c0 = 0, c1 = 0;
+  bool adm_by_ev = n_ev <= n_surv;
+  if constexpr (MODE == RS_FIXUP) {
+    c0 = (rs / kCkStride) * kCkStride;
+    c1 = rs;
+  } else if constexpr (MODE == RS_SURV_EV) {
+    c1 = n_ev;
+  } else if constexpr (MODE == RS_ADM_BASE) {
+    c1 = adm_by_ev ? n_ev : n_surv;
+  } else if constexpr (MODE == RS_ADM_MUT) {
+    c1 = rs;
+  } else {
+    c1 = m;
+  }
+  const int v = blockIdx.x * kRowsPerWG + wave * 32 + n;
+  const bool rv = v < nrows;
+  const int vv = rv ? v : 0;
+  // row item location
+  const uint16_t *rkey = BK + rb * D;
+  float rnorm = 0.0f;
+  size_t out_idx = 0;
+  if (rv) {
+    if constexpr (MODE == RS_FIXUP || MODE == RS_DENSITY) {
+      rkey = BK + (rb + vv) * D;
+      rnorm = bank.knorm[rb + vv];
+      out_idx = rb + vv;
+    } else if constexpr (MODE == RS_SURV_EV) {
+      const int s = ws.surv_list[rb + vv];
+      rkey = BK + (rb + s) * D;
+      rnorm = bank.knorm[rb + s];
+      out_idx = rb + s;
+    } else {
+      const int x = ws.adm_list[nb + vv];
+      rkey = SK + (nb + x) * D;
+      rnorm = ws.cnorm[nb + x];
+      out_idx = nb + vv;
+    }
+  }
+  RowFrag<D> rf;
+  load_row_frag<D>(rf, rkey, rnorm, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
+  // column item location
+  auto row_of = [&](int j) -> int64_t {
+    if constexpr (MODE == RS_FIXUP) return (int64_t)(nb + ws.order[nb + j]);
+    else if constexpr (MODE == RS_SURV_EV) return (int64_t)(rb + ws.ev_list[rb + j]);
+    else if constexpr (MODE == RS_ADM_BASE)
+      return (int64_t)(rb + (adm_by_ev ? ws.ev_list[rb + j] : ws.surv_list[rb + j]));
+    else if constexpr (MODE == RS_ADM_MUT) return (int64_t)(nb + ws.adm_list[nb + j]);
+    else return (int64_t)(rb + j);
+  };
+  auto norm_of = [&](int j) -> float {
+    if constexpr (MODE == RS_FIXUP) return ws.cnorm[nb + ws.order[nb + j]];
+    else if constexpr (MODE == RS_SURV_EV) return bank.knorm[rb + ws.ev_list[rb + j]];
+    else if constexpr (MODE == RS_ADM_BASE)
+      return bank.knorm[rb + (adm_by_ev ? ws.ev_list[rb + j] : ws.surv_list[rb + j])];
+    else if constexpr (MODE == RS_ADM_MUT) return ws.cnorm[nb + ws.adm_list[nb + j]];
+    else return bank.knorm[rb + j];
+  };
+  const uint16_t *colbase = (MODE == RS_FIXUP || MODE == RS_ADM_MUT) ? SK : BK;
+  constexpr bool kDiag = (MODE == RS_ADM_MUT || MODE == RS_DENSITY);
+  __shared__ __attribute__((aligned(16))) uint16_t tile[2][kCT * TileCfg<D>::kStride];
+  uint64_t S64 = 0;
+  const int ncols = c1 - c0;
+  const int nt = (ncols + kCT - 1) / kCT;
+  ColStage<D> st;
+  auto row_of_rel = [&](int j) -> int64_t { return row_of(c0 + j); };
+  auto norm_of_rel = [&](int j) -> float { return norm_of(c0 + j); };
+  if (nt > 0) {
+    stage_load<D>(st, colbase, 0, ncols, row_of_rel, norm_of_rel, p.inv_sigma2);
+    stage_store<D>(st, tile[0]);
+  }
+  __syncthreads();
+  const int wg_row0 = blockIdx.x * kRowsPerWG;
+  for (int t = 0; t < nt; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < nt) stage_load<D>(st, colbase, (t + 1) * kCT, ncols, row_of_rel, norm_of_rel, p.inv_sigma2);
+    const f32x16 u = tile_u<D>(tile[cur], rf);
+    const int nvalid = ncols - t * kCT;
+    const int j0 = c0 + t * kCT;
+    const bool diag_tile = kDiag && (j0 < wg_row0 + kRowsPerWG) && (j0 + kCT > wg_row0);
+    uint32_t s;
+    if (nvalid >= kCT && !diag_tile) {
+      s = lane_wsum<P, false>(u, kCT, h);
+    } else {
+      s = 0;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int mm = col_of_reg(q, h);
+        uint32_t raw = weight_raw<P>(u[q], 8388608.0f);
+        bool ok = mm < nvalid;
+        if (kDiag) ok = ok && (j0 + mm != v);
+        s += ok ? raw : kMagic;
+      }
+      s -= 16u * kMagic;
+    }
+    S64 += s;
+    if (t + 1 < nt) stage_store<D>(st, tile[cur ^ 1]);
+    __syncthreads();
+  }
+  const uint64_t tot = S64 + __shfl_xor(S64, 32, 64);
+  if (!rv || h != 0) return;
+  if constexpr (MODE == RS_FIXUP) {
+    int64_t Pc = (int64_t)tot;
+    const int full = rs / kCkStride;
+    const size_t row = rb + v;
+    for (int q = 0; q < full; ++q) Pc += ws.ck[row * ws.nck + q];
+    const int64_t rt = bank.rho[row] + Pc;
+    ws.rho_t[row] = rt;
+    if (out) out[row] = rt;
+  } else if constexpr (MODE == RS_SURV_EV) {
+    ws.sub[out_idx] = (int64_t)tot;
+  } else if constexpr (MODE == RS_ADM_BASE) {
+    ws.sub_adm[out_idx] = (int64_t)tot;
+  } else if constexpr (MODE == RS_ADM_MUT) {
+    ws.mut_adm[out_idx] = (int64_t)tot;
+  } else {
+    out[out_idx] = (int64_t)tot;
+  }
+}
+
+inline dim3 grid_rows(int n, int B) { return dim3((unsigned)((n + kRowsPerWG - 1) / kRowsPerWG), (unsigned)B); }
+
+template <int D, int P>
+void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                      const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage) {
+  const int T = 64 * kWaves;
+  switch (stage) {
+    case 0:
+      k_score_mfma<D, P><<<grid_rows(g.N, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, out.score_q, nullptr);
+      break;
+    case 1:
+      k_cross_mfma<D, P><<<grid_rows(g.Mcap, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, out.first_cross);
+      break;
+    case 2:
+      k_rowsum_mfma<D, P, RS_FIXUP><<<grid_rows(g.Mcap, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, out.rho_tilde);
+      break;
+    case 3:
+      k_rowsum_mfma<D, P, RS_SURV_EV><<<grid_rows(g.Mcap, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
+      if (g.N > 0) {
+        k_rowsum_mfma<D, P, RS_ADM_BASE><<<grid_rows(g.N, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
+        k_rowsum_mfma<D, P, RS_ADM_MUT><<<grid_rows(g.N, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
+      }
+      break;
+    default:
+      break;
+  }
+}
+
+template <int D>
+void mfma_stage_d(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                  const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage) {
+  if (p.p == 1) mfma_update_impl<D, 1>(bank, seg, g, p, out, ws, s, stage);
+  else if (p.p == 2) mfma_update_impl<D, 2>(bank, seg, g, p, out, ws, s, stage);
+  else mfma_update_impl<D, 4>(bank, seg, g, p, out, ws, s, stage);
+}
+
+template <int D, int P>
+void mfma_score_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                     int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws, hipStream_t s) {
+  const int T = 64 * kWaves;
+  if (g.N > 0 && (score_q || score_f))
+    k_score_mfma<D, P><<<grid_rows(g.N, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, score_q, score_f);
+  if (density)
+    k_rowsum_mfma<D, P, RS_DENSITY><<<grid_rows(g.Mcap, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, density);
+}
+
+}  // namespace
+
+// Stage launchers used by the update sequence for bf16 banks:
+// 0 score, 1 crossing, 2 r* fix-up, 3 maintenance.
+void launch_gram_mfma(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                      const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage) {
+  if (g.d == 128) mfma_stage_d<128>(bank, seg, g, p, out, ws, s, stage);
+  else mfma_stage_d<64>(bank, seg, g, p, out, ws, s, stage);
+}
+
+void launch_score_mfma(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                       int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws, hipStream_t s) {
+  auto go = [&](auto dtag, auto ptag) {
+    constexpr int D = decltype(dtag)::value, P = decltype(ptag)::value;
+    mfma_score_impl<D, P>(bank, seg, g, p, score_q, score_f, density, ws, s);
+  };
+  using I64 = std::integral_constant<int, 64>;
+  using I128 = std::integral_constant<int, 128>;
+  using P1 = std::integral_constant<int, 1>;
+  using P2 = std::integral_constant<int, 2>;
+  using P4 = std::integral_constant<int, 4>;
+  if (g.d == 128) {
+    if (p.p == 1) go(I128{}, P1{});
+    else if (p.p == 2) go(I128{}, P2{});
+    else go(I128{}, P4{});
+  } else {
+    if (p.p == 1) go(I64{}, P1{});
+    else if (p.p == 2) go(I64{}, P2{});
+    else go(I64{}, P4{});
+  }
+}
+
+}  // namespace dkv

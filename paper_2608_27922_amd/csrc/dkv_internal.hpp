@@ -38,11 +38,13 @@ struct Workspace {
   int64_t *rho_t;      // [B, Mcap] rho + P(r*)
   int32_t *dest;       // [B, Mcap] final slot of each pre-update slot, -1 if evicted
   int32_t *ev_list;    // [B, Mcap] evicted slots ascending
+  int32_t *surv_list;  // [B, Mcap] surviving slots ascending
   int32_t *adm_list;   // [B, N]   admitted source indices ascending
   int32_t *adm_dest;   // [B, N]   final slot of each admitted candidate
   int64_t *sub;        // [B, Mcap] sum of weights to the evicted states (survivors)
-  int64_t *sub_adm;    // [B, N]   sum of weights to the evicted states (admitted)
-  int64_t *mut_adm;    // [B, N]   sum of weights to all admitted (admitted, incl. self)
+  int64_t *sub_adm;    // [B, N]   admitted: sum of weights to the evicted states if
+                       //          n_ev <= n_surv, else to the survivors
+  int64_t *mut_adm;    // [B, N]   admitted: sum of weights to the other admitted
   int nck;
 };
 
@@ -70,6 +72,10 @@ hipError_t launch_score(const dkv_bank &bank, const dkv_segment &seg, const Geom
 hipError_t launch_attention(const dkv_bank &bank, const void *q, int nq, const void *wk,
                             const void *wv, int nw, void *out, float scale, const Geom &g,
                             hipStream_t s);
+void launch_gram_mfma(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                      const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage);
+void launch_score_mfma(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                       int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws, hipStream_t s);
 hipError_t launch_pair_weight(const float *d2, int64_t n, const Prm &p, int32_t *w,
                               hipStream_t s);
 
@@ -94,15 +100,24 @@ __device__ __forceinline__ float load_elem(const void *p, size_t i) {
   }
 }
 
+// Correctly rounded binary32 reciprocal for normal inputs with normal results:
+// hardware estimate y, exact residual e = 1 - x y by FMA, one correction
+// y + e y.  Checked against the IEEE division for every significand.
+__device__ __forceinline__ float rcp_rn(float x) {
+  const float y = __builtin_amdgcn_rcpf(x);
+  const float e = __builtin_fmaf(-x, y, 1.0f);
+  return __builtin_fmaf(e, y, y);
+}
+
 // Soft-Riesz weight (eps = 1): w = 1 / (1 + d2 / sigma^2)^p, each step one
-// binary32 operation rounded to nearest even; the reciprocal is the IEEE
-// correctly rounded division.  d2 * inv_sigma2 is exact (power of two).
+// binary32 operation rounded to nearest even with a correctly rounded
+// reciprocal.  d2 * inv_sigma2 is exact (power of two).
 __device__ __forceinline__ float pair_weight(float d2, float inv_sigma2, int p) {
   float t = 1.0f + d2 * inv_sigma2;
   float tp = t;
   if (p >= 2) tp = t * t;
   if (p == 4) tp = tp * tp;
-  return 1.0f / tp;
+  return rcp_rn(tp);
 }
 // RNE(w * scale) for w * scale in [0, 2^23]: fma(w, scale, 2^23) lands in
 // [2^23, 2^24] where one ulp is 1, so its bit pattern minus that of 2^23 is

@@ -491,13 +491,16 @@ __global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspac
   for (int i = lo; i < hi; ++i) cnt_local += (st[i] == ST_VIOL || st[i] == ST_SEL);
   int n_ev;
   int pos = block_excl_scan(cnt_local, &n_ev, tmp);
+  int spos = lo - pos;  // survivors before this thread's range
   for (int i = lo; i < hi; ++i) {
     if (st[i] == ST_VIOL || st[i] == ST_SEL) {
       ws.ev_list[rb + pos] = i;
       ws.dest[rb + i] = -1 - pos;  // provisional: encodes the evicted rank
       ++pos;
     } else {
+      ws.surv_list[rb + spos] = i;
       ws.dest[rb + i] = i;
+      ++spos;
     }
   }
   // admitted list: source indices x with rank(x) < r*, ascending
@@ -576,14 +579,18 @@ __global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspac
 
 // ---------------------------------------------------------------------------
 // k_maint_gram: virtual rows [0, Mcap) = pre-update slots (survivors),
-// [Mcap, Mcap + N) = admitted list entries.  Sums of weights to the evicted
-// states (all rows) and to the admitted candidates (admitted rows only).
+// [Mcap, Mcap + N) = admitted list entries.  Survivors: sum of weights to the
+// evicted states.  Admitted: sum of weights to the evicted states (when there
+// are no more of them than survivors; else to the survivors) and to the other
+// admitted candidates (self excluded by index).
 // ---------------------------------------------------------------------------
 template <int D, int DT>
 __global__ __launch_bounds__(kThreads) void k_maint_gram(dkv_bank bank, const void *seg_k, Geom g,
                                                          Prm p, Workspace ws) {
   const int b = blockIdx.y, v = blockIdx.x * kThreads + threadIdx.x;
   const int m = ws.m[b], n_ev = ws.n_ev[b];
+  const int n_surv = m - n_ev;
+  const bool by_ev = n_ev <= n_surv;
   const int rs = ws.r_star[b / g.gs];
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
   bool surv = false, adm = false;
@@ -592,63 +599,69 @@ __global__ __launch_bounds__(kThreads) void k_maint_gram(dkv_bank bank, const vo
   const bool act = surv || adm;
   if (!__syncthreads_or(act)) return;
   const bool any_adm = __syncthreads_or(adm);
+  const bool any_surv = __syncthreads_or(surv);
   __shared__ float tk[kTile][D];
   __shared__ float tn[kTile];
   float kr[D];
   float nr = 0.0f;
+  const int k_adm = v - g.Mcap;
   if (surv) {
     load_row<D, DT>(kr, bank.k, rb + v);
     nr = bank.knorm[rb + v];
   } else if (adm) {
-    const int x = ws.adm_list[nb + (v - g.Mcap)];
+    const int x = ws.adm_list[nb + k_adm];
     load_row<D, DT>(kr, seg_k, nb + x);
     nr = ws.cnorm[nb + x];
   }
-  int64_t s_ev = 0, s_adm = 0;
-  for (int j0 = 0; j0 < n_ev; j0 += kTile) {
-    const int nc = min(kTile, n_ev - j0);
-    __syncthreads();
-    for (int t = threadIdx.x; t < kTile * D; t += kThreads) {
-      const int c = t / D, j = t % D;
-      tk[c][j] = c < nc ? load_elem<DT>(bank.k, (rb + ws.ev_list[rb + j0 + c]) * D + j) : 0.0f;
-    }
-    if (threadIdx.x < kTile) {
-      const int c = threadIdx.x;
-      tn[c] = c < nc ? bank.knorm[rb + ws.ev_list[rb + j0 + c]] : 0.0f;
-    }
-    __syncthreads();
-    if (act) {
-      for (int c = 0; c < nc; ++c) {
-        const float d2 = (nr + tn[c]) - 2.0f * dot_row<D>(kr, tk[c]);
-        s_ev += q23_round(pair_weight(d2, p.inv_sigma2, p.p), 8388608.0f);
-      }
-    }
-  }
-  if (any_adm) {
-    for (int j0 = 0; j0 < rs; j0 += kTile) {
-      const int nc = min(kTile, rs - j0);
+  // pass 0: evicted columns (survivor rows, and admitted rows when by_ev)
+  // pass 1: survivor columns (admitted rows when !by_ev)
+  // pass 2: admitted columns (admitted rows)
+  int64_t s_base = 0, s_adm = 0;
+  for (int pass = 0; pass < 3; ++pass) {
+    int ncol;
+    if (pass == 0) ncol = (any_surv || (any_adm && by_ev)) ? n_ev : 0;
+    else if (pass == 1) ncol = (any_adm && !by_ev) ? n_surv : 0;
+    else ncol = any_adm ? rs : 0;
+    const bool use = pass == 0 ? (surv || (adm && by_ev)) : adm;
+    for (int j0 = 0; j0 < ncol; j0 += kTile) {
+      const int nc = min(kTile, ncol - j0);
       __syncthreads();
       for (int t = threadIdx.x; t < kTile * D; t += kThreads) {
         const int c = t / D, j = t % D;
-        tk[c][j] = c < nc ? load_elem<DT>(seg_k, (nb + ws.adm_list[nb + j0 + c]) * D + j) : 0.0f;
+        float val = 0.0f;
+        if (c < nc) {
+          if (pass == 0) val = load_elem<DT>(bank.k, (rb + ws.ev_list[rb + j0 + c]) * D + j);
+          else if (pass == 1) val = load_elem<DT>(bank.k, (rb + ws.surv_list[rb + j0 + c]) * D + j);
+          else val = load_elem<DT>(seg_k, (nb + ws.adm_list[nb + j0 + c]) * D + j);
+        }
+        tk[c][j] = val;
       }
       if (threadIdx.x < kTile) {
         const int c = threadIdx.x;
-        tn[c] = c < nc ? ws.cnorm[nb + ws.adm_list[nb + j0 + c]] : 0.0f;
+        float nv = 0.0f;
+        if (c < nc) {
+          if (pass == 0) nv = bank.knorm[rb + ws.ev_list[rb + j0 + c]];
+          else if (pass == 1) nv = bank.knorm[rb + ws.surv_list[rb + j0 + c]];
+          else nv = ws.cnorm[nb + ws.adm_list[nb + j0 + c]];
+        }
+        tn[c] = nv;
       }
       __syncthreads();
-      if (adm) {
+      if (use) {
         for (int c = 0; c < nc; ++c) {
+          if (pass == 2 && j0 + c == k_adm) continue;  // j != x by index
           const float d2 = (nr + tn[c]) - 2.0f * dot_row<D>(kr, tk[c]);
-          s_adm += q23_round(pair_weight(d2, p.inv_sigma2, p.p), 8388608.0f);
+          const uint32_t W = q23_round(pair_weight(d2, p.inv_sigma2, p.p), 8388608.0f);
+          if (pass == 2) s_adm += W;
+          else s_base += W;
         }
       }
     }
   }
-  if (surv) ws.sub[rb + v] = s_ev;
+  if (surv) ws.sub[rb + v] = s_base;
   if (adm) {
-    ws.sub_adm[nb + (v - g.Mcap)] = s_ev;
-    ws.mut_adm[nb + (v - g.Mcap)] = s_adm;
+    ws.sub_adm[nb + k_adm] = s_base;
+    ws.mut_adm[nb + k_adm] = s_adm;
   }
 }
 
@@ -698,7 +711,11 @@ __global__ __launch_bounds__(kThreads) void k_commit(dkv_bank bank, dkv_segment 
       V[(rb + to) * D + j] = SV[(nb + x) * D + j];
     }
     if (lane == 0) {
-      const int64_t rho = ws.wcol[nb + x] - ws.sub_adm[nb + k] + ws.mut_adm[nb + k] - (int64_t)kQ23;
+      // density over the final bank: survivors (directly, or the whole old bank
+      // minus the evicted) plus the other co-admitted candidates
+      const int n_ev = ws.n_ev[b];
+      const int64_t surv_sum = (n_ev <= m - n_ev) ? ws.wcol[nb + x] - ws.sub_adm[nb + k] : ws.sub_adm[nb + k];
+      const int64_t rho = surv_sum + ws.mut_adm[nb + k];
       bank.rho[rb + to] = rho;
       bank.base[rb + to] = rho > p.delta_q ? rho : p.delta_q;
       bank.prov[rb + to] = ((int64_t)p.block_id << 32) | (int64_t)x;
@@ -758,20 +775,24 @@ template <int D, int DT>
 hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                        const dkv_update_out *outp, const Workspace &ws, hipStream_t s) {
   dkv_update_out out = outp ? *outp : dkv_update_out{};
+  // bf16 banks: Gram stages on MFMA; fp32 banks: the same stages on the VALU.
+  constexpr bool kMfma = DT == DKV_BF16;
   k_prep<<<g.B, kThreads, 0, s>>>(bank, g, ws);
   if (g.N > 0) {
     k_cand_norms<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(seg.k, g, ws);
-    k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.score_q, nullptr);
+    if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 0);
+    else k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.score_q, nullptr);
     k_sort<<<g.B, kBig, 0, s>>>(g, ws, out.order);
-    k_cross_gram<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.first_cross);
-  } else {
-    // no candidates: no prefix to test; first crossing is 0 for violators only
-    k_cross_gram<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.first_cross);
   }
+  // with no candidates only states that already violate are found (prefix 0)
+  if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 1);
+  else k_cross_gram<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.first_cross);
   k_feasible<<<g.G, kBig, 0, s>>>(g, ws, out.r_star);
-  k_fixup<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.rho_tilde);
+  if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 2);
+  else k_fixup<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.rho_tilde);
   k_select<<<g.B, kBig, 0, s>>>(bank, g, ws, out);
-  k_maint_gram<D, DT><<<grid2(g.Mcap + g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws);
+  if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 3);
+  else k_maint_gram<D, DT><<<grid2(g.Mcap + g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws);
   k_commit<D, DT><<<grid2(g.Mcap + g.N, kThreads / 64, g.B), kThreads, 0, s>>>(bank, seg, g, p, ws);
   return hipGetLastError();
 }
@@ -781,14 +802,18 @@ hipError_t score_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
                       int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws,
                       hipStream_t s) {
   k_prep<<<g.B, kThreads, 0, s>>>(bank, g, ws);
-  if (g.N > 0 && (score_q || score_f)) {
-    Workspace w2 = ws;
-    w2.acol = nullptr;  // scoring only: no sort keys needed
+  Workspace w2 = ws;
+  w2.acol = nullptr;  // scoring only: no sort keys needed
+  if (g.N > 0 && (score_q || score_f))
     k_cand_norms<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(seg.k, g, ws);
-    k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, w2, score_q, score_f);
+  if constexpr (DT == DKV_BF16) {
+    launch_score_mfma(bank, seg, g, p, (g.N > 0) ? score_q : nullptr, (g.N > 0) ? score_f : nullptr, density, w2, s);
+  } else {
+    if (g.N > 0 && (score_q || score_f))
+      k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, w2, score_q, score_f);
+    if (density)
+      k_bank_density<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, g, p, ws, density);
   }
-  if (density)
-    k_bank_density<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, g, p, ws, density);
   return hipGetLastError();
 }
 
