@@ -34,7 +34,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, help="workload: 1 (tiny) or 2 (one layer, 12 heads)")
+    ap.add_argument("--workload", default="single_layer", help="tiny or single_layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=1, help="heads in the oracle sample")
     return ap.parse_args()
@@ -74,9 +74,9 @@ def main():
     import torch
     from paper_2608_27922_amd import api, synth
 
-    cfg = synth.CONFIGS[args.config]
+    cfg = synth.WORKLOADS[args.workload]
     if not cfg.starts_full:
-        raise SystemExit("bench workload must be a single-update configuration (1 or 2)")
+        raise SystemExit("bench workload must be a single-update workload (tiny or single_layer)")
     torch.cuda.set_device(0)
     dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     case = synth.single_update_case(cfg)
@@ -134,7 +134,7 @@ def main():
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg.dtype, "data": "synthetic",
-        "config": {"workload": f"config {cfg.key} ({cfg.name}): {cfg.layers} layer x {cfg.heads} heads, d={d}, "
+        "config": {"workload": f"{cfg.name}: {cfg.layers} layer x {cfg.heads} heads, d={d}, "
                                f"{cfg.dtype}, budget {cfg.budget} (starts full), segment {N} (30% near-duplicates), "
                                f"{cfg.n_query} queries over bank + {cfg.n_window}-token window",
                    "banks": B, "group_size": cfg.group_size, "candidates": N, "budget": cfg.budget,

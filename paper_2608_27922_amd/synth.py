@@ -34,7 +34,7 @@ GRID_MAX = 127     # |integer| <= 127
 
 @dataclass(frozen=True)
 class Config:
-    key: int
+    seed_id: int               # seeds this workload's random streams
     name: str
     layers: int
     heads: int
@@ -60,17 +60,22 @@ class Config:
         return self.layers * self.heads
 
 
-CONFIGS: Dict[int, Config] = {
-    1: Config(1, "tiny", 1, 2, 64, "f32", 64, 64, 64, 256, 8, 1, 2, 5, starts_full=True),
-    2: Config(2, "single_layer", 1, 12, 128, "bf16", 4680, 4680, 4680, 4680, 64, 1, 12, 6,
-              starts_full=True, dup_frac=0.3),
-    3: Config(3, "rollout", 30, 12, 128, "bf16", 4680, 4680, 4680, 9360, 64, 20, 12, 6,
-              drift=0.05),
-    4: Config(4, "long_rollout", 30, 12, 128, "bf16", 4680, 4680, 4680, 18720, 256, 80, 12, 6,
-              active=16, revisit=10),
-    5: Config(5, "headwise_budgets", 30, 12, 128, "bf16", 4680, 4680, 4680, 18720, 64, 160, 1, 6,
-              drift=0.05, ragged=(2340, 4680, 9360, 18720)),
-}
+WORKLOADS: Dict[str, Config] = {c.name: c for c in (
+    # 1 layer x 2 heads, d 64, fp32, budget 256 (starts full), 64 candidates, 64 queries + 64 window
+    Config(1, "tiny", 1, 2, 64, "f32", 64, 64, 64, 256, 8, 1, 2, 5, starts_full=True),
+    # 1 layer x 12 heads, d 128, bf16, budget 4680 (starts full), 4680 candidates with 30%
+    # near-duplicates, 4680 queries over bank + 4680 window
+    Config(2, "single_layer", 1, 12, 128, "bf16", 4680, 4680, 4680, 4680, 64, 1, 12, 6,
+           starts_full=True, dup_frac=0.3),
+    # 30 layers x 12 heads, 20 blocks of 4680 into budget 9360, drifting centres
+    Config(3, "rollout", 30, 12, 128, "bf16", 4680, 4680, 4680, 9360, 64, 20, 12, 6, drift=0.05),
+    # 30 layers x 12 heads, 80 blocks into budget 18720, 256 clusters, recurring sets every 10 blocks
+    Config(4, "long_rollout", 30, 12, 128, "bf16", 4680, 4680, 4680, 18720, 256, 80, 12, 6,
+           active=16, revisit=10),
+    # 30 layers x 12 heads, 160 blocks, per-head budgets from {2340, 4680, 9360, 18720}, heads independent
+    Config(5, "headwise_budgets", 30, 12, 128, "bf16", 4680, 4680, 4680, 18720, 64, 160, 1, 6,
+           drift=0.05, ragged=(2340, 4680, 9360, 18720)),
+)}
 
 ROLE_CENTRES, ROLE_K, ROLE_V, ROLE_Q, ROLE_DUP, ROLE_BUDGET, ROLE_DRIFT, ROLE_ACTIVE = range(8)
 
@@ -100,7 +105,7 @@ def budgets(cfg: Config, seed: int = 0) -> np.ndarray:
     """Per-(layer, head) budgets, shape (layers * heads,)."""
     if not cfg.ragged:
         return np.full(cfg.banks, cfg.budget, np.int32)
-    r = _rng(seed, cfg.key, ROLE_BUDGET)
+    r = _rng(seed, cfg.seed_id, ROLE_BUDGET)
     return np.asarray(cfg.ragged, np.int32)[r.integers(0, len(cfg.ragged), cfg.banks)]
 
 
@@ -113,7 +118,7 @@ class HeadStream:
 
     def __init__(self, cfg: Config, layer: int, head: int, seed: int = 0):
         self.cfg, self.layer, self.head, self.seed = cfg, layer, head, seed
-        r = _rng(seed, cfg.key, layer, head, ROLE_CENTRES)
+        r = _rng(seed, cfg.seed_id, layer, head, ROLE_CENTRES)
         g = r.standard_normal((cfg.clusters, cfg.d))
         self._c0 = g / np.linalg.norm(g, axis=1, keepdims=True)
         self._centres = {0: self._c0}
@@ -125,7 +130,7 @@ class HeadStream:
         last = max(k for k in self._centres if k <= t)
         c = self._centres[last]
         for s in range(last + 1, t + 1):
-            u = _rng(self.seed, self.cfg.key, self.layer, self.head, ROLE_DRIFT, s).standard_normal(c.shape)
+            u = _rng(self.seed, self.cfg.seed_id, self.layer, self.head, ROLE_DRIFT, s).standard_normal(c.shape)
             u /= np.linalg.norm(u, axis=1, keepdims=True)
             c = c + self.cfg.drift * u
             c = c / np.linalg.norm(c, axis=1, keepdims=True)
@@ -138,11 +143,11 @@ class HeadStream:
             return np.arange(cfg.clusters)
         if cfg.revisit and t >= cfg.revisit and t % cfg.revisit == 0:
             return self.active_set(t - cfg.revisit)
-        r = _rng(self.seed, cfg.key, self.layer, self.head, ROLE_ACTIVE, t)
+        r = _rng(self.seed, cfg.seed_id, self.layer, self.head, ROLE_ACTIVE, t)
         return np.sort(r.choice(cfg.clusters, cfg.active, replace=False))
 
     def _mixture(self, role: int, t: int, n: int) -> np.ndarray:
-        r = _rng(self.seed, self.cfg.key, self.layer, self.head, role, t)
+        r = _rng(self.seed, self.cfg.seed_id, self.layer, self.head, role, t)
         act = self.active_set(t)
         z = act[r.integers(0, act.size, n)]
         noise = r.standard_normal((n, self.cfg.d), dtype=np.float32)
@@ -162,7 +167,7 @@ class HeadStream:
         (cosine > 0.95) of uniformly drawn rows of bank_keys."""
         cfg = self.cfg
         n = K.shape[0]
-        r = _rng(self.seed, cfg.key, self.layer, self.head, ROLE_DUP, t)
+        r = _rng(self.seed, cfg.seed_id, self.layer, self.head, ROLE_DUP, t)
         k = int(round(cfg.dup_frac * n))
         rows = np.sort(r.choice(n, k, replace=False))
         src = r.integers(0, bank_keys.shape[0], k)

@@ -78,7 +78,7 @@ def _run_rollout(cfg, blocks, prm, budgets=None, dup_every=0, trace=True, init_f
     return bank, obanks
 
 
-SMALL = dict(key=77, name="small", layers=1, n_query=40, n_window=24, clusters=6, blocks=6, sigma2_log2=4,
+SMALL = dict(seed_id=77, name="small", layers=1, n_query=40, n_window=24, clusters=6, blocks=6, sigma2_log2=4,
              drift=0.05)
 
 
@@ -227,19 +227,20 @@ def test_score_and_bank_density():
 
 # ----------------------------------------------------------------------------- configs 1 and 2
 
-def _starts_full_case(key):
-    cfg = synth.CONFIGS[key]
+def _starts_full_case(name):
+    cfg = synth.WORKLOADS[name]
     prm = api.Params(sigma2_log2=cfg.sigma2_log2)
     case = synth.single_update_case(cfg)
     return cfg, prm, case
 
 
-@pytest.mark.parametrize("key", [1, 2])
-def test_config_update_and_attention(key):
-    """Config 1 (tiny, fp32) and config 2 (one layer x 12 heads, d 128, bf16, N = M = 4680,
-    30% near-duplicates): bank built by the empty-bank rule, one update, then attention."""
-    _log(f"config {key}")
-    cfg, prm, case = _starts_full_case(key)
+@pytest.mark.parametrize("name", ["tiny", "single_layer"])
+def test_workload_update_and_attention(name):
+    """tiny (1 layer x 2 heads, d 64, fp32, budget 256, 64 candidates) and single_layer (1 layer x
+    12 heads, d 128, bf16, N = M = 4680, 30% near-duplicates): bank built by the empty-bank rule,
+    one update, then attention."""
+    _log(f"workload {name}")
+    cfg, prm, case = _starts_full_case(name)
     B, gs, d, dt, M, N = cfg.heads, cfg.group_size, cfg.d, cfg.dtype, cfg.budget, cfg.n_cand
     op = oracle_params(prm)
     bank = api.Bank(B, M, d, dtype=torch.bfloat16 if dt == "bf16" else torch.float32, group_size=gs)
@@ -251,9 +252,9 @@ def test_config_update_and_attention(key):
         torch.cuda.synchronize()
         _log(f"  block {blk}: GPU done, running oracle")
         new, recs = oracle_step(ob, K, V, blk, op, gs)
-        assert_trace_equal(out, recs, gs, ob, K.shape[1], ctx=f"config {key} block {blk}")
+        assert_trace_equal(out, recs, gs, ob, K.shape[1], ctx=f"{name} block {blk}")
         for b in range(B):
-            assert_bank_equal(bank, b, new[b], ctx=f"config {key} block {blk}")
+            assert_bank_equal(bank, b, new[b], ctx=f"{name} block {blk}")
         ob = new
         _log(f"  block {blk}: r* = {recs[0].r_star}, evicted {[int(x) for x in out.n_evicted.cpu()][:4]}")
     q, wk, wv = case["q"], case["win_K"], case["win_V"]

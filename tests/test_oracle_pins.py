@@ -259,7 +259,7 @@ def test_tiny_rollout_matches_exact_bruteforce(seed):
 # ---------------------------------------------------------------- invariants on cluster data
 
 def _small_cfg(**kw):
-    base = dict(key=91, name="pin", layers=1, heads=4, d=16, dtype="f32", n_cand=24,
+    base = dict(seed_id=91, name="pin", layers=1, heads=4, d=16, dtype="f32", n_cand=24,
                 n_query=8, n_window=8, budget=48, clusters=4, blocks=10, group_size=4,
                 sigma2_log2=3, drift=0.05)
     base.update(kw)
