@@ -11,7 +11,7 @@ namespace dkv {
 
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-size_t workspace_layout(int B, int G, int Mcap, int N, Workspace *ws, char *base) {
+size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base) {
   size_t off = 0;
   const size_t Bz = (size_t)B, Mz = (size_t)Mcap, Nz = (size_t)(N > 0 ? N : 1);
   const int nck = (N + kCkStride - 1) / kCkStride;
@@ -33,7 +33,6 @@ size_t workspace_layout(int B, int G, int Mcap, int N, Workspace *ws, char *base
   w.bs = (float *)take(Bz * Mz * 4);
   w.acol = (int64_t *)take(Bz * Nz * 8);
   w.wcol = (int64_t *)take(Bz * Nz * 8);
-  w.skey = (uint64_t *)take(Bz * Nz * 8);
   w.order = (int32_t *)take(Bz * Nz * 4);
   w.rank = (int32_t *)take(Bz * Nz * 4);
   w.first = (int32_t *)take(Bz * Mz * 4);
@@ -47,6 +46,10 @@ size_t workspace_layout(int B, int G, int Mcap, int N, Workspace *ws, char *base
   w.sub = (int64_t *)take(Bz * Mz * 8);
   w.sub_adm = (int64_t *)take(Bz * Nz * 8);
   w.mut_adm = (int64_t *)take(Bz * Nz * 8);
+  w.hole_list = (int32_t *)take(Bz * Mz * 4);
+  w.sk = (uint16_t *)take(Bz * Nz * (size_t)d * 2);
+  w.snorm = (float *)take(Bz * Nz * 4);
+  w.feas = (uint8_t *)take(Bz * (Nz + 1));
   w.nck = nck > 0 ? nck : 1;
   if (ws) *ws = w;
   return off;
@@ -117,7 +120,7 @@ int densitykv_workspace_size(const dkv_bank *bank, int32_t n_cand, size_t *bytes
   if (!bytes) return DKV_ERR_INVALID;
   if (n_cand < 0 || n_cand > DKV_MAX_CANDIDATES) return DKV_ERR_SHAPE;
   *bytes = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity, n_cand,
-                            nullptr, nullptr);
+                            bank->head_dim, nullptr, nullptr);
   return DKV_OK;
 }
 
@@ -131,7 +134,7 @@ int densitykv_score(const dkv_bank *bank, const dkv_segment *seg, const dkv_para
   if (rc) return rc;
   Workspace ws{};
   const size_t need = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity,
-                                       seg->n, &ws, static_cast<char *>(workspace));
+                                       seg->n, bank->head_dim, &ws, static_cast<char *>(workspace));
   if (!workspace || workspace_bytes < need) return DKV_ERR_WORKSPACE;
   const Geom g = geom_of(bank, seg->n);
   hipError_t e = launch_score(*bank, *seg, g, p, cand_score_q, cand_score_f32, bank_density_q, ws,
@@ -148,7 +151,7 @@ int densitykv_update_bank(dkv_bank *bank, const dkv_segment *seg, const dkv_para
   if (rc) return rc;
   Workspace ws{};
   const size_t need = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity,
-                                       seg->n, &ws, static_cast<char *>(workspace));
+                                       seg->n, bank->head_dim, &ws, static_cast<char *>(workspace));
   if (!workspace || workspace_bytes < need) return DKV_ERR_WORKSPACE;
   const Geom g = geom_of(bank, seg->n);
   hipError_t e = launch_update(*bank, *seg, g, p, out, ws, static_cast<hipStream_t>(stream));

@@ -102,100 +102,73 @@ __global__ __launch_bounds__(kAThreads) void k_attn_rowwise(dkv_bank bank, const
 // bf16 path on MFMA (v_mfma_f32_32x32x16_bf16).
 //
 // A workgroup of 4 waves owns 128 queries, 32 per wave.  Per tile of 64 keys:
-//   S^T = K Q^T   A = K tile (LDS, row-major), B = Q^T (registers):
-//                 lane l <-> query l % 32, registers <-> 16 keys per 32-key half,
-//                 so the softmax row statistics stay inside the lane (plus one
-//                 exchange with lane l ^ 32);
-//   O^T += V^T P^T  B = P straight from the S registers (bf16), A = V^T read
-//                 from a transposed LDS copy of the V tile.  Inside each 16-key
-//                 K step the key order is permuted identically in both operands
-//                 (slot 8h + j <-> key 8 (j / 4) + 4 h + j % 4), which is what
-//                 the S register layout provides.
-// Keys and values are staged global -> registers -> LDS with double buffering.
+//   S^T = K Q^T     A = K tile (LDS), B = Q^T (registers): lane l <-> query
+//                   l % 32, registers <-> keys, so the softmax row statistics
+//                   stay inside the lane (plus one exchange with lane l ^ 32);
+//   O^T += V^T P^T  B = P straight from the S registers (bf16); A = V^T read
+//                   from the row-major V tile with the transposing LDS read
+//                   (ds_read_b64_tr_b16).  Inside each 16-key K step the key
+//                   order is permuted identically in both operands
+//                   (slot 8h + j <-> key 8 (j / 4) + 4 h + j % 4).
+// K and V tiles go global -> LDS with 16-byte direct-to-LDS loads (no VGPR
+// staging), double-buffered; rows are stored with an XOR swizzle of their
+// 16-byte chunks so that both the K reads and the transposed V reads are free
+// of LDS bank conflicts.
 // ---------------------------------------------------------------------------
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kFWaves = 4;
 constexpr int kFQ = 32 * kFWaves;  // queries per workgroup
 constexpr int kFK = 64;            // keys per tile
 
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+// Two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const f32x2 v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
 template <int D>
 struct FCfg {
-  static constexpr int kKStride = D + 8;     // bf16 per K row in LDS (odd multiple of 16 B)
-  static constexpr int kVStride = kFK + 8;   // bf16 per transposed V row
-  static constexpr int kKChunks = D / 8;     // 16-byte chunks per key row
-  static constexpr int kKLoads = kFK * kKChunks / (64 * kFWaves);
-  static constexpr int kVGroups = D / 8;     // 8-wide dv groups
-  static constexpr int kVKeys = kFK * kVGroups / (64 * kFWaves);  // keys per thread (4 consecutive)
+  static constexpr int kRowBytes = 2 * D;           // one K or V row
+  static constexpr int kChunks = D / 8;             // 16-byte chunks per row
+  static constexpr int kRowsPerLoad = 1024 / kRowBytes;   // rows per 1 KB direct load
+  static constexpr int kLoadsPerTile = kFK / kRowsPerLoad;  // per tensor, per workgroup
+  static constexpr int kTileBytes = kFK * kRowBytes;
 };
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return (uint32_t)f32_to_bf16_bits(lo) | ((uint32_t)f32_to_bf16_bits(hi) << 16);
-}
-
+// Physical 16-byte chunk of logical chunk c of row r (K: conflict-free 16-byte
+// reads of one chunk across 16 rows; V: conflict-free transposed 8-byte reads
+// of 4 chunks across 4 rows).
 template <int D>
-struct FStage {
-  u32x4 k[FCfg<D>::kKLoads];
-  u32x4 v[FCfg<D>::kVKeys];
-};
-
+__device__ __forceinline__ int k_swz(int r, int c) { return c ^ (r % FCfg<D>::kChunks); }
 template <int D>
-__device__ __forceinline__ const uint16_t *key_row(const uint16_t *bk, const uint16_t *wk, size_t rb, size_t wb,
-                                                   int key, int m) {
-  return key < m ? bk + (rb + key) * D : wk + (wb + (key - m)) * D;
-}
+__device__ __forceinline__ int v_swz(int r, int c) { return c ^ ((4 * (r % 4)) % FCfg<D>::kChunks); }
 
+// Issue the direct-to-LDS loads of one tile (rows [0, nvalid) of kbase/vbase;
+// rows beyond nvalid repeat the last real row so that every value is finite).
 template <int D>
-__device__ __forceinline__ void fstage_load(FStage<D> &st, const uint16_t *bk, const uint16_t *bv,
-                                            const uint16_t *wk, const uint16_t *wv, size_t rb, size_t wb, int t0,
-                                            int m, int total) {
+__device__ __forceinline__ void ftile_issue(const uint16_t *kbase, const uint16_t *vbase, int nvalid,
+                                            char *kbuf, char *vbuf) {
+  constexpr int RPL = FCfg<D>::kRowsPerLoad, CH = FCfg<D>::kChunks;
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int rsub = l / CH, pc = l % CH;
 #pragma unroll
-  for (int q = 0; q < FCfg<D>::kKLoads; ++q) {
-    const int c = threadIdx.x + q * 64 * kFWaves;
-    const int key = t0 + c / FCfg<D>::kKChunks, ch = c % FCfg<D>::kKChunks;
-    u32x4 x = {0, 0, 0, 0};
-    if (key < total) x = *reinterpret_cast<const u32x4 *>(key_row<D>(bk, wk, rb, wb, key, m) + ch * 8);
-    st.k[q] = x;
-  }
-  const int dg = threadIdx.x % FCfg<D>::kVGroups;
-  const int kg = threadIdx.x / FCfg<D>::kVGroups;
-#pragma unroll
-  for (int q = 0; q < FCfg<D>::kVKeys; ++q) {
-    const int key = t0 + kg * FCfg<D>::kVKeys + q;
-    u32x4 x = {0, 0, 0, 0};
-    if (key < total) x = *reinterpret_cast<const u32x4 *>(key_row<D>(bv, wv, rb, wb, key, m) + dg * 8);
-    st.v[q] = x;
-  }
-}
-
-template <int D>
-__device__ __forceinline__ void fstage_store(const FStage<D> &st, uint16_t *ks, uint16_t *vt) {
-#pragma unroll
-  for (int q = 0; q < FCfg<D>::kKLoads; ++q) {
-    const int c = threadIdx.x + q * 64 * kFWaves;
-    const int key = c / FCfg<D>::kKChunks, ch = c % FCfg<D>::kKChunks;
-    *reinterpret_cast<u32x4 *>(ks + key * FCfg<D>::kKStride + ch * 8) = st.k[q];
-  }
-  // transpose kVKeys keys x 8 dv in registers, store 8 rows of kVKeys keys
-  const int dg = threadIdx.x % FCfg<D>::kVGroups;
-  const int kg = threadIdx.x / FCfg<D>::kVGroups;
-  constexpr int NK = FCfg<D>::kVKeys;
-  static_assert(NK == 2 || NK == 4, "transposed V staging assumes 2 or 4 keys per thread");
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int w = j >> 1, sh = (j & 1) * 16;
-    uint16_t *dst = vt + (dg * 8 + j) * FCfg<D>::kVStride + kg * NK;
-    const uint32_t e0 = (st.v[0][w] >> sh) & 0xFFFF, e1 = (st.v[1][w] >> sh) & 0xFFFF;
-    if constexpr (NK == 4) {
-      const uint32_t e2 = (st.v[2][w] >> sh) & 0xFFFF, e3 = (st.v[3][w] >> sh) & 0xFFFF;
-      u32x2 pk = {e0 | (e1 << 16), e2 | (e3 << 16)};
-      *reinterpret_cast<u32x2 *>(dst) = pk;
-    } else {
-      *reinterpret_cast<uint32_t *>(dst) = e0 | (e1 << 16);
-    }
+  for (int q = 0; q < FCfg<D>::kLoadsPerTile / kFWaves; ++q) {
+    const int blk = wave * (FCfg<D>::kLoadsPerTile / kFWaves) + q;
+    const int r = blk * RPL + rsub;
+    const int rr = r < nvalid ? r : nvalid - 1;
+    __builtin_amdgcn_global_load_lds(kbase + (size_t)rr * D + 8 * k_swz<D>(r, pc),
+                                     (lds_void *)(kbuf + blk * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(vbase + (size_t)rr * D + 8 * v_swz<D>(r, pc),
+                                     (lds_void *)(vbuf + blk * 1024), 16, 0, 0);
   }
 }
 
@@ -205,16 +178,16 @@ __global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, co
                                                                uint16_t *out, float c, Geom g) {
   constexpr int KS = D / 16;   // K steps of S
   constexpr int DT = D / 32;   // dv tiles of O
+  constexpr int RB = FCfg<D>::kRowBytes;
   const int b = blockIdx.y;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
   const int M = clampi(bank.budget[b], 0, g.Mcap);
   const int m = clampi(bank.occupancy[b], 0, M);
-  const int total = m + nw;
   const size_t rb = (size_t)b * g.Mcap, wb = (size_t)b * nw;
   const uint16_t *bk = static_cast<const uint16_t *>(bank.k);
   const uint16_t *bv = static_cast<const uint16_t *>(bank.v);
-  __shared__ __attribute__((aligned(16))) uint16_t ks[2][kFK * FCfg<D>::kKStride];
-  __shared__ __attribute__((aligned(16))) uint16_t vt[2][D * FCfg<D>::kVStride];
+  __shared__ __attribute__((aligned(1024))) char kbuf[2][FCfg<D>::kTileBytes];
+  __shared__ __attribute__((aligned(1024))) char vbuf[2][FCfg<D>::kTileBytes];
 
   const int qi = blockIdx.x * kFQ + wave * 32 + n;
   const bool qv = qi < nq;
@@ -231,31 +204,55 @@ __global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, co
   for (int t = 0; t < DT; ++t) o[t] = f32x16{};
   float mrun = -INFINITY, lrun = 0.0f;
 
-  const int nt = (total + kFK - 1) / kFK;
-  FStage<D> st;
+  // Tiles never straddle the bank/window boundary: ceil(m/64) bank tiles, then
+  // ceil(nw/64) window tiles, so every tile has one (scalar) base pointer.
+  const int nt0 = (m + kFK - 1) / kFK;
+  const int nt = nt0 + (nw + kFK - 1) / kFK;
+  auto tile_src = [&](int t, const uint16_t *&kp, const uint16_t *&vp, int &nv) {
+    if (t < nt0) {
+      kp = bk + (rb + (size_t)t * kFK) * D;
+      vp = bv + (rb + (size_t)t * kFK) * D;
+      nv = min(kFK, m - t * kFK);
+    } else {
+      const int tw = t - nt0;
+      kp = wk + (wb + (size_t)tw * kFK) * D;
+      vp = wv + (wb + (size_t)tw * kFK) * D;
+      nv = min(kFK, nw - tw * kFK);
+    }
+  };
+  const uint16_t *kp, *vp;
+  int nv_cur = 0, nv_next = 0;
   if (nt > 0) {
-    fstage_load<D>(st, bk, bv, wk, wv, rb, wb, 0, m, total);
-    fstage_store<D>(st, ks[0], vt[0]);
+    tile_src(0, kp, vp, nv_cur);
+    ftile_issue<D>(kp, vp, nv_cur, kbuf[0], vbuf[0]);
   }
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  // transposed V read: lane group gq = l / 16 (h = gq / 2), member cq = l % 16
+  const int gq = l >> 4, cq = l & 15;
   for (int t = 0; t < nt; ++t) {
     const int cur = t & 1;
-    const int t0 = t * kFK;
-    if (t + 1 < nt) fstage_load<D>(st, bk, bv, wk, wv, rb, wb, t0 + kFK, m, total);
+    if (t + 1 < nt) {
+      tile_src(t + 1, kp, vp, nv_next);
+      ftile_issue<D>(kp, vp, nv_next, kbuf[cur ^ 1], vbuf[cur ^ 1]);
+    }
+    const char *kt = kbuf[cur];
+    const char *vtile = vbuf[cur];
     // S^T for two 32-key halves
     f32x16 sc[2];
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
-      const uint16_t *src = ks[cur] + (32 * sub + n) * FCfg<D>::kKStride + 8 * h;
+      const int key = 32 * sub + n;
       bf16x8 a[KS];
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) a[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(src + 16 * kk));
+      for (int kk = 0; kk < KS; ++kk)
+        a[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(kt + key * RB + 16 * k_swz<D>(key, 2 * kk + h)));
       f32x16 acc = {};
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], qf[kk], acc, 0, 0, 0);
       sc[sub] = acc;
     }
-    const int nvalid = total - t0;
+    const int nvalid = nv_cur;
     if (nvalid < kFK) {
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub)
@@ -269,29 +266,35 @@ __global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, co
 #pragma unroll
     for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, sc[1][i]);
     tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float mnew = fmaxf(mrun, tmax);
-    const float corr = exp2f((mrun - mnew) * c);
-    const float moff = -mnew * c;
-    mrun = mnew;
+    // Lazy rescaling: the reference maximum only moves when a score exceeds it
+    // by more than 2^8 in the exp2 domain, so P stays within [0, 256] and the
+    // accumulated O and l are rescaled rarely (exact: the final division by l
+    // removes the common factor).
+    const bool grow = tmax * c > mrun * c + 8.0f;
+    if (__any(grow)) {
+      const float mnew = grow ? tmax : mrun;
+      const float corr = __builtin_amdgcn_exp2f((mrun - mnew) * c);
+      mrun = mnew;
+      lrun *= corr;
+#pragma unroll
+      for (int t2 = 0; t2 < DT; ++t2)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[t2][i] *= corr;
+    }
+    const float moff = -mrun * c;
     float psum = 0.0f;
     uint32_t pb[2][8];
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
 #pragma unroll
       for (int i = 0; i < 16; i += 2) {
-        const float p0 = exp2f(__builtin_fmaf(sc[sub][i], c, moff));
-        const float p1 = exp2f(__builtin_fmaf(sc[sub][i + 1], c, moff));
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[sub][i], c, moff));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[sub][i + 1], c, moff));
         psum += p0 + p1;
         pb[sub][i >> 1] = pack_bf16x2(p0, p1);
       }
     }
-    lrun = lrun * corr + psum;
-    if (corr != 1.0f) {
-#pragma unroll
-      for (int t2 = 0; t2 < DT; ++t2)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) o[t2][i] *= corr;
-    }
+    lrun += psum;
     // O^T += V^T P^T
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
@@ -299,18 +302,23 @@ __global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, co
       for (int kst = 0; kst < 2; ++kst) {
         u32x4 bp = {pb[sub][4 * kst + 0], pb[sub][4 * kst + 1], pb[sub][4 * kst + 2], pb[sub][4 * kst + 3]};
         const bf16x8 bop = __builtin_bit_cast(bf16x8, bp);
-        const int key0 = 32 * sub + 16 * kst + 4 * h;
+        const int key0 = 32 * sub + 16 * kst + 4 * (gq >> 1) + (cq >> 2);
 #pragma unroll
         for (int t2 = 0; t2 < DT; ++t2) {
-          const uint16_t *vr = vt[cur] + (32 * t2 + n) * FCfg<D>::kVStride + key0;
-          const u32x2 lo = *reinterpret_cast<const u32x2 *>(vr);
-          const u32x2 hi = *reinterpret_cast<const u32x2 *>(vr + 8);
-          const u32x4 av = {lo[0], lo[1], hi[0], hi[1]};
+          const int dvb = 8 * t2 + 4 * (gq & 1) + (cq & 3);  // 8-byte dv block
+          const int ka = key0, kb = key0 + 8;
+          const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4 *)(vtile + ka * RB + 16 * v_swz<D>(ka, dvb >> 1) + 8 * (dvb & 1)));
+          const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (lds_i16x4 *)(vtile + kb * RB + 16 * v_swz<D>(kb, dvb >> 1) + 8 * (dvb & 1)));
+          const u32x2 lo2 = __builtin_bit_cast(u32x2, lo), hi2 = __builtin_bit_cast(u32x2, hi);
+          const u32x4 av = {lo2[0], lo2[1], hi2[0], hi2[1]};
           o[t2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), bop, o[t2], 0, 0, 0);
         }
       }
     }
-    if (t + 1 < nt) fstage_store<D>(st, ks[cur ^ 1], vt[cur ^ 1]);
+    nv_cur = nv_next;
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   }
   const float ltot = lrun + __shfl_xor(lrun, 32, 64);
@@ -319,10 +327,10 @@ __global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, co
 #pragma unroll
   for (int t2 = 0; t2 < DT; ++t2) {
 #pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      const int dv = 32 * t2 + 8 * gq + 4 * h;
-      u32x2 pk = {pack_bf16x2(o[t2][4 * gq] * inv, o[t2][4 * gq + 1] * inv),
-                  pack_bf16x2(o[t2][4 * gq + 2] * inv, o[t2][4 * gq + 3] * inv)};
+    for (int gg = 0; gg < 4; ++gg) {
+      const int dv = 32 * t2 + 8 * gg + 4 * h;
+      u32x2 pk = {pack_bf16x2(o[t2][4 * gg] * inv, o[t2][4 * gg + 1] * inv),
+                  pack_bf16x2(o[t2][4 * gg + 2] * inv, o[t2][4 * gg + 3] * inv)};
       *reinterpret_cast<u32x2 *>(out + qrow * D + dv) = pk;
     }
   }

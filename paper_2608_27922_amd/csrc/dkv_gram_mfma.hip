@@ -3,13 +3,18 @@
 // Every Gram stage evaluates Soft-Riesz weights w(k_i, k_j) (Eq. 2) for a set
 // of "row" items against a stream of "column" items and reduces them per row:
 //
-//   k_score_mfma   rows = candidates, columns = all bank states:
+//   k_score_mfma   rows = candidates, columns = bank states:
 //                  S_x = sum_i RNE(w_ix bs_i), Wcol_x = sum_i W_ix  (Eq. 6)
-//   k_cross_mfma   rows = bank states, columns = candidates in score order:
-//                  running prefix P_i(r) and the first r with a violation
-//                  (Eqs. 8-9), prefix checkpoints every 256 candidates
-//   k_rowsum_mfma  plain row sums for the r* fix-up, the exact maintenance
-//                  (Supp. C) and the from-scratch bank density (Eq. 3)
+//   k_rowsum_mfma  row sums: per-256-candidate chunk sums over the ordered
+//                  candidates (the prefix checkpoints of Eqs. 8-9), the r*
+//                  fix-up, the exact maintenance (Supp. C) and the
+//                  from-scratch bank density (Eq. 3)
+//   k_cross_find   per bank state: the chunk in which its prefix density first
+//                  reaches tau b, then the exact prefix length inside it
+//
+// The column range of every Gram is split over workgroups (grid dimension y);
+// partial integer sums are combined with 64-bit atomic adds, which are exact
+// and order-independent.
 //
 // Layout: a workgroup of 4 waves owns 128 row items; wave w owns 32 of them,
 // held for the whole kernel as the B operand of v_mfma_f32_32x32x16_bf16
@@ -62,10 +67,12 @@ __device__ __forceinline__ void split3(float x, uint16_t &h, uint16_t &m, uint16
 
 constexpr uint16_t kOne = 0x3F80;  // bf16 1.0
 
-template <int P>
+// FOLD: the MFMA already added the 1 of t = 1 + u (exact when sigma^2 <= 2^11,
+// where every partial sum stays below 2^24 units of 2^-12 / sigma^2).
+template <int P, bool FOLD>
 __device__ __forceinline__ uint32_t weight_raw(float u, float scale) {
   // raw bits of fma(w, scale, 2^23): kMagic + RNE(w * scale)
-  const float t = 1.0f + u;
+  const float t = FOLD ? u : 1.0f + u;
   float tp = t;
   if constexpr (P >= 2) tp = t * t;
   if constexpr (P == 4) tp = tp * tp;
@@ -82,8 +89,8 @@ struct RowFrag {
 };
 
 // Load the B operand for row item (lane % 32): keys scaled by -2/sigma^2, then
-// the aug step [1, 1, 1, n_hi, n_mid, n_lo, 0, 0] (half 0) / zeros (half 1).
-template <int D>
+// the aug step [1, 1, 1, n_hi, n_mid, n_lo, fold, 0] (half 0) / zeros (half 1).
+template <int D, bool FOLD>
 __device__ __forceinline__ void load_row_frag(RowFrag<D> &rf, const uint16_t *key, float norm, bool valid,
                                               float neg2_inv_s2, float inv_s2) {
   const int h = (threadIdx.x & 63) >> 5;
@@ -107,7 +114,7 @@ __device__ __forceinline__ void load_row_frag(RowFrag<D> &rf, const uint16_t *ke
     aug[0] = (uint32_t)kOne | ((uint32_t)kOne << 16);
     aug[1] = (uint32_t)kOne | ((uint32_t)nh << 16);
     aug[2] = (uint32_t)nm | ((uint32_t)nl << 16);
-    aug[3] = 0;
+    aug[3] = FOLD ? (uint32_t)kOne : 0u;
   }
   rf.b[TileCfg<D>::kSteps] = __builtin_bit_cast(bf16x8, aug);
 }
@@ -144,7 +151,7 @@ __device__ __forceinline__ void stage_load(ColStage<D> &st, const uint16_t *base
       a[0] = (uint32_t)nh | ((uint32_t)nm << 16);
       a[1] = (uint32_t)nl | ((uint32_t)kOne << 16);
       a[2] = (uint32_t)kOne | ((uint32_t)kOne << 16);
-      a[3] = 0;
+      a[3] = (uint32_t)kOne;  // times the row's fold slot
     }
     st.aug0 = a;
   }
@@ -185,12 +192,12 @@ __device__ __forceinline__ f32x16 tile_u(const uint16_t *lds, const RowFrag<D> &
 __device__ __forceinline__ int col_of_reg(int i, int h) { return 8 * (i >> 2) + 4 * h + (i & 3); }
 
 // Sum over this lane's 16 weights (as integers), columns >= nvalid masked out.
-template <int P, bool MASK>
+template <int P, bool MASK, bool FOLD>
 __device__ __forceinline__ uint32_t lane_wsum(const f32x16 &u, int nvalid, int h) {
   uint32_t s = 0;
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
-    uint32_t raw = weight_raw<P>(u[i], 8388608.0f);
+    uint32_t raw = weight_raw<P, FOLD>(u[i], 8388608.0f);
     if constexpr (MASK) raw = col_of_reg(i, h) < nvalid ? raw : kMagic;
     s += raw;
   }
@@ -198,15 +205,20 @@ __device__ __forceinline__ uint32_t lane_wsum(const f32x16 &u, int nvalid, int h
 }
 
 // ---------------------------------------------------------------------------
-// Score: rows = candidates, columns = bank states [0, m).
+// Score: rows = candidates, columns = bank states [c0, c1) of this split.
 // ---------------------------------------------------------------------------
-template <int D, int P>
+constexpr int kColsPerSplit = 1024;
+
+template <int D, int P, bool FOLD>
 __global__ __launch_bounds__(64 * kWaves) void k_score_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
-                                                           Workspace ws, int64_t *out_q, float *out_f) {
-  const int b = blockIdx.y;
+                                                           Workspace ws) {
+  const int b = blockIdx.z;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
   const int x = blockIdx.x * kRowsPerWG + wave * 32 + n;
   const int m = ws.m[b];
+  const int c0 = blockIdx.y * kColsPerSplit;
+  if (c0 >= m) return;
+  const int ncols = min(kColsPerSplit, m - c0);
   __shared__ __attribute__((aligned(16))) uint16_t tile[2][kCT * TileCfg<D>::kStride];
   __shared__ __attribute__((aligned(16))) float tbs[2][kCT];
   const uint16_t *K = static_cast<const uint16_t *>(seg_k);
@@ -214,30 +226,27 @@ __global__ __launch_bounds__(64 * kWaves) void k_score_mfma(dkv_bank bank, const
   const bool rv = x < g.N;
   const size_t xr = (size_t)b * g.N + (rv ? x : 0);
   RowFrag<D> rf;
-  load_row_frag<D>(rf, K + xr * D, rv ? ws.cnorm[xr] : 0.0f, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
-  const size_t rb = (size_t)b * g.Mcap;
+  load_row_frag<D, FOLD>(rf, K + xr * D, rv ? ws.cnorm[xr] : 0.0f, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
+  const size_t rb = (size_t)b * g.Mcap + c0;
   auto row_of = [&](int i) -> int64_t { return (int64_t)(rb + i); };
   auto norm_of = [&](int i) -> float { return bank.knorm[rb + i]; };
   uint64_t A64 = 0, W64 = 0;
-  const int nt = (m + kCT - 1) / kCT;
+  const int nt = (ncols + kCT - 1) / kCT;
   ColStage<D> st;
   float bs_next = 0.0f;
-  if (nt > 0) {
-    stage_load<D>(st, BK, 0, m, row_of, norm_of, p.inv_sigma2);
-    if (threadIdx.x < kCT) bs_next = (int)threadIdx.x < m ? ws.bs[rb + threadIdx.x] : 0.0f;
-    stage_store<D>(st, tile[0]);
-    if (threadIdx.x < kCT) tbs[0][threadIdx.x] = bs_next;
-  }
+  stage_load<D>(st, BK, 0, ncols, row_of, norm_of, p.inv_sigma2);
+  if (threadIdx.x < kCT) bs_next = (int)threadIdx.x < ncols ? ws.bs[rb + threadIdx.x] : 0.0f;
+  stage_store<D>(st, tile[0]);
+  if (threadIdx.x < kCT) tbs[0][threadIdx.x] = bs_next;
   __syncthreads();
   for (int t = 0; t < nt; ++t) {
     const int cur = t & 1;
     const int j0n = (t + 1) * kCT;
     if (t + 1 < nt) {
-      stage_load<D>(st, BK, j0n, m, row_of, norm_of, p.inv_sigma2);
-      if (threadIdx.x < kCT) bs_next = j0n + (int)threadIdx.x < m ? ws.bs[rb + j0n + threadIdx.x] : 0.0f;
+      stage_load<D>(st, BK, j0n, ncols, row_of, norm_of, p.inv_sigma2);
+      if (threadIdx.x < kCT) bs_next = j0n + (int)threadIdx.x < ncols ? ws.bs[rb + j0n + threadIdx.x] : 0.0f;
     }
     const f32x16 u = tile_u<D>(tile[cur], rf);
-    // per-column score scales for this lane's 16 columns
     float bsv[16];
 #pragma unroll
     for (int gq = 0; gq < 4; ++gq) {
@@ -247,12 +256,12 @@ __global__ __launch_bounds__(64 * kWaves) void k_score_mfma(dkv_bank bank, const
       bsv[4 * gq + 2] = v.z;
       bsv[4 * gq + 3] = v.w;
     }
-    const int nvalid = m - t * kCT;
+    const int nvalid = ncols - t * kCT;
     uint32_t sw = 0, sa = 0;
     if (nvalid >= kCT) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float tt = 1.0f + u[i];
+        const float tt = FOLD ? u[i] : 1.0f + u[i];
         float tp = tt;
         if constexpr (P >= 2) tp = tt * tt;
         if constexpr (P == 4) tp = tp * tp;
@@ -265,7 +274,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_score_mfma(dkv_bank bank, const
     } else {
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        const float tt = 1.0f + u[i];
+        const float tt = FOLD ? u[i] : 1.0f + u[i];
         float tp = tt;
         if constexpr (P >= 2) tp = tt * tt;
         if constexpr (P == 4) tp = tp * tp;
@@ -289,175 +298,85 @@ __global__ __launch_bounds__(64 * kWaves) void k_score_mfma(dkv_bank bank, const
   const uint64_t At = A64 + __shfl_xor(A64, 32, 64);
   if (!rv || h != 0) return;
   const size_t o = (size_t)b * g.N + x;
-  if (ws.acol) {
-    ws.acol[o] = (int64_t)At;
-    ws.wcol[o] = (int64_t)Wt;
-    ws.skey[o] = (At << 13) | (uint64_t)x;
-  }
-  if (out_q) out_q[o] = (int64_t)At;
-  if (out_f) out_f[o] = m > 0 ? (float)(ldexp((double)At, ws.E[b] - 23) / (double)m) : 0.0f;
-}
-
-// ---------------------------------------------------------------------------
-// Crossing: rows = bank states, columns = candidates order[0..R).
-// ---------------------------------------------------------------------------
-template <int D, int P>
-__global__ __launch_bounds__(64 * kWaves) void k_cross_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
-                                                           Workspace ws, int32_t *out_first) {
-  const int b = blockIdx.y;
-  const int m = ws.m[b], R = ws.R[b];
-  if ((int)blockIdx.x * kRowsPerWG >= m) return;
-  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
-  const int i = blockIdx.x * kRowsPerWG + wave * 32 + n;
-  __shared__ __attribute__((aligned(16))) uint16_t tile[2][kCT * TileCfg<D>::kStride];
-  const uint16_t *K = static_cast<const uint16_t *>(seg_k);
-  const uint16_t *BK = static_cast<const uint16_t *>(bank.k);
-  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
-  const bool rv = i < m;
-  const size_t row = rb + (rv ? i : 0);
-  RowFrag<D> rf;
-  load_row_frag<D>(rf, BK + row * D, rv ? bank.knorm[row] : 0.0f, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
-  int64_t thr = 0;
-  if (rv) {
-    const int64_t lim = ((int64_t)p.tau_num * bank.base[row] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
-    thr = lim - bank.rho[row];
-  }
-  int first = thr <= 0 ? 0 : R + 1;
-  int64_t P64 = 0;
-  uint32_t ck = 0;
-  auto row_of = [&](int j) -> int64_t { return (int64_t)(nb + ws.order[nb + j]); };
-  auto norm_of = [&](int j) -> float { return ws.cnorm[nb + ws.order[nb + j]]; };
-  const int nt = (R + kCT - 1) / kCT;
-  ColStage<D> st;
-  if (nt > 0) {
-    stage_load<D>(st, K, 0, R, row_of, norm_of, p.inv_sigma2);
-    stage_store<D>(st, tile[0]);
-  }
-  __syncthreads();
-  for (int t = 0; t < nt; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < nt) stage_load<D>(st, K, (t + 1) * kCT, R, row_of, norm_of, p.inv_sigma2);
-    const f32x16 u = tile_u<D>(tile[cur], rf);
-    const int nvalid = R - t * kCT;
-    uint32_t wv[16];
-    uint32_t s = 0;
-#pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      uint32_t raw = weight_raw<P>(u[q], 8388608.0f);
-      if (nvalid < kCT) raw = col_of_reg(q, h) < nvalid ? raw : kMagic;
-      wv[q] = raw - kMagic;
-      s += raw;
-    }
-    s -= 16u * kMagic;
-    const uint32_t tsum = s + __shfl_xor(s, 32, 64);
-    const int64_t Pn = P64 + tsum;
-    const bool cross_here = rv && first > R && Pn >= thr;
-    if (__any(cross_here)) {
-      // exact position inside the tile: prefix in column order
-      uint32_t other[16];
-#pragma unroll
-      for (int q = 0; q < 16; ++q) other[q] = __shfl_xor(wv[q], 32, 64);
-      int64_t run = P64;
-      int f = -1;
-#pragma unroll
-      for (int mm = 0; mm < 32; ++mm) {
-        const int gq = mm >> 2, q = 4 * (gq >> 1) + (mm & 3);
-        const bool from_h1 = (gq & 1) != 0;
-        const uint32_t w = (from_h1 == (h == 1)) ? wv[q] : other[q];
-        run += w;
-        if (f < 0 && run >= thr) f = mm;
-      }
-      if (cross_here) first = t * kCT + f + 1;
-    }
-    P64 = Pn;
-    ck += tsum;
-    if (((t + 1) % (kCkStride / kCT)) == 0) {
-      if (rv && h == 0) ws.ck[row * ws.nck + ((t + 1) / (kCkStride / kCT) - 1)] = ck;
-      ck = 0;
-    }
-    if (t + 1 < nt) stage_store<D>(st, tile[cur ^ 1]);
-    __syncthreads();
-  }
-  if (!rv || h != 0) return;
-  ws.first[row] = first;
-  if (out_first) out_first[row] = first;
+  atomicAdd(reinterpret_cast<unsigned long long *>(&ws.acol[o]), (unsigned long long)At);
+  atomicAdd(reinterpret_cast<unsigned long long *>(&ws.wcol[o]), (unsigned long long)Wt);
 }
 
 // ---------------------------------------------------------------------------
 // Row sums.  MODE selects rows, columns and where the sum goes.
 // ---------------------------------------------------------------------------
-enum RowSumMode { RS_FIXUP = 0, RS_SURV_EV = 1, RS_ADM_BASE = 2, RS_ADM_MUT = 3, RS_DENSITY = 4 };
+enum RowSumMode { RS_CHUNK = 0, RS_FIXUP = 1, RS_SURV_EV = 2, RS_ADM_BASE = 3, RS_ADM_MUT = 4, RS_DENSITY = 5 };
 
-struct RSSetup {
-  int nrows;
-  int c0, c1;          // column range [c0, c1)
-  const uint16_t *rk;  // row keys base (element offset via rrow)
-  const uint16_t *ck;  // column keys base
-  bool diag;           // exclude column == row (same list, same index)
-};
+constexpr int kChunksPerSplit = 4;   // RS_CHUNK: 4 x 256 ordered candidates per workgroup
 
-template <int D, int P, int MODE>
+template <int D, int P, int MODE, bool FOLD>
 __global__ __launch_bounds__(64 * kWaves) void k_rowsum_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
                                                             Workspace ws, int64_t *out) {
-  const int b = blockIdx.y;
+  const int b = blockIdx.z;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
   const int m = ws.m[b];
   const uint16_t *SK = static_cast<const uint16_t *>(seg_k);
   const uint16_t *BK = static_cast<const uint16_t *>(bank.k);
-  const int n_ev = (MODE == RS_DENSITY || MODE == RS_FIXUP) ? 0 : ws.n_ev[b];
-  const int rs = (MODE == RS_DENSITY) ? 0 : ws.r_star[b / g.gs];
+  const uint16_t *SORTK = ws.sk;
+  constexpr bool kNeedEv = MODE == RS_SURV_EV || MODE == RS_ADM_BASE || MODE == RS_ADM_MUT;
+  const int n_ev = kNeedEv ? ws.n_ev[b] : 0;
+  const int rs = (MODE == RS_FIXUP || kNeedEv) ? ws.r_star[b / g.gs] : 0;
   const int n_surv = m - n_ev;
+  const bool adm_by_ev = n_ev <= n_surv;
   // rows
   int nrows;
-  if constexpr (MODE == RS_FIXUP || MODE == RS_DENSITY) nrows = m;
+  if constexpr (MODE == RS_CHUNK || MODE == RS_FIXUP || MODE == RS_DENSITY) nrows = m;
   else if constexpr (MODE == RS_SURV_EV) nrows = n_surv;
   else nrows = rs;
   if ((int)blockIdx.x * kRowsPerWG >= nrows) return;
-  // columns: [c0, c1) of a list
+  // columns of this workgroup: [c0, c1) of the mode's column list
   int c0 = 0, c1 = 0;
-  bool adm_by_ev = n_ev <= n_surv;
-  if constexpr (MODE == RS_FIXUP) {
+  if constexpr (MODE == RS_CHUNK) {
+    const int R = ws.R[b];
+    c0 = blockIdx.y * kChunksPerSplit * kCkStride;
+    c1 = min(R, c0 + kChunksPerSplit * kCkStride);
+  } else if constexpr (MODE == RS_FIXUP) {
     c0 = (rs / kCkStride) * kCkStride;
     c1 = rs;
-  } else if constexpr (MODE == RS_SURV_EV) {
-    c1 = n_ev;
-  } else if constexpr (MODE == RS_ADM_BASE) {
-    c1 = adm_by_ev ? n_ev : n_surv;
-  } else if constexpr (MODE == RS_ADM_MUT) {
-    c1 = rs;
   } else {
-    c1 = m;
+    int total;
+    if constexpr (MODE == RS_SURV_EV) total = n_ev;
+    else if constexpr (MODE == RS_ADM_BASE) total = adm_by_ev ? n_ev : n_surv;
+    else if constexpr (MODE == RS_ADM_MUT) total = rs;
+    else total = m;
+    c0 = blockIdx.y * kColsPerSplit;
+    c1 = min(total, c0 + kColsPerSplit);
   }
+  if (MODE != RS_FIXUP && c0 >= c1) return;  // the fix-up always writes rho~, even for r* % 256 == 0
   const int v = blockIdx.x * kRowsPerWG + wave * 32 + n;
   const bool rv = v < nrows;
-  const int vv = rv ? v : 0;
-  // row item location
+  // row item
   const uint16_t *rkey = BK + rb * D;
   float rnorm = 0.0f;
   size_t out_idx = 0;
   if (rv) {
-    if constexpr (MODE == RS_FIXUP || MODE == RS_DENSITY) {
-      rkey = BK + (rb + vv) * D;
-      rnorm = bank.knorm[rb + vv];
-      out_idx = rb + vv;
+    if constexpr (MODE == RS_CHUNK || MODE == RS_FIXUP || MODE == RS_DENSITY) {
+      rkey = BK + (rb + v) * D;
+      rnorm = bank.knorm[rb + v];
+      out_idx = rb + v;
     } else if constexpr (MODE == RS_SURV_EV) {
-      const int s = ws.surv_list[rb + vv];
+      const int s = ws.surv_list[rb + v];
       rkey = BK + (rb + s) * D;
       rnorm = bank.knorm[rb + s];
       out_idx = rb + s;
     } else {
-      const int x = ws.adm_list[nb + vv];
+      const int x = ws.adm_list[nb + v];
       rkey = SK + (nb + x) * D;
       rnorm = ws.cnorm[nb + x];
-      out_idx = nb + vv;
+      out_idx = nb + v;
     }
   }
   RowFrag<D> rf;
-  load_row_frag<D>(rf, rkey, rnorm, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
-  // column item location
+  load_row_frag<D, FOLD>(rf, rkey, rnorm, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
+  // column items (absolute index j in the mode's list)
   auto row_of = [&](int j) -> int64_t {
-    if constexpr (MODE == RS_FIXUP) return (int64_t)(nb + ws.order[nb + j]);
+    if constexpr (MODE == RS_CHUNK || MODE == RS_FIXUP) return (int64_t)(nb + j);
     else if constexpr (MODE == RS_SURV_EV) return (int64_t)(rb + ws.ev_list[rb + j]);
     else if constexpr (MODE == RS_ADM_BASE)
       return (int64_t)(rb + (adm_by_ev ? ws.ev_list[rb + j] : ws.surv_list[rb + j]));
@@ -465,17 +384,18 @@ __global__ __launch_bounds__(64 * kWaves) void k_rowsum_mfma(dkv_bank bank, cons
     else return (int64_t)(rb + j);
   };
   auto norm_of = [&](int j) -> float {
-    if constexpr (MODE == RS_FIXUP) return ws.cnorm[nb + ws.order[nb + j]];
+    if constexpr (MODE == RS_CHUNK || MODE == RS_FIXUP) return ws.snorm[nb + j];
     else if constexpr (MODE == RS_SURV_EV) return bank.knorm[rb + ws.ev_list[rb + j]];
     else if constexpr (MODE == RS_ADM_BASE)
       return bank.knorm[rb + (adm_by_ev ? ws.ev_list[rb + j] : ws.surv_list[rb + j])];
     else if constexpr (MODE == RS_ADM_MUT) return ws.cnorm[nb + ws.adm_list[nb + j]];
     else return bank.knorm[rb + j];
   };
-  const uint16_t *colbase = (MODE == RS_FIXUP || MODE == RS_ADM_MUT) ? SK : BK;
+  const uint16_t *colbase = (MODE == RS_CHUNK || MODE == RS_FIXUP) ? SORTK : (MODE == RS_ADM_MUT ? SK : BK);
   constexpr bool kDiag = (MODE == RS_ADM_MUT || MODE == RS_DENSITY);
   __shared__ __attribute__((aligned(16))) uint16_t tile[2][kCT * TileCfg<D>::kStride];
   uint64_t S64 = 0;
+  uint32_t chunk_sum = 0;
   const int ncols = c1 - c0;
   const int nt = (ncols + kCT - 1) / kCT;
   ColStage<D> st;
@@ -496,23 +416,34 @@ __global__ __launch_bounds__(64 * kWaves) void k_rowsum_mfma(dkv_bank bank, cons
     const bool diag_tile = kDiag && (j0 < wg_row0 + kRowsPerWG) && (j0 + kCT > wg_row0);
     uint32_t s;
     if (nvalid >= kCT && !diag_tile) {
-      s = lane_wsum<P, false>(u, kCT, h);
+      s = lane_wsum<P, false, FOLD>(u, kCT, h);
     } else {
       s = 0;
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int mm = col_of_reg(q, h);
-        uint32_t raw = weight_raw<P>(u[q], 8388608.0f);
+        uint32_t raw = weight_raw<P, FOLD>(u[q], 8388608.0f);
         bool ok = mm < nvalid;
         if (kDiag) ok = ok && (j0 + mm != v);
         s += ok ? raw : kMagic;
       }
       s -= 16u * kMagic;
     }
-    S64 += s;
+    if constexpr (MODE == RS_CHUNK) {
+      chunk_sum += s;
+      const bool chunk_end = ((t + 1) % (kCkStride / kCT)) == 0 || t + 1 == nt;
+      if (chunk_end) {
+        const uint32_t tot = chunk_sum + __shfl_xor(chunk_sum, 32, 64);
+        if (rv && h == 0) ws.ck[(rb + v) * ws.nck + (j0 / kCkStride)] = tot;
+        chunk_sum = 0;
+      }
+    } else {
+      S64 += s;
+    }
     if (t + 1 < nt) stage_store<D>(st, tile[cur ^ 1]);
     __syncthreads();
   }
+  if constexpr (MODE == RS_CHUNK) return;
   const uint64_t tot = S64 + __shfl_xor(S64, 32, 64);
   if (!rv || h != 0) return;
   if constexpr (MODE == RS_FIXUP) {
@@ -523,38 +454,163 @@ __global__ __launch_bounds__(64 * kWaves) void k_rowsum_mfma(dkv_bank bank, cons
     const int64_t rt = bank.rho[row] + Pc;
     ws.rho_t[row] = rt;
     if (out) out[row] = rt;
-  } else if constexpr (MODE == RS_SURV_EV) {
-    ws.sub[out_idx] = (int64_t)tot;
-  } else if constexpr (MODE == RS_ADM_BASE) {
-    ws.sub_adm[out_idx] = (int64_t)tot;
-  } else if constexpr (MODE == RS_ADM_MUT) {
-    ws.mut_adm[out_idx] = (int64_t)tot;
   } else {
-    out[out_idx] = (int64_t)tot;
+    int64_t *dst = (MODE == RS_SURV_EV || MODE == RS_DENSITY) ? ws.sub : (MODE == RS_ADM_BASE ? ws.sub_adm : ws.mut_adm);
+    atomicAdd(reinterpret_cast<unsigned long long *>(&dst[out_idx]), (unsigned long long)tot);
   }
 }
 
-inline dim3 grid_rows(int n, int B) { return dim3((unsigned)((n + kRowsPerWG - 1) / kRowsPerWG), (unsigned)B); }
-
+// ---------------------------------------------------------------------------
+// First violating prefix length of every bank state.  One wave per state:
+// scan the chunk sums, then re-walk the one chunk where the threshold is
+// reached, 4 ordered candidates per lane, with the same binary32 weights.
+// ---------------------------------------------------------------------------
 template <int D, int P>
+__global__ __launch_bounds__(256) void k_cross_find(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
+  const int b = blockIdx.y;
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + wave;
+  const int m = ws.m[b], R = ws.R[b];
+  if (i >= m) return;
+  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
+  const size_t row = rb + i;
+  const int64_t lim = ((int64_t)p.tau_num * bank.base[row] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
+  const int64_t thr = lim - bank.rho[row];
+  int first = R + 1;
+  if (thr <= 0) {
+    first = 0;
+  } else if (R > 0) {
+    const int nch = (R + kCkStride - 1) / kCkStride;
+    const uint64_t cv = l < nch ? ws.ck[row * ws.nck + l] : 0;
+    uint64_t inc = cv;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint64_t y = __shfl_up(inc, o, 64);
+      if (l >= o) inc += y;
+    }
+    const unsigned long long hit = __ballot((int64_t)inc >= thr && l < nch);
+    if (hit != 0) {
+      const int c = __ffsll(hit) - 1;
+      const int64_t before = (int64_t)__shfl(inc - cv, c, 64);
+      // re-walk chunk c: columns [256 c, min(256 c + 256, R)), lane l owns 4 of them
+      const uint16_t *rk = static_cast<const uint16_t *>(bank.k) + row * D;
+      const float nr = bank.knorm[row];
+      const int col0 = c * kCkStride + 4 * l;
+      uint32_t w4[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int col = col0 + q;
+        uint32_t W = 0;
+        if (col < R) {
+          const uint16_t *ckey = ws.sk + (nb + col) * D;
+          float acc = 0.0f;
+#pragma unroll
+          for (int j = 0; j < D; j += 8) {
+            const u32x4 a = *reinterpret_cast<const u32x4 *>(rk + j);
+            const u32x4 bb = *reinterpret_cast<const u32x4 *>(ckey + j);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              acc = __builtin_fmaf(__uint_as_float(a[e] << 16), __uint_as_float(bb[e] << 16), acc);
+              acc = __builtin_fmaf(__uint_as_float(a[e] & 0xFFFF0000u), __uint_as_float(bb[e] & 0xFFFF0000u), acc);
+            }
+          }
+          const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
+          W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
+        }
+        w4[q] = W;
+      }
+      uint32_t loc[4];
+      loc[0] = w4[0];
+      loc[1] = loc[0] + w4[1];
+      loc[2] = loc[1] + w4[2];
+      loc[3] = loc[2] + w4[3];
+      uint32_t incl = loc[3];
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(incl, o, 64);
+        if (l >= o) incl += y;
+      }
+      const int64_t base_l = before + (int64_t)(incl - loc[3]);
+      int qf = -1;
+#pragma unroll
+      for (int q = 3; q >= 0; --q)
+        if (base_l + (int64_t)loc[q] >= thr) qf = q;
+      const unsigned long long hl = __ballot(qf >= 0);
+      if (hl != 0) {
+        const int lf = __ffsll(hl) - 1;
+        const int qsel = __shfl(qf, lf, 64);
+        first = c * kCkStride + 4 * lf + qsel + 1;
+      } else {
+        first = min(R, (c + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
+      }
+    }
+  }
+  if (l == 0) {
+    ws.first[row] = first;
+    if (out_first) out_first[row] = first;
+  }
+}
+
+// Candidate keys and norms in score order (contiguous rows for the ordered passes).
+template <int D>
+__global__ __launch_bounds__(256) void k_gather_sorted(const void *seg_k, Geom g, Workspace ws) {
+  const int b = blockIdx.y;
+  const int j = blockIdx.x * 4 + (threadIdx.x >> 6), l = threadIdx.x & 63;
+  if (j >= g.N) return;
+  const size_t nb = (size_t)b * g.N;
+  const int x = ws.order[nb + j];
+  const uint32_t *src = reinterpret_cast<const uint32_t *>(static_cast<const uint16_t *>(seg_k) + (nb + x) * D);
+  uint32_t *dst = reinterpret_cast<uint32_t *>(ws.sk + (nb + j) * D);
+  for (int e = l; e < D / 2; e += 64) dst[e] = src[e];
+  if (l == 0) ws.snorm[nb + j] = ws.cnorm[nb + x];
+}
+
+// Score entry point outputs from the accumulated sums.
+__global__ void k_score_out(Geom g, Workspace ws, int64_t *out_q, float *out_f) {
+  const int b = blockIdx.y, x = blockIdx.x * blockDim.x + threadIdx.x;
+  if (x >= g.N) return;
+  const size_t o = (size_t)b * g.N + x;
+  const int m = ws.m[b];
+  const int64_t A = ws.acol[o];
+  if (out_q) out_q[o] = A;
+  if (out_f) out_f[o] = m > 0 ? (float)(ldexp((double)A, ws.E[b] - 23) / (double)m) : 0.0f;
+}
+
+__global__ void k_density_out(Geom g, Workspace ws, int64_t *out) {
+  const int b = blockIdx.y, i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= ws.m[b]) return;
+  out[(size_t)b * g.Mcap + i] = ws.sub[(size_t)b * g.Mcap + i];
+}
+
+inline unsigned cdiv(int a, int b) { return (unsigned)((a + b - 1) / b); }
+
+template <int D, int P, bool F>
 void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                       const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage) {
   const int T = 64 * kWaves;
+  const unsigned rowsM = cdiv(g.Mcap, kRowsPerWG), rowsN = cdiv(g.N > 0 ? g.N : 1, kRowsPerWG);
   switch (stage) {
-    case 0:
-      k_score_mfma<D, P><<<grid_rows(g.N, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, out.score_q, nullptr);
+    case 0:  // score + sorted copy is launched after the sort (stage 4)
+      k_score_mfma<D, P, F><<<dim3(rowsN, cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws);
       break;
-    case 1:
-      k_cross_mfma<D, P><<<grid_rows(g.Mcap, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, out.first_cross);
+    case 4:
+      k_gather_sorted<D><<<dim3(cdiv(g.N, 4), g.B), 256, 0, s>>>(seg.k, g, ws);
       break;
+    case 1: {
+      if (g.N > 0)
+        k_rowsum_mfma<D, P, RS_CHUNK, F><<<dim3(rowsM, cdiv(g.N, kChunksPerSplit * kCkStride), g.B), T, 0, s>>>(
+            bank, seg.k, g, p, ws, nullptr);
+      k_cross_find<D, P><<<dim3(cdiv(g.Mcap, 4), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
+      break;
+    }
     case 2:
-      k_rowsum_mfma<D, P, RS_FIXUP><<<grid_rows(g.Mcap, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, out.rho_tilde);
+      k_rowsum_mfma<D, P, RS_FIXUP, F><<<dim3(rowsM, 1, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, out.rho_tilde);
       break;
     case 3:
-      k_rowsum_mfma<D, P, RS_SURV_EV><<<grid_rows(g.Mcap, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
+      k_rowsum_mfma<D, P, RS_SURV_EV, F><<<dim3(rowsM, cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
       if (g.N > 0) {
-        k_rowsum_mfma<D, P, RS_ADM_BASE><<<grid_rows(g.N, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
-        k_rowsum_mfma<D, P, RS_ADM_MUT><<<grid_rows(g.N, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
+        k_rowsum_mfma<D, P, RS_ADM_BASE, F><<<dim3(rowsN, cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
+        k_rowsum_mfma<D, P, RS_ADM_MUT, F><<<dim3(rowsN, cdiv(g.N, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
       }
       break;
     default:
@@ -562,28 +618,37 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
   }
 }
 
+// The +1 of t = 1 + u rides in the MFMA when sigma^2 <= 2^11 (exact there).
+inline bool fold_one(const Prm &p) { return p.inv_sigma2 >= 1.0f / 2048.0f; }
+
 template <int D>
 void mfma_stage_d(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                   const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage) {
-  if (p.p == 1) mfma_update_impl<D, 1>(bank, seg, g, p, out, ws, s, stage);
-  else if (p.p == 2) mfma_update_impl<D, 2>(bank, seg, g, p, out, ws, s, stage);
-  else mfma_update_impl<D, 4>(bank, seg, g, p, out, ws, s, stage);
+  const bool f = fold_one(p);
+  if (p.p == 1) f ? mfma_update_impl<D, 1, true>(bank, seg, g, p, out, ws, s, stage) : mfma_update_impl<D, 1, false>(bank, seg, g, p, out, ws, s, stage);
+  else if (p.p == 2) f ? mfma_update_impl<D, 2, true>(bank, seg, g, p, out, ws, s, stage) : mfma_update_impl<D, 2, false>(bank, seg, g, p, out, ws, s, stage);
+  else f ? mfma_update_impl<D, 4, true>(bank, seg, g, p, out, ws, s, stage) : mfma_update_impl<D, 4, false>(bank, seg, g, p, out, ws, s, stage);
 }
 
-template <int D, int P>
+template <int D, int P, bool F>
 void mfma_score_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                      int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws, hipStream_t s) {
   const int T = 64 * kWaves;
-  if (g.N > 0 && (score_q || score_f))
-    k_score_mfma<D, P><<<grid_rows(g.N, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, score_q, score_f);
-  if (density)
-    k_rowsum_mfma<D, P, RS_DENSITY><<<grid_rows(g.Mcap, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, density);
+  if (g.N > 0 && (score_q || score_f)) {
+    k_score_mfma<D, P, F><<<dim3(cdiv(g.N, kRowsPerWG), cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws);
+    k_score_out<<<dim3(cdiv(g.N, 256), g.B), 256, 0, s>>>(g, ws, score_q, score_f);
+  }
+  if (density) {
+    k_rowsum_mfma<D, P, RS_DENSITY, F><<<dim3(cdiv(g.Mcap, kRowsPerWG), cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(
+        bank, seg.k, g, p, ws, density);
+    k_density_out<<<dim3(cdiv(g.Mcap, 256), g.B), 256, 0, s>>>(g, ws, density);
+  }
 }
 
 }  // namespace
 
 // Stage launchers used by the update sequence for bf16 banks:
-// 0 score, 1 crossing, 2 r* fix-up, 3 maintenance.
+// 0 score, 4 ordered copy, 1 crossing, 2 r* fix-up, 3 maintenance.
 void launch_gram_mfma(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                       const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage) {
   if (g.d == 128) mfma_stage_d<128>(bank, seg, g, p, out, ws, s, stage);
@@ -594,7 +659,8 @@ void launch_score_mfma(const dkv_bank &bank, const dkv_segment &seg, const Geom 
                        int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws, hipStream_t s) {
   auto go = [&](auto dtag, auto ptag) {
     constexpr int D = decltype(dtag)::value, P = decltype(ptag)::value;
-    mfma_score_impl<D, P>(bank, seg, g, p, score_q, score_f, density, ws, s);
+    if (fold_one(p)) mfma_score_impl<D, P, true>(bank, seg, g, p, score_q, score_f, density, ws, s);
+    else mfma_score_impl<D, P, false>(bank, seg, g, p, score_q, score_f, density, ws, s);
   };
   using I64 = std::integral_constant<int, 64>;
   using I128 = std::integral_constant<int, 128>;

@@ -30,7 +30,6 @@ struct Workspace {
   float *bs;           // [B, Mcap] score scale of each bank state
   int64_t *acol;       // [B, N]   S_x
   int64_t *wcol;       // [B, N]   sum_i W_ix over the whole pre-update bank
-  uint64_t *skey;      // [B, N]   sort keys (S_x << 13) | x
   int32_t *order;      // [B, N]   pi
   int32_t *rank;       // [B, N]   position of x in pi
   int32_t *first;      // [B, Mcap] first crossing prefix length
@@ -45,10 +44,14 @@ struct Workspace {
   int64_t *sub_adm;    // [B, N]   admitted: sum of weights to the evicted states if
                        //          n_ev <= n_surv, else to the survivors
   int64_t *mut_adm;    // [B, N]   admitted: sum of weights to the other admitted
+  int32_t *hole_list;  // [B, Mcap] holes closed by moving states (states violating before the update)
+  uint16_t *sk;        // [B, N, d] bf16 candidate keys in score order
+  float *snorm;        // [B, N]   their norms
+  uint8_t *feas;       // [B, N + 1] prefix length r feasible for this bank
   int nck;
 };
 
-size_t workspace_layout(int B, int G, int Mcap, int N, Workspace *ws, char *base);
+size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base);
 
 // Geometry and parameters passed by value to every kernel.
 struct Geom {

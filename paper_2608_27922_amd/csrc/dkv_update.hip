@@ -10,7 +10,8 @@
 //   k_sort          stable ascending order of S_x, ties by source index (Alg. 1)
 //   k_cross_gram    prefix sums over the ordered candidates, first violating
 //                   prefix of every bank state (Eqs. 8-9), tile checkpoints
-//   k_feasible      c_r for every r, e_r (Eq. 10), r* of each group (Eq. 11)
+//   k_feas_bank     c_r for every r and the flags c_r <= e_r (Eqs. 9-10)
+//   k_feas_group    r* of each group (Eq. 11)
 //   k_fixup         projected density rho~(r*) of every bank state
 //   k_select        mandatory + densest eviction (Sec. 3.4 step 3), commit plan
 //   k_maint_gram    weights to the evicted and to the co-admitted states (Supp. C)
@@ -126,6 +127,15 @@ __global__ __launch_bounds__(kThreads) void k_prep(dkv_bank bank, Geom g, Worksp
     float inv = (float)(8388608.0 / (double)bi);
     ws.bs[(size_t)b * g.Mcap + i] = ldexpf(inv, 23 - E);
   }
+  // accumulators filled with atomic adds by the Gram stages
+  for (int x = threadIdx.x; x < g.N; x += kThreads) {
+    const size_t o = (size_t)b * g.N + x;
+    ws.acol[o] = 0;
+    ws.wcol[o] = 0;
+    ws.sub_adm[o] = 0;
+    ws.mut_adm[o] = 0;
+  }
+  for (int i = threadIdx.x; i < g.Mcap; i += kThreads) ws.sub[(size_t)b * g.Mcap + i] = 0;
   if (threadIdx.x == 0) {
     ws.m[b] = m;
     ws.M[b] = Mb;
@@ -194,11 +204,8 @@ __global__ __launch_bounds__(kThreads) void k_score_gram(dkv_bank bank, const vo
   }
   if (!act) return;
   const size_t o = (size_t)b * g.N + x;
-  if (ws.acol) {
-    ws.acol[o] = (int64_t)A;
-    ws.wcol[o] = (int64_t)Wsum;
-    ws.skey[o] = (A << 13) | (uint64_t)x;
-  }
+  ws.acol[o] = (int64_t)A;
+  ws.wcol[o] = (int64_t)Wsum;
   if (out_q) out_q[o] = (int64_t)A;
   if (out_f) out_f[o] = m > 0 ? (float)(ldexp((double)A, ws.E[b] - 23) / (double)m) : 0.0f;
 }
@@ -206,13 +213,20 @@ __global__ __launch_bounds__(kThreads) void k_score_gram(dkv_bank bank, const vo
 // ---------------------------------------------------------------------------
 // k_sort: bitonic sort of the unique keys of one bank in LDS.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBig) void k_sort(Geom g, Workspace ws, int32_t *out_order) {
+__global__ __launch_bounds__(kBig) void k_sort(Geom g, Workspace ws, int32_t *out_order, int64_t *out_score) {
   const int b = blockIdx.x;
   __shared__ uint64_t s[kSortMax];
   int P = 2;
   while (P < g.N) P <<= 1;
-  for (int i = threadIdx.x; i < P; i += kBig)
-    s[i] = i < g.N ? ws.skey[(size_t)b * g.N + i] : ~0ull;
+  for (int i = threadIdx.x; i < P; i += kBig) {
+    uint64_t key = ~0ull;
+    if (i < g.N) {
+      const int64_t A = ws.acol[(size_t)b * g.N + i];
+      key = ((uint64_t)A << 13) | (uint64_t)i;  // ascending score, ties by source index
+      if (out_score) out_score[(size_t)b * g.N + i] = A;
+    }
+    s[i] = key;
+  }
   __syncthreads();
   for (int k = 2; k <= P; k <<= 1) {
     for (int j = k >> 1; j > 0; j >>= 1) {
@@ -319,34 +333,38 @@ __device__ void block_inclusive_scan_lds(int *a, int n, int *tmp) {
   __syncthreads();
 }
 
-__global__ __launch_bounds__(kBig) void k_feasible(Geom g, Workspace ws, int32_t *out_rstar) {
-  const int grp = blockIdx.x;
+// Per bank: c_r = #{i : first_i <= r} by histogram + scan, and the flag
+// c_r <= e_r = max(0, m + r - M) for every tested r (Eqs. 9-10).
+__global__ __launch_bounds__(kBig) void k_feas_bank(Geom g, Workspace ws) {
+  const int b = blockIdx.x;
   __shared__ int hist[kSortMax + 1];
-  __shared__ unsigned char ok[kSortMax + 1];
+  __shared__ int tmp[16];
+  const int R = ws.R[b];
+  const int m = ws.m[b], M = ws.M[b];
+  for (int r = threadIdx.x; r <= R; r += kBig) hist[r] = 0;
+  __syncthreads();
+  for (int i = threadIdx.x; i < m; i += kBig) {
+    const int t = ws.first[(size_t)b * g.Mcap + i];
+    if (t <= R) atomicAdd(&hist[t], 1);
+  }
+  __syncthreads();
+  block_inclusive_scan_lds(hist, R + 1, tmp);
+  uint8_t *f = ws.feas + (size_t)b * (g.N + 1);
+  for (int r = threadIdx.x; r <= R; r += kBig) f[r] = hist[r] <= max(0, m + r - M);
+}
+
+// Per group: r* = the largest r feasible for every bank of the group (Eq. 11).
+__global__ __launch_bounds__(kBig) void k_feas_group(Geom g, Workspace ws, int32_t *out_rstar) {
+  const int grp = blockIdx.x;
   __shared__ int tmp[16];
   const int b0 = grp * g.gs;
   const int R = ws.R[b0];
-  for (int r = threadIdx.x; r <= R; r += kBig) ok[r] = 1;
-  for (int j = 0; j < g.gs; ++j) {
-    const int b = b0 + j;
-    const int m = ws.m[b], M = ws.M[b];
-    for (int r = threadIdx.x; r <= R; r += kBig) hist[r] = 0;
-    __syncthreads();
-    for (int i = threadIdx.x; i < m; i += kBig) {
-      const int t = ws.first[(size_t)b * g.Mcap + i];
-      if (t <= R) atomicAdd(&hist[t], 1);
-    }
-    __syncthreads();
-    block_inclusive_scan_lds(hist, R + 1, tmp);
-    for (int r = threadIdx.x; r <= R; r += kBig) {
-      const int e = max(0, m + r - M);
-      if (hist[r] > e) ok[r] = 0;
-    }
-    __syncthreads();
-  }
   int best = 0;
-  for (int r = threadIdx.x; r <= R; r += kBig)
-    if (ok[r]) best = max(best, r);
+  for (int r = threadIdx.x; r <= R; r += kBig) {
+    bool ok = true;
+    for (int j = 0; j < g.gs && ok; ++j) ok = ws.feas[(size_t)(b0 + j) * (g.N + 1) + r] != 0;
+    if (ok) best = max(best, r);
+  }
   best = block_max(best, tmp);
   if (threadIdx.x == 0) {
     ws.r_star[grp] = best;
@@ -537,18 +555,18 @@ __global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspac
     int n_mv, n_lh;
     int pm = block_excl_scan(mv_local, &n_mv, tmp);
     int ph = block_excl_scan(lh_local, &n_lh, tmp);
-    // hole list -> stash in sub[] (free until k_maint_gram) as slot numbers
+    // list of the holes below m_new, ascending
     for (int i = lo; i < hi; ++i) {
       const int dsl = ws.dest[rb + i];
       const bool occ = dsl >= 0 || (-1 - dsl) < rs;
-      if (!occ && i < m_new) ws.sub[rb + (ph++)] = i;
+      if (!occ && i < m_new) ws.hole_list[rb + (ph++)] = i;
     }
     __syncthreads();
     for (int i = lo; i < hi; ++i) {
       const int dsl = ws.dest[rb + i];
       const bool occ = dsl >= 0 || (-1 - dsl) < rs;
       if (occ && i >= m_new) {
-        const int to = (int)ws.sub[rb + pm];
+        const int to = ws.hole_list[rb + pm];
         ++pm;
         if (dsl >= 0) {
           ws.dest[rb + i] = to;  // moving survivor
@@ -781,13 +799,15 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
   if (g.N > 0) {
     k_cand_norms<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(seg.k, g, ws);
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 0);
-    else k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.score_q, nullptr);
-    k_sort<<<g.B, kBig, 0, s>>>(g, ws, out.order);
+    else k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, nullptr, nullptr);
+    k_sort<<<g.B, kBig, 0, s>>>(g, ws, out.order, out.score_q);
+    if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 4);
   }
   // with no candidates only states that already violate are found (prefix 0)
   if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 1);
   else k_cross_gram<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.first_cross);
-  k_feasible<<<g.G, kBig, 0, s>>>(g, ws, out.r_star);
+  k_feas_bank<<<g.B, kBig, 0, s>>>(g, ws);
+  k_feas_group<<<g.G, kBig, 0, s>>>(g, ws, out.r_star);
   if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 2);
   else k_fixup<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.rho_tilde);
   k_select<<<g.B, kBig, 0, s>>>(bank, g, ws, out);
@@ -802,15 +822,13 @@ hipError_t score_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
                       int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws,
                       hipStream_t s) {
   k_prep<<<g.B, kThreads, 0, s>>>(bank, g, ws);
-  Workspace w2 = ws;
-  w2.acol = nullptr;  // scoring only: no sort keys needed
   if (g.N > 0 && (score_q || score_f))
     k_cand_norms<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(seg.k, g, ws);
   if constexpr (DT == DKV_BF16) {
-    launch_score_mfma(bank, seg, g, p, (g.N > 0) ? score_q : nullptr, (g.N > 0) ? score_f : nullptr, density, w2, s);
+    launch_score_mfma(bank, seg, g, p, (g.N > 0) ? score_q : nullptr, (g.N > 0) ? score_f : nullptr, density, ws, s);
   } else {
     if (g.N > 0 && (score_q || score_f))
-      k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, w2, score_q, score_f);
+      k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, score_q, score_f);
     if (density)
       k_bank_density<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, g, p, ws, density);
   }
