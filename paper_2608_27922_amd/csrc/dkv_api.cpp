@@ -50,6 +50,9 @@ size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, cha
   w.sk = (uint16_t *)take(Bz * Nz * (size_t)d * 2);
   w.snorm = (float *)take(Bz * Nz * 4);
   w.feas = (uint8_t *)take(Bz * (Nz + 1));
+  const int npad = ((N > 0 ? N : 1) + 511) / 512 * 512;
+  w.skeys = (uint64_t *)take(Bz * (size_t)npad * 8);
+  w.npad = npad;
   w.nck = nck > 0 ? nck : 1;
   if (ws) *ws = w;
   return off;

@@ -48,6 +48,8 @@ struct Workspace {
   uint16_t *sk;        // [B, N, d] bf16 candidate keys in score order
   float *snorm;        // [B, N]   their norms
   uint8_t *feas;       // [B, N + 1] prefix length r feasible for this bank
+  uint64_t *skeys;     // [B, npad] sort keys, sorted within 512-key chunks
+  int npad;            // N rounded up to 512
   int nck;
 };
 

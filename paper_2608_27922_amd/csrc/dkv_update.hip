@@ -7,7 +7,8 @@
 //                   score scale 1/b of every bank state (Eq. 6)
 //   k_cand_norms    |k_x|^2 of every candidate
 //   k_score_gram    S_x = sum_i RNE(w_ix / b_i scaled) and Wcol_x = sum_i W_ix (Eq. 6)
-//   k_sort          stable ascending order of S_x, ties by source index (Alg. 1)
+//   k_sort_chunks   stable ascending order of S_x, ties by source index (Alg. 1):
+//   k_sort_rank     512-key chunks sorted in registers, then ranked by search
 //   k_cross_gram    prefix sums over the ordered candidates, first violating
 //                   prefix of every bank state (Eqs. 8-9), tile checkpoints
 //   k_feas_bank     c_r for every r and the flags c_r <= e_r (Eqs. 9-10)
@@ -211,43 +212,96 @@ __global__ __launch_bounds__(kThreads) void k_score_gram(dkv_bank bank, const vo
 }
 
 // ---------------------------------------------------------------------------
-// k_sort: bitonic sort of the unique keys of one bank in LDS.
+// Candidate order: unique keys (S_x << 13) | x sorted ascending (ties of S_x
+// by source index).  k_sort_chunks: one wave sorts 512 keys held 8 per lane
+// with a bitonic network (register and lane-shuffle exchanges only).
+// k_sort_rank: the rank of a key is its position in its own chunk plus the
+// number of smaller keys in every other chunk (binary search in LDS).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBig) void k_sort(Geom g, Workspace ws, int32_t *out_order, int64_t *out_score) {
-  const int b = blockIdx.x;
-  __shared__ uint64_t s[kSortMax];
-  int P = 2;
-  while (P < g.N) P <<= 1;
-  for (int i = threadIdx.x; i < P; i += kBig) {
+constexpr int kChunk = 512;
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
+  const uint32_t lo = __shfl_xor((uint32_t)v, mask, 64);
+  const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), mask, 64);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+__global__ __launch_bounds__(64) void k_sort_chunks(Geom g, Workspace ws, int64_t *out_score) {
+  const int b = blockIdx.y, c = blockIdx.x, lane = threadIdx.x;
+  const size_t nb = (size_t)b * g.N;
+  uint64_t v[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const int idx = c * kChunk + lane * 8 + r;
     uint64_t key = ~0ull;
-    if (i < g.N) {
-      const int64_t A = ws.acol[(size_t)b * g.N + i];
-      key = ((uint64_t)A << 13) | (uint64_t)i;  // ascending score, ties by source index
-      if (out_score) out_score[(size_t)b * g.N + i] = A;
+    if (idx < g.N) {
+      const int64_t A = ws.acol[nb + idx];
+      key = ((uint64_t)A << 13) | (uint64_t)idx;  // ascending score, ties by source index
+      if (out_score) out_score[nb + idx] = A;
     }
-    s[i] = key;
+    v[r] = key;
   }
-  __syncthreads();
-  for (int k = 2; k <= P; k <<= 1) {
+#pragma unroll
+  for (int k = 2; k <= kChunk; k <<= 1) {
+#pragma unroll
     for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int t = threadIdx.x; t < (P >> 1); t += kBig) {
-        const int i = ((t / j) * 2 * j) + (t % j);
-        const int ij = i + j;
-        const bool up = (i & k) == 0;
-        const uint64_t a = s[i], c = s[ij];
-        if ((a > c) == up) {
-          s[i] = c;
-          s[ij] = a;
+      if (j >= 8) {
+        const int lm = j >> 3;
+        const bool lower = (lane & lm) == 0;
+        const bool up = ((lane * 8) & k) == 0;
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          const uint64_t pv = shfl_xor_u64(v[r], lm);
+          const uint64_t lo = v[r] < pv ? v[r] : pv, hi = v[r] < pv ? pv : v[r];
+          v[r] = (lower == up) ? lo : hi;
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 8; ++r) {
+          const int rp = r ^ j;
+          if (rp > r) {
+            const bool up = (((lane * 8) + r) & k) == 0;
+            const uint64_t a = v[r], bb = v[rp];
+            const bool sw = up ? (a > bb) : (a < bb);
+            v[r] = sw ? bb : a;
+            v[rp] = sw ? a : bb;
+          }
         }
       }
-      __syncthreads();
     }
   }
-  for (int j = threadIdx.x; j < g.N; j += kBig) {
-    const int x = (int)(s[j] & 0x1FFFull);
-    ws.order[(size_t)b * g.N + j] = x;
-    ws.rank[(size_t)b * g.N + x] = j;
-    if (out_order) out_order[(size_t)b * g.N + j] = x;
+  const size_t base = (size_t)b * ws.npad + c * kChunk + lane * 8;
+#pragma unroll
+  for (int r = 0; r < 8; ++r) ws.skeys[base + r] = v[r];
+}
+
+__global__ __launch_bounds__(kBig) void k_sort_rank(Geom g, Workspace ws, int32_t *out_order) {
+  const int b = blockIdx.y;
+  __shared__ uint64_t sk[kSortMax];
+  const int np = ws.npad;
+  const int nch = np / kChunk;
+  for (int i = threadIdx.x; i < np; i += kBig) sk[i] = ws.skeys[(size_t)b * np + i];
+  __syncthreads();
+  const size_t nb = (size_t)b * g.N;
+  for (int p = blockIdx.x * kBig + threadIdx.x; p < np; p += gridDim.x * kBig) {
+    const uint64_t key = sk[p];
+    if (key == ~0ull) continue;
+    const int c = p / kChunk;
+    int rank = p - c * kChunk;
+    for (int c2 = 0; c2 < nch; ++c2) {
+      if (c2 == c) continue;
+      int lo = c2 * kChunk, hi = lo + kChunk;  // count of keys < key in [lo, hi)
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (sk[mid] < key) lo = mid + 1;
+        else hi = mid;
+      }
+      rank += lo - c2 * kChunk;
+    }
+    const int x = (int)(key & 0x1FFFull);
+    ws.order[nb + rank] = x;
+    ws.rank[nb + x] = rank;
+    if (out_order) out_order[nb + rank] = x;
   }
 }
 
@@ -800,7 +854,8 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
     k_cand_norms<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(seg.k, g, ws);
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 0);
     else k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, nullptr, nullptr);
-    k_sort<<<g.B, kBig, 0, s>>>(g, ws, out.order, out.score_q);
+    k_sort_chunks<<<dim3((unsigned)((g.N + kChunk - 1) / kChunk), (unsigned)g.B), 64, 0, s>>>(g, ws, out.score_q);
+    k_sort_rank<<<dim3(4u, (unsigned)g.B), kBig, 0, s>>>(g, ws, out.order);
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 4);
   }
   // with no candidates only states that already violate are found (prefix 0)
