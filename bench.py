@@ -37,6 +37,8 @@ def parse():
     ap.add_argument("--workload", default="single_layer", help="tiny or single_layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=1, help="heads in the oracle sample")
+    ap.add_argument("--copy-probe-mb", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (a known-size reference for HBM counters)")
     return ap.parse_args()
 
 
@@ -147,6 +149,14 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": None},
     }
+    if args.copy_probe_mb:
+        nbytes = args.copy_probe_mb << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        result["copy_probe_bytes"] = nbytes
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(case, cfg, args.cpu_heads)
     print(json.dumps(result), flush=True)

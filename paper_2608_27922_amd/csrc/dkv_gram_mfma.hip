@@ -45,7 +45,8 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 4;
 constexpr int kRowsPerWG = 32 * kWaves;
-constexpr int kCT = 32;  // column items per tile
+constexpr int kCT = 32;  // column items per MFMA tile
+constexpr int kSI = 64;  // column items per LDS stage (two tiles, two independent MFMA chains)
 
 template <int D>
 struct TileCfg {
@@ -119,11 +120,11 @@ __device__ __forceinline__ void load_row_frag(RowFrag<D> &rf, const uint16_t *ke
   rf.b[TileCfg<D>::kSteps] = __builtin_bit_cast(bf16x8, aug);
 }
 
-// Column tile staging: each of the 256 threads moves 16-byte chunks of the
-// tile's keys; 32 threads write the aug columns.
+// Column stage staging: each of the 256 threads moves 16-byte chunks of the
+// stage's keys; 64 threads write the aug columns.
 template <int D>
 struct ColStage {
-  u32x4 chunk[(kCT * TileCfg<D>::kChunks) / (64 * kWaves)];
+  u32x4 chunk[(kSI * TileCfg<D>::kChunks) / (64 * kWaves)];
   u32x4 aug0;
 };
 
@@ -131,7 +132,7 @@ struct ColStage {
 template <int D, class RowOf, class NormOf>
 __device__ __forceinline__ void stage_load(ColStage<D> &st, const uint16_t *base, int j0, int ncols,
                                            RowOf row_of, NormOf norm_of, float inv_s2) {
-  constexpr int kPer = (kCT * TileCfg<D>::kChunks) / (64 * kWaves);
+  constexpr int kPer = (kSI * TileCfg<D>::kChunks) / (64 * kWaves);
 #pragma unroll
   for (int q = 0; q < kPer; ++q) {
     const int c = threadIdx.x + q * 64 * kWaves;
@@ -143,7 +144,7 @@ __device__ __forceinline__ void stage_load(ColStage<D> &st, const uint16_t *base
     }
     st.chunk[q] = v;
   }
-  if (threadIdx.x < kCT) {
+  if (threadIdx.x < kSI) {
     u32x4 a = {0, 0, 0, 0};
     if (j0 + (int)threadIdx.x < ncols) {
       uint16_t nh, nm, nl;
@@ -159,14 +160,14 @@ __device__ __forceinline__ void stage_load(ColStage<D> &st, const uint16_t *base
 
 template <int D>
 __device__ __forceinline__ void stage_store(const ColStage<D> &st, uint16_t *lds) {
-  constexpr int kPer = (kCT * TileCfg<D>::kChunks) / (64 * kWaves);
+  constexpr int kPer = (kSI * TileCfg<D>::kChunks) / (64 * kWaves);
 #pragma unroll
   for (int q = 0; q < kPer; ++q) {
     const int c = threadIdx.x + q * 64 * kWaves;
     const int item = c / TileCfg<D>::kChunks, ch = c % TileCfg<D>::kChunks;
     *reinterpret_cast<u32x4 *>(lds + item * TileCfg<D>::kStride + ch * 8) = st.chunk[q];
   }
-  if (threadIdx.x < kCT) {
+  if (threadIdx.x < kSI) {
     *reinterpret_cast<u32x4 *>(lds + threadIdx.x * TileCfg<D>::kStride + D) = st.aug0;
     *reinterpret_cast<u32x4 *>(lds + threadIdx.x * TileCfg<D>::kStride + D + 8) = u32x4{0, 0, 0, 0};
   }
@@ -219,8 +220,8 @@ __global__ __launch_bounds__(64 * kWaves) void k_score_mfma(dkv_bank bank, const
   const int c0 = blockIdx.y * kColsPerSplit;
   if (c0 >= m) return;
   const int ncols = min(kColsPerSplit, m - c0);
-  __shared__ __attribute__((aligned(16))) uint16_t tile[2][kCT * TileCfg<D>::kStride];
-  __shared__ __attribute__((aligned(16))) float tbs[2][kCT];
+  __shared__ __attribute__((aligned(16))) uint16_t tile[2][kSI * TileCfg<D>::kStride];
+  __shared__ __attribute__((aligned(16))) float tbs[2][kSI];
   const uint16_t *K = static_cast<const uint16_t *>(seg_k);
   const uint16_t *BK = static_cast<const uint16_t *>(bank.k);
   const bool rv = x < g.N;
@@ -231,66 +232,83 @@ __global__ __launch_bounds__(64 * kWaves) void k_score_mfma(dkv_bank bank, const
   auto row_of = [&](int i) -> int64_t { return (int64_t)(rb + i); };
   auto norm_of = [&](int i) -> float { return bank.knorm[rb + i]; };
   uint64_t A64 = 0, W64 = 0;
-  const int nt = (ncols + kCT - 1) / kCT;
+  const int ns = (ncols + kSI - 1) / kSI;
   ColStage<D> st;
   float bs_next = 0.0f;
   stage_load<D>(st, BK, 0, ncols, row_of, norm_of, p.inv_sigma2);
-  if (threadIdx.x < kCT) bs_next = (int)threadIdx.x < ncols ? ws.bs[rb + threadIdx.x] : 0.0f;
+  if (threadIdx.x < kSI) bs_next = (int)threadIdx.x < ncols ? ws.bs[rb + threadIdx.x] : 0.0f;
   stage_store<D>(st, tile[0]);
-  if (threadIdx.x < kCT) tbs[0][threadIdx.x] = bs_next;
+  if (threadIdx.x < kSI) tbs[0][threadIdx.x] = bs_next;
   __syncthreads();
-  for (int t = 0; t < nt; ++t) {
-    const int cur = t & 1;
-    const int j0n = (t + 1) * kCT;
-    if (t + 1 < nt) {
-      stage_load<D>(st, BK, j0n, ncols, row_of, norm_of, p.inv_sigma2);
-      if (threadIdx.x < kCT) bs_next = j0n + (int)threadIdx.x < ncols ? ws.bs[rb + j0n + threadIdx.x] : 0.0f;
-    }
-    const f32x16 u = tile_u<D>(tile[cur], rf);
+  // epilogue of one 32-column tile: integer sums of W and of the scaled score terms
+  auto epi = [&](auto mask_tag, const f32x16 &u, const float *tb, int nvalid, uint32_t &sw, uint32_t &sa) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     float bsv[16];
 #pragma unroll
     for (int gq = 0; gq < 4; ++gq) {
-      const float4 v = *reinterpret_cast<const float4 *>(&tbs[cur][8 * gq + 4 * h]);
+      const float4 v = *reinterpret_cast<const float4 *>(&tb[8 * gq + 4 * h]);
       bsv[4 * gq + 0] = v.x;
       bsv[4 * gq + 1] = v.y;
       bsv[4 * gq + 2] = v.z;
       bsv[4 * gq + 3] = v.w;
     }
-    const int nvalid = ncols - t * kCT;
-    uint32_t sw = 0, sa = 0;
-    if (nvalid >= kCT) {
+    sw = 0;
+    sa = 0;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float tt = FOLD ? u[i] : 1.0f + u[i];
-        float tp = tt;
-        if constexpr (P >= 2) tp = tt * tt;
-        if constexpr (P == 4) tp = tp * tp;
-        const float y = __builtin_amdgcn_rcpf(tp);
-        const float e = __builtin_fmaf(-tp, y, 1.0f);
-        const float w = __builtin_fmaf(e, y, y);
-        sw += __float_as_uint(__builtin_fmaf(w, 8388608.0f, 8388608.0f));
-        sa += __float_as_uint(__builtin_fmaf(w, bsv[i], 8388608.0f));
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float tt = FOLD ? u[i] : 1.0f + u[i];
-        float tp = tt;
-        if constexpr (P >= 2) tp = tt * tt;
-        if constexpr (P == 4) tp = tp * tp;
-        const float y = __builtin_amdgcn_rcpf(tp);
-        const float e = __builtin_fmaf(-tp, y, 1.0f);
-        const float w = __builtin_fmaf(e, y, y);
+    for (int i = 0; i < 16; ++i) {
+      const float tt = FOLD ? u[i] : 1.0f + u[i];
+      float tp = tt;
+      if constexpr (P >= 2) tp = tt * tt;
+      if constexpr (P == 4) tp = tp * tp;
+      const float y = __builtin_amdgcn_rcpf(tp);
+      const float e = __builtin_fmaf(-tp, y, 1.0f);
+      const float w = __builtin_fmaf(e, y, y);
+      uint32_t rw = __float_as_uint(__builtin_fmaf(w, 8388608.0f, 8388608.0f));
+      uint32_t ra = __float_as_uint(__builtin_fmaf(w, bsv[i], 8388608.0f));
+      if constexpr (MASK) {
         const bool ok = col_of_reg(i, h) < nvalid;
-        sw += ok ? __float_as_uint(__builtin_fmaf(w, 8388608.0f, 8388608.0f)) : kMagic;
-        sa += ok ? __float_as_uint(__builtin_fmaf(w, bsv[i], 8388608.0f)) : kMagic;
+        rw = ok ? rw : kMagic;
+        ra = ok ? ra : kMagic;
+      }
+      sw += rw;
+      sa += ra;
+    }
+    sw -= 16u * kMagic;
+    sa -= 16u * kMagic;
+  };
+  using Full = std::integral_constant<bool, false>;
+  using Part = std::integral_constant<bool, true>;
+  for (int t = 0; t < ns; ++t) {
+    const int cur = t & 1;
+    const int j0n = (t + 1) * kSI;
+    if (t + 1 < ns) {
+      stage_load<D>(st, BK, j0n, ncols, row_of, norm_of, p.inv_sigma2);
+      if (threadIdx.x < kSI) bs_next = j0n + (int)threadIdx.x < ncols ? ws.bs[rb + j0n + threadIdx.x] : 0.0f;
+    }
+    const int nv0 = ncols - t * kSI;
+    const f32x16 u0 = tile_u<D>(tile[cur], rf);
+    const f32x16 u1 = tile_u<D>(tile[cur] + kCT * TileCfg<D>::kStride, rf);
+    uint32_t sw, sa;
+    if (nv0 >= kSI) {
+      epi(Full{}, u0, tbs[cur], kCT, sw, sa);
+      W64 += sw;
+      A64 += sa;
+      epi(Full{}, u1, tbs[cur] + kCT, kCT, sw, sa);
+      W64 += sw;
+      A64 += sa;
+    } else {
+      epi(Part{}, u0, tbs[cur], nv0, sw, sa);
+      W64 += sw;
+      A64 += sa;
+      if (nv0 > kCT) {
+        epi(Part{}, u1, tbs[cur] + kCT, nv0 - kCT, sw, sa);
+        W64 += sw;
+        A64 += sa;
       }
     }
-    W64 += (uint32_t)(sw - 16u * kMagic);
-    A64 += (uint32_t)(sa - 16u * kMagic);
-    if (t + 1 < nt) {
+    if (t + 1 < ns) {
       stage_store<D>(st, tile[cur ^ 1]);
-      if (threadIdx.x < kCT) tbs[cur ^ 1][threadIdx.x] = bs_next;
+      if (threadIdx.x < kSI) tbs[cur ^ 1][threadIdx.x] = bs_next;
     }
     __syncthreads();
   }
@@ -393,54 +411,56 @@ __global__ __launch_bounds__(64 * kWaves) void k_rowsum_mfma(dkv_bank bank, cons
   };
   const uint16_t *colbase = (MODE == RS_CHUNK || MODE == RS_FIXUP) ? SORTK : (MODE == RS_ADM_MUT ? SK : BK);
   constexpr bool kDiag = (MODE == RS_ADM_MUT || MODE == RS_DENSITY);
-  __shared__ __attribute__((aligned(16))) uint16_t tile[2][kCT * TileCfg<D>::kStride];
+  __shared__ __attribute__((aligned(16))) uint16_t tile[2][kSI * TileCfg<D>::kStride];
   uint64_t S64 = 0;
   uint32_t chunk_sum = 0;
   const int ncols = c1 - c0;
-  const int nt = (ncols + kCT - 1) / kCT;
+  const int ns = (ncols + kSI - 1) / kSI;
   ColStage<D> st;
   auto row_of_rel = [&](int j) -> int64_t { return row_of(c0 + j); };
   auto norm_of_rel = [&](int j) -> float { return norm_of(c0 + j); };
-  if (nt > 0) {
+  if (ns > 0) {
     stage_load<D>(st, colbase, 0, ncols, row_of_rel, norm_of_rel, p.inv_sigma2);
     stage_store<D>(st, tile[0]);
   }
   __syncthreads();
   const int wg_row0 = blockIdx.x * kRowsPerWG;
-  for (int t = 0; t < nt; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < nt) stage_load<D>(st, colbase, (t + 1) * kCT, ncols, row_of_rel, norm_of_rel, p.inv_sigma2);
-    const f32x16 u = tile_u<D>(tile[cur], rf);
-    const int nvalid = ncols - t * kCT;
-    const int j0 = c0 + t * kCT;
+  // sum of the lane's 16 weights of one 32-column tile starting at list index j0
+  auto tile_sum = [&](const f32x16 &u, int j0, int nvalid) -> uint32_t {
     const bool diag_tile = kDiag && (j0 < wg_row0 + kRowsPerWG) && (j0 + kCT > wg_row0);
-    uint32_t s;
-    if (nvalid >= kCT && !diag_tile) {
-      s = lane_wsum<P, false, FOLD>(u, kCT, h);
-    } else {
-      s = 0;
+    if (nvalid >= kCT && !diag_tile) return lane_wsum<P, false, FOLD>(u, kCT, h);
+    uint32_t sm = 0;
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int mm = col_of_reg(q, h);
-        uint32_t raw = weight_raw<P, FOLD>(u[q], 8388608.0f);
-        bool ok = mm < nvalid;
-        if (kDiag) ok = ok && (j0 + mm != v);
-        s += ok ? raw : kMagic;
-      }
-      s -= 16u * kMagic;
+    for (int q = 0; q < 16; ++q) {
+      const int mm = col_of_reg(q, h);
+      uint32_t raw = weight_raw<P, FOLD>(u[q], 8388608.0f);
+      bool ok = mm < nvalid;
+      if (kDiag) ok = ok && (j0 + mm != v);
+      sm += ok ? raw : kMagic;
     }
+    return sm - 16u * kMagic;
+  };
+  for (int t = 0; t < ns; ++t) {
+    const int cur = t & 1;
+    if (t + 1 < ns) stage_load<D>(st, colbase, (t + 1) * kSI, ncols, row_of_rel, norm_of_rel, p.inv_sigma2);
+    const f32x16 u0 = tile_u<D>(tile[cur], rf);
+    const f32x16 u1 = tile_u<D>(tile[cur] + kCT * TileCfg<D>::kStride, rf);
+    const int nv0 = ncols - t * kSI;
+    const int j0 = c0 + t * kSI;
+    uint32_t s2 = tile_sum(u0, j0, nv0);
+    if (nv0 > kCT) s2 += tile_sum(u1, j0 + kCT, nv0 - kCT);
     if constexpr (MODE == RS_CHUNK) {
-      chunk_sum += s;
-      const bool chunk_end = ((t + 1) % (kCkStride / kCT)) == 0 || t + 1 == nt;
+      chunk_sum += s2;
+      const bool chunk_end = ((t + 1) % (kCkStride / kSI)) == 0 || t + 1 == ns;
       if (chunk_end) {
         const uint32_t tot = chunk_sum + __shfl_xor(chunk_sum, 32, 64);
         if (rv && h == 0) ws.ck[(rb + v) * ws.nck + (j0 / kCkStride)] = tot;
         chunk_sum = 0;
       }
     } else {
-      S64 += s;
+      S64 += s2;
     }
-    if (t + 1 < nt) stage_store<D>(st, tile[cur ^ 1]);
+    if (t + 1 < ns) stage_store<D>(st, tile[cur ^ 1]);
     __syncthreads();
   }
   if constexpr (MODE == RS_CHUNK) return;
@@ -461,93 +481,111 @@ __global__ __launch_bounds__(64 * kWaves) void k_rowsum_mfma(dkv_bank bank, cons
 }
 
 // ---------------------------------------------------------------------------
-// First violating prefix length of every bank state.  One wave per state:
-// scan the chunk sums, then re-walk the one chunk where the threshold is
-// reached, 4 ordered candidates per lane, with the same binary32 weights.
+// First violating prefix length of every bank state (Eqs. 8-9).
+// k_cross_scan: thread per state; the first 256-candidate chunk whose sum
+// lifts the prefix density to tau b.  States that never reach it get R + 1;
+// the others are listed for k_cross_find, which re-walks that one chunk (4
+// ordered candidates per lane, same binary32 weights) for the exact length.
 // ---------------------------------------------------------------------------
-template <int D, int P>
-__global__ __launch_bounds__(256) void k_cross_find(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
-  const int b = blockIdx.y;
-  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
-  const int i = blockIdx.x * 4 + wave;
+__global__ __launch_bounds__(256) void k_cross_scan(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
+  const int b = blockIdx.y, i = blockIdx.x * 256 + threadIdx.x;
   const int m = ws.m[b], R = ws.R[b];
   if (i >= m) return;
-  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
-  const size_t row = rb + i;
+  const size_t rb = (size_t)b * g.Mcap, row = rb + i;
   const int64_t lim = ((int64_t)p.tau_num * bank.base[row] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
   const int64_t thr = lim - bank.rho[row];
   int first = R + 1;
   if (thr <= 0) {
     first = 0;
-  } else if (R > 0) {
+  } else {
     const int nch = (R + kCkStride - 1) / kCkStride;
-    const uint64_t cv = l < nch ? ws.ck[row * ws.nck + l] : 0;
-    uint64_t inc = cv;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint64_t y = __shfl_up(inc, o, 64);
-      if (l >= o) inc += y;
-    }
-    const unsigned long long hit = __ballot((int64_t)inc >= thr && l < nch);
-    if (hit != 0) {
-      const int c = __ffsll(hit) - 1;
-      const int64_t before = (int64_t)__shfl(inc - cv, c, 64);
-      // re-walk chunk c: columns [256 c, min(256 c + 256, R)), lane l owns 4 of them
-      const uint16_t *rk = static_cast<const uint16_t *>(bank.k) + row * D;
-      const float nr = bank.knorm[row];
-      const int col0 = c * kCkStride + 4 * l;
-      uint32_t w4[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int col = col0 + q;
-        uint32_t W = 0;
-        if (col < R) {
-          const uint16_t *ckey = ws.sk + (nb + col) * D;
-          float acc = 0.0f;
-#pragma unroll
-          for (int j = 0; j < D; j += 8) {
-            const u32x4 a = *reinterpret_cast<const u32x4 *>(rk + j);
-            const u32x4 bb = *reinterpret_cast<const u32x4 *>(ckey + j);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              acc = __builtin_fmaf(__uint_as_float(a[e] << 16), __uint_as_float(bb[e] << 16), acc);
-              acc = __builtin_fmaf(__uint_as_float(a[e] & 0xFFFF0000u), __uint_as_float(bb[e] & 0xFFFF0000u), acc);
-            }
-          }
-          const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
-          W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
-        }
-        w4[q] = W;
+    int64_t P = 0;
+    for (int c = 0; c < nch; ++c) {
+      const int64_t v = ws.ck[row * ws.nck + c];
+      if (P + v >= thr) {
+        const int k = atomicAdd(&ws.xcount[b], 1);
+        ws.xlist[rb + k] = i | (c << 16);
+        ws.xbefore[rb + k] = P;
+        return;  // first written by k_cross_find
       }
-      uint32_t loc[4];
-      loc[0] = w4[0];
-      loc[1] = loc[0] + w4[1];
-      loc[2] = loc[1] + w4[2];
-      loc[3] = loc[2] + w4[3];
-      uint32_t incl = loc[3];
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(incl, o, 64);
-        if (l >= o) incl += y;
-      }
-      const int64_t base_l = before + (int64_t)(incl - loc[3]);
-      int qf = -1;
-#pragma unroll
-      for (int q = 3; q >= 0; --q)
-        if (base_l + (int64_t)loc[q] >= thr) qf = q;
-      const unsigned long long hl = __ballot(qf >= 0);
-      if (hl != 0) {
-        const int lf = __ffsll(hl) - 1;
-        const int qsel = __shfl(qf, lf, 64);
-        first = c * kCkStride + 4 * lf + qsel + 1;
-      } else {
-        first = min(R, (c + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
-      }
+      P += v;
     }
   }
-  if (l == 0) {
-    ws.first[row] = first;
-    if (out_first) out_first[row] = first;
+  ws.first[row] = first;
+  if (out_first) out_first[row] = first;
+}
+
+template <int D, int P>
+__global__ __launch_bounds__(256) void k_cross_find(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
+  const int b = blockIdx.y;
+  const int l = threadIdx.x & 63;
+  const int R = ws.R[b];
+  const int cnt = ws.xcount[b];
+  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
+  {
+    const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (k >= cnt) return;
+    const int ent = ws.xlist[rb + k];
+    const int i = ent & 0xFFFF, c = ent >> 16;
+    const int64_t before = ws.xbefore[rb + k];
+    const size_t row = rb + i;
+    const int64_t lim = ((int64_t)p.tau_num * bank.base[row] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
+    const int64_t thr = lim - bank.rho[row];
+    const uint16_t *rk = static_cast<const uint16_t *>(bank.k) + row * D;
+    const float nr = bank.knorm[row];
+    const int col0 = c * kCkStride + 4 * l;
+    uint32_t w4[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int col = col0 + q;
+      uint32_t W = 0;
+      if (col < R) {
+        const uint16_t *ckey = ws.sk + (nb + col) * D;
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = 0; j < D; j += 8) {
+          const u32x4 a = *reinterpret_cast<const u32x4 *>(rk + j);
+          const u32x4 bb = *reinterpret_cast<const u32x4 *>(ckey + j);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc = __builtin_fmaf(__uint_as_float(a[e] << 16), __uint_as_float(bb[e] << 16), acc);
+            acc = __builtin_fmaf(__uint_as_float(a[e] & 0xFFFF0000u), __uint_as_float(bb[e] & 0xFFFF0000u), acc);
+          }
+        }
+        const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
+        W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
+      }
+      w4[q] = W;
+    }
+    uint32_t loc[4];
+    loc[0] = w4[0];
+    loc[1] = loc[0] + w4[1];
+    loc[2] = loc[1] + w4[2];
+    loc[3] = loc[2] + w4[3];
+    uint32_t incl = loc[3];
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(incl, o, 64);
+      if (l >= o) incl += y;
+    }
+    const int64_t base_l = before + (int64_t)(incl - loc[3]);
+    int qf = -1;
+#pragma unroll
+    for (int q = 3; q >= 0; --q)
+      if (base_l + (int64_t)loc[q] >= thr) qf = q;
+    const unsigned long long hl = __ballot(qf >= 0);
+    int first;
+    if (hl != 0) {
+      const int lf = __ffsll(hl) - 1;
+      const int qsel = __shfl(qf, lf, 64);
+      first = c * kCkStride + 4 * lf + qsel + 1;
+    } else {
+      first = min(R, (c + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
+    }
+    if (l == 0) {
+      ws.first[row] = first;
+      if (out_first) out_first[row] = first;
+    }
   }
 }
 
@@ -600,6 +638,7 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       if (g.N > 0)
         k_rowsum_mfma<D, P, RS_CHUNK, F><<<dim3(rowsM, cdiv(g.N, kChunksPerSplit * kCkStride), g.B), T, 0, s>>>(
             bank, seg.k, g, p, ws, nullptr);
+      k_cross_scan<<<dim3(cdiv(g.Mcap, 256), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
       k_cross_find<D, P><<<dim3(cdiv(g.Mcap, 4), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
       break;
     }

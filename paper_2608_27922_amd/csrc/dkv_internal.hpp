@@ -47,7 +47,11 @@ struct Workspace {
   int32_t *hole_list;  // [B, Mcap] holes closed by moving states (states violating before the update)
   uint16_t *sk;        // [B, N, d] bf16 candidate keys in score order
   float *snorm;        // [B, N]   their norms
-  uint8_t *feas;       // [B, N + 1] prefix length r feasible for this bank
+  uint32_t *feas;      // [B, nfw] bit r: prefix length r feasible for this bank
+  int nfw;             // words per bank of feas
+  int32_t *xcount;     // [B] states whose first violation lies inside the tested prefixes
+  int32_t *xlist;      // [B, Mcap] those states: slot | (256-candidate chunk << 16)
+  int64_t *xbefore;    // [B, Mcap] their prefix sum before that chunk
   uint64_t *skeys;     // [B, npad] sort keys, sorted within 512-key chunks
   int npad;            // N rounded up to 512
   int nck;
@@ -123,6 +127,13 @@ __device__ __forceinline__ float pair_weight(float d2, float inv_sigma2, int p) 
   if (p >= 2) tp = t * t;
   if (p == 4) tp = tp * tp;
   return rcp_rn(tp);
+}
+// Score scale of a bank state (Eq. 6): fp32(2^23 / b) by one fp64 division
+// rounded to fp32, times 2^(23 - E) with E the binary exponent of the bank's
+// largest such value (so the scale is at most 2^23).  Baselines below 1 read as 1.
+__device__ __forceinline__ float score_scale(int64_t base, int E) {
+  const int64_t bi = base < 1 ? 1 : base;
+  return ldexpf((float)(8388608.0 / (double)bi), 23 - E);
 }
 // RNE(w * scale) for w * scale in [0, 2^23]: fma(w, scale, 2^23) lands in
 // [2^23, 2^24] where one ulp is 1, so its bit pattern minus that of 2^23 is

@@ -16,13 +16,15 @@
 //   k_fixup         projected density rho~(r*) of every bank state
 //   k_select        mandatory + densest eviction (Sec. 3.4 step 3), commit plan
 //   k_maint_gram    weights to the evicted and to the co-admitted states (Supp. C)
-//   k_commit        exact density maintenance, baselines (Eq. 5), K/V placement
+//   k_commit_surv   exact density maintenance of the survivors (Supp. C)
+//   k_commit_adm    admitted K/V placement, densities and baselines (Eq. 5)
 //
 // Arithmetic: keys on the 1/64 grid give exact fp32 inner products; weights are
 // binary32 with round-to-nearest-even; every sum is an integer sum of Q23
 // terms, so results do not depend on tiling or thread order.
 #include <hip/hip_runtime.h>
 
+#include <climits>
 #include <type_traits>
 
 #include "dkv_internal.hpp"
@@ -99,50 +101,61 @@ __device__ __forceinline__ float dot_row(const float (&kr)[D], const float *col)
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kThreads) void k_prep(dkv_bank bank, Geom g, Workspace ws) {
   const int b = blockIdx.x;
-  __shared__ float red[kThreads / 64];
   const int Mb = clampi(bank.budget[b], 0, g.Mcap);
   const int m = clampi(bank.occupancy[b], 0, Mb);
   // Tested prefix lengths 0..R: R = min(N, every budget of the group).
   int R = g.N;
   const int g0 = (b / g.gs) * g.gs;
   for (int j = 0; j < g.gs; ++j) R = min(R, clampi(bank.budget[g0 + j], 0, g.Mcap));
-  // Score scale: inv_i = fp32(2^23 / b_i) (fp64 division, one rounding to fp32);
-  // E = binary exponent of max_i inv_i; bs_i = inv_i * 2^(23 - E) <= 2^23.
-  float mx = 0.0f;
+  // Score scale exponent E: binary exponent of max_i fp32(2^23 / b_i), i.e. of
+  // the value at the smallest baseline (the division and rounding are monotone).
+  __shared__ long long redb[kThreads / 64];
+  long long mn = LLONG_MAX;
   for (int i = threadIdx.x; i < m; i += kThreads) {
-    int64_t bi = bank.base[(size_t)b * g.Mcap + i];
-    bi = bi < 1 ? 1 : bi;
-    float inv = (float)(8388608.0 / (double)bi);
-    mx = fmaxf(mx, inv);
+    const long long bi = bank.base[(size_t)b * g.Mcap + i];
+    mn = bi < mn ? bi : mn;
   }
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = mx;
+  for (int o = 32; o > 0; o >>= 1) {
+    const long long y = __shfl_xor(mn, o, 64);
+    mn = y < mn ? y : mn;
+  }
+  if ((threadIdx.x & 63) == 0) redb[threadIdx.x >> 6] = mn;
   __syncthreads();
-  mx = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+  for (int w = 0; w < kThreads / 64; ++w) mn = redb[w] < mn ? redb[w] : mn;
   int E = 0;
-  if (m > 0) frexpf(mx, &E);
-  for (int i = threadIdx.x; i < m; i += kThreads) {
-    int64_t bi = bank.base[(size_t)b * g.Mcap + i];
-    bi = bi < 1 ? 1 : bi;
-    float inv = (float)(8388608.0 / (double)bi);
-    ws.bs[(size_t)b * g.Mcap + i] = ldexpf(inv, 23 - E);
+  if (m > 0) {
+    const long long bi = mn < 1 ? 1 : mn;
+    frexpf((float)(8388608.0 / (double)bi), &E);
   }
-  // accumulators filled with atomic adds by the Gram stages
-  for (int x = threadIdx.x; x < g.N; x += kThreads) {
-    const size_t o = (size_t)b * g.N + x;
-    ws.acol[o] = 0;
-    ws.wcol[o] = 0;
-    ws.sub_adm[o] = 0;
-    ws.mut_adm[o] = 0;
-  }
-  for (int i = threadIdx.x; i < g.Mcap; i += kThreads) ws.sub[(size_t)b * g.Mcap + i] = 0;
   if (threadIdx.x == 0) {
     ws.m[b] = m;
     ws.M[b] = Mb;
     ws.R[b] = R;
     ws.E[b] = E;
   }
+}
+
+// Score scale of every live bank state (after k_prep has fixed E).
+__global__ void k_bscale(dkv_bank bank, Geom g, Workspace ws) {
+  const int b = blockIdx.y, i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= ws.m[b]) return;
+  const size_t o = (size_t)b * g.Mcap + i;
+  ws.bs[o] = score_scale(bank.base[o], ws.E[b]);
+}
+
+// Accumulators filled with integer atomic adds by the Gram stages.
+__global__ void k_zero(Geom g, Workspace ws) {
+  const size_t nN = (size_t)g.B * g.N, nM = (size_t)g.B * g.Mcap;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < nN; i += stride) {
+    ws.acol[i] = 0;
+    ws.wcol[i] = 0;
+    ws.sub_adm[i] = 0;
+    ws.mut_adm[i] = 0;
+  }
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < nM; i += stride) ws.sub[i] = 0;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < (size_t)g.B; i += stride) ws.xcount[i] = 0;
 }
 
 template <int D, int DT>
@@ -387,8 +400,8 @@ __device__ void block_inclusive_scan_lds(int *a, int n, int *tmp) {
   __syncthreads();
 }
 
-// Per bank: c_r = #{i : first_i <= r} by histogram + scan, and the flag
-// c_r <= e_r = max(0, m + r - M) for every tested r (Eqs. 9-10).
+// Per bank: c_r = #{i : first_i <= r} by histogram + scan, and bit r of the
+// feasibility mask set iff c_r <= e_r = max(0, m + r - M) (Eqs. 9-10).
 __global__ __launch_bounds__(kBig) void k_feas_bank(Geom g, Workspace ws) {
   const int b = blockIdx.x;
   __shared__ int hist[kSortMax + 1];
@@ -403,8 +416,15 @@ __global__ __launch_bounds__(kBig) void k_feas_bank(Geom g, Workspace ws) {
   }
   __syncthreads();
   block_inclusive_scan_lds(hist, R + 1, tmp);
-  uint8_t *f = ws.feas + (size_t)b * (g.N + 1);
-  for (int r = threadIdx.x; r <= R; r += kBig) f[r] = hist[r] <= max(0, m + r - M);
+  uint32_t *f = ws.feas + (size_t)b * ws.nfw;
+  for (int w = threadIdx.x; w < ws.nfw; w += kBig) {
+    uint32_t bits = 0;
+    for (int q = 0; q < 32; ++q) {
+      const int r = 32 * w + q;
+      if (r <= R && hist[r] <= max(0, m + r - M)) bits |= 1u << q;
+    }
+    f[w] = bits;
+  }
 }
 
 // Per group: r* = the largest r feasible for every bank of the group (Eq. 11).
@@ -412,12 +432,11 @@ __global__ __launch_bounds__(kBig) void k_feas_group(Geom g, Workspace ws, int32
   const int grp = blockIdx.x;
   __shared__ int tmp[16];
   const int b0 = grp * g.gs;
-  const int R = ws.R[b0];
   int best = 0;
-  for (int r = threadIdx.x; r <= R; r += kBig) {
-    bool ok = true;
-    for (int j = 0; j < g.gs && ok; ++j) ok = ws.feas[(size_t)(b0 + j) * (g.N + 1) + r] != 0;
-    if (ok) best = max(best, r);
+  for (int w = threadIdx.x; w < ws.nfw; w += kBig) {
+    uint32_t bits = ~0u;
+    for (int j = 0; j < g.gs; ++j) bits &= ws.feas[(size_t)(b0 + j) * ws.nfw + w];
+    if (bits) best = max(best, 32 * w + 31 - __clz(bits));
   }
   best = block_max(best, tmp);
   if (threadIdx.x == 0) {
@@ -738,61 +757,64 @@ __global__ __launch_bounds__(kThreads) void k_maint_gram(dkv_bank bank, const vo
 }
 
 // ---------------------------------------------------------------------------
-// k_commit: one wave per virtual row; new densities, baselines and placement.
+// Commit.  k_commit_surv: thread per surviving state: rho <- rho~(r*) minus its
+// weights to the evicted states (Supp. C); a state that closes a hole (only when
+// more states left than entered) moves with its key, value and metadata.
+// k_commit_adm: wave per admitted candidate: K/V row into its slot, density
+// over the final bank, frozen baseline max(rho, delta) (Eq. 5), provenance.
 // ---------------------------------------------------------------------------
 template <int D, int DT>
-__global__ __launch_bounds__(kThreads) void k_commit(dkv_bank bank, dkv_segment seg, Geom g, Prm p,
-                                                     Workspace ws) {
+__global__ __launch_bounds__(kThreads) void k_commit_surv(dkv_bank bank, Geom g, Workspace ws) {
   using E = typename std::conditional<DT == DKV_BF16, uint16_t, float>::type;
+  const int b = blockIdx.y, v = blockIdx.x * kThreads + threadIdx.x;
+  if (v >= ws.m[b]) return;
+  const size_t rb = (size_t)b * g.Mcap;
+  const int to = ws.dest[rb + v];
+  if (to < 0) return;
+  const int64_t rho = ws.rho_t[rb + v] - ws.sub[rb + v];
+  if (to != v) {
+    E *K = static_cast<E *>(bank.k);
+    E *V = static_cast<E *>(bank.v);
+    for (int j = 0; j < D; ++j) {
+      K[(rb + to) * D + j] = K[(rb + v) * D + j];
+      V[(rb + to) * D + j] = V[(rb + v) * D + j];
+    }
+    bank.base[rb + to] = bank.base[rb + v];
+    bank.prov[rb + to] = bank.prov[rb + v];
+    bank.knorm[rb + to] = bank.knorm[rb + v];
+  }
+  bank.rho[rb + to] = rho;
+}
+
+template <int D, int DT>
+__global__ __launch_bounds__(kThreads) void k_commit_adm(dkv_bank bank, dkv_segment seg, Geom g, Prm p,
+                                                         Workspace ws) {
+  using E = typename std::conditional<DT == DKV_BF16, uint16_t, float>::type;
+  constexpr int kCh = D * (int)sizeof(E) / 16;  // 16-byte chunks per key (and per value) row
   const int b = blockIdx.y;
-  const int lane = threadIdx.x & 63;
-  const int v = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
-  const int m = ws.m[b];
+  const int t = blockIdx.x * kThreads + threadIdx.x;
+  const int k = t / (2 * kCh), ch = t % (2 * kCh);
   const int rs = ws.r_star[b / g.gs];
+  if (k >= rs || k >= g.N) return;
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
-  E *K = static_cast<E *>(bank.k);
-  E *V = static_cast<E *>(bank.v);
-  const E *SK = static_cast<const E *>(seg.k);
-  const E *SV = static_cast<const E *>(seg.v);
-  if (v < g.Mcap) {
-    if (v >= m) return;
-    const int to = ws.dest[rb + v];
-    if (to < 0) return;
-    const int64_t rho = ws.rho_t[rb + v] - ws.sub[rb + v];
-    if (to != v) {
-      for (int j = lane; j < D; j += 64) {
-        K[(rb + to) * D + j] = K[(rb + v) * D + j];
-        V[(rb + to) * D + j] = V[(rb + v) * D + j];
-      }
-    }
-    if (lane == 0) {
-      bank.rho[rb + to] = rho;
-      if (to != v) {
-        bank.base[rb + to] = bank.base[rb + v];
-        bank.prov[rb + to] = bank.prov[rb + v];
-        bank.knorm[rb + to] = bank.knorm[rb + v];
-      }
-    }
-  } else {
-    const int k = v - g.Mcap;
-    if (k >= rs || k >= g.N) return;
-    const int x = ws.adm_list[nb + k];
-    const int to = ws.adm_dest[nb + k];
-    for (int j = lane; j < D; j += 64) {
-      K[(rb + to) * D + j] = SK[(nb + x) * D + j];
-      V[(rb + to) * D + j] = SV[(nb + x) * D + j];
-    }
-    if (lane == 0) {
-      // density over the final bank: survivors (directly, or the whole old bank
-      // minus the evicted) plus the other co-admitted candidates
-      const int n_ev = ws.n_ev[b];
-      const int64_t surv_sum = (n_ev <= m - n_ev) ? ws.wcol[nb + x] - ws.sub_adm[nb + k] : ws.sub_adm[nb + k];
-      const int64_t rho = surv_sum + ws.mut_adm[nb + k];
-      bank.rho[rb + to] = rho;
-      bank.base[rb + to] = rho > p.delta_q ? rho : p.delta_q;
-      bank.prov[rb + to] = ((int64_t)p.block_id << 32) | (int64_t)x;
-      bank.knorm[rb + to] = ws.cnorm[nb + x];
-    }
+  const int x = ws.adm_list[nb + k];
+  const int to = ws.adm_dest[nb + k];
+  const bool isv = ch >= kCh;
+  const int c = isv ? ch - kCh : ch;
+  const E *src = static_cast<const E *>(isv ? seg.v : seg.k) + (nb + x) * D;
+  E *dst = static_cast<E *>(isv ? bank.v : bank.k) + (rb + to) * D;
+  reinterpret_cast<uint4 *>(dst)[c] = reinterpret_cast<const uint4 *>(src)[c];
+  if (ch == 0) {
+    // density over the final bank: survivors (directly, or the whole old bank
+    // minus the evicted) plus the other co-admitted candidates
+    const int m = ws.m[b];
+    const int n_ev = ws.n_ev[b];
+    const int64_t surv_sum = (n_ev <= m - n_ev) ? ws.wcol[nb + x] - ws.sub_adm[nb + k] : ws.sub_adm[nb + k];
+    const int64_t rho = surv_sum + ws.mut_adm[nb + k];
+    bank.rho[rb + to] = rho;
+    bank.base[rb + to] = rho > p.delta_q ? rho : p.delta_q;
+    bank.prov[rb + to] = ((int64_t)p.block_id << 32) | (int64_t)x;
+    bank.knorm[rb + to] = ws.cnorm[nb + x];
   }
 }
 
@@ -850,6 +872,8 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
   // bf16 banks: Gram stages on MFMA; fp32 banks: the same stages on the VALU.
   constexpr bool kMfma = DT == DKV_BF16;
   k_prep<<<g.B, kThreads, 0, s>>>(bank, g, ws);
+  k_zero<<<1024, 256, 0, s>>>(g, ws);
+  k_bscale<<<grid2(g.Mcap, 256, g.B), 256, 0, s>>>(bank, g, ws);
   if (g.N > 0) {
     k_cand_norms<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(seg.k, g, ws);
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 0);
@@ -868,7 +892,8 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
   k_select<<<g.B, kBig, 0, s>>>(bank, g, ws, out);
   if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 3);
   else k_maint_gram<D, DT><<<grid2(g.Mcap + g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws);
-  k_commit<D, DT><<<grid2(g.Mcap + g.N, kThreads / 64, g.B), kThreads, 0, s>>>(bank, seg, g, p, ws);
+  k_commit_surv<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, g, ws);
+  if (g.N > 0) k_commit_adm<D, DT><<<grid2(g.N * (2 * D * (DT == DKV_BF16 ? 2 : 4) / 16), kThreads, g.B), kThreads, 0, s>>>(bank, seg, g, p, ws);
   return hipGetLastError();
 }
 
@@ -877,6 +902,8 @@ hipError_t score_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
                       int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws,
                       hipStream_t s) {
   k_prep<<<g.B, kThreads, 0, s>>>(bank, g, ws);
+  k_zero<<<1024, 256, 0, s>>>(g, ws);
+  k_bscale<<<grid2(g.Mcap, 256, g.B), 256, 0, s>>>(bank, g, ws);
   if (g.N > 0 && (score_q || score_f))
     k_cand_norms<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(seg.k, g, ws);
   if constexpr (DT == DKV_BF16) {
