@@ -18,8 +18,10 @@ the CPU oracle timed on a bounded sample.
 """
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -27,6 +29,9 @@ import numpy as np
 
 PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
+ROOT = os.path.dirname(os.path.abspath(__file__))
+ATTN_SOURCE = os.path.join(ROOT, "paper_2608_27922_amd", "csrc", "dkv_attention.hip")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_attn_mfma_single_layer_traffic.md")
 
 
 def parse():
@@ -38,8 +43,25 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-heads", type=int, default=1, help="heads in the oracle sample")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
-                    help="also run a plain device copy of this many MiB (a known-size reference for HBM counters)")
+                    help="also run a plain elementwise copy (negation) of this many MiB: the known-size "
+                         "reference that scales the HBM byte counters")
     return ap.parse_args()
+
+
+def measured_traffic():
+    """HBM bytes per launch of the attention kernel from the committed counter summary
+    (FETCH_SIZE + WRITE_SIZE, each scaled by the copy-kernel calibration), or None when
+    the summary is absent or the kernel source changed after the counters were taken."""
+    try:
+        text = open(TRAFFIC_SUMMARY).read()
+    except OSError:
+        return None
+    want = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
+    val = re.search(r"traffic_bytes_per_launch:\s*([0-9]+)", text)
+    if not want or not val:
+        return None
+    have = hashlib.sha256(open(ATTN_SOURCE, "rb").read()).hexdigest()
+    return int(val.group(1)) if have == want.group(1) else None
 
 
 def cpu_baseline(case, cfg, n_heads):
@@ -147,14 +169,14 @@ def main():
         "attention_tflops": round(att_tflops, 2),
         "roofline": {"bound": "mfma", "kernel": "bank attention", "achieved": round(att_tflops, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": None},
+                     "traffic": measured_traffic()},
     }
     if args.copy_probe_mb:
         nbytes = args.copy_probe_mb << 20
         src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
         for _ in range(3):
-            dst.copy_(src)
+            torch.neg(src, out=dst)      # reads and writes nbytes each
         torch.cuda.synchronize()
         result["copy_probe_bytes"] = nbytes
     if not args.no_cpu_baseline:

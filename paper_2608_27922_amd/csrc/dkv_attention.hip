@@ -123,9 +123,10 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kFWaves = 4;
+constexpr int kFWaves = 8;
 constexpr int kFQ = 32 * kFWaves;  // queries per workgroup
 constexpr int kFK = 64;            // keys per tile
+constexpr int kFStages = 3;        // K/V tiles resident in LDS (2 in flight while 1 is used)
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -152,11 +153,13 @@ __device__ __forceinline__ int k_swz(int r, int c) { return c ^ (r % FCfg<D>::kC
 template <int D>
 __device__ __forceinline__ int v_swz(int r, int c) { return c ^ ((4 * (r % 4)) % FCfg<D>::kChunks); }
 
-// Issue the direct-to-LDS loads of one tile (rows [0, nvalid) of kbase/vbase;
+// Issue the direct-to-LDS loads of one K or V tile (rows [0, nvalid) of base;
 // rows beyond nvalid repeat the last real row so that every value is finite).
-template <int D>
-__device__ __forceinline__ void ftile_issue(const uint16_t *kbase, const uint16_t *vbase, int nvalid,
-                                            char *kbuf, char *vbuf) {
+// Lane i of a load writes 16 bytes at LDS offset 16 i of its 1 KB block, i.e.
+// physical chunk pc of row r; it fetches logical chunk swz(r, pc) (the XOR
+// swizzle is an involution, so logical chunk c lands at physical swz(r, c)).
+template <int D, bool kIsV>
+__device__ __forceinline__ void ftile_issue(const uint16_t *base, int nvalid, char *buf) {
   constexpr int RPL = FCfg<D>::kRowsPerLoad, CH = FCfg<D>::kChunks;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int rsub = l / CH, pc = l % CH;
@@ -165,20 +168,39 @@ __device__ __forceinline__ void ftile_issue(const uint16_t *kbase, const uint16_
     const int blk = wave * (FCfg<D>::kLoadsPerTile / kFWaves) + q;
     const int r = blk * RPL + rsub;
     const int rr = r < nvalid ? r : nvalid - 1;
-    __builtin_amdgcn_global_load_lds(kbase + (size_t)rr * D + 8 * k_swz<D>(r, pc),
-                                     (lds_void *)(kbuf + blk * 1024), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(vbase + (size_t)rr * D + 8 * v_swz<D>(r, pc),
-                                     (lds_void *)(vbuf + blk * 1024), 16, 0, 0);
+    const int cs = kIsV ? v_swz<D>(r, pc) : k_swz<D>(r, pc);
+    __builtin_amdgcn_global_load_lds(base + (size_t)rr * D + 8 * cs, (lds_void *)(buf + blk * 1024), 16, 0, 0);
   }
 }
 
+// Lazy softmax bound: the reference maximum is only raised when a lane's tile
+// sum of exp2 terms exceeds 2^16 (or is not finite), so every P stays below
+// 2^16 and the running sums stay far from overflow; the final division by l
+// removes the common factor exactly.
+constexpr float kLazyLimit = 65536.0f;
+
+// s_waitcnt immediate (gfx9 encoding): at most n vector-memory operations
+// outstanding and no LDS operation outstanding (expcnt left alone).
+constexpr int waitcnt_vm_lgkm0(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
+
+// Workgroup barrier for the K/V stages.  Each thread has already waited for
+// its own direct-to-LDS loads of the stage about to be read (and for its LDS
+// reads), so the barrier needs no memory fence; the "memory" clobber keeps
+// the compiler from moving LDS accesses across it, and leaving out the fence
+// keeps it from also waiting for the next stage's loads, which stay in flight.
+__device__ __forceinline__ void stage_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
 template <int D>
-__global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, const uint16_t *q, int nq,
+__global__ __launch_bounds__(64 * kFWaves, 1) void k_attn_mfma(dkv_bank bank, const uint16_t *q, int nq,
                                                                const uint16_t *wk, const uint16_t *wv, int nw,
                                                                uint16_t *out, float c, Geom g) {
   constexpr int KS = D / 16;   // K steps of S
   constexpr int DT = D / 32;   // dv tiles of O
   constexpr int RB = FCfg<D>::kRowBytes;
+  constexpr int TB = FCfg<D>::kTileBytes;
+  // direct-to-LDS loads per thread for one K + V tile
+  constexpr int kTileLoads = 2 * (FCfg<D>::kLoadsPerTile / kFWaves);
+  static_assert(FCfg<D>::kLoadsPerTile % kFWaves == 0, "tile loads must split evenly over the waves");
   const int b = blockIdx.y;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
   const int M = clampi(bank.budget[b], 0, g.Mcap);
@@ -186,8 +208,11 @@ __global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, co
   const size_t rb = (size_t)b * g.Mcap, wb = (size_t)b * nw;
   const uint16_t *bk = static_cast<const uint16_t *>(bank.k);
   const uint16_t *bv = static_cast<const uint16_t *>(bank.v);
-  __shared__ __attribute__((aligned(1024))) char kbuf[2][FCfg<D>::kTileBytes];
-  __shared__ __attribute__((aligned(1024))) char vbuf[2][FCfg<D>::kTileBytes];
+  // One LDS array per stage (not one indexed array): with the stage known at
+  // compile time the compiler can tell that reads of one stage never wait for
+  // the direct-to-LDS loads still filling the others.
+  __shared__ __attribute__((aligned(1024))) char k0[TB], k1[TB], k2[TB];
+  __shared__ __attribute__((aligned(1024))) char v0[TB], v1[TB], v2[TB];
 
   const int qi = blockIdx.x * kFQ + wave * 32 + n;
   const bool qv = qi < nq;
@@ -203,42 +228,37 @@ __global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, co
 #pragma unroll
   for (int t = 0; t < DT; ++t) o[t] = f32x16{};
   float mrun = -INFINITY, lrun = 0.0f;
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
 
   // Tiles never straddle the bank/window boundary: ceil(m/64) bank tiles, then
   // ceil(nw/64) window tiles, so every tile has one (scalar) base pointer.
   const int nt0 = (m + kFK - 1) / kFK;
   const int nt = nt0 + (nw + kFK - 1) / kFK;
-  auto tile_src = [&](int t, const uint16_t *&kp, const uint16_t *&vp, int &nv) {
+  auto nvalid_of = [&](int t) { return t < nt0 ? min(kFK, m - t * kFK) : min(kFK, nw - (t - nt0) * kFK); };
+  auto issue = [&](int t, char *kd, char *vd) {
+    if (t >= nt) return;
+    const int nv = nvalid_of(t);
     if (t < nt0) {
-      kp = bk + (rb + (size_t)t * kFK) * D;
-      vp = bv + (rb + (size_t)t * kFK) * D;
-      nv = min(kFK, m - t * kFK);
+      ftile_issue<D, false>(bk + (rb + (size_t)t * kFK) * D, nv, kd);
+      ftile_issue<D, true>(bv + (rb + (size_t)t * kFK) * D, nv, vd);
     } else {
-      const int tw = t - nt0;
-      kp = wk + (wb + (size_t)tw * kFK) * D;
-      vp = wv + (wb + (size_t)tw * kFK) * D;
-      nv = min(kFK, nw - tw * kFK);
+      const size_t r0 = wb + (size_t)(t - nt0) * kFK;
+      ftile_issue<D, false>(wk + r0 * D, nv, kd);
+      ftile_issue<D, true>(wv + r0 * D, nv, vd);
     }
   };
-  const uint16_t *kp, *vp;
-  int nv_cur = 0, nv_next = 0;
-  if (nt > 0) {
-    tile_src(0, kp, vp, nv_cur);
-    ftile_issue<D>(kp, vp, nv_cur, kbuf[0], vbuf[0]);
-  }
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
   // transposed V read: lane group gq = l / 16 (h = gq / 2), member cq = l % 16
   const int gq = l >> 4, cq = l & 15;
-  for (int t = 0; t < nt; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < nt) {
-      tile_src(t + 1, kp, vp, nv_next);
-      ftile_issue<D>(kp, vp, nv_next, kbuf[cur ^ 1], vbuf[cur ^ 1]);
-    }
-    const char *kt = kbuf[cur];
-    const char *vtile = vbuf[cur];
-    // S^T for two 32-key halves
+
+  // Tile t lives in stage t % 3.  Wait for its loads (the loads of tile t + 1
+  // may stay in flight), then at the barrier every wave has finished tile
+  // t - 1, so its stage receives tile t + 2.  Then S^T = K Q^T, softmax
+  // update, O^T += V^T P^T.
+  auto step = [&](int t, const char *kt, const char *vtile, char *kn, char *vn) {
+    if (t + 1 < nt) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kTileLoads));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+    stage_barrier();
+    issue(t + 2, kn, vn);
     f32x16 sc[2];
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
@@ -252,7 +272,7 @@ __global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, co
       for (int kk = 0; kk < KS; ++kk) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], qf[kk], acc, 0, 0, 0);
       sc[sub] = acc;
     }
-    const int nvalid = nv_cur;
+    const int nvalid = nvalid_of(t);
     if (nvalid < kFK) {
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub)
@@ -260,19 +280,31 @@ __global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, co
         for (int i = 0; i < 16; ++i)
           if (32 * sub + 8 * (i >> 2) + 4 * h + (i & 3) >= nvalid) sc[sub][i] = -INFINITY;
     }
-    float tmax = sc[0][0];
+    uint32_t pb[2][8];
+    float psum = 0.0f;
+    auto exps = [&](float moff) {
+      float ps[2] = {0.0f, 0.0f};
 #pragma unroll
-    for (int i = 1; i < 16; ++i) tmax = fmaxf(tmax, sc[0][i]);
+      for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, sc[1][i]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    // Lazy rescaling: the reference maximum only moves when a score exceeds it
-    // by more than 2^8 in the exp2 domain, so P stays within [0, 256] and the
-    // accumulated O and l are rescaled rarely (exact: the final division by l
-    // removes the common factor).
-    const bool grow = tmax * c > mrun * c + 8.0f;
-    if (__any(grow)) {
-      const float mnew = grow ? tmax : mrun;
+        for (int i = 0; i < 16; i += 2) {
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[sub][i], c, moff));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[sub][i + 1], c, moff));
+          pb[sub][i >> 1] = pack_bf16x2(p0, p1);
+          // row sum of the bf16 weights actually multiplied into O
+          ps[sub] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, pb[sub][i >> 1]), ones, ps[sub], false);
+        }
+      psum = ps[0] + ps[1];
+    };
+    exps(-mrun * c);
+    if (__any(!(psum <= kLazyLimit))) {
+      float tmax = sc[0][0];
+#pragma unroll
+      for (int i = 1; i < 16; ++i) tmax = fmaxf(tmax, sc[0][i]);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) tmax = fmaxf(tmax, sc[1][i]);
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      const float mnew = fmaxf(mrun, tmax);
       const float corr = __builtin_amdgcn_exp2f((mrun - mnew) * c);
       mrun = mnew;
       lrun *= corr;
@@ -280,22 +312,9 @@ __global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, co
       for (int t2 = 0; t2 < DT; ++t2)
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[t2][i] *= corr;
-    }
-    const float moff = -mrun * c;
-    float psum = 0.0f;
-    uint32_t pb[2][8];
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-#pragma unroll
-      for (int i = 0; i < 16; i += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[sub][i], c, moff));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[sub][i + 1], c, moff));
-        psum += p0 + p1;
-        pb[sub][i >> 1] = pack_bf16x2(p0, p1);
-      }
+      exps(-mrun * c);
     }
     lrun += psum;
-    // O^T += V^T P^T
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
 #pragma unroll
@@ -317,9 +336,14 @@ __global__ __launch_bounds__(64 * kFWaves, 2) void k_attn_mfma(dkv_bank bank, co
         }
       }
     }
-    nv_cur = nv_next;
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+  };
+
+  issue(0, k0, v0);
+  issue(1, k1, v1);
+  for (int t = 0; t < nt; t += 3) {
+    step(t, k0, v0, k2, v2);
+    if (t + 1 < nt) step(t + 1, k1, v1, k0, v0);
+    if (t + 2 < nt) step(t + 2, k2, v2, k1, v1);
   }
   const float ltot = lrun + __shfl_xor(lrun, 32, 64);
   if (!qv) return;

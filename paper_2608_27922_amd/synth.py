@@ -213,3 +213,28 @@ def single_update_case(cfg: Config, layer: int = 0, seed: int = 0, heads: Option
 def random_grid_keys(rng: np.random.Generator, shape, scale: float = 0.5) -> np.ndarray:
     """Generic grid keys for small tests (not a config workload)."""
     return snap_keys(scale * rng.standard_normal(shape))
+
+
+def torch_layer_block(cfg: Config, layer: int, t: int, n: int, device, seed: int = 0):
+    """Keys and values of one block for every head of one layer, drawn on the GPU.
+
+    Same recipe as HeadStream (unit-norm centres fixed per (layer, head), tokens
+    = centre + 0.3 N(0, I), keys snapped to the grid, values rounded to the
+    storage dtype) from a seeded torch generator, without the drift / recurrence
+    schedule.  Used to fill the layers that are not compared with the oracle in
+    full-size runs, where generating 360 banks on the host would dominate."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed((seed * 1_000_003 + cfg.seed_id * 10_007 + layer) & 0x7FFFFFFF)
+    H, d = cfg.heads, cfg.d
+    c = torch.randn(H, cfg.clusters, d, generator=gen, device=device)
+    c = c / c.norm(dim=-1, keepdim=True)
+    gen.manual_seed((seed * 1_000_003 + cfg.seed_id * 10_007 + layer * 131 + 7 * t + 1) & 0x7FFFFFFF)
+    out = []
+    for _role in range(2):
+        z = torch.randint(0, cfg.clusters, (H, n), generator=gen, device=device)
+        x = torch.gather(c, 1, z[..., None].expand(H, n, d)) + 0.3 * torch.randn(H, n, d, generator=gen, device=device)
+        out.append(x)
+    k = (torch.clamp(torch.round(out[0] * GRID), -GRID_MAX, GRID_MAX) / GRID)
+    dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    return k.to(dt).contiguous(), out[1].to(dt).contiguous()

@@ -1,0 +1,206 @@
+"""Full-size runs of the three 30-layer x 12-head rollout workloads: all 360 banks
+updated by one launch per block, as the library is used.  Needs an MI355X.
+
+Parity with the oracle: one sampled layer of each run is drawn from the seeded
+input generator, and after every block the device results for its 12 banks
+(candidate order, scores, first crossings, projected densities, eviction and
+admission lists, and the committed bank bytes) must hash to the digests the
+oracle wrote for the same inputs (tests/golden/make_rollout_digests.py; the
+oracle needs minutes per block at these budgets, so it is not rerun here).
+After the last block, sampled query rows of the bank attention are compared
+with the oracle's fp64 attention within the bf16 tolerance.
+
+Properties checked on every one of the 360 banks after every block, at full
+size: occupancy within budget; r* shared inside each layer; the eviction count
+equals max(0, m + r* - M); the order sorts the score keys; the admitted set is
+the first r* of the order; every violator at r* is evicted and every other
+evicted state is at least as dense as every kept one; the violation flags agree
+with the projected densities; the maintained density equals the density
+recomputed from scratch; the growth bound rho < tau b; the baseline floor; and
+every retained token carries the key and value it was admitted with.
+The 29 layers that are not compared with the oracle draw their tokens on the
+device from a seeded torch generator.
+"""
+
+import json
+import os
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+from golden.make_rollout_digests import RUNS, attention_rows, digest, layer_block  # noqa: E402
+from gpu_util import attention_error, dev, host  # noqa: E402
+from paper_2608_27922_amd import api, synth  # noqa: E402
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    api.lib()
+
+
+def _bank_entry(bank, out, b, m_before, n):
+    m = int(bank.occupancy[b])
+    ne, na = int(out.n_evicted[b]), int(out.n_admitted[b])
+    i64 = lambda t: t.cpu().numpy().astype(np.int64)
+    return {
+        "m_before": m_before, "m_after": m, "n_evicted": ne, "n_admitted": na,
+        "order": digest(out.order[b, :n].cpu().numpy(), np.int32),
+        "score_q": digest(i64(out.score_q[b, :n]), np.int64),
+        "first_cross": digest(out.first_cross[b, :m_before].cpu().numpy(), np.int32),
+        "rho_tilde": digest(i64(out.rho_tilde[b, :m_before]), np.int64),
+        "evicted": digest(out.evicted[b, :ne].cpu().numpy(), np.int32),
+        "admitted": digest(out.admitted[b, :na].cpu().numpy(), np.int32),
+        "prov": digest(i64(bank.prov[b, :m]), np.int64), "rho": digest(i64(bank.rho[b, :m]), np.int64),
+        "base": digest(i64(bank.base[b, :m]), np.int64),
+        "knorm": digest(bank.knorm[b, :m].cpu().numpy(), np.float32),
+        "k": digest(host(bank.k[b, :m]), np.float32), "v": digest(host(bank.v[b, :m]), np.float32),
+    }
+
+
+def _properties(bank, out, prm, m_prev, base_prev, hist_k, hist_v, gs, N, ctx):
+    B, Mcap = bank.B, bank.Mcap
+    ar = torch.arange(Mcap, device="cuda")
+    occ = bank.occupancy.long()
+    budget = bank.budget.long()
+    rs = out.r_star.long().repeat_interleave(gs)
+    assert torch.all(occ <= budget), f"{ctx}: occupancy above budget"
+    assert torch.equal(out.n_admitted.long(), rs), f"{ctx}: admitted count differs from the group's r*"
+    e = torch.clamp(m_prev + rs - budget, min=0)
+    assert torch.equal(out.n_evicted.long(), e), f"{ctx}: eviction count differs from max(0, m + r* - M)"
+    assert torch.equal(occ, m_prev + rs - e), f"{ctx}: occupancy differs from m + r* - e"
+
+    # order sorts the score keys (S << 13 | x) ascending; empty banks keep source order
+    src = torch.arange(N, device="cuda")
+    keys = (out.score_q[:, :N] << 13) | src
+    sk = torch.gather(keys, 1, out.order[:, :N].long())
+    assert bool(torch.all(sk[:, 1:] > sk[:, :-1])), f"{ctx}: order does not sort the score keys"
+    assert torch.equal(torch.sort(out.order[:, :N], dim=1).values.long(), src.expand(B, N)), f"{ctx}: order not a permutation"
+    # admitted set = first r* of the order
+    first = torch.where(src[None, :] < rs[:, None], out.order[:, :N].long(), N)
+    adm = torch.where(src[None, :] < rs[:, None], out.admitted[:, :N].long(), N)
+    assert torch.equal(torch.sort(first, 1).values, adm), f"{ctx}: admitted set is not the order's prefix"
+
+    # eviction rule on the old slots
+    old = ar[None, :] < m_prev[:, None]
+    viol_fc = (out.first_cross.long() <= rs[:, None]) & old
+    ev_mask = torch.zeros(B, Mcap + 1, dtype=torch.bool, device="cuda")
+    ev_idx = torch.where(ar[None, :] < out.n_evicted[:, None].long(), out.evicted.long(), Mcap)
+    ev_mask.scatter_(1, ev_idx, True)
+    ev_mask = ev_mask[:, :Mcap]
+    assert bool(torch.all(ev_mask[viol_fc])), f"{ctx}: a violator at r* was not evicted"
+    kept_nv = old & ~ev_mask & ~viol_fc
+    fill = ev_mask & ~viol_fc
+    neg = torch.iinfo(torch.int64).min
+    kept_max = torch.where(kept_nv, out.rho_tilde, torch.full_like(out.rho_tilde, neg)).amax(1)
+    fill_min = torch.where(fill, out.rho_tilde, torch.full_like(out.rho_tilde, torch.iinfo(torch.int64).max)).amin(1)
+    assert bool(torch.all(fill_min >= kept_max)), f"{ctx}: a kept state is denser than an evicted one"
+
+    occupied = ar[None, :] < occ[:, None]
+    rho, base = bank.rho, bank.base
+    assert bool(torch.all(base[occupied] >= prm.delta_q)), f"{ctx}: baseline below delta"
+    assert bool(torch.all((rho[occupied] << prm.tau_log2_den) < prm.tau_num * base[occupied])), \
+        f"{ctx}: growth bound rho < tau b violated"
+    # the first crossings (prefix-scan kernels) agree with the projected densities at r*
+    # (fix-up kernel): violation at r* <=> 2^k rho~ >= T b
+    viol_rt = ((out.rho_tilde << prm.tau_log2_den) >= prm.tau_num * base_prev) & old
+    assert torch.equal(viol_rt, viol_fc), f"{ctx}: first crossings disagree with the projected densities"
+    # exact maintenance: maintained rho == density recomputed from scratch
+    z = torch.zeros(B, 1, bank.d, dtype=bank.dtype, device="cuda")
+    _, _, dens = api.score(bank, z, z, prm, want_q=False, want_f32=False, want_density=True)
+    assert torch.equal(dens[occupied], rho[occupied]), f"{ctx}: maintained density differs from recomputation"
+    # provenance unique; each retained token holds the key/value it was admitted with
+    prov = torch.where(occupied, bank.prov, torch.full_like(bank.prov, -1))
+    sp = torch.sort(prov, 1).values
+    dup = (sp[:, 1:] == sp[:, :-1]) & (sp[:, 1:] >= 0)
+    assert not bool(torch.any(dup)), f"{ctx}: duplicate provenance inside a bank"
+    blk = (bank.prov >> 32)[occupied]
+    sidx = (bank.prov & 0xFFFFFFFF)[occupied]
+    bidx = torch.arange(B, device="cuda")[:, None].expand(B, Mcap)[occupied]
+    assert bool(torch.all((blk >= 0) & (blk < len(hist_k)) & (sidx < N))), f"{ctx}: provenance out of range"
+    hk = torch.stack(hist_k)   # [T, B, N, d]
+    hv = torch.stack(hist_v)
+    assert torch.equal(bank.k[occupied], hk[blk, bidx, sidx]), f"{ctx}: a retained key differs from its admitted key"
+    assert torch.equal(bank.v[occupied], hv[blk, bidx, sidx]), f"{ctx}: a retained value differs from its admitted value"
+
+
+@pytest.mark.parametrize("name", list(RUNS))
+def test_full_size_workload(name):
+    path = os.path.join(GOLDEN, f"rollout_{name}.json")
+    if not os.path.exists(path):
+        pytest.skip(f"oracle digests for {name} not generated")
+    with open(path) as f:
+        gold = json.load(f)
+    ref_att = np.load(os.path.join(GOLDEN, f"rollout_{name}_attention.npy"))
+    cfg = synth.WORKLOADS[name]
+    blocks, layer, att_heads = gold["blocks"], gold["layer"], gold["attention_heads"]
+    H, d, N, gs = cfg.heads, cfg.d, cfg.n_cand, cfg.group_size
+    B = cfg.layers * H
+    print(f"workload {name}: {B} banks, {blocks} blocks, sampled layer {layer}", flush=True)
+    budgets = synth.budgets(cfg)
+    assert [int(x) for x in budgets[layer * H:(layer + 1) * H]] == gold["budgets"]
+    prm = api.Params(sigma2_log2=cfg.sigma2_log2)
+    bank = api.Bank(B, int(budgets.max()), d, dtype=torch.bfloat16, group_size=gs,
+                    budget=torch.from_numpy(budgets))
+    ws = api.alloc_workspace(bank, N)
+    streams = [synth.HeadStream(cfg, layer, h) for h in range(H)]
+    hist_k, hist_v = [], []
+    sl = slice(layer * H, (layer + 1) * H)
+    for t in range(blocks):
+        K = torch.empty(B, N, d, dtype=torch.bfloat16, device="cuda")
+        V = torch.empty_like(K)
+        for L in range(cfg.layers):
+            if L != layer:
+                K[L * H:(L + 1) * H], V[L * H:(L + 1) * H] = synth.torch_layer_block(cfg, L, t, N, "cuda")
+        Kl, Vl = layer_block(cfg, streams, t)
+        K[sl], V[sl] = dev(Kl, "bf16"), dev(Vl, "bf16")
+        hist_k.append(K)
+        hist_v.append(V)
+        m_prev = bank.occupancy.long().clone()
+        base_prev = bank.base.clone()
+        out = api.UpdateOut(bank, N, trace=True)
+        api.update_bank(bank, K, V, t, prm, workspace=ws, out=out)
+        torch.cuda.synchronize()
+        ctx = f"{name} block {t}"
+        step = gold["steps"][t]
+        for g, rs in enumerate(step["r_star"]):
+            assert int(out.r_star[layer * H // gs + g]) == rs, f"{ctx}: r* of group {g}"
+        for h in range(H):
+            got = _bank_entry(bank, out, layer * H + h, int(m_prev[layer * H + h]), N)
+            want = step["heads"][h]
+            bad = [k for k in want if got[k] != want[k]]
+            assert not bad, f"{ctx} head {h}: differs from the oracle in {bad}"
+        _properties(bank, out, prm, m_prev, base_prev, hist_k, hist_v, gs, N, ctx)
+        print(f"  block {t}: r* {step['r_star'][:3]} occupancy {gold['steps'][t]['heads'][0]['m_after']} ok",
+              flush=True)
+    q = torch.empty(B, cfg.n_query, d, dtype=torch.bfloat16, device="cuda")
+    wk = torch.empty(B, cfg.n_window, d, dtype=torch.bfloat16, device="cuda")
+    for L in range(cfg.layers):
+        if L != layer:
+            q[L * H:(L + 1) * H], _ = synth.torch_layer_block(cfg, L, blocks, cfg.n_query, "cuda")
+    wk_all, wv_all = [], []
+    for L in range(cfg.layers):
+        k_, v_ = synth.torch_layer_block(cfg, L, blocks + 1, cfg.n_window, "cuda")
+        wk_all.append(k_)
+        wv_all.append(v_)
+    wk, wv = torch.cat(wk_all).contiguous(), torch.cat(wv_all).contiguous()
+    q[sl] = dev(np.stack([s.queries(blocks) for s in streams]), "bf16")
+    wk[sl] = dev(np.stack([s.keys(blocks, cfg.n_window) for s in streams]), "bf16")
+    wv[sl] = dev(np.stack([s.values(blocks, cfg.n_window) for s in streams]), "bf16")
+    o = api.bank_attention(bank, q, wk, wv)
+    rows = torch.from_numpy(attention_rows(cfg.n_query)).cuda()
+    worst = 0.0
+    for i, h in enumerate(att_heads):
+        got = host(o[layer * H + h].index_select(0, rows))
+        worst = max(worst, attention_error(got, ref_att[i]))
+    assert torch.isfinite(o.float()).all(), "non-finite attention output"
+    print(f"  attention: max row-normalised error {worst:.3e} over {len(att_heads)} heads x {rows.numel()} rows",
+          flush=True)
+    assert worst <= 2e-2
