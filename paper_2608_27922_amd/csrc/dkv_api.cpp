@@ -14,7 +14,8 @@ static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base) {
   size_t off = 0;
   const size_t Bz = (size_t)B, Mz = (size_t)Mcap, Nz = (size_t)(N > 0 ? N : 1);
-  const int nck = (N + kCkStride - 1) / kCkStride;
+  // chunk sums per row, padded to a multiple of 4 so that rows are 16-byte aligned
+  const int nck = ((N + kCkStride - 1) / kCkStride + 3) / 4 * 4;
   auto take = [&](size_t bytes) -> char * {
     char *p = base ? base + off : nullptr;
     off += align256(bytes);
@@ -36,7 +37,7 @@ size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, cha
   w.order = (int32_t *)take(Bz * Nz * 4);
   w.rank = (int32_t *)take(Bz * Nz * 4);
   w.first = (int32_t *)take(Bz * Mz * 4);
-  w.ck = (uint32_t *)take(Bz * Mz * (size_t)(nck > 0 ? nck : 1) * 4);
+  w.ck = (uint32_t *)take(Bz * Mz * (size_t)(nck > 0 ? nck : 4) * 4);
   w.rho_t = (int64_t *)take(Bz * Mz * 8);
   w.dest = (int32_t *)take(Bz * Mz * 4);
   w.ev_list = (int32_t *)take(Bz * Mz * 4);
@@ -58,7 +59,7 @@ size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, cha
   const int npad = ((N > 0 ? N : 1) + 511) / 512 * 512;
   w.skeys = (uint64_t *)take(Bz * (size_t)npad * 8);
   w.npad = npad;
-  w.nck = nck > 0 ? nck : 1;
+  w.nck = nck > 0 ? nck : 4;
   if (ws) *ws = w;
   return off;
 }

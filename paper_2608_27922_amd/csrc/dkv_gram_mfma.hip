@@ -5,7 +5,7 @@
 //
 //   k_score_mfma   rows = candidates, columns = bank states:
 //                  S_x = sum_i RNE(w_ix bs_i), Wcol_x = sum_i W_ix  (Eq. 6)
-//   k_rowsum_mfma  row sums: per-256-candidate chunk sums over the ordered
+//   k_rowsum_mfma  row sums: per-64-candidate chunk sums over the ordered
 //                  candidates (the prefix checkpoints of Eqs. 8-9), the r*
 //                  fix-up, the exact maintenance (Supp. C) and the
 //                  from-scratch bank density (Eq. 3)
@@ -211,7 +211,7 @@ __device__ __forceinline__ uint32_t lane_wsum(const f32x16 &u, int nvalid, int h
 constexpr int kColsPerSplit = 1024;
 
 template <int D, int P, bool FOLD>
-__global__ __launch_bounds__(64 * kWaves) void k_score_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
+__global__ __launch_bounds__(64 * kWaves, 2) void k_score_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
                                                            Workspace ws) {
   const int b = blockIdx.z;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
@@ -325,10 +325,10 @@ __global__ __launch_bounds__(64 * kWaves) void k_score_mfma(dkv_bank bank, const
 // ---------------------------------------------------------------------------
 enum RowSumMode { RS_CHUNK = 0, RS_FIXUP = 1, RS_SURV_EV = 2, RS_ADM_BASE = 3, RS_ADM_MUT = 4, RS_DENSITY = 5 };
 
-constexpr int kChunksPerSplit = 4;   // RS_CHUNK: 4 x 256 ordered candidates per workgroup
+constexpr int kChunksPerSplit = 1024 / kCkStride;   // RS_CHUNK: 1024 ordered candidates per workgroup
 
 template <int D, int P, int MODE, bool FOLD>
-__global__ __launch_bounds__(64 * kWaves) void k_rowsum_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
+__global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
                                                             Workspace ws, int64_t *out) {
   const int b = blockIdx.z;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
@@ -464,14 +464,25 @@ __global__ __launch_bounds__(64 * kWaves) void k_rowsum_mfma(dkv_bank bank, cons
     __syncthreads();
   }
   if constexpr (MODE == RS_CHUNK) return;
-  const uint64_t tot = S64 + __shfl_xor(S64, 32, 64);
+  uint64_t tot = S64;
+  if constexpr (MODE == RS_FIXUP) {
+    // plus the whole chunks before r*: the two half-waves sum alternate 4-chunk groups
+    const int full = rs / kCkStride;
+    if (rv) {
+      const uint4 *ckr = reinterpret_cast<const uint4 *>(ws.ck + (rb + v) * ws.nck);
+      for (int c4 = h; 4 * c4 < full; c4 += 2) {
+        const uint4 q = ckr[c4];
+        const int c = 4 * c4;
+        tot += (uint64_t)q.x + (c + 1 < full ? (uint64_t)q.y : 0) + (c + 2 < full ? (uint64_t)q.z : 0) +
+               (c + 3 < full ? (uint64_t)q.w : 0);
+      }
+    }
+  }
+  tot += __shfl_xor(tot, 32, 64);
   if (!rv || h != 0) return;
   if constexpr (MODE == RS_FIXUP) {
-    int64_t Pc = (int64_t)tot;
-    const int full = rs / kCkStride;
     const size_t row = rb + v;
-    for (int q = 0; q < full; ++q) Pc += ws.ck[row * ws.nck + q];
-    const int64_t rt = bank.rho[row] + Pc;
+    const int64_t rt = bank.rho[row] + (int64_t)tot;
     ws.rho_t[row] = rt;
     if (out) out[row] = rt;
   } else {
@@ -482,10 +493,10 @@ __global__ __launch_bounds__(64 * kWaves) void k_rowsum_mfma(dkv_bank bank, cons
 
 // ---------------------------------------------------------------------------
 // First violating prefix length of every bank state (Eqs. 8-9).
-// k_cross_scan: thread per state; the first 256-candidate chunk whose sum
+// k_cross_scan: thread per state; the first 64-candidate chunk whose sum
 // lifts the prefix density to tau b.  States that never reach it get R + 1;
-// the others are listed for k_cross_find, which re-walks that one chunk (4
-// ordered candidates per lane, same binary32 weights) for the exact length.
+// the others are listed for k_cross_find, which re-walks that one chunk (one
+// ordered candidate per lane, same binary32 weights) for the exact length.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_cross_scan(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
   const int b = blockIdx.y, i = blockIdx.x * 256 + threadIdx.x;
@@ -499,16 +510,27 @@ __global__ __launch_bounds__(256) void k_cross_scan(dkv_bank bank, Geom g, Prm p
     first = 0;
   } else {
     const int nch = (R + kCkStride - 1) / kCkStride;
+    const uint4 *ckr = reinterpret_cast<const uint4 *>(ws.ck + row * ws.nck);
+    const int n4 = (nch + 3) / 4;
     int64_t P = 0;
-    for (int c = 0; c < nch; ++c) {
-      const int64_t v = ws.ck[row * ws.nck + c];
-      if (P + v >= thr) {
-        const int k = atomicAdd(&ws.xcount[b], 1);
-        ws.xlist[rb + k] = i | (c << 16);
-        ws.xbefore[rb + k] = P;
-        return;  // first written by k_cross_find
+    // batches of 8 x 4 chunk sums, all loads of a batch in flight together
+    for (int c8 = 0; c8 < n4; c8 += 8) {
+      uint4 q[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) q[e] = c8 + e < n4 ? ckr[c8 + e] : uint4{0, 0, 0, 0};
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        const int c = 4 * c8 + e;
+        const uint32_t v = e % 4 == 0 ? q[e / 4].x : e % 4 == 1 ? q[e / 4].y : e % 4 == 2 ? q[e / 4].z : q[e / 4].w;
+        if (c >= nch) break;
+        if (P + v >= thr) {
+          const int k = atomicAdd(&ws.xcount[b], 1);
+          ws.xlist[rb + k] = i | (c << 16);
+          ws.xbefore[rb + k] = P;
+          return;  // first written by k_cross_find
+        }
+        P += v;
       }
-      P += v;
     }
   }
   ws.first[row] = first;
@@ -533,55 +555,35 @@ __global__ __launch_bounds__(256) void k_cross_find(dkv_bank bank, Geom g, Prm p
     const int64_t thr = lim - bank.rho[row];
     const uint16_t *rk = static_cast<const uint16_t *>(bank.k) + row * D;
     const float nr = bank.knorm[row];
-    const int col0 = c * kCkStride + 4 * l;
-    uint32_t w4[4];
+    // one ordered candidate per lane: column c * 64 + l
+    static_assert(kCkStride == 64, "one column per lane");
+    const int col = c * kCkStride + l;
+    uint32_t W = 0;
+    if (col < R) {
+      const uint16_t *ckey = ws.sk + (nb + col) * D;
+      float acc = 0.0f;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int col = col0 + q;
-      uint32_t W = 0;
-      if (col < R) {
-        const uint16_t *ckey = ws.sk + (nb + col) * D;
-        float acc = 0.0f;
+      for (int j = 0; j < D; j += 8) {
+        const u32x4 a = *reinterpret_cast<const u32x4 *>(rk + j);
+        const u32x4 bb = *reinterpret_cast<const u32x4 *>(ckey + j);
 #pragma unroll
-        for (int j = 0; j < D; j += 8) {
-          const u32x4 a = *reinterpret_cast<const u32x4 *>(rk + j);
-          const u32x4 bb = *reinterpret_cast<const u32x4 *>(ckey + j);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            acc = __builtin_fmaf(__uint_as_float(a[e] << 16), __uint_as_float(bb[e] << 16), acc);
-            acc = __builtin_fmaf(__uint_as_float(a[e] & 0xFFFF0000u), __uint_as_float(bb[e] & 0xFFFF0000u), acc);
-          }
+        for (int e = 0; e < 4; ++e) {
+          acc = __builtin_fmaf(__uint_as_float(a[e] << 16), __uint_as_float(bb[e] << 16), acc);
+          acc = __builtin_fmaf(__uint_as_float(a[e] & 0xFFFF0000u), __uint_as_float(bb[e] & 0xFFFF0000u), acc);
         }
-        const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
-        W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
       }
-      w4[q] = W;
+      const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
+      W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
     }
-    uint32_t loc[4];
-    loc[0] = w4[0];
-    loc[1] = loc[0] + w4[1];
-    loc[2] = loc[1] + w4[2];
-    loc[3] = loc[2] + w4[3];
-    uint32_t incl = loc[3];
+    uint32_t incl = W;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
       const uint32_t y = __shfl_up(incl, o, 64);
       if (l >= o) incl += y;
     }
-    const int64_t base_l = before + (int64_t)(incl - loc[3]);
-    int qf = -1;
-#pragma unroll
-    for (int q = 3; q >= 0; --q)
-      if (base_l + (int64_t)loc[q] >= thr) qf = q;
-    const unsigned long long hl = __ballot(qf >= 0);
-    int first;
-    if (hl != 0) {
-      const int lf = __ffsll(hl) - 1;
-      const int qsel = __shfl(qf, lf, 64);
-      first = c * kCkStride + 4 * lf + qsel + 1;
-    } else {
-      first = min(R, (c + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
-    }
+    const unsigned long long hl = __ballot(before + (int64_t)incl >= thr);
+    const int first = hl != 0 ? c * kCkStride + (__ffsll(hl) - 1) + 1
+                              : min(R, (c + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
     if (l == 0) {
       ws.first[row] = first;
       if (out_first) out_first[row] = first;

@@ -11,7 +11,7 @@ namespace dkv {
 
 constexpr uint32_t kQ23 = 1u << 23;          // weight 1.0 in fixed point
 constexpr uint32_t kMagic = 0x4B000000u;     // bit pattern of 2^23 as binary32
-constexpr int kCkStride = 256;               // prefix checkpoint spacing (candidates)
+constexpr int kCkStride = 64;                // prefix checkpoint spacing (candidates)
 constexpr int kSortMax = 8192;               // padded sort size (N <= 8191)
 
 // ---------------------------------------------------------------------------
@@ -33,7 +33,7 @@ struct Workspace {
   int32_t *order;      // [B, N]   pi
   int32_t *rank;       // [B, N]   position of x in pi
   int32_t *first;      // [B, Mcap] first crossing prefix length
-  uint32_t *ck;        // [B, Mcap, nck] prefix sums over each 256-candidate tile
+  uint32_t *ck;        // [B, Mcap, nck] sums over each kCkStride-candidate chunk of the order
   int64_t *rho_t;      // [B, Mcap] rho + P(r*)
   int32_t *dest;       // [B, Mcap] final slot of each pre-update slot, -1 if evicted
   int32_t *ev_list;    // [B, Mcap] evicted slots ascending

@@ -546,6 +546,13 @@ __global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspac
   int nv;
   (void)block_excl_scan(nv_local, &nv, tmp);
   int need = e - nv;
+  if (need > 0 && need >= m - nv) {
+    // every non-violator is evicted too (e = m): no ranking needed
+    for (int i = threadIdx.x; i < m; i += kBig)
+      if (st[i] == ST_CAND) st[i] = ST_SEL;
+    need = 0;
+    __syncthreads();
+  }
   if (need > 0) {
     for (int pass = 0; pass < 15; ++pass) {
       for (int t = threadIdx.x; t < 256; t += kBig) hist[t] = 0;
