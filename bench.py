@@ -7,9 +7,9 @@ attention of the next block's queries over the retained bank plus the local
 window.  Workload (default): one layer x 12 heads, d = 128, bf16, per-head
 budget 4,680, banks start full (built by the empty-bank rule), one incoming
 segment of 4,680 candidates with 30% near-duplicates, 4,680 queries over
-bank + a 4,680-token window.  Every step restores the pre-update bank with a
-device-to-device copy (inside the timed region) so that all steps do the same
-work.
+bank + a 4,680-token window.  Every step restores the pre-update bank with one
+device-to-device copy of the packed bank state (inside the timed region) so
+that all steps do the same work.
 
 Prints one JSON line.  value = candidate tokens per second per layer-head for
 the whole step (update + attention); the update-only rate and the attention
@@ -114,12 +114,12 @@ def main():
     ws = api.alloc_workspace(bank, max(N, cfg.budget))
     api.update_bank(bank, init_k, init_v, 0, prm, workspace=ws)   # starts full (empty-bank rule)
     torch.cuda.synchronize()
-    snap = bank.state_dict()
+    snap = bank.snapshot()
     out = torch.empty_like(q)
     stream = torch.cuda.current_stream()
 
     def step(ev=None):
-        bank.load_state_dict(snap)
+        bank.restore(snap)
         if ev is not None:
             ev[0].record(stream)
         api.update_bank(bank, seg_k, seg_v, 1, prm, workspace=ws)

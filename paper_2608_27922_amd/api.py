@@ -118,23 +118,36 @@ def _dtype_code(dt: torch.dtype) -> int:
 
 
 class Bank:
-    """Device state of B = num_banks (layer, head) banks, row stride `capacity`."""
+    """Device state of B = num_banks (layer, head) banks, row stride `capacity`.
+
+    All state tensors are views into one device allocation (256-byte aligned
+    sections), so a whole-bank checkpoint is a single copy (snapshot/restore)."""
+
+    _FIELDS = ("k", "v", "knorm", "rho", "base", "prov", "occupancy", "budget")
 
     def __init__(self, num_banks: int, capacity: int, head_dim: int, dtype=torch.bfloat16,
                  group_size: int = 1, budget=None, device="cuda"):
         self.B, self.Mcap, self.d, self.gs = num_banks, capacity, head_dim, group_size
         self.dtype = dtype
         dev = torch.device(device)
-        self.k = torch.zeros(num_banks, capacity, head_dim, dtype=dtype, device=dev)
-        self.v = torch.zeros_like(self.k)
-        self.knorm = torch.zeros(num_banks, capacity, dtype=torch.float32, device=dev)
-        self.rho = torch.zeros(num_banks, capacity, dtype=torch.int64, device=dev)
-        self.base = torch.zeros_like(self.rho)
-        self.prov = torch.zeros_like(self.rho)
-        self.occupancy = torch.zeros(num_banks, dtype=torch.int32, device=dev)
+        B, M, d = num_banks, capacity, head_dim
+        layout = [("k", dtype, (B, M, d)), ("v", dtype, (B, M, d)), ("knorm", torch.float32, (B, M)),
+                  ("rho", torch.int64, (B, M)), ("base", torch.int64, (B, M)), ("prov", torch.int64, (B, M)),
+                  ("occupancy", torch.int32, (B,)), ("budget", torch.int32, (B,))]
+        offs, total = [], 0
+        for name, dt, shape in layout:
+            nbytes = torch.empty((), dtype=dt).element_size()
+            for x in shape:
+                nbytes *= x
+            offs.append((name, dt, shape, total, nbytes))
+            total += (nbytes + 255) // 256 * 256
+        self._buf = torch.zeros(max(total, 256), dtype=torch.uint8, device=dev)
+        for name, dt, shape, off, nbytes in offs:
+            setattr(self, name, self._buf[off:off + nbytes].view(dt).view(shape))
         if budget is None:
-            budget = torch.full((num_banks,), capacity, dtype=torch.int32)
-        self.budget = torch.as_tensor(budget, dtype=torch.int32).to(dev).contiguous()
+            self.budget.fill_(capacity)
+        else:
+            self.budget.copy_(torch.as_tensor(budget, dtype=torch.int32))
 
     def c(self) -> DkvBank:
         return DkvBank(self.B, self.gs, self.d, self.Mcap, _dtype_code(self.dtype), self.k.data_ptr(),
@@ -142,12 +155,20 @@ class Bank:
                        self.prov.data_ptr(), self.occupancy.data_ptr(), self.budget.data_ptr())
 
     def state_dict(self):
-        """Checkpoint of the bank state (device tensors cloned)."""
-        return {n: getattr(self, n).clone() for n in ("k", "v", "knorm", "rho", "base", "prov", "occupancy", "budget")}
+        """Checkpoint of the bank state, one cloned device tensor per field."""
+        return {n: getattr(self, n).clone() for n in self._FIELDS}
 
     def load_state_dict(self, sd):
         for n, t in sd.items():
             getattr(self, n).copy_(t)
+
+    def snapshot(self) -> torch.Tensor:
+        """Checkpoint of the whole bank state as one device buffer."""
+        return self._buf.clone()
+
+    def restore(self, snap: torch.Tensor):
+        """Restore a snapshot() of this bank (one device-to-device copy on the current stream)."""
+        self._buf.copy_(snap)
 
 
 def workspace_size(bank: Bank, n_cand: int) -> int:
