@@ -50,12 +50,12 @@ size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, cha
   w.hole_list = (int32_t *)take(Bz * Mz * 4);
   w.sk = (uint16_t *)take(Bz * Nz * (size_t)d * 2);
   w.snorm = (float *)take(Bz * Nz * 4);
+  w.baug = (uint4 *)take(Bz * Mz * 16);
+  w.caug = (uint4 *)take(Bz * Nz * 16);
+  w.saug = (uint4 *)take(Bz * Nz * 16);
   const int nfw = ((N > 0 ? N : 0) + 1 + 31) / 32;
   w.feas = (uint32_t *)take(Bz * (size_t)nfw * 4);
   w.nfw = nfw;
-  w.xcount = (int32_t *)take(Bz * 4);
-  w.xlist = (int32_t *)take(Bz * Mz * 4);
-  w.xbefore = (int64_t *)take(Bz * Mz * 8);
   const int npad = ((N > 0 ? N : 1) + 511) / 512 * 512;
   w.skeys = (uint64_t *)take(Bz * (size_t)npad * 8);
   w.npad = npad;

@@ -9,7 +9,7 @@
 //                  candidates (the prefix checkpoints of Eqs. 8-9), the r*
 //                  fix-up, the exact maintenance (Supp. C) and the
 //                  from-scratch bank density (Eq. 3)
-//   k_cross_find   per bank state: the chunk in which its prefix density first
+//   k_cross        per bank state: the chunk in which its prefix density first
 //                  reaches tau b, then the exact prefix length inside it
 //
 // The column range of every Gram is split over workgroups (grid dimension y);
@@ -18,9 +18,10 @@
 //
 // Layout: a workgroup of 4 waves owns 128 row items; wave w owns 32 of them,
 // held for the whole kernel as the B operand of v_mfma_f32_32x32x16_bf16
-// (lane l <-> row item l % 32).  Column items stream through LDS in tiles of 32
-// (double-buffered, padded rows) and form the A operand, so each lane ends up
-// with 16 weights of its own row item and reduces them in registers.
+// (lane l <-> row item l % 32).  Column items stream through LDS in stages of 64
+// (three stages resident, loaded global -> LDS directly, key rows swizzled)
+// and form the A operand, so each lane ends up with 16 weights of its own row
+// item and reduces them in registers.
 //
 // Exactness: with keys on the 1/64 grid every partial sum of the contraction
 // is an exact multiple of 2^-18 below 2^24 units, so the MFMA result
@@ -51,7 +52,6 @@ constexpr int kSI = 64;  // column items per LDS stage (two tiles, two independe
 template <int D>
 struct TileCfg {
   static constexpr int kSteps = D / 16;     // K steps over the key
-  static constexpr int kStride = D + 24;    // bf16 per LDS row: key, 16 aug, 8 pad (odd multiple of 16 B)
   static constexpr int kChunks = D / 8;     // 16-byte chunks per key
 };
 
@@ -120,74 +120,100 @@ __device__ __forceinline__ void load_row_frag(RowFrag<D> &rf, const uint16_t *ke
   rf.b[TileCfg<D>::kSteps] = __builtin_bit_cast(bf16x8, aug);
 }
 
-// Column stage staging: each of the 256 threads moves 16-byte chunks of the
-// stage's keys; 64 threads write the aug columns.
+// ---------------------------------------------------------------------------
+// Column stages in LDS: 64 column items per stage, three stages resident (two
+// loading while one is used).  Keys go global -> LDS with 16-byte direct-to-LDS
+// loads (no VGPR staging); a key row is 2 d bytes with its 16-byte chunk c
+// stored at c ^ (row % chunks), so that the A-operand reads (32 rows, one chunk
+// each) are free of bank conflicts.  Each item's extra K step (column_aug,
+// precomputed per update) and, for the score, its score scale follow.
+// ---------------------------------------------------------------------------
 template <int D>
-struct ColStage {
-  u32x4 chunk[(kSI * TileCfg<D>::kChunks) / (64 * kWaves)];
-  u32x4 aug0;
+struct SCfg {
+  static constexpr int CH = D / 8;             // 16-byte chunks per key row
+  static constexpr int RB = 2 * D;             // key row bytes
+  static constexpr int RPL = 1024 / RB;        // rows per 1 KB load
+  static constexpr int NB = kSI * RB / 1024;   // 1 KB loads per stage
+  static constexpr int PER = NB / kWaves;      // key loads per thread per stage
+  static constexpr int KEYB = kSI * RB;        // key bytes per stage
+  static constexpr int AUGB = kSI * 16;        // aug bytes per stage
+  static_assert(NB % kWaves == 0, "key loads split evenly over the waves");
 };
+// direct-to-LDS loads per thread per stage: keys, aug (+ score scale)
+template <int D, bool kBs>
+constexpr int stage_ops() { return SCfg<D>::PER + 1 + (kBs ? 1 : 0); }
 
-// item_row(i) returns the element offset of column item i's key, or -1.
-template <int D, class RowOf, class NormOf>
-__device__ __forceinline__ void stage_load(ColStage<D> &st, const uint16_t *base, int j0, int ncols,
-                                           RowOf row_of, NormOf norm_of, float inv_s2) {
-  constexpr int kPer = (kSI * TileCfg<D>::kChunks) / (64 * kWaves);
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Global rows fetched by this thread for the stage starting at column j0 (its
+// key loads, then its aug / scale item); items past ncols repeat the last one.
+template <int D, class RowOf>
+__device__ __forceinline__ void stage_rows(int64_t (&rows)[SCfg<D>::PER + 1], int j0, int ncols, RowOf row_of) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
 #pragma unroll
-  for (int q = 0; q < kPer; ++q) {
-    const int c = threadIdx.x + q * 64 * kWaves;
-    const int item = c / TileCfg<D>::kChunks, ch = c % TileCfg<D>::kChunks;
-    u32x4 v = {0, 0, 0, 0};
-    if (j0 + item < ncols) {
-      const int64_t r = row_of(j0 + item);
-      v = *reinterpret_cast<const u32x4 *>(base + r * D + ch * 8);
-    }
-    st.chunk[q] = v;
+  for (int q = 0; q < SCfg<D>::PER; ++q) {
+    const int r = (wave * SCfg<D>::PER + q) * SCfg<D>::RPL + l / SCfg<D>::CH;
+    rows[q] = row_of(min(j0 + r, ncols - 1));
   }
-  if (threadIdx.x < kSI) {
-    u32x4 a = {0, 0, 0, 0};
-    if (j0 + (int)threadIdx.x < ncols) {
-      uint16_t nh, nm, nl;
-      split3(norm_of(j0 + (int)threadIdx.x) * inv_s2, nh, nm, nl);
-      a[0] = (uint32_t)nh | ((uint32_t)nm << 16);
-      a[1] = (uint32_t)nl | ((uint32_t)kOne << 16);
-      a[2] = (uint32_t)kOne | ((uint32_t)kOne << 16);
-      a[3] = (uint32_t)kOne;  // times the row's fold slot
-    }
-    st.aug0 = a;
+  rows[SCfg<D>::PER] = row_of(min(j0 + 16 * wave + (l & 15), ncols - 1));
+}
+
+template <int D, bool kBs>
+__device__ __forceinline__ void stage_dma(const int64_t (&rows)[SCfg<D>::PER + 1], const uint16_t *keys,
+                                          const uint4 *augs, const float *bs, char *kb, char *ab, float *sb) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
+#pragma unroll
+  for (int q = 0; q < SCfg<D>::PER; ++q) {
+    const int blk = wave * SCfg<D>::PER + q;
+    const int r = blk * SCfg<D>::RPL + l / SCfg<D>::CH;
+    const int c = (l % SCfg<D>::CH) ^ (r % SCfg<D>::CH);
+    __builtin_amdgcn_global_load_lds((void *)(keys + rows[q] * D + 8 * c), (lds_void *)(kb + blk * 1024), 16, 0, 0);
+  }
+  // items 16 w .. 16 w + 15: lanes 0-15 of wave w (LDS address = base + lane * size)
+  if (l < 16) {
+    __builtin_amdgcn_global_load_lds((void *)(augs + rows[SCfg<D>::PER]), (lds_void *)(ab + 256 * wave), 16, 0, 0);
+    if constexpr (kBs)
+      __builtin_amdgcn_global_load_lds((void *)(bs + rows[SCfg<D>::PER]), (lds_void *)(sb + 16 * wave), 4, 0, 0);
   }
 }
 
-template <int D>
-__device__ __forceinline__ void stage_store(const ColStage<D> &st, uint16_t *lds) {
-  constexpr int kPer = (kSI * TileCfg<D>::kChunks) / (64 * kWaves);
-#pragma unroll
-  for (int q = 0; q < kPer; ++q) {
-    const int c = threadIdx.x + q * 64 * kWaves;
-    const int item = c / TileCfg<D>::kChunks, ch = c % TileCfg<D>::kChunks;
-    *reinterpret_cast<u32x4 *>(lds + item * TileCfg<D>::kStride + ch * 8) = st.chunk[q];
-  }
-  if (threadIdx.x < kSI) {
-    *reinterpret_cast<u32x4 *>(lds + threadIdx.x * TileCfg<D>::kStride + D) = st.aug0;
-    *reinterpret_cast<u32x4 *>(lds + threadIdx.x * TileCfg<D>::kStride + D + 8) = u32x4{0, 0, 0, 0};
-  }
-}
+// s_waitcnt immediate (gfx9 encoding): at most n vector-memory operations
+// outstanding and no LDS operation outstanding (expcnt left alone).
+constexpr int waitcnt_vm_lgkm0(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
 
-// u for the 16 (column item, row item) pairs of this lane: column items
-// m_i = 8 (i / 4) + 4 h + (i % 4), row item = lane % 32.
+// Stage barrier without a memory fence: each thread has waited for its own
+// loads of the stage about to be read, so the loads of later stages stay in
+// flight; the "memory" clobber keeps LDS accesses from moving across it.
+__device__ __forceinline__ void stage_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// u for both 32-item tiles of a stage: A fragments from the swizzled key rows
+// and the aug step, two interleaved MFMA chains.
 template <int D>
-__device__ __forceinline__ f32x16 tile_u(const uint16_t *lds, const RowFrag<D> &rf) {
-  const int l = threadIdx.x & 63;
-  const uint16_t *src = lds + (l & 31) * TileCfg<D>::kStride + 8 * (l >> 5);
-  bf16x8 a[TileCfg<D>::kSteps + 1];
+__device__ __forceinline__ void stage_u(const char *kb, const char *ab, const RowFrag<D> &rf, f32x16 &u0,
+                                        f32x16 &u1) {
+  constexpr int KS = TileCfg<D>::kSteps;
+  const int l = threadIdx.x & 63, h = l >> 5, r0 = l & 31, r1 = 32 + r0;
+  bf16x8 a0[KS + 1], a1[KS + 1];
 #pragma unroll
-  for (int kk = 0; kk <= TileCfg<D>::kSteps; ++kk)
-    a[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(src + 16 * kk));
-  f32x16 acc = {};
+  for (int kk = 0; kk < KS; ++kk) {
+    const int c = 2 * kk + h;
+    a0[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(
+                                            kb + r0 * SCfg<D>::RB + 16 * (c ^ (r0 % SCfg<D>::CH))));
+    a1[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(
+                                            kb + r1 * SCfg<D>::RB + 16 * (c ^ (r1 % SCfg<D>::CH))));
+  }
+  // the aug step: both half-waves read the item's 16 bytes; the row fragment's
+  // second half is zero, so the h = 1 copy contributes nothing
+  a0[KS] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(ab + 16 * r0));
+  a1[KS] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(ab + 16 * r1));
+  f32x16 x0 = {}, x1 = {};
 #pragma unroll
-  for (int kk = 0; kk <= TileCfg<D>::kSteps; ++kk)
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], rf.b[kk], acc, 0, 0, 0);
-  return acc;
+  for (int kk = 0; kk <= KS; ++kk) {
+    x0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[kk], rf.b[kk], x0, 0, 0, 0);
+    x1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[kk], rf.b[kk], x1, 0, 0, 0);
+  }
+  u0 = x0;
+  u1 = x1;
 }
 
 __device__ __forceinline__ int col_of_reg(int i, int h) { return 8 * (i >> 2) + 4 * h + (i & 3); }
@@ -220,8 +246,10 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_score_mfma(dkv_bank bank, co
   const int c0 = blockIdx.y * kColsPerSplit;
   if (c0 >= m) return;
   const int ncols = min(kColsPerSplit, m - c0);
-  __shared__ __attribute__((aligned(16))) uint16_t tile[2][kSI * TileCfg<D>::kStride];
-  __shared__ __attribute__((aligned(16))) float tbs[2][kSI];
+  constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
+  __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
+  __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
+  __shared__ __attribute__((aligned(16))) float s0[kSI], s1[kSI], s2[kSI];
   const uint16_t *K = static_cast<const uint16_t *>(seg_k);
   const uint16_t *BK = static_cast<const uint16_t *>(bank.k);
   const bool rv = x < g.N;
@@ -230,18 +258,11 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_score_mfma(dkv_bank bank, co
   load_row_frag<D, FOLD>(rf, K + xr * D, rv ? ws.cnorm[xr] : 0.0f, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
   const size_t rb = (size_t)b * g.Mcap + c0;
   auto row_of = [&](int i) -> int64_t { return (int64_t)(rb + i); };
-  auto norm_of = [&](int i) -> float { return bank.knorm[rb + i]; };
   uint64_t A64 = 0, W64 = 0;
   const int ns = (ncols + kSI - 1) / kSI;
-  ColStage<D> st;
-  float bs_next = 0.0f;
-  stage_load<D>(st, BK, 0, ncols, row_of, norm_of, p.inv_sigma2);
-  if (threadIdx.x < kSI) bs_next = (int)threadIdx.x < ncols ? ws.bs[rb + threadIdx.x] : 0.0f;
-  stage_store<D>(st, tile[0]);
-  if (threadIdx.x < kSI) tbs[0][threadIdx.x] = bs_next;
-  __syncthreads();
   // epilogue of one 32-column tile: integer sums of W and of the scaled score terms
-  auto epi = [&](auto mask_tag, const f32x16 &u, const float *tb, int nvalid, uint32_t &sw, uint32_t &sa) {
+  auto epi = [&](auto mask_tag, const f32x16 &u, const float *tb, int nvalid, uint32_t &sw, uint32_t &sa)
+      __attribute__((always_inline)) {
     constexpr bool MASK = decltype(mask_tag)::value;
     float bsv[16];
 #pragma unroll
@@ -278,39 +299,51 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_score_mfma(dkv_bank bank, co
   };
   using Full = std::integral_constant<bool, false>;
   using Part = std::integral_constant<bool, true>;
-  for (int t = 0; t < ns; ++t) {
-    const int cur = t & 1;
-    const int j0n = (t + 1) * kSI;
-    if (t + 1 < ns) {
-      stage_load<D>(st, BK, j0n, ncols, row_of, norm_of, p.inv_sigma2);
-      if (threadIdx.x < kSI) bs_next = j0n + (int)threadIdx.x < ncols ? ws.bs[rb + j0n + threadIdx.x] : 0.0f;
+  constexpr int kOps = stage_ops<D, true>();
+  int64_t rows[SCfg<D>::PER + 1];
+  // stage t in buffers (t % 3); rows of stage t + 2 loaded one step ahead
+  auto step = [&](int t, const char *kb, const char *ab, const float *sb, char *kn, char *an, float *sn)
+      __attribute__((always_inline)) {
+    if (t + 1 < ns) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kOps));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+    stage_barrier();
+    if (t + 2 < ns) {
+      stage_dma<D, true>(rows, BK, ws.baug, ws.bs, kn, an, sn);
+      if (t + 3 < ns) stage_rows<D>(rows, (t + 3) * kSI, ncols, row_of);
     }
+    f32x16 u0, u1;
+    stage_u<D>(kb, ab, rf, u0, u1);
     const int nv0 = ncols - t * kSI;
-    const f32x16 u0 = tile_u<D>(tile[cur], rf);
-    const f32x16 u1 = tile_u<D>(tile[cur] + kCT * TileCfg<D>::kStride, rf);
     uint32_t sw, sa;
     if (nv0 >= kSI) {
-      epi(Full{}, u0, tbs[cur], kCT, sw, sa);
+      epi(Full{}, u0, sb, kCT, sw, sa);
       W64 += sw;
       A64 += sa;
-      epi(Full{}, u1, tbs[cur] + kCT, kCT, sw, sa);
+      epi(Full{}, u1, sb + kCT, kCT, sw, sa);
       W64 += sw;
       A64 += sa;
     } else {
-      epi(Part{}, u0, tbs[cur], nv0, sw, sa);
+      epi(Part{}, u0, sb, nv0, sw, sa);
       W64 += sw;
       A64 += sa;
       if (nv0 > kCT) {
-        epi(Part{}, u1, tbs[cur] + kCT, nv0 - kCT, sw, sa);
+        epi(Part{}, u1, sb + kCT, nv0 - kCT, sw, sa);
         W64 += sw;
         A64 += sa;
       }
     }
-    if (t + 1 < ns) {
-      stage_store<D>(st, tile[cur ^ 1]);
-      if (threadIdx.x < kSI) tbs[cur ^ 1][threadIdx.x] = bs_next;
-    }
-    __syncthreads();
+  };
+  stage_rows<D>(rows, 0, ncols, row_of);
+  stage_dma<D, true>(rows, BK, ws.baug, ws.bs, k0, a0, s0);
+  if (ns > 1) {
+    stage_rows<D>(rows, kSI, ncols, row_of);
+    stage_dma<D, true>(rows, BK, ws.baug, ws.bs, k1, a1, s1);
+    if (ns > 2) stage_rows<D>(rows, 2 * kSI, ncols, row_of);
+  }
+  for (int t = 0; t < ns; t += 3) {
+    step(t, k0, a0, s0, k2, a2, s2);
+    if (t + 1 < ns) step(t + 1, k1, a1, s1, k0, a0, s0);
+    if (t + 2 < ns) step(t + 2, k2, a2, s2, k1, a1, s1);
   }
   const uint64_t Wt = W64 + __shfl_xor(W64, 32, 64);
   const uint64_t At = A64 + __shfl_xor(A64, 32, 64);
@@ -327,16 +360,24 @@ enum RowSumMode { RS_CHUNK = 0, RS_FIXUP = 1, RS_SURV_EV = 2, RS_ADM_BASE = 3, R
 
 constexpr int kChunksPerSplit = 1024 / kCkStride;   // RS_CHUNK: 1024 ordered candidates per workgroup
 
+// The three LDS stages of a Gram workgroup (separate arrays: with the stage
+// known at compile time, reads of one stage never wait for loads into another).
+template <int D>
+struct StageBufs {
+  char *k0, *k1, *k2, *a0, *a1, *a2;
+};
+
+// Body of one row-sum workgroup (bx, by, bz) = (row block, column split, bank).
 template <int D, int P, int MODE, bool FOLD>
-__global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
-                                                            Workspace ws, int64_t *out) {
-  const int b = blockIdx.z;
+__device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *seg_k, const Geom &g, const Prm &p,
+                                            const Workspace &ws, int64_t *out, int bx, int by, int bz,
+                                            const StageBufs<D> &sb) {
+  const int b = bz;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
   const int m = ws.m[b];
   const uint16_t *SK = static_cast<const uint16_t *>(seg_k);
   const uint16_t *BK = static_cast<const uint16_t *>(bank.k);
-  const uint16_t *SORTK = ws.sk;
   constexpr bool kNeedEv = MODE == RS_SURV_EV || MODE == RS_ADM_BASE || MODE == RS_ADM_MUT;
   const int n_ev = kNeedEv ? ws.n_ev[b] : 0;
   const int rs = (MODE == RS_FIXUP || kNeedEv) ? ws.r_star[b / g.gs] : 0;
@@ -347,12 +388,12 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
   if constexpr (MODE == RS_CHUNK || MODE == RS_FIXUP || MODE == RS_DENSITY) nrows = m;
   else if constexpr (MODE == RS_SURV_EV) nrows = n_surv;
   else nrows = rs;
-  if ((int)blockIdx.x * kRowsPerWG >= nrows) return;
+  if ((int)bx * kRowsPerWG >= nrows) return;
   // columns of this workgroup: [c0, c1) of the mode's column list
   int c0 = 0, c1 = 0;
   if constexpr (MODE == RS_CHUNK) {
     const int R = ws.R[b];
-    c0 = blockIdx.y * kChunksPerSplit * kCkStride;
+    c0 = by * kChunksPerSplit * kCkStride;
     c1 = min(R, c0 + kChunksPerSplit * kCkStride);
   } else if constexpr (MODE == RS_FIXUP) {
     c0 = (rs / kCkStride) * kCkStride;
@@ -363,11 +404,11 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
     else if constexpr (MODE == RS_ADM_BASE) total = adm_by_ev ? n_ev : n_surv;
     else if constexpr (MODE == RS_ADM_MUT) total = rs;
     else total = m;
-    c0 = blockIdx.y * kColsPerSplit;
+    c0 = by * kColsPerSplit;
     c1 = min(total, c0 + kColsPerSplit);
   }
   if (MODE != RS_FIXUP && c0 >= c1) return;  // the fix-up always writes rho~, even for r* % 256 == 0
-  const int v = blockIdx.x * kRowsPerWG + wave * 32 + n;
+  const int v = bx * kRowsPerWG + wave * 32 + n;
   const bool rv = v < nrows;
   // row item
   const uint16_t *rkey = BK + rb * D;
@@ -401,32 +442,17 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
     else if constexpr (MODE == RS_ADM_MUT) return (int64_t)(nb + ws.adm_list[nb + j]);
     else return (int64_t)(rb + j);
   };
-  auto norm_of = [&](int j) -> float {
-    if constexpr (MODE == RS_CHUNK || MODE == RS_FIXUP) return ws.snorm[nb + j];
-    else if constexpr (MODE == RS_SURV_EV) return bank.knorm[rb + ws.ev_list[rb + j]];
-    else if constexpr (MODE == RS_ADM_BASE)
-      return bank.knorm[rb + (adm_by_ev ? ws.ev_list[rb + j] : ws.surv_list[rb + j])];
-    else if constexpr (MODE == RS_ADM_MUT) return ws.cnorm[nb + ws.adm_list[nb + j]];
-    else return bank.knorm[rb + j];
-  };
-  const uint16_t *colbase = (MODE == RS_CHUNK || MODE == RS_FIXUP) ? SORTK : (MODE == RS_ADM_MUT ? SK : BK);
+  const uint16_t *colbase = (MODE == RS_CHUNK || MODE == RS_FIXUP) ? ws.sk : (MODE == RS_ADM_MUT ? SK : BK);
+  const uint4 *colaug = (MODE == RS_CHUNK || MODE == RS_FIXUP) ? ws.saug : (MODE == RS_ADM_MUT ? ws.caug : ws.baug);
   constexpr bool kDiag = (MODE == RS_ADM_MUT || MODE == RS_DENSITY);
-  __shared__ __attribute__((aligned(16))) uint16_t tile[2][kSI * TileCfg<D>::kStride];
   uint64_t S64 = 0;
   uint32_t chunk_sum = 0;
   const int ncols = c1 - c0;
   const int ns = (ncols + kSI - 1) / kSI;
-  ColStage<D> st;
   auto row_of_rel = [&](int j) -> int64_t { return row_of(c0 + j); };
-  auto norm_of_rel = [&](int j) -> float { return norm_of(c0 + j); };
-  if (ns > 0) {
-    stage_load<D>(st, colbase, 0, ncols, row_of_rel, norm_of_rel, p.inv_sigma2);
-    stage_store<D>(st, tile[0]);
-  }
-  __syncthreads();
-  const int wg_row0 = blockIdx.x * kRowsPerWG;
+  const int wg_row0 = bx * kRowsPerWG;
   // sum of the lane's 16 weights of one 32-column tile starting at list index j0
-  auto tile_sum = [&](const f32x16 &u, int j0, int nvalid) -> uint32_t {
+  auto tile_sum = [&](const f32x16 &u, int j0, int nvalid) __attribute__((always_inline)) -> uint32_t {
     const bool diag_tile = kDiag && (j0 < wg_row0 + kRowsPerWG) && (j0 + kCT > wg_row0);
     if (nvalid >= kCT && !diag_tile) return lane_wsum<P, false, FOLD>(u, kCT, h);
     uint32_t sm = 0;
@@ -440,11 +466,25 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
     }
     return sm - 16u * kMagic;
   };
-  for (int t = 0; t < ns; ++t) {
-    const int cur = t & 1;
-    if (t + 1 < ns) stage_load<D>(st, colbase, (t + 1) * kSI, ncols, row_of_rel, norm_of_rel, p.inv_sigma2);
-    const f32x16 u0 = tile_u<D>(tile[cur], rf);
-    const f32x16 u1 = tile_u<D>(tile[cur] + kCT * TileCfg<D>::kStride, rf);
+  constexpr int kOps = stage_ops<D, false>();
+  // Stage t in buffers t % 3.  The global rows of stage t + 2 were fetched one
+  // step earlier (list lookups for the maintenance stages), so issuing its
+  // loads never waits for the loads still in flight.
+  // Two row sets used alternately (the loop is unrolled 6 = lcm(3, 2) times),
+  // so that no register copy waits for a lookup still in flight.
+  int64_t rowsA[SCfg<D>::PER + 1], rowsB[SCfg<D>::PER + 1];
+  using Rows = int64_t[SCfg<D>::PER + 1];
+  auto step = [&](int t, const char *kb, const char *ab, char *kn, char *an, Rows &use, Rows &fill)
+      __attribute__((always_inline)) {
+    if (t + 1 < ns) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kOps));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+    stage_barrier();
+    if (t + 2 < ns) {
+      if (t + 3 < ns) stage_rows<D>(fill, (t + 3) * kSI, ncols, row_of_rel);
+      stage_dma<D, false>(use, colbase, colaug, nullptr, kn, an, nullptr);
+    }
+    f32x16 u0, u1;
+    stage_u<D>(kb, ab, rf, u0, u1);
     const int nv0 = ncols - t * kSI;
     const int j0 = c0 + t * kSI;
     uint32_t s2 = tile_sum(u0, j0, nv0);
@@ -460,8 +500,25 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
     } else {
       S64 += s2;
     }
-    if (t + 1 < ns) stage_store<D>(st, tile[cur ^ 1]);
-    __syncthreads();
+  };
+  if (ns > 0) {
+    stage_rows<D>(rowsA, 0, ncols, row_of_rel);
+    stage_dma<D, false>(rowsA, colbase, colaug, nullptr, sb.k0, sb.a0, nullptr);
+    if (ns > 1) {
+      stage_rows<D>(rowsB, kSI, ncols, row_of_rel);
+      stage_dma<D, false>(rowsB, colbase, colaug, nullptr, sb.k1, sb.a1, nullptr);
+      if (ns > 2) stage_rows<D>(rowsA, 2 * kSI, ncols, row_of_rel);
+    }
+  }
+  // step t issues stage t + 2 with the rows fetched at step t - 1 and fetches
+  // those of stage t + 3: stage t + 2 uses rowsA when t is even
+  for (int t = 0; t < ns; t += 6) {
+    step(t, sb.k0, sb.a0, sb.k2, sb.a2, rowsA, rowsB);
+    if (t + 1 < ns) step(t + 1, sb.k1, sb.a1, sb.k0, sb.a0, rowsB, rowsA);
+    if (t + 2 < ns) step(t + 2, sb.k2, sb.a2, sb.k1, sb.a1, rowsA, rowsB);
+    if (t + 3 < ns) step(t + 3, sb.k0, sb.a0, sb.k2, sb.a2, rowsB, rowsA);
+    if (t + 4 < ns) step(t + 4, sb.k1, sb.a1, sb.k0, sb.a0, rowsA, rowsB);
+    if (t + 5 < ns) step(t + 5, sb.k2, sb.a2, sb.k1, sb.a1, rowsB, rowsA);
   }
   if constexpr (MODE == RS_CHUNK) return;
   uint64_t tot = S64;
@@ -491,18 +548,59 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
   }
 }
 
+template <int D, int P, int MODE, bool FOLD>
+__global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
+                                                            Workspace ws, int64_t *out) {
+  constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
+  __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
+  __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
+  const StageBufs<D> sb{k0, k1, k2, a0, a1, a2};
+  rowsum_body<D, P, MODE, FOLD>(bank, seg_k, g, p, ws, out, blockIdx.x, blockIdx.y, blockIdx.z, sb);
+}
+
+// The three maintenance sums in one launch (Supp. C): survivors x evicted,
+// admitted x (evicted or survivors), admitted x admitted; blockIdx.x selects
+// the stage and its row block.
+template <int D, int P, bool FOLD>
+__global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
+                                                           Workspace ws, int nx_surv, int nx_adm) {
+  constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
+  __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
+  __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
+  const StageBufs<D> sb{k0, k1, k2, a0, a1, a2};
+  const int bx = blockIdx.x;
+  if (bx < nx_surv)
+    rowsum_body<D, P, RS_SURV_EV, FOLD>(bank, seg_k, g, p, ws, nullptr, bx, blockIdx.y, blockIdx.z, sb);
+  else if (bx < nx_surv + nx_adm)
+    rowsum_body<D, P, RS_ADM_BASE, FOLD>(bank, seg_k, g, p, ws, nullptr, bx - nx_surv, blockIdx.y, blockIdx.z, sb);
+  else
+    rowsum_body<D, P, RS_ADM_MUT, FOLD>(bank, seg_k, g, p, ws, nullptr, bx - nx_surv - nx_adm, blockIdx.y,
+                                        blockIdx.z, sb);
+}
+
 // ---------------------------------------------------------------------------
-// First violating prefix length of every bank state (Eqs. 8-9).
-// k_cross_scan: thread per state; the first 64-candidate chunk whose sum
-// lifts the prefix density to tau b.  States that never reach it get R + 1;
-// the others are listed for k_cross_find, which re-walks that one chunk (one
-// ordered candidate per lane, same binary32 weights) for the exact length.
+// First violating prefix length of every bank state (Eqs. 8-9), one wave per
+// state.  The chunk sums of the ordered candidates (64 per chunk, two chunks
+// per lane) are prefix-summed across the wave; the first chunk whose end lifts
+// rho + P to tau b (2^k (rho + P) >= T b, integers) is re-walked with one
+// ordered candidate per lane (same binary32 weights) for the exact length.
+// States that never reach the bound within the tested prefixes get R + 1.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_cross_scan(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
-  const int b = blockIdx.y, i = blockIdx.x * 256 + threadIdx.x;
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+  const uint32_t lo = __shfl((uint32_t)v, src, 64), hi = __shfl((uint32_t)(v >> 32), src, 64);
+  return ((uint64_t)hi << 32) | lo;
+}
+
+template <int D, int P>
+__global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
+  static_assert(kCkStride == 64, "one candidate per lane in the exact walk");
+  static_assert((DKV_MAX_CANDIDATES + kCkStride - 1) / kCkStride <= 128, "two chunk sums per lane");
+  const int b = blockIdx.y;
+  const int l = threadIdx.x & 63;
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int m = ws.m[b], R = ws.R[b];
-  if (i >= m) return;
-  const size_t rb = (size_t)b * g.Mcap, row = rb + i;
+  if (i >= m) return;  // whole wave
+  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N, row = rb + i;
   const int64_t lim = ((int64_t)p.tau_num * bank.base[row] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
   const int64_t thr = lim - bank.rho[row];
   int first = R + 1;
@@ -510,99 +608,78 @@ __global__ __launch_bounds__(256) void k_cross_scan(dkv_bank bank, Geom g, Prm p
     first = 0;
   } else {
     const int nch = (R + kCkStride - 1) / kCkStride;
-    const uint4 *ckr = reinterpret_cast<const uint4 *>(ws.ck + row * ws.nck);
-    const int n4 = (nch + 3) / 4;
-    int64_t P = 0;
-    // batches of 8 x 4 chunk sums, all loads of a batch in flight together
-    for (int c8 = 0; c8 < n4; c8 += 8) {
-      uint4 q[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) q[e] = c8 + e < n4 ? ckr[c8 + e] : uint4{0, 0, 0, 0};
-#pragma unroll
-      for (int e = 0; e < 32; ++e) {
-        const int c = 4 * c8 + e;
-        const uint32_t v = e % 4 == 0 ? q[e / 4].x : e % 4 == 1 ? q[e / 4].y : e % 4 == 2 ? q[e / 4].z : q[e / 4].w;
-        if (c >= nch) break;
-        if (P + v >= thr) {
-          const int k = atomicAdd(&ws.xcount[b], 1);
-          ws.xlist[rb + k] = i | (c << 16);
-          ws.xbefore[rb + k] = P;
-          return;  // first written by k_cross_find
-        }
-        P += v;
-      }
-    }
-  }
-  ws.first[row] = first;
-  if (out_first) out_first[row] = first;
-}
-
-template <int D, int P>
-__global__ __launch_bounds__(256) void k_cross_find(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
-  const int b = blockIdx.y;
-  const int l = threadIdx.x & 63;
-  const int R = ws.R[b];
-  const int cnt = ws.xcount[b];
-  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
-  {
-    const int k = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (k >= cnt) return;
-    const int ent = ws.xlist[rb + k];
-    const int i = ent & 0xFFFF, c = ent >> 16;
-    const int64_t before = ws.xbefore[rb + k];
-    const size_t row = rb + i;
-    const int64_t lim = ((int64_t)p.tau_num * bank.base[row] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
-    const int64_t thr = lim - bank.rho[row];
-    const uint16_t *rk = static_cast<const uint16_t *>(bank.k) + row * D;
-    const float nr = bank.knorm[row];
-    // one ordered candidate per lane: column c * 64 + l
-    static_assert(kCkStride == 64, "one column per lane");
-    const int col = c * kCkStride + l;
-    uint32_t W = 0;
-    if (col < R) {
-      const uint16_t *ckey = ws.sk + (nb + col) * D;
-      float acc = 0.0f;
-#pragma unroll
-      for (int j = 0; j < D; j += 8) {
-        const u32x4 a = *reinterpret_cast<const u32x4 *>(rk + j);
-        const u32x4 bb = *reinterpret_cast<const u32x4 *>(ckey + j);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc = __builtin_fmaf(__uint_as_float(a[e] << 16), __uint_as_float(bb[e] << 16), acc);
-          acc = __builtin_fmaf(__uint_as_float(a[e] & 0xFFFF0000u), __uint_as_float(bb[e] & 0xFFFF0000u), acc);
-        }
-      }
-      const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
-      W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
-    }
-    uint32_t incl = W;
+    const uint32_t *ckr = ws.ck + row * ws.nck;
+    const uint32_t c0 = 2 * l < nch ? ckr[2 * l] : 0u;
+    const uint32_t c1 = 2 * l + 1 < nch ? ckr[2 * l + 1] : 0u;
+    uint64_t incl = (uint64_t)c0 + c1;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t y = __shfl_up(incl, o, 64);
+      const uint64_t y = __shfl_up((uint32_t)incl, o, 64) | ((uint64_t)__shfl_up((uint32_t)(incl >> 32), o, 64) << 32);
       if (l >= o) incl += y;
     }
-    const unsigned long long hl = __ballot(before + (int64_t)incl >= thr);
-    const int first = hl != 0 ? c * kCkStride + (__ffsll(hl) - 1) + 1
-                              : min(R, (c + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
-    if (l == 0) {
-      ws.first[row] = first;
-      if (out_first) out_first[row] = first;
+    const uint64_t before = incl - c0 - c1;  // chunks < 2 l
+    const bool hit0 = 2 * l < nch && (int64_t)(before + c0) >= thr;
+    const bool hit1 = 2 * l + 1 < nch && (int64_t)incl >= thr;
+    const unsigned long long hl = __ballot(hit0 || hit1);
+    if (hl != 0) {
+      const int lf = __ffsll(hl) - 1;
+      const bool second = !__shfl((int)hit0, lf, 64);
+      const int c = 2 * lf + (second ? 1 : 0);
+      const int64_t pb = (int64_t)shfl_u64(second ? before + c0 : before, lf);  // prefix before chunk c
+      const uint16_t *rk = static_cast<const uint16_t *>(bank.k) + row * D;
+      const float nr = bank.knorm[row];
+      const int col = c * kCkStride + l;
+      uint32_t W = 0;
+      if (col < R) {
+        const uint16_t *ckey = ws.sk + (nb + col) * D;
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = 0; j < D; j += 8) {
+          const u32x4 a = *reinterpret_cast<const u32x4 *>(rk + j);
+          const u32x4 bb = *reinterpret_cast<const u32x4 *>(ckey + j);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc = __builtin_fmaf(__uint_as_float(a[e] << 16), __uint_as_float(bb[e] << 16), acc);
+            acc = __builtin_fmaf(__uint_as_float(a[e] & 0xFFFF0000u), __uint_as_float(bb[e] & 0xFFFF0000u), acc);
+          }
+        }
+        const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
+        W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
+      }
+      uint32_t wi = W;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(wi, o, 64);
+        if (l >= o) wi += y;
+      }
+      const unsigned long long h2 = __ballot(pb + (int64_t)wi >= thr);
+      first = h2 != 0 ? c * kCkStride + (__ffsll(h2) - 1) + 1
+                      : min(R, (c + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
     }
+  }
+  if (l == 0) {
+    ws.first[row] = first;
+    if (out_first) out_first[row] = first;
   }
 }
 
-// Candidate keys and norms in score order (contiguous rows for the ordered passes).
+// Candidate keys and norms in score order, so that the ordered passes stream
+// contiguous rows: one thread per 16-byte chunk of a key row.
 template <int D>
-__global__ __launch_bounds__(256) void k_gather_sorted(const void *seg_k, Geom g, Workspace ws) {
+__global__ __launch_bounds__(256) void k_gather_sorted(const void *seg_k, Geom g, Workspace ws, float inv_s2) {
+  constexpr int CH = D / 8;  // 16-byte chunks per bf16 row
   const int b = blockIdx.y;
-  const int j = blockIdx.x * 4 + (threadIdx.x >> 6), l = threadIdx.x & 63;
+  const int t = blockIdx.x * 256 + threadIdx.x;
+  const int j = t / CH, c = t % CH;
   if (j >= g.N) return;
   const size_t nb = (size_t)b * g.N;
   const int x = ws.order[nb + j];
-  const uint32_t *src = reinterpret_cast<const uint32_t *>(static_cast<const uint16_t *>(seg_k) + (nb + x) * D);
-  uint32_t *dst = reinterpret_cast<uint32_t *>(ws.sk + (nb + j) * D);
-  for (int e = l; e < D / 2; e += 64) dst[e] = src[e];
-  if (l == 0) ws.snorm[nb + j] = ws.cnorm[nb + x];
+  const u32x4 *src = reinterpret_cast<const u32x4 *>(static_cast<const uint16_t *>(seg_k) + (nb + x) * D);
+  reinterpret_cast<u32x4 *>(ws.sk + (nb + j) * D)[c] = src[c];
+  if (c == 0) {
+    ws.snorm[nb + j] = ws.cnorm[nb + x];
+    ws.saug[nb + j] = ws.caug[nb + x];
+  }
 }
 
 // Score entry point outputs from the accumulated sums.
@@ -630,30 +707,28 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
   const int T = 64 * kWaves;
   const unsigned rowsM = cdiv(g.Mcap, kRowsPerWG), rowsN = cdiv(g.N > 0 ? g.N : 1, kRowsPerWG);
   switch (stage) {
-    case 0:  // score + sorted copy is launched after the sort (stage 4)
+    case 0:  // score; the ordered copy is launched after the sort (stage 4)
       k_score_mfma<D, P, F><<<dim3(rowsN, cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws);
       break;
     case 4:
-      k_gather_sorted<D><<<dim3(cdiv(g.N, 4), g.B), 256, 0, s>>>(seg.k, g, ws);
+      k_gather_sorted<D><<<dim3(cdiv(g.N * (D / 8), 256), g.B), 256, 0, s>>>(seg.k, g, ws, p.inv_sigma2);
       break;
     case 1: {
       if (g.N > 0)
         k_rowsum_mfma<D, P, RS_CHUNK, F><<<dim3(rowsM, cdiv(g.N, kChunksPerSplit * kCkStride), g.B), T, 0, s>>>(
             bank, seg.k, g, p, ws, nullptr);
-      k_cross_scan<<<dim3(cdiv(g.Mcap, 256), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
-      k_cross_find<D, P><<<dim3(cdiv(g.Mcap, 4), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
+      k_cross<D, P><<<dim3(cdiv(g.Mcap, 4), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
       break;
     }
     case 2:
       k_rowsum_mfma<D, P, RS_FIXUP, F><<<dim3(rowsM, 1, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, out.rho_tilde);
       break;
-    case 3:
-      k_rowsum_mfma<D, P, RS_SURV_EV, F><<<dim3(rowsM, cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
-      if (g.N > 0) {
-        k_rowsum_mfma<D, P, RS_ADM_BASE, F><<<dim3(rowsN, cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
-        k_rowsum_mfma<D, P, RS_ADM_MUT, F><<<dim3(rowsN, cdiv(g.N, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws, nullptr);
-      }
+    case 3: {
+      const int nadm = g.N > 0 ? (int)rowsN : 0;
+      const unsigned ysplit = cdiv(g.Mcap > g.N ? g.Mcap : g.N, kColsPerSplit);
+      k_maint_mfma<D, P, F><<<dim3(rowsM + 2 * nadm, ysplit, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, (int)rowsM, nadm);
       break;
+    }
     default:
       break;
   }

@@ -47,11 +47,11 @@ struct Workspace {
   int32_t *hole_list;  // [B, Mcap] holes closed by moving states (states violating before the update)
   uint16_t *sk;        // [B, N, d] bf16 candidate keys in score order
   float *snorm;        // [B, N]   their norms
+  uint4 *baug;         // [B, Mcap] column aug step of each bank state (column_aug)
+  uint4 *caug;         // [B, N]   of each candidate, source order
+  uint4 *saug;         // [B, N]   of each candidate, score order
   uint32_t *feas;      // [B, nfw] bit r: prefix length r feasible for this bank
   int nfw;             // words per bank of feas
-  int32_t *xcount;     // [B] states whose first violation lies inside the tested prefixes
-  int32_t *xlist;      // [B, Mcap] those states: slot | (256-candidate chunk << 16)
-  int64_t *xbefore;    // [B, Mcap] their prefix sum before that chunk
   uint64_t *skeys;     // [B, npad] sort keys, sorted within 512-key chunks
   int npad;            // N rounded up to 512
   int nck;
@@ -140,6 +140,18 @@ __device__ __forceinline__ float score_scale(int64_t base, int E) {
 // the rounded integer.
 __device__ __forceinline__ uint32_t q23_round(float w, float scale) {
   return __float_as_uint(__builtin_fmaf(w, scale, 8388608.0f)) - kMagic;
+}
+// Column item's extra K step of the MFMA Gram (bf16 x 8): its norm / sigma^2
+// split exactly into three bf16 pieces, then four ones (the row item's norm
+// pieces and the folded 1 of t = 1 + u), then 0.
+__device__ __forceinline__ uint4 column_aug(float norm, float inv_s2) {
+  const float x = norm * inv_s2;
+  const uint16_t h = f32_to_bf16_bits(x);
+  const float r = x - bf16_bits_to_f32(h);
+  const uint16_t m = f32_to_bf16_bits(r);
+  const uint16_t l = f32_to_bf16_bits(r - bf16_bits_to_f32(m));
+  constexpr uint32_t one = 0x3F80u;
+  return uint4{(uint32_t)h | ((uint32_t)m << 16), (uint32_t)l | (one << 16), one | (one << 16), one};
 }
 #endif
 

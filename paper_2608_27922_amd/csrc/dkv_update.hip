@@ -3,9 +3,9 @@
 // One update of every bank from one block (Supp. C, Algorithm 1) is the kernel
 // sequence below, all on the caller's stream, with r* kept on the device:
 //
-//   k_prep          clamp occupancy/budget, tested prefix R of the group (Eq. 11),
-//                   score scale 1/b of every bank state (Eq. 6)
-//   k_cand_norms    |k_x|^2 of every candidate
+//   k_begin         clamp occupancy/budget, tested prefix R of the group (Eq. 11),
+//                   score scale 1/b of every bank state (Eq. 6), |k_x|^2 of
+//                   every candidate, cleared accumulators
 //   k_score_gram    S_x = sum_i RNE(w_ix / b_i scaled) and Wcol_x = sum_i W_ix (Eq. 6)
 //   k_sort_chunks   stable ascending order of S_x, ties by source index (Alg. 1):
 //   k_sort_rank     512-key chunks sorted in registers, then ranked by search
@@ -16,8 +16,8 @@
 //   k_fixup         projected density rho~(r*) of every bank state
 //   k_select        mandatory + densest eviction (Sec. 3.4 step 3), commit plan
 //   k_maint_gram    weights to the evicted and to the co-admitted states (Supp. C)
-//   k_commit_surv   exact density maintenance of the survivors (Supp. C)
-//   k_commit_adm    admitted K/V placement, densities and baselines (Eq. 5)
+//   k_commit        exact density maintenance of the survivors (Supp. C),
+//                   admitted K/V placement, densities and baselines (Eq. 5)
 //
 // Arithmetic: keys on the 1/64 grid give exact fp32 inner products; weights are
 // binary32 with round-to-nearest-even; every sum is an integer sum of Q23
@@ -97,10 +97,42 @@ __device__ __forceinline__ float dot_row(const float (&kr)[D], const float *col)
 }
 
 // ---------------------------------------------------------------------------
-// k_prep: one workgroup (256 threads) per bank.
+// k_begin: grid (1 + ceil(max(N, Mcap) / 256), B).  Workgroup 0 of a bank
+// clamps occupancy and budget, fixes the tested prefix R of its group (Eq. 11)
+// and the score exponent E, then writes the score scale of every live state
+// (Eq. 6); the other workgroups compute candidate norms, the column aug steps
+// of candidates and bank states, and clear the accumulators that the Gram
+// stages fill with atomic adds.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) void k_prep(dkv_bank bank, Geom g, Workspace ws) {
-  const int b = blockIdx.x;
+template <int D, int DT>
+__global__ __launch_bounds__(kThreads) void k_begin(dkv_bank bank, const void *seg_k, Geom g, Workspace ws,
+                                                    float inv_s2, int norms) {
+  const int b = blockIdx.y;
+  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
+  if (blockIdx.x > 0) {
+    const int j = (blockIdx.x - 1) * kThreads + threadIdx.x;
+    if (j < g.N) {
+      if (norms) {
+        float s = 0.0f;
+        for (int q = 0; q < D; ++q) {
+          const float v = load_elem<DT>(seg_k, (nb + j) * D + q);
+          s = __builtin_fmaf(v, v, s);
+        }
+        ws.cnorm[nb + j] = s;
+        ws.caug[nb + j] = column_aug(s, inv_s2);
+      }
+      ws.acol[nb + j] = 0;
+      ws.wcol[nb + j] = 0;
+      ws.sub_adm[nb + j] = 0;
+      ws.mut_adm[nb + j] = 0;
+    }
+    if (j < g.Mcap) {
+      ws.sub[rb + j] = 0;
+      const int mj = clampi(bank.occupancy[b], 0, clampi(bank.budget[b], 0, g.Mcap));
+      if (j < mj) ws.baug[rb + j] = column_aug(bank.knorm[rb + j], inv_s2);
+    }
+    return;
+  }
   const int Mb = clampi(bank.budget[b], 0, g.Mcap);
   const int m = clampi(bank.occupancy[b], 0, Mb);
   // Tested prefix lengths 0..R: R = min(N, every budget of the group).
@@ -112,7 +144,7 @@ __global__ __launch_bounds__(kThreads) void k_prep(dkv_bank bank, Geom g, Worksp
   __shared__ long long redb[kThreads / 64];
   long long mn = LLONG_MAX;
   for (int i = threadIdx.x; i < m; i += kThreads) {
-    const long long bi = bank.base[(size_t)b * g.Mcap + i];
+    const long long bi = bank.base[rb + i];
     mn = bi < mn ? bi : mn;
   }
 #pragma unroll
@@ -128,6 +160,7 @@ __global__ __launch_bounds__(kThreads) void k_prep(dkv_bank bank, Geom g, Worksp
     const long long bi = mn < 1 ? 1 : mn;
     frexpf((float)(8388608.0 / (double)bi), &E);
   }
+  for (int i = threadIdx.x; i < m; i += kThreads) ws.bs[rb + i] = score_scale(bank.base[rb + i], E);
   if (threadIdx.x == 0) {
     ws.m[b] = m;
     ws.M[b] = Mb;
@@ -136,39 +169,12 @@ __global__ __launch_bounds__(kThreads) void k_prep(dkv_bank bank, Geom g, Worksp
   }
 }
 
-// Score scale of every live bank state (after k_prep has fixed E).
-__global__ void k_bscale(dkv_bank bank, Geom g, Workspace ws) {
-  const int b = blockIdx.y, i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= ws.m[b]) return;
-  const size_t o = (size_t)b * g.Mcap + i;
-  ws.bs[o] = score_scale(bank.base[o], ws.E[b]);
-}
-
-// Accumulators filled with integer atomic adds by the Gram stages.
-__global__ void k_zero(Geom g, Workspace ws) {
-  const size_t nN = (size_t)g.B * g.N, nM = (size_t)g.B * g.Mcap;
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < nN; i += stride) {
-    ws.acol[i] = 0;
-    ws.wcol[i] = 0;
-    ws.sub_adm[i] = 0;
-    ws.mut_adm[i] = 0;
-  }
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < nM; i += stride) ws.sub[i] = 0;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < (size_t)g.B; i += stride) ws.xcount[i] = 0;
-}
-
 template <int D, int DT>
-__global__ __launch_bounds__(kThreads) void k_cand_norms(const void *seg_k, Geom g, Workspace ws) {
-  const int b = blockIdx.y, x = blockIdx.x * kThreads + threadIdx.x;
-  if (x >= g.N) return;
-  const size_t row = (size_t)b * g.N + x;
-  float s = 0.0f;
-  for (int j = 0; j < D; ++j) {
-    float v = load_elem<DT>(seg_k, row * D + j);
-    s = __builtin_fmaf(v, v, s);
-  }
-  ws.cnorm[row] = s;
+void launch_begin(const dkv_bank &bank, const void *seg_k, const Geom &g, const Prm &p, const Workspace &ws,
+                  bool norms, hipStream_t s) {
+  const int span = g.N > g.Mcap ? g.N : g.Mcap;
+  k_begin<D, DT><<<dim3((unsigned)(1 + (span + kThreads - 1) / kThreads), (unsigned)g.B), kThreads, 0, s>>>(
+      bank, seg_k, g, ws, p.inv_sigma2, norms ? 1 : 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -771,9 +777,9 @@ __global__ __launch_bounds__(kThreads) void k_maint_gram(dkv_bank bank, const vo
 // over the final bank, frozen baseline max(rho, delta) (Eq. 5), provenance.
 // ---------------------------------------------------------------------------
 template <int D, int DT>
-__global__ __launch_bounds__(kThreads) void k_commit_surv(dkv_bank bank, Geom g, Workspace ws) {
+__device__ __forceinline__ void commit_surv(const dkv_bank &bank, const Geom &g, const Workspace &ws, int bx) {
   using E = typename std::conditional<DT == DKV_BF16, uint16_t, float>::type;
-  const int b = blockIdx.y, v = blockIdx.x * kThreads + threadIdx.x;
+  const int b = blockIdx.y, v = bx * kThreads + threadIdx.x;
   if (v >= ws.m[b]) return;
   const size_t rb = (size_t)b * g.Mcap;
   const int to = ws.dest[rb + v];
@@ -794,12 +800,12 @@ __global__ __launch_bounds__(kThreads) void k_commit_surv(dkv_bank bank, Geom g,
 }
 
 template <int D, int DT>
-__global__ __launch_bounds__(kThreads) void k_commit_adm(dkv_bank bank, dkv_segment seg, Geom g, Prm p,
-                                                         Workspace ws) {
+__device__ __forceinline__ void commit_adm(const dkv_bank &bank, const dkv_segment &seg, const Geom &g,
+                                           const Prm &p, const Workspace &ws, int bx) {
   using E = typename std::conditional<DT == DKV_BF16, uint16_t, float>::type;
   constexpr int kCh = D * (int)sizeof(E) / 16;  // 16-byte chunks per key (and per value) row
   const int b = blockIdx.y;
-  const int t = blockIdx.x * kThreads + threadIdx.x;
+  const int t = bx * kThreads + threadIdx.x;
   const int k = t / (2 * kCh), ch = t % (2 * kCh);
   const int rs = ws.r_star[b / g.gs];
   if (k >= rs || k >= g.N) return;
@@ -823,6 +829,16 @@ __global__ __launch_bounds__(kThreads) void k_commit_adm(dkv_bank bank, dkv_segm
     bank.prov[rb + to] = ((int64_t)p.block_id << 32) | (int64_t)x;
     bank.knorm[rb + to] = ws.cnorm[nb + x];
   }
+}
+
+// Commit (Eq. 12) in one launch: the first nx_surv workgroups update the
+// survivors (and move the few that close holes), the rest place the admitted
+// candidates.  The two write disjoint slots.
+template <int D, int DT>
+__global__ __launch_bounds__(kThreads) void k_commit(dkv_bank bank, dkv_segment seg, Geom g, Prm p, Workspace ws,
+                                                     int nx_surv) {
+  if ((int)blockIdx.x < nx_surv) commit_surv<D, DT>(bank, g, ws, blockIdx.x);
+  else commit_adm<D, DT>(bank, seg, g, p, ws, blockIdx.x - nx_surv);
 }
 
 // ---------------------------------------------------------------------------
@@ -878,11 +894,8 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
   dkv_update_out out = outp ? *outp : dkv_update_out{};
   // bf16 banks: Gram stages on MFMA; fp32 banks: the same stages on the VALU.
   constexpr bool kMfma = DT == DKV_BF16;
-  k_prep<<<g.B, kThreads, 0, s>>>(bank, g, ws);
-  k_zero<<<1024, 256, 0, s>>>(g, ws);
-  k_bscale<<<grid2(g.Mcap, 256, g.B), 256, 0, s>>>(bank, g, ws);
+  launch_begin<D, DT>(bank, seg.k, g, p, ws, g.N > 0, s);
   if (g.N > 0) {
-    k_cand_norms<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(seg.k, g, ws);
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 0);
     else k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, nullptr, nullptr);
     k_sort_chunks<<<dim3((unsigned)((g.N + kChunk - 1) / kChunk), (unsigned)g.B), 64, 0, s>>>(g, ws, out.score_q);
@@ -899,8 +912,11 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
   k_select<<<g.B, kBig, 0, s>>>(bank, g, ws, out);
   if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 3);
   else k_maint_gram<D, DT><<<grid2(g.Mcap + g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws);
-  k_commit_surv<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, g, ws);
-  if (g.N > 0) k_commit_adm<D, DT><<<grid2(g.N * (2 * D * (DT == DKV_BF16 ? 2 : 4) / 16), kThreads, g.B), kThreads, 0, s>>>(bank, seg, g, p, ws);
+  {
+    const int nxs = (g.Mcap + kThreads - 1) / kThreads;
+    const int nxa = g.N > 0 ? (g.N * (2 * D * (DT == DKV_BF16 ? 2 : 4) / 16) + kThreads - 1) / kThreads : 0;
+    k_commit<D, DT><<<dim3((unsigned)(nxs + nxa), (unsigned)g.B), kThreads, 0, s>>>(bank, seg, g, p, ws, nxs);
+  }
   return hipGetLastError();
 }
 
@@ -908,11 +924,7 @@ template <int D, int DT>
 hipError_t score_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                       int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws,
                       hipStream_t s) {
-  k_prep<<<g.B, kThreads, 0, s>>>(bank, g, ws);
-  k_zero<<<1024, 256, 0, s>>>(g, ws);
-  k_bscale<<<grid2(g.Mcap, 256, g.B), 256, 0, s>>>(bank, g, ws);
-  if (g.N > 0 && (score_q || score_f))
-    k_cand_norms<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(seg.k, g, ws);
+  launch_begin<D, DT>(bank, seg.k, g, p, ws, g.N > 0 && (score_q || score_f), s);
   if constexpr (DT == DKV_BF16) {
     launch_score_mfma(bank, seg, g, p, (g.N > 0) ? score_q : nullptr, (g.N > 0) ? score_f : nullptr, density, ws, s);
   } else {
