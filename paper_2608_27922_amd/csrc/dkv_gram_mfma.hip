@@ -579,87 +579,131 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, co
 }
 
 // ---------------------------------------------------------------------------
-// First violating prefix length of every bank state (Eqs. 8-9), one wave per
-// state.  The chunk sums of the ordered candidates (64 per chunk, two chunks
-// per lane) are prefix-summed across the wave; the first chunk whose end lifts
-// rho + P to tau b (2^k (rho + P) >= T b, integers) is re-walked with one
-// ordered candidate per lane (same binary32 weights) for the exact length.
-// States that never reach the bound within the tested prefixes get R + 1.
+// First violating prefix length of every bank state (Eqs. 8-9).  A wave takes
+// eight states, one per group of 8 lanes; each lane adds 16 of the state's
+// 64-candidate chunk sums, a scan over the group gives every chunk's end
+// prefix, and the first chunk whose end lifts rho + P to tau b
+// (2^k (rho + P) >= T b, integers) is found by ballot.  For each state that
+// crosses, the whole wave then re-walks that chunk with one ordered candidate
+// per lane (same binary32 weights) for the exact length.  States that never
+// reach the bound within the tested prefixes get R + 1.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
   const uint32_t lo = __shfl((uint32_t)v, src, 64), hi = __shfl((uint32_t)(v >> 32), src, 64);
   return ((uint64_t)hi << 32) | lo;
 }
 
+constexpr int kCrossLanes = 8;                      // lanes per state
+constexpr int kCrossPerLane = 16;                   // chunk sums per lane
+constexpr int kCrossStates = 64 / kCrossLanes;      // states per wave
+
 template <int D, int P>
 __global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
   static_assert(kCkStride == 64, "one candidate per lane in the exact walk");
-  static_assert((DKV_MAX_CANDIDATES + kCkStride - 1) / kCkStride <= 128, "two chunk sums per lane");
+  static_assert((DKV_MAX_CANDIDATES + kCkStride - 1) / kCkStride <= kCrossLanes * kCrossPerLane,
+                "every chunk sum of a state is held by its lane group");
   const int b = blockIdx.y;
-  const int l = threadIdx.x & 63;
-  const int i = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int l = threadIdx.x & 63, grp = l / kCrossLanes, q = l % kCrossLanes;
+  const int i0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kCrossStates;
   const int m = ws.m[b], R = ws.R[b];
-  if (i >= m) return;  // whole wave
-  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N, row = rb + i;
+  if (i0 >= m) return;  // whole wave
+  const int i = i0 + grp;
+  const bool valid = i < m;
+  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
+  const size_t row = rb + (valid ? i : i0);
   const int64_t lim = ((int64_t)p.tau_num * bank.base[row] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
   const int64_t thr = lim - bank.rho[row];
-  int first = R + 1;
-  if (thr <= 0) {
-    first = 0;
-  } else {
-    const int nch = (R + kCkStride - 1) / kCkStride;
-    const uint32_t *ckr = ws.ck + row * ws.nck;
-    const uint32_t c0 = 2 * l < nch ? ckr[2 * l] : 0u;
-    const uint32_t c1 = 2 * l + 1 < nch ? ckr[2 * l + 1] : 0u;
-    uint64_t incl = (uint64_t)c0 + c1;
+  const int nch = (R + kCkStride - 1) / kCkStride;
+  // this lane's chunk sums [16 q, 16 q + 16)
+  uint32_t c[kCrossPerLane];
+  const uint4 *ckr = reinterpret_cast<const uint4 *>(ws.ck + row * ws.nck);
+#pragma unroll
+  for (int v4 = 0; v4 < kCrossPerLane / 4; ++v4) {
+    const int c0 = kCrossPerLane * q + 4 * v4;
+    uint4 x = {0u, 0u, 0u, 0u};
+    if (c0 < nch) x = ckr[c0 / 4];  // rows hold nck >= nch sums, a multiple of 4
+    c[4 * v4 + 0] = c0 + 0 < nch ? x.x : 0u;
+    c[4 * v4 + 1] = c0 + 1 < nch ? x.y : 0u;
+    c[4 * v4 + 2] = c0 + 2 < nch ? x.z : 0u;
+    c[4 * v4 + 3] = c0 + 3 < nch ? x.w : 0u;
+  }
+  uint64_t tot = 0;
+#pragma unroll
+  for (int t = 0; t < kCrossPerLane; ++t) tot += c[t];
+  uint64_t incl = tot;
+#pragma unroll
+  for (int o = 1; o < kCrossLanes; o <<= 1) {
+    const uint64_t y = (uint64_t)__shfl_up((uint32_t)incl, o, kCrossLanes) |
+                       ((uint64_t)__shfl_up((uint32_t)(incl >> 32), o, kCrossLanes) << 32);
+    if (q >= o) incl += y;
+  }
+  // first chunk of this lane whose end prefix reaches thr, and the prefix before it
+  uint64_t run = incl - tot, pre = 0;
+  int ft = -1;
+#pragma unroll
+  for (int t = 0; t < kCrossPerLane; ++t) {
+    const uint64_t nx = run + c[t];
+    if (ft < 0 && kCrossPerLane * q + t < nch && (int64_t)nx >= thr) {
+      ft = t;
+      pre = run;
+    }
+    run = nx;
+  }
+  const bool thr_pos = thr > 0;
+  const unsigned long long hits = __ballot(valid && thr_pos && ft >= 0);
+  // group result (held by every lane of the group): crossing chunk and prefix before it
+  const unsigned gbits = (unsigned)(hits >> (kCrossLanes * grp)) & ((1u << kCrossLanes) - 1);
+  const int src = kCrossLanes * grp + (gbits ? __ffs(gbits) - 1 : 0);
+  const int ch = kCrossPerLane * (src % kCrossLanes) + __shfl(ft, src, 64);
+  const uint64_t pb = shfl_u64(pre, src);
+  int first = thr_pos ? R + 1 : 0;
+  // exact walk, one crossing state at a time (wave-uniform loop)
+  unsigned long long todo = 0;
+#pragma unroll
+  for (int s2 = 0; s2 < kCrossStates; ++s2)
+    if ((hits >> (kCrossLanes * s2)) & ((1ull << kCrossLanes) - 1)) todo |= 1ull << s2;
+  while (todo) {
+    const int s2 = __ffsll(todo) - 1;
+    todo &= todo - 1;
+    const int sl = kCrossLanes * s2;  // first lane of that state's group
+    const size_t srow = rb + i0 + s2;
+    const int c_s = __shfl(ch, sl, 64);
+    const int64_t pb_s = (int64_t)shfl_u64(pb, sl);
+    const int64_t thr_s = (int64_t)shfl_u64((uint64_t)thr, sl);
+    const uint16_t *rk = static_cast<const uint16_t *>(bank.k) + srow * D;
+    const float nr = bank.knorm[srow];
+    const int col = c_s * kCkStride + l;
+    uint32_t W = 0;
+    if (col < R) {
+      const uint16_t *ckey = ws.sk + (nb + col) * D;
+      float acc = 0.0f;
+#pragma unroll
+      for (int j = 0; j < D; j += 8) {
+        const u32x4 ra = *reinterpret_cast<const u32x4 *>(rk + j);
+        const u32x4 rc = *reinterpret_cast<const u32x4 *>(ckey + j);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc = __builtin_fmaf(__uint_as_float(ra[e] << 16), __uint_as_float(rc[e] << 16), acc);
+          acc = __builtin_fmaf(__uint_as_float(ra[e] & 0xFFFF0000u), __uint_as_float(rc[e] & 0xFFFF0000u), acc);
+        }
+      }
+      const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
+      W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
+    }
+    uint32_t wi = W;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-      const uint64_t y = __shfl_up((uint32_t)incl, o, 64) | ((uint64_t)__shfl_up((uint32_t)(incl >> 32), o, 64) << 32);
-      if (l >= o) incl += y;
+      const uint32_t y = __shfl_up(wi, o, 64);
+      if (l >= o) wi += y;
     }
-    const uint64_t before = incl - c0 - c1;  // chunks < 2 l
-    const bool hit0 = 2 * l < nch && (int64_t)(before + c0) >= thr;
-    const bool hit1 = 2 * l + 1 < nch && (int64_t)incl >= thr;
-    const unsigned long long hl = __ballot(hit0 || hit1);
-    if (hl != 0) {
-      const int lf = __ffsll(hl) - 1;
-      const bool second = !__shfl((int)hit0, lf, 64);
-      const int c = 2 * lf + (second ? 1 : 0);
-      const int64_t pb = (int64_t)shfl_u64(second ? before + c0 : before, lf);  // prefix before chunk c
-      const uint16_t *rk = static_cast<const uint16_t *>(bank.k) + row * D;
-      const float nr = bank.knorm[row];
-      const int col = c * kCkStride + l;
-      uint32_t W = 0;
-      if (col < R) {
-        const uint16_t *ckey = ws.sk + (nb + col) * D;
-        float acc = 0.0f;
-#pragma unroll
-        for (int j = 0; j < D; j += 8) {
-          const u32x4 a = *reinterpret_cast<const u32x4 *>(rk + j);
-          const u32x4 bb = *reinterpret_cast<const u32x4 *>(ckey + j);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            acc = __builtin_fmaf(__uint_as_float(a[e] << 16), __uint_as_float(bb[e] << 16), acc);
-            acc = __builtin_fmaf(__uint_as_float(a[e] & 0xFFFF0000u), __uint_as_float(bb[e] & 0xFFFF0000u), acc);
-          }
-        }
-        const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
-        W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
-      }
-      uint32_t wi = W;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(wi, o, 64);
-        if (l >= o) wi += y;
-      }
-      const unsigned long long h2 = __ballot(pb + (int64_t)wi >= thr);
-      first = h2 != 0 ? c * kCkStride + (__ffsll(h2) - 1) + 1
-                      : min(R, (c + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
-    }
+    const unsigned long long h2 = __ballot(pb_s + (int64_t)wi >= thr_s);
+    const int f = h2 != 0 ? c_s * kCkStride + (__ffsll(h2) - 1) + 1
+                          : min(R, (c_s + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
+    if (grp == s2) first = f;
   }
-  if (l == 0) {
-    ws.first[row] = first;
-    if (out_first) out_first[row] = first;
+  if (valid && q == 0) {
+    ws.first[rb + i] = first;
+    if (out_first) out_first[rb + i] = first;
   }
 }
 
@@ -717,7 +761,7 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       if (g.N > 0)
         k_rowsum_mfma<D, P, RS_CHUNK, F><<<dim3(rowsM, cdiv(g.N, kChunksPerSplit * kCkStride), g.B), T, 0, s>>>(
             bank, seg.k, g, p, ws, nullptr);
-      k_cross<D, P><<<dim3(cdiv(g.Mcap, 4), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
+      k_cross<D, P><<<dim3(cdiv(g.Mcap, 4 * kCrossStates), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
       break;
     }
     case 2:

@@ -113,10 +113,33 @@ __global__ __launch_bounds__(kThreads) void k_begin(dkv_bank bank, const void *s
     const int j = (blockIdx.x - 1) * kThreads + threadIdx.x;
     if (j < g.N) {
       if (norms) {
+        // |k|^2 in element order, 16-byte loads
         float s = 0.0f;
-        for (int q = 0; q < D; ++q) {
-          const float v = load_elem<DT>(seg_k, (nb + j) * D + q);
-          s = __builtin_fmaf(v, v, s);
+        if constexpr (DT == DKV_BF16) {
+          const uint4 *src = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(seg_k) + (nb + j) * D);
+          uint4 x[D / 8];
+#pragma unroll
+          for (int q = 0; q < D / 8; ++q) x[q] = src[q];
+#pragma unroll
+          for (int q = 0; q < D / 8; ++q) {
+            const uint32_t w4[4] = {x[q].x, x[q].y, x[q].z, x[q].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const float lo = __uint_as_float(w4[e] << 16), hi = __uint_as_float(w4[e] & 0xFFFF0000u);
+              s = __builtin_fmaf(lo, lo, s);
+              s = __builtin_fmaf(hi, hi, s);
+            }
+          }
+        } else {
+          const float4 *src = reinterpret_cast<const float4 *>(static_cast<const float *>(seg_k) + (nb + j) * D);
+#pragma unroll 8
+          for (int q = 0; q < D / 4; ++q) {
+            const float4 x = src[q];
+            s = __builtin_fmaf(x.x, x.x, s);
+            s = __builtin_fmaf(x.y, x.y, s);
+            s = __builtin_fmaf(x.z, x.z, s);
+            s = __builtin_fmaf(x.w, x.w, s);
+          }
         }
         ws.cnorm[nb + j] = s;
         ws.caug[nb + j] = column_aug(s, inv_s2);
@@ -143,9 +166,16 @@ __global__ __launch_bounds__(kThreads) void k_begin(dkv_bank bank, const void *s
   // the value at the smallest baseline (the division and rounding are monotone).
   __shared__ long long redb[kThreads / 64];
   long long mn = LLONG_MAX;
-  for (int i = threadIdx.x; i < m; i += kThreads) {
-    const long long bi = bank.base[rb + i];
-    mn = bi < mn ? bi : mn;
+  // four independent loads per round trip
+  for (int i0 = threadIdx.x; i0 < m; i0 += 4 * kThreads) {
+    long long bq[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * kThreads;
+      bq[u] = i < m ? (long long)bank.base[rb + i] : LLONG_MAX;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) mn = bq[u] < mn ? bq[u] : mn;
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
@@ -160,7 +190,19 @@ __global__ __launch_bounds__(kThreads) void k_begin(dkv_bank bank, const void *s
     const long long bi = mn < 1 ? 1 : mn;
     frexpf((float)(8388608.0 / (double)bi), &E);
   }
-  for (int i = threadIdx.x; i < m; i += kThreads) ws.bs[rb + i] = score_scale(bank.base[rb + i], E);
+  for (int i0 = threadIdx.x; i0 < m; i0 += 4 * kThreads) {
+    long long bq[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * kThreads;
+      bq[u] = i < m ? (long long)bank.base[rb + i] : 1;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * kThreads;
+      if (i < m) ws.bs[rb + i] = score_scale(bq[u], E);
+    }
+  }
   if (threadIdx.x == 0) {
     ws.m[b] = m;
     ws.M[b] = Mb;
@@ -899,7 +941,7 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 0);
     else k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, nullptr, nullptr);
     k_sort_chunks<<<dim3((unsigned)((g.N + kChunk - 1) / kChunk), (unsigned)g.B), 64, 0, s>>>(g, ws, out.score_q);
-    k_sort_rank<<<dim3(4u, (unsigned)g.B), kBig, 0, s>>>(g, ws, out.order);
+    k_sort_rank<<<dim3((unsigned)((ws.npad + kBig - 1) / kBig), (unsigned)g.B), kBig, 0, s>>>(g, ws, out.order);
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 4);
   }
   // with no candidates only states that already violate are found (prefix 0)
