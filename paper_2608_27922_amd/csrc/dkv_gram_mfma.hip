@@ -617,11 +617,12 @@ __global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Wor
   // this lane's chunk sums [16 q, 16 q + 16)
   uint32_t c[kCrossPerLane];
   const uint4 *ckr = reinterpret_cast<const uint4 *>(ws.ck + row * ws.nck);
+  const int nq4 = ws.nck / 4;  // 16-byte groups per row (nck >= nch, a multiple of 4)
 #pragma unroll
   for (int v4 = 0; v4 < kCrossPerLane / 4; ++v4) {
     const int c0 = kCrossPerLane * q + 4 * v4;
     uint4 x = {0u, 0u, 0u, 0u};
-    if (c0 < nch) x = ckr[c0 / 4];  // rows hold nck >= nch sums, a multiple of 4
+    if (nq4 > 0) x = ckr[min(c0 / 4, nq4 - 1)];  // clamped, unconditional per lane
     c[4 * v4 + 0] = c0 + 0 < nch ? x.x : 0u;
     c[4 * v4 + 1] = c0 + 1 < nch ? x.y : 0u;
     c[4 * v4 + 2] = c0 + 2 < nch ? x.z : 0u;
@@ -708,21 +709,39 @@ __global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Wor
 }
 
 // Candidate keys and norms in score order, so that the ordered passes stream
-// contiguous rows: one thread per 16-byte chunk of a key row.
+// contiguous rows: one thread per 16-byte chunk of kGatherRows key rows
+// (every load and store instruction covers whole rows).
+constexpr int kGatherRows = 4;
+
 template <int D>
 __global__ __launch_bounds__(256) void k_gather_sorted(const void *seg_k, Geom g, Workspace ws, float inv_s2) {
-  constexpr int CH = D / 8;  // 16-byte chunks per bf16 row
+  constexpr int CH = D / 8;      // 16-byte chunks per bf16 row
+  constexpr int RPP = 256 / CH;  // rows per workgroup pass
+  static_assert(kGatherRows <= CH, "one metadata lane per row of the group");
   const int b = blockIdx.y;
-  const int t = blockIdx.x * 256 + threadIdx.x;
-  const int j = t / CH, c = t % CH;
-  if (j >= g.N) return;
+  const int c = threadIdx.x % CH;
+  const int j0 = blockIdx.x * RPP * kGatherRows + threadIdx.x / CH;
   const size_t nb = (size_t)b * g.N;
-  const int x = ws.order[nb + j];
-  const u32x4 *src = reinterpret_cast<const u32x4 *>(static_cast<const uint16_t *>(seg_k) + (nb + x) * D);
-  reinterpret_cast<u32x4 *>(ws.sk + (nb + j) * D)[c] = src[c];
-  if (c == 0) {
-    ws.snorm[nb + j] = ws.cnorm[nb + x];
-    ws.saug[nb + j] = ws.caug[nb + x];
+  if (blockIdx.x * RPP * kGatherRows >= g.N) return;  // whole workgroup
+  // loads from clamped (in-range) rows, unconditional so that they overlap
+  int xs[kGatherRows];
+#pragma unroll
+  for (int u = 0; u < kGatherRows; ++u) xs[u] = ws.order[nb + min(j0 + u * RPP, g.N - 1)];
+  u32x4 tmp[kGatherRows];
+#pragma unroll
+  for (int u = 0; u < kGatherRows; ++u)
+    tmp[u] = reinterpret_cast<const u32x4 *>(static_cast<const uint16_t *>(seg_k) + (nb + xs[u]) * D)[c];
+#pragma unroll
+  for (int u = 0; u < kGatherRows; ++u)
+    if (j0 + u * RPP < g.N) reinterpret_cast<u32x4 *>(ws.sk + (nb + j0 + u * RPP) * D)[c] = tmp[u];
+  // lane c < kGatherRows of a row group copies the norm and norm step of row c
+  if (c < kGatherRows) {
+    const int j = j0 + c * RPP;
+    if (j < g.N) {
+      const int x = ws.order[nb + j];
+      ws.snorm[nb + j] = ws.cnorm[nb + x];
+      ws.saug[nb + j] = ws.caug[nb + x];
+    }
   }
 }
 
@@ -755,7 +774,7 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       k_score_mfma<D, P, F><<<dim3(rowsN, cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws);
       break;
     case 4:
-      k_gather_sorted<D><<<dim3(cdiv(g.N * (D / 8), 256), g.B), 256, 0, s>>>(seg.k, g, ws, p.inv_sigma2);
+      k_gather_sorted<D><<<dim3(cdiv(g.N, 256 / (D / 8) * kGatherRows), g.B), 256, 0, s>>>(seg.k, g, ws, p.inv_sigma2);
       break;
     case 1: {
       if (g.N > 0)

@@ -172,7 +172,8 @@ __global__ __launch_bounds__(kThreads) void k_begin(dkv_bank bank, const void *s
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int i = i0 + u * kThreads;
-      bq[u] = i < m ? (long long)bank.base[rb + i] : LLONG_MAX;
+      const long long bv = bank.base[rb + min(i, m - 1)];  // clamped, unconditional
+      bq[u] = i < m ? bv : LLONG_MAX;
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) mn = bq[u] < mn ? bq[u] : mn;
@@ -195,7 +196,7 @@ __global__ __launch_bounds__(kThreads) void k_begin(dkv_bank bank, const void *s
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int i = i0 + u * kThreads;
-      bq[u] = i < m ? (long long)bank.base[rb + i] : 1;
+      bq[u] = bank.base[rb + min(i, m - 1)];  // clamped, unconditional
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
@@ -584,12 +585,33 @@ __global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspac
   __shared__ int sh_bucket, sh_below, sh_cnt;
   const size_t rb = (size_t)b * g.Mcap;
 
-  // violators and candidates for the fill
+  // this thread's candidate ranks (admitted list below), loaded up front
+  const int N = g.N;
+  const size_t nb = (size_t)b * N;
+  constexpr int kPerN = (DKV_MAX_CANDIDATES + kBig - 1) / kBig;
+  const int perN = (N + kBig - 1) / kBig;
+  const int loN = min(N, (int)threadIdx.x * perN), hiN = min(N, loN + perN);
+  int rk[kPerN];
+#pragma unroll
+  for (int u = 0; u < kPerN; ++u) {
+    const int r = N > 0 ? ws.rank[nb + min(loN + u, N - 1)] : INT_MAX;  // clamped, unconditional
+    rk[u] = loN + u < hiN ? r : INT_MAX;
+  }
+  // violators and candidates for the fill (four independent loads per round trip)
   int nv_local = 0;
-  for (int i = threadIdx.x; i < m; i += kBig) {
-    const bool v = ws.first[rb + i] <= rs;
-    st[i] = v ? ST_VIOL : ST_CAND;
-    nv_local += v;
+  for (int i0 = threadIdx.x; i0 < m; i0 += 4 * kBig) {
+    int f[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) f[u] = ws.first[rb + min(i0 + u * kBig, m - 1)];  // clamped, unconditional
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = i0 + u * kBig;
+      if (i < m) {
+        const bool v = f[u] <= rs;
+        st[i] = v ? ST_VIOL : ST_CAND;
+        nv_local += v;
+      }
+    }
   }
   int nv;
   (void)block_excl_scan(nv_local, &nv, tmp);
@@ -642,6 +664,7 @@ __global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspac
     if (st[i] == ST_VIOL || st[i] == ST_SEL) {
       ws.ev_list[rb + pos] = i;
       ws.dest[rb + i] = -1 - pos;  // provisional: encodes the evicted rank
+      if (pos < rs) ws.adm_dest[nb + pos] = i;  // admitted entry pos fills the pos-th evicted slot
       ++pos;
     } else {
       ws.surv_list[rb + spos] = i;
@@ -649,21 +672,20 @@ __global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspac
       ++spos;
     }
   }
-  // admitted list: source indices x with rank(x) < r*, ascending
-  const int N = g.N;
-  const size_t nb = (size_t)b * N;
-  const int perN = (N + kBig - 1) / kBig;
-  const int loN = min(N, (int)threadIdx.x * perN), hiN = min(N, loN + perN);
+  // admitted list: source indices x with rank(x) < r*, ascending; entries
+  // beyond the evicted slots are appended after the old occupancy
   int ca = 0;
-  for (int x = loN; x < hiN; ++x) ca += ws.rank[nb + x] < rs;
+#pragma unroll
+  for (int u = 0; u < kPerN; ++u) ca += rk[u] < rs;
   int n_adm;
   int pa = block_excl_scan(ca, &n_adm, tmp);
   __syncthreads();
   const int m_new = m - n_ev + rs;
-  for (int x = loN; x < hiN; ++x) {
-    if (ws.rank[nb + x] < rs) {
-      ws.adm_list[nb + pa] = x;
-      ws.adm_dest[nb + pa] = pa < n_ev ? ws.ev_list[rb + pa] : m + (pa - n_ev);
+#pragma unroll
+  for (int u = 0; u < kPerN; ++u) {
+    if (rk[u] < rs) {
+      ws.adm_list[nb + pa] = loN + u;
+      if (pa >= n_ev) ws.adm_dest[nb + pa] = m + (pa - n_ev);
       ++pa;
     }
   }
@@ -841,35 +863,57 @@ __device__ __forceinline__ void commit_surv(const dkv_bank &bank, const Geom &g,
   bank.rho[rb + to] = rho;
 }
 
+constexpr int kCommitRows = 1;  // admitted tokens per thread (more was measured slower)
+
 template <int D, int DT>
 __device__ __forceinline__ void commit_adm(const dkv_bank &bank, const dkv_segment &seg, const Geom &g,
                                            const Prm &p, const Workspace &ws, int bx) {
   using E = typename std::conditional<DT == DKV_BF16, uint16_t, float>::type;
   constexpr int kCh = D * (int)sizeof(E) / 16;  // 16-byte chunks per key (and per value) row
+  constexpr int kTokWG = kThreads / (2 * kCh);  // tokens per workgroup pass
+  static_assert(kThreads % (2 * kCh) == 0, "whole tokens per workgroup pass");
+  static_assert(kCommitRows <= 2 * kCh, "one metadata lane per token of the group");
   const int b = blockIdx.y;
-  const int t = bx * kThreads + threadIdx.x;
-  const int k = t / (2 * kCh), ch = t % (2 * kCh);
-  const int rs = ws.r_star[b / g.gs];
-  if (k >= rs || k >= g.N) return;
+  const int ch = threadIdx.x % (2 * kCh);
+  const int k0 = bx * kTokWG * kCommitRows + threadIdx.x / (2 * kCh);
+  const int rs = min(ws.r_star[b / g.gs], g.N);
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
-  const int x = ws.adm_list[nb + k];
-  const int to = ws.adm_dest[nb + k];
   const bool isv = ch >= kCh;
   const int c = isv ? ch - kCh : ch;
-  const E *src = static_cast<const E *>(isv ? seg.v : seg.k) + (nb + x) * D;
-  E *dst = static_cast<E *>(isv ? bank.v : bank.k) + (rb + to) * D;
-  reinterpret_cast<uint4 *>(dst)[c] = reinterpret_cast<const uint4 *>(src)[c];
-  if (ch == 0) {
+  if (bx * kTokWG * kCommitRows >= rs) return;  // whole workgroup
+  // loads from clamped (in-range) entries, unconditional so that they overlap;
+  // only the stores are predicated
+  int xs[kCommitRows], tos[kCommitRows];
+#pragma unroll
+  for (int u = 0; u < kCommitRows; ++u) {
+    const int kc = min(k0 + u * kTokWG, rs - 1);
+    xs[u] = ws.adm_list[nb + kc];
+    tos[u] = ws.adm_dest[nb + kc];
+  }
+  uint4 tmp[kCommitRows];
+#pragma unroll
+  for (int u = 0; u < kCommitRows; ++u)
+    tmp[u] = reinterpret_cast<const uint4 *>(static_cast<const E *>(isv ? seg.v : seg.k) + (nb + xs[u]) * D)[c];
+#pragma unroll
+  for (int u = 0; u < kCommitRows; ++u)
+    if (k0 + u * kTokWG < rs)
+      reinterpret_cast<uint4 *>(static_cast<E *>(isv ? bank.v : bank.k) + (rb + tos[u]) * D)[c] = tmp[u];
+  if (ch < kCommitRows) {
     // density over the final bank: survivors (directly, or the whole old bank
-    // minus the evicted) plus the other co-admitted candidates
-    const int m = ws.m[b];
-    const int n_ev = ws.n_ev[b];
-    const int64_t surv_sum = (n_ev <= m - n_ev) ? ws.wcol[nb + x] - ws.sub_adm[nb + k] : ws.sub_adm[nb + k];
-    const int64_t rho = surv_sum + ws.mut_adm[nb + k];
-    bank.rho[rb + to] = rho;
-    bank.base[rb + to] = rho > p.delta_q ? rho : p.delta_q;
-    bank.prov[rb + to] = ((int64_t)p.block_id << 32) | (int64_t)x;
-    bank.knorm[rb + to] = ws.cnorm[nb + x];
+    // minus the evicted) plus the other co-admitted candidates; lane ch of the
+    // token group writes the metadata of its ch-th token
+    const int k = k0 + ch * kTokWG;
+    if (k < rs) {
+      const int m = ws.m[b];
+      const int n_ev = ws.n_ev[b];
+      const int x = ws.adm_list[nb + k], to = ws.adm_dest[nb + k];
+      const int64_t surv_sum = (n_ev <= m - n_ev) ? ws.wcol[nb + x] - ws.sub_adm[nb + k] : ws.sub_adm[nb + k];
+      const int64_t rho = surv_sum + ws.mut_adm[nb + k];
+      bank.rho[rb + to] = rho;
+      bank.base[rb + to] = rho > p.delta_q ? rho : p.delta_q;
+      bank.prov[rb + to] = ((int64_t)p.block_id << 32) | (int64_t)x;
+      bank.knorm[rb + to] = ws.cnorm[nb + x];
+    }
   }
 }
 
@@ -956,7 +1000,8 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
   else k_maint_gram<D, DT><<<grid2(g.Mcap + g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws);
   {
     const int nxs = (g.Mcap + kThreads - 1) / kThreads;
-    const int nxa = g.N > 0 ? (g.N * (2 * D * (DT == DKV_BF16 ? 2 : 4) / 16) + kThreads - 1) / kThreads : 0;
+    const int tok_per_wg = kThreads / (2 * D * (DT == DKV_BF16 ? 2 : 4) / 16) * kCommitRows;
+    const int nxa = g.N > 0 ? (g.N + tok_per_wg - 1) / tok_per_wg : 0;
     k_commit<D, DT><<<dim3((unsigned)(nxs + nxa), (unsigned)g.B), kThreads, 0, s>>>(bank, seg, g, p, ws, nxs);
   }
   return hipGetLastError();
