@@ -59,6 +59,19 @@ C11 Maintenance (Supp. C, "Exact density maintenance"): survivors
     rho <- Phi over the final bank, b <- max(rho, delta).
 C12 Empty bank: the first min(N, M) candidates in source order, rho = Phi of
     the resulting bank, b = max(rho, delta) (Alg. 1, first branch).
+
+Policy ablations (Supp. E, "Candidate ordering", "Density baseline",
+"Eviction rule"; Table 1(b)), each off by default:
+V1  source_order: the tested prefixes follow the candidates' source order
+    instead of the score order; the scores are still reported.
+V2  refresh_base: after every update every retained state's baseline is
+    recomputed from its current density, b <- max(rho, delta).
+V3  eviction = "densest": no mandatory set; the e_{r*} states of largest
+    rho~(r*) are released (ties as in C9).  The prefix rule (C7-C8) is
+    unchanged, so a violator that is not among them stays in the bank.
+V4  eviction = "mandatory_source": all violators, then the non-violators in
+    source order, read as admission order (ascending provenance, then slot).
+The independent per-head variant is a layer of one head (group size 1).
 """
 
 from __future__ import annotations
@@ -81,6 +94,10 @@ class Params:
     tau_num: int = 2
     tau_log2_den: int = 0
     delta_q: int = 8  # RNE(1e-6 * 2^23)
+    # policy ablations (V1-V4 above); the defaults are the paper's policy
+    source_order: bool = False
+    refresh_base: bool = False
+    eviction: str = "default"  # "default" | "densest" | "mandatory_source"
 
     def __post_init__(self):
         if self.p not in (1, 2, 4):
@@ -89,6 +106,8 @@ class Params:
             raise ValueError("tau must be a positive dyadic rational")
         if self.delta_q < 1:
             raise ValueError("delta must be at least one fixed-point unit")
+        if self.eviction not in ("default", "densest", "mandatory_source"):
+            raise ValueError("eviction must be 'default', 'densest' or 'mandatory_source'")
 
     @property
     def tau(self) -> float:
@@ -257,7 +276,10 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
             scores.append((None, 0))
         else:
             S, E, _ = candidate_scores(bank.K, bank.base, Kc64[h], prm)
-            orders.append(np.argsort(S, kind="stable").astype(np.int64))  # ties: source order
+            if prm.source_order:
+                orders.append(np.arange(N, dtype=np.int64))               # V1
+            else:
+                orders.append(np.argsort(S, kind="stable").astype(np.int64))  # ties: source order
             scores.append((S, E))
 
     # ---- Step 2: violators c_r for every tested prefix, shared r* (Eqs. 8-11)
@@ -301,12 +323,18 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
         e = e_of(h, r_star)
         rho_t = bank.rho + prefix[h][:, r_star] if m else np.zeros(0, np.int64)
         viol = _violates(rho_t, bank.base, prm)
+        if prm.eviction == "densest":
+            viol = np.zeros(m, bool)                                    # V3: no mandatory set
         mandatory = np.nonzero(viol)[0]
         evict = list(mandatory)
         if len(evict) < e:
             rest = np.nonzero(~viol)[0]
-            # decreasing rho~(r*); ties: earlier admission (provenance), then slot
-            key_order = np.lexsort((rest, bank.prov[rest], -rho_t[rest]))
+            if prm.eviction == "mandatory_source":
+                # V4: admission order (provenance), then slot
+                key_order = np.lexsort((rest, bank.prov[rest]))
+            else:
+                # decreasing rho~(r*); ties: earlier admission (provenance), then slot
+                key_order = np.lexsort((rest, bank.prov[rest], -rho_t[rest]))
             evict.extend(rest[key_order[: e - len(evict)]])
         evicted = np.array(sorted(int(s) for s in evict), np.int64)
         admitted = np.sort(pi[:r_star])
@@ -363,6 +391,8 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
             for dst, src in zip(low_holes, movers):
                 K[dst], V[dst] = K[src], V[src]
                 rho[dst], base[dst], prov[dst] = rho[src], base[src], prov[src]
+        if prm.refresh_base:
+            base = np.maximum(rho, prm.delta_q)                         # V2
         nb = BankState(bank.budget, K[:m_new].copy(), V[:m_new].copy(), rho[:m_new].copy(),
                        base[:m_new].copy(), prov[:m_new].copy())
         new_heads.append(nb)

@@ -8,6 +8,11 @@ density is recomputed from scratch over the final bank.  This is the paper's
 update (Sec. 3.4, Eqs. 5-12; Supp. C, Algorithm 1) evaluated in real
 arithmetic, so any oracle decision on a well-separated tiny case must agree
 with it, and every oracle fixed-point density must round to it.
+
+The policy ablations of Table 1(b) (Supp. E) are options of ``update``:
+source-order candidates, refreshed baselines, densest-only eviction and
+mandatory + source-order eviction (source order of a bank state = its
+admission order, i.e. ascending provenance).
 """
 
 from fractions import Fraction as F
@@ -24,11 +29,14 @@ def phi(keys, i, sigma2, p):
     return sum((weight(keys[i], keys[j], sigma2, p) for j in range(len(keys)) if j != i), F(0))
 
 
-def update(bank, cands, M, sigma2=1, p=1, tau=F(2), delta=F(1, 10 ** 6), block_id=1):
+def update(bank, cands, M, sigma2=1, p=1, tau=F(2), delta=F(1, 10 ** 6), block_id=1, r_star=None,
+           source_order=False, refresh_base=False, eviction="default"):
     """bank: list of dicts {key, b, prov}; cands: list of key tuples (source order).
 
-    Returns (new_bank, info) where new_bank lists dicts {key, rho, b, prov} in the
-    commit layout survivors-in-place / admitted-into-holes-then-appended."""
+    ``r_star`` forces the admitted prefix length (a layer's shared r*); by default
+    it is this bank's own largest feasible r.  Returns (new_bank, info) where
+    new_bank lists dicts {key, rho, b, prov} in the commit layout
+    survivors-in-place / admitted-into-holes-then-appended."""
     N, m = len(cands), len(bank)
     R = min(N, M)
     keys = [s["key"] for s in bank]
@@ -38,7 +46,7 @@ def update(bank, cands, M, sigma2=1, p=1, tau=F(2), delta=F(1, 10 ** 6), block_i
     else:
         scores = [sum((weight(k, x, sigma2, p) / s["b"] for k, s in zip(keys, bank)), F(0)) / m
                   for x in cands]
-        pi = sorted(range(N), key=lambda x: (scores[x], x))
+        pi = list(range(N)) if source_order else sorted(range(N), key=lambda x: (scores[x], x))
     c, proj = [], []
     for r in range(R + 1):
         hyp = keys + [cands[pi[j]] for j in range(r)]
@@ -47,11 +55,16 @@ def update(bank, cands, M, sigma2=1, p=1, tau=F(2), delta=F(1, 10 ** 6), block_i
         c.append(sum(1 for i in range(m) if pr[i] / bank[i]["b"] >= tau))
     e = [max(0, m + r - M) for r in range(R + 1)]
     feas = [r for r in range(R + 1) if c[r] <= e[r]]
-    r_star = max(feas) if feas else 0
+    if r_star is None:
+        r_star = max(feas) if feas else 0
     pr = proj[r_star]
     viol = [i for i in range(m) if pr[i] / bank[i]["b"] >= tau]
-    evict = list(viol)
-    rest = sorted((i for i in range(m) if i not in viol), key=lambda i: (-pr[i], bank[i]["prov"], i))
+    evict = [] if eviction == "densest" else list(viol)
+    if eviction == "mandatory_source":
+        fill_key = lambda i: (bank[i]["prov"], i)
+    else:
+        fill_key = lambda i: (-pr[i], bank[i]["prov"], i)
+    rest = sorted((i for i in range(m) if i not in evict), key=fill_key)
     evict += rest[: max(0, e[r_star] - len(evict))]
     evict = sorted(evict)
     admitted = sorted(pi[:r_star])
@@ -70,7 +83,7 @@ def update(bank, cands, M, sigma2=1, p=1, tau=F(2), delta=F(1, 10 ** 6), block_i
     fk = [s["key"] for s in new_bank]
     for i, s in enumerate(new_bank):
         s["rho"] = phi(fk, i, sigma2, p)
-        if s["b"] is None:
+        if s["b"] is None or refresh_base:
             s["b"] = max(s["rho"], delta)
     info = dict(r_star=r_star, pi=pi, scores=scores, c=c, e=e, evicted=evict, admitted=admitted,
                 violators=viol, projected=pr)

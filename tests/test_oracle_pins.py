@@ -256,6 +256,78 @@ def test_tiny_rollout_matches_exact_bruteforce(seed):
                 assert abs(q / Q23 - float(ref)) <= heads[h].m * 2.0 ** -22
 
 
+POLICIES = {
+    "source_order": dict(source_order=True),
+    "refresh_base": dict(refresh_base=True),
+    "densest": dict(eviction="densest"),
+    "mandatory_source": dict(eviction="mandatory_source"),
+}
+
+
+@pytest.mark.parametrize("policy", list(POLICIES))
+def test_policy_rollouts_match_exact_bruteforce(policy):
+    """The policy ablations of Table 1(b) (Supp. E): on random multi-head rollouts the
+    oracle's order, violator counts, shared r*, eviction and admission sets, commit
+    layout, densities and baselines equal the exact-rational brute force run with the
+    same policy, and the policy changes at least one decision against the default."""
+    kw = POLICIES[policy]
+    d, H, M = 2, 3, 7
+    prm = Params(sigma2_log2=0, p=2, **kw)
+    differs = 0
+    for seed in range(4):
+        rng = np.random.default_rng(100 + seed)
+        heads = [BankState.empty(M, d) for _ in range(H)]
+        for blk in range(1, 8):
+            N = int(rng.integers(2, 6))
+            Ks = [np.rint(rng.standard_normal((N, d)) * 4) / 2 for _ in range(H)]
+            new, rec = update_layer(heads, Ks, [k.astype(np.float32) for k in Ks], blk, prm)
+            cands = [[tuple(F(float(v)) for v in row) for row in Ks[h]] for h in range(H)]
+            infos = [xr.update(_to_exact_bank(heads[h]), cands[h], M, sigma2=1, p=2, block_id=blk, **kw)[1]
+                     for h in range(H)]
+            feas = [r for r in range(rec.R + 1) if all(infos[h]["c"][r] <= infos[h]["e"][r] for h in range(H))]
+            assert rec.r_star == (max(feas) if feas else 0)
+            for h in range(H):
+                xb, info = xr.update(_to_exact_bank(heads[h]), cands[h], M, sigma2=1, p=2, block_id=blk,
+                                     r_star=rec.r_star, **kw)
+                _, dflt = xr.update(_to_exact_bank(heads[h]), cands[h], M, sigma2=1, p=2, block_id=blk,
+                                    r_star=rec.r_star)
+                hr, nb = rec.heads[h], new[h]
+                assert list(hr.c) == info["c"]
+                if heads[h].m:
+                    assert list(hr.pi) == info["pi"]
+                assert hr.evicted.tolist() == info["evicted"]
+                assert hr.admitted.tolist() == info["admitted"]
+                assert nb.prov.tolist() == [s["prov"] for s in xb]
+                tol = max(nb.m, 1) * 2.0 ** -22
+                for q, s in zip(nb.rho, xb):
+                    assert abs(q / Q23 - float(s["rho"])) <= tol
+                for q, s in zip(nb.base, xb):
+                    assert abs(q / Q23 - float(s["b"])) <= tol
+                if policy == "source_order":
+                    differs += heads[h].m > 0 and info["pi"] != sorted(range(N), key=lambda x: (info["scores"][x], x))
+                elif policy == "refresh_base":
+                    old = {int(pv): int(bs) for pv, bs in zip(heads[h].prov, heads[h].base)}
+                    differs += any(int(pv) in old and int(bs) != old[int(pv)] for pv, bs in zip(nb.prov, nb.base))
+                else:
+                    differs += info["evicted"] != dflt["evicted"]
+            heads = new
+    assert differs > 0, "the policy never changed a decision in these rollouts"
+
+
+def test_refresh_base_keeps_delta_floor():
+    """Refreshed baselines (Table 1(b), Supp. E) still obey b >= delta (Eq. 5): isolated
+    keys have rho = 0 after the update, so every refreshed baseline is delta."""
+    prm = Params(sigma2_log2=0, p=2, refresh_base=True)
+    keys = np.array([[0.0], [1000.0]])
+    bank, _ = update_layer([BankState.empty(4, 1)], [keys], [keys.astype(np.float32)], 0, prm)
+    new, rec = update_layer(bank, [np.array([[-1000.0]])], [np.zeros((1, 1), np.float32)], 1, prm)
+    assert rec.r_star == 1 and new[0].m == 3
+    assert new[0].rho.tolist() == [0, 0, 0]
+    assert new[0].base.tolist() == [prm.delta_q] * 3
+    xb, _ = xr.update(_to_exact_bank(bank[0]), [(F(-1000),)], 4, sigma2=1, p=2, refresh_base=True)
+    assert [float(s["b"]) for s in xb] == [1e-6] * 3
+
+
 # ---------------------------------------------------------------- invariants on cluster data
 
 def _small_cfg(**kw):
