@@ -32,6 +32,8 @@ PEAK_HBM_GBS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 ATTN_SOURCE = os.path.join(ROOT, "paper_2608_27922_amd", "csrc", "dkv_attention.hip")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_attn_mfma_single_layer_traffic.md")
+# dkv_params.flags of each policy ablation (Table 1(b); independent per-head = group size 1)
+POLICIES = {"default": 0, "source_order": 0x1, "refresh_base": 0x2, "densest_only": 0x4, "source_fill": 0x8}
 
 
 def parse():
@@ -41,6 +43,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="single_layer", help="tiny or single_layer")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--policy", default="default", choices=sorted(POLICIES),
+                    help="policy ablation of Table 1(b) run by the update (default: the paper's policy)")
     ap.add_argument("--cpu-heads", type=int, default=12,
                     help="heads in the oracle sample (12 = the whole single_layer step, about 10 s on 16 host threads)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -107,6 +111,7 @@ def main():
     case = synth.single_update_case(cfg)
     to = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dt).cuda().contiguous()
     prm = api.Params(sigma2_log2=cfg.sigma2_log2)
+    run_prm = api.Params(sigma2_log2=cfg.sigma2_log2, flags=POLICIES[args.policy])
     B, N, d = cfg.heads, cfg.n_cand, cfg.d
     bank = api.Bank(B, cfg.budget, d, dtype=dt, group_size=cfg.group_size)
     init_k, init_v = to(case["init_K"]), to(case["init_V"])
@@ -123,7 +128,7 @@ def main():
         bank.restore(snap)
         if ev is not None:
             ev[0].record(stream)
-        api.update_bank(bank, seg_k, seg_v, 1, prm, workspace=ws)
+        api.update_bank(bank, seg_k, seg_v, 1, run_prm, workspace=ws)
         if ev is not None:
             ev[1].record(stream)
         api.bank_attention(bank, q, wk, wv, out=out)
@@ -163,7 +168,7 @@ def main():
                                f"{cfg.dtype}, budget {cfg.budget} (starts full), segment {N} (30% near-duplicates), "
                                f"{cfg.n_query} queries over bank + {cfg.n_window}-token window",
                    "banks": B, "group_size": cfg.group_size, "candidates": N, "budget": cfg.budget,
-                   "queries": cfg.n_query, "window": cfg.n_window, "head_dim": d},
+                   "queries": cfg.n_query, "window": cfg.n_window, "head_dim": d, "policy": args.policy},
         "update_ms": round(upd_ms, 4),
         "update_tokens_per_s_per_layer_head": round(N / (upd_ms * 1e-3), 1),
         "attention_ms": round(att_ms, 4),
@@ -180,7 +185,7 @@ def main():
             torch.neg(src, out=dst)      # reads and writes nbytes each
         torch.cuda.synchronize()
         result["copy_probe_bytes"] = nbytes
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.policy == "default":
         result["cpu_baseline"] = cpu_baseline(case, cfg, min(args.cpu_heads, cfg.heads))
     print(json.dumps(result), flush=True)
 

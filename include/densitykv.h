@@ -48,7 +48,7 @@ extern "C" {
 
 typedef enum {
   DKV_OK = 0,
-  DKV_ERR_INVALID = -1,     /* NULL pointer, bad enum, flags != 0               */
+  DKV_ERR_INVALID = -1,     /* NULL pointer, bad enum, unknown policy flags     */
   DKV_ERR_SHAPE = -2,       /* sizes out of range or inconsistent               */
   DKV_ERR_UNSUPPORTED = -3, /* head_dim, p or sigma^2 not supported             */
   DKV_ERR_WORKSPACE = -4,   /* workspace NULL or smaller than required          */
@@ -114,8 +114,30 @@ typedef struct {
   int32_t tau_num;      /* tau = tau_num / 2^tau_log2_den, tau > 1, tau_num <= 2^16 */
   int32_t tau_log2_den; /* 0..8 */
   int64_t delta_q;      /* baseline floor in Q23 units, 1..2^40 */
-  uint32_t flags;       /* reserved, must be 0 */
+  uint32_t flags;       /* 0 (the paper's policy) or DKV_POLICY_* bits below */
 } dkv_params;
+
+/* Policy ablations of Table 1(b), defined in the supplementary ablation details
+ * (Supp. E: "Candidate ordering", "Density baseline", "Eviction rule").  They
+ * change only the prefix order, the baseline update or the eviction fill; the
+ * Gram stages, the prefix feasibility test (Eqs. 8-11) and the maintenance are
+ * the same.  DENSEST_ONLY and SOURCE_FILL are exclusive; any other bit is
+ * rejected with DKV_ERR_INVALID.  (The independent per-head variant is
+ * group_size = 1.)
+ *   SOURCE_ORDER  the tested prefixes follow the candidates' source order
+ *                 instead of the score order (scores are still computed and
+ *                 reported in score_q)
+ *   REFRESH_BASE  after the update every retained state's baseline is
+ *                 recomputed from its maintained density: b = max(rho, delta)
+ *   DENSEST_ONLY  no mandatory set: the e_{r*} states of largest rho~(r*) are
+ *                 released (ties: smaller provenance, then lower slot); a
+ *                 violator outside them stays in the bank
+ *   SOURCE_FILL   all violators, then the non-violators in admission order
+ *                 (ascending provenance, then slot) until e_{r*} are released */
+#define DKV_POLICY_SOURCE_ORDER 0x1u
+#define DKV_POLICY_REFRESH_BASE 0x2u
+#define DKV_POLICY_DENSEST_ONLY 0x4u
+#define DKV_POLICY_SOURCE_FILL 0x8u
 
 /* Optional outputs of densitykv_update_bank (any pointer may be NULL).
  *   r_star       [G]        admitted prefix length of each group (Eq. 11)

@@ -19,6 +19,12 @@ LIB_PATH = os.path.join(_HERE, "libdensitykv.so")
 
 DKV_BF16, DKV_F32 = 0, 1
 MAX_CANDIDATES, MAX_CAPACITY, MAX_BLOCK_ID = 8191, 32767, 16777215
+# dkv_params.flags: policy ablations of Table 1(b) (0 = the paper's policy)
+POLICY_SOURCE_ORDER = 0x1   # prefixes in source order instead of score order
+POLICY_REFRESH_BASE = 0x2   # b = max(rho, delta) for every retained state after the update
+POLICY_DENSEST_ONLY = 0x4   # no mandatory set: release the e densest states
+POLICY_SOURCE_FILL = 0x8    # violators, then fill in admission order
+
 ENTRY_POINTS = ("densitykv_workspace_size", "densitykv_score", "densitykv_update_bank",
                 "densitykv_bank_attention", "densitykv_pair_weight_q23", "densitykv_status_string")
 

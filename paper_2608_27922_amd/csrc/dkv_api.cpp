@@ -91,7 +91,10 @@ int check_segment(const dkv_segment *sg) {
 
 int check_params(const dkv_params *p, Prm *out, int block_id) {
   if (!p) return DKV_ERR_INVALID;
-  if (p->flags != 0) return DKV_ERR_INVALID;
+  const uint32_t known = DKV_POLICY_SOURCE_ORDER | DKV_POLICY_REFRESH_BASE | DKV_POLICY_DENSEST_ONLY |
+                         DKV_POLICY_SOURCE_FILL;
+  if (p->flags & ~known) return DKV_ERR_INVALID;
+  if ((p->flags & DKV_POLICY_DENSEST_ONLY) && (p->flags & DKV_POLICY_SOURCE_FILL)) return DKV_ERR_INVALID;
   if (p->p != 1 && p->p != 2 && p->p != 4) return DKV_ERR_UNSUPPORTED;
   if (p->sigma2_log2 < -8 || p->sigma2_log2 > 16) return DKV_ERR_UNSUPPORTED;
   if (p->tau_log2_den < 0 || p->tau_log2_den > 8) return DKV_ERR_RANGE;
@@ -104,6 +107,7 @@ int check_params(const dkv_params *p, Prm *out, int block_id) {
   out->tau_shift = p->tau_log2_den;
   out->delta_q = p->delta_q;
   out->block_id = block_id;
+  out->flags = p->flags;
   return DKV_OK;
 }
 

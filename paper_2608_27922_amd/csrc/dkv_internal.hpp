@@ -69,6 +69,7 @@ struct Prm {
   int tau_num, tau_shift;
   int64_t delta_q;
   int block_id;
+  uint32_t flags;  // DKV_POLICY_* bits
 };
 
 // Launchers (host functions defined in the .hip sources; return hipError_t).

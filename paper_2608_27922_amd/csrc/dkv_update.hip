@@ -288,7 +288,7 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
   return ((uint64_t)hi << 32) | lo;
 }
 
-__global__ __launch_bounds__(64) void k_sort_chunks(Geom g, Workspace ws, int64_t *out_score) {
+__global__ __launch_bounds__(64) void k_sort_chunks(Geom g, Workspace ws, int64_t *out_score, int source_order) {
   const int b = blockIdx.y, c = blockIdx.x, lane = threadIdx.x;
   const size_t nb = (size_t)b * g.N;
   uint64_t v[8];
@@ -298,7 +298,8 @@ __global__ __launch_bounds__(64) void k_sort_chunks(Geom g, Workspace ws, int64_
     uint64_t key = ~0ull;
     if (idx < g.N) {
       const int64_t A = ws.acol[nb + idx];
-      key = ((uint64_t)A << 13) | (uint64_t)idx;  // ascending score, ties by source index
+      // ascending score, ties by source index; or source order alone (policy ablation)
+      key = source_order ? (uint64_t)idx : (((uint64_t)A << 13) | (uint64_t)idx);
       if (out_score) out_score[nb + idx] = A;
     }
     v[r] = key;
@@ -574,7 +575,11 @@ __device__ __forceinline__ int sel_digit(const Workspace &ws, const dkv_bank &ba
 }
 
 __global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspace ws,
-                                                 dkv_update_out out) {
+                                                 dkv_update_out out, uint32_t flags) {
+  // policy ablations: no mandatory set, or a fill in admission order (key
+  // (provenance, slot): the radix passes over rho~ are skipped)
+  const bool no_mandatory = (flags & DKV_POLICY_DENSEST_ONLY) != 0;
+  const int first_pass = (flags & DKV_POLICY_SOURCE_FILL) ? 5 : 0;
   const int b = blockIdx.x;
   const int m = ws.m[b];
   const int rs = ws.r_star[b / g.gs];
@@ -607,7 +612,7 @@ __global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspac
     for (int u = 0; u < 4; ++u) {
       const int i = i0 + u * kBig;
       if (i < m) {
-        const bool v = f[u] <= rs;
+        const bool v = !no_mandatory && f[u] <= rs;
         st[i] = v ? ST_VIOL : ST_CAND;
         nv_local += v;
       }
@@ -624,7 +629,7 @@ __global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspac
     __syncthreads();
   }
   if (need > 0) {
-    for (int pass = 0; pass < 15; ++pass) {
+    for (int pass = first_pass; pass < 15; ++pass) {
       for (int t = threadIdx.x; t < 256; t += kBig) hist[t] = 0;
       __syncthreads();
       for (int i = threadIdx.x; i < m; i += kBig)
@@ -841,7 +846,8 @@ __global__ __launch_bounds__(kThreads) void k_maint_gram(dkv_bank bank, const vo
 // over the final bank, frozen baseline max(rho, delta) (Eq. 5), provenance.
 // ---------------------------------------------------------------------------
 template <int D, int DT>
-__device__ __forceinline__ void commit_surv(const dkv_bank &bank, const Geom &g, const Workspace &ws, int bx) {
+__device__ __forceinline__ void commit_surv(const dkv_bank &bank, const Geom &g, const Prm &p, const Workspace &ws,
+                                            int bx) {
   using E = typename std::conditional<DT == DKV_BF16, uint16_t, float>::type;
   const int b = blockIdx.y, v = bx * kThreads + threadIdx.x;
   if (v >= ws.m[b]) return;
@@ -861,6 +867,8 @@ __device__ __forceinline__ void commit_surv(const dkv_bank &bank, const Geom &g,
     bank.knorm[rb + to] = bank.knorm[rb + v];
   }
   bank.rho[rb + to] = rho;
+  // refreshed baselines (policy ablation): b = max(rho, delta) after the update
+  if (p.flags & DKV_POLICY_REFRESH_BASE) bank.base[rb + to] = rho > p.delta_q ? rho : p.delta_q;
 }
 
 constexpr int kCommitRows = 1;  // admitted tokens per thread (more was measured slower)
@@ -923,7 +931,7 @@ __device__ __forceinline__ void commit_adm(const dkv_bank &bank, const dkv_segme
 template <int D, int DT>
 __global__ __launch_bounds__(kThreads) void k_commit(dkv_bank bank, dkv_segment seg, Geom g, Prm p, Workspace ws,
                                                      int nx_surv) {
-  if ((int)blockIdx.x < nx_surv) commit_surv<D, DT>(bank, g, ws, blockIdx.x);
+  if ((int)blockIdx.x < nx_surv) commit_surv<D, DT>(bank, g, p, ws, blockIdx.x);
   else commit_adm<D, DT>(bank, seg, g, p, ws, blockIdx.x - nx_surv);
 }
 
@@ -984,7 +992,8 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
   if (g.N > 0) {
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 0);
     else k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, nullptr, nullptr);
-    k_sort_chunks<<<dim3((unsigned)((g.N + kChunk - 1) / kChunk), (unsigned)g.B), 64, 0, s>>>(g, ws, out.score_q);
+    k_sort_chunks<<<dim3((unsigned)((g.N + kChunk - 1) / kChunk), (unsigned)g.B), 64, 0, s>>>(
+        g, ws, out.score_q, (p.flags & DKV_POLICY_SOURCE_ORDER) ? 1 : 0);
     k_sort_rank<<<dim3((unsigned)((ws.npad + kBig - 1) / kBig), (unsigned)g.B), kBig, 0, s>>>(g, ws, out.order);
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 4);
   }
@@ -995,7 +1004,7 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
   k_feas_group<<<g.G, kBig, 0, s>>>(g, ws, out.r_star);
   if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 2);
   else k_fixup<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.rho_tilde);
-  k_select<<<g.B, kBig, 0, s>>>(bank, g, ws, out);
+  k_select<<<g.B, kBig, 0, s>>>(bank, g, ws, out, p.flags);
   if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 3);
   else k_maint_gram<D, DT><<<grid2(g.Mcap + g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws);
   {

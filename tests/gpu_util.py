@@ -21,8 +21,12 @@ def host(t: torch.Tensor) -> np.ndarray:
 
 
 def oracle_params(p: api.Params) -> OParams:
+    f = p.flags
+    eviction = ("densest" if f & api.POLICY_DENSEST_ONLY else
+                "mandatory_source" if f & api.POLICY_SOURCE_FILL else "default")
     return OParams(sigma2_log2=p.sigma2_log2, p=p.p, tau_num=p.tau_num, tau_log2_den=p.tau_log2_den,
-                   delta_q=p.delta_q)
+                   delta_q=p.delta_q, source_order=bool(f & api.POLICY_SOURCE_ORDER),
+                   refresh_base=bool(f & api.POLICY_REFRESH_BASE), eviction=eviction)
 
 
 def mirror(bank: api.Bank, b: int) -> BankState:

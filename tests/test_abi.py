@@ -78,7 +78,9 @@ def test_update_rejects_bad_arguments_before_launch(L):
     assert upd(b, seg, api.Params(tau_num=1).c(), 1 << 40) == -5          # tau must exceed 1
     assert upd(b, seg, api.Params(tau_num=2, tau_log2_den=1).c(), 1 << 40) == -5
     assert upd(b, seg, api.Params(delta_q=0).c(), 1 << 40) == -5
-    assert upd(b, seg, api.Params(flags=1).c(), 1 << 40) == -1
+    assert upd(b, seg, api.Params(flags=0x10).c(), 1 << 40) == -1          # unknown policy bit
+    both = api.POLICY_DENSEST_ONLY | api.POLICY_SOURCE_FILL
+    assert upd(b, seg, api.Params(flags=both).c(), 1 << 40) == -1          # exclusive eviction policies
     assert upd(b, api.DkvSegment(9000, 3, 1, 1), good, 1 << 40) == -2
     assert upd(b, api.DkvSegment(100, -1, 1, 1), good, 1 << 40) == -5
     assert upd(b, api.DkvSegment(100, 3, None, 1), good, 1 << 40) == -1

@@ -122,6 +122,23 @@ def test_rollout_parameter_sweep(tau, p, s):
     _run_rollout(cfg, 5, api.Params(sigma2_log2=s, p=p, tau_num=tau[0], tau_log2_den=tau[1]), dup_every=2)
 
 
+POLICY_FLAGS = {"source_order": api.POLICY_SOURCE_ORDER, "refresh_base": api.POLICY_REFRESH_BASE,
+                "densest_only": api.POLICY_DENSEST_ONLY, "source_fill": api.POLICY_SOURCE_FILL,
+                "source_order+refresh": api.POLICY_SOURCE_ORDER | api.POLICY_REFRESH_BASE}
+
+
+@pytest.mark.parametrize("dt,d", [("bf16", 128), ("f32", 64)])
+@pytest.mark.parametrize("policy", list(POLICY_FLAGS))
+def test_rollout_policy_ablations(policy, dt, d):
+    """The policy ablations of Table 1(b): same rollout shape as the default test,
+    near-duplicate blocks (mandatory evictions) and full banks (fills), every
+    intermediate and the committed bank bit-exact against the oracle run with the
+    same policy."""
+    _log(f"rollout policy {policy} dt={dt} d={d}")
+    cfg = synth.Config(heads=6, d=d, dtype=dt, n_cand=200, budget=300, group_size=3, **SMALL)
+    _run_rollout(cfg, 6, api.Params(sigma2_log2=4 if d == 64 else 5, flags=POLICY_FLAGS[policy]), dup_every=2)
+
+
 def test_empty_bank_more_candidates_than_budget():
     """Alg. 1 first branch: first min(N, M) source-ordered candidates, N > M."""
     _log("empty bank N > M")
