@@ -11,7 +11,8 @@
  *   densitykv_score           Soft-Riesz candidate scores (Eq. 6) and, on
  *                             request, every bank state's density (Eq. 3);
  *   densitykv_update_bank     the full update of Algorithm 1 for all banks;
- *   densitykv_bank_attention  softmax(q k^T * scale) v over [bank; window].
+ *   densitykv_bank_attention  softmax(q k^T * scale) v over [bank; window];
+ *   densitykv_bank_attention_sink  the same over [bank; window; sink].
  *
  * Conventions shared by every entry point
  *   - Every pointer inside the structs and every array argument is DEVICE
@@ -216,6 +217,23 @@ int densitykv_update_bank(dkv_bank *bank, const dkv_segment *seg, const dkv_para
 int densitykv_bank_attention(const dkv_bank *bank, const void *q, int32_t n_query,
                              const void *win_k, const void *win_v, int32_t n_window,
                              void *out, float softmax_scale, void *stream);
+
+/*
+ * The same attention in the paper's deployment context (Supp. D, memory
+ * budget and temporal alignment): a first-frame sink, the local window and the
+ * retained bank read together, out = softmax(q K^T * scale) V with
+ * K = [bank k[0:m_b]; window k; sink k].  Arguments as densitykv_bank_attention,
+ * plus
+ *   sink_k, sink_v [B, n_sink, d]  bank dtype; may be NULL when n_sink = 0
+ * Keys are used as given (already post-RoPE, memory keys with the temporal
+ * coordinate set as the backbone does); no mask is applied.  Same errors as
+ * densitykv_bank_attention, and DKV_ERR_INVALID for a NULL sink with
+ * n_sink > 0.  densitykv_bank_attention is this call with n_sink = 0.
+ */
+int densitykv_bank_attention_sink(const dkv_bank *bank, const void *q, int32_t n_query,
+                                  const void *sink_k, const void *sink_v, int32_t n_sink,
+                                  const void *win_k, const void *win_v, int32_t n_window,
+                                  void *out, float softmax_scale, void *stream);
 
 /*
  * The per-pair contract on its own: w_q23[i] = RNE(w(d2[i]) * 2^23) with

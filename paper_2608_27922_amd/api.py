@@ -26,7 +26,8 @@ POLICY_DENSEST_ONLY = 0x4   # no mandatory set: release the e densest states
 POLICY_SOURCE_FILL = 0x8    # violators, then fill in admission order
 
 ENTRY_POINTS = ("densitykv_workspace_size", "densitykv_score", "densitykv_update_bank",
-                "densitykv_bank_attention", "densitykv_pair_weight_q23", "densitykv_status_string")
+                "densitykv_bank_attention", "densitykv_bank_attention_sink", "densitykv_pair_weight_q23",
+                "densitykv_status_string")
 
 _vp = ctypes.c_void_p
 
@@ -71,6 +72,8 @@ def lib() -> ctypes.CDLL:
                                             ctypes.c_size_t, _vp]
         L.densitykv_bank_attention.argtypes = [P(DkvBank), _vp, ctypes.c_int32, _vp, _vp, ctypes.c_int32, _vp,
                                                ctypes.c_float, _vp]
+        L.densitykv_bank_attention_sink.argtypes = [P(DkvBank), _vp, ctypes.c_int32, _vp, _vp, ctypes.c_int32,
+                                                    _vp, _vp, ctypes.c_int32, _vp, ctypes.c_float, _vp]
         L.densitykv_pair_weight_q23.argtypes = [_vp, ctypes.c_int64, P(DkvParams), _vp, _vp]
         L.densitykv_status_string.argtypes = [ctypes.c_int]
         L.densitykv_status_string.restype = ctypes.c_char_p
@@ -259,24 +262,49 @@ def update_bank(bank: Bank, seg_k: Optional[torch.Tensor], seg_v: Optional[torch
     return out
 
 
+def _kv_segment(bank: Bank, k: Optional[torch.Tensor], v: Optional[torch.Tensor], what: str) -> int:
+    if k is None:
+        return 0
+    if k.dim() != 3 or k.shape[0] != bank.B or k.shape[2] != bank.d or v is None or v.shape != k.shape:
+        raise ValueError(f"{what} must be [num_banks, n, head_dim] keys and values")
+    if not (k.is_contiguous() and v.is_contiguous()) or k.dtype != bank.dtype or v.dtype != bank.dtype:
+        raise ValueError(f"{what} tensors must be contiguous in the bank dtype")
+    return int(k.shape[1])
+
+
+def _check_q(bank: Bank, q: torch.Tensor):
+    if q.dim() != 3 or q.shape[0] != bank.B or q.shape[2] != bank.d or q.dtype != bank.dtype or not q.is_contiguous():
+        raise ValueError("q must be a contiguous [num_banks, n_query, head_dim] tensor in the bank dtype")
+
+
 def bank_attention(bank: Bank, q: torch.Tensor, win_k: Optional[torch.Tensor], win_v: Optional[torch.Tensor],
                    softmax_scale: Optional[float] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
     """densitykv_bank_attention: softmax(q [bank; window]^T * scale) [bank; window]."""
-    if q.dim() != 3 or q.shape[0] != bank.B or q.shape[2] != bank.d or q.dtype != bank.dtype or not q.is_contiguous():
-        raise ValueError("q must be a contiguous [num_banks, n_query, head_dim] tensor in the bank dtype")
-    nw = 0
-    if win_k is not None:
-        if win_k.shape[0] != bank.B or win_k.shape[2] != bank.d or win_v is None or win_v.shape != win_k.shape:
-            raise ValueError("window must be [num_banks, n_window, head_dim] keys and values")
-        if not (win_k.is_contiguous() and win_v.is_contiguous()) or win_k.dtype != bank.dtype or win_v.dtype != bank.dtype:
-            raise ValueError("window tensors must be contiguous in the bank dtype")
-        nw = int(win_k.shape[1])
+    _check_q(bank, q)
+    nw = _kv_segment(bank, win_k, win_v, "window")
     if out is None:
         out = torch.empty_like(q)
     scale = (1.0 / bank.d ** 0.5) if softmax_scale is None else float(softmax_scale)
     cb = bank.c()
     _check(lib().densitykv_bank_attention(ctypes.byref(cb), _ptr(q), int(q.shape[1]), _ptr(win_k), _ptr(win_v),
                                           nw, _ptr(out), ctypes.c_float(scale), _stream()), "bank_attention")
+    return out
+
+
+def bank_attention_sink(bank: Bank, q: torch.Tensor, sink_k: Optional[torch.Tensor], sink_v: Optional[torch.Tensor],
+                        win_k: Optional[torch.Tensor], win_v: Optional[torch.Tensor],
+                        softmax_scale: Optional[float] = None, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """densitykv_bank_attention_sink: softmax over [bank; window; sink]."""
+    _check_q(bank, q)
+    ns = _kv_segment(bank, sink_k, sink_v, "sink")
+    nw = _kv_segment(bank, win_k, win_v, "window")
+    if out is None:
+        out = torch.empty_like(q)
+    scale = (1.0 / bank.d ** 0.5) if softmax_scale is None else float(softmax_scale)
+    cb = bank.c()
+    _check(lib().densitykv_bank_attention_sink(ctypes.byref(cb), _ptr(q), int(q.shape[1]), _ptr(sink_k),
+                                               _ptr(sink_v), ns, _ptr(win_k), _ptr(win_v), nw, _ptr(out),
+                                               ctypes.c_float(scale), _stream()), "bank_attention_sink")
     return out
 
 

@@ -171,19 +171,29 @@ int densitykv_update_bank(dkv_bank *bank, const dkv_segment *seg, const dkv_para
   return e == hipSuccess ? DKV_OK : DKV_ERR_HIP;
 }
 
+int densitykv_bank_attention_sink(const dkv_bank *bank, const void *q, int32_t n_query, const void *sink_k,
+                                  const void *sink_v, int32_t n_sink, const void *win_k, const void *win_v,
+                                  int32_t n_window, void *out, float softmax_scale, void *stream) {
+  int rc = check_bank(bank);
+  if (rc) return rc;
+  if (n_query < 0 || n_window < 0 || n_sink < 0 || n_query > (1 << 24) || n_window > (1 << 24) ||
+      n_sink > (1 << 24))
+    return DKV_ERR_SHAPE;
+  if (n_query > 0 && (!q || !out)) return DKV_ERR_INVALID;
+  if (n_window > 0 && (!win_k || !win_v)) return DKV_ERR_INVALID;
+  if (n_sink > 0 && (!sink_k || !sink_v)) return DKV_ERR_INVALID;
+  if (!(softmax_scale > 0.0f) || softmax_scale > 1e6f) return DKV_ERR_RANGE;
+  const Geom g = geom_of(bank, 0);
+  hipError_t e = launch_attention(*bank, q, n_query, KvSeg{win_k, win_v, n_window}, KvSeg{sink_k, sink_v, n_sink},
+                                  out, softmax_scale, g, static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? DKV_OK : DKV_ERR_HIP;
+}
+
 int densitykv_bank_attention(const dkv_bank *bank, const void *q, int32_t n_query, const void *win_k,
                              const void *win_v, int32_t n_window, void *out, float softmax_scale,
                              void *stream) {
-  int rc = check_bank(bank);
-  if (rc) return rc;
-  if (n_query < 0 || n_window < 0 || n_query > (1 << 24) || n_window > (1 << 24)) return DKV_ERR_SHAPE;
-  if (n_query > 0 && (!q || !out)) return DKV_ERR_INVALID;
-  if (n_window > 0 && (!win_k || !win_v)) return DKV_ERR_INVALID;
-  if (!(softmax_scale > 0.0f) || softmax_scale > 1e6f) return DKV_ERR_RANGE;
-  const Geom g = geom_of(bank, 0);
-  hipError_t e = launch_attention(*bank, q, n_query, win_k, win_v, n_window, out, softmax_scale, g,
-                                  static_cast<hipStream_t>(stream));
-  return e == hipSuccess ? DKV_OK : DKV_ERR_HIP;
+  return densitykv_bank_attention_sink(bank, q, n_query, nullptr, nullptr, 0, win_k, win_v, n_window, out,
+                                       softmax_scale, stream);
 }
 
 int densitykv_pair_weight_q23(const float *d2, int64_t n, const dkv_params *prm, int32_t *w_q23,

@@ -1,8 +1,10 @@
-// Native attention over [retained bank; local window] on gfx950.
+// Native attention over [retained bank; local window; sink] on gfx950.
 //
-// out = softmax(q K^T * scale) V with K = [bank k[0:m_b]; window k], the
-// backbone's own attention reading the retained bank together with the local
-// window (Sec. 1, Fig. 1; logit of Sec. 3.2).  Online (streaming) softmax in
+// out = softmax(q K^T * scale) V with K = [bank k[0:m_b]; window k; sink k],
+// the backbone's own attention reading the retained bank together with the
+// local window (Sec. 1, Fig. 1; logit of Sec. 3.2) and, in the paper's
+// deployment context, a first-frame sink (Supp. D, memory budget and temporal
+// alignment).  Every segment is optional.  Online (streaming) softmax in
 // fp32 over key tiles staged in LDS; exp2 with the scale folded into log2(e).
 #include <hip/hip_runtime.h>
 
@@ -21,13 +23,14 @@ __device__ __forceinline__ int clampi(int v, int lo, int hi) { return v < lo ? l
 // One thread per query row; every thread of the block walks the same key tiles.
 template <int D, int DT>
 __global__ __launch_bounds__(kAThreads) void k_attn_rowwise(dkv_bank bank, const void *q, int nq,
-                                                            const void *wk, const void *wv, int nw,
-                                                            void *out, float scale_log2, Geom g) {
+                                                            KvSeg win, KvSeg sink, void *out, float scale_log2,
+                                                            Geom g) {
   const int b = blockIdx.y, qi = blockIdx.x * kAThreads + threadIdx.x;
   const bool act = qi < nq;
   const int M = clampi(bank.budget[b], 0, g.Mcap);
   const int m = clampi(bank.occupancy[b], 0, M);
-  const int total = m + nw;
+  const int nw = win.n, ns = sink.n;
+  const int total = m + nw + ns;
   __shared__ float tk[kATile][D];
   __shared__ float tv[kATile][D];
   float qr[D], o[D];
@@ -51,10 +54,14 @@ __global__ __launch_bounds__(kAThreads) void k_attn_rowwise(dkv_bank bank, const
           const size_t r = ((size_t)b * g.Mcap + key) * D + j;
           kv = load_elem<DT>(bank.k, r);
           vv = load_elem<DT>(bank.v, r);
-        } else {
+        } else if (key < m + nw) {
           const size_t r = ((size_t)b * nw + (key - m)) * D + j;
-          kv = load_elem<DT>(wk, r);
-          vv = load_elem<DT>(wv, r);
+          kv = load_elem<DT>(win.k, r);
+          vv = load_elem<DT>(win.v, r);
+        } else {
+          const size_t r = ((size_t)b * ns + (key - m - nw)) * D + j;
+          kv = load_elem<DT>(sink.k, r);
+          vv = load_elem<DT>(sink.v, r);
         }
       }
       tk[c][j] = kv;
@@ -192,7 +199,7 @@ __device__ __forceinline__ void stage_barrier() { asm volatile("s_barrier" ::: "
 
 template <int D>
 __global__ __launch_bounds__(64 * kFWaves, 1) void k_attn_mfma(dkv_bank bank, const uint16_t *q, int nq,
-                                                               const uint16_t *wk, const uint16_t *wv, int nw,
+                                                               KvSeg win, KvSeg sink,
                                                                uint16_t *out, float c, Geom g) {
   constexpr int KS = D / 16;   // K steps of S
   constexpr int DT = D / 32;   // dv tiles of O
@@ -205,7 +212,10 @@ __global__ __launch_bounds__(64 * kFWaves, 1) void k_attn_mfma(dkv_bank bank, co
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
   const int M = clampi(bank.budget[b], 0, g.Mcap);
   const int m = clampi(bank.occupancy[b], 0, M);
-  const size_t rb = (size_t)b * g.Mcap, wb = (size_t)b * nw;
+  const int nw = win.n, ns = sink.n;
+  const size_t rb = (size_t)b * g.Mcap, wb = (size_t)b * nw, sb = (size_t)b * ns;
+  const uint16_t *wk = static_cast<const uint16_t *>(win.k), *wv = static_cast<const uint16_t *>(win.v);
+  const uint16_t *sk = static_cast<const uint16_t *>(sink.k), *sv = static_cast<const uint16_t *>(sink.v);
   const uint16_t *bk = static_cast<const uint16_t *>(bank.k);
   const uint16_t *bv = static_cast<const uint16_t *>(bank.v);
   // One LDS array per stage (not one indexed array): with the stage known at
@@ -233,18 +243,25 @@ __global__ __launch_bounds__(64 * kFWaves, 1) void k_attn_mfma(dkv_bank bank, co
   // Tiles never straddle the bank/window boundary: ceil(m/64) bank tiles, then
   // ceil(nw/64) window tiles, so every tile has one (scalar) base pointer.
   const int nt0 = (m + kFK - 1) / kFK;
-  const int nt = nt0 + (nw + kFK - 1) / kFK;
-  auto nvalid_of = [&](int t) { return t < nt0 ? min(kFK, m - t * kFK) : min(kFK, nw - (t - nt0) * kFK); };
+  const int nt1 = nt0 + (nw + kFK - 1) / kFK;
+  const int nt = nt1 + (ns + kFK - 1) / kFK;
+  auto nvalid_of = [&](int t) {
+    return t < nt0 ? min(kFK, m - t * kFK) : (t < nt1 ? min(kFK, nw - (t - nt0) * kFK) : min(kFK, ns - (t - nt1) * kFK));
+  };
   auto issue = [&](int t, char *kd, char *vd) {
     if (t >= nt) return;
     const int nv = nvalid_of(t);
     if (t < nt0) {
       ftile_issue<D, false>(bk + (rb + (size_t)t * kFK) * D, nv, kd);
       ftile_issue<D, true>(bv + (rb + (size_t)t * kFK) * D, nv, vd);
-    } else {
+    } else if (t < nt1) {
       const size_t r0 = wb + (size_t)(t - nt0) * kFK;
       ftile_issue<D, false>(wk + r0 * D, nv, kd);
       ftile_issue<D, true>(wv + r0 * D, nv, vd);
+    } else {
+      const size_t r0 = sb + (size_t)(t - nt1) * kFK;
+      ftile_issue<D, false>(sk + r0 * D, nv, kd);
+      ftile_issue<D, true>(sv + r0 * D, nv, vd);
     }
   };
   // transposed V read: lane group gq = l / 16 (h = gq / 2), member cq = l % 16
@@ -361,30 +378,29 @@ __global__ __launch_bounds__(64 * kFWaves, 1) void k_attn_mfma(dkv_bank bank, co
 }
 
 template <int D, int DT>
-hipError_t attn_impl(const dkv_bank &bank, const void *q, int nq, const void *wk, const void *wv, int nw,
+hipError_t attn_impl(const dkv_bank &bank, const void *q, int nq, KvSeg win, KvSeg sink,
                      void *out, float scale, const Geom &g, hipStream_t s) {
   if (nq <= 0) return hipSuccess;
   const float scale_log2 = scale * 1.4426950408889634f;
   if constexpr (DT == DKV_BF16) {
     dim3 grid((unsigned)((nq + kFQ - 1) / kFQ), (unsigned)g.B);
     k_attn_mfma<D><<<grid, 64 * kFWaves, 0, s>>>(bank, static_cast<const uint16_t *>(q), nq,
-                                                 static_cast<const uint16_t *>(wk), static_cast<const uint16_t *>(wv),
-                                                 nw, static_cast<uint16_t *>(out), scale_log2, g);
+                                                 win, sink, static_cast<uint16_t *>(out), scale_log2, g);
   } else {
     dim3 grid((unsigned)((nq + kAThreads - 1) / kAThreads), (unsigned)g.B);
-    k_attn_rowwise<D, DT><<<grid, kAThreads, 0, s>>>(bank, q, nq, wk, wv, nw, out, scale_log2, g);
+    k_attn_rowwise<D, DT><<<grid, kAThreads, 0, s>>>(bank, q, nq, win, sink, out, scale_log2, g);
   }
   return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_attention(const dkv_bank &bank, const void *q, int nq, const void *wk, const void *wv,
-                            int nw, void *out, float scale, const Geom &g, hipStream_t s) {
-  if (g.d == 128 && g.dtype == DKV_BF16) return attn_impl<128, DKV_BF16>(bank, q, nq, wk, wv, nw, out, scale, g, s);
-  if (g.d == 128 && g.dtype == DKV_F32) return attn_impl<128, DKV_F32>(bank, q, nq, wk, wv, nw, out, scale, g, s);
-  if (g.d == 64 && g.dtype == DKV_BF16) return attn_impl<64, DKV_BF16>(bank, q, nq, wk, wv, nw, out, scale, g, s);
-  return attn_impl<64, DKV_F32>(bank, q, nq, wk, wv, nw, out, scale, g, s);
+hipError_t launch_attention(const dkv_bank &bank, const void *q, int nq, KvSeg win, KvSeg sink, void *out,
+                            float scale, const Geom &g, hipStream_t s) {
+  if (g.d == 128 && g.dtype == DKV_BF16) return attn_impl<128, DKV_BF16>(bank, q, nq, win, sink, out, scale, g, s);
+  if (g.d == 128 && g.dtype == DKV_F32) return attn_impl<128, DKV_F32>(bank, q, nq, win, sink, out, scale, g, s);
+  if (g.d == 64 && g.dtype == DKV_BF16) return attn_impl<64, DKV_BF16>(bank, q, nq, win, sink, out, scale, g, s);
+  return attn_impl<64, DKV_F32>(bank, q, nq, win, sink, out, scale, g, s);
 }
 
 }  // namespace dkv

@@ -79,9 +79,14 @@ hipError_t launch_update(const dkv_bank &bank, const dkv_segment &seg, const Geo
 hipError_t launch_score(const dkv_bank &bank, const dkv_segment &seg, const Geom &g,
                         const Prm &p, int64_t *score_q, float *score_f32, int64_t *density,
                         const Workspace &ws, hipStream_t s);
-hipError_t launch_attention(const dkv_bank &bank, const void *q, int nq, const void *wk,
-                            const void *wv, int nw, void *out, float scale, const Geom &g,
-                            hipStream_t s);
+// One extra key/value segment of the attention context: [B, n, d] device arrays.
+struct KvSeg {
+  const void *k;
+  const void *v;
+  int n;
+};
+hipError_t launch_attention(const dkv_bank &bank, const void *q, int nq, KvSeg win, KvSeg sink,
+                            void *out, float scale, const Geom &g, hipStream_t s);
 void launch_gram_mfma(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                       const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage);
 void launch_score_mfma(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,

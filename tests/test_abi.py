@@ -99,6 +99,10 @@ def test_attention_rejects_bad_arguments(L):
     assert att(10, 0, None, None, 0.1) == -1
     assert att(10, 0, 1, None, 0.0) == -5
     assert att(10, 0, 1, None, float("nan")) == -5
+    sink = lambda ns, sk: L.densitykv_bank_attention_sink(ctypes.byref(b), 1, 10, sk, sk, ns, None, None, 0, 1,
+                                                          ctypes.c_float(0.1), None)
+    assert sink(5, None) == -1                                               # sink missing
+    assert sink(-1, None) == -2
 
 
 def test_pair_weight_rejects_bad_arguments(L):

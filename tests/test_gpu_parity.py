@@ -14,8 +14,8 @@ pytestmark = pytest.mark.gpu
 
 from oracle import Q23, BankState, attention, candidate_scores, density_from_scratch, weight_q23  # noqa: E402
 from paper_2608_27922_amd import api, synth  # noqa: E402
-from gpu_util import (assert_bank_equal, assert_trace_equal, attention_error, dev, host, mirror,  # noqa: E402
-                      oracle_params, oracle_step)
+from gpu_util import (TORCH_DT, assert_bank_equal, assert_trace_equal, attention_error, dev, host,  # noqa: E402
+                      mirror, oracle_params, oracle_step)
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -318,3 +318,90 @@ def test_attention_edge_cases(dt, d):
             ref = attention(q[b], Kb[b, :m], Vb[b, :m], wk[b], wv[b], 1.0 / np.sqrt(d))
             err = attention_error(got[b], ref)
             assert err <= tol, (nq, nw, b, err)
+
+
+# ----------------------------------------------------------------------------- sink + window + bank
+
+@pytest.mark.parametrize("dt,d", [("bf16", 128), ("f32", 64), ("bf16", 64), ("f32", 128)])
+def test_sink_attention_edge_cases(dt, d):
+    """[bank; window; sink] with every segment present or absent, ragged lengths and
+    occupancies, against the fp64 oracle over the concatenated keys."""
+    _log(f"sink attention edges {dt} {d}")
+    rng = np.random.default_rng(33)
+    B, M = 4, 200
+    occ = [200, 0, 77, 5]
+    bank = api.Bank(B, M, d, dtype=TORCH_DT[dt], group_size=1, budget=torch.tensor([200, 0, 77, 5], dtype=torch.int32))
+    Kb = synth.to_storage(rng.standard_normal((B, M, d)), dt)
+    Vb = synth.to_storage(rng.standard_normal((B, M, d)), dt)
+    bank.k.copy_(dev(Kb, dt))
+    bank.v.copy_(dev(Vb, dt))
+    bank.occupancy.copy_(torch.tensor(occ, dtype=torch.int32))
+    tol = 2e-2 if dt == "bf16" else 1e-5
+    for nq, nw, ns in [(70, 33, 65), (1, 0, 1), (130, 64, 0), (64, 0, 129), (5, 1, 64)]:
+        q = synth.to_storage(rng.standard_normal((B, nq, d)), dt)
+        seg = lambda n: synth.to_storage(rng.standard_normal((B, n, d)), dt)
+        wk, wv, sk, sv = seg(nw), seg(nw), seg(ns), seg(ns)
+        o = api.bank_attention_sink(bank, dev(q, dt), dev(sk, dt) if ns else None, dev(sv, dt) if ns else None,
+                                    dev(wk, dt) if nw else None, dev(wv, dt) if nw else None)
+        torch.cuda.synchronize()
+        got = host(o)
+        for b in range(B):
+            m = occ[b]
+            if m + nw + ns == 0:
+                assert np.all(got[b] == 0)
+                continue
+            ref = attention(q[b], Kb[b, :m], Vb[b, :m], np.concatenate([wk[b], sk[b]]), np.concatenate([wv[b], sv[b]]),
+                            1.0 / np.sqrt(d))
+            err = attention_error(got[b], ref)
+            assert err <= tol, (nq, nw, ns, b, err)
+
+
+def test_sink_attention_without_sink_is_bank_attention():
+    """n_sink = 0 is the two-segment call (the same kernel, bit for bit)."""
+    _log("sink attention n_sink=0")
+    cfg = synth.WORKLOADS["tiny"]
+    rng = np.random.default_rng(5)
+    B, M, d = 3, 150, 128
+    bank = api.Bank(B, M, d, dtype=torch.bfloat16, group_size=3)
+    bank.k.copy_(dev(synth.to_storage(rng.standard_normal((B, M, d)), "bf16"), "bf16"))
+    bank.v.copy_(dev(synth.to_storage(rng.standard_normal((B, M, d)), "bf16"), "bf16"))
+    bank.occupancy.fill_(131)
+    q = dev(synth.to_storage(rng.standard_normal((B, 77, d)), "bf16"), "bf16")
+    wk = dev(synth.to_storage(rng.standard_normal((B, 90, d)), "bf16"), "bf16")
+    wv = dev(synth.to_storage(rng.standard_normal((B, 90, d)), "bf16"), "bf16")
+    a = api.bank_attention(bank, q, wk, wv)
+    b2 = api.bank_attention_sink(bank, q, None, None, wk, wv)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b2)
+
+
+def test_sink_attention_deployment_shape():
+    """The paper's deployment context at full size: 12 heads, d = 128, bf16, a
+    1,560-token sink, a 7,800-token window and banks of up to 9,360 retained states
+    (ragged occupancy), 4,680 queries; 64 sampled query rows per head against the
+    fp64 oracle (clustered keys on the grid, as in the rollout workloads)."""
+    _log("sink attention deployment shape")
+    cfg = synth.Config(seed_id=41, name="deploy", layers=1, heads=12, d=128, dtype="bf16", n_cand=4680,
+                       n_query=4680, n_window=7800, budget=9360, clusters=64, blocks=1, group_size=12,
+                       sigma2_log2=6, drift=0.0)
+    B, d, M = cfg.heads, cfg.d, cfg.budget
+    occ = np.array([9360, 9360, 9001, 4680, 9360, 64, 9360, 9359, 1, 9360, 7777, 9360], np.int32)
+    bank = api.Bank(B, M, d, dtype=torch.bfloat16, group_size=B)
+    kb, vb = synth.torch_layer_block(cfg, 0, 0, M, "cuda", seed=1)
+    sk, sv = synth.torch_layer_block(cfg, 0, 1, 1560, "cuda", seed=1)
+    wk, wv = synth.torch_layer_block(cfg, 0, 2, 7800, "cuda", seed=1)
+    q, _ = synth.torch_layer_block(cfg, 0, 3, cfg.n_query, "cuda", seed=1)
+    bank.k.copy_(kb)
+    bank.v.copy_(vb)
+    bank.occupancy.copy_(torch.from_numpy(occ))
+    o = api.bank_attention_sink(bank, q, sk, sv, wk, wv)
+    torch.cuda.synchronize()
+    rows = np.random.default_rng(3).choice(cfg.n_query, 64, replace=False)
+    rows[:2] = [0, cfg.n_query - 1]
+    for b in range(B):
+        m = int(occ[b])
+        ref = attention(host(q[b])[rows], host(bank.k[b, :m]), host(bank.v[b, :m]),
+                        np.concatenate([host(wk[b]), host(sk[b])]), np.concatenate([host(wv[b]), host(sv[b])]),
+                        1.0 / np.sqrt(d))
+        err = attention_error(host(o[b])[rows], ref)
+        assert err <= 2e-2, (b, m, err)

@@ -487,6 +487,28 @@ def test_attention_special_cases():
     assert np.allclose(out, np.repeat(V.mean(0, keepdims=True), 4, 0), atol=1e-14)
 
 
+def test_attention_key_order_invariance():
+    """Softmax attention does not depend on the order of the keys (with their values):
+    the sink + window + bank context (Supp. D) is the bank call with the sink appended
+    to the window, whatever the segment order."""
+    rng = np.random.default_rng(8)
+    d = 16
+    q = rng.standard_normal((9, d))
+    Kb, Vb = rng.standard_normal((30, d)), rng.standard_normal((30, d))
+    Kw, Vw = rng.standard_normal((11, d)), rng.standard_normal((11, d))
+    Ks, Vs = rng.standard_normal((7, d)), rng.standard_normal((7, d))
+    a = attention(q, Kb, Vb, np.concatenate([Kw, Ks]), np.concatenate([Vw, Vs]), 0.25)
+    perm = rng.permutation(48)
+    K = np.concatenate([Kb, Kw, Ks])[perm]
+    V = np.concatenate([Vb, Vw, Vs])[perm]
+    b = attention(q, K[:20], V[:20], K[20:], V[20:], 0.25)
+    assert np.allclose(a, b, rtol=0, atol=1e-12)
+    # brute force: explicit softmax weights over the concatenated keys
+    s = q @ np.concatenate([Kb, Kw, Ks]).T * 0.25
+    w = np.exp(s) / np.exp(s).sum(1, keepdims=True)
+    assert np.allclose(a, w @ np.concatenate([Vb, Vw, Vs]), rtol=0, atol=1e-12)
+
+
 def test_attention_matches_torch_sdpa_fp64():
     torch = pytest.importorskip("torch")
     rng = np.random.default_rng(9)
