@@ -72,6 +72,11 @@ V3  eviction = "densest": no mandatory set; the e_{r*} states of largest
 V4  eviction = "mandatory_source": all violators, then the non-violators in
     source order, read as admission order (ascending provenance, then slot).
 The independent per-head variant is a layer of one head (group size 1).
+V5  kv_descriptor: the retention geometry uses the concatenated vector [k; v]
+    (Supp. E, "Retention geometry"; the post-RoPE [K;V] rows of Table 1(b))
+    for every density, score and crossing; attention and the stored rows are
+    unchanged.  C0 then applies to the values too (the synthetic values of
+    this mode are drawn on the key grid).
 """
 
 from __future__ import annotations
@@ -98,6 +103,7 @@ class Params:
     source_order: bool = False
     refresh_base: bool = False
     eviction: str = "default"  # "default" | "densest" | "mandatory_source"
+    kv_descriptor: bool = False
 
     def __post_init__(self):
         if self.p not in (1, 2, 4):
@@ -266,6 +272,14 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
     R = min(N, min(h.budget for h in heads))
     Kc64 = [np.asarray(k, np.float64) for k in cand_K]
 
+    def desc(K, V):
+        """Retention descriptor: the key, or [key; value] (V5)."""
+        K = np.asarray(K, np.float64)
+        return np.hstack([K, np.asarray(V, np.float64)]) if prm.kv_descriptor else K
+
+    Dc = [desc(Kc64[h], cand_V[h]) for h in range(H)]                  # candidate descriptors
+    Db = [desc(heads[h].K, heads[h].V) for h in range(H)]              # bank descriptors
+
     # ---- Step 1: per-head candidate order (Eq. 6-7; Alg. 1) ----------------
     orders, scores = [], []
     for h in range(H):
@@ -275,7 +289,7 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
             orders.append(np.arange(N, dtype=np.int64))
             scores.append((None, 0))
         else:
-            S, E, _ = candidate_scores(bank.K, bank.base, Kc64[h], prm)
+            S, E, _ = candidate_scores(Db[h], bank.base, Dc[h], prm)
             if prm.source_order:
                 orders.append(np.arange(N, dtype=np.int64))               # V1
             else:
@@ -290,7 +304,7 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
         if m == 0:
             P = np.zeros((0, R + 1), np.int64)
         else:
-            Wc = weight_q23(pair_d2(bank.K, Kc64[h][pi[:R]]), prm)      # (m, R)
+            Wc = weight_q23(pair_d2(Db[h], Dc[h][pi[:R]]), prm)        # (m, R)
             # Column-wise cumulative sums give every prefix contribution at once
             # (Supp. C, "Decision granularity versus computational tiling").
             P = np.concatenate([np.zeros((m, 1), np.int64), np.cumsum(Wc, axis=1)], axis=1)
@@ -343,20 +357,21 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
         ev_mask[evicted] = True
         surv = np.nonzero(~ev_mask)[0]
         Kc, Vc = Kc64[h], np.asarray(cand_V[h])
+        Dbh, Dch = Db[h], Dc[h]
 
         # Exact density maintenance for survivors.
         rho_surv = bank.rho[surv].copy()
         if surv.size and admitted.size:
-            rho_surv += weight_q23(pair_d2(bank.K[surv], Kc[admitted]), prm).sum(axis=1)
+            rho_surv += weight_q23(pair_d2(Dbh[surv], Dch[admitted]), prm).sum(axis=1)
         if surv.size and evicted.size:
-            rho_surv -= weight_q23(pair_d2(bank.K[surv], bank.K[evicted]), prm).sum(axis=1)
+            rho_surv -= weight_q23(pair_d2(Dbh[surv], Dbh[evicted]), prm).sum(axis=1)
 
         # New states: density over the final bank (co-admitted included), frozen.
         if admitted.size:
             rho_new = np.zeros(admitted.size, np.int64)
             if surv.size:
-                rho_new += weight_q23(pair_d2(Kc[admitted], bank.K[surv]), prm).sum(axis=1)
-            rho_new += density_from_scratch(Kc[admitted], prm)
+                rho_new += weight_q23(pair_d2(Dch[admitted], Dbh[surv]), prm).sum(axis=1)
+            rho_new += density_from_scratch(Dch[admitted], prm)
             base_new = np.maximum(rho_new, prm.delta_q)
         else:
             rho_new = np.zeros(0, np.int64)

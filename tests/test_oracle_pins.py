@@ -314,6 +314,59 @@ def test_policy_rollouts_match_exact_bruteforce(policy):
     assert differs > 0, "the policy never changed a decision in these rollouts"
 
 
+def _to_exact_bank_kv(bank: BankState):
+    return [{"key": tuple(F(float(v)) for v in np.concatenate([bank.K[i], bank.V[i]])),
+             "b": F(int(bank.base[i]), Q23), "prov": int(bank.prov[i])} for i in range(bank.m)]
+
+
+def test_kv_descriptor_rollouts_match_exact_bruteforce():
+    """The [K; V] retention geometry (Supp. E, "Retention geometry"): on random
+    multi-head rollouts every decision, the commit layout and the densities equal the
+    exact-rational brute force run on the concatenated key-value descriptors, the
+    stored keys and values are the candidates' own rows, and the geometry changes at
+    least one decision against the key-only default."""
+    d, H, M = 2, 3, 7
+    prm = Params(sigma2_log2=1, p=2, kv_descriptor=True)
+    key_only = Params(sigma2_log2=1, p=2)
+    differs = 0
+    for seed in range(4):
+        rng = np.random.default_rng(200 + seed)
+        heads = [BankState.empty(M, d) for _ in range(H)]
+        ref_heads = [BankState.empty(M, d) for _ in range(H)]
+        for blk in range(1, 8):
+            N = int(rng.integers(2, 6))
+            Ks = [np.rint(rng.standard_normal((N, d)) * 4) / 2 for _ in range(H)]
+            Vs = [(np.rint(rng.standard_normal((N, d)) * 4) / 2).astype(np.float32) for _ in range(H)]
+            new, rec = update_layer(heads, Ks, Vs, blk, prm)
+            _, rec_k = update_layer(heads, Ks, Vs, blk, key_only)
+            cands = [[tuple(F(float(v)) for v in np.concatenate([Ks[h][i], Vs[h][i]])) for i in range(N)]
+                     for h in range(H)]
+            infos = [xr.update(_to_exact_bank_kv(heads[h]), cands[h], M, sigma2=2, p=2, block_id=blk)[1]
+                     for h in range(H)]
+            feas = [r for r in range(rec.R + 1) if all(infos[h]["c"][r] <= infos[h]["e"][r] for h in range(H))]
+            assert rec.r_star == (max(feas) if feas else 0)
+            for h in range(H):
+                xb, info = xr.update(_to_exact_bank_kv(heads[h]), cands[h], M, sigma2=2, p=2, block_id=blk,
+                                     r_star=rec.r_star)
+                hr, nb = rec.heads[h], new[h]
+                assert list(hr.c) == info["c"]
+                if heads[h].m:
+                    assert list(hr.pi) == info["pi"]
+                assert hr.evicted.tolist() == info["evicted"] and hr.admitted.tolist() == info["admitted"]
+                assert nb.prov.tolist() == [s["prov"] for s in xb]
+                for i, s in enumerate(xb):
+                    assert tuple(F(float(v)) for v in np.concatenate([nb.K[i], nb.V[i]])) == s["key"]
+                tol = max(nb.m, 1) * 2.0 ** -22
+                for q, s in zip(nb.rho, xb):
+                    assert abs(q / Q23 - float(s["rho"])) <= tol
+                for q, s in zip(nb.base, xb):
+                    assert abs(q / Q23 - float(s["b"])) <= tol
+                differs += (hr.evicted.tolist() != rec_k.heads[h].evicted.tolist() or
+                            hr.pi.tolist() != rec_k.heads[h].pi.tolist())
+            heads = new
+    assert differs > 0, "the [K; V] descriptor never changed a decision in these rollouts"
+
+
 def test_refresh_base_keeps_delta_floor():
     """Refreshed baselines (Table 1(b), Supp. E) still obey b >= delta (Eq. 5): isolated
     keys have rho = 0 after the update, so every refreshed baseline is delta."""
