@@ -33,7 +33,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 ATTN_SOURCE = os.path.join(ROOT, "paper_2608_27922_amd", "csrc", "dkv_attention.hip")
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_attn_mfma_single_layer_traffic.md")
 # dkv_params.flags of each policy ablation (Table 1(b); independent per-head = group size 1)
-POLICIES = {"default": 0, "source_order": 0x1, "refresh_base": 0x2, "densest_only": 0x4, "source_fill": 0x8}
+# (kv_descriptor: the [K; V] retention geometry; the workload's values are not on the key grid, so
+# this mode is a timing run only, its decisions carry the fp32 rounding of the descriptor Gram)
+POLICIES = {"default": 0, "source_order": 0x1, "refresh_base": 0x2, "densest_only": 0x4, "source_fill": 0x8,
+            "kv_descriptor": 0x10}
 
 
 def parse():

@@ -134,11 +134,20 @@ typedef struct {
  *                 released (ties: smaller provenance, then lower slot); a
  *                 violator outside them stays in the bank
  *   SOURCE_FILL   all violators, then the non-violators in admission order
- *                 (ascending provenance, then slot) until e_{r*} are released */
+ *                 (ascending provenance, then slot) until e_{r*} are released
+ *   KV_DESCRIPTOR the retention geometry uses the concatenated [k; v] row
+ *                 (2 d elements; Supp. E "Retention geometry", the post-RoPE
+ *                 [K;V] rows of Table 1(b)) for every density, score and
+ *                 crossing; attention is unchanged.  bf16 banks only
+ *                 (DKV_ERR_UNSUPPORTED otherwise); the values must then lie on
+ *                 the key grid for exact decisions, the segment's v is
+ *                 required (DKV_ERR_INVALID), and knorm holds |k|^2 + |v|^2, so
+ *                 a bank must be updated and scored with one geometry. */
 #define DKV_POLICY_SOURCE_ORDER 0x1u
 #define DKV_POLICY_REFRESH_BASE 0x2u
 #define DKV_POLICY_DENSEST_ONLY 0x4u
 #define DKV_POLICY_SOURCE_FILL 0x8u
+#define DKV_POLICY_KV_DESCRIPTOR 0x10u
 
 /* Optional outputs of densitykv_update_bank (any pointer may be NULL).
  *   r_star       [G]        admitted prefix length of each group (Eq. 11)

@@ -24,6 +24,7 @@ POLICY_SOURCE_ORDER = 0x1   # prefixes in source order instead of score order
 POLICY_REFRESH_BASE = 0x2   # b = max(rho, delta) for every retained state after the update
 POLICY_DENSEST_ONLY = 0x4   # no mandatory set: release the e densest states
 POLICY_SOURCE_FILL = 0x8    # violators, then fill in admission order
+POLICY_KV_DESCRIPTOR = 0x10  # densities on the concatenated [k; v] rows (bf16 banks; values on the key grid)
 
 ENTRY_POINTS = ("densitykv_workspace_size", "densitykv_score", "densitykv_update_bank",
                 "densitykv_bank_attention", "densitykv_bank_attention_sink", "densitykv_pair_weight_q23",

@@ -48,7 +48,7 @@ size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, cha
   w.sub_adm = (int64_t *)take(Bz * Nz * 8);
   w.mut_adm = (int64_t *)take(Bz * Nz * 8);
   w.hole_list = (int32_t *)take(Bz * Mz * 4);
-  w.sk = (uint16_t *)take(Bz * Nz * (size_t)d * 2);
+  w.sk = (uint16_t *)take(Bz * Nz * (size_t)d * 4);  // ordered descriptors: up to [k; v], 2 d bf16
   w.snorm = (float *)take(Bz * Nz * 4);
   w.baug = (uint4 *)take(Bz * Mz * 16);
   w.caug = (uint4 *)take(Bz * Nz * 16);
@@ -92,7 +92,7 @@ int check_segment(const dkv_segment *sg) {
 int check_params(const dkv_params *p, Prm *out, int block_id) {
   if (!p) return DKV_ERR_INVALID;
   const uint32_t known = DKV_POLICY_SOURCE_ORDER | DKV_POLICY_REFRESH_BASE | DKV_POLICY_DENSEST_ONLY |
-                         DKV_POLICY_SOURCE_FILL;
+                         DKV_POLICY_SOURCE_FILL | DKV_POLICY_KV_DESCRIPTOR;
   if (p->flags & ~known) return DKV_ERR_INVALID;
   if ((p->flags & DKV_POLICY_DENSEST_ONLY) && (p->flags & DKV_POLICY_SOURCE_FILL)) return DKV_ERR_INVALID;
   if (p->p != 1 && p->p != 2 && p->p != 4) return DKV_ERR_UNSUPPORTED;
@@ -108,6 +108,15 @@ int check_params(const dkv_params *p, Prm *out, int block_id) {
   out->delta_q = p->delta_q;
   out->block_id = block_id;
   out->flags = p->flags;
+  return DKV_OK;
+}
+
+// The [K; V] retention geometry runs on the bf16 MFMA path and reads the
+// candidates' values.
+int check_geometry(const dkv_bank *bk, const dkv_segment *seg, const Prm &p) {
+  if (!(p.flags & DKV_POLICY_KV_DESCRIPTOR)) return DKV_OK;
+  if (bk->dtype != DKV_BF16) return DKV_ERR_UNSUPPORTED;
+  if (seg->n > 0 && !seg->v) return DKV_ERR_INVALID;
   return DKV_OK;
 }
 
@@ -144,6 +153,7 @@ int densitykv_score(const dkv_bank *bank, const dkv_segment *seg, const dkv_para
   if (!rc) rc = check_segment(seg);
   Prm p{};
   if (!rc) rc = check_params(prm, &p, seg->block_id);
+  if (!rc) rc = check_geometry(bank, seg, p);
   if (rc) return rc;
   Workspace ws{};
   const size_t need = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity,
@@ -161,6 +171,7 @@ int densitykv_update_bank(dkv_bank *bank, const dkv_segment *seg, const dkv_para
   if (!rc) rc = check_segment(seg);
   Prm p{};
   if (!rc) rc = check_params(prm, &p, seg->block_id);
+  if (!rc) rc = check_geometry(bank, seg, p);
   if (rc) return rc;
   Workspace ws{};
   const size_t need = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity,

@@ -83,6 +83,25 @@ __device__ __forceinline__ uint32_t weight_raw(float u, float scale) {
   return __float_as_uint(__builtin_fmaf(w, scale, 8388608.0f));
 }
 
+// Source of retention descriptors of dimension D: row r's descriptor is k[r]
+// (rows of D elements) or, for the [K; V] geometry (SPLIT), the concatenation
+// [k[r]; v[r]] of two rows of D / 2 elements.  desc_chunk gives its 16-byte
+// chunk c (8 bf16).
+struct Desc {
+  const uint16_t *k;
+  const uint16_t *v;
+};
+
+template <int D, bool SPLIT>
+__device__ __forceinline__ const uint16_t *desc_chunk(const Desc &s, int64_t row, int c) {
+  if constexpr (!SPLIT) {
+    return s.k + row * D + 8 * c;
+  } else {
+    constexpr int H = D / 2;
+    return c < H / 8 ? s.k + row * H + 8 * c : s.v + row * H + 8 * (c - H / 8);
+  }
+}
+
 // Row fragment: B operand of every K step for this lane's row item.
 template <int D>
 struct RowFrag {
@@ -91,14 +110,14 @@ struct RowFrag {
 
 // Load the B operand for row item (lane % 32): keys scaled by -2/sigma^2, then
 // the aug step [1, 1, 1, n_hi, n_mid, n_lo, fold, 0] (half 0) / zeros (half 1).
-template <int D, bool FOLD>
-__device__ __forceinline__ void load_row_frag(RowFrag<D> &rf, const uint16_t *key, float norm, bool valid,
+template <int D, bool FOLD, bool SPLIT>
+__device__ __forceinline__ void load_row_frag(RowFrag<D> &rf, const Desc &src, int64_t row, float norm, bool valid,
                                               float neg2_inv_s2, float inv_s2) {
   const int h = (threadIdx.x & 63) >> 5;
 #pragma unroll
   for (int kk = 0; kk < TileCfg<D>::kSteps; ++kk) {
     u32x4 raw = {0, 0, 0, 0};
-    if (valid) raw = *reinterpret_cast<const u32x4 *>(key + 16 * kk + 8 * h);
+    if (valid) raw = *reinterpret_cast<const u32x4 *>(desc_chunk<D, SPLIT>(src, row, 2 * kk + h));
     u32x4 sc;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -158,8 +177,8 @@ __device__ __forceinline__ void stage_rows(int64_t (&rows)[SCfg<D>::PER + 1], in
   rows[SCfg<D>::PER] = row_of(min(j0 + 16 * wave + (l & 15), ncols - 1));
 }
 
-template <int D, bool kBs>
-__device__ __forceinline__ void stage_dma(const int64_t (&rows)[SCfg<D>::PER + 1], const uint16_t *keys,
+template <int D, bool kBs, bool SPLIT>
+__device__ __forceinline__ void stage_dma(const int64_t (&rows)[SCfg<D>::PER + 1], const Desc &keys,
                                           const uint4 *augs, const float *bs, char *kb, char *ab, float *sb) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
 #pragma unroll
@@ -167,7 +186,8 @@ __device__ __forceinline__ void stage_dma(const int64_t (&rows)[SCfg<D>::PER + 1
     const int blk = wave * SCfg<D>::PER + q;
     const int r = blk * SCfg<D>::RPL + l / SCfg<D>::CH;
     const int c = (l % SCfg<D>::CH) ^ (r % SCfg<D>::CH);
-    __builtin_amdgcn_global_load_lds((void *)(keys + rows[q] * D + 8 * c), (lds_void *)(kb + blk * 1024), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((void *)desc_chunk<D, SPLIT>(keys, rows[q], c), (lds_void *)(kb + blk * 1024), 16,
+                                     0, 0);
   }
   // items 16 w .. 16 w + 15: lanes 0-15 of wave w (LDS address = base + lane * size)
   if (l < 16) {
@@ -236,9 +256,9 @@ __device__ __forceinline__ uint32_t lane_wsum(const f32x16 &u, int nvalid, int h
 // ---------------------------------------------------------------------------
 constexpr int kColsPerSplit = 1024;
 
-template <int D, int P, bool FOLD>
-__global__ __launch_bounds__(64 * kWaves, 2) void k_score_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
-                                                           Workspace ws) {
+template <int D, int P, bool FOLD, bool KV>
+__global__ __launch_bounds__(64 * kWaves, 2) void k_score_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
+                                                           Geom g, Prm p, Workspace ws) {
   const int b = blockIdx.z;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
   const int x = blockIdx.x * kRowsPerWG + wave * 32 + n;
@@ -250,12 +270,12 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_score_mfma(dkv_bank bank, co
   __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
   __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
   __shared__ __attribute__((aligned(16))) float s0[kSI], s1[kSI], s2[kSI];
-  const uint16_t *K = static_cast<const uint16_t *>(seg_k);
-  const uint16_t *BK = static_cast<const uint16_t *>(bank.k);
+  const Desc K{static_cast<const uint16_t *>(seg_k), static_cast<const uint16_t *>(seg_v)};
+  const Desc BK{static_cast<const uint16_t *>(bank.k), static_cast<const uint16_t *>(bank.v)};
   const bool rv = x < g.N;
   const size_t xr = (size_t)b * g.N + (rv ? x : 0);
   RowFrag<D> rf;
-  load_row_frag<D, FOLD>(rf, K + xr * D, rv ? ws.cnorm[xr] : 0.0f, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
+  load_row_frag<D, FOLD, KV>(rf, K, (int64_t)xr, rv ? ws.cnorm[xr] : 0.0f, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
   const size_t rb = (size_t)b * g.Mcap + c0;
   auto row_of = [&](int i) -> int64_t { return (int64_t)(rb + i); };
   uint64_t A64 = 0, W64 = 0;
@@ -308,7 +328,7 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_score_mfma(dkv_bank bank, co
     else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
     stage_barrier();
     if (t + 2 < ns) {
-      stage_dma<D, true>(rows, BK, ws.baug, ws.bs, kn, an, sn);
+      stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, kn, an, sn);
       if (t + 3 < ns) stage_rows<D>(rows, (t + 3) * kSI, ncols, row_of);
     }
     f32x16 u0, u1;
@@ -334,10 +354,10 @@ __global__ __launch_bounds__(64 * kWaves, 2) void k_score_mfma(dkv_bank bank, co
     }
   };
   stage_rows<D>(rows, 0, ncols, row_of);
-  stage_dma<D, true>(rows, BK, ws.baug, ws.bs, k0, a0, s0);
+  stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k0, a0, s0);
   if (ns > 1) {
     stage_rows<D>(rows, kSI, ncols, row_of);
-    stage_dma<D, true>(rows, BK, ws.baug, ws.bs, k1, a1, s1);
+    stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k1, a1, s1);
     if (ns > 2) stage_rows<D>(rows, 2 * kSI, ncols, row_of);
   }
   for (int t = 0; t < ns; t += 3) {
@@ -368,16 +388,18 @@ struct StageBufs {
 };
 
 // Body of one row-sum workgroup (bx, by, bz) = (row block, column split, bank).
-template <int D, int P, int MODE, bool FOLD>
-__device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *seg_k, const Geom &g, const Prm &p,
-                                            const Workspace &ws, int64_t *out, int bx, int by, int bz,
+template <int D, int P, int MODE, bool FOLD, bool KV>
+__device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *seg_k, const void *seg_v, const Geom &g,
+                                            const Prm &p, const Workspace &ws, int64_t *out, int bx, int by, int bz,
                                             const StageBufs<D> &sb) {
   const int b = bz;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
   const int m = ws.m[b];
-  const uint16_t *SK = static_cast<const uint16_t *>(seg_k);
-  const uint16_t *BK = static_cast<const uint16_t *>(bank.k);
+  // descriptors: candidates, bank states, ordered candidates (stored concatenated)
+  const Desc SK{static_cast<const uint16_t *>(seg_k), static_cast<const uint16_t *>(seg_v)};
+  const Desc BK{static_cast<const uint16_t *>(bank.k), static_cast<const uint16_t *>(bank.v)};
+  const Desc OK{ws.sk, nullptr};
   constexpr bool kNeedEv = MODE == RS_SURV_EV || MODE == RS_ADM_BASE || MODE == RS_ADM_MUT;
   const int n_ev = kNeedEv ? ws.n_ev[b] : 0;
   const int rs = (MODE == RS_FIXUP || kNeedEv) ? ws.r_star[b / g.gs] : 0;
@@ -411,28 +433,30 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   const int v = bx * kRowsPerWG + wave * 32 + n;
   const bool rv = v < nrows;
   // row item
-  const uint16_t *rkey = BK + rb * D;
+  Desc rsrc = BK;
+  int64_t rrow = (int64_t)rb;
   float rnorm = 0.0f;
   size_t out_idx = 0;
   if (rv) {
     if constexpr (MODE == RS_CHUNK || MODE == RS_FIXUP || MODE == RS_DENSITY) {
-      rkey = BK + (rb + v) * D;
+      rrow = (int64_t)(rb + v);
       rnorm = bank.knorm[rb + v];
       out_idx = rb + v;
     } else if constexpr (MODE == RS_SURV_EV) {
       const int s = ws.surv_list[rb + v];
-      rkey = BK + (rb + s) * D;
+      rrow = (int64_t)(rb + s);
       rnorm = bank.knorm[rb + s];
       out_idx = rb + s;
     } else {
       const int x = ws.adm_list[nb + v];
-      rkey = SK + (nb + x) * D;
+      rsrc = SK;
+      rrow = (int64_t)(nb + x);
       rnorm = ws.cnorm[nb + x];
       out_idx = nb + v;
     }
   }
   RowFrag<D> rf;
-  load_row_frag<D, FOLD>(rf, rkey, rnorm, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
+  load_row_frag<D, FOLD, KV>(rf, rsrc, rrow, rnorm, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
   // column items (absolute index j in the mode's list)
   auto row_of = [&](int j) -> int64_t {
     if constexpr (MODE == RS_CHUNK || MODE == RS_FIXUP) return (int64_t)(nb + j);
@@ -442,7 +466,9 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
     else if constexpr (MODE == RS_ADM_MUT) return (int64_t)(nb + ws.adm_list[nb + j]);
     else return (int64_t)(rb + j);
   };
-  const uint16_t *colbase = (MODE == RS_CHUNK || MODE == RS_FIXUP) ? ws.sk : (MODE == RS_ADM_MUT ? SK : BK);
+  const Desc colbase = (MODE == RS_CHUNK || MODE == RS_FIXUP) ? OK : (MODE == RS_ADM_MUT ? SK : BK);
+  // the ordered candidates are stored as whole descriptors; the others are split for [K; V]
+  constexpr bool kColSplit = KV && !(MODE == RS_CHUNK || MODE == RS_FIXUP);
   const uint4 *colaug = (MODE == RS_CHUNK || MODE == RS_FIXUP) ? ws.saug : (MODE == RS_ADM_MUT ? ws.caug : ws.baug);
   constexpr bool kDiag = (MODE == RS_ADM_MUT || MODE == RS_DENSITY);
   uint64_t S64 = 0;
@@ -481,7 +507,7 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
     stage_barrier();
     if (t + 2 < ns) {
       if (t + 3 < ns) stage_rows<D>(fill, (t + 3) * kSI, ncols, row_of_rel);
-      stage_dma<D, false>(use, colbase, colaug, nullptr, kn, an, nullptr);
+      stage_dma<D, false, kColSplit>(use, colbase, colaug, nullptr, kn, an, nullptr);
     }
     f32x16 u0, u1;
     stage_u<D>(kb, ab, rf, u0, u1);
@@ -503,10 +529,10 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   };
   if (ns > 0) {
     stage_rows<D>(rowsA, 0, ncols, row_of_rel);
-    stage_dma<D, false>(rowsA, colbase, colaug, nullptr, sb.k0, sb.a0, nullptr);
+    stage_dma<D, false, kColSplit>(rowsA, colbase, colaug, nullptr, sb.k0, sb.a0, nullptr);
     if (ns > 1) {
       stage_rows<D>(rowsB, kSI, ncols, row_of_rel);
-      stage_dma<D, false>(rowsB, colbase, colaug, nullptr, sb.k1, sb.a1, nullptr);
+      stage_dma<D, false, kColSplit>(rowsB, colbase, colaug, nullptr, sb.k1, sb.a1, nullptr);
       if (ns > 2) stage_rows<D>(rowsA, 2 * kSI, ncols, row_of_rel);
     }
   }
@@ -548,33 +574,34 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   }
 }
 
-template <int D, int P, int MODE, bool FOLD>
-__global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
-                                                            Workspace ws, int64_t *out) {
+template <int D, int P, int MODE, bool FOLD, bool KV>
+__global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
+                                                            Geom g, Prm p, Workspace ws, int64_t *out) {
   constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
   __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
   __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
   const StageBufs<D> sb{k0, k1, k2, a0, a1, a2};
-  rowsum_body<D, P, MODE, FOLD>(bank, seg_k, g, p, ws, out, blockIdx.x, blockIdx.y, blockIdx.z, sb);
+  rowsum_body<D, P, MODE, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, out, blockIdx.x, blockIdx.y, blockIdx.z, sb);
 }
 
 // The three maintenance sums in one launch (Supp. C): survivors x evicted,
 // admitted x (evicted or survivors), admitted x admitted; blockIdx.x selects
 // the stage and its row block.
-template <int D, int P, bool FOLD>
-__global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, const void *seg_k, Geom g, Prm p,
-                                                           Workspace ws, int nx_surv, int nx_adm) {
+template <int D, int P, bool FOLD, bool KV>
+__global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
+                                                           Geom g, Prm p, Workspace ws, int nx_surv, int nx_adm) {
   constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
   __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
   __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
   const StageBufs<D> sb{k0, k1, k2, a0, a1, a2};
   const int bx = blockIdx.x;
   if (bx < nx_surv)
-    rowsum_body<D, P, RS_SURV_EV, FOLD>(bank, seg_k, g, p, ws, nullptr, bx, blockIdx.y, blockIdx.z, sb);
+    rowsum_body<D, P, RS_SURV_EV, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, bx, blockIdx.y, blockIdx.z, sb);
   else if (bx < nx_surv + nx_adm)
-    rowsum_body<D, P, RS_ADM_BASE, FOLD>(bank, seg_k, g, p, ws, nullptr, bx - nx_surv, blockIdx.y, blockIdx.z, sb);
+    rowsum_body<D, P, RS_ADM_BASE, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, bx - nx_surv, blockIdx.y, blockIdx.z,
+                                         sb);
   else
-    rowsum_body<D, P, RS_ADM_MUT, FOLD>(bank, seg_k, g, p, ws, nullptr, bx - nx_surv - nx_adm, blockIdx.y,
+    rowsum_body<D, P, RS_ADM_MUT, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, bx - nx_surv - nx_adm, blockIdx.y,
                                         blockIdx.z, sb);
 }
 
@@ -597,7 +624,7 @@ constexpr int kCrossLanes = 8;                      // lanes per state
 constexpr int kCrossPerLane = 16;                   // chunk sums per lane
 constexpr int kCrossStates = 64 / kCrossLanes;      // states per wave
 
-template <int D, int P>
+template <int D, int P, bool KV>
 __global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
   static_assert(kCkStride == 64, "one candidate per lane in the exact walk");
   static_assert((DKV_MAX_CANDIDATES + kCkStride - 1) / kCkStride <= kCrossLanes * kCrossPerLane,
@@ -671,7 +698,7 @@ __global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Wor
     const int c_s = __shfl(ch, sl, 64);
     const int64_t pb_s = (int64_t)shfl_u64(pb, sl);
     const int64_t thr_s = (int64_t)shfl_u64((uint64_t)thr, sl);
-    const uint16_t *rk = static_cast<const uint16_t *>(bank.k) + srow * D;
+    const Desc bd{static_cast<const uint16_t *>(bank.k), static_cast<const uint16_t *>(bank.v)};
     const float nr = bank.knorm[srow];
     const int col = c_s * kCkStride + l;
     uint32_t W = 0;
@@ -680,7 +707,7 @@ __global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Wor
       float acc = 0.0f;
 #pragma unroll
       for (int j = 0; j < D; j += 8) {
-        const u32x4 ra = *reinterpret_cast<const u32x4 *>(rk + j);
+        const u32x4 ra = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(bd, (int64_t)srow, j / 8));
         const u32x4 rc = *reinterpret_cast<const u32x4 *>(ckey + j);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
@@ -713,8 +740,8 @@ __global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Wor
 // (every load and store instruction covers whole rows).
 constexpr int kGatherRows = 4;
 
-template <int D>
-__global__ __launch_bounds__(256) void k_gather_sorted(const void *seg_k, Geom g, Workspace ws, float inv_s2) {
+template <int D, bool KV>
+__global__ __launch_bounds__(256) void k_gather_sorted(const void *seg_k, const void *seg_v, Geom g, Workspace ws) {
   constexpr int CH = D / 8;      // 16-byte chunks per bf16 row
   constexpr int RPP = 256 / CH;  // rows per workgroup pass
   static_assert(kGatherRows <= CH, "one metadata lane per row of the group");
@@ -723,6 +750,7 @@ __global__ __launch_bounds__(256) void k_gather_sorted(const void *seg_k, Geom g
   const int j0 = blockIdx.x * RPP * kGatherRows + threadIdx.x / CH;
   const size_t nb = (size_t)b * g.N;
   if (blockIdx.x * RPP * kGatherRows >= g.N) return;  // whole workgroup
+  const Desc src{static_cast<const uint16_t *>(seg_k), static_cast<const uint16_t *>(seg_v)};
   // loads from clamped (in-range) rows, unconditional so that they overlap
   int xs[kGatherRows];
 #pragma unroll
@@ -730,7 +758,7 @@ __global__ __launch_bounds__(256) void k_gather_sorted(const void *seg_k, Geom g
   u32x4 tmp[kGatherRows];
 #pragma unroll
   for (int u = 0; u < kGatherRows; ++u)
-    tmp[u] = reinterpret_cast<const u32x4 *>(static_cast<const uint16_t *>(seg_k) + (nb + xs[u]) * D)[c];
+    tmp[u] = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(src, (int64_t)(nb + xs[u]), c));
 #pragma unroll
   for (int u = 0; u < kGatherRows; ++u)
     if (j0 + u * RPP < g.N) reinterpret_cast<u32x4 *>(ws.sk + (nb + j0 + u * RPP) * D)[c] = tmp[u];
@@ -764,32 +792,36 @@ __global__ void k_density_out(Geom g, Workspace ws, int64_t *out) {
 
 inline unsigned cdiv(int a, int b) { return (unsigned)((a + b - 1) / b); }
 
-template <int D, int P, bool F>
+// D is the descriptor dimension: the key dimension, or twice it for the
+// [K; V] geometry (KV: the candidates' values seg_v and bank.v are read too).
+template <int D, int P, bool F, bool KV>
 void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                       const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage) {
   const int T = 64 * kWaves;
   const unsigned rowsM = cdiv(g.Mcap, kRowsPerWG), rowsN = cdiv(g.N > 0 ? g.N : 1, kRowsPerWG);
+  const void *sv = seg.v;
   switch (stage) {
     case 0:  // score; the ordered copy is launched after the sort (stage 4)
-      k_score_mfma<D, P, F><<<dim3(rowsN, cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws);
+      k_score_mfma<D, P, F, KV><<<dim3(rowsN, cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws);
       break;
     case 4:
-      k_gather_sorted<D><<<dim3(cdiv(g.N, 256 / (D / 8) * kGatherRows), g.B), 256, 0, s>>>(seg.k, g, ws, p.inv_sigma2);
+      k_gather_sorted<D, KV><<<dim3(cdiv(g.N, 256 / (D / 8) * kGatherRows), g.B), 256, 0, s>>>(seg.k, sv, g, ws);
       break;
     case 1: {
       if (g.N > 0)
-        k_rowsum_mfma<D, P, RS_CHUNK, F><<<dim3(rowsM, cdiv(g.N, kChunksPerSplit * kCkStride), g.B), T, 0, s>>>(
-            bank, seg.k, g, p, ws, nullptr);
-      k_cross<D, P><<<dim3(cdiv(g.Mcap, 4 * kCrossStates), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
+        k_rowsum_mfma<D, P, RS_CHUNK, F, KV><<<dim3(rowsM, cdiv(g.N, kChunksPerSplit * kCkStride), g.B), T, 0, s>>>(
+            bank, seg.k, sv, g, p, ws, nullptr);
+      k_cross<D, P, KV><<<dim3(cdiv(g.Mcap, 4 * kCrossStates), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
       break;
     }
     case 2:
-      k_rowsum_mfma<D, P, RS_FIXUP, F><<<dim3(rowsM, 1, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, out.rho_tilde);
+      k_rowsum_mfma<D, P, RS_FIXUP, F, KV><<<dim3(rowsM, 1, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, out.rho_tilde);
       break;
     case 3: {
       const int nadm = g.N > 0 ? (int)rowsN : 0;
       const unsigned ysplit = cdiv(g.Mcap > g.N ? g.Mcap : g.N, kColsPerSplit);
-      k_maint_mfma<D, P, F><<<dim3(rowsM + 2 * nadm, ysplit, g.B), T, 0, s>>>(bank, seg.k, g, p, ws, (int)rowsM, nadm);
+      k_maint_mfma<D, P, F, KV><<<dim3(rowsM + 2 * nadm, ysplit, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, (int)rowsM,
+                                                                              nadm);
       break;
     }
     default:
@@ -800,60 +832,66 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
 // The +1 of t = 1 + u rides in the MFMA when sigma^2 <= 2^11 (exact there).
 inline bool fold_one(const Prm &p) { return p.inv_sigma2 >= 1.0f / 2048.0f; }
 
-template <int D>
+template <int D, bool KV>
 void mfma_stage_d(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                   const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage) {
   const bool f = fold_one(p);
-  if (p.p == 1) f ? mfma_update_impl<D, 1, true>(bank, seg, g, p, out, ws, s, stage) : mfma_update_impl<D, 1, false>(bank, seg, g, p, out, ws, s, stage);
-  else if (p.p == 2) f ? mfma_update_impl<D, 2, true>(bank, seg, g, p, out, ws, s, stage) : mfma_update_impl<D, 2, false>(bank, seg, g, p, out, ws, s, stage);
-  else f ? mfma_update_impl<D, 4, true>(bank, seg, g, p, out, ws, s, stage) : mfma_update_impl<D, 4, false>(bank, seg, g, p, out, ws, s, stage);
+  if (p.p == 1) f ? mfma_update_impl<D, 1, true, KV>(bank, seg, g, p, out, ws, s, stage) : mfma_update_impl<D, 1, false, KV>(bank, seg, g, p, out, ws, s, stage);
+  else if (p.p == 2) f ? mfma_update_impl<D, 2, true, KV>(bank, seg, g, p, out, ws, s, stage) : mfma_update_impl<D, 2, false, KV>(bank, seg, g, p, out, ws, s, stage);
+  else f ? mfma_update_impl<D, 4, true, KV>(bank, seg, g, p, out, ws, s, stage) : mfma_update_impl<D, 4, false, KV>(bank, seg, g, p, out, ws, s, stage);
 }
 
-template <int D, int P, bool F>
+template <int D, int P, bool F, bool KV>
 void mfma_score_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                      int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws, hipStream_t s) {
   const int T = 64 * kWaves;
   if (g.N > 0 && (score_q || score_f)) {
-    k_score_mfma<D, P, F><<<dim3(cdiv(g.N, kRowsPerWG), cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, g, p, ws);
+    k_score_mfma<D, P, F, KV><<<dim3(cdiv(g.N, kRowsPerWG), cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(
+        bank, seg.k, seg.v, g, p, ws);
     k_score_out<<<dim3(cdiv(g.N, 256), g.B), 256, 0, s>>>(g, ws, score_q, score_f);
   }
   if (density) {
-    k_rowsum_mfma<D, P, RS_DENSITY, F><<<dim3(cdiv(g.Mcap, kRowsPerWG), cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(
-        bank, seg.k, g, p, ws, density);
+    k_rowsum_mfma<D, P, RS_DENSITY, F, KV><<<dim3(cdiv(g.Mcap, kRowsPerWG), cdiv(g.Mcap, kColsPerSplit), g.B), T, 0,
+                                              s>>>(bank, seg.k, seg.v, g, p, ws, density);
     k_density_out<<<dim3(cdiv(g.Mcap, 256), g.B), 256, 0, s>>>(g, ws, density);
   }
 }
 
+template <int D, bool KV>
+void mfma_score_d(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p, int64_t *score_q,
+                  float *score_f, int64_t *density, const Workspace &ws, hipStream_t s) {
+  const bool f = fold_one(p);
+  if (p.p == 1) f ? mfma_score_impl<D, 1, true, KV>(bank, seg, g, p, score_q, score_f, density, ws, s) : mfma_score_impl<D, 1, false, KV>(bank, seg, g, p, score_q, score_f, density, ws, s);
+  else if (p.p == 2) f ? mfma_score_impl<D, 2, true, KV>(bank, seg, g, p, score_q, score_f, density, ws, s) : mfma_score_impl<D, 2, false, KV>(bank, seg, g, p, score_q, score_f, density, ws, s);
+  else f ? mfma_score_impl<D, 4, true, KV>(bank, seg, g, p, score_q, score_f, density, ws, s) : mfma_score_impl<D, 4, false, KV>(bank, seg, g, p, score_q, score_f, density, ws, s);
+}
+
+inline bool kv_geometry(const Prm &p) { return (p.flags & DKV_POLICY_KV_DESCRIPTOR) != 0; }
+
 }  // namespace
 
 // Stage launchers used by the update sequence for bf16 banks:
-// 0 score, 4 ordered copy, 1 crossing, 2 r* fix-up, 3 maintenance.
+// 0 score, 4 ordered copy, 1 crossing, 2 r* fix-up, 3 maintenance.  The
+// descriptor dimension is the key dimension, or twice it for [K; V].
 void launch_gram_mfma(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                       const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage) {
-  if (g.d == 128) mfma_stage_d<128>(bank, seg, g, p, out, ws, s, stage);
-  else mfma_stage_d<64>(bank, seg, g, p, out, ws, s, stage);
+  if (kv_geometry(p)) {
+    if (g.d == 128) mfma_stage_d<256, true>(bank, seg, g, p, out, ws, s, stage);
+    else mfma_stage_d<128, true>(bank, seg, g, p, out, ws, s, stage);
+  } else {
+    if (g.d == 128) mfma_stage_d<128, false>(bank, seg, g, p, out, ws, s, stage);
+    else mfma_stage_d<64, false>(bank, seg, g, p, out, ws, s, stage);
+  }
 }
 
 void launch_score_mfma(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                        int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws, hipStream_t s) {
-  auto go = [&](auto dtag, auto ptag) {
-    constexpr int D = decltype(dtag)::value, P = decltype(ptag)::value;
-    if (fold_one(p)) mfma_score_impl<D, P, true>(bank, seg, g, p, score_q, score_f, density, ws, s);
-    else mfma_score_impl<D, P, false>(bank, seg, g, p, score_q, score_f, density, ws, s);
-  };
-  using I64 = std::integral_constant<int, 64>;
-  using I128 = std::integral_constant<int, 128>;
-  using P1 = std::integral_constant<int, 1>;
-  using P2 = std::integral_constant<int, 2>;
-  using P4 = std::integral_constant<int, 4>;
-  if (g.d == 128) {
-    if (p.p == 1) go(I128{}, P1{});
-    else if (p.p == 2) go(I128{}, P2{});
-    else go(I128{}, P4{});
+  if (kv_geometry(p)) {
+    if (g.d == 128) mfma_score_d<256, true>(bank, seg, g, p, score_q, score_f, density, ws, s);
+    else mfma_score_d<128, true>(bank, seg, g, p, score_q, score_f, density, ws, s);
   } else {
-    if (p.p == 1) go(I64{}, P1{});
-    else if (p.p == 2) go(I64{}, P2{});
-    else go(I64{}, P4{});
+    if (g.d == 128) mfma_score_d<128, false>(bank, seg, g, p, score_q, score_f, density, ws, s);
+    else mfma_score_d<64, false>(bank, seg, g, p, score_q, score_f, density, ws, s);
   }
 }
 

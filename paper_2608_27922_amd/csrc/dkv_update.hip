@@ -105,29 +105,32 @@ __device__ __forceinline__ float dot_row(const float (&kr)[D], const float *col)
 // stages fill with atomic adds.
 // ---------------------------------------------------------------------------
 template <int D, int DT>
-__global__ __launch_bounds__(kThreads) void k_begin(dkv_bank bank, const void *seg_k, Geom g, Workspace ws,
-                                                    float inv_s2, int norms) {
+__global__ __launch_bounds__(kThreads) void k_begin(dkv_bank bank, const void *seg_k, const void *seg_v, Geom g,
+                                                    Workspace ws, float inv_s2, int norms) {
   const int b = blockIdx.y;
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
   if (blockIdx.x > 0) {
     const int j = (blockIdx.x - 1) * kThreads + threadIdx.x;
     if (j < g.N) {
       if (norms) {
-        // |k|^2 in element order, 16-byte loads
+        // |k|^2 (then + |v|^2 for the [K; V] geometry) in element order, 16-byte loads
         float s = 0.0f;
         if constexpr (DT == DKV_BF16) {
-          const uint4 *src = reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(seg_k) + (nb + j) * D);
-          uint4 x[D / 8];
+          for (int part = 0; part < (seg_v ? 2 : 1); ++part) {
+            const uint4 *src =
+                reinterpret_cast<const uint4 *>(static_cast<const uint16_t *>(part ? seg_v : seg_k) + (nb + j) * D);
+            uint4 x[D / 8];
 #pragma unroll
-          for (int q = 0; q < D / 8; ++q) x[q] = src[q];
+            for (int q = 0; q < D / 8; ++q) x[q] = src[q];
 #pragma unroll
-          for (int q = 0; q < D / 8; ++q) {
-            const uint32_t w4[4] = {x[q].x, x[q].y, x[q].z, x[q].w};
+            for (int q = 0; q < D / 8; ++q) {
+              const uint32_t w4[4] = {x[q].x, x[q].y, x[q].z, x[q].w};
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-              const float lo = __uint_as_float(w4[e] << 16), hi = __uint_as_float(w4[e] & 0xFFFF0000u);
-              s = __builtin_fmaf(lo, lo, s);
-              s = __builtin_fmaf(hi, hi, s);
+              for (int e = 0; e < 4; ++e) {
+                const float lo = __uint_as_float(w4[e] << 16), hi = __uint_as_float(w4[e] & 0xFFFF0000u);
+                s = __builtin_fmaf(lo, lo, s);
+                s = __builtin_fmaf(hi, hi, s);
+              }
             }
           }
         } else {
@@ -213,11 +216,13 @@ __global__ __launch_bounds__(kThreads) void k_begin(dkv_bank bank, const void *s
 }
 
 template <int D, int DT>
-void launch_begin(const dkv_bank &bank, const void *seg_k, const Geom &g, const Prm &p, const Workspace &ws,
+void launch_begin(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p, const Workspace &ws,
                   bool norms, hipStream_t s) {
   const int span = g.N > g.Mcap ? g.N : g.Mcap;
+  // [K; V] geometry: candidate norms over the concatenated key-value rows
+  const void *seg_v = (p.flags & DKV_POLICY_KV_DESCRIPTOR) ? seg.v : nullptr;
   k_begin<D, DT><<<dim3((unsigned)(1 + (span + kThreads - 1) / kThreads), (unsigned)g.B), kThreads, 0, s>>>(
-      bank, seg_k, g, ws, p.inv_sigma2, norms ? 1 : 0);
+      bank, seg.k, seg_v, g, ws, p.inv_sigma2, norms ? 1 : 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -988,7 +993,7 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
   dkv_update_out out = outp ? *outp : dkv_update_out{};
   // bf16 banks: Gram stages on MFMA; fp32 banks: the same stages on the VALU.
   constexpr bool kMfma = DT == DKV_BF16;
-  launch_begin<D, DT>(bank, seg.k, g, p, ws, g.N > 0, s);
+  launch_begin<D, DT>(bank, seg, g, p, ws, g.N > 0, s);
   if (g.N > 0) {
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 0);
     else k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, nullptr, nullptr);
@@ -1020,7 +1025,7 @@ template <int D, int DT>
 hipError_t score_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                       int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws,
                       hipStream_t s) {
-  launch_begin<D, DT>(bank, seg.k, g, p, ws, g.N > 0 && (score_q || score_f), s);
+  launch_begin<D, DT>(bank, seg, g, p, ws, g.N > 0 && (score_q || score_f), s);
   if constexpr (DT == DKV_BF16) {
     launch_score_mfma(bank, seg, g, p, (g.N > 0) ? score_q : nullptr, (g.N > 0) ? score_f : nullptr, density, ws, s);
   } else {

@@ -26,7 +26,8 @@ def oracle_params(p: api.Params) -> OParams:
                 "mandatory_source" if f & api.POLICY_SOURCE_FILL else "default")
     return OParams(sigma2_log2=p.sigma2_log2, p=p.p, tau_num=p.tau_num, tau_log2_den=p.tau_log2_den,
                    delta_q=p.delta_q, source_order=bool(f & api.POLICY_SOURCE_ORDER),
-                   refresh_base=bool(f & api.POLICY_REFRESH_BASE), eviction=eviction)
+                   refresh_base=bool(f & api.POLICY_REFRESH_BASE), eviction=eviction,
+                   kv_descriptor=bool(f & api.POLICY_KV_DESCRIPTOR))
 
 
 def mirror(bank: api.Bank, b: int) -> BankState:
@@ -52,7 +53,7 @@ def oracle_step(obanks, K, V, block_id, prm: OParams, gs: int):
     return new, recs
 
 
-def assert_bank_equal(bank: api.Bank, b: int, ob: BankState, ctx=""):
+def assert_bank_equal(bank: api.Bank, b: int, ob: BankState, ctx="", kv=False):
     m = int(bank.occupancy[b].item())
     assert m == ob.m, f"{ctx} bank {b}: occupancy {m} != {ob.m}"
     prov = bank.prov[b, :m].cpu().numpy()
@@ -62,7 +63,10 @@ def assert_bank_equal(bank: api.Bank, b: int, ob: BankState, ctx=""):
     assert np.array_equal(bank.rho[b, :m].cpu().numpy(), ob.rho), f"{ctx} bank {b}: rho differs"
     assert np.array_equal(bank.base[b, :m].cpu().numpy(), ob.base), f"{ctx} bank {b}: base differs"
     kn = bank.knorm[b, :m].cpu().numpy().astype(np.float64)
-    assert np.array_equal(kn, (ob.K * ob.K).sum(1)), f"{ctx} bank {b}: knorm differs"
+    ref = (ob.K * ob.K).sum(1)
+    if kv:  # [K; V] geometry: the descriptor norm
+        ref = ref + (np.asarray(ob.V, np.float64) ** 2).sum(1)
+    assert np.array_equal(kn, ref), f"{ctx} bank {b}: knorm differs"
 
 
 def assert_trace_equal(out: api.UpdateOut, recs, gs: int, prev_obanks, N: int, ctx=""):

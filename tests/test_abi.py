@@ -78,9 +78,13 @@ def test_update_rejects_bad_arguments_before_launch(L):
     assert upd(b, seg, api.Params(tau_num=1).c(), 1 << 40) == -5          # tau must exceed 1
     assert upd(b, seg, api.Params(tau_num=2, tau_log2_den=1).c(), 1 << 40) == -5
     assert upd(b, seg, api.Params(delta_q=0).c(), 1 << 40) == -5
-    assert upd(b, seg, api.Params(flags=0x10).c(), 1 << 40) == -1          # unknown policy bit
+    assert upd(b, seg, api.Params(flags=0x20).c(), 1 << 40) == -1          # unknown policy bits
+    assert upd(b, seg, api.Params(flags=0x80000000).c(), 1 << 40) == -1
     both = api.POLICY_DENSEST_ONLY | api.POLICY_SOURCE_FILL
     assert upd(b, seg, api.Params(flags=both).c(), 1 << 40) == -1          # exclusive eviction policies
+    kv = api.Params(flags=api.POLICY_KV_DESCRIPTOR).c()
+    assert upd(_bank(api, dtype=1), seg, kv, 1 << 40) == -3                 # [K; V] geometry: bf16 banks only
+    assert upd(b, api.DkvSegment(100, 3, 1, None), kv, 1 << 40) == -1       # ... and needs the values
     assert upd(b, api.DkvSegment(9000, 3, 1, 1), good, 1 << 40) == -2
     assert upd(b, api.DkvSegment(100, -1, 1, 1), good, 1 << 40) == -5
     assert upd(b, api.DkvSegment(100, 3, None, 1), good, 1 << 40) == -1

@@ -12,7 +12,8 @@ torch = pytest.importorskip("torch")
 
 pytestmark = pytest.mark.gpu
 
-from oracle import Q23, BankState, attention, candidate_scores, density_from_scratch, weight_q23  # noqa: E402
+from oracle import (Q23, BankState, attention, candidate_scores, density_from_scratch, update_layer,  # noqa: E402
+                    weight_q23)
 from paper_2608_27922_amd import api, synth  # noqa: E402
 from gpu_util import (TORCH_DT, assert_bank_equal, assert_trace_equal, attention_error, dev, host,  # noqa: E402
                       mirror, oracle_params, oracle_step)
@@ -46,7 +47,8 @@ def test_pair_weight_exhaustive(s, p):
 
 # ----------------------------------------------------------------------------- rollouts
 
-def _run_rollout(cfg, blocks, prm, budgets=None, dup_every=0, trace=True, init_full=False, check_every=1):
+def _run_rollout(cfg, blocks, prm, budgets=None, dup_every=0, trace=True, init_full=False, check_every=1,
+                 grid_values=False):
     """Rollout over one layer of `cfg`: GPU update + oracle update per block, compared."""
     B, gs, d, dt = cfg.heads, cfg.group_size, cfg.d, cfg.dtype
     if budgets is None:
@@ -61,6 +63,8 @@ def _run_rollout(cfg, blocks, prm, budgets=None, dup_every=0, trace=True, init_f
         n = Mcap if (init_full and t == 0) else cfg.n_cand
         K = np.stack([s.keys(t, n) for s in streams])
         V = np.stack([s.values(t, n) for s in streams])
+        if grid_values:  # the [K; V] geometry needs values on the key grid too (exact descriptor Gram)
+            V = (np.clip(np.rint(V * 64.0), -127, 127) / 64.0).astype(np.float32)
         if dup_every and t > 0 and t % dup_every == 0:
             for h in range(B):
                 if obanks[h].m:
@@ -73,7 +77,7 @@ def _run_rollout(cfg, blocks, prm, budgets=None, dup_every=0, trace=True, init_f
             if trace:
                 assert_trace_equal(out, recs, gs, obanks, n, ctx=f"block {t}")
             for b in range(B):
-                assert_bank_equal(bank, b, new[b], ctx=f"block {t}")
+                assert_bank_equal(bank, b, new[b], ctx=f"block {t}", kv=bool(prm.flags & api.POLICY_KV_DESCRIPTOR))
         obanks = new
     return bank, obanks
 
@@ -137,6 +141,42 @@ def test_rollout_policy_ablations(policy, dt, d):
     _log(f"rollout policy {policy} dt={dt} d={d}")
     cfg = synth.Config(heads=6, d=d, dtype=dt, n_cand=200, budget=300, group_size=3, **SMALL)
     _run_rollout(cfg, 6, api.Params(sigma2_log2=4 if d == 64 else 5, flags=POLICY_FLAGS[policy]), dup_every=2)
+
+
+@pytest.mark.parametrize("dt,d", [("bf16", 128), ("bf16", 64)])
+def test_rollout_kv_descriptor(dt, d):
+    """The [K; V] retention geometry (descriptor dimension 2 d: 256 and 128) on the
+    near-duplicate rollout, every intermediate and the committed bank bit-exact against
+    the oracle run on the concatenated descriptors."""
+    _log(f"rollout kv descriptor dt={dt} d={d}")
+    cfg = synth.Config(heads=6, d=d, dtype=dt, n_cand=200, budget=300, group_size=3, **SMALL)
+    _run_rollout(cfg, 6, api.Params(sigma2_log2=5 if d == 64 else 6, flags=api.POLICY_KV_DESCRIPTOR), dup_every=2,
+                 grid_values=True)
+
+
+def test_kv_descriptor_score_and_density():
+    """densitykv_score with the [K; V] geometry: candidate scores and the bank's own
+    densities against the oracle on concatenated descriptors."""
+    _log("score kv descriptor")
+    rng = np.random.default_rng(12)
+    B, M, N, d = 3, 200, 150, 128
+    grid = lambda a: np.clip(np.rint(a * 64.0), -127, 127) / 64.0
+    Kb, Vb = grid(rng.standard_normal((B, M, d)) * 0.4), grid(rng.standard_normal((B, M, d)) * 0.4)
+    Kc, Vc = grid(rng.standard_normal((B, N, d)) * 0.4), grid(rng.standard_normal((B, N, d)) * 0.4)
+    prm = api.Params(sigma2_log2=6, flags=api.POLICY_KV_DESCRIPTOR)
+    op = oracle_params(prm)
+    bank = api.Bank(B, M, d, dtype=torch.bfloat16, group_size=1)
+    # build the banks through the update (empty-bank rule), then score a second segment
+    api.update_bank(bank, dev(Kb, "bf16"), dev(Vb, "bf16"), 0, prm)
+    sq, _, dens = api.score(bank, dev(Kc, "bf16"), dev(Vc, "bf16"), prm, want_density=True)
+    torch.cuda.synchronize()
+    for b in range(B):
+        ob = BankState.empty(M, d)
+        (ob,), _ = update_layer([ob], [Kb[b]], [Vb[b].astype(np.float32)], 0, op)
+        desc_b = np.hstack([ob.K, ob.V.astype(np.float64)])
+        S, _, _ = candidate_scores(desc_b, ob.base, np.hstack([Kc[b], Vc[b]]), op)
+        assert np.array_equal(sq[b].cpu().numpy(), S), f"bank {b}: scores differ"
+        assert np.array_equal(dens[b, :ob.m].cpu().numpy(), density_from_scratch(desc_b, op)), f"bank {b}: density"
 
 
 def test_empty_bank_more_candidates_than_budget():
