@@ -876,6 +876,7 @@ __device__ __forceinline__ void commit_surv(const dkv_bank &bank, const Geom &g,
   if (p.flags & DKV_POLICY_REFRESH_BASE) bank.base[rb + to] = rho > p.delta_q ? rho : p.delta_q;
 }
 
+typedef uint32_t vu4 __attribute__((ext_vector_type(4)));
 constexpr int kCommitRows = 1;  // admitted tokens per thread (more was measured slower)
 
 template <int D, int DT>
@@ -903,14 +904,16 @@ __device__ __forceinline__ void commit_adm(const dkv_bank &bank, const dkv_segme
     xs[u] = ws.adm_list[nb + kc];
     tos[u] = ws.adm_dest[nb + kc];
   }
-  uint4 tmp[kCommitRows];
+  vu4 tmp[kCommitRows];
 #pragma unroll
   for (int u = 0; u < kCommitRows; ++u)
-    tmp[u] = reinterpret_cast<const uint4 *>(static_cast<const E *>(isv ? seg.v : seg.k) + (nb + xs[u]) * D)[c];
+    tmp[u] = reinterpret_cast<const vu4 *>(static_cast<const E *>(isv ? seg.v : seg.k) + (nb + xs[u]) * D)[c];
 #pragma unroll
   for (int u = 0; u < kCommitRows; ++u)
     if (k0 + u * kTokWG < rs)
-      reinterpret_cast<uint4 *>(static_cast<E *>(isv ? bank.v : bank.k) + (rb + tos[u]) * D)[c] = tmp[u];
+      // streaming store: the bank rows are not read again by this update
+      __builtin_nontemporal_store(tmp[u], reinterpret_cast<vu4 *>(static_cast<E *>(isv ? bank.v : bank.k) +
+                                                                  (rb + tos[u]) * D) + c);
   if (ch < kCommitRows) {
     // density over the final bank: survivors (directly, or the whole old bank
     // minus the evicted) plus the other co-admitted candidates; lane ch of the

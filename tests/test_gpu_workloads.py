@@ -204,3 +204,45 @@ def test_full_size_workload(name):
     print(f"  attention: max row-normalised error {worst:.3e} over {len(att_heads)} heads x {rows.numel()} rows",
           flush=True)
     assert worst <= 2e-2
+
+
+def test_interface_limits():
+    """N = 8,191 candidates and a budget of 32,767 states (the interface maxima: the
+    13-bit source index of the sort key and the 15-bit slot of the eviction key), two
+    heads sharing the prefix: fills, partial admissions, mandatory and fill evictions,
+    every block against the stored oracle digests plus the full-bank properties."""
+    from golden.make_limit_digests import BLOCKS, TAU_NUM, block_inputs, limits_config
+    path = os.path.join(GOLDEN, "limits.json")
+    if not os.path.exists(path):
+        pytest.skip("oracle digests for the interface limits not generated")
+    with open(path) as f:
+        gold = json.load(f)
+    cfg = limits_config()
+    H, d, N = cfg.heads, cfg.d, cfg.n_cand
+    print(f"limits: {H} banks, N {N}, budget {cfg.budget}, {BLOCKS} blocks", flush=True)
+    prm = api.Params(sigma2_log2=cfg.sigma2_log2, tau_num=TAU_NUM)
+    bank = api.Bank(H, cfg.budget, d, dtype=torch.bfloat16, group_size=cfg.group_size)
+    ws = api.alloc_workspace(bank, N)
+    streams = [synth.HeadStream(cfg, 0, h) for h in range(H)]
+    hist_k, hist_v = [], []
+    for t in range(BLOCKS):
+        bank_keys = [host(bank.k[h, :int(bank.occupancy[h])]) for h in range(H)]
+        Kn, Vn = block_inputs(cfg, streams, t, bank_keys)
+        K, V = dev(Kn, "bf16"), dev(Vn, "bf16")
+        hist_k.append(K)
+        hist_v.append(V)
+        m_prev = bank.occupancy.long().clone()
+        base_prev = bank.base.clone()
+        out = api.UpdateOut(bank, N, trace=True)
+        api.update_bank(bank, K, V, t, prm, workspace=ws, out=out)
+        torch.cuda.synchronize()
+        ctx = f"limits block {t}"
+        step = gold["steps"][t]
+        assert int(out.r_star[0]) == step["r_star"][0], f"{ctx}: r*"
+        for h in range(H):
+            got = _bank_entry(bank, out, h, int(m_prev[h]), N)
+            want = step["heads"][h]
+            bad = [k for k in want if got[k] != want[k]]
+            assert not bad, f"{ctx} head {h}: differs from the oracle in {bad}"
+        _properties(bank, out, prm, m_prev, base_prev, hist_k, hist_v, cfg.group_size, N, ctx)
+        print(f"  block {t}: r* {step['r_star'][0]} occupancy {[int(x) for x in bank.occupancy.cpu()]} ok", flush=True)
