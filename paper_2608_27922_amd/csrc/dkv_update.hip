@@ -1,21 +1,24 @@
 // DensityKV bank update and candidate scoring on gfx950.
 //
 // One update of every bank from one block (Supp. C, Algorithm 1) is the kernel
-// sequence below, all on the caller's stream, with r* kept on the device:
+// sequence below, all on the caller's stream, with r* kept on the device.  The
+// Gram stages of bf16 banks run on MFMA (dkv_gram_mfma.hip: k_score_mfma,
+// k_gather_sorted, k_rowsum_mfma, k_cross, k_maint_mfma); fp32 banks use the
+// VALU kernels of this file (k_score_gram, k_cross_gram, k_fixup, k_maint_gram).
 //
 //   k_begin         clamp occupancy/budget, tested prefix R of the group (Eq. 11),
 //                   score scale 1/b of every bank state (Eq. 6), |k_x|^2 of
-//                   every candidate, cleared accumulators
-//   k_score_gram    S_x = sum_i RNE(w_ix / b_i scaled) and Wcol_x = sum_i W_ix (Eq. 6)
+//                   every candidate, norm steps, cleared accumulators
+//   score           S_x = sum_i RNE(w_ix / b_i scaled) and Wcol_x = sum_i W_ix (Eq. 6)
 //   k_sort_chunks   stable ascending order of S_x, ties by source index (Alg. 1):
 //   k_sort_rank     512-key chunks sorted in registers, then ranked by search
-//   k_cross_gram    prefix sums over the ordered candidates, first violating
-//                   prefix of every bank state (Eqs. 8-9), tile checkpoints
+//   crossing        prefix sums over the ordered candidates (64-candidate
+//                   chunk sums), first violating prefix of every bank state (Eqs. 8-9)
 //   k_feas_bank     c_r for every r and the flags c_r <= e_r (Eqs. 9-10)
 //   k_feas_group    r* of each group (Eq. 11)
-//   k_fixup         projected density rho~(r*) of every bank state
+//   fix-up          projected density rho~(r*) of every bank state
 //   k_select        mandatory + densest eviction (Sec. 3.4 step 3), commit plan
-//   k_maint_gram    weights to the evicted and to the co-admitted states (Supp. C)
+//   maintenance     weights to the evicted and to the co-admitted states (Supp. C)
 //   k_commit        exact density maintenance of the survivors (Supp. C),
 //                   admitted K/V placement, densities and baselines (Eq. 5)
 //
@@ -505,7 +508,8 @@ __global__ __launch_bounds__(kBig) void k_feas_group(Geom g, Workspace ws, int32
 }
 
 // ---------------------------------------------------------------------------
-// k_fixup: rho~_i(r*) = rho_i + checkpointed tiles + the partial tile.
+// k_fixup: rho~_i(r*) = rho_i + the whole 64-candidate chunk sums before r*
+// + the partial chunk.
 // ---------------------------------------------------------------------------
 template <int D, int DT>
 __global__ __launch_bounds__(kThreads) void k_fixup(dkv_bank bank, const void *seg_k, Geom g, Prm p,
@@ -844,11 +848,12 @@ __global__ __launch_bounds__(kThreads) void k_maint_gram(dkv_bank bank, const vo
 }
 
 // ---------------------------------------------------------------------------
-// Commit.  k_commit_surv: thread per surviving state: rho <- rho~(r*) minus its
+// Commit.  commit_surv: thread per surviving state: rho <- rho~(r*) minus its
 // weights to the evicted states (Supp. C); a state that closes a hole (only when
 // more states left than entered) moves with its key, value and metadata.
-// k_commit_adm: wave per admitted candidate: K/V row into its slot, density
-// over the final bank, frozen baseline max(rho, delta) (Eq. 5), provenance.
+// commit_adm: 16-byte chunk per thread of the admitted K/V rows into their
+// slots; one lane per token writes its density over the final bank, frozen
+// baseline max(rho, delta) (Eq. 5), provenance and norm.
 // ---------------------------------------------------------------------------
 template <int D, int DT>
 __device__ __forceinline__ void commit_surv(const dkv_bank &bank, const Geom &g, const Prm &p, const Workspace &ws,
