@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kAThreads) void k_attn_rowwise(dkv_bank bank, const
 // ---------------------------------------------------------------------------
 // bf16 path on MFMA (v_mfma_f32_32x32x16_bf16).
 //
-// A workgroup of 4 waves owns 128 queries, 32 per wave.  Per tile of 64 keys:
+// A workgroup of 8 waves owns 256 queries, 32 per wave.  Per tile of 64 keys:
 //   S^T = K Q^T     A = K tile (LDS), B = Q^T (registers): lane l <-> query
 //                   l % 32, registers <-> keys, so the softmax row statistics
 //                   stay inside the lane (plus one exchange with lane l ^ 32);
@@ -118,7 +118,8 @@ __global__ __launch_bounds__(kAThreads) void k_attn_rowwise(dkv_bank bank, const
 //                   order is permuted identically in both operands
 //                   (slot 8h + j <-> key 8 (j / 4) + 4 h + j % 4).
 // K and V tiles go global -> LDS with 16-byte direct-to-LDS loads (no VGPR
-// staging), double-buffered; rows are stored with an XOR swizzle of their
+// staging) into a ring of three stages (two tiles in flight while one is
+// used); rows are stored with an XOR swizzle of their
 // 16-byte chunks so that both the K reads and the transposed V reads are free
 // of LDS bank conflicts.
 // ---------------------------------------------------------------------------

@@ -257,7 +257,7 @@ __device__ __forceinline__ uint32_t lane_wsum(const f32x16 &u, int nvalid, int h
 constexpr int kColsPerSplit = 1024;
 
 template <int D, int P, bool FOLD, bool KV>
-__global__ __launch_bounds__(64 * kWaves, 2) void k_score_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
+__global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
                                                            Geom g, Prm p, Workspace ws) {
   const int b = blockIdx.z;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;

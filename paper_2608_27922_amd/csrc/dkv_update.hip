@@ -299,18 +299,18 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
 __global__ __launch_bounds__(64) void k_sort_chunks(Geom g, Workspace ws, int64_t *out_score, int source_order) {
   const int b = blockIdx.y, c = blockIdx.x, lane = threadIdx.x;
   const size_t nb = (size_t)b * g.N;
+  // clamped, unconditional loads (so that all eight are in flight at once)
+  int64_t A[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) A[r] = ws.acol[nb + min(c * kChunk + lane * 8 + r, g.N - 1)];
   uint64_t v[8];
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
     const int idx = c * kChunk + lane * 8 + r;
-    uint64_t key = ~0ull;
-    if (idx < g.N) {
-      const int64_t A = ws.acol[nb + idx];
-      // ascending score, ties by source index; or source order alone (policy ablation)
-      key = source_order ? (uint64_t)idx : (((uint64_t)A << 13) | (uint64_t)idx);
-      if (out_score) out_score[nb + idx] = A;
-    }
-    v[r] = key;
+    // ascending score, ties by source index; or source order alone (policy ablation)
+    const uint64_t key = source_order ? (uint64_t)idx : (((uint64_t)A[r] << 13) | (uint64_t)idx);
+    v[r] = idx < g.N ? key : ~0ull;
+    if (out_score && idx < g.N) out_score[nb + idx] = A[r];
   }
 #pragma unroll
   for (int k = 2; k <= kChunk; k <<= 1) {
@@ -351,7 +351,16 @@ __global__ __launch_bounds__(kBig) void k_sort_rank(Geom g, Workspace ws, int32_
   __shared__ uint64_t sk[kSortMax];
   const int np = ws.npad;
   const int nch = np / kChunk;
-  for (int i = threadIdx.x; i < np; i += kBig) sk[i] = ws.skeys[(size_t)b * np + i];
+  {
+    // clamped, unconditional loads, all in flight at once
+    constexpr int kPer = kSortMax / kBig;
+    uint64_t t[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) t[u] = ws.skeys[(size_t)b * np + min((int)threadIdx.x + u * kBig, np - 1)];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u)
+      if ((int)threadIdx.x + u * kBig < np) sk[threadIdx.x + u * kBig] = t[u];
+  }
   __syncthreads();
   const size_t nb = (size_t)b * g.N;
   for (int p = blockIdx.x * kBig + threadIdx.x; p < np; p += gridDim.x * kBig) {
@@ -468,32 +477,54 @@ __global__ __launch_bounds__(kBig) void k_feas_bank(Geom g, Workspace ws) {
   const int m = ws.m[b], M = ws.M[b];
   for (int r = threadIdx.x; r <= R; r += kBig) hist[r] = 0;
   __syncthreads();
-  for (int i = threadIdx.x; i < m; i += kBig) {
-    const int t = ws.first[(size_t)b * g.Mcap + i];
-    if (t <= R) atomicAdd(&hist[t], 1);
+  // four independent (clamped, unconditional) loads per round trip
+  for (int i0 = threadIdx.x; i0 < m; i0 += 4 * kBig) {
+    int t[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) t[u] = ws.first[(size_t)b * g.Mcap + min(i0 + u * kBig, m - 1)];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (i0 + u * kBig < m && t[u] <= R) atomicAdd(&hist[t[u]], 1);
   }
   __syncthreads();
   block_inclusive_scan_lds(hist, R + 1, tmp);
+  // one wave per 64 values of r: the flags by ballot, two mask words per wave
   uint32_t *f = ws.feas + (size_t)b * ws.nfw;
-  for (int w = threadIdx.x; w < ws.nfw; w += kBig) {
-    uint32_t bits = 0;
-    for (int q = 0; q < 32; ++q) {
-      const int r = 32 * w + q;
-      if (r <= R && hist[r] <= max(0, m + r - M)) bits |= 1u << q;
-    }
-    f[w] = bits;
+  const int lane = threadIdx.x & 63;
+  for (int w2 = threadIdx.x >> 6; 2 * w2 < ws.nfw; w2 += kBig / 64) {
+    const int r = 64 * w2 + lane;
+    const bool ok = r <= R && hist[r <= R ? r : 0] <= max(0, m + r - M);
+    const unsigned long long bits = __ballot(ok);
+    if (lane == 0) f[2 * w2] = (uint32_t)bits;
+    if (lane == 1 && 2 * w2 + 1 < ws.nfw) f[2 * w2 + 1] = (uint32_t)(bits >> 32);
   }
 }
 
 // Per group: r* = the largest r feasible for every bank of the group (Eq. 11).
 __global__ __launch_bounds__(kBig) void k_feas_group(Geom g, Workspace ws, int32_t *out_rstar) {
+  constexpr int kMaxWords = (DKV_MAX_CANDIDATES + 1 + 31) / 32;
   const int grp = blockIdx.x;
   __shared__ int tmp[16];
+  __shared__ uint32_t mask[kMaxWords];
   const int b0 = grp * g.gs;
+  const int nfw = ws.nfw, tot = g.gs * nfw;
+  for (int w = threadIdx.x; w < nfw; w += kBig) mask[w] = ~0u;
+  __syncthreads();
+  // the group's masks are consecutive (bank j of the group, word w at j * nfw + w):
+  // AND them into LDS, four independent (clamped, unconditional) loads per round trip
+  const uint32_t *gf = ws.feas + (size_t)b0 * nfw;
+  for (int i0 = threadIdx.x; i0 < tot; i0 += 4 * kBig) {
+    uint32_t v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = gf[min(i0 + u * kBig, tot - 1)];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (i0 + u * kBig < tot) atomicAnd(&mask[(i0 + u * kBig) % nfw], v[u]);
+  }
+  __syncthreads();
   int best = 0;
-  for (int w = threadIdx.x; w < ws.nfw; w += kBig) {
-    uint32_t bits = ~0u;
-    for (int j = 0; j < g.gs; ++j) bits &= ws.feas[(size_t)(b0 + j) * ws.nfw + w];
+  for (int w = threadIdx.x; w < nfw; w += kBig) {
+    const uint32_t bits = mask[w];
     if (bits) best = max(best, 32 * w + 31 - __clz(bits));
   }
   best = block_max(best, tmp);
@@ -851,9 +882,9 @@ __global__ __launch_bounds__(kThreads) void k_maint_gram(dkv_bank bank, const vo
 // Commit.  commit_surv: thread per surviving state: rho <- rho~(r*) minus its
 // weights to the evicted states (Supp. C); a state that closes a hole (only when
 // more states left than entered) moves with its key, value and metadata.
-// commit_adm: 16-byte chunk per thread of the admitted K/V rows into their
-// slots; one lane per token writes its density over the final bank, frozen
-// baseline max(rho, delta) (Eq. 5), provenance and norm.
+// commit_adm: the admitted K/V rows into their slots, four 16-byte chunks of
+// one token per thread; the first lane of each token writes its density over
+// the final bank, frozen baseline max(rho, delta) (Eq. 5), provenance and norm.
 // ---------------------------------------------------------------------------
 template <int D, int DT>
 __device__ __forceinline__ void commit_surv(const dkv_bank &bank, const Geom &g, const Prm &p, const Workspace &ws,
@@ -882,59 +913,60 @@ __device__ __forceinline__ void commit_surv(const dkv_bank &bank, const Geom &g,
 }
 
 typedef uint32_t vu4 __attribute__((ext_vector_type(4)));
-constexpr int kCommitRows = 1;  // admitted tokens per thread (more was measured slower)
+constexpr int kCommitChunks = 4;  // 16-byte chunks of one admitted token per thread (1 and 2 were slower)
+
+// Admitted tokens per workgroup of the commit: a token's K and V rows are
+// 2 * D * sizeof(E) / 16 chunks, kCommitChunks per thread.
+template <int D, int DT>
+__host__ __device__ constexpr int commit_tok_per_wg() {
+  return kThreads / (2 * D * (DT == DKV_BF16 ? 2 : 4) / 16 / kCommitChunks);
+}
 
 template <int D, int DT>
 __device__ __forceinline__ void commit_adm(const dkv_bank &bank, const dkv_segment &seg, const Geom &g,
                                            const Prm &p, const Workspace &ws, int bx) {
   using E = typename std::conditional<DT == DKV_BF16, uint16_t, float>::type;
   constexpr int kCh = D * (int)sizeof(E) / 16;  // 16-byte chunks per key (and per value) row
-  constexpr int kTokWG = kThreads / (2 * kCh);  // tokens per workgroup pass
-  static_assert(kThreads % (2 * kCh) == 0, "whole tokens per workgroup pass");
-  static_assert(kCommitRows <= 2 * kCh, "one metadata lane per token of the group");
+  constexpr int kLanes = 2 * kCh / kCommitChunks;  // lanes per token
+  constexpr int kTokWG = commit_tok_per_wg<D, DT>();
+  static_assert(2 * kCh % kCommitChunks == 0 && kThreads % kLanes == 0, "whole tokens per workgroup");
   const int b = blockIdx.y;
-  const int ch = threadIdx.x % (2 * kCh);
-  const int k0 = bx * kTokWG * kCommitRows + threadIdx.x / (2 * kCh);
+  const int j = threadIdx.x % kLanes;
+  const int k = bx * kTokWG + threadIdx.x / kLanes;
   const int rs = min(ws.r_star[b / g.gs], g.N);
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
-  const bool isv = ch >= kCh;
-  const int c = isv ? ch - kCh : ch;
-  if (bx * kTokWG * kCommitRows >= rs) return;  // whole workgroup
-  // loads from clamped (in-range) entries, unconditional so that they overlap;
+  if (bx * kTokWG >= rs) return;  // whole workgroup
+  // loads from a clamped (in-range) entry, unconditional so that they overlap;
   // only the stores are predicated
-  int xs[kCommitRows], tos[kCommitRows];
+  const int kc = min(k, rs - 1);
+  const int x = ws.adm_list[nb + kc], to = ws.adm_dest[nb + kc];
+  vu4 tmp[kCommitChunks];
 #pragma unroll
-  for (int u = 0; u < kCommitRows; ++u) {
-    const int kc = min(k0 + u * kTokWG, rs - 1);
-    xs[u] = ws.adm_list[nb + kc];
-    tos[u] = ws.adm_dest[nb + kc];
+  for (int u = 0; u < kCommitChunks; ++u) {
+    const int cc = j + kLanes * u;  // chunk of the token's [K row; V row]
+    const bool isv = cc >= kCh;
+    tmp[u] = reinterpret_cast<const vu4 *>(static_cast<const E *>(isv ? seg.v : seg.k) + (nb + x) * D)[cc - (isv ? kCh : 0)];
   }
-  vu4 tmp[kCommitRows];
+  if (k >= rs) return;
 #pragma unroll
-  for (int u = 0; u < kCommitRows; ++u)
-    tmp[u] = reinterpret_cast<const vu4 *>(static_cast<const E *>(isv ? seg.v : seg.k) + (nb + xs[u]) * D)[c];
-#pragma unroll
-  for (int u = 0; u < kCommitRows; ++u)
-    if (k0 + u * kTokWG < rs)
-      // streaming store: the bank rows are not read again by this update
-      __builtin_nontemporal_store(tmp[u], reinterpret_cast<vu4 *>(static_cast<E *>(isv ? bank.v : bank.k) +
-                                                                  (rb + tos[u]) * D) + c);
-  if (ch < kCommitRows) {
+  for (int u = 0; u < kCommitChunks; ++u) {
+    const int cc = j + kLanes * u;
+    const bool isv = cc >= kCh;
+    // streaming store: the bank rows are not read again by this update
+    __builtin_nontemporal_store(tmp[u], reinterpret_cast<vu4 *>(static_cast<E *>(isv ? bank.v : bank.k) + (rb + to) * D) +
+                                            (cc - (isv ? kCh : 0)));
+  }
+  if (j == 0) {
     // density over the final bank: survivors (directly, or the whole old bank
-    // minus the evicted) plus the other co-admitted candidates; lane ch of the
-    // token group writes the metadata of its ch-th token
-    const int k = k0 + ch * kTokWG;
-    if (k < rs) {
-      const int m = ws.m[b];
-      const int n_ev = ws.n_ev[b];
-      const int x = ws.adm_list[nb + k], to = ws.adm_dest[nb + k];
-      const int64_t surv_sum = (n_ev <= m - n_ev) ? ws.wcol[nb + x] - ws.sub_adm[nb + k] : ws.sub_adm[nb + k];
-      const int64_t rho = surv_sum + ws.mut_adm[nb + k];
-      bank.rho[rb + to] = rho;
-      bank.base[rb + to] = rho > p.delta_q ? rho : p.delta_q;
-      bank.prov[rb + to] = ((int64_t)p.block_id << 32) | (int64_t)x;
-      bank.knorm[rb + to] = ws.cnorm[nb + x];
-    }
+    // minus the evicted) plus the other co-admitted candidates
+    const int m = ws.m[b];
+    const int n_ev = ws.n_ev[b];
+    const int64_t surv_sum = (n_ev <= m - n_ev) ? ws.wcol[nb + x] - ws.sub_adm[nb + k] : ws.sub_adm[nb + k];
+    const int64_t rho = surv_sum + ws.mut_adm[nb + k];
+    bank.rho[rb + to] = rho;
+    bank.base[rb + to] = rho > p.delta_q ? rho : p.delta_q;
+    bank.prov[rb + to] = ((int64_t)p.block_id << 32) | (int64_t)x;
+    bank.knorm[rb + to] = ws.cnorm[nb + x];
   }
 }
 
@@ -1022,7 +1054,7 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
   else k_maint_gram<D, DT><<<grid2(g.Mcap + g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws);
   {
     const int nxs = (g.Mcap + kThreads - 1) / kThreads;
-    const int tok_per_wg = kThreads / (2 * D * (DT == DKV_BF16 ? 2 : 4) / 16) * kCommitRows;
+    const int tok_per_wg = commit_tok_per_wg<D, DT>();
     const int nxa = g.N > 0 ? (g.N + tok_per_wg - 1) / tok_per_wg : 0;
     k_commit<D, DT><<<dim3((unsigned)(nxs + nxa), (unsigned)g.B), kThreads, 0, s>>>(bank, seg, g, p, ws, nxs);
   }
