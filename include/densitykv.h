@@ -83,7 +83,7 @@ typedef enum { DKV_BF16 = 0, DKV_F32 = 1 } dkv_dtype;
  * member's budget; with equal budgets this is exactly Eq. 11.
  */
 typedef struct {
-  int32_t num_banks;
+  int32_t num_banks; /* B >= 1, with B * max(capacity, DKV_MAX_CANDIDATES) < 2^31 */
   int32_t group_size;
   int32_t head_dim;  /* 64 or 128 */
   int32_t capacity;  /* Mcap, row stride of every per-slot array, 1..DKV_MAX_CAPACITY */

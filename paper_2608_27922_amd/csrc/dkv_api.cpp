@@ -76,6 +76,9 @@ int check_bank(const dkv_bank *bk) {
   if (bk->head_dim != 64 && bk->head_dim != 128) return DKV_ERR_UNSUPPORTED;
   if (bk->num_banks < 1 || bk->group_size < 1 || bk->num_banks % bk->group_size != 0) return DKV_ERR_SHAPE;
   if (bk->capacity < 1 || bk->capacity > DKV_MAX_CAPACITY) return DKV_ERR_SHAPE;
+  // bank rows and candidate rows are indexed with 32-bit integers in the kernels
+  const int64_t rows = (int64_t)bk->num_banks * (bk->capacity > DKV_MAX_CANDIDATES ? bk->capacity : DKV_MAX_CANDIDATES);
+  if (rows >= (int64_t(1) << 31)) return DKV_ERR_SHAPE;
   if (!bk->k || !bk->v || !bk->knorm || !bk->rho || !bk->base || !bk->prov || !bk->occupancy || !bk->budget)
     return DKV_ERR_INVALID;
   return DKV_OK;

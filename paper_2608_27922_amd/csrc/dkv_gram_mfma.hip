@@ -167,18 +167,18 @@ typedef __attribute__((address_space(3))) void lds_void;
 // Global rows fetched by this thread for the stage starting at column j0 (its
 // key loads, then its aug / scale item); items past ncols repeat the last one.
 template <int D, class RowOf>
-__device__ __forceinline__ void stage_rows(int64_t (&rows)[SCfg<D>::PER + 1], int j0, int ncols, RowOf row_of) {
+__device__ __forceinline__ void stage_rows(int32_t (&rows)[SCfg<D>::PER + 1], int j0, int ncols, RowOf row_of) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
 #pragma unroll
   for (int q = 0; q < SCfg<D>::PER; ++q) {
     const int r = (wave * SCfg<D>::PER + q) * SCfg<D>::RPL + l / SCfg<D>::CH;
-    rows[q] = row_of(min(j0 + r, ncols - 1));
+    rows[q] = (int32_t)row_of(min(j0 + r, ncols - 1));
   }
-  rows[SCfg<D>::PER] = row_of(min(j0 + 16 * wave + (l & 15), ncols - 1));
+  rows[SCfg<D>::PER] = (int32_t)row_of(min(j0 + 16 * wave + (l & 15), ncols - 1));
 }
 
 template <int D, bool kBs, bool SPLIT>
-__device__ __forceinline__ void stage_dma(const int64_t (&rows)[SCfg<D>::PER + 1], const Desc &keys,
+__device__ __forceinline__ void stage_dma(const int32_t (&rows)[SCfg<D>::PER + 1], const Desc &keys,
                                           const uint4 *augs, const float *bs, char *kb, char *ab, float *sb) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
 #pragma unroll
@@ -186,14 +186,14 @@ __device__ __forceinline__ void stage_dma(const int64_t (&rows)[SCfg<D>::PER + 1
     const int blk = wave * SCfg<D>::PER + q;
     const int r = blk * SCfg<D>::RPL + l / SCfg<D>::CH;
     const int c = (l % SCfg<D>::CH) ^ (r % SCfg<D>::CH);
-    __builtin_amdgcn_global_load_lds((void *)desc_chunk<D, SPLIT>(keys, rows[q], c), (lds_void *)(kb + blk * 1024), 16,
+    __builtin_amdgcn_global_load_lds((void *)desc_chunk<D, SPLIT>(keys, (int64_t)rows[q], c), (lds_void *)(kb + blk * 1024), 16,
                                      0, 0);
   }
   // items 16 w .. 16 w + 15: lanes 0-15 of wave w (LDS address = base + lane * size)
   if (l < 16) {
-    __builtin_amdgcn_global_load_lds((void *)(augs + rows[SCfg<D>::PER]), (lds_void *)(ab + 256 * wave), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((void *)(augs + (int64_t)rows[SCfg<D>::PER]), (lds_void *)(ab + 256 * wave), 16, 0, 0);
     if constexpr (kBs)
-      __builtin_amdgcn_global_load_lds((void *)(bs + rows[SCfg<D>::PER]), (lds_void *)(sb + 16 * wave), 4, 0, 0);
+      __builtin_amdgcn_global_load_lds((void *)(bs + (int64_t)rows[SCfg<D>::PER]), (lds_void *)(sb + 16 * wave), 4, 0, 0);
   }
 }
 
@@ -320,7 +320,7 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
   using Full = std::integral_constant<bool, false>;
   using Part = std::integral_constant<bool, true>;
   constexpr int kOps = stage_ops<D, true>();
-  int64_t rows[SCfg<D>::PER + 1];
+  int32_t rows[SCfg<D>::PER + 1];
   // stage t in buffers (t % 3); rows of stage t + 2 loaded one step ahead
   auto step = [&](int t, const char *kb, const char *ab, const float *sb, char *kn, char *an, float *sn)
       __attribute__((always_inline)) {
@@ -385,7 +385,35 @@ constexpr int kChunksPerSplit = 1024 / kCkStride;   // RS_CHUNK: 1024 ordered ca
 template <int D>
 struct StageBufs {
   char *k0, *k1, *k2, *a0, *a1, *a2;
+  uint32_t *cb;  // [3][kSI] column sums of the stages (admitted x admitted only), or null
 };
+
+// DPP move (the partner lane's value) with a compile-time control.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, 0xF, 0xF, false);
+}
+// Transposing reduction over the 16 lanes of a DPP row: the lane holds eight
+// values a[i] (the first butterfly level already applied), returns the row
+// sum for value index lane % 16.  Each level keeps the half of the values
+// selected by one lane bit and adds the partner's copy of it: half-row mirror
+// (bit 2), quad permutations (bits 1, 0).
+__device__ __forceinline__ uint32_t row_transpose_tail(const uint32_t (&a)[8], int l) {
+  uint32_t c[4], d[2];
+  const bool b2 = (l >> 2) & 1, b1 = (l >> 1) & 1, b0 = l & 1;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t keep = b2 ? a[i + 4] : a[i], send = b2 ? a[i] : a[i + 4];
+    c[i] = keep + dpp_mov<0x141>(send);  // row_half_mirror: lane 7 - x within 8 (bit 2 flipped)
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const uint32_t keep = b1 ? c[i + 2] : c[i], send = b1 ? c[i] : c[i + 2];
+    d[i] = keep + dpp_mov<0x4E>(send);  // quad_perm [2,3,0,1]: lane x ^ 2
+  }
+  const uint32_t keep = b0 ? d[1] : d[0], send = b0 ? d[0] : d[1];
+  return keep + dpp_mov<0xB1>(send);  // quad_perm [1,0,3,2]: lane x ^ 1
+}
 
 // Body of one row-sum workgroup (bx, by, bz) = (row block, column split, bank).
 template <int D, int P, int MODE, bool FOLD, bool KV>
@@ -426,9 +454,17 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
     else if constexpr (MODE == RS_ADM_BASE) total = adm_by_ev ? n_ev : n_surv;
     else if constexpr (MODE == RS_ADM_MUT) total = rs;
     else total = m;
-    c0 = by * kColsPerSplit;
-    c1 = min(total, c0 + kColsPerSplit);
+    // admitted x admitted: half splits, since a row block only takes the
+    // columns from its own block on (finer work items balance the triangle)
+    constexpr int kSplit = MODE == RS_ADM_MUT ? kColsPerSplit / 2 : kColsPerSplit;
+    c0 = by * kSplit;
+    c1 = min(total, c0 + kSplit);
   }
+  // admitted x admitted is symmetric (W_xy = W_yx exactly, keys on the grid):
+  // a workgroup takes the column stages from its own row block on; the diagonal
+  // block gives row sums, every stage above it row and column sums
+  constexpr bool kSym = MODE == RS_ADM_MUT;
+  if constexpr (kSym) c0 = max(c0, (int)bx * kRowsPerWG);
   if (MODE != RS_FIXUP && c0 >= c1) return;  // the fix-up always writes rho~, even for r* % 256 == 0
   const int v = bx * kRowsPerWG + wave * 32 + n;
   const bool rv = v < nrows;
@@ -492,14 +528,52 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
     }
     return sm - 16u * kMagic;
   };
+  // column sums of one 32-column tile above the diagonal block: every lane's 16
+  // weights (masked rows and columns as zero), the row partials by DPP
+  // butterfly, and one LDS add per lane (the two rows of each half-wave add
+  // partials of the same 16 columns); returns the lane's row sum
+  const bool rows_full = wg_row0 + kRowsPerWG <= nrows;
+  auto sym_tile = [&](const f32x16 &u, int nvalid, uint32_t *cb, int off) __attribute__((always_inline)) -> uint32_t {
+    const bool full = nvalid >= kCT && rows_full;
+    const bool b3 = (l >> 3) & 1;
+    uint32_t a[8], rsum = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      // values i and i + 8, then the first butterfly level (row mirror: lane
+      // 15 - x, bit 3 flipped)
+      uint32_t r0 = weight_raw<P, FOLD>(u[i], 8388608.0f), r1 = weight_raw<P, FOLD>(u[i + 8], 8388608.0f);
+      if (!full) {
+        r0 = (rv && col_of_reg(i, h) < nvalid) ? r0 : kMagic;
+        r1 = (rv && col_of_reg(i + 8, h) < nvalid) ? r1 : kMagic;
+      }
+      rsum += r0 + r1;
+      const uint32_t keep = b3 ? r1 : r0, send = b3 ? r0 : r1;
+      a[i] = keep + dpp_mov<0x140>(send);
+    }
+    const uint32_t csum = row_transpose_tail(a, l) - 16u * kMagic;
+    atomicAdd(&cb[off + col_of_reg(l & 15, h)], csum);
+    return rsum - 16u * kMagic;
+  };
+  // column sums of stage t (whose adds finished before the barrier just passed)
+  // to the global sums; the buffer is cleared for stage t + 3
+  auto flush_cols = [&](int t) __attribute__((always_inline)) {
+    const int j0 = c0 + t * kSI;
+    if (j0 < wg_row0 + kRowsPerWG || l >= kSI / kWaves) return;
+    uint32_t *cb = sb.cb + (t % 3) * kSI;
+    const int idx = wave * (kSI / kWaves) + l;
+    const uint32_t val = cb[idx];
+    cb[idx] = 0;
+    if (j0 + idx < c1 && val != 0)
+      atomicAdd(reinterpret_cast<unsigned long long *>(&ws.mut_adm[nb + j0 + idx]), (unsigned long long)val);
+  };
   constexpr int kOps = stage_ops<D, false>();
   // Stage t in buffers t % 3.  The global rows of stage t + 2 were fetched one
   // step earlier (list lookups for the maintenance stages), so issuing its
   // loads never waits for the loads still in flight.
   // Two row sets used alternately (the loop is unrolled 6 = lcm(3, 2) times),
   // so that no register copy waits for a lookup still in flight.
-  int64_t rowsA[SCfg<D>::PER + 1], rowsB[SCfg<D>::PER + 1];
-  using Rows = int64_t[SCfg<D>::PER + 1];
+  int32_t rowsA[SCfg<D>::PER + 1], rowsB[SCfg<D>::PER + 1];
+  using Rows = int32_t[SCfg<D>::PER + 1];
   auto step = [&](int t, const char *kb, const char *ab, char *kn, char *an, Rows &use, Rows &fill)
       __attribute__((always_inline)) {
     if (t + 1 < ns) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kOps));
@@ -509,12 +583,22 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
       if (t + 3 < ns) stage_rows<D>(fill, (t + 3) * kSI, ncols, row_of_rel);
       stage_dma<D, false, kColSplit>(use, colbase, colaug, nullptr, kn, an, nullptr);
     }
+    if constexpr (kSym) {
+      if (t > 0) flush_cols(t - 1);
+    }
     f32x16 u0, u1;
     stage_u<D>(kb, ab, rf, u0, u1);
     const int nv0 = ncols - t * kSI;
     const int j0 = c0 + t * kSI;
-    uint32_t s2 = tile_sum(u0, j0, nv0);
-    if (nv0 > kCT) s2 += tile_sum(u1, j0 + kCT, nv0 - kCT);
+    uint32_t s2;
+    if (kSym && j0 >= wg_row0 + kRowsPerWG) {
+      uint32_t *cb = sb.cb + (t % 3) * kSI;
+      s2 = sym_tile(u0, nv0, cb, 0);
+      if (nv0 > kCT) s2 += sym_tile(u1, nv0 - kCT, cb, kCT);
+    } else {
+      s2 = tile_sum(u0, j0, nv0);
+      if (nv0 > kCT) s2 += tile_sum(u1, j0 + kCT, nv0 - kCT);
+    }
     if constexpr (MODE == RS_CHUNK) {
       chunk_sum += s2;
       const bool chunk_end = ((t + 1) % (kCkStride / kSI)) == 0 || t + 1 == ns;
@@ -527,6 +611,10 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
       S64 += s2;
     }
   };
+  if constexpr (kSym) {
+    // cleared before the first stage barrier
+    for (int i = threadIdx.x; i < 3 * kSI; i += 64 * kWaves) sb.cb[i] = 0;
+  }
   if (ns > 0) {
     stage_rows<D>(rowsA, 0, ncols, row_of_rel);
     stage_dma<D, false, kColSplit>(rowsA, colbase, colaug, nullptr, sb.k0, sb.a0, nullptr);
@@ -545,6 +633,13 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
     if (t + 3 < ns) step(t + 3, sb.k0, sb.a0, sb.k2, sb.a2, rowsB, rowsA);
     if (t + 4 < ns) step(t + 4, sb.k1, sb.a1, sb.k0, sb.a0, rowsA, rowsB);
     if (t + 5 < ns) step(t + 5, sb.k2, sb.a2, sb.k1, sb.a1, rowsB, rowsA);
+  }
+  if constexpr (kSym) {
+    if (ns > 0) {
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+      stage_barrier();
+      flush_cols(ns - 1);
+    }
   }
   if constexpr (MODE == RS_CHUNK) return;
   uint64_t tot = S64;
@@ -580,7 +675,7 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
   constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
   __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
   __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
-  const StageBufs<D> sb{k0, k1, k2, a0, a1, a2};
+  const StageBufs<D> sb{k0, k1, k2, a0, a1, a2, nullptr};
   rowsum_body<D, P, MODE, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, out, blockIdx.x, blockIdx.y, blockIdx.z, sb);
 }
 
@@ -593,7 +688,8 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, co
   constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
   __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
   __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
-  const StageBufs<D> sb{k0, k1, k2, a0, a1, a2};
+  __shared__ __attribute__((aligned(16))) uint32_t cb[3 * kSI];
+  const StageBufs<D> sb{k0, k1, k2, a0, a1, a2, cb};
   const int bx = blockIdx.x;
   if (bx < nx_surv)
     rowsum_body<D, P, RS_SURV_EV, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, bx, blockIdx.y, blockIdx.z, sb);
@@ -601,8 +697,8 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, co
     rowsum_body<D, P, RS_ADM_BASE, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, bx - nx_surv, blockIdx.y, blockIdx.z,
                                          sb);
   else
-    rowsum_body<D, P, RS_ADM_MUT, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, bx - nx_surv - nx_adm, blockIdx.y,
-                                        blockIdx.z, sb);
+    rowsum_body<D, P, RS_ADM_MUT, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, (bx - nx_surv - nx_adm) >> 1,
+                                        2 * blockIdx.y + ((bx - nx_surv - nx_adm) & 1), blockIdx.z, sb);
 }
 
 // ---------------------------------------------------------------------------
@@ -820,7 +916,9 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
     case 3: {
       const int nadm = g.N > 0 ? (int)rowsN : 0;
       const unsigned ysplit = cdiv(g.Mcap > g.N ? g.Mcap : g.N, kColsPerSplit);
-      k_maint_mfma<D, P, F, KV><<<dim3(rowsM + 2 * nadm, ysplit, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, (int)rowsM,
+      // x: survivor row blocks, admitted row blocks (x evicted or survivors),
+      // admitted row blocks x two half column splits (x admitted)
+      k_maint_mfma<D, P, F, KV><<<dim3(rowsM + 3 * nadm, ysplit, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, (int)rowsM,
                                                                               nadm);
       break;
     }

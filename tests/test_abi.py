@@ -60,6 +60,13 @@ def test_workspace_size_and_shape_checks(L):
     assert L.densitykv_workspace_size(ctypes.byref(_bank(api, head_dim=96)), 10, ctypes.byref(sz)) == -3
     assert L.densitykv_workspace_size(ctypes.byref(_bank(api, group_size=5)), 10, ctypes.byref(sz)) == -2
     assert L.densitykv_workspace_size(ctypes.byref(_bank(api, capacity=40000)), 10, ctypes.byref(sz)) == -2
+    # rows are 32-bit indices in the kernels: B * max(capacity, 8191) < 2^31
+    assert L.densitykv_workspace_size(ctypes.byref(_bank(api, num_banks=65538, group_size=1, capacity=32767)), 10,
+                                      ctypes.byref(sz)) == 0
+    assert L.densitykv_workspace_size(ctypes.byref(_bank(api, num_banks=65539, group_size=1, capacity=32767)), 10,
+                                      ctypes.byref(sz)) == -2
+    assert L.densitykv_workspace_size(ctypes.byref(_bank(api, num_banks=262177, group_size=1, capacity=16)), 10,
+                                      ctypes.byref(sz)) == -2
     assert L.densitykv_workspace_size(ctypes.byref(_bank(api, dtype=7)), 10, ctypes.byref(sz)) == -1
     assert L.densitykv_workspace_size(ctypes.byref(_bank(api)), 9000, ctypes.byref(sz)) == -2
     assert L.densitykv_workspace_size(None, 10, ctypes.byref(sz)) == -1
