@@ -14,7 +14,9 @@ that all steps do the same work.
 Prints one JSON line.  value = candidate tokens per second per layer-head for
 the whole step (update + attention); the update-only rate and the attention
 TFLOP/s are reported beside it, with the roofline of the dominant kernel and
-the CPU oracle timed on a bounded sample.
+the CPU oracle timed on a bounded sample.  Two extra fields time the sink +
+window + bank attention at the paper's deployment shape and one block of the
+rollout configuration at full scale (360 banks in one launch).
 """
 
 import argparse
@@ -52,6 +54,8 @@ def parse():
                     help="heads in the oracle sample (12 = the whole single_layer step, about 10 s on 16 host threads)")
     ap.add_argument("--no-sink-attention", action="store_true",
                     help="skip the extra measurement of the sink + window + bank attention at the deployment shape")
+    ap.add_argument("--no-rollout-block", action="store_true",
+                    help="skip the extra measurement of one rollout block at full scale (360 banks)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="also run a plain elementwise copy (negation) of this many MiB: the known-size "
                          "reference that scales the HBM byte counters")
@@ -106,6 +110,65 @@ def sink_attention(api, synth, torch, steps=10):
     tf = flops / (ms * 1e-3) / 1e12
     return {"context": f"sink {ns} + window {nw} + bank {M} keys, {nq} queries, {B} heads, d={d}, bf16",
             "ms": round(ms, 4), "tflops": round(tf, 2), "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4)}
+
+
+def rollout_block(api, synth, torch, steps=3):
+    """One block of the rollout configuration at full scale: 30 layers x 12 heads
+    (360 banks, one launch), d = 128, bf16, budget 9,360, 4,680 candidates per
+    bank, 4,680 queries over bank + 4,680-token window.  Three blocks fill the
+    banks first (device-drawn, as the non-compared layers of the full-size
+    tests); each timed step restores that state, updates with block 3 and runs
+    the attention.  Timed with HIP events on the stream."""
+    cfg = synth.WORKLOADS["rollout"]
+    L, H, d, N, M, nq = cfg.layers, cfg.heads, cfg.d, cfg.n_cand, cfg.budget, cfg.n_query
+    B = L * H
+
+    def block(t, n, seed=0):
+        ks, vs = zip(*(synth.torch_layer_block(cfg, layer, t, n, "cuda", seed=seed) for layer in range(L)))
+        return torch.cat(ks).contiguous(), torch.cat(vs).contiguous()
+
+    bank = api.Bank(B, M, d, dtype=torch.bfloat16, group_size=cfg.group_size)
+    ws = api.alloc_workspace(bank, N)
+    prm = api.Params(sigma2_log2=cfg.sigma2_log2)
+    for t in range(3):
+        k, v = block(t, N)
+        api.update_bank(bank, k, v, t, prm, workspace=ws)
+    seg_k, seg_v = block(3, N)
+    q, _ = block(3, nq, seed=1)
+    del k, v
+    out = torch.empty_like(q)
+    upd = api.UpdateOut(bank, N)
+    torch.cuda.synchronize()
+    snap = bank.snapshot()
+    stream = torch.cuda.current_stream()
+    times = []
+    for it in range(steps + 1):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record(stream)
+        bank.restore(snap)
+        ev[1].record(stream)
+        api.update_bank(bank, seg_k, seg_v, 3, prm, workspace=ws, out=upd)
+        ev[2].record(stream)
+        api.bank_attention(bank, q, seg_k, seg_v, out=out)
+        ev[3].record(stream)
+        torch.cuda.synchronize()
+        if it > 0:   # the first pass is a warm-up
+            times.append([ev[0].elapsed_time(ev[3]), ev[1].elapsed_time(ev[2]), ev[2].elapsed_time(ev[3])])
+    step_ms, upd_ms, att_ms = (float(np.mean(c)) for c in zip(*times))
+    m_after = bank.occupancy.cpu().numpy()
+    flops = float(sum(4.0 * nq * (int(m) + N) * d for m in m_after))
+    tf = flops / (att_ms * 1e-3) / 1e12
+    res = {"context": f"rollout: {L} layers x {H} heads ({B} banks, one launch), d={d}, bf16, budget {M}, "
+                      f"block 3 ({N} candidates) into full banks, {nq} queries over bank + {N}-token window",
+           "ms_per_step": round(step_ms, 3), "update_ms": round(upd_ms, 3), "attention_ms": round(att_ms, 3),
+           "tokens_per_s_per_layer_head": round(N / (step_ms * 1e-3), 1),
+           "update_tokens_per_s_per_layer_head": round(N / (upd_ms * 1e-3), 1),
+           "attention_tflops": round(tf, 2), "attention_frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+           "mean_r_star": round(float(upd.r_star.float().mean().item()), 1),
+           "mean_occupancy": round(float(m_after.mean()), 1)}
+    del bank, ws, snap, seg_k, seg_v, q, out
+    torch.cuda.empty_cache()
+    return res
 
 
 def cpu_baseline(case, cfg, n_heads):
@@ -218,6 +281,8 @@ def main():
     }
     if not args.no_sink_attention:
         result["sink_attention"] = sink_attention(api, synth, torch)
+    if not args.no_rollout_block:
+        result["rollout_block"] = rollout_block(api, synth, torch)
     if args.copy_probe_mb:
         nbytes = args.copy_probe_mb << 20
         src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
