@@ -56,6 +56,8 @@ def parse():
                     help="skip the extra measurement of the sink + window + bank attention at the deployment shape")
     ap.add_argument("--no-rollout-block", action="store_true",
                     help="skip the extra measurement of one rollout block at full scale (360 banks)")
+    ap.add_argument("--rollout-block-only", action="store_true",
+                    help="run only the full-scale rollout block and print its figures (for profiling)")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="also run a plain elementwise copy (negation) of this many MiB: the known-size "
                          "reference that scales the HBM byte counters")
@@ -205,6 +207,10 @@ def main():
     import torch
     from paper_2608_27922_amd import api, synth
 
+    if args.rollout_block_only:
+        torch.cuda.set_device(0)
+        print(json.dumps({"rollout_block": rollout_block(api, synth, torch, steps=args.steps)}), flush=True)
+        return
     cfg = synth.WORKLOADS[args.workload]
     if not cfg.starts_full:
         raise SystemExit("bench workload must be a single-update workload (tiny or single_layer)")

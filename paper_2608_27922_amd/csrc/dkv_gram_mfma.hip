@@ -786,6 +786,18 @@ __global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Wor
 #pragma unroll
   for (int s2 = 0; s2 < kCrossStates; ++s2)
     if ((hits >> (kCrossLanes * s2)) & ((1ull << kCrossLanes) - 1)) todo |= 1ull << s2;
+  // The lane's ordered candidate of the chunk being walked stays in registers
+  // while consecutive crossing states share that chunk (often every crossing
+  // state of a wave does: the early chunks hold the candidates most similar
+  // to the bank); descriptors of 2 d elements are re-read per state.
+  constexpr bool kCache = D <= 128;
+  const Desc bd{static_cast<const uint16_t *>(bank.k), static_cast<const uint16_t *>(bank.v)};
+  u32x4 cc[kCache ? D / 8 : 1];
+  float cn = 0.0f;
+  int cached = -1;
+  (void)cc;
+  (void)cn;
+  (void)cached;
   while (todo) {
     const int s2 = __ffsll(todo) - 1;
     todo &= todo - 1;
@@ -794,11 +806,33 @@ __global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Wor
     const int c_s = __shfl(ch, sl, 64);
     const int64_t pb_s = (int64_t)shfl_u64(pb, sl);
     const int64_t thr_s = (int64_t)shfl_u64((uint64_t)thr, sl);
-    const Desc bd{static_cast<const uint16_t *>(bank.k), static_cast<const uint16_t *>(bank.v)};
     const float nr = bank.knorm[srow];
     const int col = c_s * kCkStride + l;
     uint32_t W = 0;
-    if (col < R) {
+    if constexpr (kCache) {
+      // clamped (in-range) candidate, unconditional loads; lanes past R add nothing
+      const size_t crow = nb + min(col, R - 1);
+      if (c_s != cached) {  // wave-uniform
+        const uint16_t *ckey = ws.sk + crow * D;
+#pragma unroll
+        for (int j = 0; j < D; j += 8) cc[j / 8] = *reinterpret_cast<const u32x4 *>(ckey + j);
+        cn = ws.snorm[crow];
+        cached = c_s;
+      }
+      float acc = 0.0f;
+#pragma unroll
+      for (int j = 0; j < D; j += 8) {
+        const u32x4 ra = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(bd, (int64_t)srow, j / 8));
+        const u32x4 rc = cc[j / 8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc = __builtin_fmaf(__uint_as_float(ra[e] << 16), __uint_as_float(rc[e] << 16), acc);
+          acc = __builtin_fmaf(__uint_as_float(ra[e] & 0xFFFF0000u), __uint_as_float(rc[e] & 0xFFFF0000u), acc);
+        }
+      }
+      const float d2 = (nr + cn) - 2.0f * acc;
+      if (col < R) W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
+    } else if (col < R) {
       const uint16_t *ckey = ws.sk + (nb + col) * D;
       float acc = 0.0f;
 #pragma unroll
