@@ -11,7 +11,7 @@
 //                   every candidate, norm steps, cleared accumulators
 //   score           S_x = sum_i RNE(w_ix / b_i scaled) and Wcol_x = sum_i W_ix (Eq. 6)
 //   k_sort_chunks   stable ascending order of S_x, ties by source index (Alg. 1):
-//   k_sort_rank     512-key chunks sorted in registers, then ranked by search
+//   k_sort_rank     512-key chunks sorted in LDS, then ranked by search
 //   crossing        prefix sums over the ordered candidates (64-candidate
 //                   chunk sums), first violating prefix of every bank state (Eqs. 8-9)
 //   k_feas_bank     c_r for every r and the flags c_r <= e_r (Eqs. 9-10)
@@ -283,69 +283,53 @@ __global__ __launch_bounds__(kThreads) void k_score_gram(dkv_bank bank, const vo
 
 // ---------------------------------------------------------------------------
 // Candidate order: unique keys (S_x << 13) | x sorted ascending (ties of S_x
-// by source index).  k_sort_chunks: one wave sorts 512 keys held 8 per lane
-// with a bitonic network (register and lane-shuffle exchanges only).
+// by source index).  k_sort_chunks: a workgroup sorts a chunk of 512 keys in
+// LDS with a bitonic network (one compare-exchange per thread and stage).
 // k_sort_rank: the rank of a key is its position in its own chunk plus the
-// number of smaller keys in every other chunk (binary search in LDS).
+// number of smaller keys in every other chunk, found by branch-free binary
+// searches that run in lockstep over all chunks (ten dependent LDS rounds).
 // ---------------------------------------------------------------------------
 constexpr int kChunk = 512;
+constexpr int kSortThreads = kChunk / 2;
+constexpr int kMaxChunks = kSortMax / kChunk;
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
-  const uint32_t lo = __shfl_xor((uint32_t)v, mask, 64);
-  const uint32_t hi = __shfl_xor((uint32_t)(v >> 32), mask, 64);
-  return ((uint64_t)hi << 32) | lo;
-}
-
-__global__ __launch_bounds__(64) void k_sort_chunks(Geom g, Workspace ws, int64_t *out_score, int source_order) {
-  const int b = blockIdx.y, c = blockIdx.x, lane = threadIdx.x;
+__global__ __launch_bounds__(kSortThreads) void k_sort_chunks(Geom g, Workspace ws, int64_t *out_score,
+                                                              int source_order) {
+  const int b = blockIdx.y, c = blockIdx.x, t = threadIdx.x;
   const size_t nb = (size_t)b * g.N;
-  // clamped, unconditional loads (so that all eight are in flight at once)
-  int64_t A[8];
+  __shared__ uint64_t v[kChunk];
+  // two keys per thread, clamped, unconditional loads
+  int64_t A[2];
 #pragma unroll
-  for (int r = 0; r < 8; ++r) A[r] = ws.acol[nb + min(c * kChunk + lane * 8 + r, g.N - 1)];
-  uint64_t v[8];
+  for (int u = 0; u < 2; ++u) A[u] = ws.acol[nb + min(c * kChunk + t + u * kSortThreads, g.N - 1)];
 #pragma unroll
-  for (int r = 0; r < 8; ++r) {
-    const int idx = c * kChunk + lane * 8 + r;
+  for (int u = 0; u < 2; ++u) {
+    const int idx = c * kChunk + t + u * kSortThreads;
     // ascending score, ties by source index; or source order alone (policy ablation)
-    const uint64_t key = source_order ? (uint64_t)idx : (((uint64_t)A[r] << 13) | (uint64_t)idx);
-    v[r] = idx < g.N ? key : ~0ull;
-    if (out_score && idx < g.N) out_score[nb + idx] = A[r];
+    const uint64_t key = source_order ? (uint64_t)idx : (((uint64_t)A[u] << 13) | (uint64_t)idx);
+    v[t + u * kSortThreads] = idx < g.N ? key : ~0ull;
+    if (out_score && idx < g.N) out_score[nb + idx] = A[u];
   }
-#pragma unroll
+  __syncthreads();
   for (int k = 2; k <= kChunk; k <<= 1) {
-#pragma unroll
     for (int j = k >> 1; j > 0; j >>= 1) {
-      if (j >= 8) {
-        const int lm = j >> 3;
-        const bool lower = (lane & lm) == 0;
-        const bool up = ((lane * 8) & k) == 0;
-#pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          const uint64_t pv = shfl_xor_u64(v[r], lm);
-          const uint64_t lo = v[r] < pv ? v[r] : pv, hi = v[r] < pv ? pv : v[r];
-          v[r] = (lower == up) ? lo : hi;
-        }
-      } else {
-#pragma unroll
-        for (int r = 0; r < 8; ++r) {
-          const int rp = r ^ j;
-          if (rp > r) {
-            const bool up = (((lane * 8) + r) & k) == 0;
-            const uint64_t a = v[r], bb = v[rp];
-            const bool sw = up ? (a > bb) : (a < bb);
-            v[r] = sw ? bb : a;
-            v[rp] = sw ? a : bb;
-          }
-        }
+      // the t-th index i with bit j clear, against i + j; ascending where bit k of i is clear
+      const int i = ((t & ~(j - 1)) << 1) | (t & (j - 1));
+      const uint64_t x = v[i], y = v[i + j];
+      const bool up = (i & k) == 0;
+      if (up ? (x > y) : (x < y)) {
+        v[i] = y;
+        v[i + j] = x;
       }
+      __syncthreads();
     }
   }
-  const size_t base = (size_t)b * ws.npad + c * kChunk + lane * 8;
+  const size_t base = (size_t)b * ws.npad + (size_t)c * kChunk;
 #pragma unroll
-  for (int r = 0; r < 8; ++r) ws.skeys[base + r] = v[r];
+  for (int u = 0; u < 2; ++u) ws.skeys[base + t + u * kSortThreads] = v[t + u * kSortThreads];
 }
 
+template <int NCH>  // chunk slots searched (>= the number of chunks)
 __global__ __launch_bounds__(kBig) void k_sort_rank(Geom g, Workspace ws, int32_t *out_order) {
   const int b = blockIdx.y;
   __shared__ uint64_t sk[kSortMax];
@@ -367,16 +351,26 @@ __global__ __launch_bounds__(kBig) void k_sort_rank(Geom g, Workspace ws, int32_
     const uint64_t key = sk[p];
     if (key == ~0ull) continue;
     const int c = p / kChunk;
-    int rank = p - c * kChunk;
-    for (int c2 = 0; c2 < nch; ++c2) {
-      if (c2 == c) continue;
-      int lo = c2 * kChunk, hi = lo + kChunk;  // count of keys < key in [lo, hi)
-      while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (sk[mid] < key) lo = mid + 1;
-        else hi = mid;
+    // count of keys < key in every chunk: cnt grows by half while the key at
+    // cnt + half - 1 is smaller (at most 511), then by one more if the key at
+    // cnt is smaller; chunks past the last one read the last one and are masked
+    int cnt[NCH];
+#pragma unroll
+    for (int c2 = 0; c2 < NCH; ++c2) cnt[c2] = 0;
+#pragma unroll
+    for (int half = kChunk / 2; half >= 1; half >>= 1) {
+#pragma unroll
+      for (int c2 = 0; c2 < NCH; ++c2) {
+        const int base = min(c2, nch - 1) * kChunk;
+        cnt[c2] += sk[base + cnt[c2] + half - 1] < key ? half : 0;
       }
-      rank += lo - c2 * kChunk;
+    }
+    int rank = p - c * kChunk;
+#pragma unroll
+    for (int c2 = 0; c2 < NCH; ++c2) {
+      const int base = min(c2, nch - 1) * kChunk;
+      const int n2 = cnt[c2] + (sk[base + cnt[c2]] < key ? 1 : 0);
+      if (c2 < nch && c2 != c) rank += n2;
     }
     const int x = (int)(key & 0x1FFFull);
     ws.order[nb + rank] = x;
@@ -1037,9 +1031,16 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
   if (g.N > 0) {
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 0);
     else k_score_gram<D, DT><<<grid2(g.N, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, nullptr, nullptr);
-    k_sort_chunks<<<dim3((unsigned)((g.N + kChunk - 1) / kChunk), (unsigned)g.B), 64, 0, s>>>(
+    k_sort_chunks<<<dim3((unsigned)((g.N + kChunk - 1) / kChunk), (unsigned)g.B), kSortThreads, 0, s>>>(
         g, ws, out.score_q, (p.flags & DKV_POLICY_SOURCE_ORDER) ? 1 : 0);
-    k_sort_rank<<<dim3((unsigned)((ws.npad + kBig - 1) / kBig), (unsigned)g.B), kBig, 0, s>>>(g, ws, out.order);
+    {
+      const dim3 grid((unsigned)((ws.npad + kBig - 1) / kBig), (unsigned)g.B);
+      const int nch = ws.npad / kChunk;
+      if (nch <= 4) k_sort_rank<4><<<grid, kBig, 0, s>>>(g, ws, out.order);
+      else if (nch <= 8) k_sort_rank<8><<<grid, kBig, 0, s>>>(g, ws, out.order);
+      else if (nch <= 12) k_sort_rank<12><<<grid, kBig, 0, s>>>(g, ws, out.order);
+      else k_sort_rank<kMaxChunks><<<grid, kBig, 0, s>>>(g, ws, out.order);
+    }
     if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 4);
   }
   // with no candidates only states that already violate are found (prefix 0)
