@@ -102,6 +102,16 @@ def test_rollout_checkpoint_tiles():
     _run_rollout(cfg, 4, api.Params(sigma2_log2=5), dup_every=2)
 
 
+@pytest.mark.parametrize("n", [1, 64, 65, 512, 513, 1025])
+def test_rollout_candidate_count_boundaries(n):
+    """Candidate counts at the edges of the 64-candidate chunks, the 512-key sort
+    chunks, the 128-row Gram blocks and the 512-column admitted x admitted splits
+    (budget 1,100: the first blocks admit everything, later ones evict)."""
+    _log(f"rollout candidate count n={n}")
+    cfg = synth.Config(heads=2, d=128, dtype="bf16", n_cand=n, budget=1100, group_size=2, **SMALL)
+    _run_rollout(cfg, 4, api.Params(sigma2_log2=5), dup_every=2)
+
+
 def test_rollout_ragged_budgets_independent_heads():
     """group_size = 1 with per-head budgets (the independent per-head variant)."""
     _log("rollout ragged budgets")
