@@ -786,78 +786,136 @@ __global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Wor
 #pragma unroll
   for (int s2 = 0; s2 < kCrossStates; ++s2)
     if ((hits >> (kCrossLanes * s2)) & ((1ull << kCrossLanes) - 1)) todo |= 1ull << s2;
-  // The lane's ordered candidate of the chunk being walked stays in registers
-  // while consecutive crossing states share that chunk (often every crossing
-  // state of a wave does: the early chunks hold the candidates most similar
-  // to the bank); descriptors of 2 d elements are re-read per state.
-  constexpr bool kCache = D <= 128;
   const Desc bd{static_cast<const uint16_t *>(bank.k), static_cast<const uint16_t *>(bank.v)};
-  u32x4 cc[kCache ? D / 8 : 1];
-  float cn = 0.0f;
-  int cached = -1;
-  (void)cc;
-  (void)cn;
-  (void)cached;
-  while (todo) {
-    const int s2 = __ffsll(todo) - 1;
-    todo &= todo - 1;
-    const int sl = kCrossLanes * s2;  // first lane of that state's group
-    const size_t srow = rb + i0 + s2;
-    const int c_s = __shfl(ch, sl, 64);
-    const int64_t pb_s = (int64_t)shfl_u64(pb, sl);
-    const int64_t thr_s = (int64_t)shfl_u64((uint64_t)thr, sl);
-    const float nr = bank.knorm[srow];
-    const int col = c_s * kCkStride + l;
-    uint32_t W = 0;
-    if constexpr (kCache) {
-      // clamped (in-range) candidate, unconditional loads; lanes past R add nothing
-      const size_t crow = nb + min(col, R - 1);
-      if (c_s != cached) {  // wave-uniform
+  if constexpr (D <= 128) {
+    // Exact walk on the matrix cores, all the wave's states that cross in
+    // the same chunk at once: A = the eight states (rows 0-7: lanes 0-7 of
+    // each half-wave, zeros elsewhere), B = the chunk's 64 ordered candidates
+    // in two tiles of 32 (lane n <-> candidate n of the tile), so register
+    // r4 < 4 of lane (n, h) holds the dot product of state 4 h + r4 with
+    // candidate n.  The dot products are exact on the key grid, as in the
+    // chunk sums; then the same binary32 weights, a prefix over the 32
+    // lanes of each tile, and a ballot for the first length reaching the
+    // threshold.
+    constexpr int KSW = D / 16;
+    const int n32 = l & 31, hw = l >> 5;
+    bf16x8 sa[KSW];
+    {
+      const int64_t arow = (int64_t)(rb + min(i0 + (n32 < kCrossStates ? n32 : 0), m - 1));
+#pragma unroll
+      for (int kk = 0; kk < KSW; ++kk) {
+        const u32x4 x = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(bd, arow, 2 * kk + hw));
+        sa[kk] = __builtin_bit_cast(bf16x8, n32 < kCrossStates ? x : u32x4{0u, 0u, 0u, 0u});
+      }
+    }
+    float nrq[4];
+    int64_t pbq[4], thq[4];
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int st = 4 * hw + r4;
+      nrq[r4] = bank.knorm[rb + min(i0 + st, m - 1)];
+      pbq[r4] = (int64_t)shfl_u64(pb, kCrossLanes * st);
+      thq[r4] = (int64_t)shfl_u64((uint64_t)thr, kCrossLanes * st);
+    }
+    while (todo) {
+      const int s0 = __ffsll(todo) - 1;
+      const int c_s = __shfl(ch, kCrossLanes * s0, 64);
+      // the states of this wave that cross in the same chunk (group leaders vote)
+      const unsigned long long lead = __ballot(q == 0 && ch == c_s);
+      unsigned long long same = 0;
+#pragma unroll
+      for (int s2 = 0; s2 < kCrossStates; ++s2)
+        if ((lead >> (kCrossLanes * s2)) & 1ull) same |= 1ull << s2;
+      same &= todo;
+      todo &= ~same;
+      f32x16 acc[2];
+      float cn[2];
+      int cols[2];
+#pragma unroll
+      for (int tl = 0; tl < 2; ++tl) {
+        cols[tl] = c_s * kCkStride + 32 * tl + n32;
+        // clamped (in-range) candidate; lanes past R add nothing
+        const size_t crow = nb + min(cols[tl], R - 1);
         const uint16_t *ckey = ws.sk + crow * D;
+        cn[tl] = ws.snorm[crow];
+        f32x16 ac = {};
 #pragma unroll
-        for (int j = 0; j < D; j += 8) cc[j / 8] = *reinterpret_cast<const u32x4 *>(ckey + j);
-        cn = ws.snorm[crow];
-        cached = c_s;
+        for (int kk = 0; kk < KSW; ++kk) {
+          const u32x4 bx = *reinterpret_cast<const u32x4 *>(ckey + 16 * kk + 8 * hw);
+          ac = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa[kk], __builtin_bit_cast(bf16x8, bx), ac, 0, 0, 0);
+        }
+        acc[tl] = ac;
       }
-      float acc = 0.0f;
 #pragma unroll
-      for (int j = 0; j < D; j += 8) {
-        const u32x4 ra = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(bd, (int64_t)srow, j / 8));
-        const u32x4 rc = cc[j / 8];
+      for (int r4 = 0; r4 < 4; ++r4) {
+        uint32_t w[2];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc = __builtin_fmaf(__uint_as_float(ra[e] << 16), __uint_as_float(rc[e] << 16), acc);
-          acc = __builtin_fmaf(__uint_as_float(ra[e] & 0xFFFF0000u), __uint_as_float(rc[e] & 0xFFFF0000u), acc);
+        for (int tl = 0; tl < 2; ++tl) {
+          const float d2 = (nrq[r4] + cn[tl]) - 2.0f * acc[tl][r4];
+          w[tl] = cols[tl] < R ? weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic : 0u;
+        }
+#pragma unroll
+        for (int o = 1; o < 32; o <<= 1) {
+          const uint32_t y0 = __shfl_up(w[0], o, 32), y1 = __shfl_up(w[1], o, 32);
+          if (n32 >= o) {
+            w[0] += y0;
+            w[1] += y1;
+          }
+        }
+        w[1] += __shfl(w[0], 31, 32);  // the first tile's total
+        const unsigned long long h0 = __ballot(pbq[r4] + (int64_t)w[0] >= thq[r4]);
+        const unsigned long long h1 = __ballot(pbq[r4] + (int64_t)w[1] >= thq[r4]);
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int st = 4 * hh + r4;
+          if (!((same >> st) & 1ull)) continue;
+          const unsigned m0 = (unsigned)(h0 >> (32 * hh)), m1 = (unsigned)(h1 >> (32 * hh));
+          // no hit is unreachable when both passes agree (exact Gram)
+          const int f = m0 ? c_s * kCkStride + __ffs(m0) : (m1 ? c_s * kCkStride + 32 + __ffs(m1) : min(R, (c_s + 1) * kCkStride));
+          if (grp == st) first = f;
         }
       }
-      const float d2 = (nr + cn) - 2.0f * acc;
-      if (col < R) W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
-    } else if (col < R) {
-      const uint16_t *ckey = ws.sk + (nb + col) * D;
-      float acc = 0.0f;
+    }
+  } else {
+    // wide descriptors: one crossing state at a time, one ordered candidate per lane
+    while (todo) {
+      const int s2 = __ffsll(todo) - 1;
+      todo &= todo - 1;
+      const int sl = kCrossLanes * s2;  // first lane of that state's group
+      const size_t srow = rb + i0 + s2;
+      const int c_s = __shfl(ch, sl, 64);
+      const int64_t pb_s = (int64_t)shfl_u64(pb, sl);
+      const int64_t thr_s = (int64_t)shfl_u64((uint64_t)thr, sl);
+      const float nr = bank.knorm[srow];
+      const int col = c_s * kCkStride + l;
+      uint32_t W = 0;
+      if (col < R) {
+        const uint16_t *ckey = ws.sk + (nb + col) * D;
+        float acc = 0.0f;
 #pragma unroll
-      for (int j = 0; j < D; j += 8) {
-        const u32x4 ra = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(bd, (int64_t)srow, j / 8));
-        const u32x4 rc = *reinterpret_cast<const u32x4 *>(ckey + j);
+        for (int j = 0; j < D; j += 8) {
+          const u32x4 ra = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(bd, (int64_t)srow, j / 8));
+          const u32x4 rc = *reinterpret_cast<const u32x4 *>(ckey + j);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc = __builtin_fmaf(__uint_as_float(ra[e] << 16), __uint_as_float(rc[e] << 16), acc);
-          acc = __builtin_fmaf(__uint_as_float(ra[e] & 0xFFFF0000u), __uint_as_float(rc[e] & 0xFFFF0000u), acc);
+          for (int e = 0; e < 4; ++e) {
+            acc = __builtin_fmaf(__uint_as_float(ra[e] << 16), __uint_as_float(rc[e] << 16), acc);
+            acc = __builtin_fmaf(__uint_as_float(ra[e] & 0xFFFF0000u), __uint_as_float(rc[e] & 0xFFFF0000u), acc);
+          }
         }
+        const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
+        W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
       }
-      const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
-      W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
-    }
-    uint32_t wi = W;
+      uint32_t wi = W;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t y = __shfl_up(wi, o, 64);
-      if (l >= o) wi += y;
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(wi, o, 64);
+        if (l >= o) wi += y;
+      }
+      const unsigned long long h2 = __ballot(pb_s + (int64_t)wi >= thr_s);
+      const int f = h2 != 0 ? c_s * kCkStride + (__ffsll(h2) - 1) + 1
+                            : min(R, (c_s + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
+      if (grp == s2) first = f;
     }
-    const unsigned long long h2 = __ballot(pb_s + (int64_t)wi >= thr_s);
-    const int f = h2 != 0 ? c_s * kCkStride + (__ffsll(h2) - 1) + 1
-                          : min(R, (c_s + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
-    if (grp == s2) first = f;
   }
   if (valid && q == 0) {
     ws.first[rb + i] = first;
