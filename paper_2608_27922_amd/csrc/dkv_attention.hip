@@ -356,9 +356,10 @@ __global__ __launch_bounds__(64 * kFWaves, 1) void k_attn_mfma(dkv_bank bank, co
     }
   };
 
+  static_assert(kFStages == 3, "the loop below cycles through three stage buffers");
   issue(0, k0, v0);
   issue(1, k1, v1);
-  for (int t = 0; t < nt; t += 3) {
+  for (int t = 0; t < nt; t += kFStages) {
     step(t, k0, v0, k2, v2);
     if (t + 1 < nt) step(t + 1, k1, v1, k0, v0);
     if (t + 2 < nt) step(t + 2, k2, v2, k1, v1);

@@ -706,9 +706,11 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, co
 // eight states, one per group of 8 lanes; each lane adds 16 of the state's
 // 64-candidate chunk sums, a scan over the group gives every chunk's end
 // prefix, and the first chunk whose end lifts rho + P to tau b
-// (2^k (rho + P) >= T b, integers) is found by ballot.  For each state that
-// crosses, the whole wave then re-walks that chunk with one ordered candidate
-// per lane (same binary32 weights) for the exact length.  States that never
+// (2^k (rho + P) >= T b, integers) is found by ballot.  Then the exact length
+// inside that chunk, with the same binary32 weights: for descriptors of up to
+// 128 elements one 8 x 64 MFMA Gram per distinct crossing chunk covers every
+// state of the wave that crosses there; wider descriptors re-walk the chunk
+// one state at a time with one ordered candidate per lane.  States that never
 // reach the bound within the tested prefixes get R + 1.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
@@ -937,7 +939,7 @@ __global__ __launch_bounds__(256) void k_gather_sorted(const void *seg_k, const 
   const int c = threadIdx.x % CH;
   const int j0 = blockIdx.x * RPP * kGatherRows + threadIdx.x / CH;
   const size_t nb = (size_t)b * g.N;
-  if (blockIdx.x * RPP * kGatherRows >= g.N) return;  // whole workgroup
+  if ((int)blockIdx.x * RPP * kGatherRows >= g.N) return;  // whole workgroup
   const Desc src{static_cast<const uint16_t *>(seg_k), static_cast<const uint16_t *>(seg_v)};
   // loads from clamped (in-range) rows, unconditional so that they overlap
   int xs[kGatherRows];

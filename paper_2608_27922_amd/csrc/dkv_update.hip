@@ -388,7 +388,7 @@ __global__ __launch_bounds__(kThreads) void k_cross_gram(dkv_bank bank, const vo
                                                          Prm p, Workspace ws, int32_t *out_first) {
   const int b = blockIdx.y, i = blockIdx.x * kThreads + threadIdx.x;
   const int m = ws.m[b], R = ws.R[b];
-  if (blockIdx.x * kThreads >= m) return;  // uniform: no live state in this block
+  if ((int)blockIdx.x * kThreads >= m) return;  // uniform: no live state in this block
   const bool act = i < m;
   __shared__ float tk[kTile][D];
   __shared__ float tn[kTile];
@@ -541,7 +541,7 @@ __global__ __launch_bounds__(kThreads) void k_fixup(dkv_bank bank, const void *s
                                                     Workspace ws, int64_t *out_rho_t) {
   const int b = blockIdx.y, i = blockIdx.x * kThreads + threadIdx.x;
   const int m = ws.m[b];
-  if (blockIdx.x * kThreads >= m) return;
+  if ((int)blockIdx.x * kThreads >= m) return;
   const bool act = i < m;
   const int rs = ws.r_star[b / g.gs];
   const int full = rs / kCkStride;
@@ -982,7 +982,7 @@ __global__ __launch_bounds__(kThreads) void k_bank_density(dkv_bank bank, Geom g
                                                            int64_t *out) {
   const int b = blockIdx.y, i = blockIdx.x * kThreads + threadIdx.x;
   const int m = ws.m[b];
-  if (blockIdx.x * kThreads >= m) return;
+  if ((int)blockIdx.x * kThreads >= m) return;
   const bool act = i < m;
   const size_t rb = (size_t)b * g.Mcap;
   __shared__ float tk[kTile][D];
@@ -1001,7 +1001,7 @@ __global__ __launch_bounds__(kThreads) void k_bank_density(dkv_bank bank, Geom g
       const int c = t / D, j = t % D;
       tk[c][j] = c < nc ? load_elem<DT>(bank.k, (rb + j0 + c) * D + j) : 0.0f;
     }
-    if (threadIdx.x < kTile) tn[threadIdx.x] = threadIdx.x < nc ? bank.knorm[rb + j0 + threadIdx.x] : 0.0f;
+    if (threadIdx.x < kTile) tn[threadIdx.x] = (int)threadIdx.x < nc ? bank.knorm[rb + j0 + threadIdx.x] : 0.0f;
     __syncthreads();
     if (act) {
       for (int c = 0; c < nc; ++c) {
