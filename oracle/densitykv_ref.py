@@ -77,6 +77,23 @@ V5  kv_descriptor: the retention geometry uses the concatenated vector [k; v]
     for every density, score and crossing; attention and the stored rows are
     unchanged.  C0 then applies to the values too (the synthetic values of
     this mode are drawn on the key grid).
+V6  sequential: within-block competition (Supp. E, "Within-block competition":
+    sequential density-gated admission, earlier candidates immediately affect
+    later ones).  Reading: the candidates keep the order of C6 (or V1), fixed
+    at the start of the block, and are taken one at a time.  Step j tests the
+    j-th candidate x of every head as a one-candidate prefix against that
+    head's current bank, which already holds the candidates admitted at
+    earlier steps with their exactly maintained densities and their baselines
+    frozen when they entered: violators are the states with
+    2^k (rho_i + W_ix) >= T b_i, e = max(0, m + 1 - M) (so e <= 1), and the
+    j-th candidates enter iff every head of the layer has at most e violators
+    (a rejected step drops them).  On entry each head releases its violator,
+    or, with none and e = 1, its state of largest rho_i + W_ix (ties as C9);
+    survivors rho_i += W_ix - W_i,released; the new state's rho is the sum of
+    W_xi over the survivors, b = max(rho, delta); it takes the released slot,
+    else the next free one.  A head whose bank is empty at the start of the
+    block takes the empty-bank rule (C12) and stays out of the shared test.
+    V2 is applied at the end of the block; V3-V5 are not combined with V6.
 """
 
 from __future__ import annotations
@@ -104,6 +121,7 @@ class Params:
     refresh_base: bool = False
     eviction: str = "default"  # "default" | "densest" | "mandatory_source"
     kv_descriptor: bool = False
+    sequential: bool = False
 
     def __post_init__(self):
         if self.p not in (1, 2, 4):
@@ -114,6 +132,8 @@ class Params:
             raise ValueError("delta must be at least one fixed-point unit")
         if self.eviction not in ("default", "densest", "mandatory_source"):
             raise ValueError("eviction must be 'default', 'densest' or 'mandatory_source'")
+        if self.sequential and (self.eviction != "default" or self.kv_descriptor):
+            raise ValueError("the sequential variant combines only with source_order and refresh_base")
 
     @property
     def tau(self) -> float:
@@ -169,6 +189,8 @@ class UpdateRecord:
     r_star: int
     R: int
     heads: List[HeadRecord] = field(default_factory=list)
+    # sequential variant (V6): per step, whether the j-th candidates entered
+    steps: Optional[np.ndarray] = None
 
 
 # ----------------------------------------------------------------------------
@@ -268,6 +290,8 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
         raise ValueError("every head receives the same number of candidates")
     if N >= (1 << 13):
         raise ValueError("at most 8191 candidates per block")
+    if prm.sequential:
+        return _update_layer_sequential(heads, cand_K, cand_V, block_id, prm)
     # Prefix lengths tested: 0 <= r <= min(N, M) (Eq. 11).
     R = min(N, min(h.budget for h in heads))
     Kc64 = [np.asarray(k, np.float64) for k in cand_K]
@@ -416,6 +440,113 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
                                        c=counts[h], e=e, rho_tilde=rho_t, evicted=evicted,
                                        admitted=admitted,
                                        admitted_slot=np.array(slots, np.int64)))
+    return new_heads, record
+
+
+def _update_layer_sequential(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
+                             cand_V: Sequence[np.ndarray], block_id: int, prm: Params):
+    """Within-block sequential competition (V6), one candidate per step."""
+    H, N = len(heads), int(cand_K[0].shape[0])
+    Kc64 = [np.asarray(k, np.float64) for k in cand_K]
+    empty = [heads[h].m == 0 for h in range(H)]
+    # the empty-bank rule for the heads that start empty (C12, through the default path)
+    start = {}
+    for h in range(H):
+        if empty[h]:
+            nb, rec1 = update_layer([heads[h]], [cand_K[h]], [cand_V[h]], block_id,
+                                    Params(prm.sigma2_log2, prm.p, prm.tau_num, prm.tau_log2_den, prm.delta_q,
+                                           refresh_base=prm.refresh_base))
+            start[h] = (nb[0], rec1.heads[0])
+    # candidate order fixed at the start of the block (C6 / V1)
+    orders, scores = [], []
+    for h in range(H):
+        if empty[h]:
+            orders.append(np.arange(N, dtype=np.int64))
+            scores.append((None, 0))
+            continue
+        S, E, _ = candidate_scores(heads[h].K, heads[h].base, Kc64[h], prm)
+        orders.append(np.arange(N, dtype=np.int64) if prm.source_order
+                      else np.argsort(S, kind="stable").astype(np.int64))
+        scores.append((S, E))
+    # working banks: slots [0, m), capacity M
+    work = []
+    for h in range(H):
+        b = heads[h]
+        cap = max(b.budget, b.m)
+        d = b.K.shape[1] if b.m else Kc64[h].shape[1]
+        Vc = np.asarray(cand_V[h])
+        K = np.zeros((cap, d), np.float64)
+        V = np.zeros((cap,) + Vc.shape[1:], Vc.dtype)
+        K[:b.m], V[:b.m] = b.K, b.V
+        rho, base, prov = (np.zeros(cap, np.int64) for _ in range(3))
+        rho[:b.m], base[:b.m], prov[:b.m] = b.rho, b.base, b.prov
+        work.append(dict(K=K, V=V, rho=rho, base=base, prov=prov, m=b.m, released=set(), entered=[]))
+    live = [h for h in range(H) if not empty[h]]
+    steps = np.zeros(N, bool)
+    for j in range(N):
+        tests = {}
+        ok = True
+        for h in live:
+            w, x = work[h], int(orders[h][j])
+            m = w["m"]
+            W = weight_q23(pair_d2(w["K"][:m], Kc64[h][x:x + 1]), prm)[:, 0]
+            rt = w["rho"][:m] + W
+            viol = np.nonzero(_violates(rt, w["base"][:m], prm))[0]
+            e = max(0, m + 1 - heads[h].budget)
+            tests[h] = (x, W, rt, viol, e)
+            ok = ok and viol.size <= e
+        if not ok or not live:
+            continue
+        steps[j] = True
+        for h in live:
+            w = work[h]
+            x, W, rt, viol, e = tests[h]
+            m = w["m"]
+            if viol.size:
+                ev = int(viol[0])
+            elif e == 1:
+                slots = np.arange(m)
+                ev = int(slots[np.lexsort((slots, w["prov"][:m], -rt))[0]])  # C9 ties
+            else:
+                ev = -1
+            surv = np.array([s for s in range(m) if s != ev], np.int64)
+            if ev >= 0 and surv.size:
+                Wev = weight_q23(pair_d2(w["K"][surv], w["K"][ev:ev + 1]), prm)[:, 0]
+            else:
+                Wev = np.zeros(surv.size, np.int64)
+            w["rho"][surv] = rt[surv] - Wev
+            rho_x = int(W[surv].sum())
+            t = ev if ev >= 0 else m
+            if ev >= 0:
+                if (int(w["prov"][ev]) >> 32) != int(block_id):
+                    w["released"].add(ev)          # an old state left its slot
+            else:
+                w["m"] = m + 1
+            w["K"][t], w["V"][t] = Kc64[h][x], np.asarray(cand_V[h])[x]
+            w["rho"][t], w["base"][t] = rho_x, max(rho_x, prm.delta_q)
+            w["prov"][t] = (int(block_id) << 32) | x
+    record = UpdateRecord(r_star=int(steps.sum()), R=N, steps=steps)
+    new_heads = []
+    for h in range(H):
+        if empty[h]:
+            nb, hr = start[h]
+            new_heads.append(nb)
+            record.heads.append(hr)
+            continue
+        w, m = work[h], work[h]["m"]
+        base = w["base"][:m].copy()
+        if prm.refresh_base:
+            base = np.maximum(w["rho"][:m], prm.delta_q)
+        nb = BankState(heads[h].budget, w["K"][:m].copy(), w["V"][:m].copy(), w["rho"][:m].copy(), base,
+                       w["prov"][:m].copy())
+        new_heads.append(nb)
+        fresh = (nb.prov >> 32) == int(block_id)
+        admitted = np.sort((nb.prov[fresh] & 0xFFFFFFFF).astype(np.int64))
+        S, E = scores[h]
+        none = np.zeros(0, np.int64)
+        record.heads.append(HeadRecord(pi=orders[h], score_q=S, score_exp=E, first_cross=none, c=none,
+                                       e=0, rho_tilde=none, evicted=np.array(sorted(w["released"]), np.int64),
+                                       admitted=admitted, admitted_slot=np.nonzero(fresh)[0].astype(np.int64)))
     return new_heads, record
 
 

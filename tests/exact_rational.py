@@ -12,7 +12,8 @@ with it, and every oracle fixed-point density must round to it.
 The policy ablations of Table 1(b) (Supp. E) are options of ``update``:
 source-order candidates, refreshed baselines, densest-only eviction and
 mandatory + source-order eviction (source order of a bank state = its
-admission order, i.e. ascending provenance).
+admission order, i.e. ascending provenance).  ``update_sequential`` is the
+within-block competition variant, one candidate per step for a whole layer.
 """
 
 from fractions import Fraction as F
@@ -94,3 +95,63 @@ def build(cands, M, **kw):
     """A bank produced by the empty-bank rule from ``cands``."""
     bank, _ = update([], cands, M, **kw)
     return bank
+
+
+def update_sequential(banks, cands, Ms, sigma2=1, p=1, tau=F(2), delta=F(1, 10 ** 6), block_id=1,
+                      source_order=False, refresh_base=False):
+    """Within-block sequential competition for a layer (Supp. E): step j offers the
+    j-th candidate of every head (order fixed at the start of the block) to that
+    head's current bank; every density is recomputed from its definition over the
+    hypothetical bank.  The step is taken iff every head whose bank was not empty
+    at the start has at most e = max(0, m + 1 - M) violators; then each such head
+    releases its violator, or with none and e = 1 its densest state (ties: earlier
+    provenance, then slot), and the candidate takes that slot (else the next one)
+    with baseline max(Phi over the bank it enters, delta).  Heads that start empty
+    take the empty-bank rule.  Returns (new banks, info)."""
+    H, N = len(banks), len(cands[0])
+    out, orders, live = [None] * H, [None] * H, []
+    for h in range(H):
+        if not banks[h]:
+            out[h] = update([], cands[h], Ms[h], sigma2=sigma2, p=p, tau=tau, delta=delta, block_id=block_id,
+                            refresh_base=refresh_base)[0]
+            continue
+        live.append(h)
+        keys = [s["key"] for s in banks[h]]
+        sc = [sum((weight(k, x, sigma2, p) / s["b"] for k, s in zip(keys, banks[h])), F(0)) / len(keys)
+              for x in cands[h]]
+        orders[h] = list(range(N)) if source_order else sorted(range(N), key=lambda x: (sc[x], x))
+    work = {h: [{"key": s["key"], "b": s["b"], "prov": s["prov"]} for s in banks[h]] for h in live}
+    steps = []
+    for j in range(N):
+        tests, ok = {}, bool(live)
+        for h in live:
+            bank, x = work[h], orders[h][j]
+            hyp = [s["key"] for s in bank] + [cands[h][x]]
+            pr = [phi(hyp, i, sigma2, p) for i in range(len(bank))]
+            viol = [i for i in range(len(bank)) if pr[i] / bank[i]["b"] >= tau]
+            e = max(0, len(bank) + 1 - Ms[h])
+            tests[h] = (x, pr, viol, e)
+            ok = ok and len(viol) <= e
+        steps.append(ok)
+        if not ok:
+            continue
+        for h in live:
+            x, pr, viol, e = tests[h]
+            bank = work[h]
+            if viol:
+                t = viol[0]
+            elif e == 1:
+                t = min(range(len(bank)), key=lambda i: (-pr[i], bank[i]["prov"], i))
+            else:
+                t = len(bank)
+                bank.append(None)
+            bank[t] = {"key": cands[h][x], "b": None, "prov": (block_id << 32) | x}
+            bank[t]["b"] = max(phi([s["key"] for s in bank], t, sigma2, p), delta)
+    for h in live:
+        keys = [s["key"] for s in work[h]]
+        for i, s in enumerate(work[h]):
+            s["rho"] = phi(keys, i, sigma2, p)
+            if refresh_base:
+                s["b"] = max(s["rho"], delta)
+        out[h] = work[h]
+    return out, dict(steps=steps, orders=orders)

@@ -314,6 +314,70 @@ def test_policy_rollouts_match_exact_bruteforce(policy):
     assert differs > 0, "the policy never changed a decision in these rollouts"
 
 
+@pytest.mark.parametrize("kw", [dict(tau_num=3), dict(tau_num=2), dict(tau_num=3, source_order=True),
+                                dict(tau_num=3, refresh_base=True)])
+def test_sequential_rollouts_match_exact_bruteforce(kw):
+    """Within-block sequential competition (Supp. E): on random multi-head rollouts
+    the oracle's per-step decisions, commit layout, densities and baselines equal
+    the exact-rational brute force, which recomputes every density from its
+    definition at every step; the rollouts take steps with releases, release states
+    admitted earlier in the same block, and decide differently from the default."""
+    d, H, M = 2, 3, 6
+    prm = Params(sigma2_log2=0, p=2, sequential=True, **kw)
+    dflt = Params(sigma2_log2=0, p=2, **{k: v for k, v in kw.items() if k != "sequential"})
+    taken = released_same_block = differs = 0
+    for seed in range(4):
+        rng = np.random.default_rng(300 + seed)
+        heads = [BankState.empty(M, d) for _ in range(H)]
+        for blk in range(1, 8):
+            N = int(rng.integers(3, 7))
+            Ks = [np.rint(rng.standard_normal((N, d)) * 4) / 2 for _ in range(H)]
+            cands = [[tuple(F(float(v)) for v in row) for row in Ks[h]] for h in range(H)]
+            xb, info = xr.update_sequential([_to_exact_bank(b) for b in heads], cands, [M] * H, sigma2=1, p=2,
+                                            tau=F(kw["tau_num"]), block_id=blk,
+                                            source_order=kw.get("source_order", False),
+                                            refresh_base=kw.get("refresh_base", False))
+            new, rec = update_layer(heads, Ks, [k.astype(np.float32) for k in Ks], blk, prm)
+            ref, _ = update_layer(heads, Ks, [k.astype(np.float32) for k in Ks], blk, dflt)
+            if any(b.m for b in heads):
+                assert rec.steps.tolist() == info["steps"]
+                taken += int(rec.steps.sum())
+                released_same_block += sum(int(rec.steps.sum()) - len(rec.heads[h].admitted) for h in range(H))
+            for h in range(H):
+                nb = new[h]
+                if heads[h].m:
+                    assert rec.heads[h].pi.tolist() == info["orders"][h]
+                assert nb.prov.tolist() == [s["prov"] for s in xb[h]]
+                assert np.array_equal(nb.K, np.array([[float(v) for v in s["key"]] for s in xb[h]]).reshape(nb.K.shape))
+                tol = max(nb.m, 1) * 2.0 ** -22
+                for q, s in zip(nb.rho, xb[h]):
+                    assert abs(q / Q23 - float(s["rho"])) <= tol
+                for q, s in zip(nb.base, xb[h]):
+                    assert abs(q / Q23 - float(s["b"])) <= tol
+                differs += nb.prov.tolist() != ref[h].prov.tolist()
+            heads = new
+    assert taken > 0 and differs > 0
+    if kw["tau_num"] == 3:
+        assert released_same_block > 0, "no state admitted earlier in a block was released by a later one"
+
+
+def test_sequential_release_tie_goes_to_earlier_admission():
+    """An exact densest-release tie in the sequential variant: bank {-10, -1, 1, 10}
+    (full, M = 4), candidate 0, tau = 4 so that no state violates; -1 and 1 have the
+    same projected density, and the earlier-admitted -1 (smaller provenance) leaves."""
+    prm = Params(sigma2_log2=0, p=1, tau_num=4, sequential=True)
+    keys = np.array([[-10.0], [-1.0], [1.0], [10.0]])
+    bank, _ = update_layer([BankState.empty(4, 1)], [keys], [keys.astype(np.float32)], 0, prm)
+    assert bank[0].prov.tolist() == [0, 1, 2, 3]
+    new, rec = update_layer(bank, [np.array([[0.0]])], [np.zeros((1, 1), np.float32)], 1, prm)
+    assert rec.steps.tolist() == [True]
+    assert new[0].prov.tolist() == [0, (1 << 32) | 0, 2, 3]
+    xb, info = xr.update_sequential([_to_exact_bank(bank[0])], [[(F(0),)]], [4], sigma2=1, p=1, tau=F(4),
+                                    block_id=1)
+    assert info["steps"] == [True]
+    assert [s["prov"] for s in xb[0]] == new[0].prov.tolist()
+
+
 def _to_exact_bank_kv(bank: BankState):
     return [{"key": tuple(F(float(v)) for v in np.concatenate([bank.K[i], bank.V[i]])),
              "b": F(int(bank.base[i]), Q23), "prov": int(bank.prov[i])} for i in range(bank.m)]
