@@ -124,7 +124,7 @@ typedef struct {
  * Gram stages, the prefix feasibility test (Eqs. 8-11) and the maintenance are
  * the same.  DENSEST_ONLY and SOURCE_FILL are exclusive; any other bit is
  * rejected with DKV_ERR_INVALID.  (The independent per-head variant is
- * group_size = 1.)
+ * group_size = 1.)  SEQUENTIAL (below) replaces the prefix test itself.
  *   SOURCE_ORDER  the tested prefixes follow the candidates' source order
  *                 instead of the score order (scores are still computed and
  *                 reported in score_q)
@@ -148,6 +148,30 @@ typedef struct {
 #define DKV_POLICY_DENSEST_ONLY 0x4u
 #define DKV_POLICY_SOURCE_FILL 0x8u
 #define DKV_POLICY_KV_DESCRIPTOR 0x10u
+/* Within-block sequential competition (Supp. E, "Within-block competition":
+ * sequential density-gated admission, earlier candidates immediately affect
+ * later ones).  The candidates keep the order above, fixed at the start of the
+ * block, and are offered one at a time: step j tests the j-th candidate x of
+ * every bank of the group as a one-candidate prefix against that bank as it is
+ * at that step (earlier admissions included, with exactly maintained
+ * densities and baselines frozen when they entered).  Violators are the states
+ * with 2^k (rho_i + W_ix) >= T b_i and e = max(0, m + 1 - M) <= 1; the step is
+ * taken iff every bank of the group has at most e violators.  Then each bank
+ * releases its violator, or with none and e = 1 its state of largest
+ * rho_i + W_ix (ties: smaller provenance, then lower slot); survivors get
+ * rho_i += W_ix - W_i,released; x gets rho = sum of W_xi over the survivors and
+ * b = max(rho, delta), in the released slot or the next free one.  A rejected
+ * step drops its candidates.  A bank that is empty at the start of the block
+ * takes the empty-bank rule and stays out of the shared test.  Combines with
+ * SOURCE_ORDER and REFRESH_BASE only (DKV_ERR_INVALID otherwise); bf16 banks
+ * only (DKV_ERR_UNSUPPORTED); group_size <= 256 (DKV_ERR_SHAPE).  The update
+ * keeps the pairwise weights of [bank; candidates] in the workspace:
+ * densitykv_workspace_size_policy adds num_banks * (capacity + n)^2 * 4 bytes.
+ * Outputs: r_star = steps taken, n_admitted / admitted = this block's
+ * candidates in the final bank, n_evicted / evicted = pre-update slots whose
+ * state left; first_cross and rho_tilde are not written.  The steps are
+ * inherently sequential: one workgroup per group walks them in order. */
+#define DKV_POLICY_SEQUENTIAL 0x20u
 
 /* Optional outputs of densitykv_update_bank (any pointer may be NULL).
  *   r_star       [G]        admitted prefix length of each group (Eq. 11)
@@ -177,6 +201,10 @@ typedef struct {
 /* Bytes of device workspace densitykv_score / densitykv_update_bank need for
  * this bank geometry and n_cand candidates per bank.  Host-only; enqueues nothing. */
 int densitykv_workspace_size(const dkv_bank *bank, int32_t n_cand, size_t *bytes);
+
+/* The same for the given dkv_params.flags: larger with DKV_POLICY_SEQUENTIAL,
+ * equal to densitykv_workspace_size otherwise.  Host-only. */
+int densitykv_workspace_size_policy(const dkv_bank *bank, int32_t n_cand, uint32_t flags, size_t *bytes);
 
 /*
  * Candidate scores against the current banks (Eq. 6; Supp. C), without

@@ -176,7 +176,7 @@ class HeadRecord:
     score_q: Optional[np.ndarray]  # S_x of C6 in source order, or None for an empty bank
     score_exp: int                 # E of C6 (0 for an empty bank)
     first_cross: np.ndarray        # per old slot: smallest r with a violation, R+1 if none
-    c: np.ndarray                  # violator counts c_r, r = 0..R
+    c: np.ndarray                  # violator counts c_r, r = 0..R (sequential: per step)
     e: int                         # e_{r*}
     rho_tilde: np.ndarray          # per old slot: rho + P(r*)
     evicted: np.ndarray            # old slots, ascending
@@ -483,6 +483,7 @@ def _update_layer_sequential(heads: Sequence[BankState], cand_K: Sequence[np.nda
         work.append(dict(K=K, V=V, rho=rho, base=base, prov=prov, m=b.m, released=set(), entered=[]))
     live = [h for h in range(H) if not empty[h]]
     steps = np.zeros(N, bool)
+    nviol = np.zeros((H, N), np.int64)   # violators of every head at every step (record only)
     for j in range(N):
         tests = {}
         ok = True
@@ -494,6 +495,7 @@ def _update_layer_sequential(heads: Sequence[BankState], cand_K: Sequence[np.nda
             viol = np.nonzero(_violates(rt, w["base"][:m], prm))[0]
             e = max(0, m + 1 - heads[h].budget)
             tests[h] = (x, W, rt, viol, e)
+            nviol[h, j] = viol.size
             ok = ok and viol.size <= e
         if not ok or not live:
             continue
@@ -544,7 +546,7 @@ def _update_layer_sequential(heads: Sequence[BankState], cand_K: Sequence[np.nda
         admitted = np.sort((nb.prov[fresh] & 0xFFFFFFFF).astype(np.int64))
         S, E = scores[h]
         none = np.zeros(0, np.int64)
-        record.heads.append(HeadRecord(pi=orders[h], score_q=S, score_exp=E, first_cross=none, c=none,
+        record.heads.append(HeadRecord(pi=orders[h], score_q=S, score_exp=E, first_cross=none, c=nviol[h],
                                        e=0, rho_tilde=none, evicted=np.array(sorted(w["released"]), np.int64),
                                        admitted=admitted, admitted_slot=np.nonzero(fresh)[0].astype(np.int64)))
     return new_heads, record

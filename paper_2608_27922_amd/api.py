@@ -25,8 +25,10 @@ POLICY_REFRESH_BASE = 0x2   # b = max(rho, delta) for every retained state after
 POLICY_DENSEST_ONLY = 0x4   # no mandatory set: release the e densest states
 POLICY_SOURCE_FILL = 0x8    # violators, then fill in admission order
 POLICY_KV_DESCRIPTOR = 0x10  # densities on the concatenated [k; v] rows (bf16 banks; values on the key grid)
+POLICY_SEQUENTIAL = 0x20    # within-block sequential competition (bf16 banks; larger workspace)
 
-ENTRY_POINTS = ("densitykv_workspace_size", "densitykv_score", "densitykv_update_bank",
+ENTRY_POINTS = ("densitykv_workspace_size", "densitykv_workspace_size_policy", "densitykv_score",
+                "densitykv_update_bank",
                 "densitykv_bank_attention", "densitykv_bank_attention_sink", "densitykv_pair_weight_q23",
                 "densitykv_status_string")
 
@@ -67,6 +69,8 @@ def lib() -> ctypes.CDLL:
         L = ctypes.CDLL(LIB_PATH)
         P = ctypes.POINTER
         L.densitykv_workspace_size.argtypes = [P(DkvBank), ctypes.c_int32, P(ctypes.c_size_t)]
+        L.densitykv_workspace_size_policy.argtypes = [P(DkvBank), ctypes.c_int32, ctypes.c_uint32,
+                                                      P(ctypes.c_size_t)]
         L.densitykv_score.argtypes = [P(DkvBank), P(DkvSegment), P(DkvParams), _vp, _vp, _vp, _vp,
                                       ctypes.c_size_t, _vp]
         L.densitykv_update_bank.argtypes = [P(DkvBank), P(DkvSegment), P(DkvParams), P(DkvUpdateOut), _vp,
@@ -181,15 +185,20 @@ class Bank:
         self._buf.copy_(snap)
 
 
-def workspace_size(bank: Bank, n_cand: int) -> int:
+def workspace_size(bank: Bank, n_cand: int, flags: int = 0) -> int:
+    """densitykv_workspace_size, or densitykv_workspace_size_policy for non-zero flags."""
     out = ctypes.c_size_t(0)
     cb = bank.c()
-    _check(lib().densitykv_workspace_size(ctypes.byref(cb), int(n_cand), ctypes.byref(out)), "workspace_size")
+    if flags:
+        _check(lib().densitykv_workspace_size_policy(ctypes.byref(cb), int(n_cand), int(flags), ctypes.byref(out)),
+               "workspace_size_policy")
+    else:
+        _check(lib().densitykv_workspace_size(ctypes.byref(cb), int(n_cand), ctypes.byref(out)), "workspace_size")
     return int(out.value)
 
 
-def alloc_workspace(bank: Bank, n_cand: int) -> torch.Tensor:
-    return torch.empty(workspace_size(bank, n_cand), dtype=torch.uint8, device=bank.k.device)
+def alloc_workspace(bank: Bank, n_cand: int, flags: int = 0) -> torch.Tensor:
+    return torch.empty(workspace_size(bank, n_cand, flags), dtype=torch.uint8, device=bank.k.device)
 
 
 def _segment(seg_k: Optional[torch.Tensor], seg_v: Optional[torch.Tensor], n: int, block_id: int):
@@ -218,7 +227,7 @@ def score(bank: Bank, seg_k: torch.Tensor, seg_v: torch.Tensor, params: Params =
     sq = torch.zeros(bank.B, n, dtype=torch.int64, device=dev) if want_q else None
     sf = torch.zeros(bank.B, n, dtype=torch.float32, device=dev) if want_f32 else None
     dens = torch.zeros(bank.B, bank.Mcap, dtype=torch.int64, device=dev) if want_density else None
-    ws = workspace if workspace is not None else alloc_workspace(bank, n)
+    ws = workspace if workspace is not None else alloc_workspace(bank, n, params.flags)
     cb, cs, cp = bank.c(), _segment(seg_k, seg_v, n, 0), params.c()
     _check(lib().densitykv_score(ctypes.byref(cb), ctypes.byref(cs), ctypes.byref(cp), _ptr(sq), _ptr(sf),
                                  _ptr(dens), _ptr(ws), ws.numel(), _stream()), "score")
@@ -254,7 +263,7 @@ def update_bank(bank: Bank, seg_k: Optional[torch.Tensor], seg_v: Optional[torch
                 out: Optional[UpdateOut] = None) -> Optional[UpdateOut]:
     """densitykv_update_bank: updates `bank` in place on the current stream."""
     n = _check_seg(bank, seg_k, seg_v)
-    ws = workspace if workspace is not None else alloc_workspace(bank, n)
+    ws = workspace if workspace is not None else alloc_workspace(bank, n, params.flags)
     cb, cs, cp = bank.c(), _segment(seg_k, seg_v, n, block_id), params.c()
     co = out.c() if out is not None else None
     _check(lib().densitykv_update_bank(ctypes.byref(cb), ctypes.byref(cs), ctypes.byref(cp),

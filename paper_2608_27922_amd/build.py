@@ -13,7 +13,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libdensitykv.so")
-SOURCES = ["dkv_api.cpp", "dkv_update.hip", "dkv_gram_mfma.hip", "dkv_attention.hip"]
+SOURCES = ["dkv_api.cpp", "dkv_update.hip", "dkv_gram_mfma.hip", "dkv_attention.hip", "dkv_sequential.hip"]
 ARCH = "gfx950"
 
 FLAGS = [

@@ -11,7 +11,7 @@ namespace dkv {
 
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base) {
+size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base, bool seq) {
   size_t off = 0;
   const size_t Bz = (size_t)B, Mz = (size_t)Mcap, Nz = (size_t)(N > 0 ? N : 1);
   // chunk sums per row, padded to a multiple of 4 so that rows are 16-byte aligned
@@ -60,6 +60,13 @@ size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, cha
   w.skeys = (uint64_t *)take(Bz * (size_t)npad * 8);
   w.npad = npad;
   w.nck = nck > 0 ? nck : 4;
+  if (seq) {
+    const size_t L = (size_t)Mcap + (size_t)(N > 0 ? N : 0);
+    w.gram = (uint32_t *)take(Bz * L * L * 4);
+    w.grow = (int32_t *)take(Bz * Mz * 4);
+    w.lim = (int64_t *)take(Bz * Mz * 8);
+    w.gram_ld = (int)L;
+  }
   if (ws) *ws = w;
   return off;
 }
@@ -95,9 +102,12 @@ int check_segment(const dkv_segment *sg) {
 int check_params(const dkv_params *p, Prm *out, int block_id) {
   if (!p) return DKV_ERR_INVALID;
   const uint32_t known = DKV_POLICY_SOURCE_ORDER | DKV_POLICY_REFRESH_BASE | DKV_POLICY_DENSEST_ONLY |
-                         DKV_POLICY_SOURCE_FILL | DKV_POLICY_KV_DESCRIPTOR;
+                         DKV_POLICY_SOURCE_FILL | DKV_POLICY_KV_DESCRIPTOR | DKV_POLICY_SEQUENTIAL;
   if (p->flags & ~known) return DKV_ERR_INVALID;
   if ((p->flags & DKV_POLICY_DENSEST_ONLY) && (p->flags & DKV_POLICY_SOURCE_FILL)) return DKV_ERR_INVALID;
+  if ((p->flags & DKV_POLICY_SEQUENTIAL) &&
+      (p->flags & (DKV_POLICY_DENSEST_ONLY | DKV_POLICY_SOURCE_FILL | DKV_POLICY_KV_DESCRIPTOR)))
+    return DKV_ERR_INVALID;
   if (p->p != 1 && p->p != 2 && p->p != 4) return DKV_ERR_UNSUPPORTED;
   if (p->sigma2_log2 < -8 || p->sigma2_log2 > 16) return DKV_ERR_UNSUPPORTED;
   if (p->tau_log2_den < 0 || p->tau_log2_den > 8) return DKV_ERR_RANGE;
@@ -117,6 +127,10 @@ int check_params(const dkv_params *p, Prm *out, int block_id) {
 // The [K; V] retention geometry runs on the bf16 MFMA path and reads the
 // candidates' values.
 int check_geometry(const dkv_bank *bk, const dkv_segment *seg, const Prm &p) {
+  if (p.flags & DKV_POLICY_SEQUENTIAL) {
+    if (bk->dtype != DKV_BF16) return DKV_ERR_UNSUPPORTED;
+    if (bk->group_size > kSeqMaxGroup) return DKV_ERR_SHAPE;
+  }
   if (!(p.flags & DKV_POLICY_KV_DESCRIPTOR)) return DKV_OK;
   if (bk->dtype != DKV_BF16) return DKV_ERR_UNSUPPORTED;
   if (seg->n > 0 && !seg->v) return DKV_ERR_INVALID;
@@ -149,6 +163,16 @@ int densitykv_workspace_size(const dkv_bank *bank, int32_t n_cand, size_t *bytes
   return DKV_OK;
 }
 
+int densitykv_workspace_size_policy(const dkv_bank *bank, int32_t n_cand, uint32_t flags, size_t *bytes) {
+  int rc = check_bank(bank);
+  if (rc) return rc;
+  if (!bytes) return DKV_ERR_INVALID;
+  if (n_cand < 0 || n_cand > DKV_MAX_CANDIDATES) return DKV_ERR_SHAPE;
+  *bytes = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity, n_cand,
+                            bank->head_dim, nullptr, nullptr, (flags & DKV_POLICY_SEQUENTIAL) != 0);
+  return DKV_OK;
+}
+
 int densitykv_score(const dkv_bank *bank, const dkv_segment *seg, const dkv_params *prm,
                     int64_t *cand_score_q, float *cand_score_f32, int64_t *bank_density_q,
                     void *workspace, size_t workspace_bytes, void *stream) {
@@ -178,7 +202,8 @@ int densitykv_update_bank(dkv_bank *bank, const dkv_segment *seg, const dkv_para
   if (rc) return rc;
   Workspace ws{};
   const size_t need = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity,
-                                       seg->n, bank->head_dim, &ws, static_cast<char *>(workspace));
+                                       seg->n, bank->head_dim, &ws, static_cast<char *>(workspace),
+                                       (p.flags & DKV_POLICY_SEQUENTIAL) != 0);
   if (!workspace || workspace_bytes < need) return DKV_ERR_WORKSPACE;
   const Geom g = geom_of(bank, seg->n);
   hipError_t e = launch_update(*bank, *seg, g, p, out, ws, static_cast<hipStream_t>(stream));

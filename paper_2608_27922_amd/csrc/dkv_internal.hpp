@@ -55,9 +55,15 @@ struct Workspace {
   uint64_t *skeys;     // [B, npad] sort keys, sorted within 512-key chunks
   int npad;            // N rounded up to 512
   int nck;
+  // sequential competition only (null otherwise)
+  uint32_t *gram;      // [B, L, L] W between the items [slots 0..Mcap); candidates 0..N)], L = Mcap + N
+  int32_t *grow;       // [B, Mcap] item of the state in each slot (slot s, or Mcap + candidate)
+  int64_t *lim;        // [B, Mcap] ceil(T b / 2^k): the state violates when rho + W reaches it
+  int gram_ld;         // L
 };
 
-size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base);
+size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base, bool seq = false);
+constexpr int kSeqMaxGroup = 256;  // banks per group in the sequential competition
 
 // Geometry and parameters passed by value to every kernel.
 struct Geom {
@@ -93,6 +99,9 @@ void launch_score_mfma(const dkv_bank &bank, const dkv_segment &seg, const Geom 
                        int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws, hipStream_t s);
 hipError_t launch_pair_weight(const float *d2, int64_t n, const Prm &p, int32_t *w,
                               hipStream_t s);
+// Within-block sequential competition after the order is known (bf16 banks).
+hipError_t launch_sequential(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
+                             const dkv_update_out &out, const Workspace &ws, hipStream_t s);
 
 #if defined(__HIPCC__)
 // ---------------------------------------------------------------------------

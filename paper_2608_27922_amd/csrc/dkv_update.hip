@@ -1041,8 +1041,10 @@ hipError_t update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom 
       else if (nch <= 12) k_sort_rank<12><<<grid, kBig, 0, s>>>(g, ws, out.order);
       else k_sort_rank<kMaxChunks><<<grid, kBig, 0, s>>>(g, ws, out.order);
     }
-    if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 4);
   }
+  // within-block sequential competition: the rest is one candidate per step
+  if (kMfma && (p.flags & DKV_POLICY_SEQUENTIAL)) return launch_sequential(bank, seg, g, p, out, ws, s);
+  if (g.N > 0 && kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 4);
   // with no candidates only states that already violate are found (prefix 0)
   if (kMfma) launch_gram_mfma(bank, seg, g, p, out, ws, s, 1);
   else k_cross_gram<D, DT><<<grid2(g.Mcap, kThreads, g.B), kThreads, 0, s>>>(bank, seg.k, g, p, ws, out.first_cross);

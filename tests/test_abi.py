@@ -85,13 +85,25 @@ def test_update_rejects_bad_arguments_before_launch(L):
     assert upd(b, seg, api.Params(tau_num=1).c(), 1 << 40) == -5          # tau must exceed 1
     assert upd(b, seg, api.Params(tau_num=2, tau_log2_den=1).c(), 1 << 40) == -5
     assert upd(b, seg, api.Params(delta_q=0).c(), 1 << 40) == -5
-    assert upd(b, seg, api.Params(flags=0x20).c(), 1 << 40) == -1          # unknown policy bits
+    assert upd(b, seg, api.Params(flags=0x40).c(), 1 << 40) == -1          # unknown policy bits
     assert upd(b, seg, api.Params(flags=0x80000000).c(), 1 << 40) == -1
     both = api.POLICY_DENSEST_ONLY | api.POLICY_SOURCE_FILL
     assert upd(b, seg, api.Params(flags=both).c(), 1 << 40) == -1          # exclusive eviction policies
     kv = api.Params(flags=api.POLICY_KV_DESCRIPTOR).c()
     assert upd(_bank(api, dtype=1), seg, kv, 1 << 40) == -3                 # [K; V] geometry: bf16 banks only
     assert upd(b, api.DkvSegment(100, 3, 1, None), kv, 1 << 40) == -1       # ... and needs the values
+    seq = api.POLICY_SEQUENTIAL
+    for other in (api.POLICY_DENSEST_ONLY, api.POLICY_SOURCE_FILL, api.POLICY_KV_DESCRIPTOR):
+        assert upd(b, seg, api.Params(flags=seq | other).c(), 1 << 40) == -1  # sequential combines with 0x1, 0x2 only
+    assert upd(_bank(api, dtype=1), seg, api.Params(flags=seq).c(), 1 << 40) == -3   # bf16 banks only
+    assert upd(_bank(api, num_banks=300, group_size=300), seg, api.Params(flags=seq).c(), 1 << 40) == -2
+    sz, szs = ctypes.c_size_t(), ctypes.c_size_t()
+    assert L.densitykv_workspace_size(ctypes.byref(b), 100, ctypes.byref(sz)) == 0
+    assert L.densitykv_workspace_size_policy(ctypes.byref(b), 100, 0, ctypes.byref(szs)) == 0
+    assert szs.value == sz.value
+    assert L.densitykv_workspace_size_policy(ctypes.byref(b), 100, seq, ctypes.byref(szs)) == 0
+    assert szs.value >= sz.value + 12 * (4680 + 100) ** 2 * 4               # the pairwise weights
+    assert upd(b, seg, api.Params(flags=seq).c(), sz.value) == -4           # default-size workspace is too small
     assert upd(b, api.DkvSegment(9000, 3, 1, 1), good, 1 << 40) == -2
     assert upd(b, api.DkvSegment(100, -1, 1, 1), good, 1 << 40) == -5
     assert upd(b, api.DkvSegment(100, 3, None, 1), good, 1 << 40) == -1

@@ -75,7 +75,8 @@ def _run_rollout(cfg, blocks, prm, budgets=None, dup_every=0, trace=True, init_f
         new, recs = oracle_step(obanks, K, V, t, op, gs)
         if t % check_every == 0 or t == blocks - 1:
             if trace:
-                assert_trace_equal(out, recs, gs, obanks, n, ctx=f"block {t}")
+                assert_trace_equal(out, recs, gs, obanks, n, ctx=f"block {t}",
+                                   sequential=bool(prm.flags & api.POLICY_SEQUENTIAL))
             for b in range(B):
                 assert_bank_equal(bank, b, new[b], ctx=f"block {t}", kv=bool(prm.flags & api.POLICY_KV_DESCRIPTOR))
         obanks = new
@@ -162,6 +163,74 @@ def test_rollout_kv_descriptor(dt, d):
     cfg = synth.Config(heads=6, d=d, dtype=dt, n_cand=200, budget=300, group_size=3, **SMALL)
     _run_rollout(cfg, 6, api.Params(sigma2_log2=5 if d == 64 else 6, flags=api.POLICY_KV_DESCRIPTOR), dup_every=2,
                  grid_values=True)
+
+
+@pytest.mark.parametrize("dt,d,tau", [("bf16", 128, 3), ("bf16", 64, 3), ("bf16", 128, 2)])
+def test_rollout_sequential_competition(dt, d, tau):
+    """Within-block sequential competition (DKV_POLICY_SEQUENTIAL): 6 banks in 2
+    groups of 3, budget 300, 200 candidates per block with near-duplicate blocks;
+    the first block fills the empty banks (empty-bank rule), then every step of
+    every block is decided on the device.  Order, scores, steps taken, admitted and
+    released lists, and the committed banks (layout, K/V, rho, base, knorm) are
+    bit-exact against the oracle."""
+    _log(f"rollout sequential dt={dt} d={d} tau={tau}")
+    cfg = synth.Config(heads=6, d=d, dtype=dt, n_cand=200, budget=300, group_size=3, **SMALL)
+    prm = api.Params(sigma2_log2=4 if d == 64 else 5, tau_num=tau, flags=api.POLICY_SEQUENTIAL)
+    _run_rollout(cfg, 5, prm, dup_every=2)
+
+
+def test_sequential_violators_and_rejected_steps():
+    """Sequential competition with exact duplicates of bank keys among sparse grid
+    keys (sigma^2 = 4, d = 128), on two bank sets that both start empty.  Score
+    order fills the banks and then takes steps that release a violator; source
+    order on a bank that is not full rejects the steps whose candidate makes a
+    state violate.  Every block bit-exact against the oracle, which must see both
+    kinds of steps."""
+    _log("sequential violators and rejected steps")
+    B, gs, d, M = 3, 3, 128, 300
+    taken_with_violator = rejected = 0
+    for schedule in ([0, 0, 0], [0, api.POLICY_SOURCE_ORDER]):
+        rng = np.random.default_rng(5)
+        bank = api.Bank(B, M, d, dtype=torch.bfloat16, group_size=gs)
+        obanks = [BankState.empty(M, d) for _ in range(B)]
+        for t, flags in enumerate(schedule):
+            prm = api.Params(sigma2_log2=2, flags=api.POLICY_SEQUENTIAL | flags)
+            if t == 0:
+                # 230 keys and exact copies of the first 20 of them
+                K = np.stack([np.concatenate([k, k[:20]])
+                              for k in (synth.random_grid_keys(rng, (230, d)) for _ in range(B))])
+            else:
+                # 100 copies of bank keys and 100 fresh keys, shuffled
+                K = np.stack([np.concatenate([obanks[h].K[rng.choice(obanks[h].m, 100, replace=False)].astype(np.float32),
+                                              synth.random_grid_keys(rng, (100, d))]) for h in range(B)])
+                for h in range(B):
+                    rng.shuffle(K[h])
+            V = synth.random_grid_keys(rng, K.shape)
+            n = K.shape[1]
+            out = api.UpdateOut(bank, n, trace=True)
+            api.update_bank(bank, dev(K, "bf16"), dev(V, "bf16"), t, prm, out=out)
+            torch.cuda.synchronize()
+            new, recs = oracle_step(obanks, K, V, t, oracle_params(prm), gs)
+            ctx = f"schedule {schedule} block {t}"
+            assert_trace_equal(out, recs, gs, obanks, n, ctx=ctx, sequential=True)
+            for b in range(B):
+                assert_bank_equal(bank, b, new[b], ctx=ctx)
+            if t > 0:
+                rec = recs[0]
+                rejected += int((~rec.steps).sum())
+                taken_with_violator += sum(int(((hr.c > 0) & rec.steps).sum()) for hr in rec.heads)
+            obanks = new
+    assert rejected > 0 and taken_with_violator > 0
+
+
+def test_rollout_sequential_with_source_order_and_refresh():
+    """The sequential competition combined with source-order candidates and
+    refreshed baselines (the combinations it admits), independent heads."""
+    _log("rollout sequential + source order + refresh")
+    cfg = synth.Config(heads=4, d=128, dtype="bf16", n_cand=150, budget=250, group_size=1, **SMALL)
+    prm = api.Params(sigma2_log2=5, tau_num=3,
+                     flags=api.POLICY_SEQUENTIAL | api.POLICY_SOURCE_ORDER | api.POLICY_REFRESH_BASE)
+    _run_rollout(cfg, 4, prm, dup_every=2)
 
 
 def test_kv_descriptor_score_and_density():
