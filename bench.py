@@ -36,9 +36,10 @@ ATTN_SOURCE = os.path.join(ROOT, "paper_2608_27922_amd", "csrc", "dkv_attention.
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_attn_mfma_single_layer_traffic.md")
 # dkv_params.flags of each policy ablation (Table 1(b); independent per-head = group size 1)
 # (kv_descriptor: the [K; V] retention geometry; the workload's values are not on the key grid, so
-# this mode is a timing run only, its decisions carry the fp32 rounding of the descriptor Gram)
+# this mode is a timing run only, its decisions carry the fp32 rounding of the descriptor Gram;
+# sequential: the within-block competition of Supp. E, one candidate per step, one workgroup per group)
 POLICIES = {"default": 0, "source_order": 0x1, "refresh_base": 0x2, "densest_only": 0x4, "source_fill": 0x8,
-            "kv_descriptor": 0x10}
+            "kv_descriptor": 0x10, "sequential": 0x20}
 
 
 def parse():
@@ -225,7 +226,7 @@ def main():
     init_k, init_v = to(case["init_K"]), to(case["init_V"])
     seg_k, seg_v = to(case["seg_K"]), to(case["seg_V"])
     q, wk, wv = to(case["q"]), to(case["win_K"]), to(case["win_V"])
-    ws = api.alloc_workspace(bank, max(N, cfg.budget))
+    ws = api.alloc_workspace(bank, max(N, cfg.budget), run_prm.flags)
     api.update_bank(bank, init_k, init_v, 0, prm, workspace=ws)   # starts full (empty-bank rule)
     torch.cuda.synchronize()
     snap = bank.snapshot()
