@@ -59,11 +59,14 @@ struct Workspace {
   uint32_t *gram;      // [B, L, L] W between the items [slots 0..Mcap); candidates 0..N)], L = Mcap + N
   int32_t *grow;       // [B, Mcap] item of the state in each slot (slot s, or Mcap + candidate)
   int64_t *lim;        // [B, Mcap] ceil(T b / 2^k): the state violates when rho + W reaches it
+  uint64_t *seq_rec;   // [G, 2, kSeqMaxMembers, 8] per-step records of the workgroups of a group
+  uint32_t *seq_arrive;  // [G] records posted so far by the group's workgroups
   int gram_ld;         // L
 };
 
 size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base, bool seq = false);
 constexpr int kSeqMaxGroup = 256;  // banks per group in the sequential competition
+constexpr int kSeqMaxMembers = 64;  // workgroups per group in the multi-workgroup walk
 
 // Geometry and parameters passed by value to every kernel.
 struct Geom {

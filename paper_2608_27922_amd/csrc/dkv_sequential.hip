@@ -129,11 +129,97 @@ __device__ __forceinline__ int64_t wave_sum_i64(int64_t v) {
   return v;
 }
 
+__device__ __forceinline__ int64_t lim_of(int64_t base, const Prm &p) {
+  return ((int64_t)p.tau_num * base + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
+}
+
+// Set-up of bank b by one wave: per-slot items and limits of a bank that holds
+// states; a bank that is empty takes the empty-bank rule (the first min(N, M)
+// candidates in source order, densities over that bank; Alg. 1, first branch).
+// Returns the occupancy the steps start from.
+__device__ int seq_setup_bank(const dkv_bank &bank, const Geom &g, const Prm &p, const Workspace &ws, int b, int l) {
+  const int L = ws.gram_ld, Mcap = g.Mcap, N = g.N;
+  const size_t rb = (size_t)b * Mcap;
+  const int m0 = ws.m[b];
+  if (m0 > 0) {
+    for (int s = l; s < m0; s += 64) {
+      ws.grow[rb + s] = s;
+      ws.lim[rb + s] = lim_of(bank.base[rb + s], p);
+    }
+    return m0;
+  }
+  const int na = min(N, ws.M[b]);
+  for (int x = 0; x < na; ++x) {
+    const uint32_t *wr = ws.gram + ((size_t)b * L + Mcap + x) * L + Mcap;
+    int64_t acc = 0;
+    for (int y = l; y < na; y += 64)
+      if (y != x) acc += wr[y];
+    acc = wave_sum_i64(acc);
+    if (l == (x & 63)) {
+      bank.rho[rb + x] = acc;
+      const int64_t bs = acc > p.delta_q ? acc : p.delta_q;
+      bank.base[rb + x] = bs;
+      ws.lim[rb + x] = lim_of(bs, p);
+      ws.grow[rb + x] = Mcap + x;
+      bank.prov[rb + x] = ((int64_t)p.block_id << 32) | (int64_t)x;
+      bank.knorm[rb + x] = ws.cnorm[(size_t)b * N + x];
+    }
+  }
+  return na;
+}
+
+// Results of bank b by one wave, from its final occupancy m and the occupancy
+// m0 it held before the update: refreshed baselines, the admitted candidates
+// (ascending source index) and the pre-update slots whose state left.
+__device__ void seq_results_bank(const dkv_bank &bank, const Geom &g, const Prm &p, const Workspace &ws,
+                                 const dkv_update_out &out, int b, int l, int m, int m0) {
+  const int Mcap = g.Mcap, N = g.N;
+  const size_t rb = (size_t)b * Mcap, nb = (size_t)b * N;
+  if (l == 0) bank.occupancy[b] = m;
+  if (p.flags & DKV_POLICY_REFRESH_BASE)
+    for (int s = l; s < m; s += 64) {
+      const int64_t r = bank.rho[rb + s];
+      bank.base[rb + s] = r > p.delta_q ? r : p.delta_q;
+    }
+  for (int x = l; x < N; x += 64) ws.rank[nb + x] = 0;
+  __threadfence_block();
+  for (int s = l; s < m; s += 64) {
+    const int gsl = ws.grow[rb + s];
+    if (gsl >= Mcap) ws.rank[nb + (gsl - Mcap)] = 1;
+  }
+  __threadfence_block();
+  int na = 0;
+  for (int x0 = 0; x0 < N; x0 += 64) {
+    const int x = x0 + l;
+    const bool in = x < N && ws.rank[nb + x] != 0;
+    const unsigned long long bal = __ballot(in);
+    if (in && out.admitted) out.admitted[nb + na + __popcll(bal & ((1ull << l) - 1))] = x;
+    na += __popcll(bal);
+  }
+  if (out.admitted)
+    for (int x = na + l; x < N; x += 64) out.admitted[nb + x] = -1;
+  int nv = 0;
+  for (int s0 = 0; s0 < m0; s0 += 64) {
+    const int s = s0 + l;
+    const bool gone = s < m0 && ws.grow[rb + s] != s;
+    const unsigned long long bal = __ballot(gone);
+    if (gone && out.evicted) out.evicted[rb + nv + __popcll(bal & ((1ull << l) - 1))] = s;
+    nv += __popcll(bal);
+  }
+  if (out.evicted)
+    for (int s = nv + l; s < Mcap; s += 64) out.evicted[rb + s] = -1;
+  if (l == 0) {
+    if (out.n_admitted) out.n_admitted[b] = na;
+    if (out.n_evicted) out.n_evicted[b] = nv;
+  }
+}
+
 // ---------------------------------------------------------------------------
-// k_seq: the steps of one group.  Per bank, a slot's state lives in the bank
-// arrays (rho, base, prov, knorm) and in ws.grow / ws.lim; every slot is read
-// and written by the same lane (slot % 64) of the bank's wave, and a wave
-// fences its memory operations at the end of each step.
+// k_seq: the steps of one group in one workgroup (any bank size).  Per bank, a
+// slot's state lives in the bank arrays (rho, base, prov, knorm) and in
+// ws.grow / ws.lim; every slot is read and written by the same lane
+// (slot % 64) of the bank's wave, and a wave fences its memory operations at
+// the end of each step.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64 * kSeqWaves) void k_seq(dkv_bank bank, Geom g, Prm p, Workspace ws,
                                                        dkv_update_out out) {
@@ -147,40 +233,14 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq(dkv_bank bank, Geom g, P
   int steps_taken = 0;
   if (threadIdx.x == 0) any_live = 0;
   __syncthreads();
-  // ---- set-up: per-slot items and limits; empty banks take the empty-bank rule
   for (int hh = wave; hh < g.gs; hh += nw) {
     const int b = grp * g.gs + hh;
-    const size_t rb = (size_t)b * Mcap;
     const int m0 = ws.m[b];
-    const int M = ws.M[b];
-    if (l == 0) m0s[hh] = m0;
-    if (m0 > 0 && l == 0) any_live = 1;
-    if (m0 > 0) {
-      for (int s = l; s < m0; s += 64) {
-        ws.grow[rb + s] = s;
-        ws.lim[rb + s] = ((int64_t)p.tau_num * bank.base[rb + s] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
-      }
-      if (l == 0) mcur[hh] = m0;
-    } else {
-      // the first min(N, M) candidates in source order, densities over that bank (Alg. 1, first branch)
-      const int na = min(N, M);
-      for (int x = 0; x < na; ++x) {
-        const uint32_t *wr = ws.gram + ((size_t)b * L + Mcap + x) * L + Mcap;
-        int64_t acc = 0;
-        for (int y = l; y < na; y += 64)
-          if (y != x) acc += wr[y];
-        acc = wave_sum_i64(acc);
-        if (l == (x & 63)) {
-          bank.rho[rb + x] = acc;
-          const int64_t bs = acc > p.delta_q ? acc : p.delta_q;
-          bank.base[rb + x] = bs;
-          ws.lim[rb + x] = ((int64_t)p.tau_num * bs + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
-          ws.grow[rb + x] = Mcap + x;
-          bank.prov[rb + x] = ((int64_t)p.block_id << 32) | (int64_t)x;
-          bank.knorm[rb + x] = ws.cnorm[(size_t)b * N + x];
-        }
-      }
-      if (l == 0) mcur[hh] = na;
+    const int mc = seq_setup_bank(bank, g, p, ws, b, l);
+    if (l == 0) {
+      m0s[hh] = m0;
+      mcur[hh] = mc;
+      if (m0 > 0) any_live = 1;
     }
   }
   __threadfence_block();
@@ -248,7 +308,7 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq(dkv_bank bank, Geom g, P
         bank.rho[rb + t] = sum;
         const int64_t bs = sum > p.delta_q ? sum : p.delta_q;
         bank.base[rb + t] = bs;
-        ws.lim[rb + t] = ((int64_t)p.tau_num * bs + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
+        ws.lim[rb + t] = lim_of(bs, p);
         ws.grow[rb + t] = Mcap + x;
         bank.prov[rb + t] = ((int64_t)p.block_id << 32) | (int64_t)x;
         bank.knorm[rb + t] = ws.cnorm[(size_t)b * N + x];
@@ -257,51 +317,293 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq(dkv_bank bank, Geom g, P
     }
     __threadfence_block();
   }
-  // ---- results
   if (threadIdx.x == 0 && out.r_star) out.r_star[grp] = steps_taken;
+  for (int hh = wave; hh < g.gs; hh += nw)
+    seq_results_bank(bank, g, p, ws, out, grp * g.gs + hh, l, mcur[hh], m0s[hh]);
+}
+
+// ---------------------------------------------------------------------------
+// Multi-workgroup walk.  Workgroup (b, q) of a bank holds the slots
+// q * kCoopSlots + k * 256 + thread (k < kCoopS) in registers: rho, limit,
+// item and provenance.  Per step every workgroup posts one record (its
+// violator count, its first violator, its densest state and the sum of its
+// weights to the candidate) to global memory and advances the group's
+// counter with release semantics at device scope; wave 0 of every workgroup
+// waits for the counter, reads the group's records and takes the shared
+// decision.  The weights to the next candidate are gathered while the
+// records are exchanged.  Launched cooperatively, so all workgroups of the
+// grid are resident together and every wait ends; a wait that still exceeds
+// kSpinCap polls ends the walk with r_star = -1.
+// ---------------------------------------------------------------------------
+constexpr int kCoopS = 8;
+constexpr int kCoopSlots = 256 * kCoopS;
+constexpr int kSpinCap = 1 << 22;
+
+// record words: 0 cnt | e << 32, 1 vmin | W(vmin) << 32, 2 item(vmin) | best slot << 32,
+// 3 W(best) | item(best) << 32, 4 best rt, 5 best prov, 6 sum of W
+struct Rec {
+  int cnt, e, vmin, best_slot;
+  uint32_t wv, gv, wb, gb;
+  int64_t rt, prov, total;
+};
+__device__ __forceinline__ void rec_merge(Rec &a, const Rec &o) {
+  a.cnt += o.cnt;
+  a.total += o.total;
+  if (o.vmin < a.vmin) {
+    a.vmin = o.vmin;
+    a.wv = o.wv;
+    a.gv = o.gv;
+  }
+  if (better(Best{o.rt, o.prov, o.best_slot}, Best{a.rt, a.prov, a.best_slot})) {
+    a.rt = o.rt;
+    a.prov = o.prov;
+    a.best_slot = o.best_slot;
+    a.wb = o.wb;
+    a.gb = o.gb;
+  }
+}
+__device__ __forceinline__ Rec rec_shfl(const Rec &r, int src) {
+  auto sh64 = [&](int64_t v) {
+    const uint32_t lo = __shfl((uint32_t)v, src, 64), hi = __shfl((uint32_t)((uint64_t)v >> 32), src, 64);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+  };
+  Rec o;
+  o.cnt = __shfl(r.cnt, src, 64);
+  o.e = __shfl(r.e, src, 64);
+  o.vmin = __shfl(r.vmin, src, 64);
+  o.best_slot = __shfl(r.best_slot, src, 64);
+  o.wv = __shfl(r.wv, src, 64);
+  o.gv = __shfl(r.gv, src, 64);
+  o.wb = __shfl(r.wb, src, 64);
+  o.gb = __shfl(r.gb, src, 64);
+  o.rt = sh64(r.rt);
+  o.prov = sh64(r.prov);
+  o.total = sh64(r.total);
+  return o;
+}
+__device__ __forceinline__ Rec rec_wave(Rec r, int l) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) rec_merge(r, rec_shfl(r, l ^ o));
+  return r;
+}
+
+__global__ __launch_bounds__(64 * kSeqWaves) void k_seq_setup(dkv_bank bank, Geom g, Prm p, Workspace ws) {
+  const int grp = blockIdx.x, nw = blockDim.x >> 6;
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   for (int hh = wave; hh < g.gs; hh += nw) {
     const int b = grp * g.gs + hh;
-    const size_t rb = (size_t)b * Mcap, nb = (size_t)b * N;
-    const int m = mcur[hh], m0 = m0s[hh];
-    if (l == 0) bank.occupancy[b] = m;
-    if (p.flags & DKV_POLICY_REFRESH_BASE)
-      for (int s = l; s < m; s += 64) {
-        const int64_t r = bank.rho[rb + s];
-        bank.base[rb + s] = r > p.delta_q ? r : p.delta_q;
-      }
-    // this block's candidates in the final bank, ascending source index
-    for (int x = l; x < N; x += 64) ws.rank[nb + x] = 0;
-    __threadfence_block();
-    for (int s = l; s < m; s += 64) {
-      const int gsl = ws.grow[rb + s];
-      if (gsl >= Mcap) ws.rank[nb + (gsl - Mcap)] = 1;
-    }
-    __threadfence_block();
-    int na = 0;
-    for (int x0 = 0; x0 < N; x0 += 64) {
-      const int x = x0 + l;
-      const bool in = x < N && ws.rank[nb + x] != 0;
-      const unsigned long long bal = __ballot(in);
-      if (in && out.admitted) out.admitted[nb + na + __popcll(bal & ((1ull << l) - 1))] = x;
-      na += __popcll(bal);
-    }
-    if (out.admitted)
-      for (int x = na + l; x < N; x += 64) out.admitted[nb + x] = -1;
-    // pre-update slots whose state left, ascending
-    int nv = 0;
-    for (int s0 = 0; s0 < m0; s0 += 64) {
-      const int s = s0 + l;
-      const bool gone = s < m0 && ws.grow[rb + s] != s;
-      const unsigned long long bal = __ballot(gone);
-      if (gone && out.evicted) out.evicted[rb + nv + __popcll(bal & ((1ull << l) - 1))] = s;
-      nv += __popcll(bal);
-    }
-    if (out.evicted)
-      for (int s = nv + l; s < Mcap; s += 64) out.evicted[rb + s] = -1;
+    const int mc = seq_setup_bank(bank, g, p, ws, b, l);
     if (l == 0) {
-      if (out.n_admitted) out.n_admitted[b] = na;
-      if (out.n_evicted) out.n_evicted[b] = nv;
+      ws.m_new[b] = mc;
+      ws.n_ev[b] = 0;  // set to 1 by a workgroup of the bank whose walk timed out
     }
+  }
+  if (threadIdx.x == 0) {
+    ws.seq_arrive[grp] = 0;
+    ws.r_star[grp] = 0;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_seq_coop(dkv_bank bank, Geom g, Prm p, Workspace ws, int P) {
+  const int b = blockIdx.x / P, q = blockIdx.x % P;
+  const int grp = b / g.gs, hh = b % g.gs;
+  const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63;
+  const int L = ws.gram_ld, Mcap = g.Mcap, N = g.N;
+  if (ws.m[b] == 0) return;  // empty at the start: the empty-bank rule, outside the walk
+  __shared__ Rec red[4];
+  __shared__ int dec_admit, dec_ev, dec_gev, dec_stop;
+  __shared__ int64_t dec_sum;
+  const size_t rb = (size_t)b * Mcap, nb = (size_t)b * N;
+  const int s0 = q * kCoopSlots;
+  const int nmem = g.gs * P;
+  int nlive = 0;
+  for (int h2 = 0; h2 < g.gs; ++h2) nlive += ws.m[grp * g.gs + h2] > 0 ? 1 : 0;
+  const uint32_t per_step = (uint32_t)(nlive * P);
+  // wave 0, lane l reads the record of member l = (head l / P, part l % P)
+  const bool lane_live = l < nmem && ws.m[grp * g.gs + l / P] > 0;
+  int m = ws.m_new[b];
+  const int M = ws.M[b];
+  const uint32_t *gb = ws.gram + (size_t)b * L * L;
+  int64_t rho[kCoopS], lim[kCoopS], prov[kCoopS];
+  int item[kCoopS];
+  uint32_t wn[kCoopS];
+#pragma unroll
+  for (int k = 0; k < kCoopS; ++k) {
+    const int s = s0 + k * 256 + tid;
+    const bool lv = s < m;
+    rho[k] = lv ? bank.rho[rb + s] : 0;
+    lim[k] = lv ? ws.lim[rb + s] : 0;
+    prov[k] = lv ? bank.prov[rb + s] : 0;
+    item[k] = lv ? ws.grow[rb + s] : 0;
+  }
+  {
+    const uint32_t *row = gb + (size_t)(Mcap + ws.order[nb]) * L;
+#pragma unroll
+    for (int k = 0; k < kCoopS; ++k) wn[k] = s0 + k * 256 + tid < m ? row[item[k]] : 0u;
+  }
+  int steps_taken = 0, stop = 0;
+  uint64_t *recs = ws.seq_rec + (size_t)grp * 2 * kSeqMaxMembers * 8;
+  for (int j = 0; j < N && !stop; ++j) {
+    const int x = ws.order[nb + j];
+    uint32_t wx[kCoopS];
+    // ---- test of this workgroup's slots against candidate x
+    Rec r{0, m + 1 > M ? 1 : 0, INT_MAX, INT_MAX, 0u, 0u, 0u, 0u, INT64_MIN, INT64_MAX, 0};
+#pragma unroll
+    for (int k = 0; k < kCoopS; ++k) {
+      wx[k] = wn[k];
+      const int s = s0 + k * 256 + tid;
+      if (s < m) {
+        const int64_t rt = rho[k] + (int64_t)wx[k];
+        if (rt >= lim[k]) {
+          ++r.cnt;
+          if (s < r.vmin) {
+            r.vmin = s;
+            r.wv = wx[k];
+            r.gv = (uint32_t)item[k];
+          }
+        }
+        if (better(Best{rt, prov[k], s}, Best{r.rt, r.prov, r.best_slot})) {
+          r.rt = rt;
+          r.prov = prov[k];
+          r.best_slot = s;
+          r.wb = wx[k];
+          r.gb = (uint32_t)item[k];
+        }
+        r.total += wx[k];
+      }
+    }
+    r = rec_wave(r, l);
+    if (l == 0) red[wave] = r;
+    __syncthreads();
+    if (tid == 0) {
+      Rec w = red[0];
+#pragma unroll
+      for (int v = 1; v < 4; ++v) rec_merge(w, red[v]);
+      uint64_t *dst = recs + ((size_t)(j & 1) * kSeqMaxMembers + hh * P + q) * 8;
+      dst[0] = (uint32_t)w.cnt | ((uint64_t)(uint32_t)w.e << 32);
+      dst[1] = (uint32_t)w.vmin | ((uint64_t)w.wv << 32);
+      dst[2] = w.gv | ((uint64_t)(uint32_t)w.best_slot << 32);
+      dst[3] = w.wb | ((uint64_t)w.gb << 32);
+      dst[4] = (uint64_t)w.rt;
+      dst[5] = (uint64_t)w.prov;
+      dst[6] = (uint64_t)w.total;
+      __hip_atomic_fetch_add(ws.seq_arrive + grp, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    // ---- gather the weights to the next candidate while the records travel
+    if (j + 1 < N) {
+      const uint32_t *row = gb + (size_t)(Mcap + ws.order[nb + j + 1]) * L;
+#pragma unroll
+      for (int k = 0; k < kCoopS; ++k) wn[k] = s0 + k * 256 + tid < m ? row[item[k]] : 0u;
+    }
+    if (wave == 0) {
+      const uint32_t target = (uint32_t)(j + 1) * per_step;
+      int polls = 0;
+      while (__hip_atomic_load(ws.seq_arrive + grp, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target &&
+             polls < kSpinCap) {
+        __builtin_amdgcn_s_sleep(1);
+        ++polls;
+      }
+      const int timed_out = polls >= kSpinCap;
+      Rec o{0, 0, INT_MAX, INT_MAX, 0u, 0u, 0u, 0u, INT64_MIN, INT64_MAX, 0};
+      if (lane_live && !timed_out) {
+        const uint64_t *src = recs + ((size_t)(j & 1) * kSeqMaxMembers + l) * 8;
+        const uint64_t w0 = src[0], w1 = src[1], w2 = src[2], w3 = src[3];
+        o.cnt = (int)(uint32_t)w0;
+        o.e = (int)(uint32_t)(w0 >> 32);
+        o.vmin = (int)(uint32_t)w1;
+        o.wv = (uint32_t)(w1 >> 32);
+        o.gv = (uint32_t)w2;
+        o.best_slot = (int)(uint32_t)(w2 >> 32);
+        o.wb = (uint32_t)w3;
+        o.gb = (uint32_t)(w3 >> 32);
+        o.rt = (int64_t)src[4];
+        o.prov = (int64_t)src[5];
+        o.total = (int64_t)src[6];
+      }
+      // merge the parts of each bank into its first part's lane
+      for (int i = 1; i < P; ++i) {
+        const Rec v = rec_shfl(o, l + i < 64 ? l + i : l);
+        if (l % P == 0 && l + i < nmem) rec_merge(o, v);
+      }
+      const bool lead = l % P == 0 && lane_live;
+      const unsigned long long bad = __ballot(lead && o.cnt > o.e);
+      const Rec own = rec_shfl(o, hh * P);
+      if (l == 0) {
+        const int admit = bad == 0ull ? 1 : 0;
+        const int ev = own.cnt > 0 ? own.vmin : (own.e ? own.best_slot : -1);
+        dec_admit = admit;
+        dec_ev = ev;
+        dec_gev = (int)(own.cnt > 0 ? own.gv : own.gb);
+        dec_sum = own.total - (ev >= 0 ? (int64_t)(own.cnt > 0 ? own.wv : own.wb) : 0);
+        dec_stop = timed_out;
+      }
+    }
+    __syncthreads();
+    stop = dec_stop;
+    if (stop || !dec_admit) continue;
+    ++steps_taken;
+    const int ev = dec_ev;
+    if (ev >= 0) {
+      const uint32_t *row = gb + (size_t)dec_gev * L;
+#pragma unroll
+      for (int k = 0; k < kCoopS; ++k) {
+        const int s = s0 + k * 256 + tid;
+        if (s < m && s != ev) rho[k] += (int64_t)wx[k] - (int64_t)row[item[k]];
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < kCoopS; ++k)
+        if (s0 + k * 256 + tid < m) rho[k] += (int64_t)wx[k];
+    }
+    const int t = ev >= 0 ? ev : m;
+    const int tl = t - s0;
+    if (tl >= 0 && tl < kCoopSlots && (tl & 255) == tid) {
+      const int kt = tl >> 8;
+      const int64_t sum = dec_sum;
+      const int64_t bs = sum > p.delta_q ? sum : p.delta_q;
+      const uint32_t wnew = j + 1 < N ? gb[(size_t)(Mcap + ws.order[nb + j + 1]) * L + Mcap + x] : 0u;
+#pragma unroll
+      for (int k = 0; k < kCoopS; ++k)
+        if (k == kt) {
+          rho[k] = sum;
+          lim[k] = lim_of(bs, p);
+          item[k] = Mcap + x;
+          prov[k] = ((int64_t)p.block_id << 32) | (int64_t)x;
+          wn[k] = wnew;
+        }
+      bank.base[rb + t] = bs;
+      bank.prov[rb + t] = ((int64_t)p.block_id << 32) | (int64_t)x;
+      bank.knorm[rb + t] = ws.cnorm[nb + x];
+    }
+    if (ev < 0) ++m;
+  }
+#pragma unroll
+  for (int k = 0; k < kCoopS; ++k) {
+    const int s = s0 + k * 256 + tid;
+    if (s < m) {
+      bank.rho[rb + s] = rho[k];
+      ws.grow[rb + s] = item[k];
+    }
+  }
+  if (tid == 0 && stop) ws.n_ev[b] = 1;
+  if (q == 0 && tid == 0) {
+    ws.m_new[b] = m;
+    atomicMax(ws.r_star + grp, steps_taken);  // equal in every workgroup of the group
+  }
+}
+
+__global__ __launch_bounds__(64 * kSeqWaves) void k_seq_results(dkv_bank bank, Geom g, Prm p, Workspace ws,
+                                                               dkv_update_out out) {
+  const int grp = blockIdx.x, nw = blockDim.x >> 6;
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
+  if (threadIdx.x == 0 && out.r_star) {
+    int timed_out = 0;
+    for (int h2 = 0; h2 < g.gs; ++h2) timed_out |= ws.n_ev[grp * g.gs + h2];
+    out.r_star[grp] = timed_out ? -1 : ws.r_star[grp];
+  }
+  for (int hh = wave; hh < g.gs; hh += nw) {
+    const int b = grp * g.gs + hh;
+    seq_results_bank(bank, g, p, ws, out, b, l, ws.m_new[b], ws.m[b]);
   }
 }
 
@@ -329,6 +631,17 @@ __global__ __launch_bounds__(256) void k_seq_commit(dkv_bank bank, dkv_segment s
   reinterpret_cast<u32x4 *>(dst)[cc] = reinterpret_cast<const u32x4 *>(src)[cc];
 }
 
+// Whether a cooperative launch of nblocks k_seq_coop workgroups fits the
+// current device (all of them resident at once).
+bool coop_fits(int nblocks) {
+  int dev = 0, coop = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess || !coop) return false;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return false;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_seq_coop, 256, 0) != hipSuccess) return false;
+  return (long)per_cu * cus >= nblocks;
+}
+
 template <int D>
 hipError_t seq_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                     const dkv_update_out &out, const Workspace &ws, hipStream_t s) {
@@ -338,7 +651,21 @@ hipError_t seq_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g,
     k_seq_gram<D><<<grid, 256, 0, s>>>(bank, seg, g, p, ws);
   }
   const int waves = g.gs < kSeqWaves ? g.gs : kSeqWaves;
-  k_seq<<<g.G, 64 * waves, 0, s>>>(bank, g, p, ws, out);
+  int P = (g.Mcap + kCoopSlots - 1) / kCoopSlots;
+  if (g.N > 0 && g.gs * P <= kSeqMaxMembers && coop_fits(g.B * P)) {
+    k_seq_setup<<<g.G, 64 * waves, 0, s>>>(bank, g, p, ws);
+    dkv_bank a_bank = bank;
+    Geom a_g = g;
+    Prm a_p = p;
+    Workspace a_ws = ws;
+    void *args[] = {&a_bank, &a_g, &a_p, &a_ws, &P};
+    const hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k_seq_coop),
+                                                    dim3((unsigned)(g.B * P)), dim3(256), args, 0, s);
+    if (e != hipSuccess) return e;
+    k_seq_results<<<g.G, 64 * waves, 0, s>>>(bank, g, p, ws, out);
+  } else {
+    k_seq<<<g.G, 64 * waves, 0, s>>>(bank, g, p, ws, out);
+  }
   if (g.N > 0) {
     constexpr int kSlots = 256 / (2 * (D / 8));
     k_seq_commit<D><<<dim3((unsigned)((g.Mcap + kSlots - 1) / kSlots), (unsigned)g.B), 256, 0, s>>>(bank, seg, g,

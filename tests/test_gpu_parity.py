@@ -179,6 +179,60 @@ def test_rollout_sequential_competition(dt, d, tau):
     _run_rollout(cfg, 5, prm, dup_every=2)
 
 
+def test_sequential_banks_spanning_workgroups():
+    """Sequential competition on banks of 2,500-2,600 slots (ragged budgets 2,600 /
+    2,500 / 2,560): each bank's slots span two workgroups of the multi-workgroup
+    walk, so every step merges the records of six workgroups.  The first block
+    fills the banks from empty with 2,300 keys and exact copies of 200 of them
+    (sigma^2 = 1/2, d = 128); then 100 copies of bank keys and 100 fresh keys per
+    block, in source order (rejected steps on banks that are not full) and in
+    score order (steps that release a violator).  Every block bit-exact against
+    the oracle, which must see both kinds of steps."""
+    _log("sequential banks spanning workgroups")
+    rng = np.random.default_rng(7)
+    budgets = np.array([2600, 2500, 2560], np.int32)
+    B, gs, d = 3, 3, 128
+    bank = api.Bank(B, int(budgets.max()), d, dtype=torch.bfloat16, group_size=gs,
+                    budget=torch.from_numpy(budgets))
+    obanks = [BankState.empty(int(M), d) for M in budgets]
+    taken_with_violator = rejected = 0
+    for t, flags in enumerate([0, api.POLICY_SOURCE_ORDER, 0]):
+        prm = api.Params(sigma2_log2=-1, flags=api.POLICY_SEQUENTIAL | flags)
+        if t == 0:
+            K = np.stack([np.concatenate([k, k[:200]])
+                          for k in (synth.random_grid_keys(rng, (2300, d)) for _ in range(B))])
+        else:
+            K = np.stack([np.concatenate([obanks[h].K[rng.choice(obanks[h].m, 100, replace=False)].astype(np.float32),
+                                          synth.random_grid_keys(rng, (100, d))]) for h in range(B)])
+            for h in range(B):
+                rng.shuffle(K[h])
+        V = synth.random_grid_keys(rng, K.shape)
+        n = K.shape[1]
+        out = api.UpdateOut(bank, n, trace=True)
+        api.update_bank(bank, dev(K, "bf16"), dev(V, "bf16"), t, prm, out=out)
+        torch.cuda.synchronize()
+        new, recs = oracle_step(obanks, K, V, t, oracle_params(prm), gs)
+        assert_trace_equal(out, recs, gs, obanks, n, ctx=f"block {t}", sequential=True)
+        for b in range(B):
+            assert_bank_equal(bank, b, new[b], ctx=f"block {t}")
+        if t > 0:
+            rec = recs[0]
+            rejected += int((~rec.steps).sum())
+            taken_with_violator += sum(int(((hr.c > 0) & rec.steps).sum()) for hr in rec.heads)
+        obanks = new
+    assert rejected > 0 and taken_with_violator > 0
+
+
+def test_sequential_wide_group():
+    """Sequential competition with 72 banks sharing each step (more banks than
+    the multi-workgroup walk takes, so one workgroup walks the group): budget 120,
+    80 candidates per block, near-duplicate blocks; bit-exact against the oracle."""
+    _log("sequential wide group")
+    cfg = synth.Config(heads=72, d=64, dtype="bf16", n_cand=80, budget=120, group_size=72, **SMALL)
+    prm = api.Params(sigma2_log2=4, tau_num=3, flags=api.POLICY_SEQUENTIAL)
+    _run_rollout(cfg, 4, prm, dup_every=2)
+
+
 def test_sequential_violators_and_rejected_steps():
     """Sequential competition with exact duplicates of bank keys among sparse grid
     keys (sigma^2 = 4, d = 128), on two bank sets that both start empty.  Score
