@@ -166,11 +166,17 @@ typedef struct {
  * SOURCE_ORDER and REFRESH_BASE only (DKV_ERR_INVALID otherwise); bf16 banks
  * only (DKV_ERR_UNSUPPORTED); group_size <= 256 (DKV_ERR_SHAPE).  The update
  * keeps the pairwise weights of [bank; candidates] in the workspace:
- * densitykv_workspace_size_policy adds num_banks * (capacity + n)^2 * 4 bytes.
+ * densitykv_workspace_size_policy adds num_banks * (capacity + n)^2 * 4 bytes
+ * (plus 12 bytes per slot and 8 KiB per group).
  * Outputs: r_star = steps taken, n_admitted / admitted = this block's
  * candidates in the final bank, n_evicted / evicted = pre-update slots whose
  * state left; first_cross and rho_tilde are not written.  The steps are
- * inherently sequential: one workgroup per group walks them in order. */
+ * inherently sequential: the workgroups that hold a group's banks exchange
+ * one record per step through the workspace (when all of them fit on the
+ * device at once; otherwise one workgroup walks the group).  r_star = -1
+ * reports a walk whose wait for those records exceeded its bound, leaving
+ * the group's banks undefined; with the launch guarantees in place this does
+ * not occur. */
 #define DKV_POLICY_SEQUENTIAL 0x20u
 
 /* Optional outputs of densitykv_update_bank (any pointer may be NULL).

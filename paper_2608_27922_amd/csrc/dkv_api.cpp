@@ -66,7 +66,6 @@ size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, cha
     w.grow = (int32_t *)take(Bz * Mz * 4);
     w.lim = (int64_t *)take(Bz * Mz * 8);
     w.seq_rec = (uint64_t *)take((size_t)G * 2 * kSeqMaxMembers * 8 * 8);
-    w.seq_arrive = (uint32_t *)take((size_t)G * 4);
     w.gram_ld = (int)L;
   }
   if (ws) *ws = w;

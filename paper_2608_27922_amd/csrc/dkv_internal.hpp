@@ -60,7 +60,6 @@ struct Workspace {
   int32_t *grow;       // [B, Mcap] item of the state in each slot (slot s, or Mcap + candidate)
   int64_t *lim;        // [B, Mcap] ceil(T b / 2^k): the state violates when rho + W reaches it
   uint64_t *seq_rec;   // [G, 2, kSeqMaxMembers, 8] per-step records of the workgroups of a group
-  uint32_t *seq_arrive;  // [G] records posted so far by the group's workgroups
   int gram_ld;         // L
 };
 

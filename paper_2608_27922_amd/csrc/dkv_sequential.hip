@@ -82,11 +82,14 @@ __global__ __launch_bounds__(256) void k_seq_gram(dkv_bank bank, dkv_segment seg
 #pragma unroll
   for (int q = 0; q < 16; ++q) ncm[q] = __shfl(nc, tile_col(q, h), 32);  // column item's norm (lane cm of this half)
   if (!live(ru)) return;
-  uint32_t *row = ws.gram + ((size_t)b * L + ru) * L;
+  // W is symmetric (the same products summed in the same order, and |a|^2 +
+  // |b|^2 commutes), so W(ru, u) is stored at [u][ru]: the 32 lanes of a half
+  // write 32 consecutive entries of one row.
+  uint32_t *col = ws.gram + (size_t)b * L * L + ru;
 #pragma unroll
   for (int q = 0; q < 16; ++q) {
     const int u = c0 + tile_col(q, h);
-    if (u < L && live(u)) row[u] = weight_q((nr + ncm[q]) - 2.0f * acc[q], p);
+    if (u < L && live(u)) col[(size_t)u * L] = weight_q((nr + ncm[q]) - 2.0f * acc[q], p);
   }
 }
 
@@ -324,19 +327,21 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq(dkv_bank bank, Geom g, P
 
 // ---------------------------------------------------------------------------
 // Multi-workgroup walk.  Workgroup (b, q) of a bank holds the slots
-// q * kCoopSlots + k * 256 + thread (k < kCoopS) in registers: rho, limit,
+// q * kCoopSlots + k * kCoopThreads + thread (k < kCoopS) in registers: rho, limit,
 // item and provenance.  Per step every workgroup posts one record (its
 // violator count, its first violator, its densest state and the sum of its
-// weights to the candidate) to global memory and advances the group's
-// counter with release semantics at device scope; wave 0 of every workgroup
-// waits for the counter, reads the group's records and takes the shared
-// decision.  The weights to the next candidate are gathered while the
-// records are exchanged.  Launched cooperatively, so all workgroups of the
-// grid are resident together and every wait ends; a wait that still exceeds
-// kSpinCap polls ends the walk with r_star = -1.
+// weights to the candidate) to global memory as step-tagged words; wave 0 of
+// every workgroup polls the group's records until they carry the step's tag
+// and takes the shared decision from them.  The weights to the next
+// candidate are gathered while the records are exchanged.  Launched
+// cooperatively, so all workgroups of the grid are resident together and
+// every wait ends; a wait that still exceeds kSpinCap polls ends the walk
+// with r_star = -1.
 // ---------------------------------------------------------------------------
-constexpr int kCoopS = 8;
-constexpr int kCoopSlots = 256 * kCoopS;
+constexpr int kCoopThreads = 256;  // threads of a workgroup of the walk
+constexpr int kCoopS = 8;          // slots per thread
+constexpr int kCoopWaves = kCoopThreads / 64;
+constexpr int kCoopSlots = kCoopThreads * kCoopS;
 constexpr int kSpinCap = 1 << 22;
 
 // record words: 0 cnt | e << 32, 1 vmin | W(vmin) << 32, 2 item(vmin) | best slot << 32,
@@ -387,6 +392,42 @@ __device__ __forceinline__ Rec rec_wave(Rec r, int l) {
   return r;
 }
 
+// A record travels as kRecWords 64-bit words, each with a 48-bit payload and
+// the step tag j + 1 in its top 16 bits (N < 2^13): counts, slots (< 2^15,
+// 0xFFFF for none) and items (< 2^16) in 16 bits, weights (<= 2^23) in 24,
+// densities (< 2^39) in 48, the provenance in two 32-bit halves.  Each word
+// is stored and loaded as one relaxed device-scope atomic, so a reader that
+// sees the tag in every word has the whole record of that step.
+constexpr int kRecWords = 7;
+constexpr uint64_t kPayload = (1ull << 48) - 1;
+__device__ __forceinline__ uint64_t slot16(int s) { return s == INT_MAX ? 0xFFFFull : (uint64_t)s; }
+__device__ __forceinline__ int unslot16(uint64_t v) { return v == 0xFFFFull ? INT_MAX : (int)v; }
+__device__ __forceinline__ void rec_encode(const Rec &w, uint64_t *v) {
+  v[0] = (uint64_t)w.cnt | slot16(w.vmin) << 16 | slot16(w.best_slot) << 32;
+  v[1] = (uint64_t)w.wv | (uint64_t)w.gv << 24 | (uint64_t)w.e << 40;
+  v[2] = (uint64_t)w.wb | (uint64_t)w.gb << 24;
+  v[3] = w.rt == INT64_MIN ? 0ull : (uint64_t)(w.rt + 1);
+  v[4] = (uint64_t)w.prov & 0xFFFFFFFFull;
+  v[5] = (uint64_t)w.prov >> 32;
+  v[6] = (uint64_t)w.total;
+}
+__device__ __forceinline__ Rec rec_decode(const uint64_t *v) {
+  Rec o;
+  o.cnt = (int)(v[0] & 0xFFFF);
+  o.vmin = unslot16((v[0] >> 16) & 0xFFFF);
+  o.best_slot = unslot16((v[0] >> 32) & 0xFFFF);
+  o.wv = (uint32_t)(v[1] & 0xFFFFFF);
+  o.gv = (uint32_t)((v[1] >> 24) & 0xFFFF);
+  o.e = (int)((v[1] >> 40) & 1);
+  o.wb = (uint32_t)(v[2] & 0xFFFFFF);
+  o.gb = (uint32_t)((v[2] >> 24) & 0xFFFF);
+  const uint64_t r3 = v[3] & kPayload;
+  o.rt = r3 == 0 ? INT64_MIN : (int64_t)r3 - 1;
+  o.prov = (int64_t)(((v[5] & 0xFFFFFFFFull) << 32) | (v[4] & 0xFFFFFFFFull));
+  o.total = (int64_t)(v[6] & kPayload);
+  return o;
+}
+
 __global__ __launch_bounds__(64 * kSeqWaves) void k_seq_setup(dkv_bank bank, Geom g, Prm p, Workspace ws) {
   const int grp = blockIdx.x, nw = blockDim.x >> 6;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
@@ -398,27 +439,24 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq_setup(dkv_bank bank, Geo
       ws.n_ev[b] = 0;  // set to 1 by a workgroup of the bank whose walk timed out
     }
   }
-  if (threadIdx.x == 0) {
-    ws.seq_arrive[grp] = 0;
-    ws.r_star[grp] = 0;
-  }
+  if (threadIdx.x == 0) ws.r_star[grp] = 0;
+  // no record of this call carries a step tag yet
+  uint64_t *recs = ws.seq_rec + (size_t)grp * 2 * kSeqMaxMembers * 8;
+  for (int i = threadIdx.x; i < 2 * kSeqMaxMembers * 8; i += blockDim.x) recs[i] = 0;
 }
 
-__global__ __launch_bounds__(256) void k_seq_coop(dkv_bank bank, Geom g, Prm p, Workspace ws, int P) {
+__global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g, Prm p, Workspace ws, int P) {
   const int b = blockIdx.x / P, q = blockIdx.x % P;
   const int grp = b / g.gs, hh = b % g.gs;
   const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63;
   const int L = ws.gram_ld, Mcap = g.Mcap, N = g.N;
   if (ws.m[b] == 0) return;  // empty at the start: the empty-bank rule, outside the walk
-  __shared__ Rec red[4];
+  __shared__ Rec red[kCoopWaves];
   __shared__ int dec_admit, dec_ev, dec_gev, dec_stop;
   __shared__ int64_t dec_sum;
   const size_t rb = (size_t)b * Mcap, nb = (size_t)b * N;
   const int s0 = q * kCoopSlots;
   const int nmem = g.gs * P;
-  int nlive = 0;
-  for (int h2 = 0; h2 < g.gs; ++h2) nlive += ws.m[grp * g.gs + h2] > 0 ? 1 : 0;
-  const uint32_t per_step = (uint32_t)(nlive * P);
   // wave 0, lane l reads the record of member l = (head l / P, part l % P)
   const bool lane_live = l < nmem && ws.m[grp * g.gs + l / P] > 0;
   int m = ws.m_new[b];
@@ -429,29 +467,31 @@ __global__ __launch_bounds__(256) void k_seq_coop(dkv_bank bank, Geom g, Prm p, 
   uint32_t wn[kCoopS];
 #pragma unroll
   for (int k = 0; k < kCoopS; ++k) {
-    const int s = s0 + k * 256 + tid;
+    const int s = s0 + k * kCoopThreads + tid;
     const bool lv = s < m;
     rho[k] = lv ? bank.rho[rb + s] : 0;
     lim[k] = lv ? ws.lim[rb + s] : 0;
     prov[k] = lv ? bank.prov[rb + s] : 0;
     item[k] = lv ? ws.grow[rb + s] : 0;
   }
+  int x_next = ws.order[nb];
   {
-    const uint32_t *row = gb + (size_t)(Mcap + ws.order[nb]) * L;
+    const uint32_t *row = gb + (size_t)(Mcap + x_next) * L;
 #pragma unroll
-    for (int k = 0; k < kCoopS; ++k) wn[k] = s0 + k * 256 + tid < m ? row[item[k]] : 0u;
+    for (int k = 0; k < kCoopS; ++k) wn[k] = s0 + k * kCoopThreads + tid < m ? row[item[k]] : 0u;
   }
   int steps_taken = 0, stop = 0;
   uint64_t *recs = ws.seq_rec + (size_t)grp * 2 * kSeqMaxMembers * 8;
   for (int j = 0; j < N && !stop; ++j) {
-    const int x = ws.order[nb + j];
+    const int x = x_next;
+    if (j + 1 < N) x_next = ws.order[nb + j + 1];
     uint32_t wx[kCoopS];
     // ---- test of this workgroup's slots against candidate x
     Rec r{0, m + 1 > M ? 1 : 0, INT_MAX, INT_MAX, 0u, 0u, 0u, 0u, INT64_MIN, INT64_MAX, 0};
 #pragma unroll
     for (int k = 0; k < kCoopS; ++k) {
       wx[k] = wn[k];
-      const int s = s0 + k * 256 + tid;
+      const int s = s0 + k * kCoopThreads + tid;
       if (s < m) {
         const int64_t rt = rho[k] + (int64_t)wx[k];
         if (rt >= lim[k]) {
@@ -478,48 +518,42 @@ __global__ __launch_bounds__(256) void k_seq_coop(dkv_bank bank, Geom g, Prm p, 
     if (tid == 0) {
       Rec w = red[0];
 #pragma unroll
-      for (int v = 1; v < 4; ++v) rec_merge(w, red[v]);
+      for (int v = 1; v < kCoopWaves; ++v) rec_merge(w, red[v]);
+      uint64_t v[kRecWords];
+      rec_encode(w, v);
       uint64_t *dst = recs + ((size_t)(j & 1) * kSeqMaxMembers + hh * P + q) * 8;
-      dst[0] = (uint32_t)w.cnt | ((uint64_t)(uint32_t)w.e << 32);
-      dst[1] = (uint32_t)w.vmin | ((uint64_t)w.wv << 32);
-      dst[2] = w.gv | ((uint64_t)(uint32_t)w.best_slot << 32);
-      dst[3] = w.wb | ((uint64_t)w.gb << 32);
-      dst[4] = (uint64_t)w.rt;
-      dst[5] = (uint64_t)w.prov;
-      dst[6] = (uint64_t)w.total;
-      __hip_atomic_fetch_add(ws.seq_arrive + grp, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      const uint64_t tag = (uint64_t)(j + 1) << 48;
+#pragma unroll
+      for (int i = 0; i < kRecWords; ++i)
+        __hip_atomic_store(dst + i, v[i] | tag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     // ---- gather the weights to the next candidate while the records travel
     if (j + 1 < N) {
-      const uint32_t *row = gb + (size_t)(Mcap + ws.order[nb + j + 1]) * L;
+      const uint32_t *row = gb + (size_t)(Mcap + x_next) * L;
 #pragma unroll
-      for (int k = 0; k < kCoopS; ++k) wn[k] = s0 + k * 256 + tid < m ? row[item[k]] : 0u;
+      for (int k = 0; k < kCoopS; ++k) wn[k] = s0 + k * kCoopThreads + tid < m ? row[item[k]] : 0u;
     }
     if (wave == 0) {
-      const uint32_t target = (uint32_t)(j + 1) * per_step;
-      int polls = 0;
-      while (__hip_atomic_load(ws.seq_arrive + grp, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target &&
-             polls < kSpinCap) {
-        __builtin_amdgcn_s_sleep(1);
-        ++polls;
-      }
-      const int timed_out = polls >= kSpinCap;
       Rec o{0, 0, INT_MAX, INT_MAX, 0u, 0u, 0u, 0u, INT64_MIN, INT64_MAX, 0};
-      if (lane_live && !timed_out) {
+      int polls = 0;
+      if (lane_live) {
+        // poll until every word of member l's record carries this step's tag
         const uint64_t *src = recs + ((size_t)(j & 1) * kSeqMaxMembers + l) * 8;
-        const uint64_t w0 = src[0], w1 = src[1], w2 = src[2], w3 = src[3];
-        o.cnt = (int)(uint32_t)w0;
-        o.e = (int)(uint32_t)(w0 >> 32);
-        o.vmin = (int)(uint32_t)w1;
-        o.wv = (uint32_t)(w1 >> 32);
-        o.gv = (uint32_t)w2;
-        o.best_slot = (int)(uint32_t)(w2 >> 32);
-        o.wb = (uint32_t)w3;
-        o.gb = (uint32_t)(w3 >> 32);
-        o.rt = (int64_t)src[4];
-        o.prov = (int64_t)src[5];
-        o.total = (int64_t)src[6];
+        const uint64_t tag = (uint64_t)(j + 1);
+        uint64_t v[kRecWords];
+        for (;;) {
+          bool ready = true;
+#pragma unroll
+          for (int i = 0; i < kRecWords; ++i) {
+            v[i] = __hip_atomic_load(src + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            ready &= (v[i] >> 48) == tag;
+          }
+          if (ready || ++polls >= kSpinCap) break;
+          __builtin_amdgcn_s_sleep(1);
+        }
+        if (polls < kSpinCap) o = rec_decode(v);
       }
+      const int timed_out = __ballot(polls >= kSpinCap) != 0ull ? 1 : 0;
       // merge the parts of each bank into its first part's lane
       for (int i = 1; i < P; ++i) {
         const Rec v = rec_shfl(o, l + i < 64 ? l + i : l);
@@ -547,21 +581,21 @@ __global__ __launch_bounds__(256) void k_seq_coop(dkv_bank bank, Geom g, Prm p, 
       const uint32_t *row = gb + (size_t)dec_gev * L;
 #pragma unroll
       for (int k = 0; k < kCoopS; ++k) {
-        const int s = s0 + k * 256 + tid;
+        const int s = s0 + k * kCoopThreads + tid;
         if (s < m && s != ev) rho[k] += (int64_t)wx[k] - (int64_t)row[item[k]];
       }
     } else {
 #pragma unroll
       for (int k = 0; k < kCoopS; ++k)
-        if (s0 + k * 256 + tid < m) rho[k] += (int64_t)wx[k];
+        if (s0 + k * kCoopThreads + tid < m) rho[k] += (int64_t)wx[k];
     }
     const int t = ev >= 0 ? ev : m;
     const int tl = t - s0;
-    if (tl >= 0 && tl < kCoopSlots && (tl & 255) == tid) {
-      const int kt = tl >> 8;
+    if (tl >= 0 && tl < kCoopSlots && tl % kCoopThreads == tid) {
+      const int kt = tl / kCoopThreads;
       const int64_t sum = dec_sum;
       const int64_t bs = sum > p.delta_q ? sum : p.delta_q;
-      const uint32_t wnew = j + 1 < N ? gb[(size_t)(Mcap + ws.order[nb + j + 1]) * L + Mcap + x] : 0u;
+      const uint32_t wnew = j + 1 < N ? gb[(size_t)(Mcap + x_next) * L + Mcap + x] : 0u;
 #pragma unroll
       for (int k = 0; k < kCoopS; ++k)
         if (k == kt) {
@@ -579,7 +613,7 @@ __global__ __launch_bounds__(256) void k_seq_coop(dkv_bank bank, Geom g, Prm p, 
   }
 #pragma unroll
   for (int k = 0; k < kCoopS; ++k) {
-    const int s = s0 + k * 256 + tid;
+    const int s = s0 + k * kCoopThreads + tid;
     if (s < m) {
       bank.rho[rb + s] = rho[k];
       ws.grow[rb + s] = item[k];
@@ -638,7 +672,7 @@ bool coop_fits(int nblocks) {
   if (hipGetDevice(&dev) != hipSuccess) return false;
   if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess || !coop) return false;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return false;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_seq_coop, 256, 0) != hipSuccess) return false;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_seq_coop, kCoopThreads, 0) != hipSuccess) return false;
   return (long)per_cu * cus >= nblocks;
 }
 
@@ -660,7 +694,7 @@ hipError_t seq_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g,
     Workspace a_ws = ws;
     void *args[] = {&a_bank, &a_g, &a_p, &a_ws, &P};
     const hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k_seq_coop),
-                                                    dim3((unsigned)(g.B * P)), dim3(256), args, 0, s);
+                                                    dim3((unsigned)(g.B * P)), dim3(kCoopThreads), args, 0, s);
     if (e != hipSuccess) return e;
     k_seq_results<<<g.G, 64 * waves, 0, s>>>(bank, g, p, ws, out);
   } else {
