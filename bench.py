@@ -14,7 +14,10 @@ that all steps do the same work.
 Prints one JSON line.  value = candidate tokens per second per layer-head for
 the whole step (update + attention); the update-only rate and the attention
 TFLOP/s are reported beside it, with the roofline of the dominant kernel and
-the CPU oracle timed on a bounded sample.  Two extra fields time the sink +
+the CPU oracle timed on a bounded sample.  update_gram gives the update's
+algorithmic Gram work (pairs of the score, prefix, partial-tile and maintenance
+stages at 2 d flops each) and its rate against the bf16 MFMA peak over the
+whole update time.  Two extra fields time the sink +
 window + bank attention at the paper's deployment shape and one block of the
 rollout configuration at full scale (360 banks in one launch).
 """
@@ -113,6 +116,29 @@ def sink_attention(api, synth, torch, steps=10):
     tf = flops / (ms * 1e-3) / 1e12
     return {"context": f"sink {ns} + window {nw} + bank {M} keys, {nq} queries, {B} heads, d={d}, bf16",
             "ms": round(ms, 4), "tflops": round(tf, 2), "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4)}
+
+
+def update_gram_work(api, torch, bank, snap, seg_k, seg_v, prm, ws, N, d, upd_ms):
+    """Algorithmic Gram work of the timed update and its rate against the bf16 MFMA
+    peak: per bank m*N pairs for the candidate scores (Eq. 6), m*R for the prefix
+    densities (Eq. 8, R = min(N, M)), m*64 for the partial tile at r*, and
+    (m + r*)*e + r*^2 for the density maintenance (Supp. C), at 2 d flops per pair;
+    m, r* and e are those of the timed update (rerun once with its outputs)."""
+    bank.restore(snap)
+    m0 = bank.occupancy.cpu().numpy().astype(np.int64)
+    M = bank.budget.cpu().numpy().astype(np.int64)
+    out = api.UpdateOut(bank, N)
+    api.update_bank(bank, seg_k, seg_v, 1, prm, workspace=ws, out=out)
+    torch.cuda.synchronize()
+    r = np.repeat(out.r_star.cpu().numpy().astype(np.int64), bank.gs)
+    e = out.n_evicted.cpu().numpy().astype(np.int64)
+    R = np.minimum(N, M)
+    pairs = m0 * N + m0 * R + m0 * np.minimum(64, R) + (m0 + r) * e + r * r
+    flops = 2.0 * d * float(pairs.sum())
+    tf = flops / (upd_ms * 1e-3) / 1e12
+    return {"pairs": int(pairs.sum()), "tflop": round(flops / 1e12, 4), "tflops": round(tf, 2),
+            "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4), "r_star": int(out.r_star.max().item()),
+            "evicted_per_bank": int(e.max())}
 
 
 def rollout_block(api, synth, torch, steps=3):
@@ -286,6 +312,8 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic()},
     }
+    if args.policy != "sequential":
+        result["update_gram"] = update_gram_work(api, torch, bank, snap, seg_k, seg_v, run_prm, ws, N, d, upd_ms)
     if not args.no_sink_attention:
         result["sink_attention"] = sink_attention(api, synth, torch)
     if not args.no_rollout_block:
