@@ -223,6 +223,51 @@ def test_sequential_banks_spanning_workgroups():
     assert rejected > 0 and taken_with_violator > 0
 
 
+def test_sequential_part_boundary_and_empty_bank():
+    """Sequential competition in a group whose banks have budgets 2,049, 0 and
+    2,100: the first bank's last slot (2,048) belongs to the second workgroup of
+    the bank, so states enter a part that held none; the budget-0 bank stays
+    empty, takes the empty-bank rule every block and stays out of the shared
+    test.  d = 64, sigma^2 = 1/2, exact copies of bank keys among fresh keys,
+    source order then score order; bit-exact against the oracle, which must see
+    rejected steps and steps that release a violator."""
+    _log("sequential part boundary and empty bank")
+    rng = np.random.default_rng(11)
+    budgets = np.array([2049, 0, 2100], np.int32)
+    B, gs, d = 3, 3, 64
+    bank = api.Bank(B, int(budgets.max()), d, dtype=torch.bfloat16, group_size=gs,
+                    budget=torch.from_numpy(budgets))
+    obanks = [BankState.empty(int(M), d) for M in budgets]
+    taken_with_violator = rejected = 0
+    for t, flags in enumerate([0, api.POLICY_SOURCE_ORDER, 0]):
+        prm = api.Params(sigma2_log2=-1, flags=api.POLICY_SEQUENTIAL | flags)
+        if t == 0:
+            K = np.stack([np.concatenate([k, k[:100]])
+                          for k in (synth.random_grid_keys(rng, (1900, d)) for _ in range(B))])
+        else:
+            K = np.stack([np.concatenate([obanks[h].K[rng.choice(obanks[h].m, 100, replace=False)].astype(np.float32)
+                                          if obanks[h].m else synth.random_grid_keys(rng, (100, d)),
+                                          synth.random_grid_keys(rng, (100, d))]) for h in range(B)])
+            for h in range(B):
+                rng.shuffle(K[h])
+        V = synth.random_grid_keys(rng, K.shape)
+        n = K.shape[1]
+        out = api.UpdateOut(bank, n, trace=True)
+        api.update_bank(bank, dev(K, "bf16"), dev(V, "bf16"), t, prm, out=out)
+        torch.cuda.synchronize()
+        new, recs = oracle_step(obanks, K, V, t, oracle_params(prm), gs)
+        assert_trace_equal(out, recs, gs, obanks, n, ctx=f"block {t}", sequential=True)
+        for b in range(B):
+            assert_bank_equal(bank, b, new[b], ctx=f"block {t}")
+        if t > 0:
+            rec = recs[0]
+            rejected += int((~rec.steps).sum())
+            taken_with_violator += sum(int(((hr.c > 0) & rec.steps).sum()) for hr in rec.heads)
+        obanks = new
+    assert int(bank.occupancy[0].item()) == 2049 and int(bank.occupancy[1].item()) == 0
+    assert rejected > 0 and taken_with_violator > 0
+
+
 def test_sequential_wide_group():
     """Sequential competition with 72 banks sharing each step (more banks than
     the multi-workgroup walk takes, so one workgroup walks the group): budget 120,
