@@ -40,7 +40,7 @@ TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_attn_mfma_single_layer_traff
 # dkv_params.flags of each policy ablation (Table 1(b); independent per-head = group size 1)
 # (kv_descriptor: the [K; V] retention geometry; the workload's values are not on the key grid, so
 # this mode is a timing run only, its decisions carry the fp32 rounding of the descriptor Gram;
-# sequential: the within-block competition of Supp. E, one candidate per step, one workgroup per group)
+# sequential: the within-block competition of Supp. E, one candidate per step)
 POLICIES = {"default": 0, "source_order": 0x1, "refresh_base": 0x2, "densest_only": 0x4, "source_fill": 0x8,
             "kv_descriptor": 0x10, "sequential": 0x20}
 
