@@ -5,13 +5,20 @@
 //
 //   k_seq_gram    W between every pair of items of a bank, the items being its
 //                 slots 0..Mcap-1 (pre-update states) and its candidates, on
-//                 bf16 MFMA (32 x 32 tiles, one per wave), stored as
-//                 [B, L, L] uint32 with L = Mcap + N
-//   k_seq         one workgroup per group, one wave per bank (a wave takes
-//                 every bank_index % waves): for every step the one-candidate
-//                 violator test of each bank (a pass over its slots), the
-//                 shared decision through LDS, and on a taken step the
+//                 bf16 MFMA (32 x 32 tiles), stored as [B, L, L] uint32 with
+//                 L = Mcap + N
+//   k_seq_setup   per bank: slot items and violation limits, or the
+//                 empty-bank rule for a bank that starts empty
+//   k_seq_coop    the steps, several workgroups per group (cooperative
+//                 launch): each holds up to 2,048 slots of one bank in
+//                 registers; per step the one-candidate violator test of its
+//                 slots, one record per workgroup exchanged through global
+//                 memory, the shared decision, and on a taken step the
 //                 release, the exact density maintenance and the new state
+//   k_seq_results per bank: refreshed baselines, admitted and released lists
+//   k_seq         the same steps in one workgroup per group (one wave per
+//                 bank, the state in the bank arrays), for groups the
+//                 cooperative walk does not take
 //   k_seq_commit  the K/V rows of the slots that ended with a candidate
 //
 // Weights are the binary32 chain of the rest of the update on exact grid
@@ -39,11 +46,15 @@ __device__ __forceinline__ uint32_t weight_q(float d2, const Prm &p) {
 __device__ __forceinline__ int tile_col(int q, int h) { return 8 * (q >> 2) + 4 * h + (q & 3); }
 
 // ---------------------------------------------------------------------------
-// k_seq_gram: workgroup = 4 waves = 32 row items x 128 column items.
-// Item u < Mcap is bank slot u (live while u < m), item Mcap + x candidate x.
-// Dead items read a live row of the bank array (finite or not, their
-// products only reach outputs that are not stored).
+// k_seq_gram: workgroup = 4 waves = 32 row items x kGramCols column items; a
+// wave keeps its 32 row keys (the B operand) in registers and walks
+// kGramCols / 128 tiles of 32 columns.  Item u < Mcap is bank slot u (live
+// while u < m), item Mcap + x candidate x.  Dead items read a live row of the
+// bank array (finite or not, their products only reach outputs that are not
+// stored).
 // ---------------------------------------------------------------------------
+constexpr int kGramCols = 512;
+
 template <int D>
 __global__ __launch_bounds__(256) void k_seq_gram(dkv_bank bank, dkv_segment seg, Geom g, Prm p, Workspace ws) {
   constexpr int KS = D / 16;
@@ -55,8 +66,8 @@ __global__ __launch_bounds__(256) void k_seq_gram(dkv_bank bank, dkv_segment seg
     const int u1 = u0 + 32;
     return (u0 < m) || (u1 > Mcap && u0 < Mcap + g.N);
   };
-  const int r0 = blockIdx.y * 32, c0 = blockIdx.x * 128 + wave * 32;
-  if (!any_live(r0) || !any_live(c0) || c0 >= L) return;  // whole wave (no barrier in this kernel)
+  const int r0 = blockIdx.y * 32;
+  if (!any_live(r0)) return;  // whole workgroup (no barrier in this kernel)
   const uint16_t *bk = static_cast<const uint16_t *>(bank.k);
   const uint16_t *ck = static_cast<const uint16_t *>(seg.k);
   auto row_ptr = [&](int u) -> const uint16_t * {
@@ -67,29 +78,38 @@ __global__ __launch_bounds__(256) void k_seq_gram(dkv_bank bank, dkv_segment seg
     if (u >= Mcap && u < Mcap + g.N) return ws.cnorm[(size_t)b * g.N + (u - Mcap)];
     return u < m ? bank.knorm[(size_t)b * Mcap + u] : 0.0f;
   };
-  const int ru = r0 + n, cu = c0 + n;  // this lane's row item (B operand) and column item (A operand)
-  const uint16_t *rp = row_ptr(ru), *cp = row_ptr(cu);
-  f32x16 acc = {};
+  const int ru = r0 + n;  // this lane's row item (B operand)
+  const uint16_t *rp = row_ptr(ru);
+  bf16x8 bb[KS];
 #pragma unroll
-  for (int kk = 0; kk < KS; ++kk) {
-    const u32x4 a = *reinterpret_cast<const u32x4 *>(cp + 16 * kk + 8 * h);
-    const u32x4 bb = *reinterpret_cast<const u32x4 *>(rp + 16 * kk + 8 * h);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, bb), acc,
-                                                  0, 0, 0);
-  }
-  const float nr = norm_of(ru), nc = norm_of(cu);
-  float ncm[16];
-#pragma unroll
-  for (int q = 0; q < 16; ++q) ncm[q] = __shfl(nc, tile_col(q, h), 32);  // column item's norm (lane cm of this half)
-  if (!live(ru)) return;
+  for (int kk = 0; kk < KS; ++kk) bb[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(rp + 16 * kk + 8 * h));
+  const float nr = norm_of(ru);
+  const bool row_live = live(ru);
   // W is symmetric (the same products summed in the same order, and |a|^2 +
   // |b|^2 commutes), so W(ru, u) is stored at [u][ru]: the 32 lanes of a half
   // write 32 consecutive entries of one row.
   uint32_t *col = ws.gram + (size_t)b * L * L + ru;
+  for (int c0 = blockIdx.x * kGramCols + wave * 32; c0 < min(L, (int)(blockIdx.x + 1) * kGramCols); c0 += 128) {
+    if (!any_live(c0)) continue;  // uniform over the wave
+    const int cu = c0 + n;  // this lane's column item (A operand)
+    const uint16_t *cp = row_ptr(cu);
+    f32x16 acc = {};
 #pragma unroll
-  for (int q = 0; q < 16; ++q) {
-    const int u = c0 + tile_col(q, h);
-    if (u < L && live(u)) col[(size_t)u * L] = weight_q((nr + ncm[q]) - 2.0f * acc[q], p);
+    for (int kk = 0; kk < KS; ++kk) {
+      const u32x4 a = *reinterpret_cast<const u32x4 *>(cp + 16 * kk + 8 * h);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), bb[kk], acc, 0, 0, 0);
+    }
+    const float nc = norm_of(cu);
+    float ncm[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) ncm[q] = __shfl(nc, tile_col(q, h), 32);  // column item's norm
+    if (row_live) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int u = c0 + tile_col(q, h);
+        if (u < L && live(u)) col[(size_t)u * L] = weight_q((nr + ncm[q]) - 2.0f * acc[q], p);
+      }
+    }
   }
 }
 
@@ -515,7 +535,7 @@ __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g
     r = rec_wave(r, l);
     if (l == 0) red[wave] = r;
     __syncthreads();
-    if (tid == 0) {
+    if (tid == 0 && nmem > 1) {
       Rec w = red[0];
 #pragma unroll
       for (int v = 1; v < kCoopWaves; ++v) rec_merge(w, red[v]);
@@ -536,7 +556,14 @@ __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g
     if (wave == 0) {
       Rec o{0, 0, INT_MAX, INT_MAX, 0u, 0u, 0u, 0u, INT64_MIN, INT64_MAX, 0};
       int polls = 0;
-      if (lane_live) {
+      if (nmem == 1) {
+        // a single workgroup in the group: its own record is the decision's input
+        if (l == 0) {
+          o = red[0];
+#pragma unroll
+          for (int v = 1; v < kCoopWaves; ++v) rec_merge(o, red[v]);
+        }
+      } else if (lane_live) {
         // poll until every word of member l's record carries this step's tag
         const uint64_t *src = recs + ((size_t)(j & 1) * kSeqMaxMembers + l) * 8;
         const uint64_t tag = (uint64_t)(j + 1);
@@ -681,7 +708,7 @@ hipError_t seq_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g,
                     const dkv_update_out &out, const Workspace &ws, hipStream_t s) {
   const int L = ws.gram_ld;
   if (L > 0 && g.N > 0) {
-    const dim3 grid((unsigned)((L + 127) / 128), (unsigned)((L + 31) / 32), (unsigned)g.B);
+    const dim3 grid((unsigned)((L + kGramCols - 1) / kGramCols), (unsigned)((L + 31) / 32), (unsigned)g.B);
     k_seq_gram<D><<<grid, 256, 0, s>>>(bank, seg, g, p, ws);
   }
   const int waves = g.gs < kSeqWaves ? g.gs : kSeqWaves;
