@@ -268,6 +268,25 @@ def test_sequential_part_boundary_and_empty_bank():
     assert rejected > 0 and taken_with_violator > 0
 
 
+@pytest.mark.parametrize("n", [1, 65])
+def test_sequential_candidate_counts(n):
+    """Sequential competition with 1 and 65 candidates per block into banks that
+    the first block fills (budget 150, three banks per group), then an empty
+    segment, which must leave the banks unchanged and report no step."""
+    _log(f"sequential candidate count n={n}")
+    cfg = synth.Config(heads=3, d=128, dtype="bf16", n_cand=n, budget=150, group_size=3, **SMALL)
+    prm = api.Params(sigma2_log2=5, tau_num=3, flags=api.POLICY_SEQUENTIAL)
+    bank, _ = _run_rollout(cfg, 5, prm, dup_every=2, init_full=True)
+    before = bank.state_dict()
+    out = api.UpdateOut(bank, 0)
+    out.r_star.fill_(-7)
+    api.update_bank(bank, None, None, 9, prm, out=out)
+    torch.cuda.synchronize()
+    for name, t in bank.state_dict().items():
+        assert torch.equal(t, before[name]), name
+    assert int(out.r_star[0].item()) == 0
+
+
 def test_sequential_wide_group():
     """Sequential competition with 72 banks sharing each step (more banks than
     the multi-workgroup walk takes, so one workgroup walks the group): budget 120,
