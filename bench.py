@@ -185,6 +185,14 @@ def rollout_block(api, synth, torch, steps=3):
             times.append([ev[0].elapsed_time(ev[3]), ev[1].elapsed_time(ev[2]), ev[2].elapsed_time(ev[3])])
     step_ms, upd_ms, att_ms = (float(np.mean(c)) for c in zip(*times))
     m_after = bank.occupancy.cpu().numpy()
+    # algorithmic Gram work of the timed update (the same per-bank pair counts as update_gram)
+    r = np.repeat(upd.r_star.cpu().numpy().astype(np.int64), cfg.group_size)
+    e = upd.n_evicted.cpu().numpy().astype(np.int64)
+    bank.restore(snap)
+    m0 = bank.occupancy.cpu().numpy().astype(np.int64)
+    R = min(N, M)
+    gram_flops = 2.0 * d * float((m0 * N + m0 * R + m0 * min(64, R) + (m0 + r) * e + r * r).sum())
+    gram_tf = gram_flops / (upd_ms * 1e-3) / 1e12
     flops = float(sum(4.0 * nq * (int(m) + N) * d for m in m_after))
     tf = flops / (att_ms * 1e-3) / 1e12
     res = {"context": f"rollout: {L} layers x {H} heads ({B} banks, one launch), d={d}, bf16, budget {M}, "
@@ -193,6 +201,8 @@ def rollout_block(api, synth, torch, steps=3):
            "tokens_per_s_per_layer_head": round(N / (step_ms * 1e-3), 1),
            "update_tokens_per_s_per_layer_head": round(N / (upd_ms * 1e-3), 1),
            "attention_tflops": round(tf, 2), "attention_frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+           "update_gram_tflop": round(gram_flops / 1e12, 3), "update_gram_tflops": round(gram_tf, 2),
+           "update_gram_frac_of_bf16_peak": round(gram_tf / PEAK_BF16_TFLOPS, 4),
            "mean_r_star": round(float(upd.r_star.float().mean().item()), 1),
            "mean_occupancy": round(float(m_after.mean()), 1)}
     del bank, ws, snap, seg_k, seg_v, q, out
