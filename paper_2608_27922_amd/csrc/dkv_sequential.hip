@@ -406,10 +406,31 @@ __device__ __forceinline__ Rec rec_shfl(const Rec &r, int src) {
   o.total = sh64(r.total);
   return o;
 }
-__device__ __forceinline__ Rec rec_wave(Rec r, int l) {
+// Wave reduction of the lanes' records.  The count rides in the top bits of
+// the weight sum (a wave's sum of at most 512 weights stays below 2^32),
+// the slots and the densest state's key are reduced level by level, and the
+// weights and items of the first violator and of the densest state are then
+// read once from the lanes that hold them (a slot belongs to one lane).
+__device__ __forceinline__ Rec rec_wave(const Rec &r) {
+  int64_t sc = r.total + ((int64_t)r.cnt << 40);
+  int vmin = r.vmin;
+  Best best{r.rt, r.prov, r.best_slot};
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) rec_merge(r, rec_shfl(r, l ^ o));
-  return r;
+  for (int o = 32; o > 0; o >>= 1) {
+    sc += shfl_xor_i64(sc, o);
+    vmin = min(vmin, __shfl_xor(vmin, o, 64));
+    const Best w{shfl_xor_i64(best.rt, o), shfl_xor_i64(best.prov, o), __shfl_xor(best.slot, o, 64)};
+    if (better(w, best)) best = w;
+  }
+  Rec w{(int)(sc >> 40), r.e, vmin, best.slot, 0u, 0u, 0u, 0u, best.rt, best.prov, sc & ((1ll << 40) - 1)};
+  const unsigned long long hv = __ballot(vmin != INT_MAX && r.vmin == vmin);
+  const unsigned long long hb = __ballot(best.slot != INT_MAX && r.best_slot == best.slot);
+  const int lv = hv ? __ffsll((long long)hv) - 1 : 0, lb = hb ? __ffsll((long long)hb) - 1 : 0;
+  w.wv = __shfl(r.wv, lv, 64);
+  w.gv = __shfl(r.gv, lv, 64);
+  w.wb = __shfl(r.wb, lb, 64);
+  w.gb = __shfl(r.gb, lb, 64);
+  return w;
 }
 
 // A record travels as kRecWords 64-bit words, each with a 48-bit payload and
@@ -532,7 +553,7 @@ __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g
         r.total += wx[k];
       }
     }
-    r = rec_wave(r, l);
+    r = rec_wave(r);
     if (l == 0) red[wave] = r;
     __syncthreads();
     if (tid == 0 && nmem > 1) {
