@@ -347,7 +347,7 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq(dkv_bank bank, Geom g, P
 
 // ---------------------------------------------------------------------------
 // Multi-workgroup walk.  Workgroup (b, q) of a bank holds the slots
-// q * kCoopSlots + k * kCoopThreads + thread (k < kCoopS) in registers: rho, limit,
+// q * 256 S + k * 256 + thread (k < S, S = 8 or 16) in registers: rho, limit,
 // item and provenance.  Per step every workgroup posts one record (its
 // violator count, its first violator, its densest state and the sum of its
 // weights to the candidate) to global memory as step-tagged words; wave 0 of
@@ -359,9 +359,9 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq(dkv_bank bank, Geom g, P
 // with r_star = -1.
 // ---------------------------------------------------------------------------
 constexpr int kCoopThreads = 256;  // threads of a workgroup of the walk
-constexpr int kCoopS = 8;          // slots per thread
 constexpr int kCoopWaves = kCoopThreads / 64;
-constexpr int kCoopSlots = kCoopThreads * kCoopS;
+// slots per thread: 8 (2,048 per workgroup), or 16 when a group would need
+// more than kSeqMaxMembers workgroups of 2,048 slots
 constexpr int kSpinCap = 1 << 22;
 
 // record words: 0 cnt | e << 32, 1 vmin | W(vmin) << 32, 2 item(vmin) | best slot << 32,
@@ -486,6 +486,7 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq_setup(dkv_bank bank, Geo
   for (int i = threadIdx.x; i < 2 * kSeqMaxMembers * 8; i += blockDim.x) recs[i] = 0;
 }
 
+template <int S>
 __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g, Prm p, Workspace ws, int P) {
   const int b = blockIdx.x / P, q = blockIdx.x % P;
   const int grp = b / g.gs, hh = b % g.gs;
@@ -496,18 +497,19 @@ __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g
   __shared__ int dec_admit, dec_ev, dec_gev, dec_stop;
   __shared__ int64_t dec_sum;
   const size_t rb = (size_t)b * Mcap, nb = (size_t)b * N;
-  const int s0 = q * kCoopSlots;
+  constexpr int kSlotsWg = kCoopThreads * S;  // slots per workgroup
+  const int s0 = q * kSlotsWg;
   const int nmem = g.gs * P;
   // wave 0, lane l reads the record of member l = (head l / P, part l % P)
   const bool lane_live = l < nmem && ws.m[grp * g.gs + l / P] > 0;
   int m = ws.m_new[b];
   const int M = ws.M[b];
   const uint32_t *gb = ws.gram + (size_t)b * L * L;
-  int64_t rho[kCoopS], lim[kCoopS], prov[kCoopS];
-  int item[kCoopS];
-  uint32_t wn[kCoopS];
+  int64_t rho[S], lim[S], prov[S];
+  int item[S];
+  uint32_t wn[S];
 #pragma unroll
-  for (int k = 0; k < kCoopS; ++k) {
+  for (int k = 0; k < S; ++k) {
     const int s = s0 + k * kCoopThreads + tid;
     const bool lv = s < m;
     rho[k] = lv ? bank.rho[rb + s] : 0;
@@ -519,18 +521,18 @@ __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g
   {
     const uint32_t *row = gb + (size_t)(Mcap + x_next) * L;
 #pragma unroll
-    for (int k = 0; k < kCoopS; ++k) wn[k] = s0 + k * kCoopThreads + tid < m ? row[item[k]] : 0u;
+    for (int k = 0; k < S; ++k) wn[k] = s0 + k * kCoopThreads + tid < m ? row[item[k]] : 0u;
   }
   int steps_taken = 0, stop = 0;
   uint64_t *recs = ws.seq_rec + (size_t)grp * 2 * kSeqMaxMembers * 8;
   for (int j = 0; j < N && !stop; ++j) {
     const int x = x_next;
     if (j + 1 < N) x_next = ws.order[nb + j + 1];
-    uint32_t wx[kCoopS];
+    uint32_t wx[S];
     // ---- test of this workgroup's slots against candidate x
     Rec r{0, m + 1 > M ? 1 : 0, INT_MAX, INT_MAX, 0u, 0u, 0u, 0u, INT64_MIN, INT64_MAX, 0};
 #pragma unroll
-    for (int k = 0; k < kCoopS; ++k) {
+    for (int k = 0; k < S; ++k) {
       wx[k] = wn[k];
       const int s = s0 + k * kCoopThreads + tid;
       if (s < m) {
@@ -572,7 +574,7 @@ __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g
     if (j + 1 < N) {
       const uint32_t *row = gb + (size_t)(Mcap + x_next) * L;
 #pragma unroll
-      for (int k = 0; k < kCoopS; ++k) wn[k] = s0 + k * kCoopThreads + tid < m ? row[item[k]] : 0u;
+      for (int k = 0; k < S; ++k) wn[k] = s0 + k * kCoopThreads + tid < m ? row[item[k]] : 0u;
     }
     if (wave == 0) {
       Rec o{0, 0, INT_MAX, INT_MAX, 0u, 0u, 0u, 0u, INT64_MIN, INT64_MAX, 0};
@@ -628,24 +630,24 @@ __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g
     if (ev >= 0) {
       const uint32_t *row = gb + (size_t)dec_gev * L;
 #pragma unroll
-      for (int k = 0; k < kCoopS; ++k) {
+      for (int k = 0; k < S; ++k) {
         const int s = s0 + k * kCoopThreads + tid;
         if (s < m && s != ev) rho[k] += (int64_t)wx[k] - (int64_t)row[item[k]];
       }
     } else {
 #pragma unroll
-      for (int k = 0; k < kCoopS; ++k)
+      for (int k = 0; k < S; ++k)
         if (s0 + k * kCoopThreads + tid < m) rho[k] += (int64_t)wx[k];
     }
     const int t = ev >= 0 ? ev : m;
     const int tl = t - s0;
-    if (tl >= 0 && tl < kCoopSlots && tl % kCoopThreads == tid) {
+    if (tl >= 0 && tl < kSlotsWg && tl % kCoopThreads == tid) {
       const int kt = tl / kCoopThreads;
       const int64_t sum = dec_sum;
       const int64_t bs = sum > p.delta_q ? sum : p.delta_q;
       const uint32_t wnew = j + 1 < N ? gb[(size_t)(Mcap + x_next) * L + Mcap + x] : 0u;
 #pragma unroll
-      for (int k = 0; k < kCoopS; ++k)
+      for (int k = 0; k < S; ++k)
         if (k == kt) {
           rho[k] = sum;
           lim[k] = lim_of(bs, p);
@@ -660,7 +662,7 @@ __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g
     if (ev < 0) ++m;
   }
 #pragma unroll
-  for (int k = 0; k < kCoopS; ++k) {
+  for (int k = 0; k < S; ++k) {
     const int s = s0 + k * kCoopThreads + tid;
     if (s < m) {
       bank.rho[rb + s] = rho[k];
@@ -713,14 +715,15 @@ __global__ __launch_bounds__(256) void k_seq_commit(dkv_bank bank, dkv_segment s
   reinterpret_cast<u32x4 *>(dst)[cc] = reinterpret_cast<const u32x4 *>(src)[cc];
 }
 
-// Whether a cooperative launch of nblocks k_seq_coop workgroups fits the
+// Whether a cooperative launch of nblocks k_seq_coop<S> workgroups fits the
 // current device (all of them resident at once).
+template <int S>
 bool coop_fits(int nblocks) {
   int dev = 0, coop = 0, cus = 0, per_cu = 0;
   if (hipGetDevice(&dev) != hipSuccess) return false;
   if (hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) != hipSuccess || !coop) return false;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return false;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_seq_coop, kCoopThreads, 0) != hipSuccess) return false;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_seq_coop<S>, kCoopThreads, 0) != hipSuccess) return false;
   return (long)per_cu * cus >= nblocks;
 }
 
@@ -733,16 +736,21 @@ hipError_t seq_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g,
     k_seq_gram<D><<<grid, 256, 0, s>>>(bank, seg, g, p, ws);
   }
   const int waves = g.gs < kSeqWaves ? g.gs : kSeqWaves;
-  int P = (g.Mcap + kCoopSlots - 1) / kCoopSlots;
-  if (g.N > 0 && g.gs * P <= kSeqMaxMembers && coop_fits(g.B * P)) {
+  // workgroups per bank with 8 and with 16 slots per thread
+  int P8 = (g.Mcap + 8 * kCoopThreads - 1) / (8 * kCoopThreads);
+  int P16 = (g.Mcap + 16 * kCoopThreads - 1) / (16 * kCoopThreads);
+  const bool use8 = g.N > 0 && g.gs * P8 <= kSeqMaxMembers && coop_fits<8>(g.B * P8);
+  const bool use16 = !use8 && g.N > 0 && g.gs * P16 <= kSeqMaxMembers && coop_fits<16>(g.B * P16);
+  if (use8 || use16) {
     k_seq_setup<<<g.G, 64 * waves, 0, s>>>(bank, g, p, ws);
     dkv_bank a_bank = bank;
     Geom a_g = g;
     Prm a_p = p;
     Workspace a_ws = ws;
-    void *args[] = {&a_bank, &a_g, &a_p, &a_ws, &P};
-    const hipError_t e = hipLaunchCooperativeKernel(reinterpret_cast<const void *>(k_seq_coop),
-                                                    dim3((unsigned)(g.B * P)), dim3(kCoopThreads), args, 0, s);
+    int *P = use8 ? &P8 : &P16;
+    void *args[] = {&a_bank, &a_g, &a_p, &a_ws, P};
+    const void *kern = use8 ? reinterpret_cast<const void *>(k_seq_coop<8>) : reinterpret_cast<const void *>(k_seq_coop<16>);
+    const hipError_t e = hipLaunchCooperativeKernel(kern, dim3((unsigned)(g.B * *P)), dim3(kCoopThreads), args, 0, s);
     if (e != hipSuccess) return e;
     k_seq_results<<<g.G, 64 * waves, 0, s>>>(bank, g, p, ws, out);
   } else {

@@ -287,6 +287,48 @@ def test_sequential_candidate_counts(n):
     assert int(out.r_star[0].item()) == 0
 
 
+def test_sequential_sixteen_slots_per_thread():
+    """Sequential competition in a group of 33 banks of budget 2,100: at 2,048
+    slots per workgroup the group would need 66 workgroups, more than the walk
+    takes, so it runs with 16 slots per thread (4,096 per workgroup, 33
+    workgroups) and states enter slots past 2,048 of a workgroup.  d = 64,
+    sigma^2 = 1/2, exact copies of bank keys among fresh keys, source order
+    (every step rejected: some bank of the group has a violator) then score
+    order (steps that release a violator); bit-exact against the oracle."""
+    _log("sequential sixteen slots per thread")
+    rng = np.random.default_rng(13)
+    B, gs, d, M = 33, 33, 64, 2100
+    bank = api.Bank(B, M, d, dtype=torch.bfloat16, group_size=gs)
+    obanks = [BankState.empty(M, d) for _ in range(B)]
+    taken_with_violator = rejected = 0
+    for t, flags in enumerate([0, api.POLICY_SOURCE_ORDER, 0]):
+        prm = api.Params(sigma2_log2=-1, flags=api.POLICY_SEQUENTIAL | flags)
+        if t == 0:
+            K = np.stack([np.concatenate([k, k[:100]])
+                          for k in (synth.random_grid_keys(rng, (1900, d)) for _ in range(B))])
+        else:
+            K = np.stack([np.concatenate([obanks[h].K[rng.choice(obanks[h].m, 60, replace=False)].astype(np.float32),
+                                          synth.random_grid_keys(rng, (100, d))]) for h in range(B)])
+            for h in range(B):
+                rng.shuffle(K[h])
+        V = synth.random_grid_keys(rng, K.shape)
+        n = K.shape[1]
+        out = api.UpdateOut(bank, n, trace=True)
+        api.update_bank(bank, dev(K, "bf16"), dev(V, "bf16"), t, prm, out=out)
+        torch.cuda.synchronize()
+        new, recs = oracle_step(obanks, K, V, t, oracle_params(prm), gs)
+        assert_trace_equal(out, recs, gs, obanks, n, ctx=f"block {t}", sequential=True)
+        for b in range(B):
+            assert_bank_equal(bank, b, new[b], ctx=f"block {t}")
+        if t > 0:
+            rec = recs[0]
+            rejected += int((~rec.steps).sum())
+            taken_with_violator += sum(int(((hr.c > 0) & rec.steps).sum()) for hr in rec.heads)
+        obanks = new
+    assert int(bank.occupancy.min().item()) == M
+    assert rejected > 0 and taken_with_violator > 0
+
+
 def test_sequential_wide_group():
     """Sequential competition with 72 banks sharing each step (more banks than
     the multi-workgroup walk takes, so one workgroup walks the group): budget 120,
