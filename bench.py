@@ -324,6 +324,9 @@ def main():
     }
     if args.policy != "sequential":
         result["update_gram"] = update_gram_work(api, torch, bank, snap, seg_k, seg_v, run_prm, ws, N, d, upd_ms)
+    else:
+        # the walk offers the N candidates one per step: latency per step, not a roofline, bounds it
+        result["sequential"] = {"steps_per_update": N, "update_us_per_step": round(upd_ms * 1e3 / N, 3)}
     if not args.no_sink_attention:
         result["sink_attention"] = sink_attention(api, synth, torch)
     if not args.no_rollout_block:
