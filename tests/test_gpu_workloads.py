@@ -246,3 +246,54 @@ def test_interface_limits():
             assert not bad, f"{ctx} head {h}: differs from the oracle in {bad}"
         _properties(bank, out, prm, m_prev, base_prev, hist_k, hist_v, cfg.group_size, N, ctx)
         print(f"  block {t}: r* {step['r_star'][0]} occupancy {[int(x) for x in bank.occupancy.cpu()]} ok", flush=True)
+
+
+def test_single_layer_sequential_full_size():
+    """The within-block sequential competition at the size the benchmark times
+    (12 banks in one group, budget 4,680, banks filled by the empty-bank rule,
+    then 4,680 candidates with 30% near-duplicates offered one per step), as one
+    update call: the number of taken steps and, per bank, the order, scores,
+    released and admitted lists and the committed bank bytes must hash to the
+    digests the oracle wrote for the same inputs
+    (tests/golden/make_sequential_digests.py)."""
+    path = os.path.join(GOLDEN, "sequential_single_layer.json")
+    if not os.path.exists(path):
+        pytest.skip("oracle digests for the sequential single_layer run not generated")
+    with open(path) as f:
+        ref = json.load(f)
+    cfg = synth.WORKLOADS["single_layer"]
+    H, M, N, d = cfg.heads, cfg.budget, cfg.n_cand, cfg.d
+    print("sequential single_layer: build the case", flush=True)
+    case = synth.single_update_case(cfg)
+    bank = api.Bank(H, M, d, dtype=torch.bfloat16, group_size=cfg.group_size)
+    api.update_bank(bank, dev(case["init_K"], "bf16"), dev(case["init_V"], "bf16"), 0,
+                    api.Params(sigma2_log2=cfg.sigma2_log2))
+    torch.cuda.synchronize()
+    i64 = lambda t: t.cpu().numpy().astype(np.int64)
+    for b in range(H):
+        m = int(bank.occupancy[b])
+        got = {"m": m, "rho": digest(i64(bank.rho[b, :m]), np.int64), "base": digest(i64(bank.base[b, :m]), np.int64),
+               "prov": digest(i64(bank.prov[b, :m]), np.int64)}
+        assert got == ref["init"][b], f"initial bank {b}"
+    print("sequential single_layer: update", flush=True)
+    prm = api.Params(sigma2_log2=cfg.sigma2_log2, flags=api.POLICY_SEQUENTIAL)
+    out = api.UpdateOut(bank, N, trace=True)
+    api.update_bank(bank, dev(case["seg_K"], "bf16"), dev(case["seg_V"], "bf16"), 1, prm, out=out)
+    torch.cuda.synchronize()
+    assert int(out.r_star[0].item()) == ref["steps_taken"]
+    for b in range(H):
+        m = int(bank.occupancy[b])
+        ne, na = int(out.n_evicted[b]), int(out.n_admitted[b])
+        got = {
+            "m_after": m, "n_evicted": ne, "n_admitted": na,
+            "order": digest(out.order[b, :N].cpu().numpy(), np.int32),
+            "score_q": digest(i64(out.score_q[b, :N]), np.int64),
+            "evicted": digest(out.evicted[b, :ne].cpu().numpy(), np.int32),
+            "admitted": digest(out.admitted[b, :na].cpu().numpy(), np.int32),
+            "prov": digest(i64(bank.prov[b, :m]), np.int64), "rho": digest(i64(bank.rho[b, :m]), np.int64),
+            "base": digest(i64(bank.base[b, :m]), np.int64),
+            "knorm": digest(bank.knorm[b, :m].cpu().numpy(), np.float32),
+            "k": digest(host(bank.k[b, :m]), np.float32), "v": digest(host(bank.v[b, :m]), np.float32),
+        }
+        bad = [k for k in got if got[k] != ref["heads"][b][k]]
+        assert not bad, f"bank {b}: {bad}"
