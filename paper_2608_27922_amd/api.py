@@ -3,6 +3,18 @@
 Argument marshalling only: torch tensors supply device memory and the current
 HIP stream; every step of the hot path runs in the library's kernels.  There is
 no fallback: if the library has not been built, loading raises.
+
+Typical use (bf16 banks, one layer of 12 heads sharing the admitted prefix):
+
+    bank = Bank(12, 4680, 128, dtype=torch.bfloat16, group_size=12)
+    prm = Params(sigma2_log2=6)                      # sigma^2 = 64, p = 2, tau = 2
+    ws = alloc_workspace(bank, 4680, prm.flags)      # reuse across updates
+    out = UpdateOut(bank, 4680)                      # r*, admitted / evicted lists
+    update_bank(bank, seg_k, seg_v, block_id, prm, workspace=ws, out=out)
+    o = bank_attention(bank, q, win_k, win_v)        # queries over bank + window
+
+Policy variants are Params.flags bits (POLICY_*); the sequential competition
+needs the larger workspace that alloc_workspace(bank, n, flags) sizes.
 """
 
 from __future__ import annotations
