@@ -148,9 +148,10 @@ typedef struct {
 #define DKV_POLICY_DENSEST_ONLY 0x4u
 #define DKV_POLICY_SOURCE_FILL 0x8u
 #define DKV_POLICY_KV_DESCRIPTOR 0x10u
-/* Within-block sequential competition (Supp. E, "Within-block competition":
- * sequential density-gated admission, earlier candidates immediately affect
- * later ones).  The candidates keep the order above, fixed at the start of the
+/* Within-block sequential competition (Supp. E, "Within-block competition";
+ * Supp. C, "Insertion hysteresis"): candidates are admitted one at a time, each
+ * tested against the bank as the previous admissions of the same block left
+ * it.  The candidates keep the order above, fixed at the start of the
  * block, and are offered one at a time: step j tests the j-th candidate x of
  * every bank of the group as a one-candidate prefix against that bank as it is
  * at that step (earlier admissions included, with exactly maintained

@@ -77,9 +77,10 @@ V5  kv_descriptor: the retention geometry uses the concatenated vector [k; v]
     for every density, score and crossing; attention and the stored rows are
     unchanged.  C0 then applies to the values too (the synthetic values of
     this mode are drawn on the key grid).
-V6  sequential: within-block competition (Supp. E, "Within-block competition":
-    sequential density-gated admission, earlier candidates immediately affect
-    later ones).  Reading: the candidates keep the order of C6 (or V1), fixed
+V6  sequential: within-block competition (Supp. E, "Within-block competition";
+    Supp. C, "Insertion hysteresis"; Sec. 4.5): admission one candidate at a
+    time, each tested against the bank that the earlier candidates of the same
+    block have already changed.  Reading: the candidates keep the order of C6 (or V1), fixed
     at the start of the block, and are taken one at a time.  Step j tests the
     j-th candidate x of every head as a one-candidate prefix against that
     head's current bank, which already holds the candidates admitted at

@@ -55,6 +55,8 @@ def update(bank, cands, M, sigma2=1, p=1, tau=F(2), delta=F(1, 10 ** 6), block_i
         proj.append(pr)
         c.append(sum(1 for i in range(m) if pr[i] / bank[i]["b"] >= tau))
     e = [max(0, m + r - M) for r in range(R + 1)]
+    # first tested prefix length at which each state violates, R + 1 if none
+    first = [next((r for r in range(R + 1) if proj[r][i] / bank[i]["b"] >= tau), R + 1) for i in range(m)]
     feas = [r for r in range(R + 1) if c[r] <= e[r]]
     if r_star is None:
         r_star = max(feas) if feas else 0
@@ -87,7 +89,7 @@ def update(bank, cands, M, sigma2=1, p=1, tau=F(2), delta=F(1, 10 ** 6), block_i
         if s["b"] is None or refresh_base:
             s["b"] = max(s["rho"], delta)
     info = dict(r_star=r_star, pi=pi, scores=scores, c=c, e=e, evicted=evict, admitted=admitted,
-                violators=viol, projected=pr)
+                violators=viol, projected=pr, first_violation=first)
     return new_bank, info
 
 
@@ -122,6 +124,8 @@ def update_sequential(banks, cands, Ms, sigma2=1, p=1, tau=F(2), delta=F(1, 10 *
         orders[h] = list(range(N)) if source_order else sorted(range(N), key=lambda x: (sc[x], x))
     work = {h: [{"key": s["key"], "b": s["b"], "prov": s["prov"]} for s in banks[h]] for h in live}
     steps = []
+    counts = {h: [] for h in live}          # violators of every live head at every step
+    released = {h: set() for h in live}     # slots whose pre-block occupant was released
     for j in range(N):
         tests, ok = {}, bool(live)
         for h in live:
@@ -131,6 +135,7 @@ def update_sequential(banks, cands, Ms, sigma2=1, p=1, tau=F(2), delta=F(1, 10 *
             viol = [i for i in range(len(bank)) if pr[i] / bank[i]["b"] >= tau]
             e = max(0, len(bank) + 1 - Ms[h])
             tests[h] = (x, pr, viol, e)
+            counts[h].append(len(viol))
             ok = ok and len(viol) <= e
         steps.append(ok)
         if not ok:
@@ -145,6 +150,8 @@ def update_sequential(banks, cands, Ms, sigma2=1, p=1, tau=F(2), delta=F(1, 10 *
             else:
                 t = len(bank)
                 bank.append(None)
+            if t < len(bank) and bank[t] is not None and bank[t]["prov"] >> 32 != block_id:
+                released[h].add(t)
             bank[t] = {"key": cands[h][x], "b": None, "prov": (block_id << 32) | x}
             bank[t]["b"] = max(phi([s["key"] for s in bank], t, sigma2, p), delta)
     for h in live:
@@ -154,4 +161,5 @@ def update_sequential(banks, cands, Ms, sigma2=1, p=1, tau=F(2), delta=F(1, 10 *
             if refresh_base:
                 s["b"] = max(s["rho"], delta)
         out[h] = work[h]
-    return out, dict(steps=steps, orders=orders)
+    return out, dict(steps=steps, orders=orders, counts=counts,
+                     released={h: sorted(released[h]) for h in live})

@@ -1,18 +1,25 @@
 """Stored oracle results for the full-size 30-layer x 12-head rollout workloads.
 
-The oracle needs minutes per block for a whole layer at budgets of 9,360 and
-18,720 tokens, far too long for a test that holds a GPU.  This script runs it
-once, on the CPU, over one sampled layer of each workload and stores, per block
-and per head, the scalars of the update (r*, occupancy, evictions, admissions)
-and SHA-256 digests of every array the GPU must reproduce bit for bit (candidate
-order, scores, first crossings, projected densities, eviction and admission
-lists, and the committed bank: provenance, density, baseline, norms, keys,
-values), plus the fp64 attention of sampled query rows after the last block.
+The oracle needs one to two minutes per block for a whole layer at budgets of
+9,360 and 18,720 tokens, far too long for a test that holds a GPU.  This script
+runs it once, on the CPU, over sampled layers of each workload at the stated
+length (every block of the run) and stores, per block and per head, the scalars
+of the update (r*, occupancy, evictions, admissions) and SHA-256 digests of
+every array the GPU must reproduce bit for bit (candidate order, scores, first
+crossings, projected densities, eviction and admission lists, and the committed
+bank: provenance, density, baseline, norms, keys, values), plus the fp64
+attention of sampled query rows after the last block.
+
+Groups of heads that share no prefix (the head-wise workload runs every head as
+its own group) are independent, so they run in parallel worker processes.
 
 Inputs are the seeded HeadStream draws of the input generator module; nothing
 here reads a GPU result.  Run from the repository root:
 
-    python tests/golden/make_rollout_digests.py [workload ...]
+    python tests/golden/make_rollout_digests.py [--jobs J] [workload[:layer] ...]
+
+Output: tests/golden/rollout_<workload>_L<layer>.json and
+tests/golden/rollout_<workload>_L<layer>_attention.npy.
 """
 
 import hashlib
@@ -20,13 +27,18 @@ from typing import Dict
 
 import numpy as np
 
-# name -> (blocks, sampled layer, heads whose attention rows are stored)
+# name -> (blocks, sampled layers, heads whose attention rows are stored)
 RUNS: Dict[str, tuple] = {
-    "rollout": (8, 29, (0, 5, 11)),
-    "long_rollout": (12, 0, (0, 5, 11)),
-    "headwise_budgets": (8, 17, (0, 1, 6, 7)),
+    "rollout": (20, (0, 29), (0, 5, 11)),
+    "long_rollout": (80, (0,), (0, 5, 11)),
+    "headwise_budgets": (160, (17,), (0, 1, 6, 7)),
 }
 ATT_ROWS = 32
+
+
+def cases():
+    """(workload, layer) pairs with stored digests."""
+    return [(name, layer) for name, (_, layers, _) in RUNS.items() for layer in layers]
 
 
 def digest(a, dtype) -> str:
@@ -61,51 +73,88 @@ def head_entry(hr, nb, m_before: int, n: int):
     }
 
 
-def run(name: str, path_prefix: str):
-    import json
-
+def run_group(args):
+    """The whole run of one group of heads of the sampled layer: per block the
+    group's r* and head entries, then the fp64 attention rows of its heads that
+    are in the stored set."""
     from oracle import BankState, Params, attention, update_layer
     from paper_2608_27922_amd import synth
 
-    blocks, layer, att_heads = RUNS[name]
+    name, layer, heads = args
+    blocks, _, att_heads = RUNS[name]
+    cfg = synth.WORKLOADS[name]
+    H = cfg.heads
+    budgets = synth.budgets(cfg)[layer * H:(layer + 1) * H]
+    prm = Params(sigma2_log2=cfg.sigma2_log2)
+    streams = [synth.HeadStream(cfg, layer, h) for h in heads]
+    banks = [BankState.empty(int(budgets[h]), cfg.d) for h in heads]
+    steps = []
+    for t in range(blocks):
+        K, V = layer_block(cfg, streams, t)
+        nb, rec = update_layer(banks, [K[j].astype(np.float64) for j in range(len(heads))],
+                               [V[j] for j in range(len(heads))], t, prm)
+        steps.append((rec.r_star, [head_entry(rec.heads[j], nb[j], banks[j].m, cfg.n_cand)
+                                   for j in range(len(heads))]))
+        banks = nb
+        print(f"{name} L{layer} heads {heads[0]}-{heads[-1]} block {t}: r* {rec.r_star} "
+              f"occupancy {[b.m for b in banks][:4]}", flush=True)
+    rows = attention_rows(cfg.n_query)
+    att = {}
+    for j, h in enumerate(heads):
+        if h in att_heads:
+            s = streams[j]
+            att[h] = attention(s.queries(blocks)[rows], banks[j].K, banks[j].V, s.keys(blocks, cfg.n_window),
+                               s.values(blocks, cfg.n_window), 1.0 / np.sqrt(cfg.d))
+    return heads, steps, att
+
+
+def run(name: str, layer: int, path_prefix: str, jobs: int = 1):
+    import json
+    from concurrent.futures import ProcessPoolExecutor
+
+    from paper_2608_27922_amd import synth
+
+    blocks, _, att_heads = RUNS[name]
     cfg = synth.WORKLOADS[name]
     H, gs = cfg.heads, cfg.group_size
     budgets = synth.budgets(cfg)[layer * H:(layer + 1) * H]
-    prm = Params(sigma2_log2=cfg.sigma2_log2)
-    streams = [synth.HeadStream(cfg, layer, h) for h in range(H)]
-    banks = [BankState.empty(int(budgets[h]), cfg.d) for h in range(H)]
+    groups = [(name, layer, tuple(range(g0, g0 + gs))) for g0 in range(0, H, gs)]
+    if jobs > 1 and len(groups) > 1:
+        with ProcessPoolExecutor(max_workers=min(jobs, len(groups))) as ex:
+            results = list(ex.map(run_group, groups))
+    else:
+        results = [run_group(g) for g in groups]
     out = {"workload": name, "layer": layer, "blocks": blocks, "budgets": [int(b) for b in budgets],
            "group_size": gs, "steps": []}
     for t in range(blocks):
-        K, V = layer_block(cfg, streams, t)
-        new, step = [None] * H, {"r_star": [], "heads": []}
-        for g0 in range(0, H, gs):
-            idx = range(g0, g0 + gs)
-            nb, rec = update_layer([banks[h] for h in idx], [K[h].astype(np.float64) for h in idx],
-                                   [V[h] for h in idx], t, prm)
-            step["r_star"].append(rec.r_star)
-            for j, h in enumerate(idx):
-                new[h] = nb[j]
-                step["heads"].append(head_entry(rec.heads[j], nb[j], banks[h].m, cfg.n_cand))
-        banks = new
+        step = {"r_star": [], "heads": []}
+        for heads, steps, _ in results:
+            r_star, entries = steps[t]
+            step["r_star"].append(r_star)
+            step["heads"].extend(entries)
         out["steps"].append(step)
-        print(f"{name} block {t}: r* {step['r_star'][:4]} occupancy {[b.m for b in banks]}", flush=True)
-    q = np.stack([s.queries(blocks) for s in streams])
-    wk = np.stack([s.keys(blocks, cfg.n_window) for s in streams])
-    wv = np.stack([s.values(blocks, cfg.n_window) for s in streams])
-    rows = attention_rows(cfg.n_query)
-    ref = np.stack([attention(q[h][rows], banks[h].K, banks[h].V, wk[h], wv[h], 1.0 / np.sqrt(cfg.d))
-                    for h in att_heads])
+    att = {}
+    for _, _, a in results:
+        att.update(a)
     out["attention_heads"] = list(att_heads)
-    with open(f"{path_prefix}{name}.json", "w") as f:
+    with open(f"{path_prefix}{name}_L{layer}.json", "w") as f:
         json.dump(out, f, indent=0)
-    np.save(f"{path_prefix}{name}_attention.npy", ref)
+    np.save(f"{path_prefix}{name}_L{layer}_attention.npy", np.stack([att[h] for h in att_heads]))
 
 
 if __name__ == "__main__":
+    import argparse
     import os
     import sys
     here = os.path.dirname(os.path.abspath(__file__))
     sys.path.insert(0, os.path.dirname(os.path.dirname(here)))
-    for nm in sys.argv[1:] or list(RUNS):
-        run(nm, os.path.join(here, "rollout_"))
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--jobs", type=int, default=1, help="worker processes for independent head groups")
+    ap.add_argument("which", nargs="*", help="workload or workload:layer (default: every stored case)")
+    a = ap.parse_args()
+    todo = []
+    for w in a.which or [n for n in RUNS]:
+        nm, _, ly = w.partition(":")
+        todo += [(nm, int(ly))] if ly else [(nm, L) for L in RUNS[nm][1]]
+    for nm, ly in todo:
+        run(nm, ly, os.path.join(here, "rollout_"), a.jobs)

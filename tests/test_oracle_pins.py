@@ -168,6 +168,8 @@ def test_hand_examples_exact_bruteforce(case):
         assert info["pi"] == case["pi"]
     if "c" in case:
         assert info["c"] == case["c"]
+    if "first_cross" in case:
+        assert info["first_violation"] == case["first_cross"]
     if "scores" in case:
         assert info["scores"] == [frac(s) for s in case["scores"]]
     assert [float(s["key"][0]) for s in new] == [float(k) for k in case["final_keys"]]
@@ -194,6 +196,8 @@ def test_hand_examples_oracle(case):
         assert list(hr.pi) == case["pi"]
     if "c" in case:
         assert list(hr.c) == case["c"]
+    if "first_cross" in case:
+        assert list(hr.first_cross) == case["first_cross"]
     assert list(new.K[:, 0]) == [float(k) for k in case["final_keys"]]
     # values moved unchanged with their keys
     assert np.array_equal(new.V[new.prov >> 32 == 2, 0] - 1000.0,
