@@ -3,23 +3,31 @@
 
 A step is one pass of the whole hot path over one block: the density-guided
 update of every (layer, head) bank from the block's candidates, then the
-attention of the next block's queries over the retained bank plus the local
-window.  Workload (default): one layer x 12 heads, d = 128, bf16, per-head
-budget 4,680, banks start full (built by the empty-bank rule), one incoming
-segment of 4,680 candidates with 30% near-duplicates, 4,680 queries over
-bank + a 4,680-token window.  Every step restores the pre-update bank with one
-device-to-device copy of the packed bank state (inside the timed region) so
-that all steps do the same work.
+attention of the next block's queries over the retained bank plus that
+block's tokens as the local window.
 
-Prints one JSON line.  value = candidate tokens per second per layer-head for
-the whole step (update + attention); the update-only rate and the attention
-TFLOP/s are reported beside it, with the roofline of the dominant kernel and
-the CPU oracle timed on a bounded sample.  update_gram gives the update's
-algorithmic Gram work (pairs of the score, prefix, partial-tile and maintenance
-stages at 2 d flops each) and its rate against the bf16 MFMA peak over the
-whole update time.  Two extra fields time the sink +
-window + bank attention at the paper's deployment shape and one block of the
-rollout configuration at full scale (360 banks in one launch).
+Default workload: the long rollout, 30 layers x 12 heads (360 banks, one
+launch per call), d = 128, bf16, per-head budget 18,720, 80 blocks of 4,680
+candidates, 4,680 queries per block over bank + 4,680-token window, 256
+clusters with 16 active per block and a recurring active set every 10 blocks.
+Every input block of the run is drawn on the device before anything is timed
+(about 104 GB of the 288 GB of HBM).  The rollout starts from empty banks and
+runs its blocks in order: the first `--warmup` blocks are untimed warm-up, the
+next `--steps` blocks are the timed region (bracketed by device
+synchronisations), the remaining blocks complete the rollout; when warm-up +
+steps exceed the rollout's length it starts again from empty banks.  HIP events
+on the stream time the update and the attention of every block of the first
+full pass: the record reports block 0 (the empty-bank update) separately and
+the median and total over the others.
+
+value = candidate tokens per second per layer-head over the timed steps (every
+bank processes N candidates per step, concurrently).  Beside it: the update
+and attention times, the attention's roofline (the dominant kernel: one
+k_attn_mfma launch per attention call), the update's algorithmic Gram work
+against the bf16 MFMA peak, and the CPU oracle timed on a bounded sample of
+the same workload.  `--workload single_layer` (or `tiny`) times one update
+into full banks plus one attention instead, with the pre-update bank restored
+before every step.
 """
 
 import argparse
@@ -36,7 +44,8 @@ PEAK_BF16_TFLOPS = 2500.0
 PEAK_HBM_GBS = 8000.0
 ROOT = os.path.dirname(os.path.abspath(__file__))
 ATTN_SOURCE = os.path.join(ROOT, "paper_2608_27922_amd", "csrc", "dkv_attention.hip")
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "k_attn_mfma_single_layer_traffic.md")
+METRIC = "bank-update tokens/s per layer-head + bank-attention TFLOP/s (roofline %)"
+ROLLOUTS = ("rollout", "long_rollout", "headwise_budgets")
 # dkv_params.flags of each policy ablation (Table 1(b); independent per-head = group size 1)
 # (kv_descriptor: the [K; V] retention geometry; the workload's values are not on the key grid, so
 # this mode is a timing run only, its decisions carry the fp32 rounding of the descriptor Gram;
@@ -49,31 +58,31 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="single_layer", help="tiny or single_layer")
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="long_rollout",
+                    help="long_rollout (default), rollout, headwise_budgets, single_layer or tiny")
+    ap.add_argument("--blocks", type=int, default=0,
+                    help="rollout workloads: blocks per pass (default: the workload's full length)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--policy", default="default", choices=sorted(POLICIES),
                     help="policy ablation of Table 1(b) run by the update (default: the paper's policy)")
-    ap.add_argument("--cpu-heads", type=int, default=12,
-                    help="heads in the oracle sample (12 = the whole single_layer step, about 10 s on 16 host threads)")
+    ap.add_argument("--cpu-heads", type=int, default=0,
+                    help="heads in the oracle sample (default: 3 for the rollouts, 12 for single_layer)")
     ap.add_argument("--no-sink-attention", action="store_true",
-                    help="skip the extra measurement of the sink + window + bank attention at the deployment shape")
-    ap.add_argument("--no-rollout-block", action="store_true",
-                    help="skip the extra measurement of one rollout block at full scale (360 banks)")
-    ap.add_argument("--rollout-block-only", action="store_true",
-                    help="run only the full-scale rollout block and print its figures (for profiling)")
+                    help="single_layer: skip the sink + window + bank attention at the deployment shape")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
                     help="also run a plain elementwise copy (negation) of this many MiB: the known-size "
                          "reference that scales the HBM byte counters")
     return ap.parse_args()
 
 
-def measured_traffic():
-    """HBM bytes per launch of the attention kernel from the committed counter summary
-    (FETCH_SIZE + WRITE_SIZE, each scaled by the copy-kernel calibration), or None when
-    the summary is absent or the kernel source changed after the counters were taken."""
+def measured_traffic(workload):
+    """HBM bytes per launch of the attention kernel on this workload from the committed
+    counter summary (FETCH_SIZE + WRITE_SIZE, each scaled by the copy-kernel
+    calibration), or None when the summary is absent or the kernel source changed
+    after the counters were taken."""
     try:
-        text = open(TRAFFIC_SUMMARY).read()
+        text = open(os.path.join(ROOT, "profiles", f"k_attn_mfma_{workload}_traffic.md")).read()
     except OSError:
         return None
     want = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
@@ -83,6 +92,243 @@ def measured_traffic():
     have = hashlib.sha256(open(ATTN_SOURCE, "rb").read()).hexdigest()
     return int(val.group(1)) if have == want.group(1) else None
 
+
+def host_info():
+    """What the oracle baseline ran on: CPU model, usable cores, BLAS library and threads."""
+    info = {"cpu_model": None, "affinity_cores": len(os.sched_getaffinity(0)), "numpy": np.__version__}
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                info["cpu_model"] = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        blas = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        info["blas"] = f"{blas.get('name')} {blas.get('version')}"
+    except Exception:  # noqa: BLE001 - report what is available
+        info["blas"] = None
+    try:
+        import threadpoolctl
+        pools = threadpoolctl.threadpool_info()
+        info["blas_threads"] = max((p["num_threads"] for p in pools if p.get("user_api") == "blas"), default=None)
+        info["openmp_threads"] = max((p["num_threads"] for p in pools if p.get("user_api") == "openmp"),
+                                     default=None)
+    except Exception:  # noqa: BLE001
+        info["blas_threads"] = info["openmp_threads"] = None
+    return info
+
+
+def blas_threads(n):
+    """Set the BLAS thread count explicitly for the oracle sample."""
+    try:
+        import threadpoolctl
+        return threadpoolctl.threadpool_limits(limits=n, user_api="blas")
+    except Exception:  # noqa: BLE001
+        return None
+
+
+def gram_pairs(m, N, R, r, e):
+    """Key-key weights per bank that the update needs (Supp. C cost paragraph): the
+    candidate scores (Eq. 6) m N; the prefix densities in score order (Eq. 8) m R;
+    exact maintenance: every survivor against the admitted and the evicted states
+    (m - e)(r + e), every admitted candidate against the smaller of the evicted set
+    and the survivors r min(e, m - e) (its weights to the whole old bank are the
+    score's column sums), and the distinct pairs among the admitted r (r - 1) / 2."""
+    surv = m - e
+    return m * N + m * R + surv * (r + e) + r * np.minimum(e, surv) + r * (r - 1) // 2
+
+
+# ----------------------------------------------------------------------------
+# Rollout workloads (the default)
+# ----------------------------------------------------------------------------
+
+class _Out:
+    """dkv_update_out with only r_star and n_evicted written, into history rows."""
+
+    def __init__(self, api, r_star, n_evicted):
+        self.api, self.r_star, self.n_evicted = api, r_star, n_evicted
+
+    def c(self):
+        return self.api.DkvUpdateOut(self.r_star.data_ptr(), None, self.n_evicted.data_ptr(),
+                                     None, None, None, None, None, None)
+
+
+def rollout_cpu_baseline(cfg, n_heads):
+    """The oracle, as it stands, on a bounded sample of the rollout: the first two
+    updates (the empty-bank block, then one block into the half-filled banks) of
+    layer 0, `n_heads` heads as one group, and the attention of the next block's
+    queries for those heads (NumPy draws of the same recipe)."""
+    from oracle import BankState, Params, attention, update_layer
+    from paper_2608_27922_amd import synth
+    threads = len(os.sched_getaffinity(0))
+    lim = blas_threads(threads)
+    prm = Params(sigma2_log2=cfg.sigma2_log2)
+    budgets = synth.budgets(cfg)[:n_heads]
+    streams = [synth.HeadStream(cfg, 0, h) for h in range(n_heads)]
+    banks = [BankState.empty(int(budgets[h]), cfg.d) for h in range(n_heads)]
+    gs = min(cfg.group_size, n_heads)
+    t0 = time.perf_counter()
+    for t in range(2):
+        K = [s.keys(t, cfg.n_cand).astype(np.float64) for s in streams]
+        V = [s.values(t, cfg.n_cand) for s in streams]
+        new = []
+        for g0 in range(0, n_heads, gs):
+            nb, _ = update_layer(banks[g0:g0 + gs], K[g0:g0 + gs], V[g0:g0 + gs], t, prm)
+            new += nb
+        banks = new
+    t1 = time.perf_counter()
+    for h, s in enumerate(streams):
+        attention(s.queries(2), banks[h].K, banks[h].V, s.keys(2, cfg.n_window), s.values(2, cfg.n_window),
+                  1.0 / np.sqrt(cfg.d))
+    t2 = time.perf_counter()
+    info = host_info()
+    del lim
+    per_head = (t2 - t0) / n_heads
+    return {"value": 2 * cfg.n_cand / per_head, "unit": "tokens/s per layer-head", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{cfg.name}, layer 0, heads 0-{n_heads - 1} as one group: blocks 0 and 1 "
+                      f"({cfg.n_cand} candidates each; the empty-bank rule, then an update into banks of "
+                      f"{banks[0].m} states) plus one attention of {cfg.n_query} queries over bank + "
+                      f"{cfg.n_window} window per head; updates {t1 - t0:.2f} s, attention {t2 - t1:.2f} s; "
+                      "NumPy draws of the same recipe",
+            "host": info}
+
+
+def run_rollout(args, api, synth, torch):
+    cfg = synth.WORKLOADS[args.workload]
+    L, H, d, N, W, nq = cfg.layers, cfg.heads, cfg.d, cfg.n_cand, cfg.n_window, cfg.n_query
+    B, gs = L * H, cfg.group_size
+    G = B // gs
+    T = args.blocks or cfg.blocks
+    budgets = synth.budgets(cfg)
+    Mcap = int(budgets.max())
+    dev = torch.device("cuda:0")
+    bank = api.Bank(B, Mcap, d, dtype=torch.bfloat16, group_size=gs, budget=torch.from_numpy(budgets))
+    prm = api.Params(sigma2_log2=cfg.sigma2_log2, flags=POLICIES[args.policy])
+    ws = api.alloc_workspace(bank, N, prm.flags)
+    # every input of the pass, resident in HBM before anything is timed:
+    # block t's K/V are the candidates of update t and the window of attention t - 1
+    gen = synth.TorchRollout(cfg, dev)
+    kv = [(gen.keys(t, N), gen.values(t, N)) for t in range(T + 1)]
+    qs = [gen.queries(t) for t in range(1, T + 1)]
+    del gen
+    out = torch.empty(B, nq, d, dtype=torch.bfloat16, device=dev)
+    rs_hist = torch.zeros(T, G, dtype=torch.int32, device=dev)
+    ne_hist = torch.zeros(T, B, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    # one small update + attention first, so the first rollout block pays no one-off start-up cost
+    wb = api.Bank(gs, 64, d, dtype=torch.bfloat16, group_size=gs)
+    api.update_bank(wb, kv[0][0][:gs, :64].contiguous(), kv[0][1][:gs, :64].contiguous(), 0, prm)
+    api.bank_attention(wb, qs[0][:gs, :64].contiguous(), None, None)
+    torch.cuda.synchronize()
+    del wb
+
+    def block(t, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        api.update_bank(bank, kv[t][0], kv[t][1], t, prm, workspace=ws,
+                        out=_Out(api, rs_hist[t], ne_hist[t]))
+        if ev is not None:
+            ev[1].record(stream)
+        api.bank_attention(bank, qs[t], kv[t + 1][0], kv[t + 1][1], out=out)
+        if ev is not None:
+            ev[2].record(stream)
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(T)]
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # (pass, block) in execution order: warm-up, then the timed steps, and at least one whole pass
+    total = args.warmup + args.steps
+    schedule = [(i // T, i % T) for i in range(max(total, T))]
+    for i, (p, t) in enumerate(schedule):
+        if t == 0:
+            bank.occupancy.zero_()          # a pass starts from empty banks
+        if i == args.warmup:
+            torch.cuda.synchronize()
+            t_start.record(stream)
+        block(t, evs[t] if p == 0 else None)
+        if i == total - 1:
+            t_end.record(stream)
+    torch.cuda.synchronize()
+    timed = [t for _, t in schedule[args.warmup:total]]
+    total_ms = t_start.elapsed_time(t_end)
+    ms_step = total_ms / args.steps
+    upd = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    att = np.array([e[1].elapsed_time(e[2]) for e in evs])
+
+    # occupancy before every block, r* and evictions of every block of the first pass
+    rs = np.repeat(rs_hist.cpu().numpy().astype(np.int64), gs, axis=1)      # [T, B]
+    ne = ne_hist.cpu().numpy().astype(np.int64)
+    Mb = np.minimum(budgets.astype(np.int64), Mcap)
+    m = np.zeros((T + 1, B), np.int64)
+    for t in range(T):
+        m[t + 1] = m[t] + rs[t] - ne[t]
+    R = np.minimum(N, np.minimum.reduceat(Mb, np.arange(0, B, gs))).repeat(gs)
+    pairs = np.stack([gram_pairs(m[t], N, R, rs[t], ne[t]) for t in range(T)])     # [T, B]
+    gram_flops = 2.0 * d * pairs.sum(1)
+    att_flops = 4.0 * nq * d * (m[1:] + W).sum(1)                                     # [T]
+    att_tf = att_flops / (att * 1e-3) / 1e12
+    gram_tf = gram_flops / (upd * 1e-3) / 1e12
+    tb = np.array(timed)
+    att_tf_timed = float(att_flops[tb].sum() / (att[tb].sum() * 1e-3) / 1e12)
+    rest = np.arange(1, T)
+    commit_bytes = (rs * (4 * d + 28)).sum(1) * 2    # admitted K/V rows + metadata, read + written
+    result = {
+        "metric": METRIC,
+        "value": round(N / (ms_step * 1e-3), 1),
+        "unit": "tokens/s per layer-head",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": cfg.dtype, "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: {L} layers x {H} heads ({B} banks, one launch per call), d={d}, "
+                               f"{cfg.dtype}, budget {cfg.budget if not cfg.ragged else list(cfg.ragged)}, "
+                               f"{T} blocks of {N} candidates, {nq} queries per block over bank + {W}-token "
+                               f"window, {cfg.clusters} clusters"
+                               + (f", {cfg.active} active, recurring every {cfg.revisit} blocks" if cfg.active else "")
+                               + (f", centre drift {cfg.drift}" if cfg.drift else ""),
+                   "banks": B, "group_size": gs, "candidates": N, "budget": int(Mcap), "blocks": T,
+                   "queries": nq, "window": W, "head_dim": d, "policy": args.policy,
+                   "timed_blocks": [int(tb.min()), int(tb.max())]},
+        "update_ms": round(float(upd[tb].mean()), 4),
+        "attention_ms": round(float(att[tb].mean()), 4),
+        "attention_tflops": round(att_tf_timed, 2),
+        "roofline": {"bound": "mfma", "kernel": "k_attn_mfma (bank attention)", "achieved": round(att_tf_timed, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(att_tf_timed / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic(cfg.name)},
+        "rollout": {
+            "blocks": T,
+            "block0": {"update_ms": round(float(upd[0]), 4), "attention_ms": round(float(att[0]), 4)},
+            "median_ms": round(float(np.median(upd[rest] + att[rest])), 4) if T > 1 else None,
+            "median_update_ms": round(float(np.median(upd[rest])), 4) if T > 1 else None,
+            "median_attention_ms": round(float(np.median(att[rest])), 4) if T > 1 else None,
+            "total_ms": round(float((upd + att).sum()), 3),
+            "total_update_ms": round(float(upd.sum()), 3),
+            "total_attention_ms": round(float(att.sum()), 3),
+            "update_tokens_per_s_per_layer_head": round(T * N / (upd.sum() * 1e-3), 1),
+            "attention_tflops": round(float(att_flops.sum() / (att.sum() * 1e-3) / 1e12), 2),
+            "update_gram_tflop": round(float(gram_flops.sum() / 1e12), 3),
+            "update_gram_tflops": round(float(gram_flops.sum() / (upd.sum() * 1e-3) / 1e12), 2),
+            "update_gram_frac_of_bf16_peak": round(float(gram_flops.sum() / (upd.sum() * 1e-3) / 1e12)
+                                                   / PEAK_BF16_TFLOPS, 4),
+            "median_update_gram_frac_of_bf16_peak": round(float(np.median(gram_tf[rest])) / PEAK_BF16_TFLOPS, 4)
+            if T > 1 else None,
+            "median_attention_frac_of_bf16_peak": round(float(np.median(att_tf[rest])) / PEAK_BF16_TFLOPS, 4)
+            if T > 1 else None,
+            "r_star_mean_per_block": [round(float(x), 1) for x in rs_hist.float().mean(1).cpu().numpy()],
+            "occupancy_mean_after": round(float(m[T].mean()), 1),
+            "commit_bytes_total": int(commit_bytes.sum()),
+        },
+    }
+    del kv, qs, out, bank, ws
+    torch.cuda.empty_cache()
+    return result
+
+
+# ----------------------------------------------------------------------------
+# Single-update workloads (tiny, single_layer)
+# ----------------------------------------------------------------------------
 
 def sink_attention(api, synth, torch, steps=10):
     """densitykv_bank_attention_sink at the paper's deployment context (Supp. D): 12 heads,
@@ -118,102 +364,12 @@ def sink_attention(api, synth, torch, steps=10):
             "ms": round(ms, 4), "tflops": round(tf, 2), "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4)}
 
 
-def update_gram_work(api, torch, bank, snap, seg_k, seg_v, prm, ws, N, d, upd_ms):
-    """Algorithmic Gram work of the timed update and its rate against the bf16 MFMA
-    peak: per bank m*N pairs for the candidate scores (Eq. 6), m*R for the prefix
-    densities (Eq. 8, R = min(N, M)), m*64 for the partial tile at r*, and
-    (m + r*)*e + r*^2 for the density maintenance (Supp. C), at 2 d flops per pair;
-    m, r* and e are those of the timed update (rerun once with its outputs)."""
-    bank.restore(snap)
-    m0 = bank.occupancy.cpu().numpy().astype(np.int64)
-    M = bank.budget.cpu().numpy().astype(np.int64)
-    out = api.UpdateOut(bank, N)
-    api.update_bank(bank, seg_k, seg_v, 1, prm, workspace=ws, out=out)
-    torch.cuda.synchronize()
-    r = np.repeat(out.r_star.cpu().numpy().astype(np.int64), bank.gs)
-    e = out.n_evicted.cpu().numpy().astype(np.int64)
-    R = np.minimum(N, M)
-    pairs = m0 * N + m0 * R + m0 * np.minimum(64, R) + (m0 + r) * e + r * r
-    flops = 2.0 * d * float(pairs.sum())
-    tf = flops / (upd_ms * 1e-3) / 1e12
-    return {"pairs": int(pairs.sum()), "tflop": round(flops / 1e12, 4), "tflops": round(tf, 2),
-            "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4), "r_star": int(out.r_star.max().item()),
-            "evicted_per_bank": int(e.max())}
-
-
-def rollout_block(api, synth, torch, steps=3):
-    """One block of the rollout configuration at full scale: 30 layers x 12 heads
-    (360 banks, one launch), d = 128, bf16, budget 9,360, 4,680 candidates per
-    bank, 4,680 queries over bank + 4,680-token window.  Three blocks fill the
-    banks first (device-drawn, as the non-compared layers of the full-size
-    tests); each timed step restores that state, updates with block 3 and runs
-    the attention.  Timed with HIP events on the stream."""
-    cfg = synth.WORKLOADS["rollout"]
-    L, H, d, N, M, nq = cfg.layers, cfg.heads, cfg.d, cfg.n_cand, cfg.budget, cfg.n_query
-    B = L * H
-
-    def block(t, n, seed=0):
-        ks, vs = zip(*(synth.torch_layer_block(cfg, layer, t, n, "cuda", seed=seed) for layer in range(L)))
-        return torch.cat(ks).contiguous(), torch.cat(vs).contiguous()
-
-    bank = api.Bank(B, M, d, dtype=torch.bfloat16, group_size=cfg.group_size)
-    ws = api.alloc_workspace(bank, N)
-    prm = api.Params(sigma2_log2=cfg.sigma2_log2)
-    for t in range(3):
-        k, v = block(t, N)
-        api.update_bank(bank, k, v, t, prm, workspace=ws)
-    seg_k, seg_v = block(3, N)
-    q, _ = block(3, nq, seed=1)
-    del k, v
-    out = torch.empty_like(q)
-    upd = api.UpdateOut(bank, N)
-    torch.cuda.synchronize()
-    snap = bank.snapshot()
-    stream = torch.cuda.current_stream()
-    times = []
-    for it in range(steps + 1):
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
-        ev[0].record(stream)
-        bank.restore(snap)
-        ev[1].record(stream)
-        api.update_bank(bank, seg_k, seg_v, 3, prm, workspace=ws, out=upd)
-        ev[2].record(stream)
-        api.bank_attention(bank, q, seg_k, seg_v, out=out)
-        ev[3].record(stream)
-        torch.cuda.synchronize()
-        if it > 0:   # the first pass is a warm-up
-            times.append([ev[0].elapsed_time(ev[3]), ev[1].elapsed_time(ev[2]), ev[2].elapsed_time(ev[3])])
-    step_ms, upd_ms, att_ms = (float(np.mean(c)) for c in zip(*times))
-    m_after = bank.occupancy.cpu().numpy()
-    # algorithmic Gram work of the timed update (the same per-bank pair counts as update_gram)
-    r = np.repeat(upd.r_star.cpu().numpy().astype(np.int64), cfg.group_size)
-    e = upd.n_evicted.cpu().numpy().astype(np.int64)
-    bank.restore(snap)
-    m0 = bank.occupancy.cpu().numpy().astype(np.int64)
-    R = min(N, M)
-    gram_flops = 2.0 * d * float((m0 * N + m0 * R + m0 * min(64, R) + (m0 + r) * e + r * r).sum())
-    gram_tf = gram_flops / (upd_ms * 1e-3) / 1e12
-    flops = float(sum(4.0 * nq * (int(m) + N) * d for m in m_after))
-    tf = flops / (att_ms * 1e-3) / 1e12
-    res = {"context": f"rollout: {L} layers x {H} heads ({B} banks, one launch), d={d}, bf16, budget {M}, "
-                      f"block 3 ({N} candidates) into full banks, {nq} queries over bank + {N}-token window",
-           "ms_per_step": round(step_ms, 3), "update_ms": round(upd_ms, 3), "attention_ms": round(att_ms, 3),
-           "tokens_per_s_per_layer_head": round(N / (step_ms * 1e-3), 1),
-           "update_tokens_per_s_per_layer_head": round(N / (upd_ms * 1e-3), 1),
-           "attention_tflops": round(tf, 2), "attention_frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
-           "update_gram_tflop": round(gram_flops / 1e12, 3), "update_gram_tflops": round(gram_tf, 2),
-           "update_gram_frac_of_bf16_peak": round(gram_tf / PEAK_BF16_TFLOPS, 4),
-           "mean_r_star": round(float(upd.r_star.float().mean().item()), 1),
-           "mean_occupancy": round(float(m_after.mean()), 1)}
-    del bank, ws, snap, seg_k, seg_v, q, out
-    torch.cuda.empty_cache()
-    return res
-
-
-def cpu_baseline(case, cfg, n_heads):
+def single_cpu_baseline(case, cfg, n_heads):
     """The oracle, as it stands, on a bounded sample: one update + one attention for
     `n_heads` heads treated as one group (rank 0 only)."""
     from oracle import BankState, Params, attention, update_layer
+    threads = len(os.sched_getaffinity(0))
+    lim = blas_threads(threads)
     prm = Params(sigma2_log2=cfg.sigma2_log2)
     hs = range(n_heads)
     banks = [BankState.empty(cfg.budget, cfg.d) for _ in hs]
@@ -226,32 +382,19 @@ def cpu_baseline(case, cfg, n_heads):
     for h in hs:
         attention(case["q"][h], banks[h].K, banks[h].V, case["win_K"][h], case["win_V"][h], 1.0 / np.sqrt(cfg.d))
     t2 = time.perf_counter()
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    info = host_info()
+    del lim
     step_s = (t2 - t0) / n_heads  # per layer-head
     return {"value": cfg.n_cand / step_s, "unit": "tokens/s per layer-head", "cores": threads,
             "kind": "oracle",
             "sample": f"{n_heads} head(s) of the same workload: one update (N={cfg.n_cand} into a full bank of "
                       f"{cfg.budget}) + one attention ({cfg.n_query} queries over bank + {cfg.n_window} window), "
-                      f"update {t1 - t0:.2f} s, attention {t2 - t1:.2f} s"}
+                      f"update {t1 - t0:.2f} s, attention {t2 - t1:.2f} s",
+            "host": info}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
-                                   "(banks shard by layer without communication; see the design notes)"}))
-        sys.exit(2)
-    import torch
-    from paper_2608_27922_amd import api, synth
-
-    if args.rollout_block_only:
-        torch.cuda.set_device(0)
-        print(json.dumps({"rollout_block": rollout_block(api, synth, torch, steps=args.steps)}), flush=True)
-        return
+def run_single(args, api, synth, torch):
     cfg = synth.WORKLOADS[args.workload]
-    if not cfg.starts_full:
-        raise SystemExit("bench workload must be a single-update workload (tiny or single_layer)")
-    torch.cuda.set_device(0)
     dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     case = synth.single_update_case(cfg)
     to = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dt).cuda().contiguous()
@@ -266,14 +409,19 @@ def main():
     api.update_bank(bank, init_k, init_v, 0, prm, workspace=ws)   # starts full (empty-bank rule)
     torch.cuda.synchronize()
     snap = bank.snapshot()
+    m0 = bank.occupancy.cpu().numpy().astype(np.int64)
     out = torch.empty_like(q)
     stream = torch.cuda.current_stream()
+    G = B // cfg.group_size
+    rs_hist = torch.zeros(args.steps + 1, G, dtype=torch.int32, device="cuda")
+    ne_hist = torch.zeros(args.steps + 1, B, dtype=torch.int32, device="cuda")
 
-    def step(ev=None):
+    def step(k=None, ev=None):
         bank.restore(snap)
         if ev is not None:
             ev[0].record(stream)
-        api.update_bank(bank, seg_k, seg_v, 1, run_prm, workspace=ws)
+        o = _Out(api, rs_hist[k], ne_hist[k]) if k is not None else None
+        api.update_bank(bank, seg_k, seg_v, 1, run_prm, workspace=ws, out=o)
         if ev is not None:
             ev[1].record(stream)
         api.bank_attention(bank, q, wk, wv, out=out)
@@ -289,7 +437,7 @@ def main():
     torch.cuda.synchronize()
     t_start.record(stream)
     for k in range(args.steps):
-        step(evs[k])
+        step(k, evs[k])
     t_end.record(stream)
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
@@ -299,38 +447,68 @@ def main():
     m_after = bank.occupancy.cpu().numpy()
     att_flops = float(sum(4.0 * cfg.n_query * (int(m) + cfg.n_window) * d for m in m_after))
     att_tflops = att_flops / (att_ms * 1e-3) / 1e12
-    value = N / (ms_step * 1e-3)   # every bank processes N candidates per step, concurrently
+    r = np.repeat(rs_hist[0].cpu().numpy().astype(np.int64), cfg.group_size)
+    e = ne_hist[0].cpu().numpy().astype(np.int64)
+    R = np.minimum(N, bank.budget.cpu().numpy().astype(np.int64))
+    pairs = gram_pairs(m0, N, R, r, e)
+    gram_tf = 2.0 * d * float(pairs.sum()) / (upd_ms * 1e-3) / 1e12
 
     result = {
-        "metric": "bank-update tokens/s per layer-head + bank-attention TFLOP/s (roofline %)",
-        "value": round(value, 1),
+        "metric": METRIC,
+        "value": round(N / (ms_step * 1e-3), 1),
         "unit": "tokens/s per layer-head",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": cfg.dtype, "data": "synthetic",
         "config": {"workload": f"{cfg.name}: {cfg.layers} layer x {cfg.heads} heads, d={d}, "
-                               f"{cfg.dtype}, budget {cfg.budget} (starts full), segment {N} (30% near-duplicates), "
-                               f"{cfg.n_query} queries over bank + {cfg.n_window}-token window",
+                               f"{cfg.dtype}, budget {cfg.budget} (starts full), segment {N}"
+                               + (f" ({int(cfg.dup_frac * 100)}% near-duplicates)" if cfg.dup_frac else "")
+                               + f", {cfg.n_query} queries over bank + {cfg.n_window}-token window",
                    "banks": B, "group_size": cfg.group_size, "candidates": N, "budget": cfg.budget,
                    "queries": cfg.n_query, "window": cfg.n_window, "head_dim": d, "policy": args.policy},
         "update_ms": round(upd_ms, 4),
         "update_tokens_per_s_per_layer_head": round(N / (upd_ms * 1e-3), 1),
         "attention_ms": round(att_ms, 4),
         "attention_tflops": round(att_tflops, 2),
-        "roofline": {"bound": "mfma", "kernel": "bank attention", "achieved": round(att_tflops, 2),
+        "roofline": {"bound": "mfma", "kernel": "k_attn_mfma (bank attention)", "achieved": round(att_tflops, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(att_tflops / PEAK_BF16_TFLOPS, 4),
-                     "traffic": measured_traffic()},
+                     "traffic": measured_traffic(cfg.name)},
     }
     if args.policy != "sequential":
-        result["update_gram"] = update_gram_work(api, torch, bank, snap, seg_k, seg_v, run_prm, ws, N, d, upd_ms)
+        result["update_gram"] = {"pairs": int(pairs.sum()), "tflop": round(2.0 * d * float(pairs.sum()) / 1e12, 4),
+                                 "tflops": round(gram_tf, 2), "frac_of_bf16_peak": round(gram_tf / PEAK_BF16_TFLOPS, 4),
+                                 "r_star": int(r.max()), "evicted_per_bank": int(e.max())}
     else:
         # the walk offers the N candidates one per step: latency per step, not a roofline, bounds it
         result["sequential"] = {"steps_per_update": N, "update_us_per_step": round(upd_ms * 1e3 / N, 3)}
-    if not args.no_sink_attention:
+    if not args.no_sink_attention and cfg.name == "single_layer":
         result["sink_attention"] = sink_attention(api, synth, torch)
-    if not args.no_rollout_block:
-        result["rollout_block"] = rollout_block(api, synth, torch)
+    del bank, ws, snap
+    if not args.no_cpu_baseline and args.policy == "default":
+        result["cpu_baseline"] = single_cpu_baseline(case, cfg, min(args.cpu_heads or 12, cfg.heads))
+    return result
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                                   "(banks shard by layer without communication; see the design notes)"}))
+        sys.exit(2)
+    import torch
+    from paper_2608_27922_amd import api, synth
+
+    torch.cuda.set_device(0)
+    api.lib()
+    if args.workload in ROLLOUTS:
+        result = run_rollout(args, api, synth, torch)
+        if not args.no_cpu_baseline and args.policy == "default":
+            result["cpu_baseline"] = rollout_cpu_baseline(synth.WORKLOADS[args.workload], args.cpu_heads or 3)
+    elif args.workload in ("tiny", "single_layer"):
+        result = run_single(args, api, synth, torch)
+    else:
+        raise SystemExit(f"unknown workload {args.workload}")
     if args.copy_probe_mb:
         nbytes = args.copy_probe_mb << 20
         src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
@@ -339,8 +517,6 @@ def main():
             torch.neg(src, out=dst)      # reads and writes nbytes each
         torch.cuda.synchronize()
         result["copy_probe_bytes"] = nbytes
-    if not args.no_cpu_baseline and args.policy == "default":
-        result["cpu_baseline"] = cpu_baseline(case, cfg, min(args.cpu_heads, cfg.heads))
     print(json.dumps(result), flush=True)
 
 

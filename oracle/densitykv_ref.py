@@ -106,6 +106,12 @@ import numpy as np
 
 Q23 = 1 << 23  # fixed-point scale: weight 1.0 == 2^23
 
+# The per-head steps of one layer update share no data (only r* couples the
+# heads), so they are applied with HEAD_MAP, the builtin map unless a caller
+# that runs the oracle at full size sets a thread pool's map; the results do
+# not depend on it.
+HEAD_MAP = map
+
 
 @dataclass(frozen=True)
 class Params:
@@ -306,24 +312,22 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
     Db = [desc(heads[h].K, heads[h].V) for h in range(H)]              # bank descriptors
 
     # ---- Step 1: per-head candidate order (Eq. 6-7; Alg. 1) ----------------
-    orders, scores = [], []
-    for h in range(H):
+    def order_of(h):
         bank = heads[h]
         if bank.m == 0:
             # Empty bank: source-ordered candidates (Alg. 1, first branch).
-            orders.append(np.arange(N, dtype=np.int64))
-            scores.append((None, 0))
-        else:
-            S, E, _ = candidate_scores(Db[h], bank.base, Dc[h], prm)
-            if prm.source_order:
-                orders.append(np.arange(N, dtype=np.int64))               # V1
-            else:
-                orders.append(np.argsort(S, kind="stable").astype(np.int64))  # ties: source order
-            scores.append((S, E))
+            return np.arange(N, dtype=np.int64), (None, 0)
+        S, E, _ = candidate_scores(Db[h], bank.base, Dc[h], prm)
+        if prm.source_order:
+            return np.arange(N, dtype=np.int64), (S, E)                     # V1
+        return np.argsort(S, kind="stable").astype(np.int64), (S, E)       # ties: source order
+
+    step1 = list(HEAD_MAP(order_of, range(H)))
+    orders = [o for o, _ in step1]
+    scores = [sc for _, sc in step1]
 
     # ---- Step 2: violators c_r for every tested prefix, shared r* (Eqs. 8-11)
-    prefix, counts, first_cross = [], [], []
-    for h in range(H):
+    def prefix_of(h):
         bank, pi = heads[h], orders[h]
         m = bank.m
         if m == 0:
@@ -341,9 +345,12 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
             hit = np.nonzero(_violates(bank.rho[i] + P[i, :], bank.base[i], prm))[0]
             if hit.size:
                 fc[i] = hit[0]
-        prefix.append(P)
-        counts.append(c)
-        first_cross.append(fc)
+        return P, c, fc
+
+    step2 = list(HEAD_MAP(prefix_of, range(H)))
+    prefix = [P for P, _, _ in step2]
+    counts = [c for _, c, _ in step2]
+    first_cross = [fc for _, _, fc in step2]
 
     def e_of(h: int, r: int) -> int:               # required evictions (Eq. 10)
         return max(0, heads[h].m + r - heads[h].budget)
@@ -354,9 +361,7 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
             r_star = r                              # largest r feasible for every head
 
     # ---- Step 3: evict, commit, maintain densities (Eq. 12; Supp. C) --------
-    record = UpdateRecord(r_star=r_star, R=R)
-    new_heads = []
-    for h in range(H):
+    def commit_of(h):
         bank, pi = heads[h], orders[h]
         m = bank.m
         e = e_of(h, r_star)
@@ -435,12 +440,14 @@ def update_layer(heads: Sequence[BankState], cand_K: Sequence[np.ndarray],
             base = np.maximum(rho, prm.delta_q)                         # V2
         nb = BankState(bank.budget, K[:m_new].copy(), V[:m_new].copy(), rho[:m_new].copy(),
                        base[:m_new].copy(), prov[:m_new].copy())
-        new_heads.append(nb)
         S, E = scores[h]
-        record.heads.append(HeadRecord(pi=pi, score_q=S, score_exp=E, first_cross=first_cross[h],
-                                       c=counts[h], e=e, rho_tilde=rho_t, evicted=evicted,
-                                       admitted=admitted,
-                                       admitted_slot=np.array(slots, np.int64)))
+        return nb, HeadRecord(pi=pi, score_q=S, score_exp=E, first_cross=first_cross[h],
+                              c=counts[h], e=e, rho_tilde=rho_t, evicted=evicted,
+                              admitted=admitted, admitted_slot=np.array(slots, np.int64))
+
+    step3 = list(HEAD_MAP(commit_of, range(H)))
+    record = UpdateRecord(r_star=r_star, R=R, heads=[hr for _, hr in step3])
+    new_heads = [nb for nb, _ in step3]
     return new_heads, record
 
 

@@ -77,9 +77,7 @@ __device__ __forceinline__ uint32_t weight_raw(float u, float scale) {
   float tp = t;
   if constexpr (P >= 2) tp = t * t;
   if constexpr (P == 4) tp = tp * tp;
-  const float y = __builtin_amdgcn_rcpf(tp);
-  const float e = __builtin_fmaf(-tp, y, 1.0f);
-  const float w = __builtin_fmaf(e, y, y);
+  const float w = clamp_weight(rcp_rn(tp));
   return __float_as_uint(__builtin_fmaf(w, scale, 8388608.0f));
 }
 
@@ -301,9 +299,7 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
       float tp = tt;
       if constexpr (P >= 2) tp = tt * tt;
       if constexpr (P == 4) tp = tp * tp;
-      const float y = __builtin_amdgcn_rcpf(tp);
-      const float e = __builtin_fmaf(-tp, y, 1.0f);
-      const float w = __builtin_fmaf(e, y, y);
+      const float w = clamp_weight(rcp_rn(tp));
       uint32_t rw = __float_as_uint(__builtin_fmaf(w, 8388608.0f, 8388608.0f));
       uint32_t ra = __float_as_uint(__builtin_fmaf(w, bsv[i], 8388608.0f));
       if constexpr (MASK) {

@@ -127,13 +127,21 @@ __device__ __forceinline__ float load_elem(const void *p, size_t i) {
 }
 
 // Correctly rounded binary32 reciprocal for normal inputs with normal results:
-// hardware estimate y, exact residual e = 1 - x y by FMA, one correction
-// y + e y.  Checked against the IEEE division for every significand.
+// one Newton-Raphson step y + y (1 - x y) on the hardware estimate y, with the
+// residual 1 - x y computed exactly by a fused multiply-add (Markstein's
+// correction scheme, IBM J. Res. Dev. 34(1), 1990).  Checked against the IEEE
+// division for every significand.
 __device__ __forceinline__ float rcp_rn(float x) {
   const float y = __builtin_amdgcn_rcpf(x);
   const float e = __builtin_fmaf(-x, y, 1.0f);
   return __builtin_fmaf(e, y, y);
 }
+// A weight is at most eps^-p = 1 (t = 1 + d2 / sigma^2 >= 1).  On the key grid
+// t >= 1 holds exactly; off the grid the fp32 Gram can round d2 below 0 for
+// near-duplicates, so the weight is clamped to [0, 1].  The clamp is the output
+// modifier of the last FMA (no extra instruction) and keeps every fixed-point
+// weight within 2^23, as the Q23 rounding and the packed record fields need.
+__device__ __forceinline__ float clamp_weight(float w) { return __builtin_amdgcn_fmed3f(w, 0.0f, 1.0f); }
 
 // Soft-Riesz weight (eps = 1): w = 1 / (1 + d2 / sigma^2)^p, each step one
 // binary32 operation rounded to nearest even with a correctly rounded
@@ -143,7 +151,7 @@ __device__ __forceinline__ float pair_weight(float d2, float inv_sigma2, int p) 
   float tp = t;
   if (p >= 2) tp = t * t;
   if (p == 4) tp = tp * tp;
-  return rcp_rn(tp);
+  return clamp_weight(rcp_rn(tp));
 }
 // Score scale of a bank state (Eq. 6): fp32(2^23 / b) by one fp64 division
 // rounded to fp32, times 2^(23 - E) with E the binary exponent of the bank's

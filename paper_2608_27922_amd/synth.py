@@ -238,3 +238,75 @@ def torch_layer_block(cfg: Config, layer: int, t: int, n: int, device, seed: int
     k = (torch.clamp(torch.round(out[0] * GRID), -GRID_MAX, GRID_MAX) / GRID)
     dt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
     return k.to(dt).contiguous(), out[1].to(dt).contiguous()
+
+
+class TorchRollout:
+    """Device-side draws of a rollout workload for every (layer, head) at once.
+
+    The HeadStream recipe (unit-norm centres per (layer, head); tokens = centre
+    + 0.3 N(0, I); keys snapped to the grid, values and queries rounded to the
+    storage dtype; centre drift per block; active cluster sets with the
+    recurring set) drawn from seeded torch generators on the device, so that a
+    whole 360-bank run can be generated in HBM before it is timed.  Block t
+    depends only on (seed, workload, t, role); the numbers differ from the
+    NumPy streams, the distribution does not."""
+
+    def __init__(self, cfg: Config, device, seed: int = 0):
+        import torch
+        self.torch, self.cfg, self.device, self.seed = torch, cfg, torch.device(device), seed
+        self.B = cfg.layers * cfg.heads
+        g = self._gen(ROLE_CENTRES, 0)
+        c = torch.randn(self.B, cfg.clusters, cfg.d, generator=g, device=self.device)
+        self._centres = {0: c / c.norm(dim=-1, keepdim=True)}
+
+    def _gen(self, role: int, t: int):
+        g = self.torch.Generator(device=self.device)
+        g.manual_seed((((self.seed * 1_000_003 + self.cfg.seed_id) * 131 + role) * 100_003 + t) & 0x7FFFFFFFFFFF)
+        return g
+
+    def centres(self, t: int):
+        cfg, torch = self.cfg, self.torch
+        if cfg.drift == 0.0:
+            return self._centres[0]
+        last = max(k for k in self._centres if k <= t)
+        c = self._centres[last]
+        for s in range(last + 1, t + 1):
+            u = torch.randn(c.shape, generator=self._gen(ROLE_DRIFT, s), device=self.device)
+            c = c + cfg.drift * (u / u.norm(dim=-1, keepdim=True))
+            c = c / c.norm(dim=-1, keepdim=True)
+            self._centres[s] = c
+        for k in [k for k in self._centres if 0 < k < t]:   # keep only what later blocks need
+            del self._centres[k]
+        return c
+
+    def active_set(self, t: int):
+        """[B, A] cluster indices active in block t."""
+        cfg, torch = self.cfg, self.torch
+        if cfg.active == 0:
+            return torch.arange(cfg.clusters, device=self.device).expand(self.B, cfg.clusters)
+        if cfg.revisit and t >= cfg.revisit and t % cfg.revisit == 0:
+            return self.active_set(t - cfg.revisit)
+        r = torch.rand(self.B, cfg.clusters, generator=self._gen(ROLE_ACTIVE, t), device=self.device)
+        return r.argsort(dim=1)[:, :cfg.active]
+
+    def _mixture(self, role: int, t: int, n: int):
+        cfg, torch = self.cfg, self.torch
+        g = self._gen(role, t)
+        act = self.active_set(t)
+        z = torch.gather(act, 1, torch.randint(0, act.shape[1], (self.B, n), generator=g, device=self.device))
+        c = self.centres(t)
+        x = torch.gather(c, 1, z[..., None].expand(self.B, n, cfg.d))
+        return x.add_(torch.randn(self.B, n, cfg.d, generator=g, device=self.device), alpha=0.3)
+
+    def _dtype(self):
+        return self.torch.bfloat16 if self.cfg.dtype == "bf16" else self.torch.float32
+
+    def keys(self, t: int, n: int):
+        x = self._mixture(ROLE_K, t, n)
+        return (self.torch.clamp(self.torch.round(x * GRID), -GRID_MAX, GRID_MAX) / GRID).to(self._dtype())
+
+    def values(self, t: int, n: int):
+        return self._mixture(ROLE_V, t, n).to(self._dtype())
+
+    def queries(self, t: int):
+        return self._mixture(ROLE_Q, t, self.cfg.n_query).to(self._dtype())

@@ -16,7 +16,7 @@ its own group) are independent, so they run in parallel worker processes.
 Inputs are the seeded HeadStream draws of the input generator module; nothing
 here reads a GPU result.  Run from the repository root:
 
-    python tests/golden/make_rollout_digests.py [--jobs J] [workload[:layer] ...]
+    python tests/golden/make_rollout_digests.py [--jobs J] [--threads T] [workload[:layer] ...]
 
 Output: tests/golden/rollout_<workload>_L<layer>.json and
 tests/golden/rollout_<workload>_L<layer>_attention.npy.
@@ -150,8 +150,14 @@ if __name__ == "__main__":
     sys.path.insert(0, os.path.dirname(os.path.dirname(here)))
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=1, help="worker processes for independent head groups")
+    ap.add_argument("--threads", type=int, default=1, help="threads for the per-head steps of a layer update")
     ap.add_argument("which", nargs="*", help="workload or workload:layer (default: every stored case)")
     a = ap.parse_args()
+    if a.threads > 1:
+        from concurrent.futures import ThreadPoolExecutor
+
+        import oracle.densitykv_ref as ref
+        ref.HEAD_MAP = ThreadPoolExecutor(a.threads).map
     todo = []
     for w in a.which or [n for n in RUNS]:
         nm, _, ly = w.partition(":")

@@ -1,8 +1,10 @@
 """Full-size runs of the three 30-layer x 12-head rollout workloads: all 360 banks
 updated by one launch per block, as the library is used.  Needs an MI355X.
 
-Parity with the oracle: one sampled layer of each run is drawn from the seeded
-input generator, and after every block the device results for its 12 banks
+Parity with the oracle: sampled layers of each run (layers 0 and 29 of the
+rollout, one layer of the other two) are drawn from the seeded input generator,
+and every block of the run at its stated length (20, 80 and 160 blocks) is
+compared: after every block the device results for the sampled layer's 12 banks
 (candidate order, scores, first crossings, projected densities, eviction and
 admission lists, and the committed bank bytes) must hash to the digests the
 oracle wrote for the same inputs (tests/golden/make_rollout_digests.py; the
@@ -17,9 +19,10 @@ the first r* of the order; every violator at r* is evicted and every other
 evicted state is at least as dense as every kept one; the violation flags agree
 with the projected densities; the maintained density equals the density
 recomputed from scratch; the growth bound rho < tau b; the baseline floor; and
-every retained token carries the key and value it was admitted with.
-The 29 layers that are not compared with the oracle draw their tokens on the
-device from a seeded torch generator.
+every retained token carries the key and value it was admitted with (checked
+through 64-bit fingerprints of every admitted row, so that the history of a
+160-block run need not stay in memory).  The layers that are not compared with
+the oracle draw their tokens on the device from a seeded torch generator.
 """
 
 import json
@@ -32,7 +35,7 @@ torch = pytest.importorskip("torch")
 
 pytestmark = pytest.mark.gpu
 
-from golden.make_rollout_digests import RUNS, attention_rows, digest, layer_block  # noqa: E402
+from golden.make_rollout_digests import RUNS, attention_rows, cases, digest, layer_block  # noqa: E402
 from gpu_util import attention_error, dev, host  # noqa: E402
 from paper_2608_27922_amd import api, synth  # noqa: E402
 
@@ -65,7 +68,42 @@ def _bank_entry(bank, out, b, m_before, n):
     }
 
 
-def _properties(bank, out, prm, m_prev, base_prev, hist_k, hist_v, gs, N, ctx):
+class RowPrints:
+    """64-bit fingerprints of every candidate row of every block: a fixed random
+    linear form over the row's 32-bit words, so that a retained row can be
+    checked against the row it was admitted with without keeping the history."""
+
+    def __init__(self, d, seed=5):
+        g = torch.Generator(device="cuda")
+        g.manual_seed(seed)
+        self.w = torch.randint(1, 1 << 31, (d // 2,), generator=g, device="cuda", dtype=torch.int64)
+        self.k, self.v = [], []
+
+    def of(self, rows):
+        """[..., d] bf16 -> [...] int64."""
+        words = rows.contiguous().view(torch.int32).to(torch.int64)
+        return (words * self.w).sum(-1)
+
+    def add(self, K, V):
+        self.k.append(self.of(K))
+        self.v.append(self.of(V))
+
+    def check(self, bank, occupied, ctx, chunk=40):
+        B, Mcap = bank.B, bank.Mcap
+        hk, hv = torch.stack(self.k), torch.stack(self.v)      # [T, B, N]
+        for b0 in range(0, B, chunk):
+            b1 = min(B, b0 + chunk)
+            occ = occupied[b0:b1]
+            blk = (bank.prov[b0:b1] >> 32)[occ]
+            sidx = (bank.prov[b0:b1] & 0xFFFFFFFF)[occ]
+            bidx = torch.arange(b0, b1, device="cuda")[:, None].expand(b1 - b0, Mcap)[occ]
+            assert torch.equal(self.of(bank.k[b0:b1])[occ], hk[blk, bidx, sidx]), \
+                f"{ctx}: a retained key differs from its admitted key"
+            assert torch.equal(self.of(bank.v[b0:b1])[occ], hv[blk, bidx, sidx]), \
+                f"{ctx}: a retained value differs from its admitted value"
+
+
+def _properties(bank, out, prm, m_prev, base_prev, prints, gs, N, ctx):
     B, Mcap = bank.B, bank.Mcap
     ar = torch.arange(Mcap, device="cuda")
     occ = bank.occupancy.long()
@@ -123,24 +161,30 @@ def _properties(bank, out, prm, m_prev, base_prev, hist_k, hist_v, gs, N, ctx):
     assert not bool(torch.any(dup)), f"{ctx}: duplicate provenance inside a bank"
     blk = (bank.prov >> 32)[occupied]
     sidx = (bank.prov & 0xFFFFFFFF)[occupied]
-    bidx = torch.arange(B, device="cuda")[:, None].expand(B, Mcap)[occupied]
-    assert bool(torch.all((blk >= 0) & (blk < len(hist_k)) & (sidx < N))), f"{ctx}: provenance out of range"
-    hk = torch.stack(hist_k)   # [T, B, N, d]
-    hv = torch.stack(hist_v)
-    assert torch.equal(bank.k[occupied], hk[blk, bidx, sidx]), f"{ctx}: a retained key differs from its admitted key"
-    assert torch.equal(bank.v[occupied], hv[blk, bidx, sidx]), f"{ctx}: a retained value differs from its admitted value"
+    assert bool(torch.all((blk >= 0) & (blk < len(prints.k)) & (sidx < N))), f"{ctx}: provenance out of range"
+    prints.check(bank, occupied, ctx)
 
 
-@pytest.mark.parametrize("name", list(RUNS))
-def test_full_size_workload(name):
-    path = os.path.join(GOLDEN, f"rollout_{name}.json")
-    if not os.path.exists(path):
-        pytest.skip(f"oracle digests for {name} not generated")
-    with open(path) as f:
-        gold = json.load(f)
-    ref_att = np.load(os.path.join(GOLDEN, f"rollout_{name}_attention.npy"))
+def _golden(name, layer):
+    """Digests of (workload, sampled layer) at the stated length, else those of a
+    shorter run of the same layer (the first blocks of the same rollout)."""
+    for stem in (f"rollout_{name}_L{layer}", f"rollout_{name}"):
+        path = os.path.join(GOLDEN, stem + ".json")
+        if os.path.exists(path):
+            with open(path) as f:
+                gold = json.load(f)
+            if gold["layer"] == layer:
+                return gold, np.load(os.path.join(GOLDEN, stem + "_attention.npy"))
+    return None, None
+
+
+@pytest.mark.parametrize("name,layer", cases(), ids=[f"{n}-L{ly}" for n, ly in cases()])
+def test_full_size_workload(name, layer):
+    gold, ref_att = _golden(name, layer)
+    if gold is None:
+        pytest.skip(f"oracle digests for {name} layer {layer} not generated")
     cfg = synth.WORKLOADS[name]
-    blocks, layer, att_heads = gold["blocks"], gold["layer"], gold["attention_heads"]
+    blocks, att_heads = gold["blocks"], gold["attention_heads"]
     H, d, N, gs = cfg.heads, cfg.d, cfg.n_cand, cfg.group_size
     B = cfg.layers * H
     print(f"workload {name}: {B} banks, {blocks} blocks, sampled layer {layer}", flush=True)
@@ -151,7 +195,7 @@ def test_full_size_workload(name):
                     budget=torch.from_numpy(budgets))
     ws = api.alloc_workspace(bank, N)
     streams = [synth.HeadStream(cfg, layer, h) for h in range(H)]
-    hist_k, hist_v = [], []
+    prints = RowPrints(d)
     sl = slice(layer * H, (layer + 1) * H)
     for t in range(blocks):
         K = torch.empty(B, N, d, dtype=torch.bfloat16, device="cuda")
@@ -161,14 +205,13 @@ def test_full_size_workload(name):
                 K[L * H:(L + 1) * H], V[L * H:(L + 1) * H] = synth.torch_layer_block(cfg, L, t, N, "cuda")
         Kl, Vl = layer_block(cfg, streams, t)
         K[sl], V[sl] = dev(Kl, "bf16"), dev(Vl, "bf16")
-        hist_k.append(K)
-        hist_v.append(V)
+        prints.add(K, V)
         m_prev = bank.occupancy.long().clone()
         base_prev = bank.base.clone()
         out = api.UpdateOut(bank, N, trace=True)
         api.update_bank(bank, K, V, t, prm, workspace=ws, out=out)
         torch.cuda.synchronize()
-        ctx = f"{name} block {t}"
+        ctx = f"{name} L{layer} block {t}"
         step = gold["steps"][t]
         for g, rs in enumerate(step["r_star"]):
             assert int(out.r_star[layer * H // gs + g]) == rs, f"{ctx}: r* of group {g}"
@@ -177,11 +220,11 @@ def test_full_size_workload(name):
             want = step["heads"][h]
             bad = [k for k in want if got[k] != want[k]]
             assert not bad, f"{ctx} head {h}: differs from the oracle in {bad}"
-        _properties(bank, out, prm, m_prev, base_prev, hist_k, hist_v, gs, N, ctx)
-        print(f"  block {t}: r* {step['r_star'][:3]} occupancy {gold['steps'][t]['heads'][0]['m_after']} ok",
-              flush=True)
+        _properties(bank, out, prm, m_prev, base_prev, prints, gs, N, ctx)
+        del K, V, out
+        print(f"  block {t}: r* {step['r_star'][:3]} occupancy {step['heads'][0]['m_after']} "
+              f"evicted {sum(hh['n_evicted'] for hh in step['heads'])} ok", flush=True)
     q = torch.empty(B, cfg.n_query, d, dtype=torch.bfloat16, device="cuda")
-    wk = torch.empty(B, cfg.n_window, d, dtype=torch.bfloat16, device="cuda")
     for L in range(cfg.layers):
         if L != layer:
             q[L * H:(L + 1) * H], _ = synth.torch_layer_block(cfg, L, blocks, cfg.n_query, "cuda")
@@ -224,13 +267,12 @@ def test_interface_limits():
     bank = api.Bank(H, cfg.budget, d, dtype=torch.bfloat16, group_size=cfg.group_size)
     ws = api.alloc_workspace(bank, N)
     streams = [synth.HeadStream(cfg, 0, h) for h in range(H)]
-    hist_k, hist_v = [], []
+    prints = RowPrints(d)
     for t in range(BLOCKS):
         bank_keys = [host(bank.k[h, :int(bank.occupancy[h])]) for h in range(H)]
         Kn, Vn = block_inputs(cfg, streams, t, bank_keys)
         K, V = dev(Kn, "bf16"), dev(Vn, "bf16")
-        hist_k.append(K)
-        hist_v.append(V)
+        prints.add(K, V)
         m_prev = bank.occupancy.long().clone()
         base_prev = bank.base.clone()
         out = api.UpdateOut(bank, N, trace=True)
@@ -244,7 +286,7 @@ def test_interface_limits():
             want = step["heads"][h]
             bad = [k for k in want if got[k] != want[k]]
             assert not bad, f"{ctx} head {h}: differs from the oracle in {bad}"
-        _properties(bank, out, prm, m_prev, base_prev, hist_k, hist_v, cfg.group_size, N, ctx)
+        _properties(bank, out, prm, m_prev, base_prev, prints, cfg.group_size, N, ctx)
         print(f"  block {t}: r* {step['r_star'][0]} occupancy {[int(x) for x in bank.occupancy.cpu()]} ok", flush=True)
 
 
