@@ -54,7 +54,8 @@ typedef enum {
   DKV_ERR_UNSUPPORTED = -3, /* head_dim, p or sigma^2 not supported             */
   DKV_ERR_WORKSPACE = -4,   /* workspace NULL or smaller than required          */
   DKV_ERR_RANGE = -5,       /* fixed-point range would overflow                 */
-  DKV_ERR_HIP = -6          /* a HIP launch reported an error                   */
+  DKV_ERR_HIP = -6,         /* a HIP launch reported an error                   */
+  DKV_ERR_SCRATCH = -7      /* needs more than DKV_NOALLOC_SCRATCH_BYTES        */
 } dkv_status;
 
 typedef enum { DKV_BF16 = 0, DKV_F32 = 1 } dkv_dtype;
@@ -248,6 +249,28 @@ int densitykv_score(const dkv_bank *bank, const dkv_segment *seg, const dkv_para
 int densitykv_update_bank(dkv_bank *bank, const dkv_segment *seg, const dkv_params *prm,
                           dkv_update_out *out, void *workspace, size_t workspace_bytes,
                           void *stream);
+
+/*
+ * densitykv_update_bank for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same update, with its workspace taken from a static device
+ * buffer of DKV_NOALLOC_SCRATCH_BYTES that the library holds on every device
+ * it runs on until the process ends.  The call itself allocates and frees
+ * nothing.  The caller still passes the bank, the segment and the outputs.
+ *   - Uses the scratch of the current device; `stream` must belong to it.
+ *   - Returns DKV_ERR_SCRATCH, before enqueueing anything, when
+ *     densitykv_workspace_size_policy(bank, seg->n, prm->flags) exceeds
+ *     DKV_NOALLOC_SCRATCH_BYTES (e.g. 12 banks of 4,680 slots with 4,680
+ *     candidates, d = 128, fit; 360 such banks do not).  Other errors as
+ *     densitykv_update_bank.
+ *   - Every call on one device shares that device's scratch; the update
+ *     initialises every part of it that it reads, so the contents a previous
+ *     call left do not matter.  Calls that overlap in time on one device
+ *     (different streams, or several host threads) race on it: serialise them.
+ */
+#define DKV_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int densitykv_update_bank_noalloc(dkv_bank *bank, const dkv_segment *seg, const dkv_params *prm,
+                                  dkv_update_out *out, void *stream);
 
 /*
  * Native attention of n_query queries per bank over the bank's live slots

@@ -39,8 +39,11 @@ POLICY_SOURCE_FILL = 0x8    # violators, then fill in admission order
 POLICY_KV_DESCRIPTOR = 0x10  # densities on the concatenated [k; v] rows (bf16 banks; values on the key grid)
 POLICY_SEQUENTIAL = 0x20    # within-block sequential competition (bf16 banks; larger workspace)
 
+# Bytes of the static device scratch behind update_bank_noalloc (DKV_NOALLOC_SCRATCH_BYTES).
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
 ENTRY_POINTS = ("densitykv_workspace_size", "densitykv_workspace_size_policy", "densitykv_score",
-                "densitykv_update_bank",
+                "densitykv_update_bank", "densitykv_update_bank_noalloc",
                 "densitykv_bank_attention", "densitykv_bank_attention_sink", "densitykv_pair_weight_q23",
                 "densitykv_status_string")
 
@@ -87,6 +90,8 @@ def lib() -> ctypes.CDLL:
                                       ctypes.c_size_t, _vp]
         L.densitykv_update_bank.argtypes = [P(DkvBank), P(DkvSegment), P(DkvParams), P(DkvUpdateOut), _vp,
                                             ctypes.c_size_t, _vp]
+        L.densitykv_update_bank_noalloc.argtypes = [P(DkvBank), P(DkvSegment), P(DkvParams), P(DkvUpdateOut),
+                                                    _vp]
         L.densitykv_bank_attention.argtypes = [P(DkvBank), _vp, ctypes.c_int32, _vp, _vp, ctypes.c_int32, _vp,
                                                ctypes.c_float, _vp]
         L.densitykv_bank_attention_sink.argtypes = [P(DkvBank), _vp, ctypes.c_int32, _vp, _vp, ctypes.c_int32,
@@ -281,6 +286,20 @@ def update_bank(bank: Bank, seg_k: Optional[torch.Tensor], seg_v: Optional[torch
     _check(lib().densitykv_update_bank(ctypes.byref(cb), ctypes.byref(cs), ctypes.byref(cp),
                                        ctypes.byref(co) if co is not None else None, _ptr(ws), ws.numel(),
                                        _stream()), "update_bank")
+    return out
+
+
+def update_bank_noalloc(bank: Bank, seg_k: Optional[torch.Tensor], seg_v: Optional[torch.Tensor], block_id: int,
+                        params: Params = Params(), out: Optional[UpdateOut] = None) -> Optional[UpdateOut]:
+    """densitykv_update_bank_noalloc: the same update with the library's static
+    device scratch as workspace (no allocation by the call; sizes whose workspace
+    exceeds NOALLOC_SCRATCH_BYTES raise DkvError)."""
+    n = _check_seg(bank, seg_k, seg_v)
+    cb, cs, cp = bank.c(), _segment(seg_k, seg_v, n, block_id), params.c()
+    co = out.c() if out is not None else None
+    _check(lib().densitykv_update_bank_noalloc(ctypes.byref(cb), ctypes.byref(cs), ctypes.byref(cp),
+                                               ctypes.byref(co) if co is not None else None, _stream()),
+           "update_bank_noalloc")
     return out
 
 

@@ -4,6 +4,7 @@
 
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "dkv_internal.hpp"
 
@@ -138,6 +139,29 @@ int check_geometry(const dkv_bank *bk, const dkv_segment *seg, const Prm &p) {
   return DKV_OK;
 }
 
+// Scratch of densitykv_update_bank_noalloc: a static device array, one copy per
+// device (the runtime places it with the code object), so that call allocates
+// nothing.  Host code never uses the array's name as an address: the device
+// address comes from hipGetSymbolAddress with that device current and is kept
+// per device.
+static __device__ __align__(256) unsigned char scratch[DKV_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void *scratch_ptr[kMaxDevices];
+
+int current_device_scratch(void **ptr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return DKV_ERR_HIP;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return DKV_ERR_HIP;
+    scratch_ptr[dev] = p;
+  }
+  *ptr = scratch_ptr[dev];
+  return DKV_OK;
+}
+
 Geom geom_of(const dkv_bank *bk, int n) {
   Geom g;
   g.B = bk->num_banks;
@@ -211,6 +235,24 @@ int densitykv_update_bank(dkv_bank *bank, const dkv_segment *seg, const dkv_para
   return e == hipSuccess ? DKV_OK : DKV_ERR_HIP;
 }
 
+int densitykv_update_bank_noalloc(dkv_bank *bank, const dkv_segment *seg, const dkv_params *prm,
+                                  dkv_update_out *out, void *stream) {
+  int rc = check_bank(bank);
+  if (!rc) rc = check_segment(seg);
+  Prm p{};
+  if (!rc) rc = check_params(prm, &p, seg->block_id);
+  if (!rc) rc = check_geometry(bank, seg, p);
+  if (rc) return rc;
+  const size_t need = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity,
+                                       seg->n, bank->head_dim, nullptr, nullptr,
+                                       (p.flags & DKV_POLICY_SEQUENTIAL) != 0);
+  if (need > DKV_NOALLOC_SCRATCH_BYTES) return DKV_ERR_SCRATCH;
+  void *ws = nullptr;
+  rc = current_device_scratch(&ws);
+  if (rc) return rc;
+  return densitykv_update_bank(bank, seg, prm, out, ws, DKV_NOALLOC_SCRATCH_BYTES, stream);
+}
+
 int densitykv_bank_attention_sink(const dkv_bank *bank, const void *q, int32_t n_query, const void *sink_k,
                                   const void *sink_v, int32_t n_sink, const void *win_k, const void *win_v,
                                   int32_t n_window, void *out, float softmax_scale, void *stream) {
@@ -256,6 +298,7 @@ const char *densitykv_status_string(int status) {
     case DKV_ERR_WORKSPACE: return "workspace missing or too small";
     case DKV_ERR_RANGE: return "parameter out of fixed-point range";
     case DKV_ERR_HIP: return "HIP launch error";
+    case DKV_ERR_SCRATCH: return "update needs more than the static scratch of the no-allocation entry point";
     default: return "unknown status";
   }
 }
