@@ -16,7 +16,7 @@ its own group) are independent, so they run in parallel worker processes.
 Inputs are the seeded HeadStream draws of the input generator module; nothing
 here reads a GPU result.  Run from the repository root:
 
-    python tests/golden/make_rollout_digests.py [--jobs J] [--threads T] [workload[:layer] ...]
+    python tests/golden/make_rollout_digests.py [--jobs J] [--threads T] [--ckpt DIR] [workload[:layer] ...]
 
 Output: tests/golden/rollout_<workload>_L<layer>.json and
 tests/golden/rollout_<workload>_L<layer>_attention.npy.
@@ -73,14 +73,42 @@ def head_entry(hr, nb, m_before: int, n: int):
     }
 
 
+def _save(path, banks, steps):
+    """Checkpoint of a group's run after a block: the oracle banks and the entries so far."""
+    import json
+    import os
+    arrs = {}
+    for j, b in enumerate(banks):
+        arrs.update({f"{j}_K": b.K, f"{j}_V": b.V, f"{j}_rho": b.rho, f"{j}_base": b.base, f"{j}_prov": b.prov,
+                     f"{j}_budget": np.array(b.budget)})
+    np.savez(path + ".tmp.npz", **arrs)
+    with open(path + ".tmp.json", "w") as f:
+        json.dump(steps, f)
+    os.replace(path + ".tmp.npz", path + ".npz")
+    os.replace(path + ".tmp.json", path + ".json")
+
+
+def _load(path, n, BankState):
+    import json
+    import os
+    if not (os.path.exists(path + ".npz") and os.path.exists(path + ".json")):
+        return None, []
+    z = np.load(path + ".npz")
+    banks = [BankState(int(z[f"{j}_budget"]), z[f"{j}_K"], z[f"{j}_V"], z[f"{j}_rho"], z[f"{j}_base"],
+                       z[f"{j}_prov"]) for j in range(n)]
+    with open(path + ".json") as f:
+        return banks, [tuple(s) for s in json.load(f)]
+
+
 def run_group(args):
     """The whole run of one group of heads of the sampled layer: per block the
     group's r* and head entries, then the fp64 attention rows of its heads that
-    are in the stored set."""
+    are in the stored set.  With a checkpoint directory the run saves its state
+    after every block and resumes from the last saved block."""
     from oracle import BankState, Params, attention, update_layer
     from paper_2608_27922_amd import synth
 
-    name, layer, heads = args
+    name, layer, heads, ckpt = args
     blocks, _, att_heads = RUNS[name]
     cfg = synth.WORKLOADS[name]
     H = cfg.heads
@@ -89,13 +117,20 @@ def run_group(args):
     streams = [synth.HeadStream(cfg, layer, h) for h in heads]
     banks = [BankState.empty(int(budgets[h]), cfg.d) for h in heads]
     steps = []
-    for t in range(blocks):
+    path = f"{ckpt}/{name}_L{layer}_h{heads[0]}-{heads[-1]}" if ckpt else None
+    if path:
+        saved, saved_steps = _load(path, len(heads), BankState)
+        if saved is not None:
+            banks, steps = saved, saved_steps
+    for t in range(len(steps), blocks):
         K, V = layer_block(cfg, streams, t)
         nb, rec = update_layer(banks, [K[j].astype(np.float64) for j in range(len(heads))],
                                [V[j] for j in range(len(heads))], t, prm)
         steps.append((rec.r_star, [head_entry(rec.heads[j], nb[j], banks[j].m, cfg.n_cand)
                                    for j in range(len(heads))]))
         banks = nb
+        if path:
+            _save(path, banks, steps)
         print(f"{name} L{layer} heads {heads[0]}-{heads[-1]} block {t}: r* {rec.r_star} "
               f"occupancy {[b.m for b in banks][:4]}", flush=True)
     rows = attention_rows(cfg.n_query)
@@ -108,7 +143,7 @@ def run_group(args):
     return heads, steps, att
 
 
-def run(name: str, layer: int, path_prefix: str, jobs: int = 1):
+def run(name: str, layer: int, path_prefix: str, jobs: int = 1, ckpt=None):
     import json
     from concurrent.futures import ProcessPoolExecutor
 
@@ -118,7 +153,7 @@ def run(name: str, layer: int, path_prefix: str, jobs: int = 1):
     cfg = synth.WORKLOADS[name]
     H, gs = cfg.heads, cfg.group_size
     budgets = synth.budgets(cfg)[layer * H:(layer + 1) * H]
-    groups = [(name, layer, tuple(range(g0, g0 + gs))) for g0 in range(0, H, gs)]
+    groups = [(name, layer, tuple(range(g0, g0 + gs)), ckpt) for g0 in range(0, H, gs)]
     if jobs > 1 and len(groups) > 1:
         with ProcessPoolExecutor(max_workers=min(jobs, len(groups))) as ex:
             results = list(ex.map(run_group, groups))
@@ -151,6 +186,7 @@ if __name__ == "__main__":
     ap = argparse.ArgumentParser()
     ap.add_argument("--jobs", type=int, default=1, help="worker processes for independent head groups")
     ap.add_argument("--threads", type=int, default=1, help="threads for the per-head steps of a layer update")
+    ap.add_argument("--ckpt", default=None, help="directory for per-block checkpoints (resume after a stop)")
     ap.add_argument("which", nargs="*", help="workload or workload:layer (default: every stored case)")
     a = ap.parse_args()
     if a.threads > 1:
@@ -163,4 +199,4 @@ if __name__ == "__main__":
         nm, _, ly = w.partition(":")
         todo += [(nm, int(ly))] if ly else [(nm, L) for L in RUNS[nm][1]]
     for nm, ly in todo:
-        run(nm, ly, os.path.join(here, "rollout_"), a.jobs)
+        run(nm, ly, os.path.join(here, "rollout_"), a.jobs, a.ckpt)
