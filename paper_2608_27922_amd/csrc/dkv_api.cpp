@@ -34,7 +34,6 @@ size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, cha
   w.cnorm = (float *)take(Bz * Nz * 4);
   w.bs = (float *)take(Bz * Mz * 4);
   w.acol = (int64_t *)take(Bz * Nz * 8);
-  w.wcol = (int64_t *)take(Bz * Nz * 8);
   w.order = (int32_t *)take(Bz * Nz * 4);
   w.rank = (int32_t *)take(Bz * Nz * 4);
   w.first = (int32_t *)take(Bz * Mz * 4);

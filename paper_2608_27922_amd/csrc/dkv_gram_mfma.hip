@@ -276,10 +276,10 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
   load_row_frag<D, FOLD, KV>(rf, K, (int64_t)xr, rv ? ws.cnorm[xr] : 0.0f, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
   const size_t rb = (size_t)b * g.Mcap + c0;
   auto row_of = [&](int i) -> int64_t { return (int64_t)(rb + i); };
-  uint64_t A64 = 0, W64 = 0;
+  uint64_t A64 = 0;
   const int ns = (ncols + kSI - 1) / kSI;
-  // epilogue of one 32-column tile: integer sums of W and of the scaled score terms
-  auto epi = [&](auto mask_tag, const f32x16 &u, const float *tb, int nvalid, uint32_t &sw, uint32_t &sa)
+  // epilogue of one 32-column tile: integer sum of the scaled score terms
+  auto epi = [&](auto mask_tag, const f32x16 &u, const float *tb, int nvalid, uint32_t &sa)
       __attribute__((always_inline)) {
     constexpr bool MASK = decltype(mask_tag)::value;
     float bsv[16];
@@ -291,7 +291,6 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
       bsv[4 * gq + 2] = v.z;
       bsv[4 * gq + 3] = v.w;
     }
-    sw = 0;
     sa = 0;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -300,17 +299,10 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
       if constexpr (P >= 2) tp = tt * tt;
       if constexpr (P == 4) tp = tp * tp;
       const float w = clamp_weight(rcp_rn(tp));
-      uint32_t rw = __float_as_uint(__builtin_fmaf(w, 8388608.0f, 8388608.0f));
       uint32_t ra = __float_as_uint(__builtin_fmaf(w, bsv[i], 8388608.0f));
-      if constexpr (MASK) {
-        const bool ok = col_of_reg(i, h) < nvalid;
-        rw = ok ? rw : kMagic;
-        ra = ok ? ra : kMagic;
-      }
-      sw += rw;
+      if constexpr (MASK) ra = col_of_reg(i, h) < nvalid ? ra : kMagic;
       sa += ra;
     }
-    sw -= 16u * kMagic;
     sa -= 16u * kMagic;
   };
   using Full = std::integral_constant<bool, false>;
@@ -330,21 +322,17 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
     f32x16 u0, u1;
     stage_u<D>(kb, ab, rf, u0, u1);
     const int nv0 = ncols - t * kSI;
-    uint32_t sw, sa;
+    uint32_t sa;
     if (nv0 >= kSI) {
-      epi(Full{}, u0, sb, kCT, sw, sa);
-      W64 += sw;
+      epi(Full{}, u0, sb, kCT, sa);
       A64 += sa;
-      epi(Full{}, u1, sb + kCT, kCT, sw, sa);
-      W64 += sw;
+      epi(Full{}, u1, sb + kCT, kCT, sa);
       A64 += sa;
     } else {
-      epi(Part{}, u0, sb, nv0, sw, sa);
-      W64 += sw;
+      epi(Part{}, u0, sb, nv0, sa);
       A64 += sa;
       if (nv0 > kCT) {
-        epi(Part{}, u1, sb + kCT, nv0 - kCT, sw, sa);
-        W64 += sw;
+        epi(Part{}, u1, sb + kCT, nv0 - kCT, sa);
         A64 += sa;
       }
     }
@@ -361,12 +349,10 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
     if (t + 1 < ns) step(t + 1, k1, a1, s1, k0, a0, s0);
     if (t + 2 < ns) step(t + 2, k2, a2, s2, k1, a1, s1);
   }
-  const uint64_t Wt = W64 + __shfl_xor(W64, 32, 64);
   const uint64_t At = A64 + __shfl_xor(A64, 32, 64);
   if (!rv || h != 0) return;
   const size_t o = (size_t)b * g.N + x;
   atomicAdd(reinterpret_cast<unsigned long long *>(&ws.acol[o]), (unsigned long long)At);
-  atomicAdd(reinterpret_cast<unsigned long long *>(&ws.wcol[o]), (unsigned long long)Wt);
 }
 
 // ---------------------------------------------------------------------------
@@ -428,7 +414,6 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   const int n_ev = kNeedEv ? ws.n_ev[b] : 0;
   const int rs = (MODE == RS_FIXUP || kNeedEv) ? ws.r_star[b / g.gs] : 0;
   const int n_surv = m - n_ev;
-  const bool adm_by_ev = n_ev <= n_surv;
   // rows
   int nrows;
   if constexpr (MODE == RS_CHUNK || MODE == RS_FIXUP || MODE == RS_DENSITY) nrows = m;
@@ -447,7 +432,7 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   } else {
     int total;
     if constexpr (MODE == RS_SURV_EV) total = n_ev;
-    else if constexpr (MODE == RS_ADM_BASE) total = adm_by_ev ? n_ev : n_surv;
+    else if constexpr (MODE == RS_ADM_BASE) total = n_surv;
     else if constexpr (MODE == RS_ADM_MUT) total = rs;
     else total = m;
     // admitted x admitted: half splits, since a row block only takes the
@@ -493,8 +478,7 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   auto row_of = [&](int j) -> int64_t {
     if constexpr (MODE == RS_CHUNK || MODE == RS_FIXUP) return (int64_t)(nb + j);
     else if constexpr (MODE == RS_SURV_EV) return (int64_t)(rb + ws.ev_list[rb + j]);
-    else if constexpr (MODE == RS_ADM_BASE)
-      return (int64_t)(rb + (adm_by_ev ? ws.ev_list[rb + j] : ws.surv_list[rb + j]));
+    else if constexpr (MODE == RS_ADM_BASE) return (int64_t)(rb + ws.surv_list[rb + j]);
     else if constexpr (MODE == RS_ADM_MUT) return (int64_t)(nb + ws.adm_list[nb + j]);
     else return (int64_t)(rb + j);
   };
@@ -676,7 +660,7 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
 }
 
 // The three maintenance sums in one launch (Supp. C): survivors x evicted,
-// admitted x (evicted or survivors), admitted x admitted; blockIdx.x selects
+// admitted x survivors, admitted x admitted; blockIdx.x selects
 // the stage and its row block.
 template <int D, int P, bool FOLD, bool KV>
 __global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
@@ -1006,7 +990,7 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
     case 3: {
       const int nadm = g.N > 0 ? (int)rowsN : 0;
       const unsigned ysplit = cdiv(g.Mcap > g.N ? g.Mcap : g.N, kColsPerSplit);
-      // x: survivor row blocks, admitted row blocks (x evicted or survivors),
+      // x: survivor row blocks, admitted row blocks (x survivors),
       // admitted row blocks x two half column splits (x admitted)
       k_maint_mfma<D, P, F, KV><<<dim3(rowsM + 3 * nadm, ysplit, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, (int)rowsM,
                                                                               nadm);

@@ -29,7 +29,6 @@ struct Workspace {
   float *cnorm;        // [B, N]   |k_x|^2 of candidates
   float *bs;           // [B, Mcap] score scale of each bank state
   int64_t *acol;       // [B, N]   S_x
-  int64_t *wcol;       // [B, N]   sum_i W_ix over the whole pre-update bank
   int32_t *order;      // [B, N]   pi
   int32_t *rank;       // [B, N]   position of x in pi
   int32_t *first;      // [B, Mcap] first crossing prefix length
@@ -41,8 +40,7 @@ struct Workspace {
   int32_t *adm_list;   // [B, N]   admitted source indices ascending
   int32_t *adm_dest;   // [B, N]   final slot of each admitted candidate
   int64_t *sub;        // [B, Mcap] sum of weights to the evicted states (survivors)
-  int64_t *sub_adm;    // [B, N]   admitted: sum of weights to the evicted states if
-                       //          n_ev <= n_surv, else to the survivors
+  int64_t *sub_adm;    // [B, N]   admitted: sum of weights to the survivors
   int64_t *mut_adm;    // [B, N]   admitted: sum of weights to the other admitted
   int32_t *hole_list;  // [B, Mcap] holes closed by moving states (states violating before the update)
   uint16_t *sk;        // [B, N, d] bf16 candidate keys in score order

@@ -151,7 +151,6 @@ __global__ __launch_bounds__(kThreads) void k_begin(dkv_bank bank, const void *s
         ws.caug[nb + j] = column_aug(s, inv_s2);
       }
       ws.acol[nb + j] = 0;
-      ws.wcol[nb + j] = 0;
       ws.sub_adm[nb + j] = 0;
       ws.mut_adm[nb + j] = 0;
     }
@@ -246,7 +245,7 @@ __global__ __launch_bounds__(kThreads) void k_score_gram(dkv_bank bank, const vo
     load_row<D, DT>(kr, seg_k, (size_t)b * g.N + x);
     nr = ws.cnorm[(size_t)b * g.N + x];
   }
-  uint64_t A = 0, Wsum = 0;
+  uint64_t A = 0;
   for (int i0 = 0; i0 < m; i0 += kTile) {
     const int nc = min(kTile, m - i0);
     __syncthreads();
@@ -261,22 +260,19 @@ __global__ __launch_bounds__(kThreads) void k_score_gram(dkv_bank bank, const vo
     }
     __syncthreads();
     if (act) {
-      uint32_t a32 = 0, w32 = 0;
+      uint32_t a32 = 0;
       for (int c = 0; c < nc; ++c) {
         const float gd = dot_row<D>(kr, tk[c]);
         const float d2 = (nr + tn[c]) - 2.0f * gd;
         const float w = pair_weight(d2, p.inv_sigma2, p.p);
         a32 += q23_round(w, tb[c]);
-        w32 += q23_round(w, 8388608.0f);
       }
       A += a32;
-      Wsum += w32;
     }
   }
   if (!act) return;
   const size_t o = (size_t)b * g.N + x;
   ws.acol[o] = (int64_t)A;
-  ws.wcol[o] = (int64_t)Wsum;
   if (out_q) out_q[o] = (int64_t)A;
   if (out_f) out_f[o] = m > 0 ? (float)(ldexp((double)A, ws.E[b] - 23) / (double)m) : 0.0f;
 }
@@ -787,8 +783,7 @@ __global__ __launch_bounds__(kBig) void k_select(dkv_bank bank, Geom g, Workspac
 // ---------------------------------------------------------------------------
 // k_maint_gram: virtual rows [0, Mcap) = pre-update slots (survivors),
 // [Mcap, Mcap + N) = admitted list entries.  Survivors: sum of weights to the
-// evicted states.  Admitted: sum of weights to the evicted states (when there
-// are no more of them than survivors; else to the survivors) and to the other
+// evicted states.  Admitted: sum of weights to the survivors and to the other
 // admitted candidates (self excluded by index).
 // ---------------------------------------------------------------------------
 template <int D, int DT>
@@ -797,7 +792,6 @@ __global__ __launch_bounds__(kThreads) void k_maint_gram(dkv_bank bank, const vo
   const int b = blockIdx.y, v = blockIdx.x * kThreads + threadIdx.x;
   const int m = ws.m[b], n_ev = ws.n_ev[b];
   const int n_surv = m - n_ev;
-  const bool by_ev = n_ev <= n_surv;
   const int rs = ws.r_star[b / g.gs];
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
   bool surv = false, adm = false;
@@ -820,16 +814,16 @@ __global__ __launch_bounds__(kThreads) void k_maint_gram(dkv_bank bank, const vo
     load_row<D, DT>(kr, seg_k, nb + x);
     nr = ws.cnorm[nb + x];
   }
-  // pass 0: evicted columns (survivor rows, and admitted rows when by_ev)
-  // pass 1: survivor columns (admitted rows when !by_ev)
+  // pass 0: evicted columns (survivor rows)
+  // pass 1: survivor columns (admitted rows)
   // pass 2: admitted columns (admitted rows)
   int64_t s_base = 0, s_adm = 0;
   for (int pass = 0; pass < 3; ++pass) {
     int ncol;
-    if (pass == 0) ncol = (any_surv || (any_adm && by_ev)) ? n_ev : 0;
-    else if (pass == 1) ncol = (any_adm && !by_ev) ? n_surv : 0;
+    if (pass == 0) ncol = any_surv ? n_ev : 0;
+    else if (pass == 1) ncol = any_adm ? n_surv : 0;
     else ncol = any_adm ? rs : 0;
-    const bool use = pass == 0 ? (surv || (adm && by_ev)) : adm;
+    const bool use = pass == 0 ? surv : adm;
     for (int j0 = 0; j0 < ncol; j0 += kTile) {
       const int nc = min(kTile, ncol - j0);
       __syncthreads();
@@ -951,12 +945,8 @@ __device__ __forceinline__ void commit_adm(const dkv_bank &bank, const dkv_segme
                                             (cc - (isv ? kCh : 0)));
   }
   if (j == 0) {
-    // density over the final bank: survivors (directly, or the whole old bank
-    // minus the evicted) plus the other co-admitted candidates
-    const int m = ws.m[b];
-    const int n_ev = ws.n_ev[b];
-    const int64_t surv_sum = (n_ev <= m - n_ev) ? ws.wcol[nb + x] - ws.sub_adm[nb + k] : ws.sub_adm[nb + k];
-    const int64_t rho = surv_sum + ws.mut_adm[nb + k];
+    // density over the final bank: the survivors plus the other co-admitted candidates
+    const int64_t rho = ws.sub_adm[nb + k] + ws.mut_adm[nb + k];
     bank.rho[rb + to] = rho;
     bank.base[rb + to] = rho > p.delta_q ? rho : p.delta_q;
     bank.prov[rb + to] = ((int64_t)p.block_id << 32) | (int64_t)x;
