@@ -206,7 +206,7 @@ __device__ __forceinline__ void stage_barrier() { asm volatile("s_barrier" ::: "
 
 // u for both 32-item tiles of a stage: A fragments from the swizzled key rows
 // and the aug step, two interleaved MFMA chains.
-template <int D>
+template <int D, int AHEAD>
 __device__ __forceinline__ void stage_u(const char *kb, const char *ab, const RowFrag<D> &rf, f32x16 &u0,
                                         f32x16 &u1) {
   constexpr int KS = TileCfg<D>::kSteps;
@@ -230,8 +230,66 @@ __device__ __forceinline__ void stage_u(const char *kb, const char *ab, const Ro
     x0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[kk], rf.b[kk], x0, 0, 0, 0);
     x1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[kk], rf.b[kk], x1, 0, 0, 0);
   }
+  // AHEAD > 0: keep AHEAD fragment reads in flight ahead of the MFMAs (the LDS
+  // latency is several MFMAs long), i.e. AHEAD reads, then one MFMA and one read
+  // at a time; 0 leaves the order to the compiler (kernels with less register room)
+  if constexpr (AHEAD > 0) {
+    constexpr int kFrags = 2 * (KS + 1), kAhead = kFrags < AHEAD ? kFrags : AHEAD;
+    __builtin_amdgcn_sched_group_barrier(0x100, kAhead, 0);  // LDS reads
+#pragma unroll
+    for (int i = 0; i < kFrags - kAhead; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kAhead, 0);
+  }
   u0 = x0;
   u1 = x1;
+}
+
+// Tile-granular software pipeline of the Gram stages (descriptors of up to 128
+// elements): the 9 MFMAs of the next 32-column tile are issued interleaved with
+// the epilogue of the current tile, so that one wave keeps the matrix cores and
+// the VALU busy at the same time instead of relying on other waves.
+// frag_offsets: byte offsets of this lane's A fragments in a stage buffer
+// (tile 0; tile 1 is 32 rows further: rows r and r + 32 share the swizzle).
+template <int D>
+__device__ __forceinline__ void frag_offsets(int (&off)[TileCfg<D>::kSteps]) {
+  static_assert(32 % SCfg<D>::CH == 0, "rows r and r + 32 share the swizzle");
+  const int l = threadIdx.x & 63, h = l >> 5, r0 = l & 31;
+#pragma unroll
+  for (int kk = 0; kk < TileCfg<D>::kSteps; ++kk) off[kk] = r0 * SCfg<D>::RB + 16 * ((2 * kk + h) ^ (r0 % SCfg<D>::CH));
+}
+// The exact t = 1 + d2 / sigma^2 of one 32-column tile (half 0 or 1 of a
+// stage): the column items' A fragments from LDS times the row fragment, one
+// MFMA chain
+template <int D>
+__device__ __forceinline__ f32x16 tile_mfma(const char *kb, const char *ab, int half, const RowFrag<D> &rf,
+                                            const int (&off)[TileCfg<D>::kSteps]) {
+  constexpr int KS = TileCfg<D>::kSteps;
+  const int r0 = threadIdx.x & 31;
+  bf16x8 a[KS + 1];
+#pragma unroll
+  for (int kk = 0; kk < KS; ++kk)
+    a[kk] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(kb + 32 * half * SCfg<D>::RB + off[kk]));
+  a[KS] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(ab + 16 * (32 * half + r0)));
+  f32x16 x = {};
+#pragma unroll
+  for (int kk = 0; kk <= KS; ++kk) x = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], rf.b[kk], x, 0, 0, 0);
+  return x;
+}
+// Scheduling of the region that holds one tile_mfma and one tile epilogue:
+// LEAD LDS reads first (3 fragments, plus any other reads of the region), then
+// per MFMA one read and a slice of the epilogue.
+template <int D, int LEAD = 3>
+__device__ __forceinline__ void tile_interleave() {
+  __builtin_amdgcn_sched_group_barrier(0x100, LEAD, 0);  // LDS reads
+#pragma unroll
+  for (int i = 0; i <= TileCfg<D>::kSteps; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);  // VALU
+  }
 }
 
 __device__ __forceinline__ int col_of_reg(int i, int h) { return 8 * (i >> 2) + 4 * h + (i & 3); }
@@ -320,7 +378,7 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
       if (t + 3 < ns) stage_rows<D>(rows, (t + 3) * kSI, ncols, row_of);
     }
     f32x16 u0, u1;
-    stage_u<D>(kb, ab, rf, u0, u1);
+    stage_u<D, 0>(kb, ab, rf, u0, u1);
     const int nv0 = ncols - t * kSI;
     uint32_t sa;
     if (nv0 >= kSI) {
@@ -344,10 +402,100 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
     stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k1, a1, s1);
     if (ns > 2) stage_rows<D>(rows, 2 * kSI, ncols, row_of);
   }
+  if constexpr (D <= 128) {
+    // Tile-granular software pipeline (see tile_interleave).  Iteration t: tile 1
+    // of stage t with the epilogue of tile 0 (the score scales of both tiles
+    // read from stage t's buffer meanwhile); the wait for stage t + 1 and the
+    // barrier; stage t + 3 issued into stage t's buffers; tile 0 of stage t + 1
+    // with the epilogue of tile 1.
+    int aoff[TileCfg<D>::kSteps];
+    frag_offsets<D>(aoff);
+    auto load_bs = [&](const float *tb, float (&bsv)[16]) __attribute__((always_inline)) {
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        const float4 v = *reinterpret_cast<const float4 *>(&tb[8 * gq + 4 * h]);
+        bsv[4 * gq + 0] = v.x;
+        bsv[4 * gq + 1] = v.y;
+        bsv[4 * gq + 2] = v.z;
+        bsv[4 * gq + 3] = v.w;
+      }
+    };
+    auto epi_full = [&](const f32x16 &u, const float (&bsv)[16]) __attribute__((always_inline)) -> uint32_t {
+      uint32_t sa = 0;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float tt = FOLD ? u[i] : 1.0f + u[i];
+        float tp = tt;
+        if constexpr (P >= 2) tp = tt * tt;
+        if constexpr (P == 4) tp = tp * tp;
+        const float w = clamp_weight(rcp_rn(tp));
+        sa += __float_as_uint(__builtin_fmaf(w, bsv[i], 8388608.0f));
+      }
+      return sa - 16u * kMagic;
+    };
+    f32x16 u;
+    auto pstep = [&](int t, const char *kc, const char *ac, const float *sc, const char *kn, const char *an, char *kd,
+                     char *ad, float *sd) __attribute__((always_inline)) {
+      float b0[16], b1[16];
+      load_bs(sc, b0);
+      load_bs(sc + kCT, b1);
+      f32x16 xx = tile_mfma<D>(kc, ac, 1, rf, aoff);
+      uint32_t sa = epi_full(u, b0);
+      tile_interleave<D, 11>();  // the 8 score-scale reads lead
+      asm volatile("" : "+v"(sa));  // the epilogue of tile 0 stays beside the MFMAs of tile 1
+      u = xx;
+      if (t + 2 < ns) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kOps));
+      else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+      stage_barrier();
+      if (t + 3 < ns) {
+        stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, kd, ad, sd);
+        if (t + 4 < ns) stage_rows<D>(rows, (t + 4) * kSI, ncols, row_of);
+      }
+      xx = tile_mfma<D>(kn, an, 0, rf, aoff);
+      sa += epi_full(u, b1);
+      tile_interleave<D>();
+      u = xx;
+      A64 += sa;
+    };
+    if (ns > 0) {
+      if (ns > 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kOps));
+      else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+      stage_barrier();
+      if (ns > 2) {
+        stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k2, a2, s2);
+        if (ns > 3) stage_rows<D>(rows, 3 * kSI, ncols, row_of);
+      }
+      u = tile_mfma<D>(k0, a0, 0, rf, aoff);
+    }
+    for (int t = 0; t + 1 < ns; t += 3) {
+      pstep(t, k0, a0, s0, k1, a1, k0, a0, s0);
+      if (t + 2 < ns) pstep(t + 1, k1, a1, s1, k2, a2, k1, a1, s1);
+      if (t + 3 < ns) pstep(t + 2, k2, a2, s2, k0, a0, k2, a2, s2);
+    }
+    if (ns > 0) {  // the last stage (possibly partial): u holds its tile 0
+      const int t = ns - 1;
+      const int nv0 = ncols - t * kSI;
+      // one call per buffer: the LDS arrays stay compile-time known
+      auto last = [&](const char *kb, const char *ab, const float *sb) __attribute__((always_inline)) {
+        uint32_t sa;
+        epi(Part{}, u, sb, nv0, sa);
+        A64 += sa;
+        if (nv0 > kCT) {
+          const f32x16 xx = tile_mfma<D>(kb, ab, 1, rf, aoff);
+          epi(Part{}, xx, sb + kCT, nv0 - kCT, sa);
+          A64 += sa;
+        }
+      };
+      if (t % 3 == 0) last(k0, a0, s0);
+      else if (t % 3 == 1) last(k1, a1, s1);
+      else last(k2, a2, s2);
+    }
+  } else {
   for (int t = 0; t < ns; t += 3) {
     step(t, k0, a0, s0, k2, a2, s2);
     if (t + 1 < ns) step(t + 1, k1, a1, s1, k0, a0, s0);
     if (t + 2 < ns) step(t + 2, k2, a2, s2, k1, a1, s1);
+  }
   }
   const uint64_t At = A64 + __shfl_xor(A64, 32, 64);
   if (!rv || h != 0) return;
@@ -487,6 +635,10 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   constexpr bool kColSplit = KV && !(MODE == RS_CHUNK || MODE == RS_FIXUP);
   const uint4 *colaug = (MODE == RS_CHUNK || MODE == RS_FIXUP) ? ws.saug : (MODE == RS_ADM_MUT ? ws.caug : ws.baug);
   constexpr bool kDiag = (MODE == RS_ADM_MUT || MODE == RS_DENSITY);
+  // fragment reads kept ahead of the MFMAs where the registers allow it
+  constexpr int kStageAhead = (D <= 128 && (MODE == RS_CHUNK || MODE == RS_FIXUP || MODE == RS_DENSITY)) ? 4 : 0;
+  // the prefix-chunk Gram runs software-pipelined (below)
+  constexpr bool kPipe = MODE == RS_CHUNK && D <= 128;
   uint64_t S64 = 0;
   uint32_t chunk_sum = 0;
   const int ncols = c1 - c0;
@@ -567,7 +719,7 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
       if (t > 0) flush_cols(t - 1);
     }
     f32x16 u0, u1;
-    stage_u<D>(kb, ab, rf, u0, u1);
+    stage_u<D, kStageAhead>(kb, ab, rf, u0, u1);
     const int nv0 = ncols - t * kSI;
     const int j0 = c0 + t * kSI;
     uint32_t s2;
@@ -603,6 +755,85 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
       stage_dma<D, false, kColSplit>(rowsB, colbase, colaug, nullptr, sb.k1, sb.a1, nullptr);
       if (ns > 2) stage_rows<D>(rowsA, 2 * kSI, ncols, row_of_rel);
     }
+  }
+  if constexpr (kPipe) {
+    // Software pipeline of the prefix-chunk Gram at the granularity of one
+    // 32-column tile: the MFMAs of the next tile run interleaved with the
+    // epilogue of the current one, so that one wave keeps the matrix cores and
+    // the VALU busy at the same time.  Stage s (tiles 2 s, 2 s + 1) uses
+    // buffers s % 3 and rows (s even ? rowsA : rowsB).  Iteration t: tile 1
+    // of stage t with the epilogue of tile 0; then the wait for stage t + 1,
+    // the barrier (every wave is done with the buffers of stage t), stage t + 3
+    // issued into them, and tile 0 of stage t + 1 with the epilogue of tile 1.
+    static_assert(kCkStride == kSI, "one prefix chunk per stage");
+    int aoff[TileCfg<D>::kSteps];
+    frag_offsets<D>(aoff);
+    auto tile_mfma_ = [&](const char *kb, const char *ab, int half) __attribute__((always_inline)) -> f32x16 {
+      return tile_mfma<D>(kb, ab, half, rf, aoff);
+    };
+    auto store_chunk = [&](int t, uint32_t s2) __attribute__((always_inline)) {
+      const uint32_t tot = s2 + __shfl_xor(s2, 32, 64);
+      if (rv && h == 0) ws.ck[(rb + v) * ws.nck + ((c0 + t * kSI) / kCkStride)] = tot;
+    };
+    f32x16 u;
+    // iteration t for a full stage t that is not the last
+    auto pstep = [&](int t, const char *kc, const char *ac, const char *kn, const char *an, char *kd, char *ad,
+                     Rows &use, Rows &fill) __attribute__((always_inline)) {
+      f32x16 x = tile_mfma_(kc, ac, 1);
+      uint32_t s2 = lane_wsum<P, false, FOLD>(u, kCT, h);
+      tile_interleave<D>();
+      asm volatile("" : "+v"(s2));  // the epilogue of tile 0 stays beside the MFMAs of tile 1
+      u = x;
+      if (t + 2 < ns) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kOps));
+      else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+      stage_barrier();
+      if (t + 3 < ns) {
+        if (t + 4 < ns) stage_rows<D>(fill, (t + 4) * kSI, ncols, row_of_rel);
+        stage_dma<D, false, kColSplit>(use, colbase, colaug, nullptr, kd, ad, nullptr);
+      }
+      x = tile_mfma_(kn, an, 0);
+      s2 += lane_wsum<P, false, FOLD>(u, kCT, h);
+      tile_interleave<D>();
+      u = x;
+      store_chunk(t, s2);
+    };
+    if (ns > 0) {
+      if (ns > 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kOps));
+      else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+      stage_barrier();
+      if (ns > 2) {
+        if (ns > 3) stage_rows<D>(rowsB, 3 * kSI, ncols, row_of_rel);
+        stage_dma<D, false, kColSplit>(rowsA, colbase, colaug, nullptr, sb.k2, sb.a2, nullptr);
+      }
+      u = tile_mfma_(sb.k0, sb.a0, 0);
+    }
+    // iteration t: stage t in buffers t % 3, stage t + 1 in (t + 1) % 3, stage t + 3
+    // issued into t % 3 with rows (t odd ? rowsA : rowsB), rows of t + 4 fetched
+    for (int t = 0; t + 1 < ns; t += 6) {
+      pstep(t, sb.k0, sb.a0, sb.k1, sb.a1, sb.k0, sb.a0, rowsB, rowsA);
+      if (t + 2 < ns) pstep(t + 1, sb.k1, sb.a1, sb.k2, sb.a2, sb.k1, sb.a1, rowsA, rowsB);
+      if (t + 3 < ns) pstep(t + 2, sb.k2, sb.a2, sb.k0, sb.a0, sb.k2, sb.a2, rowsB, rowsA);
+      if (t + 4 < ns) pstep(t + 3, sb.k0, sb.a0, sb.k1, sb.a1, sb.k0, sb.a0, rowsA, rowsB);
+      if (t + 5 < ns) pstep(t + 4, sb.k1, sb.a1, sb.k2, sb.a2, sb.k1, sb.a1, rowsB, rowsA);
+      if (t + 6 < ns) pstep(t + 5, sb.k2, sb.a2, sb.k0, sb.a0, sb.k2, sb.a2, rowsA, rowsB);
+    }
+    // the last stage (possibly partial); u holds its tile 0
+    if (ns > 0) {
+      const int t = ns - 1;
+      const int nv0 = ncols - t * kSI;
+      const int j0 = c0 + t * kSI;
+      uint32_t s2 = tile_sum(u, j0, nv0);
+      if (nv0 > kCT) {
+        // one call per buffer: the LDS arrays stay compile-time known (no generic pointers)
+        f32x16 x;
+        if (t % 3 == 0) x = tile_mfma_(sb.k0, sb.a0, 1);
+        else if (t % 3 == 1) x = tile_mfma_(sb.k1, sb.a1, 1);
+        else x = tile_mfma_(sb.k2, sb.a2, 1);
+        s2 += tile_sum(x, j0 + kCT, nv0 - kCT);
+      }
+      store_chunk(t, s2);
+    }
+    return;
   }
   // step t issues stage t + 2 with the rows fetched at step t - 1 and fetches
   // those of stage t + 3: stage t + 2 uses rowsA when t is even
