@@ -166,16 +166,12 @@ def _properties(bank, out, prm, m_prev, base_prev, prints, gs, N, ctx):
 
 
 def _golden(name, layer):
-    """Digests of (workload, sampled layer) at the stated length, else those of a
-    shorter run of the same layer (the first blocks of the same rollout)."""
-    for stem in (f"rollout_{name}_L{layer}", f"rollout_{name}"):
-        path = os.path.join(GOLDEN, stem + ".json")
-        if os.path.exists(path):
-            with open(path) as f:
-                gold = json.load(f)
-            if gold["layer"] == layer:
-                return gold, np.load(os.path.join(GOLDEN, stem + "_attention.npy"))
-    return None, None
+    """Oracle digests of (workload, sampled layer) over the workload's stated length."""
+    stem = os.path.join(GOLDEN, f"rollout_{name}_L{layer}")
+    if not os.path.exists(stem + ".json"):
+        return None, None
+    with open(stem + ".json") as f:
+        return json.load(f), np.load(stem + "_attention.npy")
 
 
 @pytest.mark.parametrize("name,layer", cases(), ids=[f"{n}-L{ly}" for n, ly in cases()])
@@ -185,6 +181,7 @@ def test_full_size_workload(name, layer):
         pytest.skip(f"oracle digests for {name} layer {layer} not generated")
     cfg = synth.WORKLOADS[name]
     blocks, att_heads = gold["blocks"], gold["attention_heads"]
+    assert gold["layer"] == layer and blocks == cfg.blocks, "digests of a shorter run"
     H, d, N, gs = cfg.heads, cfg.d, cfg.n_cand, cfg.group_size
     B = cfg.layers * H
     print(f"workload {name}: {B} banks, {blocks} blocks, sampled layer {layer}", flush=True)
