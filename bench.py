@@ -32,6 +32,7 @@ before every step.
 
 import argparse
 import hashlib
+import gc
 import json
 import os
 import re
@@ -251,6 +252,9 @@ def run_rollout(args, api, synth, torch):
         if i == total - 1:
             t_end.record(stream)
     torch.cuda.synchronize()
+    seq = bool(prm.flags & api.POLICY_SEQUENTIAL)
+    if seq and bool((rs_hist < 0).any()):
+        raise SystemExit("a group's sequential walk gave up waiting for its records (r_star = -1)")
     timed = [t for _, t in schedule[args.warmup:total]]
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / args.steps
@@ -321,6 +325,10 @@ def run_rollout(args, api, synth, torch):
             "commit_bytes_total": int(commit_bytes.sum()),
         },
     }
+    if seq:   # the Gram accounting is the default update's; the sequential walk has its own
+        for k in ("update_gram_tflop", "update_gram_tflops", "update_gram_frac_of_bf16_peak",
+                  "median_update_gram_frac_of_bf16_peak"):
+            result["rollout"][k] = None
     del kv, qs, out, bank, ws
     torch.cuda.empty_cache()
     return result
@@ -440,6 +448,8 @@ def run_single(args, api, synth, torch):
         step(k, evs[k])
     t_end.record(stream)
     torch.cuda.synchronize()
+    if args.policy == "sequential" and bool((rs_hist < 0).any()):
+        raise SystemExit("a group's sequential walk gave up waiting for its records (r_star = -1)")
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / args.steps
     upd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
@@ -494,7 +504,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
-                                   "(banks shard by layer without communication; see the design notes)"}))
+                                   "(the banks of different layers would shard across GPUs with no communication)"}))
         sys.exit(2)
     import torch
     from paper_2608_27922_amd import api, synth
@@ -517,7 +527,14 @@ def main():
             torch.neg(src, out=dst)      # reads and writes nbytes each
         torch.cuda.synchronize()
         result["copy_probe_bytes"] = nbytes
+        del src, dst
     print(json.dumps(result), flush=True)
+    # Return every device allocation while the runtime (and any profiler attached
+    # to it) is fully up, rather than leaving it to the process's exit handlers.
+    torch.cuda.synchronize()
+    gc.collect()
+    torch.cuda.empty_cache()
+    torch.cuda.synchronize()
 
 
 if __name__ == "__main__":

@@ -166,10 +166,16 @@ typedef struct {
  * step drops its candidates.  A bank that is empty at the start of the block
  * takes the empty-bank rule and stays out of the shared test.  Combines with
  * SOURCE_ORDER and REFRESH_BASE only (DKV_ERR_INVALID otherwise); bf16 banks
- * only (DKV_ERR_UNSUPPORTED); group_size <= 256 (DKV_ERR_SHAPE).  The update
- * keeps the pairwise weights of [bank; candidates] in the workspace:
- * densitykv_workspace_size_policy adds num_banks * (capacity + n)^2 * 4 bytes
- * (plus 12 bytes per slot and 8 KiB per group).
+ * only (DKV_ERR_UNSUPPORTED); group_size <= 256 (DKV_ERR_SHAPE).
+ * Workspace: 12 bytes per slot and 8 KiB per group, plus an area for the
+ * pairwise weights of [bank; candidates] of whole groups,
+ * group_size * (capacity + n)^2 * 4 bytes per group.  The groups are updated
+ * in batches of as many as that area holds: densitykv_update_bank takes the
+ * batch from the workspace_bytes it is given (every byte beyond the fixed part
+ * goes to the area; DKV_ERR_WORKSPACE when not even one group fits), and
+ * densitykv_workspace_size_policy asks for the groups that fit in
+ * DKV_SEQ_WEIGHT_BYTES (at least one, at most all).  A larger workspace walks
+ * more groups at once.
  * Outputs: r_star = steps taken, n_admitted / admitted = this block's
  * candidates in the final bank, n_evicted / evicted = pre-update slots whose
  * state left; first_cross and rho_tilde are not written.  The steps are
@@ -178,8 +184,14 @@ typedef struct {
  * device at once; otherwise one workgroup walks the group).  r_star = -1
  * reports a walk whose wait for those records exceeded its bound, leaving
  * the group's banks undefined; with the launch guarantees in place this does
- * not occur. */
+ * not occur.  The call itself cannot report it (the walk runs after the call
+ * returns): a caller that must know passes r_star and reads it after the
+ * stream has completed.  Which walk runs is decided before anything is
+ * enqueued, and every write to a bank comes after the walk's launch. */
 #define DKV_POLICY_SEQUENTIAL 0x20u
+/* Pairwise-weight bytes that densitykv_workspace_size_policy sizes the
+ * sequential competition's batches for (32 GiB). */
+#define DKV_SEQ_WEIGHT_BYTES ((size_t)32 << 30)
 
 /* Optional outputs of densitykv_update_bank (any pointer may be NULL).
  *   r_star       [G]        admitted prefix length of each group (Eq. 11)
@@ -210,8 +222,10 @@ typedef struct {
  * this bank geometry and n_cand candidates per bank.  Host-only; enqueues nothing. */
 int densitykv_workspace_size(const dkv_bank *bank, int32_t n_cand, size_t *bytes);
 
-/* The same for the given dkv_params.flags: larger with DKV_POLICY_SEQUENTIAL,
- * equal to densitykv_workspace_size otherwise.  Host-only. */
+/* The same for the given dkv_params.flags: larger with DKV_POLICY_SEQUENTIAL
+ * (the fixed part plus the pairwise weights of as many whole groups as fit in
+ * DKV_SEQ_WEIGHT_BYTES, at least one), equal to densitykv_workspace_size
+ * otherwise.  Host-only. */
 int densitykv_workspace_size_policy(const dkv_bank *bank, int32_t n_cand, uint32_t flags, size_t *bytes);
 
 /*

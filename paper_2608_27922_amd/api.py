@@ -41,6 +41,7 @@ POLICY_SEQUENTIAL = 0x20    # within-block sequential competition (bf16 banks; l
 
 # Bytes of the static device scratch behind update_bank_noalloc (DKV_NOALLOC_SCRATCH_BYTES).
 NOALLOC_SCRATCH_BYTES = 64 << 20
+SEQ_WEIGHT_BYTES = 32 << 30     # pairwise-weight bytes the sequential workspace size is sized for
 
 ENTRY_POINTS = ("densitykv_workspace_size", "densitykv_workspace_size_policy", "densitykv_score",
                 "densitykv_update_bank", "densitykv_update_bank_noalloc",
@@ -214,8 +215,22 @@ def workspace_size(bank: Bank, n_cand: int, flags: int = 0) -> int:
     return int(out.value)
 
 
-def alloc_workspace(bank: Bank, n_cand: int, flags: int = 0) -> torch.Tensor:
-    return torch.empty(workspace_size(bank, n_cand, flags), dtype=torch.uint8, device=bank.k.device)
+def seq_group_weight_bytes(bank: Bank, n_cand: int) -> int:
+    """Pairwise-weight bytes of one group in the sequential competition."""
+    L = bank.Mcap + max(int(n_cand), 0)
+    return bank.gs * L * L * 4
+
+
+def alloc_workspace(bank: Bank, n_cand: int, flags: int = 0, seq_groups: Optional[int] = None) -> torch.Tensor:
+    """Workspace of densitykv_workspace_size_policy; with POLICY_SEQUENTIAL and
+    `seq_groups`, room for the pairwise weights of that many groups instead
+    (the update then walks that many groups at a time)."""
+    size = workspace_size(bank, n_cand, flags)
+    if seq_groups is not None and flags & POLICY_SEQUENTIAL:
+        per, G = seq_group_weight_bytes(bank, n_cand), bank.B // bank.gs
+        default = min(G, max(1, SEQ_WEIGHT_BYTES // per))
+        size += (min(max(int(seq_groups), 1), G) - default) * per
+    return torch.empty(size, dtype=torch.uint8, device=bank.k.device)
 
 
 def _segment(seg_k: Optional[torch.Tensor], seg_v: Optional[torch.Tensor], n: int, block_id: int):
@@ -274,13 +289,37 @@ class UpdateOut:
                             f(self.evicted), f(self.order), f(self.score_q), f(self.first_cross),
                             f(self.rho_tilde))
 
+    def walk_ok(self) -> bool:
+        """False when a group's sequential walk gave up waiting (r_star = -1);
+        synchronizes with the device."""
+        return bool(torch.all(self.r_star >= 0).item())
+
+
+class _StepCounts(UpdateOut):
+    """r_star alone: what the sequential competition always returns, so that a
+    walk that gave up (r_star = -1) can be seen after the call."""
+
+    def __init__(self, bank: Bank):
+        self.r_star = torch.zeros(bank.B // bank.gs, dtype=torch.int32, device=bank.k.device)
+        self.n_admitted = self.n_evicted = self.admitted = self.evicted = None
+        self.order = self.score_q = self.first_cross = self.rho_tilde = None
+
+
+def _outputs(bank: Bank, params: "Params", out):
+    if out is None and params.flags & POLICY_SEQUENTIAL:
+        return _StepCounts(bank)
+    return out
+
 
 def update_bank(bank: Bank, seg_k: Optional[torch.Tensor], seg_v: Optional[torch.Tensor], block_id: int,
                 params: Params = Params(), workspace: Optional[torch.Tensor] = None,
                 out: Optional[UpdateOut] = None) -> Optional[UpdateOut]:
-    """densitykv_update_bank: updates `bank` in place on the current stream."""
+    """densitykv_update_bank: updates `bank` in place on the current stream.
+    With POLICY_SEQUENTIAL and no `out`, returns an output object holding
+    r_star only (check it with walk_ok() once the stream has run)."""
     n = _check_seg(bank, seg_k, seg_v)
     ws = workspace if workspace is not None else alloc_workspace(bank, n, params.flags)
+    out = _outputs(bank, params, out)
     cb, cs, cp = bank.c(), _segment(seg_k, seg_v, n, block_id), params.c()
     co = out.c() if out is not None else None
     _check(lib().densitykv_update_bank(ctypes.byref(cb), ctypes.byref(cs), ctypes.byref(cp),
@@ -295,6 +334,7 @@ def update_bank_noalloc(bank: Bank, seg_k: Optional[torch.Tensor], seg_v: Option
     device scratch as workspace (no allocation by the call; sizes whose workspace
     exceeds NOALLOC_SCRATCH_BYTES raise DkvError)."""
     n = _check_seg(bank, seg_k, seg_v)
+    out = _outputs(bank, params, out)
     cb, cs, cp = bank.c(), _segment(seg_k, seg_v, n, block_id), params.c()
     co = out.c() if out is not None else None
     _check(lib().densitykv_update_bank_noalloc(ctypes.byref(cb), ctypes.byref(cs), ctypes.byref(cp),

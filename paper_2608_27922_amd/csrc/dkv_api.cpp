@@ -12,7 +12,8 @@ namespace dkv {
 
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base, bool seq) {
+size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base, bool seq,
+                        int seq_groups) {
   size_t off = 0;
   const size_t Bz = (size_t)B, Mz = (size_t)Mcap, Nz = (size_t)(N > 0 ? N : 1);
   // chunk sums per row, padded to a multiple of 4 so that rows are 16-byte aligned
@@ -62,11 +63,14 @@ size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, cha
   w.nck = nck > 0 ? nck : 4;
   if (seq) {
     const size_t L = (size_t)Mcap + (size_t)(N > 0 ? N : 0);
-    w.gram = (uint32_t *)take(Bz * L * L * 4);
     w.grow = (int32_t *)take(Bz * Mz * 4);
     w.lim = (int64_t *)take(Bz * Mz * 8);
     w.seq_rec = (uint64_t *)take((size_t)G * 2 * kSeqMaxMembers * 8 * 8);
     w.gram_ld = (int)L;
+    w.seq_b0 = 0;
+    w.seq_groups = seq_groups;
+    // last: the pairwise weights of seq_groups whole groups
+    w.gram = (uint32_t *)take((size_t)seq_groups * seq_group_weight_bytes(B / G, Mcap, N));
   }
   if (ws) *ws = w;
   return off;
@@ -173,6 +177,31 @@ Geom geom_of(const dkv_bank *bk, int n) {
   return g;
 }
 
+// Groups per batch of the sequential competition: as many whole groups as
+// DKV_SEQ_WEIGHT_BYTES of pairwise weights hold, at least one, at most all.
+int seq_default_groups(const dkv_bank *bank, int n) {
+  const int G = bank->num_banks / bank->group_size;
+  const size_t per = seq_group_weight_bytes(bank->group_size, bank->capacity, n);
+  const size_t fit = per > 0 ? DKV_SEQ_WEIGHT_BYTES / per : (size_t)G;
+  return (int)(fit < 1 ? 1 : (fit > (size_t)G ? (size_t)G : fit));
+}
+
+// The workspace layout of an update on `bytes` of workspace: with the
+// sequential competition, the weight area takes as many whole groups as the
+// bytes beyond the fixed part hold (at most all); 0 groups when not even one
+// fits.  Returns the bytes the layout needs (with at least one group).
+size_t update_layout(const dkv_bank *bank, int n, bool seq, size_t bytes, char *base, Workspace *ws) {
+  const int B = bank->num_banks, G = B / bank->group_size;
+  if (!seq)
+    return workspace_layout(B, G, bank->capacity, n, bank->head_dim, ws, base);
+  const size_t fixed = workspace_layout(B, G, bank->capacity, n, bank->head_dim, nullptr, nullptr, true, 0);
+  const size_t per = seq_group_weight_bytes(bank->group_size, bank->capacity, n);
+  size_t groups = bytes > fixed ? (per > 0 ? (bytes - fixed) / per : (size_t)G) : 0;
+  if (groups > (size_t)G) groups = (size_t)G;
+  workspace_layout(B, G, bank->capacity, n, bank->head_dim, ws, base, true, (int)groups);
+  return fixed + per;
+}
+
 }  // namespace
 
 extern "C" {
@@ -192,8 +221,9 @@ int densitykv_workspace_size_policy(const dkv_bank *bank, int32_t n_cand, uint32
   if (rc) return rc;
   if (!bytes) return DKV_ERR_INVALID;
   if (n_cand < 0 || n_cand > DKV_MAX_CANDIDATES) return DKV_ERR_SHAPE;
+  const bool seq = (flags & DKV_POLICY_SEQUENTIAL) != 0;
   *bytes = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity, n_cand,
-                            bank->head_dim, nullptr, nullptr, (flags & DKV_POLICY_SEQUENTIAL) != 0);
+                            bank->head_dim, nullptr, nullptr, seq, seq ? seq_default_groups(bank, n_cand) : 0);
   return DKV_OK;
 }
 
@@ -225,9 +255,8 @@ int densitykv_update_bank(dkv_bank *bank, const dkv_segment *seg, const dkv_para
   if (!rc) rc = check_geometry(bank, seg, p);
   if (rc) return rc;
   Workspace ws{};
-  const size_t need = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity,
-                                       seg->n, bank->head_dim, &ws, static_cast<char *>(workspace),
-                                       (p.flags & DKV_POLICY_SEQUENTIAL) != 0);
+  const size_t need = update_layout(bank, seg->n, (p.flags & DKV_POLICY_SEQUENTIAL) != 0, workspace_bytes,
+                                    static_cast<char *>(workspace), &ws);
   if (!workspace || workspace_bytes < need) return DKV_ERR_WORKSPACE;
   const Geom g = geom_of(bank, seg->n);
   hipError_t e = launch_update(*bank, *seg, g, p, out, ws, static_cast<hipStream_t>(stream));
@@ -242,9 +271,7 @@ int densitykv_update_bank_noalloc(dkv_bank *bank, const dkv_segment *seg, const 
   if (!rc) rc = check_params(prm, &p, seg->block_id);
   if (!rc) rc = check_geometry(bank, seg, p);
   if (rc) return rc;
-  const size_t need = workspace_layout(bank->num_banks, bank->num_banks / bank->group_size, bank->capacity,
-                                       seg->n, bank->head_dim, nullptr, nullptr,
-                                       (p.flags & DKV_POLICY_SEQUENTIAL) != 0);
+  const size_t need = update_layout(bank, seg->n, (p.flags & DKV_POLICY_SEQUENTIAL) != 0, 0, nullptr, nullptr);
   if (need > DKV_NOALLOC_SCRATCH_BYTES) return DKV_ERR_SCRATCH;
   void *ws = nullptr;
   rc = current_device_scratch(&ws);

@@ -209,7 +209,14 @@ __global__ __launch_bounds__(64 * kFWaves, 1) void k_attn_mfma(dkv_bank bank, co
   // direct-to-LDS loads per thread for one K + V tile
   constexpr int kTileLoads = 2 * (FCfg<D>::kLoadsPerTile / kFWaves);
   static_assert(FCfg<D>::kLoadsPerTile % kFWaves == 0, "tile loads must split evenly over the waves");
-  const int b = blockIdx.y;
+  // Workgroup L is dispatched to XCD L % 8.  Rank the workgroups XCD by XCD
+  // (p = workgroups on lower XCDs + L / 8) and give rank p bank p / nqb, query
+  // block p % nqb: the query blocks of a bank then run on one XCD and share
+  // its L2 for the bank's keys and values.
+  const int nqb = (nq + kFQ - 1) / kFQ;
+  const int T = (int)gridDim.x, L = (int)blockIdx.x, xcd = L % 8;
+  const int p = xcd * (T / 8) + min(xcd, T % 8) + L / 8;
+  const int b = p / nqb, qblk = p % nqb;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
   const int M = clampi(bank.budget[b], 0, g.Mcap);
   const int m = clampi(bank.occupancy[b], 0, M);
@@ -225,7 +232,7 @@ __global__ __launch_bounds__(64 * kFWaves, 1) void k_attn_mfma(dkv_bank bank, co
   __shared__ __attribute__((aligned(1024))) char k0[TB], k1[TB], k2[TB];
   __shared__ __attribute__((aligned(1024))) char v0[TB], v1[TB], v2[TB];
 
-  const int qi = blockIdx.x * kFQ + wave * 32 + n;
+  const int qi = qblk * kFQ + wave * 32 + n;
   const bool qv = qi < nq;
   bf16x8 qf[KS];
   const size_t qrow = (size_t)b * nq + (qv ? qi : 0);
@@ -385,7 +392,9 @@ hipError_t attn_impl(const dkv_bank &bank, const void *q, int nq, KvSeg win, KvS
   if (nq <= 0) return hipSuccess;
   const float scale_log2 = scale * 1.4426950408889634f;
   if constexpr (DT == DKV_BF16) {
-    dim3 grid((unsigned)((nq + kFQ - 1) / kFQ), (unsigned)g.B);
+    const long long nwg = (long long)((nq + kFQ - 1) / kFQ) * g.B;   // one-dimensional grid
+    if (nwg > 0x7fffffffLL) return hipErrorInvalidConfiguration;
+    dim3 grid((unsigned)nwg);
     k_attn_mfma<D><<<grid, 64 * kFWaves, 0, s>>>(bank, static_cast<const uint16_t *>(q), nq,
                                                  win, sink, static_cast<uint16_t *>(out), scale_log2, g);
   } else {

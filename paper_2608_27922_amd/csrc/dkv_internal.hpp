@@ -54,14 +54,25 @@ struct Workspace {
   int npad;            // N rounded up to 512
   int nck;
   // sequential competition only (null otherwise)
-  uint32_t *gram;      // [B, L, L] W between the items [slots 0..Mcap); candidates 0..N)], L = Mcap + N
+  uint32_t *gram;      // [Bw, L, L] W between the items [slots 0..Mcap); candidates 0..N)], L = Mcap + N,
+                       // for the Bw banks seq_b0 .. seq_b0 + Bw - 1 of the batch being walked
   int32_t *grow;       // [B, Mcap] item of the state in each slot (slot s, or Mcap + candidate)
   int64_t *lim;        // [B, Mcap] ceil(T b / 2^k): the state violates when rho + W reaches it
   uint64_t *seq_rec;   // [G, 2, kSeqMaxMembers, 8] per-step records of the workgroups of a group
   int gram_ld;         // L
+  int seq_b0;          // first bank of the batch whose weights gram holds
+  int seq_groups;      // groups per batch (whole groups whose weights fit in gram)
 };
 
-size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base, bool seq = false);
+// seq_groups: groups whose pairwise weights the sequential competition's area
+// holds (0 for none); the area comes last, after every fixed-size array.
+size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, char *base, bool seq = false,
+                        int seq_groups = 0);
+// Bytes of the pairwise weights of one group in the sequential competition.
+inline size_t seq_group_weight_bytes(int gs, int Mcap, int N) {
+  const size_t L = (size_t)Mcap + (size_t)(N > 0 ? N : 0);
+  return (size_t)gs * L * L * 4;
+}
 constexpr int kSeqMaxGroup = 256;  // banks per group in the sequential competition
 constexpr int kSeqMaxMembers = 64;  // workgroups per group in the multi-workgroup walk
 

@@ -3,19 +3,23 @@
 // offered one at a time, in the order fixed at the start of the block, and
 // every step is decided against the banks as the earlier steps left them.
 //
+// The groups run in batches of whole groups (as many as the workspace's
+// weight area holds); per batch:
 //   k_seq_gram    W between every pair of items of a bank, the items being its
 //                 slots 0..Mcap-1 (pre-update states) and its candidates, on
-//                 bf16 MFMA (32 x 32 tiles), stored as [B, L, L] uint32 with
-//                 L = Mcap + N
-//   k_seq_setup   per bank: slot items and violation limits, or the
-//                 empty-bank rule for a bank that starts empty
+//                 bf16 MFMA (32 x 32 tiles), stored as [batch banks, L, L]
+//                 uint32 with L = Mcap + N
+//   k_seq_setup   per bank, in the workspace: slot items and violation
+//                 limits, or the items of the empty-bank rule for a bank that
+//                 starts empty
 //   k_seq_coop    the steps, several workgroups per group (cooperative
 //                 launch): each holds up to 2,048 slots of one bank in
 //                 registers; per step the one-candidate violator test of its
 //                 slots, one record per workgroup exchanged through global
 //                 memory, the shared decision, and on a taken step the
 //                 release, the exact density maintenance and the new state
-//   k_seq_results per bank: refreshed baselines, admitted and released lists
+//   k_seq_results per bank: the states of a bank that started empty,
+//                 refreshed baselines, admitted and released lists
 //   k_seq         the same steps in one workgroup per group (one wave per
 //                 bank, the state in the bank arrays), for groups the
 //                 cooperative walk does not take
@@ -45,6 +49,12 @@ __device__ __forceinline__ uint32_t weight_q(float d2, const Prm &p) {
 // Register q of a 32 x 32 MFMA tile holds column 8 (q / 4) + 4 h + q % 4.
 __device__ __forceinline__ int tile_col(int q, int h) { return 8 * (q >> 2) + 4 * h + (q & 3); }
 
+// Pairwise weights of bank b, one of the banks of the batch being walked.
+__device__ __forceinline__ const uint32_t *bank_gram(const Workspace &ws, int b) {
+  const size_t L = (size_t)ws.gram_ld;
+  return ws.gram + (size_t)(b - ws.seq_b0) * L * L;
+}
+
 // ---------------------------------------------------------------------------
 // k_seq_gram: workgroup = 4 waves = 32 row items x kGramCols column items; a
 // wave keeps its 32 row keys (the B operand) in registers and walks
@@ -58,7 +68,7 @@ constexpr int kGramCols = 512;
 template <int D>
 __global__ __launch_bounds__(256) void k_seq_gram(dkv_bank bank, dkv_segment seg, Geom g, Prm p, Workspace ws) {
   constexpr int KS = D / 16;
-  const int b = blockIdx.z;
+  const int b = ws.seq_b0 + (int)blockIdx.z;  // bank blockIdx.z of the batch
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
   const int L = ws.gram_ld, Mcap = g.Mcap, m = ws.m[b];
   auto live = [&](int u) { return u < Mcap ? u < m : u < Mcap + g.N; };
@@ -88,7 +98,7 @@ __global__ __launch_bounds__(256) void k_seq_gram(dkv_bank bank, dkv_segment seg
   // W is symmetric (the same products summed in the same order, and |a|^2 +
   // |b|^2 commutes), so W(ru, u) is stored at [u][ru]: the 32 lanes of a half
   // write 32 consecutive entries of one row.
-  uint32_t *col = ws.gram + (size_t)b * L * L + ru;
+  uint32_t *col = ws.gram + (size_t)blockIdx.z * L * L + ru;
   for (int c0 = blockIdx.x * kGramCols + wave * 32; c0 < min(L, (int)(blockIdx.x + 1) * kGramCols); c0 += 128) {
     if (!any_live(c0)) continue;  // uniform over the wave
     const int cu = c0 + n;  // this lane's column item (A operand)
@@ -156,12 +166,13 @@ __device__ __forceinline__ int64_t lim_of(int64_t base, const Prm &p) {
   return ((int64_t)p.tau_num * base + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
 }
 
-// Set-up of bank b by one wave: per-slot items and limits of a bank that holds
-// states; a bank that is empty takes the empty-bank rule (the first min(N, M)
-// candidates in source order, densities over that bank; Alg. 1, first branch).
-// Returns the occupancy the steps start from.
+// Set-up of bank b by one wave, in the workspace only: per-slot items and
+// limits of a bank that holds states; for a bank that is empty, the items of
+// the empty-bank rule (the first min(N, M) candidates in source order; Alg. 1,
+// first branch), whose states seq_empty_commit writes.  Returns the occupancy
+// the steps start from.
 __device__ int seq_setup_bank(const dkv_bank &bank, const Geom &g, const Prm &p, const Workspace &ws, int b, int l) {
-  const int L = ws.gram_ld, Mcap = g.Mcap, N = g.N;
+  const int Mcap = g.Mcap, N = g.N;
   const size_t rb = (size_t)b * Mcap;
   const int m0 = ws.m[b];
   if (m0 > 0) {
@@ -172,23 +183,32 @@ __device__ int seq_setup_bank(const dkv_bank &bank, const Geom &g, const Prm &p,
     return m0;
   }
   const int na = min(N, ws.M[b]);
+  for (int x = l; x < na; x += 64) ws.grow[rb + x] = Mcap + x;
+  return na;
+}
+
+// The states of a bank that was empty at the start of the block (the
+// empty-bank rule): slot x holds candidate x, its density the sum of its
+// weights to the other admitted candidates.  One wave.
+__device__ void seq_empty_commit(const dkv_bank &bank, const Geom &g, const Prm &p, const Workspace &ws, int b,
+                                 int l) {
+  const int L = ws.gram_ld, Mcap = g.Mcap, N = g.N;
+  const size_t rb = (size_t)b * Mcap;
+  const int na = min(N, ws.M[b]);
+  const uint32_t *gb = bank_gram(ws, b);
   for (int x = 0; x < na; ++x) {
-    const uint32_t *wr = ws.gram + ((size_t)b * L + Mcap + x) * L + Mcap;
+    const uint32_t *wr = gb + (size_t)(Mcap + x) * L + Mcap;
     int64_t acc = 0;
     for (int y = l; y < na; y += 64)
       if (y != x) acc += wr[y];
     acc = wave_sum_i64(acc);
     if (l == (x & 63)) {
       bank.rho[rb + x] = acc;
-      const int64_t bs = acc > p.delta_q ? acc : p.delta_q;
-      bank.base[rb + x] = bs;
-      ws.lim[rb + x] = lim_of(bs, p);
-      ws.grow[rb + x] = Mcap + x;
+      bank.base[rb + x] = acc > p.delta_q ? acc : p.delta_q;
       bank.prov[rb + x] = ((int64_t)p.block_id << 32) | (int64_t)x;
       bank.knorm[rb + x] = ws.cnorm[(size_t)b * N + x];
     }
   }
-  return na;
 }
 
 // Results of bank b by one wave, from its final occupancy m and the occupancy
@@ -246,7 +266,7 @@ __device__ void seq_results_bank(const dkv_bank &bank, const Geom &g, const Prm 
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(64 * kSeqWaves) void k_seq(dkv_bank bank, Geom g, Prm p, Workspace ws,
                                                        dkv_update_out out) {
-  const int grp = blockIdx.x, nw = blockDim.x >> 6;
+  const int grp = ws.seq_b0 / g.gs + (int)blockIdx.x, nw = blockDim.x >> 6;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int L = ws.gram_ld, Mcap = g.Mcap, N = g.N;
   __shared__ int mcur[kSeqMaxGroup], m0s[kSeqMaxGroup];
@@ -260,6 +280,7 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq(dkv_bank bank, Geom g, P
     const int b = grp * g.gs + hh;
     const int m0 = ws.m[b];
     const int mc = seq_setup_bank(bank, g, p, ws, b, l);
+    if (m0 == 0) seq_empty_commit(bank, g, p, ws, b, l);
     if (l == 0) {
       m0s[hh] = m0;
       mcur[hh] = mc;
@@ -278,7 +299,7 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq(dkv_bank bank, Geom g, P
       const size_t rb = (size_t)b * Mcap;
       const int m = mcur[hh];
       const int x = ws.order[(size_t)b * N + j];
-      const uint32_t *wx = ws.gram + ((size_t)b * L + Mcap + x) * L;
+      const uint32_t *wx = bank_gram(ws, b) + (size_t)(Mcap + x) * L;
       int cnt = 0, vmin = INT_MAX;
       Best best{INT64_MIN, INT64_MAX, INT_MAX};
       for (int s = l; s < m; s += 64) {
@@ -315,8 +336,8 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq(dkv_bank bank, Geom g, P
       const int x = ws.order[(size_t)b * N + j];
       const int e = m + 1 > ws.M[b] ? 1 : 0;
       const int ev = dec_cnt[hh] > 0 ? dec_v[hh] : (e ? dec_best[hh] : -1);
-      const uint32_t *wx = ws.gram + ((size_t)b * L + Mcap + x) * L;
-      const uint32_t *wev = ev >= 0 ? ws.gram + ((size_t)b * L + ws.grow[rb + ev]) * L : nullptr;
+      const uint32_t *wx = bank_gram(ws, b) + (size_t)(Mcap + x) * L;
+      const uint32_t *wev = ev >= 0 ? bank_gram(ws, b) + (size_t)ws.grow[rb + ev] * L : nullptr;
       int64_t sum = 0;
       for (int s = l; s < m; s += 64) {
         if (s == ev) continue;
@@ -406,8 +427,9 @@ __device__ __forceinline__ Rec rec_shfl(const Rec &r, int src) {
   o.total = sh64(r.total);
   return o;
 }
-// Wave reduction of the lanes' records.  The count rides in the top bits of
-// the weight sum (a wave's sum of at most 512 weights stays below 2^32),
+// Wave reduction of the lanes' records.  The count rides in the bits from 40
+// up of the weight sum (a wave holds at most 64 x 16 = 1,024 slots, so its sum
+// of weights <= 2^23 stays at or below 2^33, under bit 40),
 // the slots and the densest state's key are reduced level by level, and the
 // weights and items of the first violator and of the densest state are then
 // read once from the lanes that hold them (a slot belongs to one lane).
@@ -470,7 +492,7 @@ __device__ __forceinline__ Rec rec_decode(const uint64_t *v) {
 }
 
 __global__ __launch_bounds__(64 * kSeqWaves) void k_seq_setup(dkv_bank bank, Geom g, Prm p, Workspace ws) {
-  const int grp = blockIdx.x, nw = blockDim.x >> 6;
+  const int grp = ws.seq_b0 / g.gs + (int)blockIdx.x, nw = blockDim.x >> 6;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   for (int hh = wave; hh < g.gs; hh += nw) {
     const int b = grp * g.gs + hh;
@@ -488,7 +510,7 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq_setup(dkv_bank bank, Geo
 
 template <int S>
 __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g, Prm p, Workspace ws, int P) {
-  const int b = blockIdx.x / P, q = blockIdx.x % P;
+  const int b = ws.seq_b0 + (int)blockIdx.x / P, q = blockIdx.x % P;
   const int grp = b / g.gs, hh = b % g.gs;
   const int tid = threadIdx.x, wave = tid >> 6, l = tid & 63;
   const int L = ws.gram_ld, Mcap = g.Mcap, N = g.N;
@@ -504,7 +526,7 @@ __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g
   const bool lane_live = l < nmem && ws.m[grp * g.gs + l / P] > 0;
   int m = ws.m_new[b];
   const int M = ws.M[b];
-  const uint32_t *gb = ws.gram + (size_t)b * L * L;
+  const uint32_t *gb = bank_gram(ws, b);
   int64_t rho[S], lim[S], prov[S];
   int item[S];
   uint32_t wn[S];
@@ -678,7 +700,7 @@ __global__ __launch_bounds__(kCoopThreads) void k_seq_coop(dkv_bank bank, Geom g
 
 __global__ __launch_bounds__(64 * kSeqWaves) void k_seq_results(dkv_bank bank, Geom g, Prm p, Workspace ws,
                                                                dkv_update_out out) {
-  const int grp = blockIdx.x, nw = blockDim.x >> 6;
+  const int grp = ws.seq_b0 / g.gs + (int)blockIdx.x, nw = blockDim.x >> 6;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   if (threadIdx.x == 0 && out.r_star) {
     int timed_out = 0;
@@ -687,6 +709,7 @@ __global__ __launch_bounds__(64 * kSeqWaves) void k_seq_results(dkv_bank bank, G
   }
   for (int hh = wave; hh < g.gs; hh += nw) {
     const int b = grp * g.gs + hh;
+    if (ws.m[b] == 0) seq_empty_commit(bank, g, p, ws, b, l);
     seq_results_bank(bank, g, p, ws, out, b, l, ws.m_new[b], ws.m[b]);
   }
 }
@@ -699,7 +722,7 @@ template <int D>
 __global__ __launch_bounds__(256) void k_seq_commit(dkv_bank bank, dkv_segment seg, Geom g, Workspace ws) {
   constexpr int CH = D / 8;             // 16-byte chunks per bf16 row
   constexpr int kSlots = 256 / (2 * CH);  // slots per workgroup
-  const int b = blockIdx.y;
+  const int b = ws.seq_b0 + (int)blockIdx.y;
   const int s = blockIdx.x * kSlots + threadIdx.x / (2 * CH);
   const int c = threadIdx.x % (2 * CH);
   const int m = bank.occupancy[b];
@@ -731,35 +754,48 @@ template <int D>
 hipError_t seq_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                     const dkv_update_out &out, const Workspace &ws, hipStream_t s) {
   const int L = ws.gram_ld;
-  if (L > 0 && g.N > 0) {
-    const dim3 grid((unsigned)((L + kGramCols - 1) / kGramCols), (unsigned)((L + 31) / 32), (unsigned)g.B);
-    k_seq_gram<D><<<grid, 256, 0, s>>>(bank, seg, g, p, ws);
-  }
   const int waves = g.gs < kSeqWaves ? g.gs : kSeqWaves;
+  // the groups run in batches of ws.seq_groups (their pairwise weights fill the area)
+  if (ws.seq_groups < 1) return hipErrorInvalidValue;
+  const int per_batch = ws.seq_groups * g.gs;   // banks
   // workgroups per bank with 8 and with 16 slots per thread
   int P8 = (g.Mcap + 8 * kCoopThreads - 1) / (8 * kCoopThreads);
   int P16 = (g.Mcap + 16 * kCoopThreads - 1) / (16 * kCoopThreads);
-  const bool use8 = g.N > 0 && g.gs * P8 <= kSeqMaxMembers && coop_fits<8>(g.B * P8);
-  const bool use16 = !use8 && g.N > 0 && g.gs * P16 <= kSeqMaxMembers && coop_fits<16>(g.B * P16);
-  if (use8 || use16) {
-    k_seq_setup<<<g.G, 64 * waves, 0, s>>>(bank, g, p, ws);
-    dkv_bank a_bank = bank;
-    Geom a_g = g;
-    Prm a_p = p;
-    Workspace a_ws = ws;
-    int *P = use8 ? &P8 : &P16;
-    void *args[] = {&a_bank, &a_g, &a_p, &a_ws, P};
-    const void *kern = use8 ? reinterpret_cast<const void *>(k_seq_coop<8>) : reinterpret_cast<const void *>(k_seq_coop<16>);
-    const hipError_t e = hipLaunchCooperativeKernel(kern, dim3((unsigned)(g.B * *P)), dim3(kCoopThreads), args, 0, s);
-    if (e != hipSuccess) return e;
-    k_seq_results<<<g.G, 64 * waves, 0, s>>>(bank, g, p, ws, out);
-  } else {
-    k_seq<<<g.G, 64 * waves, 0, s>>>(bank, g, p, ws, out);
-  }
-  if (g.N > 0) {
-    constexpr int kSlots = 256 / (2 * (D / 8));
-    k_seq_commit<D><<<dim3((unsigned)((g.Mcap + kSlots - 1) / kSlots), (unsigned)g.B), 256, 0, s>>>(bank, seg, g,
-                                                                                                  ws);
+  // Which walk runs is decided here, before anything is enqueued, for a full
+  // batch (a shorter last batch fits when a full one does).
+  const int full = per_batch < g.B ? per_batch : g.B;
+  const bool use8 = g.N > 0 && g.gs * P8 <= kSeqMaxMembers && coop_fits<8>(full * P8);
+  const bool use16 = !use8 && g.N > 0 && g.gs * P16 <= kSeqMaxMembers && coop_fits<16>(full * P16);
+  for (int b0 = 0; b0 < g.B; b0 += per_batch) {
+    const int nb = per_batch < g.B - b0 ? per_batch : g.B - b0;
+    const unsigned ngroups = (unsigned)(nb / g.gs);
+    Workspace wb = ws;
+    wb.seq_b0 = b0;
+    if (L > 0 && g.N > 0) {
+      const dim3 grid((unsigned)((L + kGramCols - 1) / kGramCols), (unsigned)((L + 31) / 32), (unsigned)nb);
+      k_seq_gram<D><<<grid, 256, 0, s>>>(bank, seg, g, p, wb);
+    }
+    if (use8 || use16) {
+      // the set-up writes the workspace only; the banks change from the walk on
+      k_seq_setup<<<ngroups, 64 * waves, 0, s>>>(bank, g, p, wb);
+      dkv_bank a_bank = bank;
+      Geom a_g = g;
+      Prm a_p = p;
+      Workspace a_ws = wb;
+      int *P = use8 ? &P8 : &P16;
+      void *args[] = {&a_bank, &a_g, &a_p, &a_ws, P};
+      const void *kern = use8 ? reinterpret_cast<const void *>(k_seq_coop<8>) : reinterpret_cast<const void *>(k_seq_coop<16>);
+      const hipError_t e = hipLaunchCooperativeKernel(kern, dim3((unsigned)(nb * *P)), dim3(kCoopThreads), args, 0, s);
+      if (e != hipSuccess) return e;
+      k_seq_results<<<ngroups, 64 * waves, 0, s>>>(bank, g, p, wb, out);
+    } else {
+      k_seq<<<ngroups, 64 * waves, 0, s>>>(bank, g, p, wb, out);
+    }
+    if (g.N > 0) {
+      constexpr int kSlots = 256 / (2 * (D / 8));
+      k_seq_commit<D><<<dim3((unsigned)((g.Mcap + kSlots - 1) / kSlots), (unsigned)nb), 256, 0, s>>>(bank, seg, g,
+                                                                                                   wb);
+    }
   }
   return hipGetLastError();
 }

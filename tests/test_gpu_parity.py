@@ -48,8 +48,9 @@ def test_pair_weight_exhaustive(s, p):
 # ----------------------------------------------------------------------------- rollouts
 
 def _run_rollout(cfg, blocks, prm, budgets=None, dup_every=0, trace=True, init_full=False, check_every=1,
-                 grid_values=False):
-    """Rollout over one layer of `cfg`: GPU update + oracle update per block, compared."""
+                 grid_values=False, seq_groups=None):
+    """Rollout over one layer of `cfg`: GPU update + oracle update per block, compared
+    (seq_groups: workspace for that many groups' pairwise weights, sequential policy)."""
     B, gs, d, dt = cfg.heads, cfg.group_size, cfg.d, cfg.dtype
     if budgets is None:
         budgets = np.full(B, cfg.budget, np.int32)
@@ -59,6 +60,10 @@ def _run_rollout(cfg, blocks, prm, budgets=None, dup_every=0, trace=True, init_f
     obanks = [BankState.empty(int(budgets[b]), d) for b in range(B)]
     op = oracle_params(prm)
     streams = [synth.HeadStream(cfg, 0, h) for h in range(B)]
+    ws = None
+    if seq_groups is not None:
+        n_max = max(Mcap if init_full else cfg.n_cand, cfg.n_cand)
+        ws = api.alloc_workspace(bank, n_max, prm.flags, seq_groups=seq_groups)
     for t in range(blocks):
         n = Mcap if (init_full and t == 0) else cfg.n_cand
         K = np.stack([s.keys(t, n) for s in streams])
@@ -70,7 +75,7 @@ def _run_rollout(cfg, blocks, prm, budgets=None, dup_every=0, trace=True, init_f
                 if obanks[h].m:
                     K[h] = streams[h].near_duplicates(K[h], obanks[h].K.astype(np.float32), t)
         out = api.UpdateOut(bank, n, trace=trace)
-        api.update_bank(bank, dev(K, dt), dev(V, dt), t, prm, out=out)
+        api.update_bank(bank, dev(K, dt), dev(V, dt), t, prm, workspace=ws, out=out)
         torch.cuda.synchronize()
         new, recs = oracle_step(obanks, K, V, t, op, gs)
         if t % check_every == 0 or t == blocks - 1:
@@ -192,6 +197,41 @@ def test_rollout_sequential_competition(dt, d, tau):
     cfg = synth.Config(heads=6, d=d, dtype=dt, n_cand=200, budget=300, group_size=3, **SMALL)
     prm = api.Params(sigma2_log2=4 if d == 64 else 5, tau_num=tau, flags=api.POLICY_SEQUENTIAL)
     _run_rollout(cfg, 5, prm, dup_every=2)
+
+
+@pytest.mark.parametrize("seq_groups", [1, 2])
+def test_sequential_batches_of_groups(seq_groups):
+    """The sequential competition with a workspace that holds the pairwise
+    weights of 1 or 2 groups: 9 banks in 3 groups of 3 (ragged budgets 300 /
+    260 / 300) are walked in batches of 1 group (three batches) or 2 groups (a
+    full batch and a ragged one), every result bit-exact against the oracle.
+    The workspace is smaller than the size query's by 2 or 1 groups of weights."""
+    _log(f"sequential batches of {seq_groups} groups")
+    cfg = synth.Config(heads=9, d=128, dtype="bf16", n_cand=200, budget=300, group_size=3, **SMALL)
+    prm = api.Params(sigma2_log2=5, tau_num=3, flags=api.POLICY_SEQUENTIAL)
+    budgets = np.array([300, 260, 300] * 3, np.int32)
+    bank = api.Bank(9, 300, 128, dtype=torch.bfloat16, group_size=3)
+    full = api.workspace_size(bank, 200, prm.flags)
+    per = api.seq_group_weight_bytes(bank, 200)
+    assert api.alloc_workspace(bank, 200, prm.flags, seq_groups=seq_groups).numel() == full - (3 - seq_groups) * per
+    _run_rollout(cfg, 5, prm, budgets=budgets, dup_every=2, seq_groups=seq_groups)
+
+
+def test_sequential_workspace_below_one_group_is_rejected():
+    """A sequential workspace without room for one group's pairwise weights is
+    DKV_ERR_WORKSPACE, and the bank is left as it was."""
+    _log("sequential workspace below one group")
+    bank = api.Bank(6, 300, 128, dtype=torch.bfloat16, group_size=3)
+    prm = api.Params(sigma2_log2=5, flags=api.POLICY_SEQUENTIAL)
+    full = api.workspace_size(bank, 200, prm.flags)   # fixed part + both groups' weights (256-byte aligned)
+    per = api.seq_group_weight_bytes(bank, 200)
+    fixed = full - (2 * per + 255) // 256 * 256
+    ws = torch.empty(fixed + per - 1, dtype=torch.uint8, device="cuda")
+    K = torch.zeros(6, 200, 128, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(api.DkvError):
+        api.update_bank(bank, K, K.clone(), 0, prm, workspace=ws)
+    torch.cuda.synchronize()
+    assert int(bank.occupancy.sum()) == 0
 
 
 def test_sequential_banks_spanning_workgroups():

@@ -336,3 +336,43 @@ def test_single_layer_sequential_full_size():
         }
         bad = [k for k in got if got[k] != ref["heads"][b][k]]
         assert not bad, f"bank {b}: {bad}"
+
+
+def test_long_rollout_sequential_full_size():
+    """The within-block sequential competition on layer 0 of the long rollout
+    (12 banks in one group, budget 18,720, 4,680 candidates per block): blocks
+    0-5, through the banks' filling (block 0 by the empty-bank rule, then about
+    4,600 taken steps per block) into the regime where every taken step releases
+    a state.  The pairwise weights of the group (12 x 23,400^2 x 4 bytes) take
+    the default workspace, one group per batch.  Per block, the number of taken
+    steps and, per bank, the order, scores, released and admitted lists and the
+    committed bank bytes must hash to the oracle's digests
+    (tests/golden/make_sequential_digests.py)."""
+    path = os.path.join(GOLDEN, "sequential_long_rollout_L0.json")
+    if not os.path.exists(path):
+        pytest.skip("oracle digests for the sequential long-rollout run not generated")
+    with open(path) as f:
+        ref = json.load(f)
+    cfg = synth.WORKLOADS["long_rollout"]
+    H, N, d = cfg.heads, cfg.n_cand, cfg.d
+    budgets = synth.budgets(cfg)[:H]
+    bank = api.Bank(H, int(budgets.max()), d, dtype=torch.bfloat16, group_size=cfg.group_size,
+                    budget=torch.from_numpy(budgets))
+    prm = api.Params(sigma2_log2=cfg.sigma2_log2, flags=api.POLICY_SEQUENTIAL)
+    ws = api.alloc_workspace(bank, N, prm.flags)
+    streams = [synth.HeadStream(cfg, 0, h) for h in range(H)]
+    assert ref["blocks"] == len(ref["steps"])
+    for t, step in enumerate(ref["steps"]):
+        print(f"sequential long rollout: block {t}", flush=True)
+        K, V = layer_block(cfg, streams, t)
+        m_prev = [int(x) for x in bank.occupancy.cpu()]
+        out = api.UpdateOut(bank, N, trace=True)
+        api.update_bank(bank, dev(K, "bf16"), dev(V, "bf16"), t, prm, workspace=ws, out=out)
+        torch.cuda.synchronize()
+        assert int(out.r_star[0].item()) == step["steps_taken"], f"block {t}: steps taken"
+        for b in range(H):
+            got = _bank_entry(bank, out, b, m_prev[b], N)
+            bad = [k for k in step["heads"][b] if got[k] != step["heads"][b][k]]
+            assert not bad, f"block {t} bank {b}: differs from the oracle in {bad}"
+        print(f"  block {t}: steps {step['steps_taken']} occupancy {[int(x) for x in bank.occupancy.cpu()][:4]} ok",
+              flush=True)
