@@ -67,8 +67,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--policy", default="default", choices=sorted(POLICIES),
                     help="policy ablation of Table 1(b) run by the update (default: the paper's policy)")
+    ap.add_argument("--seq-groups", type=int, default=0,
+                    help="sequential policy: groups whose pairwise weights the workspace holds at once "
+                         "(default: as many as fit in 32 GiB)")
     ap.add_argument("--cpu-heads", type=int, default=0,
-                    help="heads in the oracle sample (default: 3 for the rollouts, 12 for single_layer)")
+                    help="heads in the oracle sample (default: 8 for the rollouts, 12 for single_layer)")
     ap.add_argument("--no-sink-attention", action="store_true",
                     help="single_layer: skip the sink + window + bank attention at the deployment shape")
     ap.add_argument("--copy-probe-mb", type=int, default=0,
@@ -130,14 +133,14 @@ def blas_threads(n):
 
 
 def gram_pairs(m, N, R, r, e):
-    """Key-key weights per bank that the update needs (Supp. C cost paragraph): the
+    """Key-key weights per bank that the method needs (Supp. C cost paragraph): the
     candidate scores (Eq. 6) m N; the prefix densities in score order (Eq. 8) m R;
-    exact maintenance: every survivor against the admitted and the evicted states
-    (m - e)(r + e), every admitted candidate against the smaller of the evicted set
-    and the survivors r min(e, m - e) (its weights to the whole old bank are the
-    score's column sums), and the distinct pairs among the admitted r (r - 1) / 2."""
+    exact maintenance, each symmetric pair once: every survivor against the admitted
+    and the evicted states (m - e)(r + e) (the admitted candidates' densities over
+    the survivors are the same pairs), and the distinct pairs among the admitted
+    r (r - 1) / 2."""
     surv = m - e
-    return m * N + m * R + surv * (r + e) + r * np.minimum(e, surv) + r * (r - 1) // 2
+    return m * N + m * R + surv * (r + e) + r * (r - 1) // 2
 
 
 # ----------------------------------------------------------------------------
@@ -207,7 +210,7 @@ def run_rollout(args, api, synth, torch):
     dev = torch.device("cuda:0")
     bank = api.Bank(B, Mcap, d, dtype=torch.bfloat16, group_size=gs, budget=torch.from_numpy(budgets))
     prm = api.Params(sigma2_log2=cfg.sigma2_log2, flags=POLICIES[args.policy])
-    ws = api.alloc_workspace(bank, N, prm.flags)
+    ws = api.alloc_workspace(bank, N, prm.flags, seq_groups=args.seq_groups or None)
     # every input of the pass, resident in HBM before anything is timed:
     # block t's K/V are the candidates of update t and the window of attention t - 1
     gen = synth.TorchRollout(cfg, dev)
@@ -514,7 +517,7 @@ def main():
     if args.workload in ROLLOUTS:
         result = run_rollout(args, api, synth, torch)
         if not args.no_cpu_baseline and args.policy == "default":
-            result["cpu_baseline"] = rollout_cpu_baseline(synth.WORKLOADS[args.workload], args.cpu_heads or 3)
+            result["cpu_baseline"] = rollout_cpu_baseline(synth.WORKLOADS[args.workload], args.cpu_heads or 8)
     elif args.workload in ("tiny", "single_layer"):
         result = run_single(args, api, synth, torch)
     else:
