@@ -136,13 +136,7 @@ constexpr int kFQ = 32 * kFWaves;  // queries per workgroup
 constexpr int kFK = 64;            // keys per tile
 constexpr int kFStages = 3;        // K/V tiles resident in LDS (2 in flight while 1 is used)
 
-typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-// Two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  const f32x2 v = {lo, hi};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
-}
 
 template <int D>
 struct FCfg {

@@ -119,9 +119,10 @@ __device__ __forceinline__ void load_row_frag(RowFrag<D> &rf, const Desc &src, i
     u32x4 sc;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float lo = bf16_bits_to_f32((uint16_t)(raw[q] & 0xFFFF)) * neg2_inv_s2;
-      const float hi = bf16_bits_to_f32((uint16_t)(raw[q] >> 16)) * neg2_inv_s2;
-      sc[q] = (uint32_t)bf16_rne_bits(lo) | ((uint32_t)bf16_rne_bits(hi) << 16);
+      // both halves times a power of two (exact), back to bf16 in one packed conversion
+      const float lo = __uint_as_float(raw[q] << 16) * neg2_inv_s2;
+      const float hi = __uint_as_float(raw[q] & 0xFFFF0000u) * neg2_inv_s2;
+      sc[q] = pack_bf16x2(lo, hi);
     }
     rf.b[kk] = __builtin_bit_cast(bf16x8, sc);
   }

@@ -5,8 +5,10 @@
   empty-bank rule from block 0, then 4,680 candidates of block 1 (30%
   near-duplicates) offered one per step;
 * long_rollout, layer 0: 12 banks of one group, budget 18,720, blocks 0-5 of
-  4,680 candidates (the banks fill by block 4, then every taken step releases
-  a state).
+  4,680 candidates (block 0 fills the empty banks by the empty-bank rule, block
+  1 takes about 4,600 steps into banks of 4,680 states, and from block 2 on no
+  step is taken on this input: every candidate pushes some state of the group
+  over its bound).
 
 The oracle walks 4,680 steps of 12 banks in one to five minutes per block, too
 long for a test that holds a GPU, so this script runs it once on the CPU and

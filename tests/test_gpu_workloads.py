@@ -341,10 +341,11 @@ def test_single_layer_sequential_full_size():
 def test_long_rollout_sequential_full_size():
     """The within-block sequential competition on layer 0 of the long rollout
     (12 banks in one group, budget 18,720, 4,680 candidates per block): blocks
-    0-5, through the banks' filling (block 0 by the empty-bank rule, then about
-    4,600 taken steps per block) into the regime where every taken step releases
-    a state.  The pairwise weights of the group (12 x 23,400^2 x 4 bytes) take
-    the default workspace, one group per batch.  Per block, the number of taken
+    0-5 (block 0 fills the empty banks by the empty-bank rule, block 1 takes
+    about 4,600 steps into banks of 4,680 states, later blocks take none on this
+    input, every step tested against banks of 9,280 states).  The pairwise
+    weights of the group (12 x 23,400^2 x 4 bytes) take the default workspace,
+    one group per batch.  Per block, the number of taken
     steps and, per bank, the order, scores, released and admitted lists and the
     committed bank bytes must hash to the oracle's digests
     (tests/golden/make_sequential_digests.py)."""
