@@ -117,11 +117,12 @@ __global__ __launch_bounds__(kAThreads) void k_attn_rowwise(dkv_bank bank, const
 //                   (ds_read_b64_tr_b16).  Inside each 16-key K step the key
 //                   order is permuted identically in both operands
 //                   (slot 8h + j <-> key 8 (j / 4) + 4 h + j % 4).
-// K and V tiles go global -> LDS with 16-byte direct-to-LDS loads (no VGPR
+// K and V tiles go global -> LDS with 16-byte buffer loads to LDS (no VGPR
 // staging) into a ring of three stages (two tiles in flight while one is
 // used); rows are stored with an XOR swizzle of their
 // 16-byte chunks so that both the K reads and the transposed V reads are free
-// of LDS bank conflicts.
+// of LDS bank conflicts.  Within a tile the LDS fragment reads are scheduled
+// ahead of the MFMAs that use them (6 MFMAs ahead for S, 4 for P V).
 // ---------------------------------------------------------------------------
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -135,6 +136,9 @@ constexpr int kFWaves = 8;
 constexpr int kFQ = 32 * kFWaves;  // queries per workgroup
 constexpr int kFK = 64;            // keys per tile
 constexpr int kFStages = 3;        // K/V tiles resident in LDS (2 in flight while 1 is used)
+// Word 3 of a raw buffer resource: 32-bit data format, no swizzle, no
+// thread-id addressing.
+constexpr int kBufferRsrcWord3 = 0x00020000;
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
@@ -160,6 +164,10 @@ __device__ __forceinline__ int v_swz(int r, int c) { return c ^ ((4 * (r % 4)) %
 // Lane i of a load writes 16 bytes at LDS offset 16 i of its 1 KB block, i.e.
 // physical chunk pc of row r; it fetches logical chunk swz(r, pc) (the XOR
 // swizzle is an involution, so logical chunk c lands at physical swz(r, c)).
+// The loads are raw buffer loads to LDS over the tile's valid rows rather
+// than global loads to LDS: with a global load to LDS in flight the compiler
+// counts every later LDS read as possibly out of order and waits for all of
+// them before each use, which serializes the MFMAs on the LDS latency.
 template <int D, bool kIsV>
 __device__ __forceinline__ void ftile_issue(const uint16_t *base, int nvalid, char *buf) {
   constexpr int RPL = FCfg<D>::kRowsPerLoad, CH = FCfg<D>::kChunks;
@@ -171,7 +179,9 @@ __device__ __forceinline__ void ftile_issue(const uint16_t *base, int nvalid, ch
     const int r = blk * RPL + rsub;
     const int rr = r < nvalid ? r : nvalid - 1;
     const int cs = kIsV ? v_swz<D>(r, pc) : k_swz<D>(r, pc);
-    __builtin_amdgcn_global_load_lds(base + (size_t)rr * D + 8 * cs, (lds_void *)(buf + blk * 1024), 16, 0, 0);
+    const __amdgpu_buffer_rsrc_t rs =  // base and extent are uniform
+        __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, nvalid * FCfg<D>::kRowBytes, kBufferRsrcWord3);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)(buf + blk * 1024), 16, (rr * D + 8 * cs) * 2, 0, 0, 0);
   }
 }
 
@@ -291,6 +301,13 @@ __global__ __launch_bounds__(64 * kFWaves, 1) void k_attn_mfma(dkv_bank bank, co
       for (int kk = 0; kk < KS; ++kk) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk], qf[kk], acc, 0, 0, 0);
       sc[sub] = acc;
     }
+    // S block: LDS fragment reads run 6 MFMAs ahead of their use
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+#pragma unroll
+    for (int i = 0; i < 2 * KS; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (i + 6 < 2 * KS) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
     const int nvalid = nvalid_of(t);
     if (nvalid < kFK) {
 #pragma unroll
@@ -354,6 +371,13 @@ __global__ __launch_bounds__(64 * kFWaves, 1) void k_attn_mfma(dkv_bank bank, co
           o[t2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av), bop, o[t2], 0, 0, 0);
         }
       }
+    }
+    // P V block: the two transposed reads of an MFMA run 4 MFMAs ahead of it
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+    for (int i = 0; i < 4 * DT; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (i + 4 < 4 * DT) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     }
   };
 

@@ -176,23 +176,60 @@ __device__ __forceinline__ void stage_rows(int32_t (&rows)[SCfg<D>::PER + 1], in
   rows[SCfg<D>::PER] = (int32_t)row_of(min(j0 + 16 * wave + (l & 15), ncols - 1));
 }
 
+// Word 3 of a raw buffer resource: 32-bit data format, no swizzle, no
+// thread-id addressing.
+constexpr int kBufferRsrcWord3 = 0x00020000;
+
+// One 16-byte (4-byte) raw buffer load per lane to LDS, dst + 16 lane
+// (dst + 4 lane), from base + voff, with the bytes [base, base + nbytes) as
+// the buffer's extent.
+__device__ __forceinline__ void buffer_to_lds16(const void *base, int nbytes, int voff, char *dst) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, nbytes, kBufferRsrcWord3);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)dst, 16, voff, 0, 0, 0);
+}
+__device__ __forceinline__ void buffer_to_lds4(const void *base, int nbytes, int voff, char *dst) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, nbytes, kBufferRsrcWord3);
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)dst, 4, voff, 0, 0, 0);
+}
+
+// Stage loads.  Every row of a call lies in one bank's region of its arrays,
+// rows [row0, row0 + nrows) (uniform), so whole-key-row descriptors go through
+// raw buffer loads to LDS over that region: with a global load to LDS in flight
+// the compiler counts every later LDS read as possibly out of order and waits
+// for all of them before each use.  [K; V] descriptors, whose two halves come
+// from two arrays chosen per lane, keep the global loads to LDS.
 template <int D, bool kBs, bool SPLIT>
 __device__ __forceinline__ void stage_dma(const int32_t (&rows)[SCfg<D>::PER + 1], const Desc &keys,
-                                          const uint4 *augs, const float *bs, char *kb, char *ab, float *sb) {
+                                          const uint4 *augs, const float *bs, char *kb, char *ab, float *sb,
+                                          int64_t row0, int nrows) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
+  if constexpr (!SPLIT) {
+    const void *kbase = keys.k + row0 * D;
+    const int kbytes = nrows * SCfg<D>::RB;
 #pragma unroll
-  for (int q = 0; q < SCfg<D>::PER; ++q) {
-    const int blk = wave * SCfg<D>::PER + q;
-    const int r = blk * SCfg<D>::RPL + l / SCfg<D>::CH;
-    const int c = (l % SCfg<D>::CH) ^ (r % SCfg<D>::CH);
-    __builtin_amdgcn_global_load_lds((void *)desc_chunk<D, SPLIT>(keys, (int64_t)rows[q], c), (lds_void *)(kb + blk * 1024), 16,
-                                     0, 0);
+    for (int q = 0; q < SCfg<D>::PER; ++q) {
+      const int blk = wave * SCfg<D>::PER + q;
+      const int r = blk * SCfg<D>::RPL + l / SCfg<D>::CH;
+      const int c = (l % SCfg<D>::CH) ^ (r % SCfg<D>::CH);
+      buffer_to_lds16(kbase, kbytes, (int)(rows[q] - row0) * SCfg<D>::RB + 16 * c, kb + blk * 1024);
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < SCfg<D>::PER; ++q) {
+      const int blk = wave * SCfg<D>::PER + q;
+      const int r = blk * SCfg<D>::RPL + l / SCfg<D>::CH;
+      const int c = (l % SCfg<D>::CH) ^ (r % SCfg<D>::CH);
+      __builtin_amdgcn_global_load_lds((void *)desc_chunk<D, SPLIT>(keys, (int64_t)rows[q], c),
+                                       (lds_void *)(kb + blk * 1024), 16, 0, 0);
+    }
   }
   // items 16 w .. 16 w + 15: lanes 0-15 of wave w (LDS address = base + lane * size)
   if (l < 16) {
-    __builtin_amdgcn_global_load_lds((void *)(augs + (int64_t)rows[SCfg<D>::PER]), (lds_void *)(ab + 256 * wave), 16, 0, 0);
-    if constexpr (kBs)
-      __builtin_amdgcn_global_load_lds((void *)(bs + (int64_t)rows[SCfg<D>::PER]), (lds_void *)(sb + 16 * wave), 4, 0, 0);
+    const int rel = (int)(rows[SCfg<D>::PER] - row0);
+    buffer_to_lds16(augs + row0, nrows * 16, rel * 16, ab + 256 * wave);
+    if constexpr (kBs) buffer_to_lds4(bs + row0, nrows * 4, rel * 4, reinterpret_cast<char *>(sb + 16 * wave));
   }
 }
 
@@ -334,6 +371,7 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
   RowFrag<D> rf;
   load_row_frag<D, FOLD, KV>(rf, K, (int64_t)xr, rv ? ws.cnorm[xr] : 0.0f, rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
   const size_t rb = (size_t)b * g.Mcap + c0;
+  const int64_t bank_row0 = (int64_t)b * g.Mcap;  // the stage rows lie in bank b's slots
   auto row_of = [&](int i) -> int64_t { return (int64_t)(rb + i); };
   uint64_t A64 = 0;
   const int ns = (ncols + kSI - 1) / kSI;
@@ -375,7 +413,7 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
     else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
     stage_barrier();
     if (t + 2 < ns) {
-      stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, kn, an, sn);
+      stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, kn, an, sn, bank_row0, g.Mcap);
       if (t + 3 < ns) stage_rows<D>(rows, (t + 3) * kSI, ncols, row_of);
     }
     f32x16 u0, u1;
@@ -397,10 +435,10 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
     }
   };
   stage_rows<D>(rows, 0, ncols, row_of);
-  stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k0, a0, s0);
+  stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k0, a0, s0, bank_row0, g.Mcap);
   if (ns > 1) {
     stage_rows<D>(rows, kSI, ncols, row_of);
-    stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k1, a1, s1);
+    stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k1, a1, s1, bank_row0, g.Mcap);
     if (ns > 2) stage_rows<D>(rows, 2 * kSI, ncols, row_of);
   }
   if constexpr (D <= 128) {
@@ -449,7 +487,7 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
       else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
       stage_barrier();
       if (t + 3 < ns) {
-        stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, kd, ad, sd);
+        stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, kd, ad, sd, bank_row0, g.Mcap);
         if (t + 4 < ns) stage_rows<D>(rows, (t + 4) * kSI, ncols, row_of);
       }
       xx = tile_mfma<D>(kn, an, 0, rf, aoff);
@@ -463,7 +501,7 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
       else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
       stage_barrier();
       if (ns > 2) {
-        stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k2, a2, s2);
+        stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k2, a2, s2, bank_row0, g.Mcap);
         if (ns > 3) stage_rows<D>(rows, 3 * kSI, ncols, row_of);
       }
       u = tile_mfma<D>(k0, a0, 0, rf, aoff);
@@ -635,6 +673,10 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   // the ordered candidates are stored as whole descriptors; the others are split for [K; V]
   constexpr bool kColSplit = KV && !(MODE == RS_CHUNK || MODE == RS_FIXUP);
   const uint4 *colaug = (MODE == RS_CHUNK || MODE == RS_FIXUP) ? ws.saug : (MODE == RS_ADM_MUT ? ws.caug : ws.baug);
+  // the column rows lie in bank b's candidates or in its slots
+  constexpr bool kColCand = MODE == RS_CHUNK || MODE == RS_FIXUP || MODE == RS_ADM_MUT;
+  const int64_t col_row0 = kColCand ? (int64_t)nb : (int64_t)rb;
+  const int col_nrows = kColCand ? g.N : g.Mcap;  // rows of that region
   constexpr bool kDiag = (MODE == RS_ADM_MUT || MODE == RS_DENSITY);
   // fragment reads kept ahead of the MFMAs where the registers allow it
   constexpr int kStageAhead = (D <= 128 && (MODE == RS_CHUNK || MODE == RS_FIXUP || MODE == RS_DENSITY)) ? 4 : 0;
@@ -714,7 +756,7 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
     stage_barrier();
     if (t + 2 < ns) {
       if (t + 3 < ns) stage_rows<D>(fill, (t + 3) * kSI, ncols, row_of_rel);
-      stage_dma<D, false, kColSplit>(use, colbase, colaug, nullptr, kn, an, nullptr);
+      stage_dma<D, false, kColSplit>(use, colbase, colaug, nullptr, kn, an, nullptr, col_row0, col_nrows);
     }
     if constexpr (kSym) {
       if (t > 0) flush_cols(t - 1);
@@ -750,10 +792,10 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   }
   if (ns > 0) {
     stage_rows<D>(rowsA, 0, ncols, row_of_rel);
-    stage_dma<D, false, kColSplit>(rowsA, colbase, colaug, nullptr, sb.k0, sb.a0, nullptr);
+    stage_dma<D, false, kColSplit>(rowsA, colbase, colaug, nullptr, sb.k0, sb.a0, nullptr, col_row0, col_nrows);
     if (ns > 1) {
       stage_rows<D>(rowsB, kSI, ncols, row_of_rel);
-      stage_dma<D, false, kColSplit>(rowsB, colbase, colaug, nullptr, sb.k1, sb.a1, nullptr);
+      stage_dma<D, false, kColSplit>(rowsB, colbase, colaug, nullptr, sb.k1, sb.a1, nullptr, col_row0, col_nrows);
       if (ns > 2) stage_rows<D>(rowsA, 2 * kSI, ncols, row_of_rel);
     }
   }
@@ -790,7 +832,7 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
       stage_barrier();
       if (t + 3 < ns) {
         if (t + 4 < ns) stage_rows<D>(fill, (t + 4) * kSI, ncols, row_of_rel);
-        stage_dma<D, false, kColSplit>(use, colbase, colaug, nullptr, kd, ad, nullptr);
+        stage_dma<D, false, kColSplit>(use, colbase, colaug, nullptr, kd, ad, nullptr, col_row0, col_nrows);
       }
       x = tile_mfma_(kn, an, 0);
       s2 += lane_wsum<P, false, FOLD>(u, kCT, h);
@@ -804,7 +846,7 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
       stage_barrier();
       if (ns > 2) {
         if (ns > 3) stage_rows<D>(rowsB, 3 * kSI, ncols, row_of_rel);
-        stage_dma<D, false, kColSplit>(rowsA, colbase, colaug, nullptr, sb.k2, sb.a2, nullptr);
+        stage_dma<D, false, kColSplit>(rowsA, colbase, colaug, nullptr, sb.k2, sb.a2, nullptr, col_row0, col_nrows);
       }
       u = tile_mfma_(sb.k0, sb.a0, 0);
     }
