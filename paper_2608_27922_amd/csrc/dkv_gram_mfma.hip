@@ -937,22 +937,33 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
 // admitted x survivors, admitted x admitted; blockIdx.x selects
 // the stage and its row block.
 template <int D, int P, bool FOLD, bool KV>
+// One launch for the three maintenance Grams of every bank (blockIdx.z): x
+// enumerates (row block, column split) pairs, survivors x evicted first
+// (rows_surv row blocks x y_ev splits: at most N evicted states), then
+// admitted x survivors (rows_adm x y_surv), then admitted x admitted
+// (rows_adm x 2 y_ev half splits).  Pairs whose columns lie beyond what the
+// Gram can have are not launched.
 __global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
-                                                           Geom g, Prm p, Workspace ws, int nx_surv, int nx_adm) {
+                                                           Geom g, Prm p, Workspace ws, int rows_surv, int rows_adm,
+                                                           int y_ev, int y_surv) {
   constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
   __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
   __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
   __shared__ __attribute__((aligned(16))) uint32_t cb[3 * kSI];
   const StageBufs<D> sb{k0, k1, k2, a0, a1, a2, cb};
-  const int bx = blockIdx.x;
-  if (bx < nx_surv)
-    rowsum_body<D, P, RS_SURV_EV, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, bx, blockIdx.y, blockIdx.z, sb);
-  else if (bx < nx_surv + nx_adm)
-    rowsum_body<D, P, RS_ADM_BASE, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, bx - nx_surv, blockIdx.y, blockIdx.z,
-                                         sb);
-  else
-    rowsum_body<D, P, RS_ADM_MUT, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, (bx - nx_surv - nx_adm) >> 1,
-                                        2 * blockIdx.y + ((bx - nx_surv - nx_adm) & 1), blockIdx.z, sb);
+  int i = blockIdx.x;
+  const int n_se = rows_surv * y_ev, n_ab = rows_adm * y_surv;
+  if (i < n_se) {
+    rowsum_body<D, P, RS_SURV_EV, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, i % rows_surv, i / rows_surv,
+                                        blockIdx.z, sb);
+  } else if ((i -= n_se) < n_ab) {
+    rowsum_body<D, P, RS_ADM_BASE, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, i % rows_adm, i / rows_adm,
+                                         blockIdx.z, sb);
+  } else {
+    i -= n_ab;
+    rowsum_body<D, P, RS_ADM_MUT, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, i % rows_adm, i / rows_adm,
+                                        blockIdx.z, sb);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1262,12 +1273,13 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       k_rowsum_mfma<D, P, RS_FIXUP, F, KV><<<dim3(rowsM, 1, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, out.rho_tilde);
       break;
     case 3: {
+      // evicted states <= admitted <= N: their column splits cover N; the
+      // survivors' cover Mcap
       const int nadm = g.N > 0 ? (int)rowsN : 0;
-      const unsigned ysplit = cdiv(g.Mcap > g.N ? g.Mcap : g.N, kColsPerSplit);
-      // x: survivor row blocks, admitted row blocks (x survivors),
-      // admitted row blocks x two half column splits (x admitted)
-      k_maint_mfma<D, P, F, KV><<<dim3(rowsM + 3 * nadm, ysplit, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, (int)rowsM,
-                                                                              nadm);
+      const unsigned y_ev = cdiv(g.N > 0 ? g.N : 1, kColsPerSplit), y_surv = cdiv(g.Mcap, kColsPerSplit);
+      const unsigned nx = rowsM * y_ev + (unsigned)nadm * (y_surv + 2 * y_ev);
+      k_maint_mfma<D, P, F, KV><<<dim3(nx, 1, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, (int)rowsM, nadm, (int)y_ev,
+                                                             (int)y_surv);
       break;
     }
     default:
