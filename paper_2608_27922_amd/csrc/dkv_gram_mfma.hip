@@ -636,6 +636,33 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   if (MODE != RS_FIXUP && c0 >= c1) return;  // the fix-up always writes rho~, even for r* % 256 == 0
   const int v = bx * kRowsPerWG + wave * 32 + n;
   const bool rv = v < nrows;
+  // fix-up: rho~ = rho + the whole chunks before r* + (below) the partial chunk
+  auto fixup_finish = [&](uint64_t tot) __attribute__((always_inline)) {
+    // the two half-waves sum alternate 4-chunk groups
+    const int full = rs / kCkStride;
+    if (rv) {
+      const uint4 *ckr = reinterpret_cast<const uint4 *>(ws.ck + (rb + v) * ws.nck);
+      for (int c4 = h; 4 * c4 < full; c4 += 2) {
+        const uint4 q = ckr[c4];
+        const int c = 4 * c4;
+        tot += (uint64_t)q.x + (c + 1 < full ? (uint64_t)q.y : 0) + (c + 2 < full ? (uint64_t)q.z : 0) +
+               (c + 3 < full ? (uint64_t)q.w : 0);
+      }
+    }
+    tot += __shfl_xor(tot, 32, 64);
+    if (!rv || h != 0) return;
+    const size_t row = rb + v;
+    const int64_t rt = bank.rho[row] + (int64_t)tot;
+    ws.rho_t[row] = rt;
+    if (out) out[row] = rt;
+  };
+  if constexpr (MODE == RS_FIXUP) {
+    // r* on a chunk boundary (uniform over the workgroup): no Gram, whole chunks only
+    if (c0 >= c1) {
+      fixup_finish(0);
+      return;
+    }
+  }
   // row item
   Desc rsrc = BK;
   int64_t rrow = (int64_t)rb;
@@ -896,28 +923,14 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
     }
   }
   if constexpr (MODE == RS_CHUNK) return;
-  uint64_t tot = S64;
   if constexpr (MODE == RS_FIXUP) {
-    // plus the whole chunks before r*: the two half-waves sum alternate 4-chunk groups
-    const int full = rs / kCkStride;
-    if (rv) {
-      const uint4 *ckr = reinterpret_cast<const uint4 *>(ws.ck + (rb + v) * ws.nck);
-      for (int c4 = h; 4 * c4 < full; c4 += 2) {
-        const uint4 q = ckr[c4];
-        const int c = 4 * c4;
-        tot += (uint64_t)q.x + (c + 1 < full ? (uint64_t)q.y : 0) + (c + 2 < full ? (uint64_t)q.z : 0) +
-               (c + 3 < full ? (uint64_t)q.w : 0);
-      }
-    }
+    fixup_finish(S64);
+    return;
   }
+  uint64_t tot = S64;
   tot += __shfl_xor(tot, 32, 64);
   if (!rv || h != 0) return;
-  if constexpr (MODE == RS_FIXUP) {
-    const size_t row = rb + v;
-    const int64_t rt = bank.rho[row] + (int64_t)tot;
-    ws.rho_t[row] = rt;
-    if (out) out[row] = rt;
-  } else {
+  {
     int64_t *dst = (MODE == RS_SURV_EV || MODE == RS_DENSITY) ? ws.sub : (MODE == RS_ADM_BASE ? ws.sub_adm : ws.mut_adm);
     atomicAdd(reinterpret_cast<unsigned long long *>(&dst[out_idx]), (unsigned long long)tot);
   }
@@ -933,16 +946,13 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
   rowsum_body<D, P, MODE, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, out, blockIdx.x, blockIdx.y, blockIdx.z, sb);
 }
 
-// The three maintenance sums in one launch (Supp. C): survivors x evicted,
-// admitted x survivors, admitted x admitted; blockIdx.x selects
-// the stage and its row block.
-template <int D, int P, bool FOLD, bool KV>
 // One launch for the three maintenance Grams of every bank (blockIdx.z): x
 // enumerates (row block, column split) pairs, survivors x evicted first
 // (rows_surv row blocks x y_ev splits: at most N evicted states), then
 // admitted x survivors (rows_adm x y_surv), then admitted x admitted
 // (rows_adm x 2 y_ev half splits).  Pairs whose columns lie beyond what the
-// Gram can have are not launched.
+// Gram can have are not launched (Supp. C maintenance).
+template <int D, int P, bool FOLD, bool KV>
 __global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
                                                            Geom g, Prm p, Workspace ws, int rows_surv, int rows_adm,
                                                            int y_ev, int y_surv) {
