@@ -54,6 +54,7 @@ size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, cha
   w.baug = (uint4 *)take(Bz * Mz * 16);
   w.caug = (uint4 *)take(Bz * Nz * 16);
   w.saug = (uint4 *)take(Bz * Nz * 16);
+  w.maint_off = (int32_t *)take((Bz + 1) * 4);
   const int nfw = ((N > 0 ? N : 0) + 1 + 31) / 32;
   w.feas = (uint32_t *)take(Bz * (size_t)nfw * 4);
   w.nfw = nfw;

@@ -946,33 +946,96 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
   rowsum_body<D, P, MODE, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, out, blockIdx.x, blockIdx.y, blockIdx.z, sb);
 }
 
-// One launch for the three maintenance Grams of every bank (blockIdx.z): x
-// enumerates (row block, column split) pairs, survivors x evicted first
-// (rows_surv row blocks x y_ev splits: at most N evicted states), then
-// admitted x survivors (rows_adm x y_surv), then admitted x admitted
-// (rows_adm x 2 y_ev half splits).  Pairs whose columns lie beyond what the
-// Gram can have are not launched (Supp. C maintenance).
+// Maintenance work items (Supp. C): per bank, the (row block, column split)
+// pairs of its three Grams that hold pairs: survivors x evicted (row blocks of
+// the survivors x splits of the evicted), admitted x survivors, and admitted x
+// admitted (half splits).  A bank that admits nothing and releases nothing
+// has none.
+struct MaintItems {
+  int rows_s, rows_a, n_se, n_ab, n_am;
+};
+__device__ __forceinline__ MaintItems maint_items(const Geom &g, const Workspace &ws, int b) {
+  const int ne = ws.n_ev[b], rs = ws.r_star[b / g.gs], ns = ws.m[b] - ne;
+  MaintItems it;
+  it.rows_s = (ns + kRowsPerWG - 1) / kRowsPerWG;
+  it.rows_a = (rs + kRowsPerWG - 1) / kRowsPerWG;
+  it.n_se = it.rows_s * ((ne + kColsPerSplit - 1) / kColsPerSplit);
+  it.n_ab = it.rows_a * ((ns + kColsPerSplit - 1) / kColsPerSplit);
+  it.n_am = it.rows_a * ((rs + kColsPerSplit / 2 - 1) / (kColsPerSplit / 2));
+  return it;
+}
+
+// Exclusive prefix of the banks' work item counts (one workgroup).
+constexpr int kPlanThreads = 1024;
+constexpr unsigned kMaintWgs = 4096;  // maintenance workgroups (3 per CU on 256 CUs, over 5 rounds)
+__global__ __launch_bounds__(kPlanThreads) void k_maint_plan(Geom g, Workspace ws) {
+  __shared__ int32_t part[kPlanThreads];
+  int carry = 0;
+  for (int b0 = 0; b0 < g.B; b0 += kPlanThreads) {
+    const int b = b0 + (int)threadIdx.x;
+    int cnt = 0;
+    if (b < g.B) {
+      const MaintItems it = maint_items(g, ws, b);
+      cnt = it.n_se + it.n_ab + it.n_am;
+    }
+    part[threadIdx.x] = cnt;
+    __syncthreads();
+    for (int o = 1; o < kPlanThreads; o <<= 1) {  // inclusive scan
+      const int y = threadIdx.x >= (unsigned)o ? part[threadIdx.x - o] : 0;
+      __syncthreads();
+      part[threadIdx.x] += y;
+      __syncthreads();
+    }
+    if (b < g.B) ws.maint_off[b] = carry + part[threadIdx.x] - cnt;
+    carry += part[kPlanThreads - 1];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) ws.maint_off[g.B] = carry;
+}
+
+// The maintenance Grams of every bank over the planned work items: workgroup
+// k takes the items [k per, (k + 1) per) in bank order, per = total / grid
+// rounded up, so a frozen block (no item) costs one read per workgroup.
 template <int D, int P, bool FOLD, bool KV>
 __global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
-                                                           Geom g, Prm p, Workspace ws, int rows_surv, int rows_adm,
-                                                           int y_ev, int y_surv) {
+                                                           Geom g, Prm p, Workspace ws) {
   constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
   __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
   __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
   __shared__ __attribute__((aligned(16))) uint32_t cb[3 * kSI];
   const StageBufs<D> sb{k0, k1, k2, a0, a1, a2, cb};
-  int i = blockIdx.x;
-  const int n_se = rows_surv * y_ev, n_ab = rows_adm * y_surv;
-  if (i < n_se) {
-    rowsum_body<D, P, RS_SURV_EV, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, i % rows_surv, i / rows_surv,
-                                        blockIdx.z, sb);
-  } else if ((i -= n_se) < n_ab) {
-    rowsum_body<D, P, RS_ADM_BASE, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, i % rows_adm, i / rows_adm,
-                                         blockIdx.z, sb);
-  } else {
-    i -= n_ab;
-    rowsum_body<D, P, RS_ADM_MUT, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, i % rows_adm, i / rows_adm,
-                                        blockIdx.z, sb);
+  const int total = ws.maint_off[g.B];
+  const int per = (total + (int)gridDim.x - 1) / (int)gridDim.x;
+  const int w0 = (int)blockIdx.x * per, w1 = min(total, w0 + per);
+  if (w0 >= w1) return;
+  // bank of item w0: the last bank whose first item is <= w0 (banks without
+  // items share the offset of the next bank)
+  int lo = 0, hi = g.B;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (ws.maint_off[mid] <= w0) lo = mid;
+    else hi = mid;
+  }
+  int b = lo, i = w0 - ws.maint_off[b];
+  MaintItems it = maint_items(g, ws, b);
+  for (int w = w0; w < w1; ++w, ++i) {
+    while (i >= it.n_se + it.n_ab + it.n_am && b + 1 < g.B) {  // next bank with items
+      i -= it.n_se + it.n_ab + it.n_am;
+      it = maint_items(g, ws, ++b);
+    }
+    __syncthreads();  // the previous item's LDS stages are done with
+    if (i < it.n_se) {
+      rowsum_body<D, P, RS_SURV_EV, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, i % it.rows_s, i / it.rows_s, b,
+                                          sb);
+    } else if (i < it.n_se + it.n_ab) {
+      const int j = i - it.n_se;
+      rowsum_body<D, P, RS_ADM_BASE, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, j % it.rows_a, j / it.rows_a, b,
+                                           sb);
+    } else {
+      const int j = i - it.n_se - it.n_ab;
+      rowsum_body<D, P, RS_ADM_MUT, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, j % it.rows_a, j / it.rows_a, b,
+                                          sb);
+    }
   }
 }
 
@@ -1283,13 +1346,15 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       k_rowsum_mfma<D, P, RS_FIXUP, F, KV><<<dim3(rowsM, 1, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, out.rho_tilde);
       break;
     case 3: {
-      // evicted states <= admitted <= N: their column splits cover N; the
-      // survivors' cover Mcap
-      const int nadm = g.N > 0 ? (int)rowsN : 0;
+      // the work items, then a grid of at most kMaintWgs workgroups over them
+      // (evicted states <= admitted <= N: at most rowsM x splits of N, plus
+      // rowsN x (splits of Mcap + half splits of N) items per bank)
+      k_maint_plan<<<1, kPlanThreads, 0, s>>>(g, ws);
       const unsigned y_ev = cdiv(g.N > 0 ? g.N : 1, kColsPerSplit), y_surv = cdiv(g.Mcap, kColsPerSplit);
-      const unsigned nx = rowsM * y_ev + (unsigned)nadm * (y_surv + 2 * y_ev);
-      k_maint_mfma<D, P, F, KV><<<dim3(nx, 1, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, (int)rowsM, nadm, (int)y_ev,
-                                                             (int)y_surv);
+      const unsigned long long bound =
+          (unsigned long long)(rowsM * y_ev + (g.N > 0 ? rowsN : 0u) * (y_surv + 2 * y_ev)) * (unsigned)g.B;
+      const unsigned nwg = (unsigned)(bound < kMaintWgs ? (bound > 0 ? bound : 1) : kMaintWgs);
+      k_maint_mfma<D, P, F, KV><<<nwg, T, 0, s>>>(bank, seg.k, sv, g, p, ws);
       break;
     }
     default:

@@ -48,6 +48,7 @@ struct Workspace {
   uint4 *baug;         // [B, Mcap] column aug step of each bank state (column_aug)
   uint4 *caug;         // [B, N]   of each candidate, source order
   uint4 *saug;         // [B, N]   of each candidate, score order
+  int32_t *maint_off;  // [B + 1] first maintenance work item of each bank; [B] = total
   uint32_t *feas;      // [B, nfw] bit r: prefix length r feasible for this bank
   int nfw;             // words per bank of feas
   uint64_t *skeys;     // [B, npad] sort keys, sorted within 512-key chunks
