@@ -9,8 +9,9 @@
 //                  candidates (the prefix checkpoints of Eqs. 8-9), the r*
 //                  fix-up, the exact maintenance (Supp. C) and the
 //                  from-scratch bank density (Eq. 3)
-//   k_cross        per bank state: the chunk in which its prefix density first
+//   k_cross_mfma   per bank state: the chunk in which its prefix density first
 //                  reaches tau b, then the exact prefix length inside it
+//                  (k_cross_wide for descriptors wider than 128)
 //
 // The column range of every Gram is split over workgroups (grid dimension y);
 // partial integer sums are combined with 64-bit atomic adds, which are exact
@@ -1040,31 +1041,303 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, co
 }
 
 // ---------------------------------------------------------------------------
-// First violating prefix length of every bank state (Eqs. 8-9).  A wave takes
-// eight states, one per group of 8 lanes; each lane adds 16 of the state's
-// 64-candidate chunk sums, a scan over the group gives every chunk's end
-// prefix, and the first chunk whose end lifts rho + P to tau b
-// (2^k (rho + P) >= T b, integers) is found by ballot.  Then the exact length
-// inside that chunk, with the same binary32 weights: for descriptors of up to
-// 128 elements one 8 x 64 MFMA Gram per distinct crossing chunk covers every
-// state of the wave that crosses there; wider descriptors re-walk the chunk
-// one state at a time with one ordered candidate per lane.  States that never
-// reach the bound within the tested prefixes get R + 1.
+// First violating prefix length of every bank state (Eqs. 8-9).
+//
+// Chunk search: the state's group of 8 lanes holds its 64-candidate chunk
+// sums, 16 per lane; a scan over the group gives every lane's prefix, and the
+// lane whose 16 chunks contain the first prefix that lifts rho + P to tau b
+// (2^k (rho + P) >= T b, integers) finds the chunk and how much of that
+// chunk's weight is still needed.  Then the exact length inside the chunk,
+// with the same binary32 weights.  States that never reach the bound within
+// the tested prefixes get R + 1; states whose empty prefix already violates 0.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
   const uint32_t lo = __shfl((uint32_t)v, src, 64), hi = __shfl((uint32_t)(v >> 32), src, 64);
   return ((uint64_t)hi << 32) | lo;
 }
 
-constexpr int kCrossLanes = 8;                      // lanes per state
+constexpr int kCrossLanes = 8;                      // lanes per state in the chunk search
 constexpr int kCrossPerLane = 16;                   // chunk sums per lane
-constexpr int kCrossStates = 64 / kCrossLanes;      // states per wave
+constexpr int kCrossStates = 64 / kCrossLanes;      // states per chunk-search pass of a wave
 
-template <int D, int P, bool KV>
-__global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
-  static_assert(kCkStride == 64, "one candidate per lane in the exact walk");
+// v of the lane O below within a group of 8 lanes (a DPP row shift: the group
+// lies in one row of 16 lanes), 0 for the group's first O lanes (q < O).  A DPP
+// read from a lane that is switched off returns 0, so the shift runs with every
+// lane on (the empty asm keeps it out of the branch of q >= O) and the select
+// follows.
+template <int O>
+__device__ __forceinline__ uint64_t group_shr_u64(uint64_t v, int q) {
+  static_assert(O >= 1 && O < kCrossLanes, "shift within a group");
+  uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, 0x110 + O, 0xF, 0xF, true);
+  uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), 0x110 + O, 0xF, 0xF, true);
+  asm volatile("" : "+v"(lo), "+v"(hi));
+  return q >= O ? ((uint64_t)hi << 32) | lo : 0ull;
+}
+
+struct CrossFind {
+  bool pos;       // the bound lies above rho (else the empty prefix violates)
+  bool hit;       // this lane's chunks hold the first prefix that reaches it
+  int ch;         // that chunk (hit lane only)
+  uint32_t need;  // the bound minus rho minus every chunk before it, in [1, 2^29] (hit lane only)
+};
+
+// Chunk search for one bank row by lane q of its group: the loads (issued
+// together for several rows), then the search; nch chunks are tested.
+struct CrossRow {
+  int64_t base, rho;
+  uint4 x[kCrossPerLane / 4];
+};
+
+__device__ __forceinline__ CrossRow cross_load(const dkv_bank &bank, const Workspace &ws, size_t row, int q) {
+  CrossRow r;
+  r.base = bank.base[row];
+  r.rho = bank.rho[row];
+  // 16-byte groups of the row (nck >= 4, a multiple of 4, at least nch); clamped
+  const uint4 *ckr = reinterpret_cast<const uint4 *>(ws.ck + row * ws.nck);
+  const int last = ws.nck / 4 - 1;
+#pragma unroll
+  for (int v4 = 0; v4 < kCrossPerLane / 4; ++v4) r.x[v4] = ckr[min((kCrossPerLane * q) / 4 + v4, last)];
+  return r;
+}
+
+__device__ __forceinline__ CrossFind cross_find(const CrossRow &r, const Prm &p, int nch, int q) {
   static_assert((DKV_MAX_CANDIDATES + kCkStride - 1) / kCkStride <= kCrossLanes * kCrossPerLane,
                 "every chunk sum of a state is held by its lane group");
+  const int64_t lim = ((int64_t)p.tau_num * r.base + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
+  const int64_t thr = lim - r.rho;
+  uint32_t c[kCrossPerLane];
+#pragma unroll
+  for (int v4 = 0; v4 < kCrossPerLane / 4; ++v4) {
+    const int c0 = kCrossPerLane * q + 4 * v4;
+    c[4 * v4 + 0] = c0 + 0 < nch ? r.x[v4].x : 0u;
+    c[4 * v4 + 1] = c0 + 1 < nch ? r.x[v4].y : 0u;
+    c[4 * v4 + 2] = c0 + 2 < nch ? r.x[v4].z : 0u;
+    c[4 * v4 + 3] = c0 + 3 < nch ? r.x[v4].w : 0u;
+  }
+  // a chunk sum is at most 64 x 2^23 = 2^29: seven of them fit 32 bits, eight may not
+  uint32_t a7 = 0, b7 = 0;
+#pragma unroll
+  for (int t = 0; t < 7; ++t) {
+    a7 += c[t];
+    b7 += c[8 + t];
+  }
+  const uint64_t s8a = (uint64_t)a7 + c[7], tot = s8a + (uint64_t)b7 + c[15];
+  // inclusive scan over the group (DPP row shifts: a group of 8 lies in one row of 16 lanes)
+  uint64_t incl = tot;
+  incl += group_shr_u64<1>(incl, q);
+  incl += group_shr_u64<2>(incl, q);
+  incl += group_shr_u64<4>(incl, q);
+  // what this lane's chunks must still supply; the crossing lies in them iff it is in (0, tot]
+  const int64_t need_l = thr - (int64_t)(incl - tot);
+  CrossFind f;
+  f.pos = thr > 0;
+  f.hit = f.pos && need_l > 0 && need_l <= (int64_t)tot;
+  // the half of the lane's chunks that holds it, and the rest in [1, 2^32] (32 bits after -1)
+  const bool hi = need_l > (int64_t)s8a;
+  const uint32_t nd1 = (uint32_t)((uint64_t)(hi ? need_l - (int64_t)s8a : need_l) - 1u);
+  // chunks of that half before the crossing: those whose end prefix is still below the bound
+  // (the half's full sum reaches it, so at most seven, whose prefixes fit 32 bits)
+  uint32_t pr = 0, pre = 0;
+  int cnt = 0;
+#pragma unroll
+  for (int t = 0; t < 7; ++t) {
+    pr += hi ? c[8 + t] : c[t];
+    if (pr <= nd1) {
+      ++cnt;
+      pre = pr;
+    }
+  }
+  f.ch = kCrossPerLane * q + (hi ? 8 : 0) + cnt;
+  f.need = nd1 - pre + 1u;
+  return f;
+}
+
+// Descriptors of up to 128 elements: a wave takes 32 states.  The chunk search
+// runs in four passes of eight states; each state's result then moves to lanes
+// n and n + 32 (n = its index in the wave).  The exact walk: for every distinct
+// crossing chunk among the wave's states one 64 x 32 MFMA Gram, A = the chunk's
+// ordered candidates (two tiles of 32) with their norm steps, B = the 32 states
+// as the Gram stages hold row items, so lane (n, h) gets t of state n with
+// candidates 8 k + 4 h + j (registers 4 k + j) of each tile, bit for bit the t
+// that made the chunk sums; each lane keeps the Gram of its own chunk.  Then,
+// once per lane, the weights summed in candidate order (the two halves exchange
+// their 4-candidate group sums), and the crossing length is one plus the number
+// of candidates whose inclusive prefix is still below the need.
+constexpr int kCrossWaveStates = 32;
+
+template <int D, int P, bool FOLD, bool KV>
+__global__ __launch_bounds__(256, 4) void k_cross_mfma(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
+  static_assert(D <= 128 && kCkStride == 64, "two 32-candidate tiles per chunk");
+  constexpr int KSW = D / 16;
+  const int b = blockIdx.y;
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int grp = l / kCrossLanes, q = l % kCrossLanes, n32 = l & 31, hw = l >> 5;
+  const int i0 = (blockIdx.x * kWaves + wave) * kCrossWaveStates;
+  const int m = ws.m[b], R = ws.R[b];
+  if ((int)blockIdx.x * kWaves * kCrossWaveStates >= m) return;  // whole workgroup (the walk has barriers)
+  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
+  const int nch = (R + kCkStride - 1) / kCkStride;
+  // per state of this lane's column: whether its bound lies above rho, whether
+  // it crosses within the tested prefixes, the crossing chunk and the need
+  int my_ch = 0;
+  uint32_t my_need = 0;
+  bool my_pos = false, my_walk = false;
+  constexpr int kPasses = kCrossWaveStates / kCrossStates;
+  CrossRow rows[kPasses];  // every pass's loads in flight together
+#pragma unroll
+  for (int ps = 0; ps < kPasses; ++ps) rows[ps] = cross_load(bank, ws, rb + min(i0 + kCrossStates * ps + grp, m - 1), q);
+#pragma unroll
+  for (int ps = 0; ps < kPasses; ++ps) {
+    const int s = kCrossStates * ps + grp;
+    const bool valid = i0 + s < m;
+    const CrossFind f = cross_find(rows[ps], p, nch, q);
+    const unsigned long long pos = __ballot(valid && f.pos);
+    const unsigned long long hits = __ballot(valid && f.hit);
+    // group g8 of this pass -> lanes n32 = 8 ps + g8
+    const int g8 = (n32 - kCrossStates * ps) & (kCrossStates - 1);
+    const unsigned gbits = (unsigned)(hits >> (kCrossLanes * g8)) & 0xFFu;
+    const int src = kCrossLanes * g8 + (gbits ? __ffs(gbits) - 1 : 0);
+    const int ch = __shfl(f.ch, src, 64);
+    const uint32_t nd = __shfl(f.need, src, 64);
+    if ((n32 >> 3) == ps) {
+      my_ch = ch;
+      my_need = nd;
+      my_pos = (pos >> (kCrossLanes * g8)) & 1ull;
+      my_walk = gbits != 0;
+    }
+  }
+  int first = my_pos ? R + 1 : 0;
+  // the workgroup's crossing chunks (at most 128: four words)
+  __shared__ uint32_t chunk_set[4];
+  if (threadIdx.x < 4) chunk_set[threadIdx.x] = 0;
+  __syncthreads();
+  if (my_walk && hw == 0) atomicOr(&chunk_set[my_ch >> 5], 1u << (my_ch & 31));
+  __syncthreads();
+  uint32_t cs[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) cs[k] = __builtin_amdgcn_readfirstlane(chunk_set[k]);
+  if (cs[0] | cs[1] | cs[2] | cs[3]) {  // uniform over the workgroup
+    // B operand: this lane's state as the Gram stages hold a row item (keys
+    // times -2 / sigma^2 and the norm step)
+    const int64_t srow = (int64_t)(rb + min(i0 + n32, m - 1));
+    RowFrag<D> rf;
+    load_row_frag<D, FOLD, KV>(rf, Desc{static_cast<const uint16_t *>(bank.k), static_cast<const uint16_t *>(bank.v)},
+                               srow, bank.knorm[srow], true, -2.0f * p.inv_sigma2, p.inv_sigma2);
+    int aoff[TileCfg<D>::kSteps];
+    frag_offsets<D>(aoff);
+    // each crossing chunk's 64 ordered candidates go through a stage buffer
+    // (two, alternating) exactly as in the chunk-sum Gram, so t and every
+    // weight are those of the chunk sums bit for bit; each lane keeps the
+    // Gram of its own chunk
+    constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
+    __shared__ __attribute__((aligned(1024))) char kbuf[2][KB];
+    __shared__ __attribute__((aligned(16))) char abuf[2][AB];
+    const Desc OK{ws.sk, nullptr};
+    int32_t srows[SCfg<D>::PER + 1];
+    auto issue = [&](int c, int buf) __attribute__((always_inline)) {
+      const int j0 = c * kCkStride;
+      stage_rows<D>(srows, 0, min(kCkStride, R - j0), [&](int j) -> int64_t { return (int64_t)(nb + j0 + j); });
+      stage_dma<D, false, false>(srows, OK, ws.saug, nullptr, kbuf[buf], abuf[buf], nullptr, (int64_t)nb, g.N);
+    };
+    // the chunks in increasing order (uniform over the workgroup)
+    auto pop_chunk = [&]() __attribute__((always_inline)) -> int {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        if (cs[k]) {
+          const int c = 32 * k + __builtin_ctz(cs[k]);
+          cs[k] &= cs[k] - 1;
+          return c;
+        }
+      return -1;
+    };
+    f32x16 mine[2] = {};
+    bool partial = false;
+    int c = pop_chunk(), buf = 0;
+    issue(c, 0);
+    while (c >= 0) {
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+      stage_barrier();  // every wave's loads of chunk c landed; every wave is done with the other buffer
+      const int cn = pop_chunk();
+      if (cn >= 0) issue(cn, buf ^ 1);
+      partial = partial || (c + 1) * kCkStride > R;
+      const bool keep = my_walk && my_ch == c;
+      if (__ballot(keep)) {  // uniform over the wave
+#pragma unroll
+        for (int tl = 0; tl < 2; ++tl) {
+          const f32x16 x = tile_mfma<D>(kbuf[buf], abuf[buf], tl, rf, aoff);
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mine[tl][r] = keep ? x[r] : mine[tl][r];
+        }
+      }
+      c = cn;
+      buf ^= 1;
+    }
+    // weights in candidate order inside the lane (groups of four consecutive
+    // candidates, k = 0..3 of each tile, the two halves alternating); candidates
+    // past R weigh nothing (wave-uniform test: a chunk that ends past R)
+    const int ch0 = my_ch * kCkStride;
+    const int nvalid = min(kCkStride, R - ch0);
+    uint32_t w[2][16], gs[2][4];
+    auto weights = [&](auto mask_tag) __attribute__((always_inline)) {
+      constexpr bool MASK = decltype(mask_tag)::value;
+#pragma unroll
+      for (int tl = 0; tl < 2; ++tl) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          gs[tl][k] = 0;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            uint32_t W = weight_raw<P, FOLD>(mine[tl][4 * k + j], 8388608.0f) - kMagic;
+            if constexpr (MASK) {
+              asm volatile("" : "+v"(W));  // computed for every lane, then masked
+              W = 32 * tl + 8 * k + 4 * hw + j < nvalid ? W : 0u;
+            }
+            w[tl][4 * k + j] = W;
+            gs[tl][k] += W;
+          }
+        }
+      }
+    };
+    if (!__ballot(my_walk)) goto done;  // uniform over the wave
+    if (partial) weights(std::integral_constant<bool, true>{});
+    else weights(std::integral_constant<bool, false>{});
+    // inclusive prefixes in candidate order; the crossing length is one plus the
+    // number still below the need.  Candidates past R add nothing, so their
+    // prefix equals the last valid one's and they are counted only if that one
+    // was (cnt then reaches nvalid either way).
+    uint32_t run = 0, cnt = 0;
+    const uint32_t nd1 = my_need - 1u;
+#pragma unroll
+    for (int tl = 0; tl < 2; ++tl) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint32_t other = __shfl_xor(gs[tl][k], 32, 64);
+        uint32_t pr = run + (hw ? other : 0u);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          pr += w[tl][4 * k + j];
+          cnt += pr <= nd1 ? 1u : 0u;
+        }
+        run += gs[tl][k] + other;
+      }
+    }
+    cnt += __shfl_xor(cnt, 32, 64);
+    if (my_walk) first = (int)cnt < nvalid ? ch0 + (int)cnt + 1 : ch0 + nvalid;  // the latter unreachable
+  }
+done:
+  const int i = i0 + n32;
+  if (hw == 0 && i < m) {
+    ws.first[rb + i] = first;
+    if (out_first) out_first[rb + i] = first;
+  }
+}
+
+// Wider descriptors ([K; V] at d = 128): a wave takes eight states, one chunk
+// search pass, and re-walks each crossing chunk one state at a time with one
+// ordered candidate per lane.
+template <int D, int P, bool KV>
+__global__ __launch_bounds__(256) void k_cross_wide(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
+  static_assert(kCkStride == 64, "one candidate per lane in the exact walk");
   const int b = blockIdx.y;
   const int l = threadIdx.x & 63, grp = l / kCrossLanes, q = l % kCrossLanes;
   const int i0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kCrossStates;
@@ -1073,189 +1346,52 @@ __global__ __launch_bounds__(256) void k_cross(dkv_bank bank, Geom g, Prm p, Wor
   const int i = i0 + grp;
   const bool valid = i < m;
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
-  const size_t row = rb + (valid ? i : i0);
-  const int64_t lim = ((int64_t)p.tau_num * bank.base[row] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
-  const int64_t thr = lim - bank.rho[row];
   const int nch = (R + kCkStride - 1) / kCkStride;
-  // this lane's chunk sums [16 q, 16 q + 16)
-  uint32_t c[kCrossPerLane];
-  const uint4 *ckr = reinterpret_cast<const uint4 *>(ws.ck + row * ws.nck);
-  const int nq4 = ws.nck / 4;  // 16-byte groups per row (nck >= nch, a multiple of 4)
-#pragma unroll
-  for (int v4 = 0; v4 < kCrossPerLane / 4; ++v4) {
-    const int c0 = kCrossPerLane * q + 4 * v4;
-    uint4 x = {0u, 0u, 0u, 0u};
-    if (nq4 > 0) x = ckr[min(c0 / 4, nq4 - 1)];  // clamped, unconditional per lane
-    c[4 * v4 + 0] = c0 + 0 < nch ? x.x : 0u;
-    c[4 * v4 + 1] = c0 + 1 < nch ? x.y : 0u;
-    c[4 * v4 + 2] = c0 + 2 < nch ? x.z : 0u;
-    c[4 * v4 + 3] = c0 + 3 < nch ? x.w : 0u;
-  }
-  uint64_t tot = 0;
-#pragma unroll
-  for (int t = 0; t < kCrossPerLane; ++t) tot += c[t];
-  uint64_t incl = tot;
-#pragma unroll
-  for (int o = 1; o < kCrossLanes; o <<= 1) {
-    const uint64_t y = (uint64_t)__shfl_up((uint32_t)incl, o, kCrossLanes) |
-                       ((uint64_t)__shfl_up((uint32_t)(incl >> 32), o, kCrossLanes) << 32);
-    if (q >= o) incl += y;
-  }
-  // first chunk of this lane whose end prefix reaches thr, and the prefix before it
-  uint64_t run = incl - tot, pre = 0;
-  int ft = -1;
-#pragma unroll
-  for (int t = 0; t < kCrossPerLane; ++t) {
-    const uint64_t nx = run + c[t];
-    if (ft < 0 && kCrossPerLane * q + t < nch && (int64_t)nx >= thr) {
-      ft = t;
-      pre = run;
-    }
-    run = nx;
-  }
-  const bool thr_pos = thr > 0;
-  const unsigned long long hits = __ballot(valid && thr_pos && ft >= 0);
-  // group result (held by every lane of the group): crossing chunk and prefix before it
-  const unsigned gbits = (unsigned)(hits >> (kCrossLanes * grp)) & ((1u << kCrossLanes) - 1);
-  const int src = kCrossLanes * grp + (gbits ? __ffs(gbits) - 1 : 0);
-  const int ch = kCrossPerLane * (src % kCrossLanes) + __shfl(ft, src, 64);
-  const uint64_t pb = shfl_u64(pre, src);
-  int first = thr_pos ? R + 1 : 0;
-  // exact walk, one crossing state at a time (wave-uniform loop)
+  const CrossFind f = cross_find(cross_load(bank, ws, rb + (valid ? i : i0), q), p, nch, q);
+  const unsigned long long hits = __ballot(valid && f.hit);
+  int first = f.pos ? R + 1 : 0;
   unsigned long long todo = 0;
 #pragma unroll
   for (int s2 = 0; s2 < kCrossStates; ++s2)
-    if ((hits >> (kCrossLanes * s2)) & ((1ull << kCrossLanes) - 1)) todo |= 1ull << s2;
+    if ((hits >> (kCrossLanes * s2)) & 0xFFull) todo |= 1ull << s2;
   const Desc bd{static_cast<const uint16_t *>(bank.k), static_cast<const uint16_t *>(bank.v)};
-  if constexpr (D <= 128) {
-    // Exact walk on the matrix cores, all the wave's states that cross in
-    // the same chunk at once: A = the eight states (rows 0-7: lanes 0-7 of
-    // each half-wave, zeros elsewhere), B = the chunk's 64 ordered candidates
-    // in two tiles of 32 (lane n <-> candidate n of the tile), so register
-    // r4 < 4 of lane (n, h) holds the dot product of state 4 h + r4 with
-    // candidate n.  The dot products are exact on the key grid, as in the
-    // chunk sums; then the same binary32 weights, a prefix over the 32
-    // lanes of each tile, and a ballot for the first length reaching the
-    // threshold.
-    constexpr int KSW = D / 16;
-    const int n32 = l & 31, hw = l >> 5;
-    bf16x8 sa[KSW];
-    {
-      const int64_t arow = (int64_t)(rb + min(i0 + (n32 < kCrossStates ? n32 : 0), m - 1));
+  while (todo) {
+    const int s2 = __ffsll(todo) - 1;
+    todo &= todo - 1;
+    const unsigned gbits = (unsigned)(hits >> (kCrossLanes * s2)) & 0xFFu;
+    const int src = kCrossLanes * s2 + __ffs(gbits) - 1;
+    const int c_s = __shfl(f.ch, src, 64);
+    const uint32_t need = __shfl(f.need, src, 64);
+    const size_t srow = rb + i0 + s2;
+    const float nr = bank.knorm[srow];
+    const int col = c_s * kCkStride + l;
+    uint32_t W = 0;
+    if (col < R) {
+      const uint16_t *ckey = ws.sk + (nb + col) * D;
+      float acc = 0.0f;
 #pragma unroll
-      for (int kk = 0; kk < KSW; ++kk) {
-        const u32x4 x = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(bd, arow, 2 * kk + hw));
-        sa[kk] = __builtin_bit_cast(bf16x8, n32 < kCrossStates ? x : u32x4{0u, 0u, 0u, 0u});
+      for (int j = 0; j < D; j += 8) {
+        const u32x4 ra = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(bd, (int64_t)srow, j / 8));
+        const u32x4 rc = *reinterpret_cast<const u32x4 *>(ckey + j);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc = __builtin_fmaf(__uint_as_float(ra[e] << 16), __uint_as_float(rc[e] << 16), acc);
+          acc = __builtin_fmaf(__uint_as_float(ra[e] & 0xFFFF0000u), __uint_as_float(rc[e] & 0xFFFF0000u), acc);
+        }
       }
+      const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
+      W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
     }
-    float nrq[4];
-    int64_t pbq[4], thq[4];
+    uint32_t wi = W;
 #pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      const int st = 4 * hw + r4;
-      nrq[r4] = bank.knorm[rb + min(i0 + st, m - 1)];
-      pbq[r4] = (int64_t)shfl_u64(pb, kCrossLanes * st);
-      thq[r4] = (int64_t)shfl_u64((uint64_t)thr, kCrossLanes * st);
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t y = __shfl_up(wi, o, 64);
+      if (l >= o) wi += y;
     }
-    while (todo) {
-      const int s0 = __ffsll(todo) - 1;
-      const int c_s = __shfl(ch, kCrossLanes * s0, 64);
-      // the states of this wave that cross in the same chunk (group leaders vote)
-      const unsigned long long lead = __ballot(q == 0 && ch == c_s);
-      unsigned long long same = 0;
-#pragma unroll
-      for (int s2 = 0; s2 < kCrossStates; ++s2)
-        if ((lead >> (kCrossLanes * s2)) & 1ull) same |= 1ull << s2;
-      same &= todo;
-      todo &= ~same;
-      f32x16 acc[2];
-      float cn[2];
-      int cols[2];
-#pragma unroll
-      for (int tl = 0; tl < 2; ++tl) {
-        cols[tl] = c_s * kCkStride + 32 * tl + n32;
-        // clamped (in-range) candidate; lanes past R add nothing
-        const size_t crow = nb + min(cols[tl], R - 1);
-        const uint16_t *ckey = ws.sk + crow * D;
-        cn[tl] = ws.snorm[crow];
-        f32x16 ac = {};
-#pragma unroll
-        for (int kk = 0; kk < KSW; ++kk) {
-          const u32x4 bx = *reinterpret_cast<const u32x4 *>(ckey + 16 * kk + 8 * hw);
-          ac = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa[kk], __builtin_bit_cast(bf16x8, bx), ac, 0, 0, 0);
-        }
-        acc[tl] = ac;
-      }
-#pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        uint32_t w[2];
-#pragma unroll
-        for (int tl = 0; tl < 2; ++tl) {
-          const float d2 = (nrq[r4] + cn[tl]) - 2.0f * acc[tl][r4];
-          w[tl] = cols[tl] < R ? weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic : 0u;
-        }
-#pragma unroll
-        for (int o = 1; o < 32; o <<= 1) {
-          const uint32_t y0 = __shfl_up(w[0], o, 32), y1 = __shfl_up(w[1], o, 32);
-          if (n32 >= o) {
-            w[0] += y0;
-            w[1] += y1;
-          }
-        }
-        w[1] += __shfl(w[0], 31, 32);  // the first tile's total
-        const unsigned long long h0 = __ballot(pbq[r4] + (int64_t)w[0] >= thq[r4]);
-        const unsigned long long h1 = __ballot(pbq[r4] + (int64_t)w[1] >= thq[r4]);
-#pragma unroll
-        for (int hh = 0; hh < 2; ++hh) {
-          const int st = 4 * hh + r4;
-          if (!((same >> st) & 1ull)) continue;
-          const unsigned m0 = (unsigned)(h0 >> (32 * hh)), m1 = (unsigned)(h1 >> (32 * hh));
-          // no hit is unreachable when both passes agree (exact Gram)
-          const int f = m0 ? c_s * kCkStride + __ffs(m0) : (m1 ? c_s * kCkStride + 32 + __ffs(m1) : min(R, (c_s + 1) * kCkStride));
-          if (grp == st) first = f;
-        }
-      }
-    }
-  } else {
-    // wide descriptors: one crossing state at a time, one ordered candidate per lane
-    while (todo) {
-      const int s2 = __ffsll(todo) - 1;
-      todo &= todo - 1;
-      const int sl = kCrossLanes * s2;  // first lane of that state's group
-      const size_t srow = rb + i0 + s2;
-      const int c_s = __shfl(ch, sl, 64);
-      const int64_t pb_s = (int64_t)shfl_u64(pb, sl);
-      const int64_t thr_s = (int64_t)shfl_u64((uint64_t)thr, sl);
-      const float nr = bank.knorm[srow];
-      const int col = c_s * kCkStride + l;
-      uint32_t W = 0;
-      if (col < R) {
-        const uint16_t *ckey = ws.sk + (nb + col) * D;
-        float acc = 0.0f;
-#pragma unroll
-        for (int j = 0; j < D; j += 8) {
-          const u32x4 ra = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(bd, (int64_t)srow, j / 8));
-          const u32x4 rc = *reinterpret_cast<const u32x4 *>(ckey + j);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            acc = __builtin_fmaf(__uint_as_float(ra[e] << 16), __uint_as_float(rc[e] << 16), acc);
-            acc = __builtin_fmaf(__uint_as_float(ra[e] & 0xFFFF0000u), __uint_as_float(rc[e] & 0xFFFF0000u), acc);
-          }
-        }
-        const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
-        W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
-      }
-      uint32_t wi = W;
-#pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(wi, o, 64);
-        if (l >= o) wi += y;
-      }
-      const unsigned long long h2 = __ballot(pb_s + (int64_t)wi >= thr_s);
-      const int f = h2 != 0 ? c_s * kCkStride + (__ffsll(h2) - 1) + 1
-                            : min(R, (c_s + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
-      if (grp == s2) first = f;
-    }
+    const unsigned long long h2 = __ballot(wi >= need);
+    const int fc = h2 != 0 ? c_s * kCkStride + (__ffsll(h2) - 1) + 1
+                           : min(R, (c_s + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
+    if (grp == s2) first = fc;
   }
   if (valid && q == 0) {
     ws.first[rb + i] = first;
@@ -1339,7 +1475,11 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       if (g.N > 0)
         k_rowsum_mfma<D, P, RS_CHUNK, F, KV><<<dim3(rowsM, cdiv(g.N, kChunksPerSplit * kCkStride), g.B), T, 0, s>>>(
             bank, seg.k, sv, g, p, ws, nullptr);
-      k_cross<D, P, KV><<<dim3(cdiv(g.Mcap, 4 * kCrossStates), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
+      if constexpr (D <= 128)
+        k_cross_mfma<D, P, F, KV><<<dim3(cdiv(g.Mcap, 4 * kCrossWaveStates), g.B), 256, 0, s>>>(bank, g, p, ws,
+                                                                                             out.first_cross);
+      else
+        k_cross_wide<D, P, KV><<<dim3(cdiv(g.Mcap, 4 * kCrossStates), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
       break;
     }
     case 2:
