@@ -234,6 +234,49 @@ __device__ __forceinline__ void stage_dma(const int32_t (&rows)[SCfg<D>::PER + 1
   }
 }
 
+// Stages whose rows are consecutive (row i of a stage = the stage's first row
+// + i: bank slots in order, or the ordered candidates): each lane's byte
+// offsets are the same for every stage, and the stage's first row goes into the
+// uniform buffer base, so no per-stage row arithmetic runs on the VALU.
+template <int D>
+struct StageOff {
+  int key[SCfg<D>::PER];  // key loads: row r of the stage, swizzled chunk c, as r RB + 16 c
+  int item;               // aug / scale item of lanes 0-15 of each wave: 16 w + lane
+};
+
+template <int D>
+__device__ __forceinline__ StageOff<D> stage_offsets() {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
+  StageOff<D> o;
+#pragma unroll
+  for (int q = 0; q < SCfg<D>::PER; ++q) {
+    const int r = (wave * SCfg<D>::PER + q) * SCfg<D>::RPL + l / SCfg<D>::CH;
+    o.key[q] = r * SCfg<D>::RB + 16 * ((l % SCfg<D>::CH) ^ (r % SCfg<D>::CH));
+  }
+  o.item = 16 * wave + (l & 15);
+  return o;
+}
+
+// Loads of the stage whose first row is row0 + first (whole-row descriptors).
+// The buffers end where the region [row0, row0 + nrows) ends, so rows past it
+// read as zero; rows past the Gram's last column are real rows of the region,
+// masked by the epilogue like the repeated last row they replace.
+template <int D, bool kBs>
+__device__ __forceinline__ void stage_dma_seq(const StageOff<D> &o, int first, const uint16_t *keys, const uint4 *augs,
+                                              const float *bs, char *kb, char *ab, float *sb, int64_t row0,
+                                              int nrows) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
+  const int64_t r0 = row0 + first;
+  const int left = nrows - first;  // rows from the stage's first to the region's end
+#pragma unroll
+  for (int q = 0; q < SCfg<D>::PER; ++q)
+    buffer_to_lds16(keys + r0 * D, left * SCfg<D>::RB, o.key[q], kb + (wave * SCfg<D>::PER + q) * 1024);
+  if (l < 16) {
+    buffer_to_lds16(augs + r0, left * 16, o.item * 16, ab + 256 * wave);
+    if constexpr (kBs) buffer_to_lds4(bs + r0, left * 4, o.item * 4, reinterpret_cast<char *>(sb + 16 * wave));
+  }
+}
+
 // s_waitcnt immediate (gfx9 encoding): at most n vector-memory operations
 // outstanding and no LDS operation outstanding (expcnt left alone).
 constexpr int waitcnt_vm_lgkm0(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
@@ -407,6 +450,16 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
   using Part = std::integral_constant<bool, true>;
   constexpr int kOps = stage_ops<D, true>();
   int32_t rows[SCfg<D>::PER + 1];
+  // stage s: rows s kSI .. of this split; whole-row descriptors take the
+  // per-lane offsets of consecutive rows, [K; V] ones (two arrays) the row list
+  [[maybe_unused]] const StageOff<D> soff = stage_offsets<D>();
+  auto stage_rows_for = [&](int st) __attribute__((always_inline)) {
+    if constexpr (KV) stage_rows<D>(rows, st * kSI, ncols, row_of);
+  };
+  auto stage_dma_for = [&](int st, char *kd, char *ad, float *sd) __attribute__((always_inline)) {
+    if constexpr (KV) stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, kd, ad, sd, bank_row0, g.Mcap);
+    else stage_dma_seq<D, true>(soff, c0 + st * kSI, BK.k, ws.baug, ws.bs, kd, ad, sd, bank_row0, g.Mcap);
+  };
   // stage t in buffers (t % 3); rows of stage t + 2 loaded one step ahead
   auto step = [&](int t, const char *kb, const char *ab, const float *sb, char *kn, char *an, float *sn)
       __attribute__((always_inline)) {
@@ -414,8 +467,8 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
     else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
     stage_barrier();
     if (t + 2 < ns) {
-      stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, kn, an, sn, bank_row0, g.Mcap);
-      if (t + 3 < ns) stage_rows<D>(rows, (t + 3) * kSI, ncols, row_of);
+      stage_dma_for(t + 2, kn, an, sn);
+      if (t + 3 < ns) stage_rows_for(t + 3);
     }
     f32x16 u0, u1;
     stage_u<D, 0>(kb, ab, rf, u0, u1);
@@ -435,12 +488,12 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
       }
     }
   };
-  stage_rows<D>(rows, 0, ncols, row_of);
-  stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k0, a0, s0, bank_row0, g.Mcap);
+  stage_rows_for(0);
+  stage_dma_for(0, k0, a0, s0);
   if (ns > 1) {
-    stage_rows<D>(rows, kSI, ncols, row_of);
-    stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k1, a1, s1, bank_row0, g.Mcap);
-    if (ns > 2) stage_rows<D>(rows, 2 * kSI, ncols, row_of);
+    stage_rows_for(1);
+    stage_dma_for(1, k1, a1, s1);
+    if (ns > 2) stage_rows_for(2);
   }
   if constexpr (D <= 128) {
     // Tile-granular software pipeline (see tile_interleave).  Iteration t: tile 1
@@ -488,8 +541,8 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
       else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
       stage_barrier();
       if (t + 3 < ns) {
-        stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, kd, ad, sd, bank_row0, g.Mcap);
-        if (t + 4 < ns) stage_rows<D>(rows, (t + 4) * kSI, ncols, row_of);
+        stage_dma_for(t + 3, kd, ad, sd);
+        if (t + 4 < ns) stage_rows_for(t + 4);
       }
       xx = tile_mfma<D>(kn, an, 0, rf, aoff);
       sa += epi_full(u, b1);
@@ -502,8 +555,8 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
       else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
       stage_barrier();
       if (ns > 2) {
-        stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, k2, a2, s2, bank_row0, g.Mcap);
-        if (ns > 3) stage_rows<D>(rows, 3 * kSI, ncols, row_of);
+        stage_dma_for(2, k2, a2, s2);
+        if (ns > 3) stage_rows_for(3);
       }
       u = tile_mfma<D>(k0, a0, 0, rf, aoff);
     }
@@ -777,14 +830,28 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   // so that no register copy waits for a lookup still in flight.
   int32_t rowsA[SCfg<D>::PER + 1], rowsB[SCfg<D>::PER + 1];
   using Rows = int32_t[SCfg<D>::PER + 1];
+  // stage s covers list entries c0 + s kSI ..; where those are consecutive rows
+  // of one region (ordered candidates, bank slots in order) and whole-row
+  // descriptors, the loads take the per-lane offsets of consecutive rows and no
+  // row list is built
+  constexpr bool kSeqRows = !kColSplit && (MODE == RS_CHUNK || MODE == RS_FIXUP || MODE == RS_DENSITY);
+  [[maybe_unused]] const StageOff<D> soff = stage_offsets<D>();
+  auto stage_rows_for = [&](Rows &r, int st) __attribute__((always_inline)) {
+    if constexpr (!kSeqRows) stage_rows<D>(r, st * kSI, ncols, row_of_rel);
+  };
+  auto stage_dma_for = [&](const Rows &r, int st, char *kd, char *ad) __attribute__((always_inline)) {
+    if constexpr (kSeqRows)
+      stage_dma_seq<D, false>(soff, c0 + st * kSI, colbase.k, colaug, nullptr, kd, ad, nullptr, col_row0, col_nrows);
+    else stage_dma<D, false, kColSplit>(r, colbase, colaug, nullptr, kd, ad, nullptr, col_row0, col_nrows);
+  };
   auto step = [&](int t, const char *kb, const char *ab, char *kn, char *an, Rows &use, Rows &fill)
       __attribute__((always_inline)) {
     if (t + 1 < ns) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kOps));
     else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
     stage_barrier();
     if (t + 2 < ns) {
-      if (t + 3 < ns) stage_rows<D>(fill, (t + 3) * kSI, ncols, row_of_rel);
-      stage_dma<D, false, kColSplit>(use, colbase, colaug, nullptr, kn, an, nullptr, col_row0, col_nrows);
+      if (t + 3 < ns) stage_rows_for(fill, t + 3);
+      stage_dma_for(use, t + 2, kn, an);
     }
     if constexpr (kSym) {
       if (t > 0) flush_cols(t - 1);
@@ -819,12 +886,12 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
     for (int i = threadIdx.x; i < 3 * kSI; i += 64 * kWaves) sb.cb[i] = 0;
   }
   if (ns > 0) {
-    stage_rows<D>(rowsA, 0, ncols, row_of_rel);
-    stage_dma<D, false, kColSplit>(rowsA, colbase, colaug, nullptr, sb.k0, sb.a0, nullptr, col_row0, col_nrows);
+    stage_rows_for(rowsA, 0);
+    stage_dma_for(rowsA, 0, sb.k0, sb.a0);
     if (ns > 1) {
-      stage_rows<D>(rowsB, kSI, ncols, row_of_rel);
-      stage_dma<D, false, kColSplit>(rowsB, colbase, colaug, nullptr, sb.k1, sb.a1, nullptr, col_row0, col_nrows);
-      if (ns > 2) stage_rows<D>(rowsA, 2 * kSI, ncols, row_of_rel);
+      stage_rows_for(rowsB, 1);
+      stage_dma_for(rowsB, 1, sb.k1, sb.a1);
+      if (ns > 2) stage_rows_for(rowsA, 2);
     }
   }
   if constexpr (kPipe) {
@@ -859,8 +926,8 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
       else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
       stage_barrier();
       if (t + 3 < ns) {
-        if (t + 4 < ns) stage_rows<D>(fill, (t + 4) * kSI, ncols, row_of_rel);
-        stage_dma<D, false, kColSplit>(use, colbase, colaug, nullptr, kd, ad, nullptr, col_row0, col_nrows);
+        if (t + 4 < ns) stage_rows_for(fill, t + 4);
+        stage_dma_for(use, t + 3, kd, ad);
       }
       x = tile_mfma_(kn, an, 0);
       s2 += lane_wsum<P, false, FOLD>(u, kCT, h);
@@ -873,8 +940,8 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
       else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
       stage_barrier();
       if (ns > 2) {
-        if (ns > 3) stage_rows<D>(rowsB, 3 * kSI, ncols, row_of_rel);
-        stage_dma<D, false, kColSplit>(rowsA, colbase, colaug, nullptr, sb.k2, sb.a2, nullptr, col_row0, col_nrows);
+        if (ns > 3) stage_rows_for(rowsB, 3);
+        stage_dma_for(rowsA, 2, sb.k2, sb.a2);
       }
       u = tile_mfma_(sb.k0, sb.a0, 0);
     }
@@ -1166,7 +1233,7 @@ __device__ __forceinline__ CrossFind cross_find(const CrossRow &r, const Prm &p,
 constexpr int kCrossWaveStates = 32;
 
 template <int D, int P, bool FOLD, bool KV>
-__global__ __launch_bounds__(256, 4) void k_cross_mfma(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
+__global__ __launch_bounds__(256, 3) void k_cross_mfma(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
   static_assert(D <= 128 && kCkStride == 64, "two 32-candidate tiles per chunk");
   constexpr int KSW = D / 16;
   const int b = blockIdx.y;
@@ -1233,11 +1300,10 @@ __global__ __launch_bounds__(256, 4) void k_cross_mfma(dkv_bank bank, Geom g, Pr
     __shared__ __attribute__((aligned(1024))) char kbuf[2][KB];
     __shared__ __attribute__((aligned(16))) char abuf[2][AB];
     const Desc OK{ws.sk, nullptr};
-    int32_t srows[SCfg<D>::PER + 1];
+    const StageOff<D> soff = stage_offsets<D>();
     auto issue = [&](int c, int buf) __attribute__((always_inline)) {
-      const int j0 = c * kCkStride;
-      stage_rows<D>(srows, 0, min(kCkStride, R - j0), [&](int j) -> int64_t { return (int64_t)(nb + j0 + j); });
-      stage_dma<D, false, false>(srows, OK, ws.saug, nullptr, kbuf[buf], abuf[buf], nullptr, (int64_t)nb, g.N);
+      stage_dma_seq<D, false>(soff, c * kCkStride, OK.k, ws.saug, nullptr, kbuf[buf], abuf[buf], nullptr, (int64_t)nb,
+                              g.N);
     };
     // the chunks in increasing order (uniform over the workgroup)
     auto pop_chunk = [&]() __attribute__((always_inline)) -> int {
