@@ -12,8 +12,8 @@ torch = pytest.importorskip("torch")
 
 pytestmark = pytest.mark.gpu
 
-from oracle import (Q23, BankState, attention, candidate_scores, density_from_scratch, update_layer,  # noqa: E402
-                    weight_q23)
+from oracle import (Q23, BankState, attention, candidate_scores, density_from_scratch, pair_d2,  # noqa: E402
+                    update_layer, weight_q23)
 from paper_2608_27922_amd import api, synth  # noqa: E402
 from gpu_util import (TORCH_DT, assert_bank_equal, assert_trace_equal, attention_error, dev, host,  # noqa: E402
                       mirror, oracle_params, oracle_step)
@@ -553,6 +553,63 @@ def test_corrupted_bank_is_compacted():
     assert_trace_equal(out, recs, 1, obanks, 10)
     for b in range(B):
         assert_bank_equal(bank, b, new[b])
+
+
+def _spread_case(d, kv, seed):
+    """Two banks of 600 grid states (five 128-state workgroups and a partial one)
+    and 1,000 candidates (15 whole 64-candidate chunks and one of 40), with every
+    state's baseline set so that its bound lies a uniform fraction U in
+    [-0.15, 1.15] of its total weight to the candidates above rho (tau = 2:
+    2 b - rho = U T): first crossings spread over every chunk, and some states
+    never cross (U > 1) or already violate (U < 0)."""
+    prm = api.Params(sigma2_log2=5, flags=api.POLICY_KV_DESCRIPTOR if kv else 0)
+    op = oracle_params(prm)
+    B, m0, N, M = 2, 600, 1000, 2600
+    rng = np.random.default_rng(seed)
+    bank = api.Bank(B, M, d, dtype=torch.bfloat16, group_size=1)
+    vals = (lambda shape: synth.random_grid_keys(rng, shape)) if kv else \
+        (lambda shape: synth.to_storage(rng.standard_normal(shape), "bf16"))
+    K0, V0 = synth.random_grid_keys(rng, (B, m0, d)), vals((B, m0, d))
+    api.update_bank(bank, dev(K0, "bf16"), dev(V0, "bf16"), 0, prm)
+    torch.cuda.synchronize()
+    K1, V1 = synth.random_grid_keys(rng, (B, N, d)), vals((B, N, d))
+    for b in range(B):
+        ob = mirror(bank, b)
+        db = np.hstack([ob.K, ob.V.astype(np.float64)]) if kv else ob.K
+        dc = np.hstack([K1[b], V1[b]]) if kv else K1[b]
+        T = weight_q23(pair_d2(db, dc.astype(np.float64)), op).sum(axis=1)
+        U = rng.uniform(-0.15, 1.15, ob.m)
+        base = np.maximum(op.delta_q, np.floor((ob.rho + U * T) / 2)).astype(np.int64)
+        bank.base[b, :ob.m] = torch.from_numpy(base).to(bank.base.device)
+    torch.cuda.synchronize()
+    return prm, op, bank, K1, V1
+
+
+@pytest.mark.parametrize("d,kv", [(128, False), (64, False), (64, True), (128, True)])
+def test_crossing_search_spread_bounds(d, kv):
+    """First crossings over every 64-candidate chunk, the partial last chunk, the
+    never-crossing sentinel R + 1 and the already-violating 0 (Eqs. 8-9), with many
+    distinct crossing chunks inside one workgroup of states; then the rest of the
+    update.  [K; V] at d = 64 runs the matrix-core walk at descriptor dimension 128,
+    at d = 128 the VALU walk."""
+    _log(f"crossing search spread bounds d={d} kv={kv}")
+    prm, op, bank, K1, V1 = _spread_case(d, kv, 23 + d + int(kv))
+    B, N = K1.shape[0], K1.shape[1]
+    obanks = [mirror(bank, b) for b in range(B)]
+    out = api.UpdateOut(bank, N, trace=True)
+    api.update_bank(bank, dev(K1, "bf16"), dev(V1, "bf16"), 1, prm, out=out)
+    torch.cuda.synchronize()
+    new, recs = oracle_step(obanks, K1, V1, 1, op, 1)
+    for b, rec in enumerate(recs):  # the case exercises what it is for
+        fc, R = rec.heads[0].first_cross, rec.R
+        cross = (fc > 0) & (fc <= R)
+        ch = np.where(cross, (fc - 1) // 64, -1)
+        most = max(np.unique(ch[i:i + 128][ch[i:i + 128] >= 0]).size for i in range(0, fc.size, 128))
+        assert most >= 12 and (fc == 0).any() and (fc == R + 1).any() and (ch == (R - 1) // 64).any(), \
+            f"bank {b}: {most} distinct chunks per 128 states"
+    assert_trace_equal(out, recs, 1, obanks, N)
+    for b in range(B):
+        assert_bank_equal(bank, b, new[b], kv=kv)
 
 
 # ----------------------------------------------------------------------------- score entry point
