@@ -1219,12 +1219,14 @@ __device__ __forceinline__ CrossFind cross_find(const CrossRow &r, const Prm &p,
   return f;
 }
 
-// Descriptors of up to 128 elements: a wave takes 32 states.  The chunk search
-// runs in four passes of eight states; each state's result then moves to lanes
-// n and n + 32 (n = its index in the wave).  The exact walk: for every distinct
-// crossing chunk among the wave's states one 64 x 32 MFMA Gram, A = the chunk's
-// ordered candidates (two tiles of 32) with their norm steps, B = the 32 states
-// as the Gram stages hold row items, so lane (n, h) gets t of state n with
+// Descriptors of up to 128 elements: a wave takes 32 states, a workgroup 128.
+// The chunk search runs in four passes of eight states; each state's result then
+// moves to lanes n and n + 32 (n = its index in the wave).  The exact walk: the
+// workgroup's crossing chunks, in increasing order, each staged through LDS as a
+// column stage of the Gram kernels (two buffers, alternating), and in every wave
+// that has a state crossing there one 64 x 32 MFMA Gram with the Gram stages' own
+// tiles: A = the chunk's ordered candidates (two tiles of 32) with their norm
+// steps, B = the 32 states as row items, so lane (n, h) gets t of state n with
 // candidates 8 k + 4 h + j (registers 4 k + j) of each tile, bit for bit the t
 // that made the chunk sums; each lane keeps the Gram of its own chunk.  Then,
 // once per lane, the weights summed in candidate order (the two halves exchange
