@@ -159,30 +159,48 @@ __device__ __forceinline__ int k_swz(int r, int c) { return c ^ (r % FCfg<D>::kC
 template <int D>
 __device__ __forceinline__ int v_swz(int r, int c) { return c ^ ((4 * (r % 4)) % FCfg<D>::kChunks); }
 
-// Issue the direct-to-LDS loads of one K or V tile (rows [0, nvalid) of base;
-// rows beyond nvalid repeat the last real row so that every value is finite).
-// Lane i of a load writes 16 bytes at LDS offset 16 i of its 1 KB block, i.e.
-// physical chunk pc of row r; it fetches logical chunk swz(r, pc) (the XOR
-// swizzle is an involution, so logical chunk c lands at physical swz(r, c)).
-// The loads are raw buffer loads to LDS over the tile's valid rows rather
-// than global loads to LDS: with a global load to LDS in flight the compiler
-// counts every later LDS read as possibly out of order and waits for all of
-// them before each use, which serializes the MFMAs on the LDS latency.
-template <int D, bool kIsV>
-__device__ __forceinline__ void ftile_issue(const uint16_t *base, int nvalid, char *buf) {
+// The direct-to-LDS loads of one K or V tile.  Lane i of a load writes 16
+// bytes at LDS offset 16 i of its 1 KB block, i.e. physical chunk pc of row r;
+// it fetches logical chunk swz(r, pc) (the XOR swizzle is an involution, so
+// logical chunk c lands at physical swz(r, c)).  These byte offsets within a
+// tile are the same for every tile, so they are computed once per lane; the
+// tile's first row is the uniform buffer base and the buffer ends after its
+// nvalid rows, so the rows beyond read as zero (finite; their scores are
+// masked and their weights are 0).  The loads are raw buffer loads to LDS
+// rather than global loads to LDS: with a global load to LDS in flight the
+// compiler counts every later LDS read as possibly out of order and waits for
+// all of them before each use, which serializes the MFMAs on the LDS latency.
+template <int D>
+struct FTileOff {
+  static constexpr int kPerWave = FCfg<D>::kLoadsPerTile / kFWaves;  // loads per wave per tensor
+  int k[kPerWave], v[kPerWave];
+};
+
+template <int D>
+__device__ __forceinline__ FTileOff<D> ftile_offsets() {
   constexpr int RPL = FCfg<D>::kRowsPerLoad, CH = FCfg<D>::kChunks;
-  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
   const int rsub = l / CH, pc = l % CH;
+  FTileOff<D> o;
 #pragma unroll
-  for (int q = 0; q < FCfg<D>::kLoadsPerTile / kFWaves; ++q) {
-    const int blk = wave * (FCfg<D>::kLoadsPerTile / kFWaves) + q;
-    const int r = blk * RPL + rsub;
-    const int rr = r < nvalid ? r : nvalid - 1;
-    const int cs = kIsV ? v_swz<D>(r, pc) : k_swz<D>(r, pc);
-    const __amdgpu_buffer_rsrc_t rs =  // base and extent are uniform
-        __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, nvalid * FCfg<D>::kRowBytes, kBufferRsrcWord3);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)(buf + blk * 1024), 16, (rr * D + 8 * cs) * 2, 0, 0, 0);
+  for (int q = 0; q < FTileOff<D>::kPerWave; ++q) {
+    const int r = (wave * FTileOff<D>::kPerWave + q) * RPL + rsub;
+    o.k[q] = (r * D + 8 * k_swz<D>(r, pc)) * 2;
+    o.v[q] = (r * D + 8 * v_swz<D>(r, pc)) * 2;
   }
+  return o;
+}
+
+template <int D>
+__device__ __forceinline__ void ftile_issue(const uint16_t *base, int nvalid, char *buf,
+                                            const int (&voff)[FTileOff<D>::kPerWave]) {
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const __amdgpu_buffer_rsrc_t rs =  // base and extent are uniform
+      __builtin_amdgcn_make_buffer_rsrc((void *)base, (short)0, nvalid * FCfg<D>::kRowBytes, kBufferRsrcWord3);
+#pragma unroll
+  for (int q = 0; q < FTileOff<D>::kPerWave; ++q)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)(buf + (wave * FTileOff<D>::kPerWave + q) * 1024), 16,
+                                             voff[q], 0, 0, 0);
 }
 
 // Lazy softmax bound: the reference maximum is only raised when a lane's tile
@@ -260,20 +278,21 @@ __global__ __launch_bounds__(64 * kFWaves, 1) void k_attn_mfma(dkv_bank bank, co
   auto nvalid_of = [&](int t) {
     return t < nt0 ? min(kFK, m - t * kFK) : (t < nt1 ? min(kFK, nw - (t - nt0) * kFK) : min(kFK, ns - (t - nt1) * kFK));
   };
+  const FTileOff<D> toff = ftile_offsets<D>();
   auto issue = [&](int t, char *kd, char *vd) {
     if (t >= nt) return;
     const int nv = nvalid_of(t);
     if (t < nt0) {
-      ftile_issue<D, false>(bk + (rb + (size_t)t * kFK) * D, nv, kd);
-      ftile_issue<D, true>(bv + (rb + (size_t)t * kFK) * D, nv, vd);
+      ftile_issue<D>(bk + (rb + (size_t)t * kFK) * D, nv, kd, toff.k);
+      ftile_issue<D>(bv + (rb + (size_t)t * kFK) * D, nv, vd, toff.v);
     } else if (t < nt1) {
       const size_t r0 = wb + (size_t)(t - nt0) * kFK;
-      ftile_issue<D, false>(wk + r0 * D, nv, kd);
-      ftile_issue<D, true>(wv + r0 * D, nv, vd);
+      ftile_issue<D>(wk + r0 * D, nv, kd, toff.k);
+      ftile_issue<D>(wv + r0 * D, nv, vd, toff.v);
     } else {
       const size_t r0 = sb + (size_t)(t - nt1) * kFK;
-      ftile_issue<D, false>(sk + r0 * D, nv, kd);
-      ftile_issue<D, true>(sv + r0 * D, nv, vd);
+      ftile_issue<D>(sk + r0 * D, nv, kd, toff.k);
+      ftile_issue<D>(sv + r0 * D, nv, vd, toff.v);
     }
   };
   // transposed V read: lane group gq = l / 16 (h = gq / 2), member cq = l % 16
