@@ -1235,7 +1235,7 @@ __device__ __forceinline__ CrossFind cross_find(const CrossRow &r, const Prm &p,
 constexpr int kCrossWaveStates = 32;
 
 template <int D, int P, bool FOLD, bool KV>
-__global__ __launch_bounds__(256, 3) void k_cross_mfma(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
+__global__ __launch_bounds__(64 * kWaves, 3) void k_cross_mfma(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
   static_assert(D <= 128 && kCkStride == 64, "two 32-candidate tiles per chunk");
   constexpr int KSW = D / 16;
   const int b = blockIdx.y;
@@ -1544,7 +1544,7 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
         k_rowsum_mfma<D, P, RS_CHUNK, F, KV><<<dim3(rowsM, cdiv(g.N, kChunksPerSplit * kCkStride), g.B), T, 0, s>>>(
             bank, seg.k, sv, g, p, ws, nullptr);
       if constexpr (D <= 128)
-        k_cross_mfma<D, P, F, KV><<<dim3(cdiv(g.Mcap, 4 * kCrossWaveStates), g.B), 256, 0, s>>>(bank, g, p, ws,
+        k_cross_mfma<D, P, F, KV><<<dim3(cdiv(g.Mcap, kWaves * kCrossWaveStates), g.B), 64 * kWaves, 0, s>>>(bank, g, p, ws,
                                                                                              out.first_cross);
       else
         k_cross_wide<D, P, KV><<<dim3(cdiv(g.Mcap, 4 * kCrossStates), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
