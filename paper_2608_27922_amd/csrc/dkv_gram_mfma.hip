@@ -1544,8 +1544,8 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
         k_rowsum_mfma<D, P, RS_CHUNK, F, KV><<<dim3(rowsM, cdiv(g.N, kChunksPerSplit * kCkStride), g.B), T, 0, s>>>(
             bank, seg.k, sv, g, p, ws, nullptr);
       if constexpr (D <= 128)
-        k_cross_mfma<D, P, F, KV><<<dim3(cdiv(g.Mcap, kWaves * kCrossWaveStates), g.B), 64 * kWaves, 0, s>>>(bank, g, p, ws,
-                                                                                             out.first_cross);
+        k_cross_mfma<D, P, F, KV><<<dim3(cdiv(g.Mcap, kWaves * kCrossWaveStates), g.B), 64 * kWaves, 0, s>>>(
+            bank, g, p, ws, out.first_cross);
       else
         k_cross_wide<D, P, KV><<<dim3(cdiv(g.Mcap, 4 * kCrossStates), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
       break;
