@@ -11,7 +11,6 @@
 //                  from-scratch bank density (Eq. 3)
 //   k_cross_mfma   per bank state: the chunk in which its prefix density first
 //                  reaches tau b, then the exact prefix length inside it
-//                  (k_cross_wide for descriptors wider than 128)
 //
 // The column range of every Gram is split over workgroups (grid dimension y);
 // partial integer sums are combined with 64-bit atomic adds, which are exact
@@ -1118,11 +1117,6 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, co
 // with the same binary32 weights.  States that never reach the bound within
 // the tested prefixes get R + 1; states whose empty prefix already violates 0.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
-  const uint32_t lo = __shfl((uint32_t)v, src, 64), hi = __shfl((uint32_t)(v >> 32), src, 64);
-  return ((uint64_t)hi << 32) | lo;
-}
-
 constexpr int kCrossLanes = 8;                      // lanes per state in the chunk search
 constexpr int kCrossPerLane = 16;                   // chunk sums per lane
 constexpr int kCrossStates = 64 / kCrossLanes;      // states per chunk-search pass of a wave
@@ -1219,7 +1213,7 @@ __device__ __forceinline__ CrossFind cross_find(const CrossRow &r, const Prm &p,
   return f;
 }
 
-// Descriptors of up to 128 elements: a wave takes 32 states, a workgroup 128.
+// A wave takes 32 states, a workgroup 128.
 // The chunk search runs in four passes of eight states; each state's result then
 // moves to lanes n and n + 32 (n = its index in the wave).  The exact walk: the
 // workgroup's crossing chunks, in increasing order, each staged through LDS as a
@@ -1235,8 +1229,8 @@ __device__ __forceinline__ CrossFind cross_find(const CrossRow &r, const Prm &p,
 constexpr int kCrossWaveStates = 32;
 
 template <int D, int P, bool FOLD, bool KV>
-__global__ __launch_bounds__(64 * kWaves, 3) void k_cross_mfma(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
-  static_assert(D <= 128 && kCkStride == 64, "two 32-candidate tiles per chunk");
+__global__ __launch_bounds__(64 * kWaves, D <= 128 ? 3 : 2) void k_cross_mfma(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
+  static_assert(kCkStride == 64, "two 32-candidate tiles per chunk");
   constexpr int KSW = D / 16;
   const int b = blockIdx.y;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
@@ -1400,73 +1394,6 @@ done:
   }
 }
 
-// Wider descriptors ([K; V] at d = 128): a wave takes eight states, one chunk
-// search pass, and re-walks each crossing chunk one state at a time with one
-// ordered candidate per lane.
-template <int D, int P, bool KV>
-__global__ __launch_bounds__(256) void k_cross_wide(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
-  static_assert(kCkStride == 64, "one candidate per lane in the exact walk");
-  const int b = blockIdx.y;
-  const int l = threadIdx.x & 63, grp = l / kCrossLanes, q = l % kCrossLanes;
-  const int i0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * kCrossStates;
-  const int m = ws.m[b], R = ws.R[b];
-  if (i0 >= m) return;  // whole wave
-  const int i = i0 + grp;
-  const bool valid = i < m;
-  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
-  const int nch = (R + kCkStride - 1) / kCkStride;
-  const CrossFind f = cross_find(cross_load(bank, ws, rb + (valid ? i : i0), q), p, nch, q);
-  const unsigned long long hits = __ballot(valid && f.hit);
-  int first = f.pos ? R + 1 : 0;
-  unsigned long long todo = 0;
-#pragma unroll
-  for (int s2 = 0; s2 < kCrossStates; ++s2)
-    if ((hits >> (kCrossLanes * s2)) & 0xFFull) todo |= 1ull << s2;
-  const Desc bd{static_cast<const uint16_t *>(bank.k), static_cast<const uint16_t *>(bank.v)};
-  while (todo) {
-    const int s2 = __ffsll(todo) - 1;
-    todo &= todo - 1;
-    const unsigned gbits = (unsigned)(hits >> (kCrossLanes * s2)) & 0xFFu;
-    const int src = kCrossLanes * s2 + __ffs(gbits) - 1;
-    const int c_s = __shfl(f.ch, src, 64);
-    const uint32_t need = __shfl(f.need, src, 64);
-    const size_t srow = rb + i0 + s2;
-    const float nr = bank.knorm[srow];
-    const int col = c_s * kCkStride + l;
-    uint32_t W = 0;
-    if (col < R) {
-      const uint16_t *ckey = ws.sk + (nb + col) * D;
-      float acc = 0.0f;
-#pragma unroll
-      for (int j = 0; j < D; j += 8) {
-        const u32x4 ra = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(bd, (int64_t)srow, j / 8));
-        const u32x4 rc = *reinterpret_cast<const u32x4 *>(ckey + j);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc = __builtin_fmaf(__uint_as_float(ra[e] << 16), __uint_as_float(rc[e] << 16), acc);
-          acc = __builtin_fmaf(__uint_as_float(ra[e] & 0xFFFF0000u), __uint_as_float(rc[e] & 0xFFFF0000u), acc);
-        }
-      }
-      const float d2 = (nr + ws.snorm[nb + col]) - 2.0f * acc;
-      W = weight_raw<P, false>(d2 * p.inv_sigma2, 8388608.0f) - kMagic;
-    }
-    uint32_t wi = W;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const uint32_t y = __shfl_up(wi, o, 64);
-      if (l >= o) wi += y;
-    }
-    const unsigned long long h2 = __ballot(wi >= need);
-    const int fc = h2 != 0 ? c_s * kCkStride + (__ffsll(h2) - 1) + 1
-                           : min(R, (c_s + 1) * kCkStride);  // unreachable when both passes agree (exact Gram)
-    if (grp == s2) first = fc;
-  }
-  if (valid && q == 0) {
-    ws.first[rb + i] = first;
-    if (out_first) out_first[rb + i] = first;
-  }
-}
-
 // Candidate keys and norms in score order, so that the ordered passes stream
 // contiguous rows: one thread per 16-byte chunk of kGatherRows key rows
 // (every load and store instruction covers whole rows).
@@ -1543,11 +1470,8 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       if (g.N > 0)
         k_rowsum_mfma<D, P, RS_CHUNK, F, KV><<<dim3(rowsM, cdiv(g.N, kChunksPerSplit * kCkStride), g.B), T, 0, s>>>(
             bank, seg.k, sv, g, p, ws, nullptr);
-      if constexpr (D <= 128)
-        k_cross_mfma<D, P, F, KV><<<dim3(cdiv(g.Mcap, kWaves * kCrossWaveStates), g.B), 64 * kWaves, 0, s>>>(
-            bank, g, p, ws, out.first_cross);
-      else
-        k_cross_wide<D, P, KV><<<dim3(cdiv(g.Mcap, 4 * kCrossStates), g.B), 256, 0, s>>>(bank, g, p, ws, out.first_cross);
+      k_cross_mfma<D, P, F, KV><<<dim3(cdiv(g.Mcap, kWaves * kCrossWaveStates), g.B), 64 * kWaves, 0, s>>>(
+          bank, g, p, ws, out.first_cross);
       break;
     }
     case 2:
