@@ -590,8 +590,7 @@ def test_crossing_search_spread_bounds(d, kv):
     """First crossings over every 64-candidate chunk, the partial last chunk, the
     never-crossing sentinel R + 1 and the already-violating 0 (Eqs. 8-9), with many
     distinct crossing chunks inside one workgroup of states; then the rest of the
-    update.  [K; V] at d = 64 runs the matrix-core walk at descriptor dimension 128,
-    at d = 128 the VALU walk."""
+    update, also in the [K; V] geometry (descriptor dimensions 128 and 256)."""
     _log(f"crossing search spread bounds d={d} kv={kv}")
     prm, op, bank, K1, V1 = _spread_case(d, kv, 23 + d + int(kv))
     B, N = K1.shape[0], K1.shape[1]
