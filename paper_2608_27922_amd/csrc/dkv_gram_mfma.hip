@@ -44,8 +44,12 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kWaves = 4;
-constexpr int kRowsPerWG = 32 * kWaves;
+constexpr int kWaves = 4;  // waves per workgroup of the crossing search, and of the Gram stages at D <= 128
+// Waves per workgroup of the Gram stages: 8 at descriptor dimension 256, whose
+// three column stages (about 100 KB of LDS) allow one workgroup per CU, so that
+// each SIMD still holds two waves.
+template <int D>
+constexpr int gram_waves() { return D > 128 ? 8 : kWaves; }
 constexpr int kCT = 32;  // column items per MFMA tile
 constexpr int kSI = 64;  // column items per LDS stage (two tiles, two independent MFMA chains)
 
@@ -146,34 +150,39 @@ __device__ __forceinline__ void load_row_frag(RowFrag<D> &rf, const Desc &src, i
 // each) are free of bank conflicts.  Each item's extra K step (column_aug,
 // precomputed per update) and, for the score, its score scale follow.
 // ---------------------------------------------------------------------------
-template <int D>
+template <int D, int W = kWaves>
 struct SCfg {
   static constexpr int CH = D / 8;             // 16-byte chunks per key row
   static constexpr int RB = 2 * D;             // key row bytes
   static constexpr int RPL = 1024 / RB;        // rows per 1 KB load
   static constexpr int NB = kSI * RB / 1024;   // 1 KB loads per stage
-  static constexpr int PER = NB / kWaves;      // key loads per thread per stage
+  static constexpr int PER = NB / W;           // key loads per thread per stage
   static constexpr int KEYB = kSI * RB;        // key bytes per stage
   static constexpr int AUGB = kSI * 16;        // aug bytes per stage
-  static_assert(NB % kWaves == 0, "key loads split evenly over the waves");
+  static constexpr int ITEMS = kSI / W;       // aug / scale items per wave (its lanes 0 .. ITEMS - 1)
+  static_assert(NB % W == 0 && kSI % W == 0, "loads split evenly over the waves");
 };
 // direct-to-LDS loads per thread per stage: keys, aug (+ score scale)
-template <int D, bool kBs>
-constexpr int stage_ops() { return SCfg<D>::PER + 1 + (kBs ? 1 : 0); }
+template <int D, bool kBs, int W = kWaves>
+constexpr int stage_ops() { return SCfg<D, W>::PER + 1 + (kBs ? 1 : 0); }
 
 typedef __attribute__((address_space(3))) void lds_void;
 
 // Global rows fetched by this thread for the stage starting at column j0 (its
 // key loads, then its aug / scale item); items past ncols repeat the last one.
-template <int D, class RowOf>
-__device__ __forceinline__ void stage_rows(int32_t (&rows)[SCfg<D>::PER + 1], int j0, int ncols, RowOf row_of) {
+template <int D, int W>
+using StageRows = int32_t[SCfg<D, W>::PER + 1];
+
+template <int D, int W, class RowOf>
+__device__ __forceinline__ void stage_rows(StageRows<D, W> &rows, int j0, int ncols, RowOf row_of) {
+  using C = SCfg<D, W>;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
 #pragma unroll
-  for (int q = 0; q < SCfg<D>::PER; ++q) {
-    const int r = (wave * SCfg<D>::PER + q) * SCfg<D>::RPL + l / SCfg<D>::CH;
+  for (int q = 0; q < C::PER; ++q) {
+    const int r = (wave * C::PER + q) * C::RPL + l / C::CH;
     rows[q] = (int32_t)row_of(min(j0 + r, ncols - 1));
   }
-  rows[SCfg<D>::PER] = (int32_t)row_of(min(j0 + 16 * wave + (l & 15), ncols - 1));
+  rows[C::PER] = (int32_t)row_of(min(j0 + C::ITEMS * wave + l % C::ITEMS, ncols - 1));
 }
 
 // Word 3 of a raw buffer resource: 32-bit data format, no swizzle, no
@@ -200,36 +209,37 @@ __device__ __forceinline__ void buffer_to_lds4(const void *base, int nbytes, int
 // the compiler counts every later LDS read as possibly out of order and waits
 // for all of them before each use.  [K; V] descriptors, whose two halves come
 // from two arrays chosen per lane, keep the global loads to LDS.
-template <int D, bool kBs, bool SPLIT>
-__device__ __forceinline__ void stage_dma(const int32_t (&rows)[SCfg<D>::PER + 1], const Desc &keys,
+template <int D, bool kBs, bool SPLIT, int W = kWaves>
+__device__ __forceinline__ void stage_dma(const StageRows<D, W> &rows, const Desc &keys,
                                           const uint4 *augs, const float *bs, char *kb, char *ab, float *sb,
                                           int64_t row0, int nrows) {
+  using C = SCfg<D, W>;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
   if constexpr (!SPLIT) {
     const void *kbase = keys.k + row0 * D;
-    const int kbytes = nrows * SCfg<D>::RB;
+    const int kbytes = nrows * C::RB;
 #pragma unroll
-    for (int q = 0; q < SCfg<D>::PER; ++q) {
-      const int blk = wave * SCfg<D>::PER + q;
-      const int r = blk * SCfg<D>::RPL + l / SCfg<D>::CH;
-      const int c = (l % SCfg<D>::CH) ^ (r % SCfg<D>::CH);
-      buffer_to_lds16(kbase, kbytes, (int)(rows[q] - row0) * SCfg<D>::RB + 16 * c, kb + blk * 1024);
+    for (int q = 0; q < C::PER; ++q) {
+      const int blk = wave * C::PER + q;
+      const int r = blk * C::RPL + l / C::CH;
+      const int c = (l % C::CH) ^ (r % C::CH);
+      buffer_to_lds16(kbase, kbytes, (int)(rows[q] - row0) * C::RB + 16 * c, kb + blk * 1024);
     }
   } else {
 #pragma unroll
-    for (int q = 0; q < SCfg<D>::PER; ++q) {
-      const int blk = wave * SCfg<D>::PER + q;
-      const int r = blk * SCfg<D>::RPL + l / SCfg<D>::CH;
-      const int c = (l % SCfg<D>::CH) ^ (r % SCfg<D>::CH);
+    for (int q = 0; q < C::PER; ++q) {
+      const int blk = wave * C::PER + q;
+      const int r = blk * C::RPL + l / C::CH;
+      const int c = (l % C::CH) ^ (r % C::CH);
       __builtin_amdgcn_global_load_lds((void *)desc_chunk<D, SPLIT>(keys, (int64_t)rows[q], c),
                                        (lds_void *)(kb + blk * 1024), 16, 0, 0);
     }
   }
-  // items 16 w .. 16 w + 15: lanes 0-15 of wave w (LDS address = base + lane * size)
-  if (l < 16) {
-    const int rel = (int)(rows[SCfg<D>::PER] - row0);
-    buffer_to_lds16(augs + row0, nrows * 16, rel * 16, ab + 256 * wave);
-    if constexpr (kBs) buffer_to_lds4(bs + row0, nrows * 4, rel * 4, reinterpret_cast<char *>(sb + 16 * wave));
+  // items ITEMS w .. ITEMS (w + 1) - 1: lanes 0 .. ITEMS - 1 of wave w (LDS address = base + lane * size)
+  if (l < C::ITEMS) {
+    const int rel = (int)(rows[C::PER] - row0);
+    buffer_to_lds16(augs + row0, nrows * 16, rel * 16, ab + 16 * C::ITEMS * wave);
+    if constexpr (kBs) buffer_to_lds4(bs + row0, nrows * 4, rel * 4, reinterpret_cast<char *>(sb + C::ITEMS * wave));
   }
 }
 
@@ -237,22 +247,23 @@ __device__ __forceinline__ void stage_dma(const int32_t (&rows)[SCfg<D>::PER + 1
 // + i: bank slots in order, or the ordered candidates): each lane's byte
 // offsets are the same for every stage, and the stage's first row goes into the
 // uniform buffer base, so no per-stage row arithmetic runs on the VALU.
-template <int D>
+template <int D, int W = kWaves>
 struct StageOff {
-  int key[SCfg<D>::PER];  // key loads: row r of the stage, swizzled chunk c, as r RB + 16 c
-  int item;               // aug / scale item of lanes 0-15 of each wave: 16 w + lane
+  int key[SCfg<D, W>::PER];  // key loads: row r of the stage, swizzled chunk c, as r RB + 16 c
+  int item;                  // aug / scale item of lanes 0 .. ITEMS - 1 of each wave: ITEMS w + lane
 };
 
-template <int D>
-__device__ __forceinline__ StageOff<D> stage_offsets() {
+template <int D, int W = kWaves>
+__device__ __forceinline__ StageOff<D, W> stage_offsets() {
+  using C = SCfg<D, W>;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
-  StageOff<D> o;
+  StageOff<D, W> o;
 #pragma unroll
-  for (int q = 0; q < SCfg<D>::PER; ++q) {
-    const int r = (wave * SCfg<D>::PER + q) * SCfg<D>::RPL + l / SCfg<D>::CH;
-    o.key[q] = r * SCfg<D>::RB + 16 * ((l % SCfg<D>::CH) ^ (r % SCfg<D>::CH));
+  for (int q = 0; q < C::PER; ++q) {
+    const int r = (wave * C::PER + q) * C::RPL + l / C::CH;
+    o.key[q] = r * C::RB + 16 * ((l % C::CH) ^ (r % C::CH));
   }
-  o.item = 16 * wave + (l & 15);
+  o.item = C::ITEMS * wave + l % C::ITEMS;
   return o;
 }
 
@@ -260,19 +271,20 @@ __device__ __forceinline__ StageOff<D> stage_offsets() {
 // The buffers end where the region [row0, row0 + nrows) ends, so rows past it
 // read as zero; rows past the Gram's last column are real rows of the region,
 // masked by the epilogue like the repeated last row they replace.
-template <int D, bool kBs>
-__device__ __forceinline__ void stage_dma_seq(const StageOff<D> &o, int first, const uint16_t *keys, const uint4 *augs,
-                                              const float *bs, char *kb, char *ab, float *sb, int64_t row0,
-                                              int nrows) {
+template <int D, bool kBs, int W = kWaves>
+__device__ __forceinline__ void stage_dma_seq(const StageOff<D, W> &o, int first, const uint16_t *keys,
+                                              const uint4 *augs, const float *bs, char *kb, char *ab, float *sb,
+                                              int64_t row0, int nrows) {
+  using C = SCfg<D, W>;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), l = threadIdx.x & 63;
   const int64_t r0 = row0 + first;
   const int left = nrows - first;  // rows from the stage's first to the region's end
 #pragma unroll
-  for (int q = 0; q < SCfg<D>::PER; ++q)
-    buffer_to_lds16(keys + r0 * D, left * SCfg<D>::RB, o.key[q], kb + (wave * SCfg<D>::PER + q) * 1024);
-  if (l < 16) {
-    buffer_to_lds16(augs + r0, left * 16, o.item * 16, ab + 256 * wave);
-    if constexpr (kBs) buffer_to_lds4(bs + r0, left * 4, o.item * 4, reinterpret_cast<char *>(sb + 16 * wave));
+  for (int q = 0; q < C::PER; ++q)
+    buffer_to_lds16(keys + r0 * D, left * C::RB, o.key[q], kb + (wave * C::PER + q) * 1024);
+  if (l < C::ITEMS) {
+    buffer_to_lds16(augs + r0, left * 16, o.item * 16, ab + 16 * C::ITEMS * wave);
+    if constexpr (kBs) buffer_to_lds4(bs + r0, left * 4, o.item * 4, reinterpret_cast<char *>(sb + C::ITEMS * wave));
   }
 }
 
@@ -394,11 +406,12 @@ __device__ __forceinline__ uint32_t lane_wsum(const f32x16 &u, int nvalid, int h
 constexpr int kColsPerSplit = 1024;
 
 template <int D, int P, bool FOLD, bool KV>
-__global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
+__global__ __launch_bounds__(64 * gram_waves<D>(), gram_waves<D>() == 4 ? 3 : 2) void k_score_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
                                                            Geom g, Prm p, Workspace ws) {
+  constexpr int W = gram_waves<D>();
   const int b = blockIdx.z;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
-  const int x = blockIdx.x * kRowsPerWG + wave * 32 + n;
+  const int x = blockIdx.x * 32 * W + wave * 32 + n;
   const int m = ws.m[b];
   const int c0 = blockIdx.y * kColsPerSplit;
   if (c0 >= m) return;
@@ -447,17 +460,17 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_score_mfma(dkv_bank bank, co
   };
   using Full = std::integral_constant<bool, false>;
   using Part = std::integral_constant<bool, true>;
-  constexpr int kOps = stage_ops<D, true>();
-  int32_t rows[SCfg<D>::PER + 1];
+  constexpr int kOps = stage_ops<D, true, W>();
+  StageRows<D, W> rows;
   // stage s: rows s kSI .. of this split; whole-row descriptors take the
   // per-lane offsets of consecutive rows, [K; V] ones (two arrays) the row list
-  [[maybe_unused]] const StageOff<D> soff = stage_offsets<D>();
+  [[maybe_unused]] const StageOff<D, W> soff = stage_offsets<D, W>();
   auto stage_rows_for = [&](int st) __attribute__((always_inline)) {
-    if constexpr (KV) stage_rows<D>(rows, st * kSI, ncols, row_of);
+    if constexpr (KV) stage_rows<D, W>(rows, st * kSI, ncols, row_of);
   };
   auto stage_dma_for = [&](int st, char *kd, char *ad, float *sd) __attribute__((always_inline)) {
-    if constexpr (KV) stage_dma<D, true, KV>(rows, BK, ws.baug, ws.bs, kd, ad, sd, bank_row0, g.Mcap);
-    else stage_dma_seq<D, true>(soff, c0 + st * kSI, BK.k, ws.baug, ws.bs, kd, ad, sd, bank_row0, g.Mcap);
+    if constexpr (KV) stage_dma<D, true, KV, W>(rows, BK, ws.baug, ws.bs, kd, ad, sd, bank_row0, g.Mcap);
+    else stage_dma_seq<D, true, W>(soff, c0 + st * kSI, BK.k, ws.baug, ws.bs, kd, ad, sd, bank_row0, g.Mcap);
   };
   // stage t in buffers (t % 3); rows of stage t + 2 loaded one step ahead
   auto step = [&](int t, const char *kb, const char *ab, const float *sb, char *kn, char *an, float *sn)
@@ -642,6 +655,8 @@ template <int D, int P, int MODE, bool FOLD, bool KV>
 __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *seg_k, const void *seg_v, const Geom &g,
                                             const Prm &p, const Workspace &ws, int64_t *out, int bx, int by, int bz,
                                             const StageBufs<D> &sb) {
+  constexpr int W = gram_waves<D>();
+  constexpr int kRowsPerWG = 32 * W;
   const int b = bz;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
@@ -813,35 +828,35 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   // to the global sums; the buffer is cleared for stage t + 3
   auto flush_cols = [&](int t) __attribute__((always_inline)) {
     const int j0 = c0 + t * kSI;
-    if (j0 < wg_row0 + kRowsPerWG || l >= kSI / kWaves) return;
+    if (j0 < wg_row0 + kRowsPerWG || l >= kSI / W) return;
     uint32_t *cb = sb.cb + (t % 3) * kSI;
-    const int idx = wave * (kSI / kWaves) + l;
+    const int idx = wave * (kSI / W) + l;
     const uint32_t val = cb[idx];
     cb[idx] = 0;
     if (j0 + idx < c1 && val != 0)
       atomicAdd(reinterpret_cast<unsigned long long *>(&ws.mut_adm[nb + j0 + idx]), (unsigned long long)val);
   };
-  constexpr int kOps = stage_ops<D, false>();
+  constexpr int kOps = stage_ops<D, false, W>();
   // Stage t in buffers t % 3.  The global rows of stage t + 2 were fetched one
   // step earlier (list lookups for the maintenance stages), so issuing its
   // loads never waits for the loads still in flight.
   // Two row sets used alternately (the loop is unrolled 6 = lcm(3, 2) times),
   // so that no register copy waits for a lookup still in flight.
-  int32_t rowsA[SCfg<D>::PER + 1], rowsB[SCfg<D>::PER + 1];
-  using Rows = int32_t[SCfg<D>::PER + 1];
+  StageRows<D, W> rowsA, rowsB;
+  using Rows = StageRows<D, W>;
   // stage s covers list entries c0 + s kSI ..; where those are consecutive rows
   // of one region (ordered candidates, bank slots in order) and whole-row
   // descriptors, the loads take the per-lane offsets of consecutive rows and no
   // row list is built
   constexpr bool kSeqRows = !kColSplit && (MODE == RS_CHUNK || MODE == RS_FIXUP || MODE == RS_DENSITY);
-  [[maybe_unused]] const StageOff<D> soff = stage_offsets<D>();
+  [[maybe_unused]] const StageOff<D, W> soff = stage_offsets<D, W>();
   auto stage_rows_for = [&](Rows &r, int st) __attribute__((always_inline)) {
-    if constexpr (!kSeqRows) stage_rows<D>(r, st * kSI, ncols, row_of_rel);
+    if constexpr (!kSeqRows) stage_rows<D, W>(r, st * kSI, ncols, row_of_rel);
   };
   auto stage_dma_for = [&](const Rows &r, int st, char *kd, char *ad) __attribute__((always_inline)) {
     if constexpr (kSeqRows)
-      stage_dma_seq<D, false>(soff, c0 + st * kSI, colbase.k, colaug, nullptr, kd, ad, nullptr, col_row0, col_nrows);
-    else stage_dma<D, false, kColSplit>(r, colbase, colaug, nullptr, kd, ad, nullptr, col_row0, col_nrows);
+      stage_dma_seq<D, false, W>(soff, c0 + st * kSI, colbase.k, colaug, nullptr, kd, ad, nullptr, col_row0, col_nrows);
+    else stage_dma<D, false, kColSplit, W>(r, colbase, colaug, nullptr, kd, ad, nullptr, col_row0, col_nrows);
   };
   auto step = [&](int t, const char *kb, const char *ab, char *kn, char *an, Rows &use, Rows &fill)
       __attribute__((always_inline)) {
@@ -882,7 +897,7 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   };
   if constexpr (kSym) {
     // cleared before the first stage barrier
-    for (int i = threadIdx.x; i < 3 * kSI; i += 64 * kWaves) sb.cb[i] = 0;
+    for (int i = threadIdx.x; i < 3 * kSI; i += 64 * W) sb.cb[i] = 0;
   }
   if (ns > 0) {
     stage_rows_for(rowsA, 0);
@@ -1004,8 +1019,8 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
 }
 
 template <int D, int P, int MODE, bool FOLD, bool KV>
-__global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
-                                                            Geom g, Prm p, Workspace ws, int64_t *out) {
+__global__ __launch_bounds__(64 * gram_waves<D>(), gram_waves<D>() == 4 ? 3 : 2) void k_rowsum_mfma(
+    dkv_bank bank, const void *seg_k, const void *seg_v, Geom g, Prm p, Workspace ws, int64_t *out) {
   constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
   __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
   __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
@@ -1021,11 +1036,12 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_rowsum_mfma(dkv_bank bank, c
 struct MaintItems {
   int rows_s, rows_a, n_se, n_ab, n_am;
 };
-__device__ __forceinline__ MaintItems maint_items(const Geom &g, const Workspace &ws, int b) {
+// rpw: rows per workgroup of the maintenance Grams
+__device__ __forceinline__ MaintItems maint_items(const Geom &g, const Workspace &ws, int b, int rpw) {
   const int ne = ws.n_ev[b], rs = ws.r_star[b / g.gs], ns = ws.m[b] - ne;
   MaintItems it;
-  it.rows_s = (ns + kRowsPerWG - 1) / kRowsPerWG;
-  it.rows_a = (rs + kRowsPerWG - 1) / kRowsPerWG;
+  it.rows_s = (ns + rpw - 1) / rpw;
+  it.rows_a = (rs + rpw - 1) / rpw;
   it.n_se = it.rows_s * ((ne + kColsPerSplit - 1) / kColsPerSplit);
   it.n_ab = it.rows_a * ((ns + kColsPerSplit - 1) / kColsPerSplit);
   it.n_am = it.rows_a * ((rs + kColsPerSplit / 2 - 1) / (kColsPerSplit / 2));
@@ -1035,14 +1051,14 @@ __device__ __forceinline__ MaintItems maint_items(const Geom &g, const Workspace
 // Exclusive prefix of the banks' work item counts (one workgroup).
 constexpr int kPlanThreads = 1024;
 constexpr unsigned kMaintWgs = 4096;  // maintenance workgroups (3 per CU on 256 CUs, over 5 rounds)
-__global__ __launch_bounds__(kPlanThreads) void k_maint_plan(Geom g, Workspace ws) {
+__global__ __launch_bounds__(kPlanThreads) void k_maint_plan(Geom g, Workspace ws, int rpw) {
   __shared__ int32_t part[kPlanThreads];
   int carry = 0;
   for (int b0 = 0; b0 < g.B; b0 += kPlanThreads) {
     const int b = b0 + (int)threadIdx.x;
     int cnt = 0;
     if (b < g.B) {
-      const MaintItems it = maint_items(g, ws, b);
+      const MaintItems it = maint_items(g, ws, b, rpw);
       cnt = it.n_se + it.n_ab + it.n_am;
     }
     part[threadIdx.x] = cnt;
@@ -1064,8 +1080,9 @@ __global__ __launch_bounds__(kPlanThreads) void k_maint_plan(Geom g, Workspace w
 // k takes the items [k per, (k + 1) per) in bank order, per = total / grid
 // rounded up, so a frozen block (no item) costs one read per workgroup.
 template <int D, int P, bool FOLD, bool KV>
-__global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
-                                                           Geom g, Prm p, Workspace ws) {
+__global__ __launch_bounds__(64 * gram_waves<D>(), gram_waves<D>() == 4 ? 3 : 2) void k_maint_mfma(
+    dkv_bank bank, const void *seg_k, const void *seg_v, Geom g, Prm p, Workspace ws) {
+  constexpr int kRpw = 32 * gram_waves<D>();
   constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
   __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
   __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
@@ -1084,11 +1101,11 @@ __global__ __launch_bounds__(64 * kWaves, 3) void k_maint_mfma(dkv_bank bank, co
     else hi = mid;
   }
   int b = lo, i = w0 - ws.maint_off[b];
-  MaintItems it = maint_items(g, ws, b);
+  MaintItems it = maint_items(g, ws, b, kRpw);
   for (int w = w0; w < w1; ++w, ++i) {
     while (i >= it.n_se + it.n_ab + it.n_am && b + 1 < g.B) {  // next bank with items
       i -= it.n_se + it.n_ab + it.n_am;
-      it = maint_items(g, ws, ++b);
+      it = maint_items(g, ws, ++b, kRpw);
     }
     __syncthreads();  // the previous item's LDS stages are done with
     if (i < it.n_se) {
@@ -1456,8 +1473,9 @@ inline unsigned cdiv(int a, int b) { return (unsigned)((a + b - 1) / b); }
 template <int D, int P, bool F, bool KV>
 void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                       const dkv_update_out &out, const Workspace &ws, hipStream_t s, int stage) {
-  const int T = 64 * kWaves;
-  const unsigned rowsM = cdiv(g.Mcap, kRowsPerWG), rowsN = cdiv(g.N > 0 ? g.N : 1, kRowsPerWG);
+  constexpr int W = gram_waves<D>();
+  const int T = 64 * W;
+  const unsigned rowsM = cdiv(g.Mcap, 32 * W), rowsN = cdiv(g.N > 0 ? g.N : 1, 32 * W);
   const void *sv = seg.v;
   switch (stage) {
     case 0:  // score; the ordered copy is launched after the sort (stage 4)
@@ -1481,7 +1499,7 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       // the work items, then a grid of at most kMaintWgs workgroups over them
       // (evicted states <= admitted <= N: at most rowsM x splits of N, plus
       // rowsN x (splits of Mcap + half splits of N) items per bank)
-      k_maint_plan<<<1, kPlanThreads, 0, s>>>(g, ws);
+      k_maint_plan<<<1, kPlanThreads, 0, s>>>(g, ws, 32 * W);
       const unsigned y_ev = cdiv(g.N > 0 ? g.N : 1, kColsPerSplit), y_surv = cdiv(g.Mcap, kColsPerSplit);
       const unsigned long long bound =
           (unsigned long long)(rowsM * y_ev + (g.N > 0 ? rowsN : 0u) * (y_surv + 2 * y_ev)) * (unsigned)g.B;
@@ -1509,14 +1527,15 @@ void mfma_stage_d(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, c
 template <int D, int P, bool F, bool KV>
 void mfma_score_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g, const Prm &p,
                      int64_t *score_q, float *score_f, int64_t *density, const Workspace &ws, hipStream_t s) {
-  const int T = 64 * kWaves;
+  constexpr int W = gram_waves<D>();
+  const int T = 64 * W;
   if (g.N > 0 && (score_q || score_f)) {
-    k_score_mfma<D, P, F, KV><<<dim3(cdiv(g.N, kRowsPerWG), cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(
+    k_score_mfma<D, P, F, KV><<<dim3(cdiv(g.N, 32 * W), cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(
         bank, seg.k, seg.v, g, p, ws);
     k_score_out<<<dim3(cdiv(g.N, 256), g.B), 256, 0, s>>>(g, ws, score_q, score_f);
   }
   if (density) {
-    k_rowsum_mfma<D, P, RS_DENSITY, F, KV><<<dim3(cdiv(g.Mcap, kRowsPerWG), cdiv(g.Mcap, kColsPerSplit), g.B), T, 0,
+    k_rowsum_mfma<D, P, RS_DENSITY, F, KV><<<dim3(cdiv(g.Mcap, 32 * W), cdiv(g.Mcap, kColsPerSplit), g.B), T, 0,
                                               s>>>(bank, seg.k, seg.v, g, p, ws, density);
     k_density_out<<<dim3(cdiv(g.Mcap, 256), g.B), 256, 0, s>>>(g, ws, density);
   }
