@@ -273,7 +273,9 @@ def run_rollout(args, api, synth, torch):
         m[t + 1] = m[t] + rs[t] - ne[t]
     R = np.minimum(N, np.minimum.reduceat(Mb, np.arange(0, B, gs))).repeat(gs)
     pairs = np.stack([gram_pairs(m[t], N, R, rs[t], ne[t]) for t in range(T)])     # [T, B]
-    gram_flops = 2.0 * d * pairs.sum(1)
+    # each pair's Gram entry is a dot product of descriptors: the key, or [k; v] in the [K; V] geometry
+    dd = 2 * d if prm.flags & api.POLICY_KV_DESCRIPTOR else d
+    gram_flops = 2.0 * dd * pairs.sum(1)
     att_flops = 4.0 * nq * d * (m[1:] + W).sum(1)                                     # [T]
     att_tf = att_flops / (att * 1e-3) / 1e12
     gram_tf = gram_flops / (upd * 1e-3) / 1e12
@@ -464,7 +466,8 @@ def run_single(args, api, synth, torch):
     e = ne_hist[0].cpu().numpy().astype(np.int64)
     R = np.minimum(N, bank.budget.cpu().numpy().astype(np.int64))
     pairs = gram_pairs(m0, N, R, r, e)
-    gram_tf = 2.0 * d * float(pairs.sum()) / (upd_ms * 1e-3) / 1e12
+    dd = 2 * d if run_prm.flags & api.POLICY_KV_DESCRIPTOR else d   # descriptor width of the Gram
+    gram_tf = 2.0 * dd * float(pairs.sum()) / (upd_ms * 1e-3) / 1e12
 
     result = {
         "metric": METRIC,
@@ -489,7 +492,7 @@ def run_single(args, api, synth, torch):
                      "traffic": measured_traffic(cfg.name)},
     }
     if args.policy != "sequential":
-        result["update_gram"] = {"pairs": int(pairs.sum()), "tflop": round(2.0 * d * float(pairs.sum()) / 1e12, 4),
+        result["update_gram"] = {"pairs": int(pairs.sum()), "tflop": round(2.0 * dd * float(pairs.sum()) / 1e12, 4),
                                  "tflops": round(gram_tf, 2), "frac_of_bf16_peak": round(gram_tf / PEAK_BF16_TFLOPS, 4),
                                  "r_star": int(r.max()), "evicted_per_bank": int(e.max())}
     else:
