@@ -55,6 +55,8 @@ size_t workspace_layout(int B, int G, int Mcap, int N, int d, Workspace *ws, cha
   w.caug = (uint4 *)take(Bz * Nz * 16);
   w.saug = (uint4 *)take(Bz * Nz * 16);
   w.maint_off = (int32_t *)take((Bz + 1) * 4);
+  w.crossed = (int32_t *)take(Bz * 4);
+  w.more = (int32_t *)take((size_t)G * 4);
   const int nfw = ((N > 0 ? N : 0) + 1 + 31) / 32;
   w.feas = (uint32_t *)take(Bz * (size_t)nfw * 4);
   w.nfw = nfw;

@@ -1246,7 +1246,8 @@ __device__ __forceinline__ CrossFind cross_find(const CrossRow &r, const Prm &p,
 constexpr int kCrossWaveStates = 32;
 
 template <int D, int P, bool FOLD, bool KV>
-__global__ __launch_bounds__(64 * kWaves, D <= 128 ? 3 : 2) void k_cross_mfma(dkv_bank bank, Geom g, Prm p, Workspace ws, int32_t *out_first) {
+__global__ __launch_bounds__(64 * kWaves, D <= 128 ? 3 : 2) void k_cross_mfma(dkv_bank bank, Geom g, Prm p, Workspace ws,
+                                                                            int32_t *out_first, int lim, int second) {
   static_assert(kCkStride == 64, "two 32-candidate tiles per chunk");
   constexpr int KSW = D / 16;
   const int b = blockIdx.y;
@@ -1254,9 +1255,10 @@ __global__ __launch_bounds__(64 * kWaves, D <= 128 ? 3 : 2) void k_cross_mfma(dk
   const int grp = l / kCrossLanes, q = l % kCrossLanes, n32 = l & 31, hw = l >> 5;
   const int i0 = (blockIdx.x * kWaves + wave) * kCrossWaveStates;
   const int m = ws.m[b], R = ws.R[b];
+  if (second && !ws.more[b / g.gs]) return;  // the first part decided this group
   if ((int)blockIdx.x * kWaves * kCrossWaveStates >= m) return;  // whole workgroup (the walk has barriers)
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
-  const int nch = (R + kCkStride - 1) / kCkStride;
+  const int nch = min((R + kCkStride - 1) / kCkStride, lim);  // chunks tested
   // per state of this lane's column: whether its bound lies above rho, whether
   // it crosses within the tested prefixes, the crossing chunk and the need
   int my_ch = 0;
@@ -1409,6 +1411,45 @@ done:
     ws.first[rb + i] = first;
     if (out_first) out_first[rb + i] = first;
   }
+  if (!second) {  // the bank's crossings within the tested chunks
+    const unsigned long long found = __ballot(hw == 0 && i < m && first <= R);
+    if (l == 0 && found) atomicAdd(&ws.crossed[b], (int)__popcll(found));
+  }
+}
+
+// Whether a group's crossing search must go on past its first part, the first
+// kChunksPerSplit chunks of the order (every crossing r <= L = 1,024 found
+// there).  c_r only grows with r and the evictions a bank can make at a tested
+// length, max(0, m + r - M), are at most max(0, m + R - M); a bank with more
+// crossings than that within the first part is infeasible at every r >= L
+// (Eqs. 9-10), so r* < L for its group (Eq. 11), and the crossings within the
+// first part decide r*, the mandatory releases (first crossing <= r*) and the
+// projected densities at r* (chunks before r* only).  force: every state's
+// first crossing is wanted.
+__global__ __launch_bounds__(256) void k_cross_plan(Geom g, Workspace ws, int force) {
+  const int grp = blockIdx.x * 256 + threadIdx.x;
+  if (grp >= g.G) return;
+  const int b0 = grp * g.gs, R = ws.R[b0];
+  bool decided = R <= kChunksPerSplit * kCkStride;  // the first part tested every prefix
+  for (int j = 0; j < g.gs && !decided; ++j) {
+    const int b = b0 + j;
+    decided = ws.crossed[b] > max(0, ws.m[b] + R - ws.M[b]);
+  }
+  ws.more[grp] = (!decided || (force && R > kChunksPerSplit * kCkStride)) ? 1 : 0;
+}
+
+// Chunk sums of the ordered candidates past the first kChunksPerSplit chunks
+// (column splits 1, 2, ...), for the groups whose first part left r* open.
+template <int D, int P, bool FOLD, bool KV>
+__global__ __launch_bounds__(64 * gram_waves<D>(), gram_waves<D>() == 4 ? 3 : 2) void k_chunk_rest_mfma(
+    dkv_bank bank, const void *seg_k, const void *seg_v, Geom g, Prm p, Workspace ws) {
+  if (!ws.more[blockIdx.z / g.gs]) return;
+  constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
+  __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
+  __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
+  const StageBufs<D> sb{k0, k1, k2, a0, a1, a2, nullptr};
+  rowsum_body<D, P, RS_CHUNK, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, blockIdx.x, blockIdx.y + 1, blockIdx.z,
+                                        sb);
 }
 
 // Candidate keys and norms in score order, so that the ordered passes stream
@@ -1485,11 +1526,20 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       k_gather_sorted<D, KV><<<dim3(cdiv(g.N, 256 / (D / 8) * kGatherRows), g.B), 256, 0, s>>>(seg.k, sv, g, ws);
       break;
     case 1: {
+      // The crossing search in two parts: the chunk sums of the first
+      // kChunksPerSplit chunks of the order and the crossings within them; then,
+      // for the groups that this leaves open (k_cross_plan), the chunk sums of
+      // the rest and the whole search again.
+      const unsigned splits = cdiv(g.N, kChunksPerSplit * kCkStride);
+      const dim3 xgrid(cdiv(g.Mcap, kWaves * kCrossWaveStates), g.B);
       if (g.N > 0)
-        k_rowsum_mfma<D, P, RS_CHUNK, F, KV><<<dim3(rowsM, cdiv(g.N, kChunksPerSplit * kCkStride), g.B), T, 0, s>>>(
-            bank, seg.k, sv, g, p, ws, nullptr);
-      k_cross_mfma<D, P, F, KV><<<dim3(cdiv(g.Mcap, kWaves * kCrossWaveStates), g.B), 64 * kWaves, 0, s>>>(
-          bank, g, p, ws, out.first_cross);
+        k_rowsum_mfma<D, P, RS_CHUNK, F, KV><<<dim3(rowsM, 1, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, nullptr);
+      k_cross_mfma<D, P, F, KV><<<xgrid, 64 * kWaves, 0, s>>>(bank, g, p, ws, out.first_cross, kChunksPerSplit, 0);
+      if (splits > 1) {
+        k_cross_plan<<<cdiv(g.G, 256), 256, 0, s>>>(g, ws, out.first_cross != nullptr ? 1 : 0);
+        k_chunk_rest_mfma<D, P, F, KV><<<dim3(rowsM, splits - 1, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws);
+        k_cross_mfma<D, P, F, KV><<<xgrid, 64 * kWaves, 0, s>>>(bank, g, p, ws, out.first_cross, 1 << 30, 1);
+      }
       break;
     }
     case 2:

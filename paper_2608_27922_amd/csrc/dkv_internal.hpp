@@ -49,6 +49,8 @@ struct Workspace {
   uint4 *caug;         // [B, N]   of each candidate, source order
   uint4 *saug;         // [B, N]   of each candidate, score order
   int32_t *maint_off;  // [B + 1] first maintenance work item of each bank; [B] = total
+  int32_t *crossed;    // [B] states whose first crossing lies in the first part of the crossing search
+  int32_t *more;       // [G] 1 where the group's crossing search needs the prefixes past its first part
   uint32_t *feas;      // [B, nfw] bit r: prefix length r feasible for this bank
   int nfw;             // words per bank of feas
   uint64_t *skeys;     // [B, npad] sort keys, sorted within 512-key chunks

@@ -214,6 +214,7 @@ __global__ __launch_bounds__(kThreads) void k_begin(dkv_bank bank, const void *s
     ws.M[b] = Mb;
     ws.R[b] = R;
     ws.E[b] = E;
+    ws.crossed[b] = 0;
   }
 }
 
