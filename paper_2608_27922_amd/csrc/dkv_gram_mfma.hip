@@ -614,6 +614,9 @@ __global__ __launch_bounds__(64 * gram_waves<D>(), gram_waves<D>() == 4 ? 3 : 2)
 enum RowSumMode { RS_CHUNK = 0, RS_FIXUP = 1, RS_SURV_EV = 2, RS_ADM_BASE = 3, RS_ADM_MUT = 4, RS_DENSITY = 5 };
 
 constexpr int kChunksPerSplit = 1024 / kCkStride;   // RS_CHUNK: 1024 ordered candidates per workgroup
+// Ordered candidates in the first part of the crossing search (whole chunks).
+constexpr int kCrossFirst = 256;
+static_assert(kCrossFirst % kCkStride == 0, "the first part ends on a chunk boundary");
 
 // The three LDS stages of a Gram workgroup (separate arrays: with the stage
 // known at compile time, reads of one stage never wait for loads into another).
@@ -654,7 +657,7 @@ __device__ __forceinline__ uint32_t row_transpose_tail(const uint32_t (&a)[8], i
 template <int D, int P, int MODE, bool FOLD, bool KV>
 __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *seg_k, const void *seg_v, const Geom &g,
                                             const Prm &p, const Workspace &ws, int64_t *out, int bx, int by, int bz,
-                                            const StageBufs<D> &sb) {
+                                            const StageBufs<D> &sb, int cfirst = 0, int clim = 1 << 30) {
   constexpr int W = gram_waves<D>();
   constexpr int kRowsPerWG = 32 * W;
   const int b = bz;
@@ -677,10 +680,10 @@ __device__ __forceinline__ void rowsum_body(const dkv_bank &bank, const void *se
   if ((int)bx * kRowsPerWG >= nrows) return;
   // columns of this workgroup: [c0, c1) of the mode's column list
   int c0 = 0, c1 = 0;
-  if constexpr (MODE == RS_CHUNK) {
+  if constexpr (MODE == RS_CHUNK) {  // prefixes [cfirst, clim) of the order, 1,024 per split
     const int R = ws.R[b];
-    c0 = by * kChunksPerSplit * kCkStride;
-    c1 = min(R, c0 + kChunksPerSplit * kCkStride);
+    c0 = cfirst + by * kChunksPerSplit * kCkStride;
+    c1 = min(min(R, clim), c0 + kChunksPerSplit * kCkStride);
   } else if constexpr (MODE == RS_FIXUP) {
     c0 = (rs / kCkStride) * kCkStride;
     c1 = rs;
@@ -1418,8 +1421,7 @@ done:
 }
 
 // Whether a group's crossing search must go on past its first part, the first
-// kChunksPerSplit chunks of the order (every crossing r <= L = 1,024 found
-// there).  c_r only grows with r and the evictions a bank can make at a tested
+// L = kCrossFirst ordered candidates (every crossing r <= L found there).  c_r only grows with r and the evictions a bank can make at a tested
 // length, max(0, m + r - M), are at most max(0, m + R - M); a bank with more
 // crossings than that within the first part is infeasible at every r >= L
 // (Eqs. 9-10), so r* < L for its group (Eq. 11), and the crossings within the
@@ -1430,26 +1432,28 @@ __global__ __launch_bounds__(256) void k_cross_plan(Geom g, Workspace ws, int fo
   const int grp = blockIdx.x * 256 + threadIdx.x;
   if (grp >= g.G) return;
   const int b0 = grp * g.gs, R = ws.R[b0];
-  bool decided = R <= kChunksPerSplit * kCkStride;  // the first part tested every prefix
+  bool decided = R <= kCrossFirst;  // the first part tested every prefix
   for (int j = 0; j < g.gs && !decided; ++j) {
     const int b = b0 + j;
     decided = ws.crossed[b] > max(0, ws.m[b] + R - ws.M[b]);
   }
-  ws.more[grp] = (!decided || (force && R > kChunksPerSplit * kCkStride)) ? 1 : 0;
+  ws.more[grp] = (!decided || (force && R > kCrossFirst)) ? 1 : 0;
 }
 
-// Chunk sums of the ordered candidates past the first kChunksPerSplit chunks
-// (column splits 1, 2, ...), for the groups whose first part left r* open.
+// Chunk sums of the ordered prefixes [cfirst, clim) (splits of 1,024 from
+// cfirst): the first part of the crossing search, or (second) the rest, for the
+// groups whose first part left r* open.
 template <int D, int P, bool FOLD, bool KV>
-__global__ __launch_bounds__(64 * gram_waves<D>(), gram_waves<D>() == 4 ? 3 : 2) void k_chunk_rest_mfma(
-    dkv_bank bank, const void *seg_k, const void *seg_v, Geom g, Prm p, Workspace ws) {
-  if (!ws.more[blockIdx.z / g.gs]) return;
+__global__ __launch_bounds__(64 * gram_waves<D>(), gram_waves<D>() == 4 ? 3 : 2) void k_chunk_part_mfma(
+    dkv_bank bank, const void *seg_k, const void *seg_v, Geom g, Prm p, Workspace ws, int cfirst, int clim,
+    int second) {
+  if (second && !ws.more[blockIdx.z / g.gs]) return;
   constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
   __shared__ __attribute__((aligned(1024))) char k0[KB], k1[KB], k2[KB];
   __shared__ __attribute__((aligned(16))) char a0[AB], a1[AB], a2[AB];
   const StageBufs<D> sb{k0, k1, k2, a0, a1, a2, nullptr};
-  rowsum_body<D, P, RS_CHUNK, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, blockIdx.x, blockIdx.y + 1, blockIdx.z,
-                                        sb);
+  rowsum_body<D, P, RS_CHUNK, FOLD, KV>(bank, seg_k, seg_v, g, p, ws, nullptr, blockIdx.x, blockIdx.y, blockIdx.z, sb,
+                                        cfirst, clim);
 }
 
 // Candidate keys and norms in score order, so that the ordered passes stream
@@ -1527,17 +1531,18 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       break;
     case 1: {
       // The crossing search in two parts: the chunk sums of the first
-      // kChunksPerSplit chunks of the order and the crossings within them; then,
-      // for the groups that this leaves open (k_cross_plan), the chunk sums of
-      // the rest and the whole search again.
-      const unsigned splits = cdiv(g.N, kChunksPerSplit * kCkStride);
+      // kCrossFirst ordered candidates and the crossings within them; then, for
+      // the groups that this leaves open (k_cross_plan), the chunk sums of the
+      // rest and the whole search again.
       const dim3 xgrid(cdiv(g.Mcap, kWaves * kCrossWaveStates), g.B);
       if (g.N > 0)
-        k_rowsum_mfma<D, P, RS_CHUNK, F, KV><<<dim3(rowsM, 1, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, nullptr);
-      k_cross_mfma<D, P, F, KV><<<xgrid, 64 * kWaves, 0, s>>>(bank, g, p, ws, out.first_cross, kChunksPerSplit, 0);
-      if (splits > 1) {
+        k_chunk_part_mfma<D, P, F, KV><<<dim3(rowsM, 1, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, 0, kCrossFirst, 0);
+      k_cross_mfma<D, P, F, KV><<<xgrid, 64 * kWaves, 0, s>>>(bank, g, p, ws, out.first_cross,
+                                                              kCrossFirst / kCkStride, 0);
+      if (g.N > kCrossFirst) {
         k_cross_plan<<<cdiv(g.G, 256), 256, 0, s>>>(g, ws, out.first_cross != nullptr ? 1 : 0);
-        k_chunk_rest_mfma<D, P, F, KV><<<dim3(rowsM, splits - 1, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws);
+        k_chunk_part_mfma<D, P, F, KV><<<dim3(rowsM, cdiv(g.N - kCrossFirst, kChunksPerSplit * kCkStride), g.B), T,
+                                         0, s>>>(bank, seg.k, sv, g, p, ws, kCrossFirst, 1 << 30, 1);
         k_cross_mfma<D, P, F, KV><<<xgrid, 64 * kWaves, 0, s>>>(bank, g, p, ws, out.first_cross, 1 << 30, 1);
       }
       break;
