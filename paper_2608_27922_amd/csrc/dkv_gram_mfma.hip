@@ -1169,15 +1169,19 @@ struct CrossRow {
   uint4 x[kCrossPerLane / 4];
 };
 
-__device__ __forceinline__ CrossRow cross_load(const dkv_bank &bank, const Workspace &ws, size_t row, int q) {
+__device__ __forceinline__ CrossRow cross_load(const dkv_bank &bank, const Workspace &ws, size_t row, int q, int nch) {
   CrossRow r;
   r.base = bank.base[row];
   r.rho = bank.rho[row];
-  // 16-byte groups of the row (nck >= 4, a multiple of 4, at least nch); clamped
+  // 16-byte groups of the row (nck >= 4, a multiple of 4, at least nch); only
+  // those that hold tested chunks are read (the rest may be stale), clamped
   const uint4 *ckr = reinterpret_cast<const uint4 *>(ws.ck + row * ws.nck);
   const int last = ws.nck / 4 - 1;
 #pragma unroll
-  for (int v4 = 0; v4 < kCrossPerLane / 4; ++v4) r.x[v4] = ckr[min((kCrossPerLane * q) / 4 + v4, last)];
+  for (int v4 = 0; v4 < kCrossPerLane / 4; ++v4) {
+    const int grp = (kCrossPerLane * q) / 4 + v4;
+    r.x[v4] = 4 * grp < nch ? ckr[min(grp, last)] : uint4{0u, 0u, 0u, 0u};
+  }
   return r;
 }
 
@@ -1270,7 +1274,8 @@ __global__ __launch_bounds__(64 * kWaves, D <= 128 ? 3 : 2) void k_cross_mfma(dk
   constexpr int kPasses = kCrossWaveStates / kCrossStates;
   CrossRow rows[kPasses];  // every pass's loads in flight together
 #pragma unroll
-  for (int ps = 0; ps < kPasses; ++ps) rows[ps] = cross_load(bank, ws, rb + min(i0 + kCrossStates * ps + grp, m - 1), q);
+  for (int ps = 0; ps < kPasses; ++ps)
+    rows[ps] = cross_load(bank, ws, rb + min(i0 + kCrossStates * ps + grp, m - 1), q, nch);
 #pragma unroll
   for (int ps = 0; ps < kPasses; ++ps) {
     const int s = kCrossStates * ps + grp;
