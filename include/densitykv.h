@@ -205,7 +205,10 @@ typedef struct {
  *                           the state violates the growth bound, R+1 if none
  *                           within r <= R (R = min(N, budgets of the group))
  *   rho_tilde    [B, Mcap]  per pre-update slot: rho + sum of its weights to the
- *                           admitted prefix (projected density at r*, Q23)      */
+ *                           admitted prefix (projected density at r*, Q23)
+ * Without first_cross the crossing search may end after the first 256 ordered
+ * candidates for a group that some bank's crossings there already rule out of
+ * every longer prefix (Eqs. 9-11); every other output is the same either way. */
 typedef struct {
   int32_t *r_star;
   int32_t *n_admitted;
