@@ -101,21 +101,26 @@ def test_rollout_small_shared_prefix(dt, d):
     _run_rollout(cfg, 6, api.Params(sigma2_log2=4 if d == 64 else 5), dup_every=2)
 
 
-def test_rollout_checkpoint_tiles():
-    """N = 700 > 256 candidates: prefix checkpoints plus a partial tile at r*."""
-    _log("rollout checkpoint tiles")
+@pytest.mark.parametrize("trace", [True, False])
+def test_rollout_checkpoint_tiles(trace):
+    """N = 700 > 256 candidates: prefix checkpoints plus a partial tile at r*
+    (without the trace outputs the crossing search may end after its first part)."""
+    _log(f"rollout checkpoint tiles trace={trace}")
     cfg = synth.Config(heads=4, d=128, dtype="bf16", n_cand=700, budget=1000, group_size=2, **SMALL)
-    _run_rollout(cfg, 4, api.Params(sigma2_log2=5), dup_every=2)
+    _run_rollout(cfg, 4, api.Params(sigma2_log2=5), dup_every=2, trace=trace)
 
 
-@pytest.mark.parametrize("n", [1, 64, 65, 512, 513, 1025])
-def test_rollout_candidate_count_boundaries(n):
-    """Candidate counts at the edges of the 64-candidate chunks, the 512-key sort
-    chunks, the 128-row Gram blocks and the 512-column admitted x admitted splits
-    (budget 1,100: the first blocks admit everything, later ones evict)."""
-    _log(f"rollout candidate count n={n}")
+@pytest.mark.parametrize("n,trace", [(1, True), (64, True), (65, True), (256, False), (257, False), (512, True),
+                                     (513, True), (513, False), (1025, True), (1025, False)])
+def test_rollout_candidate_count_boundaries(n, trace):
+    """Candidate counts at the edges of the 64-candidate chunks, the 256-candidate
+    first part of the crossing search, the 512-key sort chunks, the 128-row Gram
+    blocks and the 512-column admitted x admitted splits (budget 1,100: the first
+    blocks admit everything, later ones evict); without the trace outputs the
+    crossing search may end after its first part."""
+    _log(f"rollout candidate count n={n} trace={trace}")
     cfg = synth.Config(heads=2, d=128, dtype="bf16", n_cand=n, budget=1100, group_size=2, **SMALL)
-    _run_rollout(cfg, 4, api.Params(sigma2_log2=5), dup_every=2)
+    _run_rollout(cfg, 4, api.Params(sigma2_log2=5), dup_every=2, trace=trace)
 
 
 def test_rollout_ragged_budgets_independent_heads():
@@ -583,6 +588,52 @@ def _spread_case(d, kv, seed):
         bank.base[b, :ob.m] = torch.from_numpy(base).to(bank.base.device)
     torch.cuda.synchronize()
     return prm, op, bank, K1, V1
+
+
+@pytest.mark.parametrize("budgets,decided", [((3000, 3000), (True, True)), ((1191, 1191), (False, False)),
+                                             ((1195, 1191), (True, False))])
+@pytest.mark.parametrize("trace", [False, True])
+def test_crossing_search_first_part(budgets, decided, trace):
+    """Two banks of one group, d = 128, three blocks of 600 candidates from one
+    cluster: the states admitted in block 1 carry baselines from a half-full bank,
+    so in block 2 all 600 cross within the first 256 ordered candidates.  A bank
+    with more crossings there than the evictions it could make at any tested
+    length, max(0, m + R - M), rules out every prefix past 256 (Eqs. 9-11):
+    budget 3,000 (E = 0) and 1,195 (E = 596) decide the group in the first part
+    (r* < 256), 1,191 (E = 600) does not (the search goes on; r* = 600 with
+    600 releases); one bank of each kind in a group decides it.  The
+    scenario is checked on the oracle's records, the banks against the oracle,
+    and with trace outputs every record too."""
+    _log(f"crossing search first part budgets={budgets} trace={trace}")
+    d, N, H = 128, 600, 2
+    rng = np.random.default_rng(91)
+    snap = lambda x: (np.clip(np.rint(x * 64.0), -127, 127) / 64.0).astype(np.float32)
+    c0 = rng.standard_normal(d)
+    c0 /= np.linalg.norm(c0)
+    prm = api.Params(sigma2_log2=5)
+    op = oracle_params(prm)
+    bank = api.Bank(H, max(budgets), d, dtype=torch.bfloat16, group_size=H,
+                    budget=torch.tensor(budgets, dtype=torch.int32))
+    obanks = [BankState.empty(b, d) for b in budgets]
+    for t in range(3):
+        K = np.stack([snap(c0 + 0.3 * rng.standard_normal((N, d))) for _ in range(H)])
+        V = torch.from_numpy(rng.standard_normal((H, N, d)).astype(np.float32)).to(torch.bfloat16).float().numpy()
+        out = api.UpdateOut(bank, N, trace=trace)
+        api.update_bank(bank, dev(K, "bf16"), dev(V, "bf16"), t, prm, out=out)
+        torch.cuda.synchronize()
+        new, recs = oracle_step(obanks, K, V, t, op, H)
+        if t == 2:  # the scenario, on the oracle
+            R = recs[0].R
+            got = tuple(bool(np.count_nonzero(recs[0].heads[h].first_cross <= 256) > max(0, obanks[h].m + R - budgets[h]))
+                        for h in range(H))
+            assert R > 256 and got == decided, f"scenario: first part decides {got}, expected {decided}"
+            assert (recs[0].r_star < 256) if any(decided) else (recs[0].r_star == 600), f"scenario: r* {recs[0].r_star}"
+        if trace:
+            assert_trace_equal(out, recs, H, obanks, N, ctx=f"block {t}")
+        assert int(out.r_star[0]) == recs[0].r_star, f"block {t}: r*"
+        for b in range(H):
+            assert_bank_equal(bank, b, new[b], ctx=f"block {t}")
+        obanks = new
 
 
 @pytest.mark.parametrize("d,kv", [(128, False), (64, False), (64, True), (128, True)])
