@@ -175,18 +175,19 @@ def test_rollout_kv_descriptor(dt, d):
                  grid_values=True)
 
 
-def test_rollout_kv_descriptor_multi_split():
+@pytest.mark.parametrize("trace", [True, False])
+def test_rollout_kv_descriptor_multi_split(trace):
     """The [K; V] geometry at descriptor dimension 256 across the tiling edges: banks of
     2,600 states filled by the empty-bank rule (three 1,024-column score splits), then
     1,100 candidates per block (three 512-key sort chunks, 18 prefix chunks, admitted x
     admitted in three half-splits of 512 columns) into full banks, every block releasing
     1,100 states by the densest fill (survivors x evicted 1,500 x 1,100); every
-    intermediate and the committed bank bit-exact against the oracle on the concatenated
-    descriptors."""
-    _log("rollout kv descriptor multi-split")
+    intermediate (with trace outputs) and the committed bank bit-exact against the
+    oracle on the concatenated descriptors."""
+    _log(f"rollout kv descriptor multi-split trace={trace}")
     cfg = synth.Config(heads=2, d=128, dtype="bf16", n_cand=1100, budget=2600, group_size=2, **SMALL)
     bank, obanks = _run_rollout(cfg, 4, api.Params(sigma2_log2=6, flags=api.POLICY_KV_DESCRIPTOR), dup_every=2,
-                                init_full=True, grid_values=True)
+                                init_full=True, grid_values=True, trace=trace)
     assert all(b.m == 2600 for b in obanks)
 
 
