@@ -409,11 +409,19 @@ template <int D, int P, bool FOLD, bool KV>
 __global__ __launch_bounds__(64 * gram_waves<D>(), gram_waves<D>() == 4 ? 3 : 2) void k_score_mfma(dkv_bank bank, const void *seg_k, const void *seg_v,
                                                            Geom g, Prm p, Workspace ws) {
   constexpr int W = gram_waves<D>();
-  const int b = blockIdx.z;
+  // One-dimensional grid over (row block, column split, bank), row blocks
+  // fastest.  Workgroup L is dispatched to XCD L % 8; ranking the workgroups
+  // XCD by XCD (r = workgroups on lower XCDs + L / 8) keeps all the work items
+  // of a bank on one XCD, in order, so that its keys and the candidates' stay
+  // in that XCD's L2.
+  const int nx = (g.N + 32 * W - 1) / (32 * W), ny = (g.Mcap + kColsPerSplit - 1) / kColsPerSplit;
+  const int T = (int)gridDim.x, L = (int)blockIdx.x, xcd = L % 8;
+  const int r = xcd * (T / 8) + min(xcd, T % 8) + L / 8;
+  const int b = r / (nx * ny), by = (r / nx) % ny, bx = r % nx;
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, h = l >> 5, n = l & 31;
-  const int x = blockIdx.x * 32 * W + wave * 32 + n;
+  const int x = bx * 32 * W + wave * 32 + n;
   const int m = ws.m[b];
-  const int c0 = blockIdx.y * kColsPerSplit;
+  const int c0 = by * kColsPerSplit;
   if (c0 >= m) return;
   const int ncols = min(kColsPerSplit, m - c0);
   constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
@@ -1529,7 +1537,8 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
   const void *sv = seg.v;
   switch (stage) {
     case 0:  // score; the ordered copy is launched after the sort (stage 4)
-      k_score_mfma<D, P, F, KV><<<dim3(rowsN, cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws);
+      k_score_mfma<D, P, F, KV><<<rowsN * cdiv(g.Mcap, kColsPerSplit) * (unsigned)g.B, T, 0, s>>>(bank, seg.k, sv, g,
+                                                                                                   p, ws);
       break;
     case 4:
       k_gather_sorted<D, KV><<<dim3(cdiv(g.N, 256 / (D / 8) * kGatherRows), g.B), 256, 0, s>>>(seg.k, sv, g, ws);
@@ -1590,7 +1599,7 @@ void mfma_score_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &g
   constexpr int W = gram_waves<D>();
   const int T = 64 * W;
   if (g.N > 0 && (score_q || score_f)) {
-    k_score_mfma<D, P, F, KV><<<dim3(cdiv(g.N, 32 * W), cdiv(g.Mcap, kColsPerSplit), g.B), T, 0, s>>>(
+    k_score_mfma<D, P, F, KV><<<cdiv(g.N, 32 * W) * cdiv(g.Mcap, kColsPerSplit) * (unsigned)g.B, T, 0, s>>>(
         bank, seg.k, seg.v, g, p, ws);
     k_score_out<<<dim3(cdiv(g.N, 256), g.B), 256, 0, s>>>(g, ws, score_q, score_f);
   }
