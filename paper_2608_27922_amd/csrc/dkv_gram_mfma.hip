@@ -1474,32 +1474,37 @@ __global__ __launch_bounds__(64 * gram_waves<D>(), gram_waves<D>() == 4 ? 3 : 2)
 // (every load and store instruction covers whole rows).
 constexpr int kGatherRows = 4;
 
+// Positions [r0, r1) of the order (r1 <= N): the first part of the crossing
+// search reads positions below kCrossFirst only, so the rest is copied (second)
+// only for the groups whose first part left r* open.
 template <int D, bool KV>
-__global__ __launch_bounds__(256) void k_gather_sorted(const void *seg_k, const void *seg_v, Geom g, Workspace ws) {
+__global__ __launch_bounds__(256) void k_gather_sorted(const void *seg_k, const void *seg_v, Geom g, Workspace ws,
+                                                       int r0, int r1, int second) {
   constexpr int CH = D / 8;      // 16-byte chunks per bf16 row
   constexpr int RPP = 256 / CH;  // rows per workgroup pass
   static_assert(kGatherRows <= CH, "one metadata lane per row of the group");
   const int b = blockIdx.y;
   const int c = threadIdx.x % CH;
-  const int j0 = blockIdx.x * RPP * kGatherRows + threadIdx.x / CH;
+  const int j0 = r0 + blockIdx.x * RPP * kGatherRows + threadIdx.x / CH;
   const size_t nb = (size_t)b * g.N;
-  if ((int)blockIdx.x * RPP * kGatherRows >= g.N) return;  // whole workgroup
+  if (r0 + (int)blockIdx.x * RPP * kGatherRows >= r1) return;  // whole workgroup
+  if (second && !ws.more[b / g.gs]) return;
   const Desc src{static_cast<const uint16_t *>(seg_k), static_cast<const uint16_t *>(seg_v)};
   // loads from clamped (in-range) rows, unconditional so that they overlap
   int xs[kGatherRows];
 #pragma unroll
-  for (int u = 0; u < kGatherRows; ++u) xs[u] = ws.order[nb + min(j0 + u * RPP, g.N - 1)];
+  for (int u = 0; u < kGatherRows; ++u) xs[u] = ws.order[nb + min(j0 + u * RPP, r1 - 1)];
   u32x4 tmp[kGatherRows];
 #pragma unroll
   for (int u = 0; u < kGatherRows; ++u)
     tmp[u] = *reinterpret_cast<const u32x4 *>(desc_chunk<D, KV>(src, (int64_t)(nb + xs[u]), c));
 #pragma unroll
   for (int u = 0; u < kGatherRows; ++u)
-    if (j0 + u * RPP < g.N) reinterpret_cast<u32x4 *>(ws.sk + (nb + j0 + u * RPP) * D)[c] = tmp[u];
+    if (j0 + u * RPP < r1) reinterpret_cast<u32x4 *>(ws.sk + (nb + j0 + u * RPP) * D)[c] = tmp[u];
   // lane c < kGatherRows of a row group copies the norm and norm step of row c
   if (c < kGatherRows) {
     const int j = j0 + c * RPP;
-    if (j < g.N) {
+    if (j < r1) {
       const int x = ws.order[nb + j];
       ws.snorm[nb + j] = ws.cnorm[nb + x];
       ws.saug[nb + j] = ws.caug[nb + x];
@@ -1540,9 +1545,12 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       k_score_mfma<D, P, F, KV><<<rowsN * cdiv(g.Mcap, kColsPerSplit) * (unsigned)g.B, T, 0, s>>>(bank, seg.k, sv, g,
                                                                                                    p, ws);
       break;
-    case 4:
-      k_gather_sorted<D, KV><<<dim3(cdiv(g.N, 256 / (D / 8) * kGatherRows), g.B), 256, 0, s>>>(seg.k, sv, g, ws);
+    case 4: {  // the positions the first part of the crossing search reads
+      const int r1 = min(g.N, kCrossFirst);
+      k_gather_sorted<D, KV><<<dim3(cdiv(r1, 256 / (D / 8) * kGatherRows), g.B), 256, 0, s>>>(seg.k, sv, g, ws, 0, r1,
+                                                                                             0);
       break;
+    }
     case 1: {
       // The crossing search in two parts: the chunk sums of the first
       // kCrossFirst ordered candidates and the crossings within them; then, for
@@ -1555,6 +1563,8 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
                                                               kCrossFirst / kCkStride, 0);
       if (g.N > kCrossFirst) {
         k_cross_plan<<<cdiv(g.G, 256), 256, 0, s>>>(g, ws, out.first_cross != nullptr ? 1 : 0);
+        k_gather_sorted<D, KV><<<dim3(cdiv(g.N - kCrossFirst, 256 / (D / 8) * kGatherRows), g.B), 256, 0, s>>>(
+            seg.k, sv, g, ws, kCrossFirst, g.N, 1);
         k_chunk_part_mfma<D, P, F, KV><<<dim3(rowsM, cdiv(g.N - kCrossFirst, kChunksPerSplit * kCkStride), g.B), T,
                                          0, s>>>(bank, seg.k, sv, g, p, ws, kCrossFirst, 1 << 30, 1);
         k_cross_mfma<D, P, F, KV><<<xgrid, 64 * kWaves, 0, s>>>(bank, g, p, ws, out.first_cross, 1 << 30, 1);
