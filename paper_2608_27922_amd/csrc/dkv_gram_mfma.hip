@@ -1316,11 +1316,12 @@ __global__ __launch_bounds__(64 * kWaves, D <= 128 ? 3 : 2) void k_cross_mfma(dk
   for (int k = 0; k < 4; ++k) cs[k] = __builtin_amdgcn_readfirstlane(chunk_set[k]);
   if (cs[0] | cs[1] | cs[2] | cs[3]) {  // uniform over the workgroup
     // B operand: this lane's state as the Gram stages hold a row item (keys
-    // times -2 / sigma^2 and the norm step)
+    // times -2 / sigma^2 and the norm step); read for the states that walk only
+    // (the others' columns of the Gram are not used)
     const int64_t srow = (int64_t)(rb + min(i0 + n32, m - 1));
     RowFrag<D> rf;
     load_row_frag<D, FOLD, KV>(rf, Desc{static_cast<const uint16_t *>(bank.k), static_cast<const uint16_t *>(bank.v)},
-                               srow, bank.knorm[srow], true, -2.0f * p.inv_sigma2, p.inv_sigma2);
+                               srow, my_walk ? bank.knorm[srow] : 0.0f, my_walk, -2.0f * p.inv_sigma2, p.inv_sigma2);
     int aoff[TileCfg<D>::kSteps];
     frag_offsets<D>(aoff);
     // each crossing chunk's 64 ordered candidates go through a stage buffer
