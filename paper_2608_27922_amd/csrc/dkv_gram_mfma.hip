@@ -1434,6 +1434,119 @@ done:
   }
 }
 
+// The first part of the crossing search in one pass: the prefix-chunk Gram of
+// the workgroup's 128 bank states over the first kCrossFirst ordered
+// candidates (4 waves x 32 states as row items, one 64-candidate chunk per
+// column stage, two stage buffers) stores each chunk sum as the chunk-sum Gram
+// does, and every state whose running prefix reaches its bound within a chunk
+// takes its first crossing there from the same weights, summed in candidate
+// order (the two half-waves exchange their 4-candidate group sums); states that
+// do not cross within the first part get R + 1, states already at their bound
+// 0.  The bank's crossings found are added to ws.crossed.
+template <int D, int P, bool FOLD, bool KV>
+__global__ __launch_bounds__(64 * kWaves, D <= 128 ? 3 : 2) void k_first_part_mfma(dkv_bank bank, Geom g, Prm p,
+                                                                                 Workspace ws, int32_t *out_first) {
+  static_assert(kCkStride == 2 * kCT, "two 32-candidate tiles per chunk");
+  const int b = blockIdx.y;
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63, n = l & 31, hw = l >> 5;
+  const int m = ws.m[b], R = ws.R[b];
+  if ((int)blockIdx.x * 32 * kWaves >= m) return;  // whole workgroup (the stages have barriers)
+  const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
+  const int v = blockIdx.x * 32 * kWaves + wave * 32 + n;
+  const bool rv = v < m;
+  const int64_t row = (int64_t)(rb + min(v, m - 1));
+  // the bound: the state violates once rho + P reaches ceil(T b / 2^k)
+  const int64_t lim = ((int64_t)p.tau_num * bank.base[row] + ((1ll << p.tau_shift) - 1)) >> p.tau_shift;
+  const int64_t thr = lim - bank.rho[row];
+  const int nch = min((R + kCkStride - 1) / kCkStride, kCrossFirst / kCkStride);
+  int first = thr > 0 ? R + 1 : 0;
+  bool open = thr > 0;  // not yet crossed
+  if (nch > 0) {
+    RowFrag<D> rf;
+    load_row_frag<D, FOLD, KV>(rf, Desc{static_cast<const uint16_t *>(bank.k), static_cast<const uint16_t *>(bank.v)},
+                               row, bank.knorm[row], rv, -2.0f * p.inv_sigma2, p.inv_sigma2);
+    int aoff[TileCfg<D>::kSteps];
+    frag_offsets<D>(aoff);
+    constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
+    __shared__ __attribute__((aligned(1024))) char kbuf[2][KB];
+    __shared__ __attribute__((aligned(16))) char abuf[2][AB];
+    const StageOff<D> soff = stage_offsets<D>();
+    auto issue = [&](int c, int buf) __attribute__((always_inline)) {
+      stage_dma_seq<D, false>(soff, c * kCkStride, ws.sk, ws.saug, nullptr, kbuf[buf], abuf[buf], nullptr, (int64_t)nb,
+                              g.N);
+    };
+    uint64_t run = 0;  // the state's prefix sum before chunk c
+    issue(0, 0);
+    for (int c = 0; c < nch; ++c) {
+      const int buf = c & 1;
+      __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+      stage_barrier();  // every wave's loads of chunk c landed; every wave is done with the other buffer
+      if (c + 1 < nch) issue(c + 1, buf ^ 1);
+      const f32x16 x0 = tile_mfma<D>(kbuf[buf], abuf[buf], 0, rf, aoff);
+      const f32x16 x1 = tile_mfma<D>(kbuf[buf], abuf[buf], 1, rf, aoff);
+      // weights in candidate order inside the lane: tile tl, register 4 k + j is
+      // candidate 32 tl + 8 k + 4 hw + j of the chunk; candidates past R weigh nothing
+      const int nvalid = min(kCkStride, R - c * kCkStride);
+      uint32_t w[2][16], gsum[2][4];
+#pragma unroll
+      for (int tl = 0; tl < 2; ++tl) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          gsum[tl][k] = 0;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            uint32_t W = weight_raw<P, FOLD>(tl ? x1[4 * k + j] : x0[4 * k + j], 8388608.0f) - kMagic;
+            asm volatile("" : "+v"(W));  // computed for every lane, then masked
+            W = 32 * tl + 8 * k + 4 * hw + j < nvalid ? W : 0u;
+            w[tl][4 * k + j] = W;
+            gsum[tl][k] += W;
+          }
+        }
+      }
+      uint32_t lane_tot = 0;
+#pragma unroll
+      for (int tl = 0; tl < 2; ++tl)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) lane_tot += gsum[tl][k];
+      const uint32_t tot = lane_tot + __shfl_xor(lane_tot, 32, 64);  // the chunk sum (at most 2^29)
+      if (rv && hw == 0) ws.ck[(rb + v) * ws.nck + c] = tot;
+      const bool hit = open && (int64_t)(run + tot) >= thr;
+      if (__ballot(hit)) {  // uniform over the wave
+        // inclusive prefixes in candidate order; the crossing is one plus the
+        // number of candidates whose prefix is still below the need
+        const uint32_t nd1 = hit ? (uint32_t)(thr - (int64_t)run) - 1u : 0u;
+        uint32_t pr = 0, cnt = 0;
+#pragma unroll
+        for (int tl = 0; tl < 2; ++tl) {
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            const uint32_t other = __shfl_xor(gsum[tl][k], 32, 64);
+            uint32_t q = pr + (hw ? other : 0u);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              q += w[tl][4 * k + j];
+              cnt += q <= nd1 ? 1u : 0u;
+            }
+            pr += gsum[tl][k] + other;
+          }
+        }
+        cnt += __shfl_xor(cnt, 32, 64);
+        if (hit) {
+          first = c * kCkStride + (int)cnt + 1;
+          open = false;
+        }
+      }
+      run += tot;
+    }
+  }
+  if (hw == 0 && rv) {
+    ws.first[rb + v] = first;
+    if (out_first) out_first[rb + v] = first;
+  }
+  const unsigned long long found = __ballot(hw == 0 && rv && first <= R);
+  if (l == 0 && found) atomicAdd(&ws.crossed[b], (int)__popcll(found));
+}
+
 // Whether a group's crossing search must go on past its first part, the first
 // L = kCrossFirst ordered candidates (every crossing r <= L found there).  c_r only grows with r and the evictions a bank can make at a tested
 // length, max(0, m + r - M), are at most max(0, m + R - M); a bank with more
@@ -1558,10 +1671,8 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
       // the groups that this leaves open (k_cross_plan), the chunk sums of the
       // rest and the whole search again.
       const dim3 xgrid(cdiv(g.Mcap, kWaves * kCrossWaveStates), g.B);
-      if (g.N > 0)
-        k_chunk_part_mfma<D, P, F, KV><<<dim3(rowsM, 1, g.B), T, 0, s>>>(bank, seg.k, sv, g, p, ws, 0, kCrossFirst, 0);
-      k_cross_mfma<D, P, F, KV><<<xgrid, 64 * kWaves, 0, s>>>(bank, g, p, ws, out.first_cross,
-                                                              kCrossFirst / kCkStride, 0);
+      k_first_part_mfma<D, P, F, KV><<<dim3(cdiv(g.Mcap, 32 * kWaves), g.B), 64 * kWaves, 0, s>>>(bank, g, p, ws,
+                                                                                                out.first_cross);
       if (g.N > kCrossFirst) {
         k_cross_plan<<<cdiv(g.G, 256), 256, 0, s>>>(g, ws, out.first_cross != nullptr ? 1 : 0);
         k_gather_sorted<D, KV><<<dim3(cdiv(g.N - kCrossFirst, 256 / (D / 8) * kGatherRows), g.B), 256, 0, s>>>(
