@@ -3,14 +3,16 @@
 // Every Gram stage evaluates Soft-Riesz weights w(k_i, k_j) (Eq. 2) for a set
 // of "row" items against a stream of "column" items and reduces them per row:
 //
-//   k_score_mfma   rows = candidates, columns = bank states:
-//                  S_x = sum_i RNE(w_ix bs_i), Wcol_x = sum_i W_ix  (Eq. 6)
-//   k_rowsum_mfma  row sums: per-64-candidate chunk sums over the ordered
-//                  candidates (the prefix checkpoints of Eqs. 8-9), the r*
-//                  fix-up, the exact maintenance (Supp. C) and the
-//                  from-scratch bank density (Eq. 3)
-//   k_cross_mfma   per bank state: the chunk in which its prefix density first
-//                  reaches tau b, then the exact prefix length inside it
+//   k_score_mfma       rows = candidates, columns = bank states:
+//                      S_x = sum_i RNE(w_ix bs_i), Wcol_x = sum_i W_ix  (Eq. 6)
+//   k_first_part_mfma  per bank state, over the first 256 ordered candidates:
+//                      64-candidate chunk sums (the prefix checkpoints of
+//                      Eqs. 8-9) and the first prefix that reaches tau b
+//   k_chunk_part_mfma  the chunk sums of the rest of the order, and
+//   k_cross_mfma       the whole crossing search, for the groups that the first
+//                      part leaves open (k_cross_plan, Eqs. 9-11)
+//   k_rowsum_mfma      row sums: the r* fix-up, the exact maintenance (Supp. C)
+//                      and the from-scratch bank density (Eq. 3)
 //
 // The column range of every Gram is split over workgroups (grid dimension y);
 // partial integer sums are combined with 64-bit atomic adds, which are exact
@@ -1245,6 +1247,8 @@ __device__ __forceinline__ CrossFind cross_find(const CrossRow &r, const Prm &p,
   return f;
 }
 
+// The whole crossing search over every tested prefix, for the groups that the
+// first part leaves open (every group when first crossings are requested).
 // A wave takes 32 states, a workgroup 128.
 // The chunk search runs in four passes of eight states; each state's result then
 // moves to lanes n and n + 32 (n = its index in the wave).  The exact walk: the
@@ -1262,7 +1266,7 @@ constexpr int kCrossWaveStates = 32;
 
 template <int D, int P, bool FOLD, bool KV>
 __global__ __launch_bounds__(64 * kWaves, D <= 128 ? 3 : 2) void k_cross_mfma(dkv_bank bank, Geom g, Prm p, Workspace ws,
-                                                                            int32_t *out_first, int lim, int second) {
+                                                                            int32_t *out_first) {
   static_assert(kCkStride == 64, "two 32-candidate tiles per chunk");
   constexpr int KSW = D / 16;
   const int b = blockIdx.y;
@@ -1270,10 +1274,10 @@ __global__ __launch_bounds__(64 * kWaves, D <= 128 ? 3 : 2) void k_cross_mfma(dk
   const int grp = l / kCrossLanes, q = l % kCrossLanes, n32 = l & 31, hw = l >> 5;
   const int i0 = (blockIdx.x * kWaves + wave) * kCrossWaveStates;
   const int m = ws.m[b], R = ws.R[b];
-  if (second && !ws.more[b / g.gs]) return;  // the first part decided this group
+  if (!ws.more[b / g.gs]) return;  // the first part decided this group
   if ((int)blockIdx.x * kWaves * kCrossWaveStates >= m) return;  // whole workgroup (the walk has barriers)
   const size_t rb = (size_t)b * g.Mcap, nb = (size_t)b * g.N;
-  const int nch = min((R + kCkStride - 1) / kCkStride, lim);  // chunks tested
+  const int nch = (R + kCkStride - 1) / kCkStride;
   // per state of this lane's column: whether its bound lies above rho, whether
   // it crosses within the tested prefixes, the crossing chunk and the need
   int my_ch = 0;
@@ -1427,10 +1431,6 @@ done:
   if (hw == 0 && i < m) {
     ws.first[rb + i] = first;
     if (out_first) out_first[rb + i] = first;
-  }
-  if (!second) {  // the bank's crossings within the tested chunks
-    const unsigned long long found = __ballot(hw == 0 && i < m && first <= R);
-    if (l == 0 && found) atomicAdd(&ws.crossed[b], (int)__popcll(found));
   }
 }
 
@@ -1679,7 +1679,7 @@ void mfma_update_impl(const dkv_bank &bank, const dkv_segment &seg, const Geom &
             seg.k, sv, g, ws, kCrossFirst, g.N, 1);
         k_chunk_part_mfma<D, P, F, KV><<<dim3(rowsM, cdiv(g.N - kCrossFirst, kChunksPerSplit * kCkStride), g.B), T,
                                          0, s>>>(bank, seg.k, sv, g, p, ws, kCrossFirst, 1 << 30, 1);
-        k_cross_mfma<D, P, F, KV><<<xgrid, 64 * kWaves, 0, s>>>(bank, g, p, ws, out.first_cross, 1 << 30, 1);
+        k_cross_mfma<D, P, F, KV><<<xgrid, 64 * kWaves, 0, s>>>(bank, g, p, ws, out.first_cross);
       }
       break;
     }

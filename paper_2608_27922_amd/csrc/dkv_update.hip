@@ -3,7 +3,8 @@
 // One update of every bank from one block (Supp. C, Algorithm 1) is the kernel
 // sequence below, all on the caller's stream, with r* kept on the device.  The
 // Gram stages of bf16 banks run on MFMA (dkv_gram_mfma.hip: k_score_mfma,
-// k_gather_sorted, k_rowsum_mfma, k_cross_mfma, k_maint_mfma); fp32 banks use the
+// k_gather_sorted, k_first_part_mfma, k_cross_plan, k_chunk_part_mfma,
+// k_cross_mfma, k_rowsum_mfma, k_maint_mfma); fp32 banks use the
 // VALU kernels of this file (k_score_gram, k_cross_gram, k_fixup, k_maint_gram).
 //
 //   k_begin         clamp occupancy/budget, tested prefix R of the group (Eq. 11),
