@@ -1468,20 +1468,25 @@ __global__ __launch_bounds__(64 * kWaves, D <= 128 ? 3 : 2) void k_first_part_mf
     int aoff[TileCfg<D>::kSteps];
     frag_offsets<D>(aoff);
     constexpr int KB = SCfg<D>::KEYB, AB = SCfg<D>::AUGB;
-    __shared__ __attribute__((aligned(1024))) char kbuf[2][KB];
-    __shared__ __attribute__((aligned(16))) char abuf[2][AB];
+    // a ring of three stage buffers (two chunks in flight), two at descriptor
+    // dimension 256, where three would leave one workgroup per CU
+    constexpr int NBUF = D <= 128 ? 3 : 2;
+    __shared__ __attribute__((aligned(1024))) char kbuf[NBUF][KB];
+    __shared__ __attribute__((aligned(16))) char abuf[NBUF][AB];
     const StageOff<D> soff = stage_offsets<D>();
     auto issue = [&](int c, int buf) __attribute__((always_inline)) {
       stage_dma_seq<D, false>(soff, c * kCkStride, ws.sk, ws.saug, nullptr, kbuf[buf], abuf[buf], nullptr, (int64_t)nb,
                               g.N);
     };
+    constexpr int kOps = stage_ops<D, false>();
     uint64_t run = 0;  // the state's prefix sum before chunk c
-    issue(0, 0);
+    for (int j = 0; j < NBUF - 1 && j < nch; ++j) issue(j, j);
     for (int c = 0; c < nch; ++c) {
-      const int buf = c & 1;
-      __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
-      stage_barrier();  // every wave's loads of chunk c landed; every wave is done with the other buffer
-      if (c + 1 < nch) issue(c + 1, buf ^ 1);
+      const int buf = c % NBUF;
+      if (NBUF == 3 && c + 1 < nch) __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(kOps));  // chunk c + 1 stays in flight
+      else __builtin_amdgcn_s_waitcnt(waitcnt_vm_lgkm0(0));
+      stage_barrier();  // every wave's loads of chunk c landed; every wave is done with chunk c - 1's buffer
+      if (c + NBUF - 1 < nch) issue(c + NBUF - 1, (c + NBUF - 1) % NBUF);
       const f32x16 x0 = tile_mfma<D>(kbuf[buf], abuf[buf], 0, rf, aoff);
       const f32x16 x1 = tile_mfma<D>(kbuf[buf], abuf[buf], 1, rf, aoff);
       // weights in candidate order inside the lane: tile tl, register 4 k + j is
