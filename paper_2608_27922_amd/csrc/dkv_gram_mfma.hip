@@ -1437,7 +1437,7 @@ done:
 // The first part of the crossing search in one pass: the prefix-chunk Gram of
 // the workgroup's 128 bank states over the first kCrossFirst ordered
 // candidates (4 waves x 32 states as row items, one 64-candidate chunk per
-// column stage, two stage buffers) stores each chunk sum as the chunk-sum Gram
+// column stage, a ring of stage buffers) stores each chunk sum as the chunk-sum Gram
 // does, and every state whose running prefix reaches its bound within a chunk
 // takes its first crossing there from the same weights, summed in candidate
 // order (the two half-waves exchange their 4-candidate group sums); states that
