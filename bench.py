@@ -323,6 +323,9 @@ def run_rollout(args, api, synth, torch):
                                                    / PEAK_BF16_TFLOPS, 4),
             "median_update_gram_frac_of_bf16_peak": round(float(np.median(gram_tf[rest])) / PEAK_BF16_TFLOPS, 4)
             if T > 1 else None,
+            "update_gram_note": "work-equivalent: the method's Gram pairs (m R prefix pairs of Eq. 8 included) over "
+                                "the update time; where the first 256 ordered candidates decide r*, the crossing "
+                                "search evaluates m x 256 of the m R prefix pairs",
             "median_attention_frac_of_bf16_peak": round(float(np.median(att_tf[rest])) / PEAK_BF16_TFLOPS, 4)
             if T > 1 else None,
             "r_star_mean_per_block": [round(float(x), 1) for x in rs_hist.float().mean(1).cpu().numpy()],
@@ -332,7 +335,7 @@ def run_rollout(args, api, synth, torch):
     }
     if seq:   # the Gram accounting is the default update's; the sequential walk has its own
         for k in ("update_gram_tflop", "update_gram_tflops", "update_gram_frac_of_bf16_peak",
-                  "median_update_gram_frac_of_bf16_peak"):
+                  "median_update_gram_frac_of_bf16_peak", "update_gram_note"):
             result["rollout"][k] = None
     del kv, qs, out, bank, ws
     torch.cuda.empty_cache()
