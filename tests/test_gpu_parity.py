@@ -164,6 +164,17 @@ def test_rollout_policy_ablations(policy, dt, d):
     _run_rollout(cfg, 6, api.Params(sigma2_log2=4 if d == 64 else 5, flags=POLICY_FLAGS[policy]), dup_every=2)
 
 
+@pytest.mark.parametrize("policy", sorted(POLICY_FLAGS))
+def test_rollout_policy_ablations_no_trace(policy):
+    """Every policy ablation with 600 candidates per block (more than the 256 of
+    the crossing search's first part) and without trace outputs, so that the
+    search may end after its first part: the committed banks bit-exact against
+    the oracle run with the same policy."""
+    _log(f"rollout policy {policy} no trace")
+    cfg = synth.Config(heads=4, d=128, dtype="bf16", n_cand=600, budget=1000, group_size=2, **SMALL)
+    _run_rollout(cfg, 5, api.Params(sigma2_log2=5, flags=POLICY_FLAGS[policy]), dup_every=2, trace=False)
+
+
 @pytest.mark.parametrize("dt,d", [("bf16", 128), ("bf16", 64)])
 def test_rollout_kv_descriptor(dt, d):
     """The [K; V] retention geometry (descriptor dimension 2 d: 256 and 128) on the
